@@ -1,0 +1,171 @@
+"""CPU oracle for multi-level RoIAlign -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path never does, and this
+package imports nothing from the GPU library (they share no code).
+
+The arithmetic lives in ``roi_oracle.c`` (plain C, OpenMP over RoIs for the
+forward and over channels for the backward).  This module compiles it with gcc
+and marshals numpy arrays through ctypes.  Everything it returns is float64.
+
+Paper anchors (MMDetection, arXiv 1906.07155): §3.1 RoIExtractor /
+SingleRoIExtractor (per-level RoI feature extraction with a RoIPooling-like
+operator), §2 (Mask R-CNN, whose RoIAlign that operator is), §3.2 (forward and
+backward every training iteration).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(_HERE, "roi_oracle.c")
+LIBRARY = os.path.join(_HERE, "liboracle.so")
+
+MODE_MATH = 0
+MODE_PARITY = 1
+_MODES = {"math": MODE_MATH, "parity": MODE_PARITY}
+
+# -ffp-contract=off: one rounding per written operation in the binary32 geometry.
+CFLAGS = ["-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+          "-fPIC", "-shared"]
+
+_lock = threading.Lock()
+_lib = None
+
+
+def build(source: str = SOURCE, output: str = LIBRARY) -> str:
+    """Compile the oracle with gcc (always recompiles)."""
+    tmp = output + ".tmp%d" % os.getpid()
+    subprocess.check_call(["gcc", *CFLAGS, source, "-o", tmp, "-lm"])
+    os.replace(tmp, output)
+    return output
+
+
+def _bind(lib):
+    f64pp = ctypes.POINTER(ctypes.c_void_p)
+    lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_level_map.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                     ctypes.c_float, ctypes.c_void_p]
+    lib.oracle_level_map.restype = None
+    lib.oracle_level_map_log2.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                          ctypes.c_double, ctypes.c_void_p]
+    lib.oracle_level_map_log2.restype = None
+    lib.oracle_roi_align_fwd.argtypes = [f64pp, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_void_p]
+    lib.oracle_roi_align_fwd.restype = None
+    lib.oracle_roi_align_bwd.argtypes = [ctypes.c_void_p, f64pp, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                         ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32,
+                                         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_int32]
+    lib.oracle_roi_align_bwd.restype = None
+    return lib
+
+
+def load(path: str | None = None):
+    """Load the compiled oracle, building it first if it is not there."""
+    global _lib
+    with _lock:
+        if path is not None:
+            return _bind(ctypes.CDLL(path))
+        if _lib is None:
+            if not os.path.exists(LIBRARY) or (
+                    os.path.getmtime(LIBRARY) < os.path.getmtime(SOURCE)):
+                build()
+            _lib = _bind(ctypes.CDLL(LIBRARY))
+        return _lib
+
+
+def num_threads(lib=None) -> int:
+    return int((lib or load()).oracle_num_threads())
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _rois(rois) -> np.ndarray:
+    r = np.ascontiguousarray(rois, dtype=np.float32)
+    if r.ndim != 2 or r.shape[1] != 5:
+        raise ValueError("rois must be [K, 5]")
+    return r
+
+
+def level_map(rois, num_levels: int, finest_scale: float = 56.0, lib=None) -> np.ndarray:
+    """Threshold form of the FPN level rule (binary32 area and thresholds)."""
+    lib = lib or load()
+    r = _rois(rois)
+    out = np.zeros(r.shape[0], dtype=np.int32)
+    lib.oracle_level_map(_ptr(r), r.shape[0], int(num_levels), float(finest_scale), _ptr(out))
+    return out
+
+
+def level_map_log2(rois, num_levels: int, finest_scale: float = 56.0, lib=None) -> np.ndarray:
+    """floor(log2(sqrt(area)/finest_scale)) clamped, in double precision."""
+    lib = lib or load()
+    r = _rois(rois)
+    out = np.zeros(r.shape[0], dtype=np.int32)
+    lib.oracle_level_map_log2(_ptr(r), r.shape[0], int(num_levels), float(finest_scale),
+                              _ptr(out))
+    return out
+
+
+def _level_args(shapes, scales):
+    if len(shapes) != len(scales) or not shapes:
+        raise ValueError("one scale per level")
+    dims = np.ascontiguousarray(np.array([list(s) for s in shapes], dtype=np.int64).reshape(-1))
+    sc = np.ascontiguousarray(np.array(scales, dtype=np.float32))
+    return dims, sc
+
+
+def roi_align_fwd(features, scales, rois, roi_levels, out_h: int, out_w: int,
+                  sampling_ratio: int, aligned: bool, mode: str = "parity",
+                  lib=None) -> np.ndarray:
+    """features: list of [N, C, H, W] arrays (any real dtype; read as float64).
+
+    Returns float64 [K, C, out_h, out_w].
+    """
+    lib = lib or load()
+    feats = [np.ascontiguousarray(f, dtype=np.float64) for f in features]
+    dims, sc = _level_args([f.shape for f in feats], scales)
+    r = _rois(rois)
+    K = r.shape[0]
+    C = feats[0].shape[1]
+    lv = None if roi_levels is None else np.ascontiguousarray(roi_levels, dtype=np.int32)
+    out = np.zeros((K, C, out_h, out_w), dtype=np.float64)
+    arr = (ctypes.c_void_p * len(feats))(*[f.ctypes.data for f in feats])
+    lib.oracle_roi_align_fwd(arr, _ptr(dims), _ptr(sc), len(feats), _ptr(r), K,
+                             None if lv is None else _ptr(lv), int(out_h), int(out_w),
+                             int(sampling_ratio), int(bool(aligned)), _MODES[mode], _ptr(out))
+    return out
+
+
+def roi_align_bwd(grad_out, shapes, scales, rois, roi_levels, out_h: int, out_w: int,
+                  sampling_ratio: int, aligned: bool, mode: str = "parity",
+                  lib=None) -> list:
+    """Transpose of roi_align_fwd.  shapes: list of (N, C, H, W) per level.
+
+    Returns a list of float64 gradient arrays, one per level.
+    """
+    lib = lib or load()
+    g = np.ascontiguousarray(grad_out, dtype=np.float64)
+    dims, sc = _level_args(shapes, scales)
+    r = _rois(rois)
+    K = r.shape[0]
+    if g.shape != (K, shapes[0][1], out_h, out_w):
+        raise ValueError("grad_out must be [K, C, out_h, out_w]")
+    lv = None if roi_levels is None else np.ascontiguousarray(roi_levels, dtype=np.int32)
+    grads = [np.zeros(tuple(s), dtype=np.float64) for s in shapes]
+    arr = (ctypes.c_void_p * len(grads))(*[x.ctypes.data for x in grads])
+    lib.oracle_roi_align_bwd(_ptr(g), arr, _ptr(dims), _ptr(sc), len(grads), _ptr(r), K,
+                             None if lv is None else _ptr(lv), int(out_h), int(out_w),
+                             int(sampling_ratio), int(bool(aligned)), _MODES[mode])
+    return grads

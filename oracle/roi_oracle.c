@@ -1,0 +1,352 @@
+/*
+ * roi_oracle.c -- plain CPU oracle for multi-level RoIAlign.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library exists so that the GPU library can be
+ * checked against something slow and obviously correct.  Only the test suite,
+ * the smoke check and the benchmark's CPU-baseline leg load it; the product path
+ * never calls it, and it shares no source, header or helper with the HIP code.
+ *
+ * What it computes (MMDetection, arXiv 1906.07155):
+ *   - §3.1 "Model Representation", RoIExtractor / SingleRoIExtractor: RoI-wise
+ *     features are extracted from "the corresponding level" of the feature
+ *     pyramid produced by the FPN neck, with a RoIPooling-like operator.
+ *   - §2 (supported frameworks) cites Mask R-CNN for the RoIAlign operator used
+ *     by the Faster/Mask R-CNN + FPN detectors; §1 ("High efficiency") states the
+ *     bbox and mask operations run on GPUs; §3.2 (training pipeline) runs forward
+ *     and backward every iteration, so the backward (the transpose) is needed too.
+ *   The paper does not spell the operator out.  The definition below is the
+ *   standard one (bilinear sampling on a regular grid inside each bin, averaged),
+ *   and every convention the paper leaves open is fixed the same way as in the
+ *   library's public header; the list of such readings lives with the design notes.
+ *
+ * Two geometry modes:
+ *   MODE_MATH   (0): every coordinate and weight in double precision.  Used by
+ *                    the invariant tests (closed forms, adjoint, brute force).
+ *   MODE_PARITY (1): the sample geometry in IEEE binary32 with one rounding per
+ *                    operation in the order written below (build with
+ *                    -ffp-contract=off so no multiply-add is fused); products and
+ *                    sums of feature values in double.  This is what the GPU is
+ *                    compared against.
+ *
+ * Layout: every feature level is a dense double array [N][C][H][W]; RoIs are
+ * float [K][5] = (batch_index, x1, y1, x2, y2) in input-image pixels; the output
+ * is a dense double array [K][C][PH][PW].
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define MODE_MATH 0
+#define MODE_PARITY 1
+
+/* Adaptive sampling grids (sampling_ratio == 0) are capped at this many samples
+ * per bin side, matching the limit the GPU library documents for the same case. */
+#define ADAPTIVE_GRID_CAP 64
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------------- */
+/* Level assignment (§3.1: "the corresponding level of feature pyramids").    */
+/* ------------------------------------------------------------------------- */
+
+/* Threshold form of the FPN rule: the level is the number of thresholds
+ * (finest_scale * 2^j)^2, j = 1 .. L-1, that the box area reaches.  Area and
+ * thresholds are binary32 values, one rounding per operation. */
+void oracle_level_map(const float *rois, int64_t K, int32_t num_levels,
+                      float finest_scale, int32_t *out)
+{
+    for (int64_t k = 0; k < K; ++k) {
+        const float *r = rois + 5 * k;
+        float w = r[3] - r[1];
+        float h = r[4] - r[2];
+        float area = w * h;
+        int32_t lvl = 0;
+        for (int32_t j = 1; j < num_levels; ++j) {
+            float side = finest_scale * (float)(1 << j);
+            float thr = side * side;
+            if (area >= thr)
+                lvl += 1;
+        }
+        out[k] = lvl;
+    }
+}
+
+/* The logarithmic statement of the same rule, in double precision:
+ * floor(log2(sqrt(w*h) / finest_scale)), clamped to [0, L-1].  Agrees with the
+ * threshold form everywhere except within rounding distance of a threshold. */
+void oracle_level_map_log2(const float *rois, int64_t K, int32_t num_levels,
+                           double finest_scale, int32_t *out)
+{
+    for (int64_t k = 0; k < K; ++k) {
+        const float *r = rois + 5 * k;
+        double w = (double)r[3] - (double)r[1];
+        double h = (double)r[4] - (double)r[2];
+        double a = w * h;
+        int32_t lvl = 0;
+        if (a > 0.0) {
+            double l = floor(log2(sqrt(a) / finest_scale));
+            if (l > (double)(num_levels - 1))
+                l = (double)(num_levels - 1);
+            if (l > 0.0)
+                lvl = (int32_t)l;
+        }
+        out[k] = lvl;
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* One axis of the sampling grid.                                             */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+    int valid;      /* sample lies inside [-1, size] */
+    int lo, hi;     /* the two neighbouring pixel indices after clamping */
+    double w_lo;    /* weight of pixel lo (1 - frac) */
+    double w_hi;    /* weight of pixel hi (frac) */
+} axis_tap;
+
+typedef struct {
+    double start_d, bin_d;   /* MODE_MATH */
+    float start_f, bin_f;    /* MODE_PARITY */
+    int grid;                /* samples per bin along this axis */
+} axis_geom;
+
+static int grid_from_bin(int sampling_ratio, double bin)
+{
+    if (sampling_ratio > 0)
+        return sampling_ratio;
+    if (!(bin > 0.0))
+        return 0;
+    double g = ceil(bin);
+    if (g > (double)ADAPTIVE_GRID_CAP)
+        g = (double)ADAPTIVE_GRID_CAP;
+    return (int)g;
+}
+
+/* RoI extent along one axis -> start, bin size and grid.
+ * start = c1*scale - off, end = c2*scale - off, length = end - start (at least 1
+ * pixel when not aligned), bin = length / P. */
+static axis_geom axis_setup(int mode, float c1, float c2, float scale, int aligned,
+                            int P, int sampling_ratio)
+{
+    axis_geom g;
+    memset(&g, 0, sizeof(g));
+    if (mode == MODE_PARITY) {
+        const float off = aligned ? 0.5f : 0.0f;
+        float s = c1 * scale;
+        s = s - off;
+        float e = c2 * scale;
+        e = e - off;
+        float len = e - s;
+        if (!aligned)
+            len = fmaxf(len, 1.0f);
+        float bin = len / (float)P;
+        g.start_f = s;
+        g.bin_f = bin;
+        g.start_d = (double)s;
+        g.bin_d = (double)bin;
+        g.grid = grid_from_bin(sampling_ratio, (double)bin);
+    } else {
+        const double off = aligned ? 0.5 : 0.0;
+        double s = (double)c1 * (double)scale - off;
+        double e = (double)c2 * (double)scale - off;
+        double len = e - s;
+        if (!aligned)
+            len = fmax(len, 1.0);
+        double bin = len / (double)P;
+        g.start_d = s;
+        g.bin_d = bin;
+        g.grid = grid_from_bin(sampling_ratio, bin);
+    }
+    return g;
+}
+
+/* Sample i (0 <= i < grid) of bin p: coordinate start + p*bin + (i + 1/2)*bin/grid,
+ * then the bilinear neighbours on a map of `size` pixels. */
+static axis_tap axis_sample(int mode, const axis_geom *g, int p, int i, int size)
+{
+    axis_tap t;
+    t.valid = 0;
+    t.lo = t.hi = 0;
+    t.w_lo = t.w_hi = 0.0;
+    if (mode == MODE_PARITY) {
+        float a = (float)p * g->bin_f;
+        float b = g->start_f + a;
+        float c = (float)i + 0.5f;
+        float d = c * g->bin_f;
+        float e = d / (float)g->grid;
+        float v = b + e;
+        if (v < -1.0f || v > (float)size)
+            return t;
+        v = fmaxf(v, 0.0f);
+        int lo = (int)v;
+        int hi;
+        if (lo >= size - 1) {
+            lo = size - 1;
+            hi = size - 1;
+            v = (float)lo;
+        } else {
+            hi = lo + 1;
+        }
+        float frac = v - (float)lo;
+        float rest = 1.0f - frac;
+        t.valid = 1;
+        t.lo = lo;
+        t.hi = hi;
+        t.w_lo = (double)rest;
+        t.w_hi = (double)frac;
+    } else {
+        double v = g->start_d + (double)p * g->bin_d +
+                   ((double)i + 0.5) * g->bin_d / (double)g->grid;
+        if (v < -1.0 || v > (double)size)
+            return t;
+        v = fmax(v, 0.0);
+        int lo = (int)v;
+        int hi;
+        if (lo >= size - 1) {
+            lo = size - 1;
+            hi = size - 1;
+            v = (double)lo;
+        } else {
+            hi = lo + 1;
+        }
+        double frac = v - (double)lo;
+        t.valid = 1;
+        t.lo = lo;
+        t.hi = hi;
+        t.w_lo = 1.0 - frac;
+        t.w_hi = frac;
+    }
+    return t;
+}
+
+/* Batch index: column 0 of the RoI, truncated toward zero; -1 when it does not
+ * name an image of the batch (such a RoI yields zeros and no gradient). */
+static int roi_batch(float v, int64_t N)
+{
+    float t = truncf(v);
+    if (!(t >= 0.0f) || !(t < (float)N))
+        return -1;
+    return (int)t;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Forward: out[k,c,ph,pw] = (1/count) * sum over samples and bilinear corners */
+/* ------------------------------------------------------------------------- */
+
+void oracle_roi_align_fwd(const double *const *feats, const int64_t *dims,
+                          const float *scales, int32_t num_levels,
+                          const float *rois, int64_t K, const int32_t *roi_levels,
+                          int32_t PH, int32_t PW, int32_t sampling_ratio,
+                          int32_t aligned, int32_t mode, double *out)
+{
+    const int64_t C = dims[1];
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t k = 0; k < K; ++k) {
+        double *o = out + k * C * PH * PW;
+        for (int64_t e = 0; e < C * PH * PW; ++e)
+            o[e] = 0.0;
+        const float *r = rois + 5 * k;
+        int lvl = roi_levels ? roi_levels[k] : 0;
+        if (lvl < 0 || lvl >= num_levels)
+            continue;
+        const int64_t N = dims[4 * lvl + 0];
+        const int64_t H = dims[4 * lvl + 2];
+        const int64_t W = dims[4 * lvl + 3];
+        int b = roi_batch(r[0], N);
+        if (b < 0)
+            continue;
+        axis_geom gx = axis_setup(mode, r[1], r[3], scales[lvl], aligned, PW, sampling_ratio);
+        axis_geom gy = axis_setup(mode, r[2], r[4], scales[lvl], aligned, PH, sampling_ratio);
+        int count = gy.grid * gx.grid;
+        if (count < 1)
+            count = 1;
+        for (int64_t c = 0; c < C; ++c) {
+            const double *F = feats[lvl] + ((int64_t)b * C + c) * H * W;
+            for (int ph = 0; ph < PH; ++ph) {
+                for (int pw = 0; pw < PW; ++pw) {
+                    double sum = 0.0;
+                    for (int iy = 0; iy < gy.grid; ++iy) {
+                        axis_tap ty = axis_sample(mode, &gy, ph, iy, (int)H);
+                        for (int ix = 0; ix < gx.grid; ++ix) {
+                            axis_tap tx = axis_sample(mode, &gx, pw, ix, (int)W);
+                            if (!ty.valid || !tx.valid)
+                                continue;
+                            sum += ty.w_lo * tx.w_lo * F[ty.lo * W + tx.lo];
+                            sum += ty.w_lo * tx.w_hi * F[ty.lo * W + tx.hi];
+                            sum += ty.w_hi * tx.w_lo * F[ty.hi * W + tx.lo];
+                            sum += ty.w_hi * tx.w_hi * F[ty.hi * W + tx.hi];
+                        }
+                    }
+                    o[(c * PH + ph) * PW + pw] = sum / (double)count;
+                }
+            }
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Backward: the transpose of the forward.  grad_feats[l][b,c,y,x] +=          */
+/* grad_out[k,c,ph,pw] * weight / count for every sample and corner that the   */
+/* forward reads.  Accumulates into grad_feats (the caller clears them).       */
+/* Channels are independent, so the loop over channels is the parallel one and */
+/* every channel plane is written by one thread in a fixed order.             */
+/* ------------------------------------------------------------------------- */
+
+void oracle_roi_align_bwd(const double *grad_out, double *const *grad_feats,
+                          const int64_t *dims, const float *scales,
+                          int32_t num_levels, const float *rois, int64_t K,
+                          const int32_t *roi_levels, int32_t PH, int32_t PW,
+                          int32_t sampling_ratio, int32_t aligned, int32_t mode)
+{
+    const int64_t C = dims[1];
+#pragma omp parallel for schedule(static)
+    for (int64_t c = 0; c < C; ++c) {
+        for (int64_t k = 0; k < K; ++k) {
+            const float *r = rois + 5 * k;
+            int lvl = roi_levels ? roi_levels[k] : 0;
+            if (lvl < 0 || lvl >= num_levels)
+                continue;
+            const int64_t N = dims[4 * lvl + 0];
+            const int64_t H = dims[4 * lvl + 2];
+            const int64_t W = dims[4 * lvl + 3];
+            int b = roi_batch(r[0], N);
+            if (b < 0)
+                continue;
+            axis_geom gx = axis_setup(mode, r[1], r[3], scales[lvl], aligned, PW, sampling_ratio);
+            axis_geom gy = axis_setup(mode, r[2], r[4], scales[lvl], aligned, PH, sampling_ratio);
+            int count = gy.grid * gx.grid;
+            if (count < 1)
+                count = 1;
+            double *G = grad_feats[lvl] + ((int64_t)b * C + c) * H * W;
+            const double *g = grad_out + (k * C + c) * PH * PW;
+            for (int ph = 0; ph < PH; ++ph) {
+                for (int pw = 0; pw < PW; ++pw) {
+                    double gv = g[ph * PW + pw] / (double)count;
+                    for (int iy = 0; iy < gy.grid; ++iy) {
+                        axis_tap ty = axis_sample(mode, &gy, ph, iy, (int)H);
+                        for (int ix = 0; ix < gx.grid; ++ix) {
+                            axis_tap tx = axis_sample(mode, &gx, pw, ix, (int)W);
+                            if (!ty.valid || !tx.valid)
+                                continue;
+                            G[ty.lo * W + tx.lo] += gv * ty.w_lo * tx.w_lo;
+                            G[ty.lo * W + tx.hi] += gv * ty.w_lo * tx.w_hi;
+                            G[ty.hi * W + tx.lo] += gv * ty.w_hi * tx.w_lo;
+                            G[ty.hi * W + tx.hi] += gv * ty.w_hi * tx.w_hi;
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
