@@ -1,0 +1,173 @@
+/*
+ * roi_extract.h -- C ABI of the MI355X multi-level RoIAlign library.
+ *
+ * The operator is the RoIExtractor of MMDetection (arXiv 1906.07155, §3.1
+ * "Model Representation"): RoI-wise features are taken from the corresponding
+ * level of an FPN feature pyramid (§3.1, Neck) with a RoIPooling-like operator,
+ * here RoIAlign (the Mask R-CNN operator, cited among the supported frameworks in
+ * §2).  The paper runs these bbox/mask operations on the GPU (§1, "High
+ * efficiency") and trains with forward and backward every iteration (§3.2).
+ *
+ * Conventions (the paper leaves them open; these are the library's definitions):
+ *   - RoI k is 5 binary32 values (batch_index, x1, y1, x2, y2) in input-image
+ *     pixels.  batch_index is truncated toward zero; a RoI whose batch index or
+ *     level index is outside the valid range yields zeros and no gradient.
+ *   - Level rule (threshold form of the FPN rule floor(log2(sqrt(wh)/s0))):
+ *     level = #{ j in 1..L-1 : (x2-x1)*(y2-y1) >= (s0*2^j)^2 }, every product and
+ *     difference rounded to binary32, s0 = finest_scale (56 for P2..P5).
+ *   - On level l with scale s, H x W map, output PH x PW, sampling ratio S:
+ *       off = aligned ? 0.5 : 0
+ *       x0 = x1*s - off,  xe = x2*s - off,  rw = xe - x0 (>= 1 if !aligned)
+ *       bw = rw / PW;     gw = S > 0 ? S : min(ceil(bw), 64)   (same for y)
+ *       sample (pw, ix):  x = (x0 + pw*bw) + ((ix + 0.5)*bw) / gw
+ *     each operation rounded to binary32 in that order (no fused multiply-add).
+ *     A sample with y < -1, y > H, x < -1 or x > W contributes zero; otherwise
+ *     y = max(y, 0), yl = (int)y, yh = yl + 1, and if yl >= H-1 then
+ *     yl = yh = H-1 and y = yl; ly = y - yl, hy = 1 - ly (same for x).
+ *       out[k,c,ph,pw] = (1/count) * sum over samples of
+ *           hy*hx*F[yl,xl] + hy*lx*F[yl,xh] + ly*hx*F[yh,xl] + ly*lx*F[yh,xh],
+ *       count = max(gh*gw, 1)   (invalid samples are counted).
+ *   - Backward is the exact transpose: grad_F[b,c,y*,x*] += g[k,c,ph,pw]*w/count
+ *     for every valid sample and corner, accumulated with fp32 atomics (the
+ *     summation order, hence the last bits, vary from run to run).
+ *
+ * Ownership and execution: the caller owns every buffer; all data pointers are
+ * device pointers except the re_level_t arrays, which are read on the host during
+ * the call.  Calls enqueue work on `stream` (a hipStream_t; NULL = the null
+ * stream) and return without synchronizing.  The library never allocates device
+ * memory and keeps no state between calls.  Argument errors are detected on the
+ * host before anything is enqueued; a launch failure is reported as
+ * RE_ERR_DEVICE.  Device-side content (RoI coordinates, level indices, plan
+ * contents) is never reported as an error: out-of-range values are clamped or
+ * skipped so every memory access stays inside the buffers described here.
+ */
+#ifndef ROI_EXTRACT_H
+#define ROI_EXTRACT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RE_OK = 0,
+    RE_ERR_INVALID_ARG = 1,   /* null pointer, bad shape/stride/dtype/size/scale */
+    RE_ERR_UNSUPPORTED = 2,   /* valid request this build does not implement */
+    RE_ERR_WORKSPACE = 3,     /* workspace missing or too small */
+    RE_ERR_DEVICE = 4         /* a HIP call or kernel launch failed */
+} re_status_t;
+
+typedef enum {
+    RE_DTYPE_F32 = 0,         /* IEEE binary32 */
+    RE_DTYPE_BF16 = 1         /* bfloat16; results are rounded to nearest-even */
+} re_dtype_t;
+
+#define RE_MAX_LEVELS 8
+#define RE_MAX_OUT 256        /* largest out_h / out_w */
+#define RE_MAX_SAMPLING 64    /* largest sampling_ratio; also the adaptive-grid cap */
+
+/* One pyramid level: a logically NCHW tensor [n, c, h, w] with element strides.
+ * stride_c == 1 (channels-last, e.g. a PyTorch channels_last tensor) selects the
+ * fast path with channel-contiguous loads; any other non-negative strides are
+ * accepted and served by a general kernel.  Every level of a pyramid has the same
+ * n, c and dtype.  `data` must be aligned to its element size. */
+typedef struct {
+    void *data;
+    int32_t dtype;            /* re_dtype_t */
+    int32_t reserved;         /* must be 0 */
+    int64_t n, c, h, w;
+    int64_t stride_n, stride_c, stride_h, stride_w;
+    float spatial_scale;      /* feature pixels per input pixel, e.g. 1/4 for P2 */
+    float reserved2;          /* must be 0 */
+} re_level_t;
+
+/* a1 -- FPN level of every RoI (§3.1: "the corresponding level of feature
+ * pyramids").  rois: device float[num_rois][5]; levels_out: device
+ * int32[num_rois], written with values in [0, num_levels).  num_levels in
+ * [1, RE_MAX_LEVELS]; finest_scale finite and > 0.  num_rois == 0 is a no-op. */
+re_status_t fpn_level_map(const float *rois, int64_t num_rois, int32_t num_levels,
+                          float finest_scale, int32_t *levels_out, void *stream);
+
+/* Bytes of device workspace a plan for num_rois RoIs over num_levels levels needs
+ * (a few bytes per RoI).  Host-only; writes *bytes. */
+re_status_t roi_extract_workspace_size(int64_t num_rois, int32_t num_levels, size_t *bytes);
+
+/* a1 + a2 in one launch -- the level of every RoI (written to levels_out, as by
+ * fpn_level_map) and the launch plan: a permutation of the RoIs ordered by
+ * (level, image, coarse spatial cell of the box centre) plus per-level offsets,
+ * stored in `workspace`.  The forward and backward walk the RoIs in plan order,
+ * so neighbouring work shares cache; any valid permutation gives the same
+ * results, and RoIs with equal keys may come in any order.  The plan stays valid
+ * for as long as rois, levels_out and the level shapes are unchanged, so one plan
+ * serves a forward and its backward.
+ *   levels: host array of num_levels descriptors (only n, h, w and spatial_scale
+ *           are read);  rois: device float[num_rois][5];
+ *   levels_out: device int32[num_rois];  workspace: device, at least
+ *           roi_extract_workspace_size() bytes. */
+re_status_t roi_extract_plan(const re_level_t *levels, int32_t num_levels,
+                             const float *rois, int64_t num_rois, float finest_scale,
+                             int32_t *levels_out, void *workspace, size_t workspace_bytes,
+                             void *stream);
+
+/* Copy of the plan's per-level offsets: a device int32[num_levels + 1] array
+ * (offsets[l] = first position of level l in plan order; offsets[num_levels] =
+ * num_rois) is written to `offsets_out` (device).  For inspection and tests. */
+re_status_t roi_extract_plan_offsets(const void *workspace, size_t workspace_bytes,
+                                     int64_t num_rois, int32_t num_levels,
+                                     int32_t *offsets_out, void *stream);
+
+/* Device pointer to the plan's permutation (int32[num_rois]) inside `workspace`,
+ * for inspection and tests.  Host-only pointer arithmetic. */
+re_status_t roi_extract_plan_perm(const void *workspace, size_t workspace_bytes,
+                                  int64_t num_rois, const int32_t **perm_out);
+
+/* a3-a5 -- RoIAlign forward.
+ *   levels/num_levels: host array of feature levels (same n, c, dtype);
+ *   rois: device float[num_rois][5];
+ *   roi_levels: device int32[num_rois] (e.g. from roi_extract_plan); may be NULL
+ *           only when num_levels == 1;
+ *   out_h, out_w in [1, RE_MAX_OUT]; sampling_ratio in [0, RE_MAX_SAMPLING]
+ *           (0 = adaptive ceil(bin size), capped at RE_MAX_SAMPLING);
+ *   aligned: 0 or 1;
+ *   out: device [num_rois][c][out_h][out_w], dense, of out_dtype;
+ *   plan: a workspace filled by roi_extract_plan for these RoIs (RoIs are then
+ *           visited in plan order), or NULL (visited in index order).
+ * Writes every element of out exactly once; results do not depend on the plan. */
+re_status_t roi_align_fwd(const re_level_t *levels, int32_t num_levels,
+                          const float *rois, int64_t num_rois, const int32_t *roi_levels,
+                          int32_t out_h, int32_t out_w, int32_t sampling_ratio,
+                          int32_t aligned, void *out, int32_t out_dtype,
+                          const void *plan, size_t plan_bytes, void *stream);
+
+/* a6 -- clear the gradient pyramid (every element of every level set to +0.0).
+ * grad_levels: host array; every level RE_DTYPE_F32. */
+re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_levels,
+                                  void *stream);
+
+/* a6 + a7 -- RoIAlign backward: adds the transpose of the forward applied to
+ * grad_out into the gradient pyramid.
+ *   grad_out: device [num_rois][c][out_h][out_w], dense, of grad_out_dtype;
+ *   grad_levels: host array of num_levels descriptors, RE_DTYPE_F32, same n, c,
+ *           h, w and spatial_scale as the forward's levels; accumulated into with
+ *           fp32 atomics (cleared first when zero_init != 0);
+ *   other arguments as roi_align_fwd. */
+re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype,
+                          const float *rois, int64_t num_rois, const int32_t *roi_levels,
+                          int32_t out_h, int32_t out_w, int32_t sampling_ratio,
+                          int32_t aligned, const re_level_t *grad_levels, int32_t num_levels,
+                          int32_t zero_init, const void *plan, size_t plan_bytes,
+                          void *stream);
+
+/* Static description of a status code. */
+const char *roi_extract_status_str(re_status_t status);
+
+/* Library version string. */
+const char *roi_extract_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROI_EXTRACT_H */

@@ -1,0 +1,19 @@
+"""MI355X-native multi-level RoIAlign (the RoIExtractor of MMDetection, arXiv 1906.07155).
+
+The work runs in hand-written HIP kernels for gfx950 behind the C ABI in
+include/roi_extract.h (libroi_extract.so, built in-tree by `build.py`).  This
+package only marshals torch tensors into that ABI.
+"""
+from .binding import (RoIExtractError, fpn_level_map, lib, plan, plan_offsets, plan_perm,
+                      roi_align_bwd, roi_align_fwd, workspace_size, zero_grad)
+
+__all__ = ["RoIExtractError", "fpn_level_map", "lib", "plan", "plan_offsets", "plan_perm",
+           "roi_align_bwd", "roi_align_fwd", "workspace_size", "zero_grad", "roi_extract",
+           "RoIAlignFunction"]
+
+
+def __getattr__(name):
+    if name in ("roi_extract", "RoIAlignFunction"):
+        from . import extractor
+        return getattr(extractor, name)
+    raise AttributeError(name)

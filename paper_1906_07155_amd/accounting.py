@@ -1,0 +1,133 @@
+"""Algorithmic byte counts for the roofline figures of the benchmark.
+
+For every RoI the forward reads a separable footprint of feature pixels: the
+distinct tap rows of its valid sample rows times the distinct tap columns of its
+valid sample columns (validity and taps are separable, so the product is exact).
+With C channels of s bytes:
+
+  E_fwd  = sum_r F_r*C*s_feat + K*C*PH*PW*s_out + 24*K        (effective bytes)
+  E_bwd  = K*C*PH*PW*s_gout + 2*sum_r F_r*C*4 + 24*K          (RMW of fp32 atomics)
+  zero   = sum_l N*C*H_l*W_l*4                                 (clearing the gradients)
+  U_*    = the same with sum_r F_r replaced by the size of the union of footprints
+  T_fwd  = K*PH*PW*gh*gw*4*C*s_feat                            (every tap, no reuse)
+
+24*K is the RoI (20 bytes) and level (4 bytes) read.  The footprints use the
+binary32 sample geometry of the operator (numpy float32 arithmetic, one rounding
+per operation); this module is measurement code and shares nothing with the
+kernels or the oracle.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Sequence, Tuple
+
+import numpy as np
+
+F32 = np.float32
+
+
+def _axis_taps(c1: np.ndarray, c2: np.ndarray, scale: float, aligned: bool, P: int, S: int,
+               size: int):
+    """Tap indices of every sample along one axis: lo, hi [K, P*S] (-1 where invalid)."""
+    off = F32(0.5 if aligned else 0.0)
+    s = c1.astype(F32) * F32(scale)
+    s = s - off
+    e = c2.astype(F32) * F32(scale)
+    e = e - off
+    ln = e - s
+    if not aligned:
+        ln = np.maximum(ln, F32(1.0))
+    b = ln / F32(P)
+    if S > 0:
+        grid = np.full(c1.shape, S, dtype=np.int64)
+    else:
+        grid = np.where(b > 0, np.minimum(np.ceil(b), 64), 0).astype(np.int64)
+    gmax = int(grid.max()) if grid.size else 0
+    K = c1.shape[0]
+    lo = np.full((K, P, max(gmax, 1)), -1, dtype=np.int64)
+    hi = np.full((K, P, max(gmax, 1)), -1, dtype=np.int64)
+    if gmax == 0:
+        return lo.reshape(K, -1), hi.reshape(K, -1), grid
+    p = np.arange(P, dtype=F32)[None, :, None]
+    i = np.arange(gmax, dtype=F32)[None, None, :]
+    t1 = p * b[:, None, None]
+    t2 = s[:, None, None] + t1
+    t3 = i + F32(0.5)
+    t4 = t3 * b[:, None, None]
+    t5 = t4 / np.maximum(grid, 1).astype(F32)[:, None, None]
+    v = t2 + t5
+    exists = np.arange(gmax)[None, None, :] < grid[:, None, None]
+    valid = exists & ~((v < F32(-1.0)) | (v > F32(size)))
+    v = np.maximum(v, F32(0.0))
+    l = np.floor(v).astype(np.int64)
+    h = l + 1
+    edge = l >= size - 1
+    l = np.where(edge, size - 1, l)
+    h = np.where(edge, size - 1, h)
+    lo[valid] = l[valid]
+    hi[valid] = h[valid]
+    return lo.reshape(K, -1), hi.reshape(K, -1), grid
+
+
+def _distinct(lo: np.ndarray, hi: np.ndarray):
+    """Per row: sorted distinct non-negative values of lo and hi."""
+    both = np.sort(np.concatenate([lo, hi], axis=1), axis=1)
+    keep = both >= 0
+    keep[:, 1:] &= both[:, 1:] != both[:, :-1]
+    return both, keep
+
+
+@dataclasses.dataclass
+class Bytes:
+    K: int
+    footprint_px: int        # sum over RoIs of F_r
+    union_px: int            # pixels in the union of footprints
+    taps_px: int             # sum over RoIs of PH*PW*gh*gw*4
+    e_fwd: int
+    e_bwd: int
+    u_fwd: int
+    u_bwd: int
+    t_fwd: int
+    zero: int
+    out_bytes: int
+
+
+def count(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[int, int]],
+          scales: Sequence[float], n_images: int, C: int, out_hw: Tuple[int, int], S: int,
+          aligned: bool, s_feat: int, s_out: int, s_gout: int) -> Bytes:
+    K = rois.shape[0]
+    PH, PW = out_hw
+    fp_total = 0
+    union_total = 0
+    taps_total = 0
+    for l, ((H, W), sc) in enumerate(zip(level_hw, scales)):
+        idx = np.flatnonzero(levels == l)
+        if idx.size == 0:
+            continue
+        r = rois[idx]
+        b = np.trunc(r[:, 0]).astype(np.int64)
+        ok = (b >= 0) & (b < n_images)
+        ylo, yhi, gy = _axis_taps(r[:, 2], r[:, 4], sc, aligned, PH, S, H)
+        xlo, xhi, gx = _axis_taps(r[:, 1], r[:, 3], sc, aligned, PW, S, W)
+        ys, ykeep = _distinct(ylo, yhi)
+        xs, xkeep = _distinct(xlo, xhi)
+        nrow = ykeep.sum(1)
+        ncol = xkeep.sum(1)
+        fp_total += int((nrow * ncol)[ok].sum())
+        taps_total += int((PH * PW * gy * gx * 4)[ok].sum())
+        masks = np.zeros((n_images, H, W), dtype=bool)
+        for j in np.flatnonzero(ok):
+            rows = ys[j][ykeep[j]]
+            cols = xs[j][xkeep[j]]
+            if rows.size and cols.size:
+                masks[b[j]][np.ix_(rows, cols)] = True
+        union_total += int(masks.sum())
+    out_elems = K * C * PH * PW
+    zero = sum(n_images * C * H * W * 4 for (H, W) in level_hw)
+    return Bytes(
+        K=K, footprint_px=fp_total, union_px=union_total, taps_px=taps_total,
+        e_fwd=fp_total * C * s_feat + out_elems * s_out + 24 * K,
+        e_bwd=out_elems * s_gout + 2 * fp_total * C * 4 + 24 * K,
+        u_fwd=union_total * C * s_feat + out_elems * s_out + 24 * K,
+        u_bwd=out_elems * s_gout + 2 * union_total * C * 4 + 24 * K,
+        t_fwd=taps_total * C * s_feat, zero=zero, out_bytes=out_elems * s_out)

@@ -1,0 +1,261 @@
+"""Thin ctypes binding of libroi_extract.so (argument marshalling only).
+
+Every operation runs in the library's HIP kernels; this module only turns torch
+tensors into the pointers, sizes and strides the C ABI (include/roi_extract.h)
+takes, and passes torch's current HIP stream.  PyTorch is used for device memory
+and streams.  If the library is not built, loading fails loudly: there is no
+fallback path.
+
+Paper anchors (MMDetection, arXiv 1906.07155): §3.1 RoIExtractor /
+SingleRoIExtractor (level map + RoI feature extraction), §3.2 (forward and
+backward every iteration).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import threading
+from typing import List, Optional, Sequence, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(HERE, "libroi_extract.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "roi_extract.h")
+
+RE_OK, RE_ERR_INVALID_ARG, RE_ERR_UNSUPPORTED, RE_ERR_WORKSPACE, RE_ERR_DEVICE = range(5)
+RE_DTYPE_F32, RE_DTYPE_BF16 = 0, 1
+MAX_LEVELS = 8
+
+
+class RoIExtractError(RuntimeError):
+    def __init__(self, status: int, where: str, text: str):
+        super().__init__("%s failed: %s (status %d)" % (where, text, status))
+        self.status = status
+
+
+class ReLevel(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("n", ctypes.c_int64), ("c", ctypes.c_int64),
+                ("h", ctypes.c_int64), ("w", ctypes.c_int64), ("stride_n", ctypes.c_int64),
+                ("stride_c", ctypes.c_int64), ("stride_h", ctypes.c_int64),
+                ("stride_w", ctypes.c_int64), ("spatial_scale", ctypes.c_float),
+                ("reserved2", ctypes.c_float)]
+
+
+_VP, _I32, _I64, _F32, _SZ = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                              ctypes.c_size_t)
+_LEVELS = ctypes.POINTER(ReLevel)
+
+SIGNATURES = {
+    "fpn_level_map": [_VP, _I64, _I32, _F32, _VP, _VP],
+    "roi_extract_workspace_size": [_I64, _I32, ctypes.POINTER(_SZ)],
+    "roi_extract_plan": [_LEVELS, _I32, _VP, _I64, _F32, _VP, _VP, _SZ, _VP],
+    "roi_extract_plan_offsets": [_VP, _SZ, _I64, _I32, _VP, _VP],
+    "roi_extract_plan_perm": [_VP, _SZ, _I64, ctypes.POINTER(_VP)],
+    "roi_align_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _VP, _I32, _VP,
+                      _SZ, _VP],
+    "roi_extract_zero_grad": [_LEVELS, _I32, _VP],
+    "roi_align_bwd": [_VP, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _LEVELS, _I32, _I32,
+                      _VP, _SZ, _VP],
+}
+
+_lock = threading.Lock()
+_lib = None
+
+
+def header_functions() -> List[str]:
+    """Names of the functions include/roi_extract.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^\s*(?:re_status_t|const char\s*\*)\s*(\w+)\s*\(", text, flags=re.M)
+
+
+def lib(path: Optional[str] = None):
+    """Load libroi_extract.so (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is not None and path is None:
+            return _lib
+        p = path or LIBRARY
+        if not os.path.exists(p):
+            raise RuntimeError("%s is not built: run __graft_entry__.build() (hipcc, gfx950)" % p)
+        L = ctypes.CDLL(p)
+        for name, argtypes in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = argtypes
+            fn.restype = ctypes.c_int
+        L.roi_extract_status_str.argtypes = [ctypes.c_int]
+        L.roi_extract_status_str.restype = ctypes.c_char_p
+        L.roi_extract_version.argtypes = []
+        L.roi_extract_version.restype = ctypes.c_char_p
+        if path is None:
+            _lib = L
+        return L
+
+
+def check(status: int, where: str) -> None:
+    if status != RE_OK:
+        raise RoIExtractError(status, where, lib().roi_extract_status_str(status).decode())
+
+
+# ---------------------------------------------------------------------------
+# torch marshalling
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return RE_DTYPE_F32
+    if t.dtype == torch.bfloat16:
+        return RE_DTYPE_BF16
+    raise TypeError("only float32 and bfloat16 tensors are supported, got %s" % t.dtype)
+
+
+def _need_cuda(t, name: str):
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor" % name)
+
+
+def stream_handle(stream=None) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def level_array(tensors: Sequence, scales: Sequence[float]):
+    """re_level_t[] describing logically-NCHW tensors (any strides)."""
+    if len(tensors) != len(scales):
+        raise ValueError("one spatial scale per level")
+    arr = (ReLevel * max(1, len(tensors)))()
+    for i, (t, s) in enumerate(zip(tensors, scales)):
+        if t.dim() != 4:
+            raise ValueError("feature level %d must be 4-D [N, C, H, W]" % i)
+        _need_cuda(t, "feature level %d" % i)
+        n, c, h, w = t.shape
+        sn, sc, sh, sw = t.stride()
+        arr[i] = ReLevel(t.data_ptr(), _dtype_code(t), 0, n, c, h, w, sn, sc, sh, sw, float(s),
+                         0.0)
+    return arr
+
+
+def _rois(rois):
+    torch = _torch()
+    if rois.dim() != 2 or rois.shape[1] != 5 or rois.dtype != torch.float32:
+        raise ValueError("rois must be a float32 [K, 5] tensor")
+    _need_cuda(rois, "rois")
+    if not rois.is_contiguous():
+        raise ValueError("rois must be contiguous")
+    return rois
+
+
+# ---------------------------------------------------------------------------
+# The C ABI, one function each
+# ---------------------------------------------------------------------------
+
+def fpn_level_map(rois, num_levels: int, finest_scale: float = 56.0, out=None, stream=None):
+    torch = _torch()
+    rois = _rois(rois)
+    K = rois.shape[0]
+    if out is None:
+        out = torch.empty(K, dtype=torch.int32, device=rois.device)
+    check(lib().fpn_level_map(rois.data_ptr(), K, num_levels, finest_scale, out.data_ptr(),
+                              stream_handle(stream)), "fpn_level_map")
+    return out
+
+
+def workspace_size(num_rois: int, num_levels: int) -> int:
+    n = ctypes.c_size_t(0)
+    check(lib().roi_extract_workspace_size(num_rois, num_levels, ctypes.byref(n)),
+          "roi_extract_workspace_size")
+    return int(n.value)
+
+
+def plan(features: Sequence, scales: Sequence[float], rois, finest_scale: float = 56.0,
+         levels_out=None, workspace=None, stream=None) -> Tuple[object, object]:
+    """Level of every RoI plus the launch plan.  Returns (roi_levels, workspace)."""
+    torch = _torch()
+    rois = _rois(rois)
+    K, L = rois.shape[0], len(features)
+    if levels_out is None:
+        levels_out = torch.empty(K, dtype=torch.int32, device=rois.device)
+    nbytes = workspace_size(K, L)
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=rois.device)
+    arr = level_array(features, scales)
+    check(lib().roi_extract_plan(arr, L, rois.data_ptr(), K, finest_scale,
+                                 levels_out.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                 stream_handle(stream)), "roi_extract_plan")
+    return levels_out, workspace
+
+
+def plan_offsets(workspace, num_rois: int, num_levels: int, stream=None):
+    torch = _torch()
+    out = torch.empty(num_levels + 1, dtype=torch.int32, device=workspace.device)
+    check(lib().roi_extract_plan_offsets(workspace.data_ptr(), workspace.numel(), num_rois,
+                                         num_levels, out.data_ptr(), stream_handle(stream)),
+          "roi_extract_plan_offsets")
+    return out
+
+
+def plan_perm(workspace, num_rois: int):
+    """The plan's permutation (a view into the workspace)."""
+    ptr = ctypes.c_void_p(0)
+    check(lib().roi_extract_plan_perm(workspace.data_ptr(), workspace.numel(), num_rois,
+                                      ctypes.byref(ptr)), "roi_extract_plan_perm")
+    off = (ptr.value or 0) - workspace.data_ptr()
+    return workspace[off:off + 4 * num_rois].view(_torch().int32)
+
+
+def roi_align_fwd(features: Sequence, scales: Sequence[float], rois, roi_levels,
+                  out_size: Tuple[int, int], sampling_ratio: int = 2, aligned: bool = True,
+                  out_dtype=None, workspace=None, out=None, stream=None):
+    torch = _torch()
+    rois = _rois(rois)
+    K, L = rois.shape[0], len(features)
+    C = features[0].shape[1]
+    ph, pw = out_size
+    odt = out_dtype or features[0].dtype
+    if out is None:
+        out = torch.empty((K, C, ph, pw), dtype=odt, device=rois.device)
+    if not out.is_contiguous():
+        raise ValueError("out must be contiguous [K, C, out_h, out_w]")
+    arr = level_array(features, scales)
+    lv = roi_levels.data_ptr() if roi_levels is not None else None
+    ws = workspace.data_ptr() if workspace is not None else None
+    wsb = workspace.numel() if workspace is not None else 0
+    check(lib().roi_align_fwd(arr, L, rois.data_ptr(), K, lv, ph, pw, sampling_ratio,
+                              int(bool(aligned)), out.data_ptr(), _dtype_code(out), ws, wsb,
+                              stream_handle(stream)), "roi_align_fwd")
+    return out
+
+
+def zero_grad(grads: Sequence, scales: Sequence[float], stream=None):
+    arr = level_array(grads, scales)
+    check(lib().roi_extract_zero_grad(arr, len(grads), stream_handle(stream)),
+          "roi_extract_zero_grad")
+
+
+def roi_align_bwd(grad_out, rois, roi_levels, out_size: Tuple[int, int], sampling_ratio: int,
+                  aligned: bool, grads: Sequence, scales: Sequence[float], zero_init: bool = True,
+                  workspace=None, stream=None):
+    """Accumulate the backward into `grads` (float32 levels, cleared first if zero_init)."""
+    rois = _rois(rois)
+    _need_cuda(grad_out, "grad_out")
+    if not grad_out.is_contiguous():
+        raise ValueError("grad_out must be contiguous [K, C, out_h, out_w]")
+    K, L = rois.shape[0], len(grads)
+    ph, pw = out_size
+    arr = level_array(grads, scales)
+    lv = roi_levels.data_ptr() if roi_levels is not None else None
+    ws = workspace.data_ptr() if workspace is not None else None
+    wsb = workspace.numel() if workspace is not None else 0
+    check(lib().roi_align_bwd(grad_out.data_ptr(), _dtype_code(grad_out), rois.data_ptr(), K, lv,
+                              ph, pw, sampling_ratio, int(bool(aligned)), arr, L,
+                              int(bool(zero_init)), ws, wsb, stream_handle(stream)),
+          "roi_align_bwd")
+    return grads

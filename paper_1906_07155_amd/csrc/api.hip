@@ -1,0 +1,338 @@
+// api.hip -- the C ABI declared in include/roi_extract.h.
+//
+// Every argument is validated on the host before anything is enqueued, and no
+// HIP runtime call is made on an error path, so argument errors are reported the
+// same way with or without a GPU.  The library allocates nothing and keeps no
+// state: all scratch lives in the caller's workspace.
+#include <cmath>
+#include <cstring>
+
+#include "internal.hpp"
+#include "roi_extract.h"
+
+using namespace rex;
+
+namespace {
+
+// Workspace layout: [0, 256) per-level offsets, then perm[K], then keys[K], each
+// region aligned to 256 bytes.
+constexpr size_t kHeader = 256;
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+size_t perm_offset() { return kHeader; }
+size_t keys_offset(int64_t K) { return kHeader + align256(static_cast<size_t>(K) * 4); }
+size_t workspace_bytes_for(int64_t K) {
+    return kHeader + 2 * align256(static_cast<size_t>(K) * 4);
+}
+
+constexpr int64_t kMaxRois = int64_t(1) << 22;
+constexpr int64_t kMaxExtent = int64_t(1) << 24;   // H, W exactly representable in binary32
+
+bool valid_dtype(int32_t d) { return d == RE_DTYPE_F32 || d == RE_DTYPE_BF16; }
+size_t dtype_size(int32_t d) { return d == RE_DTYPE_BF16 ? 2 : 4; }
+
+// Validates a pyramid and fills the kernel table.  `need_data`: data must be non-null.
+re_status_t check_levels(const re_level_t *levels, int32_t num_levels, bool need_data,
+                         LevelTable *t, bool *all_channels_last, int64_t *numel,
+                         int *dense) {
+    if (!levels) return RE_ERR_INVALID_ARG;
+    if (num_levels < 1 || num_levels > RE_MAX_LEVELS) return RE_ERR_INVALID_ARG;
+    std::memset(t, 0, sizeof(*t));
+    bool cl = true;
+    for (int l = 0; l < num_levels; ++l) {
+        const re_level_t &v = levels[l];
+        if (v.reserved != 0 || v.reserved2 != 0.0f) return RE_ERR_INVALID_ARG;
+        if (!valid_dtype(v.dtype)) return RE_ERR_INVALID_ARG;
+        if (v.n < 1 || v.c < 1 || v.h < 1 || v.w < 1) return RE_ERR_INVALID_ARG;
+        if (v.n > INT32_MAX || v.c > INT32_MAX || v.h >= kMaxExtent || v.w >= kMaxExtent)
+            return RE_ERR_INVALID_ARG;
+        if (v.stride_n < 0 || v.stride_c < 0 || v.stride_h < 0 || v.stride_w < 0)
+            return RE_ERR_INVALID_ARG;
+        if (!std::isfinite(v.spatial_scale) || !(v.spatial_scale > 0.0f)) return RE_ERR_INVALID_ARG;
+        if (l > 0 && (v.n != levels[0].n || v.c != levels[0].c || v.dtype != levels[0].dtype))
+            return RE_ERR_INVALID_ARG;
+        if (need_data && !v.data) return RE_ERR_INVALID_ARG;
+        if (v.data && reinterpret_cast<uintptr_t>(v.data) % dtype_size(v.dtype) != 0)
+            return RE_ERR_INVALID_ARG;
+        // largest element offset must fit int64 comfortably
+        const double span = double(v.n - 1) * v.stride_n + double(v.c - 1) * v.stride_c +
+                            double(v.h - 1) * v.stride_h + double(v.w - 1) * v.stride_w;
+        if (span > 9.0e18) return RE_ERR_INVALID_ARG;
+        LevelArg &a = t->l[l];
+        a.data = v.data;
+        a.sn = v.stride_n;
+        a.sc = v.stride_c;
+        a.sh = v.stride_h;
+        a.sw = v.stride_w;
+        a.H = static_cast<int32_t>(v.h);
+        a.W = static_cast<int32_t>(v.w);
+        a.scale = v.spatial_scale;
+        if (v.stride_c != 1) cl = false;
+        if (numel) numel[l] = v.n * v.c * v.h * v.w;
+        if (dense) {
+            // dense: the strides are those of a contiguous tensor for some order of dims
+            int64_t ext[4] = {v.n, v.c, v.h, v.w};
+            int64_t str[4] = {v.stride_n, v.stride_c, v.stride_h, v.stride_w};
+            int order[4] = {0, 1, 2, 3};
+            for (int i = 0; i < 4; ++i)
+                for (int j = i + 1; j < 4; ++j)
+                    if (str[order[j]] < str[order[i]] ||
+                        (str[order[j]] == str[order[i]] && ext[order[j]] < ext[order[i]])) {
+                        const int tmp = order[i];
+                        order[i] = order[j];
+                        order[j] = tmp;
+                    }
+            int64_t expect = 1;
+            bool ok = true;
+            for (int i = 0; i < 4; ++i) {
+                const int d = order[i];
+                if (ext[d] == 1) continue;
+                if (str[d] != expect) ok = false;
+                expect *= ext[d];
+            }
+            dense[l] = ok ? 1 : 0;
+        }
+    }
+    t->num = num_levels;
+    t->N = static_cast<int32_t>(levels[0].n);
+    t->C = static_cast<int32_t>(levels[0].c);
+    if (all_channels_last) *all_channels_last = cl;
+    return RE_OK;
+}
+
+re_status_t check_common(const float *rois, int64_t K, const int32_t *roi_levels,
+                         int32_t num_levels, int32_t out_h, int32_t out_w,
+                         int32_t sampling_ratio, int32_t aligned) {
+    if (K < 0 || K > kMaxRois) return RE_ERR_INVALID_ARG;
+    if (K > 0 && !rois) return RE_ERR_INVALID_ARG;
+    if (K > 0 && num_levels > 1 && !roi_levels) return RE_ERR_INVALID_ARG;
+    if (out_h < 1 || out_w < 1 || out_h > RE_MAX_OUT || out_w > RE_MAX_OUT)
+        return RE_ERR_INVALID_ARG;
+    if (sampling_ratio < 0 || sampling_ratio > RE_MAX_SAMPLING) return RE_ERR_INVALID_ARG;
+    if (aligned != 0 && aligned != 1) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(rois) % 4 != 0) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(roi_levels) % 4 != 0) return RE_ERR_INVALID_ARG;
+    return RE_OK;
+}
+
+re_status_t check_plan(const void *plan, size_t plan_bytes, int64_t K) {
+    if (!plan) return RE_OK;
+    if (reinterpret_cast<uintptr_t>(plan) % 256 != 0) return RE_ERR_WORKSPACE;
+    if (plan_bytes < workspace_bytes_for(K)) return RE_ERR_WORKSPACE;
+    return RE_OK;
+}
+
+re_status_t from_hip(hipError_t e) { return e == hipSuccess ? RE_OK : RE_ERR_DEVICE; }
+
+}  // namespace
+
+extern "C" {
+
+const char *roi_extract_version(void) { return "roi_extract 0.1 (gfx950)"; }
+
+const char *roi_extract_status_str(re_status_t s) {
+    switch (s) {
+        case RE_OK: return "ok";
+        case RE_ERR_INVALID_ARG: return "invalid argument";
+        case RE_ERR_UNSUPPORTED: return "unsupported";
+        case RE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+        case RE_ERR_DEVICE: return "HIP runtime or kernel launch error";
+    }
+    return "unknown status";
+}
+
+re_status_t roi_extract_workspace_size(int64_t num_rois, int32_t num_levels, size_t *bytes) {
+    if (!bytes || num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
+    if (num_levels < 1 || num_levels > RE_MAX_LEVELS) return RE_ERR_INVALID_ARG;
+    *bytes = workspace_bytes_for(num_rois);
+    return RE_OK;
+}
+
+re_status_t fpn_level_map(const float *rois, int64_t num_rois, int32_t num_levels,
+                          float finest_scale, int32_t *levels_out, void *stream) {
+    if (num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
+    if (num_levels < 1 || num_levels > RE_MAX_LEVELS) return RE_ERR_INVALID_ARG;
+    if (!std::isfinite(finest_scale) || !(finest_scale > 0.0f)) return RE_ERR_INVALID_ARG;
+    if (num_rois == 0) return RE_OK;
+    if (!rois || !levels_out) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(rois) % 4 || reinterpret_cast<uintptr_t>(levels_out) % 4)
+        return RE_ERR_INVALID_ARG;
+    return from_hip(launch_level_map(rois, static_cast<int32_t>(num_rois), num_levels,
+                                     finest_scale, levels_out,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+re_status_t roi_extract_plan(const re_level_t *levels, int32_t num_levels, const float *rois,
+                             int64_t num_rois, float finest_scale, int32_t *levels_out,
+                             void *workspace, size_t workspace_bytes, void *stream) {
+    LevelTable t;
+    re_status_t st = check_levels(levels, num_levels, false, &t, nullptr, nullptr, nullptr);
+    if (st != RE_OK) return st;
+    if (num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
+    if (!std::isfinite(finest_scale) || !(finest_scale > 0.0f)) return RE_ERR_INVALID_ARG;
+    if (!workspace) return RE_ERR_WORKSPACE;
+    if ((st = check_plan(workspace, workspace_bytes, num_rois)) != RE_OK) return st;
+    if (num_rois > 0 && (!rois || !levels_out)) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(rois) % 4 || reinterpret_cast<uintptr_t>(levels_out) % 4)
+        return RE_ERR_INVALID_ARG;
+
+    PlanArgs a{};
+    char *ws = static_cast<char *>(workspace);
+    a.rois = rois;
+    a.levels_out = levels_out;
+    a.offsets = reinterpret_cast<int32_t *>(ws);
+    a.perm = reinterpret_cast<int32_t *>(ws + perm_offset());
+    a.keys = reinterpret_cast<int32_t *>(ws + keys_offset(num_rois));
+    a.K = static_cast<int32_t>(num_rois);
+    a.L = num_levels;
+    a.finest_scale = finest_scale;
+    a.N = t.N;
+    // Cell size 2^shift feature pixels: the smallest shift >= 4 whose bucket count fits.
+    a.batch_in_key = 1;
+    int shift = 4;
+    int64_t nbins = 0;
+    for (;; ++shift) {
+        nbins = 0;
+        for (int l = 0; l < num_levels; ++l) {
+            const int64_t ncx = (t.l[l].W + (int64_t(1) << shift) - 1) >> shift;
+            const int64_t ncy = (t.l[l].H + (int64_t(1) << shift) - 1) >> shift;
+            nbins += (a.batch_in_key ? t.N : 1) * ncx * ncy;
+        }
+        if (nbins <= kPlanMaxBins) break;
+        if (shift >= 24) {
+            if (!a.batch_in_key) return RE_ERR_UNSUPPORTED;
+            a.batch_in_key = 0;   // very large batches: bucket by level and cell only
+            shift = 3;
+        }
+    }
+    a.cell_shift = shift;
+    a.nbins = static_cast<int32_t>(nbins);
+    int32_t base = 0;
+    for (int l = 0; l < num_levels; ++l) {
+        a.H[l] = t.l[l].H;
+        a.W[l] = t.l[l].W;
+        a.scale[l] = t.l[l].scale;
+        a.ncx[l] = static_cast<int32_t>((t.l[l].W + (1 << shift) - 1) >> shift);
+        a.ncy[l] = static_cast<int32_t>((t.l[l].H + (1 << shift) - 1) >> shift);
+        a.base[l] = base;
+        base += (a.batch_in_key ? t.N : 1) * a.ncx[l] * a.ncy[l];
+    }
+    return from_hip(launch_plan(a, static_cast<hipStream_t>(stream)));
+}
+
+re_status_t roi_extract_plan_perm(const void *workspace, size_t workspace_bytes,
+                                  int64_t num_rois, const int32_t **perm_out) {
+    if (!perm_out || !workspace) return RE_ERR_INVALID_ARG;
+    if (num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
+    re_status_t st = check_plan(workspace, workspace_bytes, num_rois);
+    if (st != RE_OK) return st;
+    *perm_out = reinterpret_cast<const int32_t *>(static_cast<const char *>(workspace) +
+                                                  perm_offset());
+    return RE_OK;
+}
+
+re_status_t roi_extract_plan_offsets(const void *workspace, size_t workspace_bytes,
+                                     int64_t num_rois, int32_t num_levels,
+                                     int32_t *offsets_out, void *stream) {
+    if (!workspace || !offsets_out) return RE_ERR_INVALID_ARG;
+    if (num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
+    if (num_levels < 1 || num_levels > RE_MAX_LEVELS) return RE_ERR_INVALID_ARG;
+    re_status_t st = check_plan(workspace, workspace_bytes, num_rois);
+    if (st != RE_OK) return st;
+    return from_hip(hipMemcpyAsync(offsets_out, workspace, (num_levels + 1) * sizeof(int32_t),
+                                   hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream)));
+}
+
+re_status_t roi_align_fwd(const re_level_t *levels, int32_t num_levels, const float *rois,
+                          int64_t num_rois, const int32_t *roi_levels, int32_t out_h,
+                          int32_t out_w, int32_t sampling_ratio, int32_t aligned, void *out,
+                          int32_t out_dtype, const void *plan, size_t plan_bytes,
+                          void *stream) {
+    LevelTable t;
+    bool cl = false;
+    re_status_t st = check_levels(levels, num_levels, true, &t, &cl, nullptr, nullptr);
+    if (st != RE_OK) return st;
+    if ((st = check_common(rois, num_rois, roi_levels, num_levels, out_h, out_w,
+                           sampling_ratio, aligned)) != RE_OK)
+        return st;
+    if (!valid_dtype(out_dtype)) return RE_ERR_INVALID_ARG;
+    if (num_rois > 0 && !out) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(out) % dtype_size(out_dtype)) return RE_ERR_INVALID_ARG;
+    if ((st = check_plan(plan, plan_bytes, num_rois)) != RE_OK) return st;
+    if (num_rois == 0) return RE_OK;
+
+    FwdArgs a{};
+    a.lv = t;
+    a.rois = rois;
+    a.roi_levels = roi_levels;
+    a.perm = plan ? reinterpret_cast<const int32_t *>(static_cast<const char *>(plan) +
+                                                      perm_offset())
+                  : nullptr;
+    a.out = out;
+    a.K = static_cast<int32_t>(num_rois);
+    a.PH = out_h;
+    a.PW = out_w;
+    a.S = sampling_ratio;
+    a.aligned = aligned;
+    const bool fast = cl && fwd_fast_available(out_h, out_w, sampling_ratio);
+    return from_hip(launch_fwd(a, levels[0].dtype, out_dtype, fast,
+                               static_cast<hipStream_t>(stream)));
+}
+
+re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_levels,
+                                  void *stream) {
+    LevelTable t;
+    int64_t numel[RE_MAX_LEVELS] = {0};
+    int dense[RE_MAX_LEVELS] = {0};
+    re_status_t st = check_levels(grad_levels, num_levels, true, &t, nullptr, numel, dense);
+    if (st != RE_OK) return st;
+    for (int l = 0; l < num_levels; ++l)
+        if (grad_levels[l].dtype != RE_DTYPE_F32) return RE_ERR_UNSUPPORTED;
+    return from_hip(launch_zero(t, numel, dense, static_cast<hipStream_t>(stream)));
+}
+
+re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype, const float *rois,
+                          int64_t num_rois, const int32_t *roi_levels, int32_t out_h,
+                          int32_t out_w, int32_t sampling_ratio, int32_t aligned,
+                          const re_level_t *grad_levels, int32_t num_levels, int32_t zero_init,
+                          const void *plan, size_t plan_bytes, void *stream) {
+    LevelTable t;
+    bool cl = false;
+    int64_t numel[RE_MAX_LEVELS] = {0};
+    int dense[RE_MAX_LEVELS] = {0};
+    re_status_t st = check_levels(grad_levels, num_levels, true, &t, &cl, numel, dense);
+    if (st != RE_OK) return st;
+    for (int l = 0; l < num_levels; ++l)
+        if (grad_levels[l].dtype != RE_DTYPE_F32) return RE_ERR_UNSUPPORTED;
+    if ((st = check_common(rois, num_rois, roi_levels, num_levels, out_h, out_w,
+                           sampling_ratio, aligned)) != RE_OK)
+        return st;
+    if (!valid_dtype(grad_out_dtype)) return RE_ERR_INVALID_ARG;
+    if (num_rois > 0 && !grad_out) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(grad_out) % dtype_size(grad_out_dtype))
+        return RE_ERR_INVALID_ARG;
+    if (zero_init != 0 && zero_init != 1) return RE_ERR_INVALID_ARG;
+    if ((st = check_plan(plan, plan_bytes, num_rois)) != RE_OK) return st;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (zero_init) {
+        if ((st = from_hip(launch_zero(t, numel, dense, s))) != RE_OK) return st;
+    }
+    if (num_rois == 0) return RE_OK;
+    BwdArgs a{};
+    a.lv = t;
+    a.gout = grad_out;
+    a.rois = rois;
+    a.roi_levels = roi_levels;
+    a.perm = plan ? reinterpret_cast<const int32_t *>(static_cast<const char *>(plan) +
+                                                      perm_offset())
+                  : nullptr;
+    a.K = static_cast<int32_t>(num_rois);
+    a.PH = out_h;
+    a.PW = out_w;
+    a.S = sampling_ratio;
+    a.aligned = aligned;
+    const bool fast = cl && bwd_fast_available(out_h, out_w, sampling_ratio);
+    return from_hip(launch_bwd(a, grad_out_dtype, fast, s));
+}
+
+}  // extern "C"

@@ -1,0 +1,222 @@
+// common.hpp -- device-side building blocks shared by the RoIAlign kernels.
+//
+// Geometry follows the definition stated in include/roi_extract.h: the sample
+// coordinates are computed in binary32 with one rounding per operation, in the
+// written order, with no contraction into fused multiply-adds (the whole library
+// is compiled with -ffp-contract=off; accumulations that should fuse call fmaf
+// explicitly).  Division is the correctly rounded IEEE division (hipcc's default).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rex {
+
+constexpr int kMaxLevels = 8;
+constexpr int kGridCap = 64;   // adaptive sampling grid cap (RE_MAX_SAMPLING)
+
+enum : int { kF32 = 0, kBF16 = 1 };
+
+// One pyramid level as the kernels see it.  Strides are in elements.
+struct LevelArg {
+    const void *data;
+    int64_t sn, sc, sh, sw;
+    int32_t H, W;
+    float scale;
+    int32_t pad;
+};
+
+struct LevelTable {
+    LevelArg l[kMaxLevels];
+    int32_t num;
+    int32_t N;
+    int32_t C;
+    int32_t pad;
+};
+
+// Level `l` of the table.  Every access uses a constant index so the kernel
+// argument block is read straight from the kernarg segment (no scratch copy).
+__device__ __forceinline__ LevelArg level_at(const LevelTable &t, int l) {
+    switch (l) {
+        case 1: return t.l[1];
+        case 2: return t.l[2];
+        case 3: return t.l[3];
+        case 4: return t.l[4];
+        case 5: return t.l[5];
+        case 6: return t.l[6];
+        case 7: return t.l[7];
+        default: return t.l[0];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// bfloat16 <-> binary32
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round to nearest, ties to even, on the 16 discarded bits; NaN stays a quiet NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+// Pointers into global memory.  Data pointers that arrive inside an argument
+// struct lose their address space, which would turn every access into a flat
+// instruction; these casts restore it.
+#define REX_GLOBAL __attribute__((address_space(1)))
+template <typename T> using gptr = REX_GLOBAL T *;
+template <typename T> using gcptr = const REX_GLOBAL T *;
+template <typename T> __device__ __forceinline__ gcptr<T> as_global(const void *p) {
+    return (gcptr<T>)(p);
+}
+template <typename T> __device__ __forceinline__ gptr<T> as_global_mut(void *p) {
+    return (gptr<T>)(p);
+}
+
+template <typename T> __device__ __forceinline__ float load_f32(gcptr<T> p);
+template <> __device__ __forceinline__ float load_f32<float>(gcptr<float> p) { return *p; }
+template <> __device__ __forceinline__ float load_f32<uint16_t>(gcptr<uint16_t> p) {
+    return bf16_to_f32(*p);
+}
+
+template <typename T> __device__ __forceinline__ void store_f32(gptr<T> p, float v);
+template <> __device__ __forceinline__ void store_f32<float>(gptr<float> p, float v) { *p = v; }
+template <> __device__ __forceinline__ void store_f32<uint16_t>(gptr<uint16_t> p, float v) {
+    *p = f32_to_bf16(v);
+}
+
+// ---------------------------------------------------------------------------
+// FPN level (threshold form), binary32
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int fpn_level(float x1, float y1, float x2, float y2, int num_levels,
+                                         float finest_scale) {
+    const float w = x2 - x1;
+    const float h = y2 - y1;
+    const float area = w * h;
+    int lvl = 0;
+    for (int j = 1; j < num_levels; ++j) {
+        const float side = finest_scale * static_cast<float>(1 << j);
+        const float thr = side * side;
+        lvl += (area >= thr) ? 1 : 0;
+    }
+    return lvl;
+}
+
+// Column 0 of a RoI: truncated toward zero; -1 if it names no image of the batch.
+__device__ __forceinline__ int roi_batch(float v, int n) {
+    const float t = truncf(v);
+    if (!(t >= 0.0f) || !(t < static_cast<float>(n))) return -1;
+    return static_cast<int>(t);
+}
+
+// ---------------------------------------------------------------------------
+// Sampling geometry along one axis
+// ---------------------------------------------------------------------------
+
+struct Axis {
+    float start;
+    float bin;
+    int grid;
+};
+
+__device__ __forceinline__ Axis axis_setup(float c1, float c2, float scale, int aligned, int P,
+                                           int S) {
+    const float off = aligned ? 0.5f : 0.0f;
+    float s = c1 * scale;
+    s = s - off;
+    float e = c2 * scale;
+    e = e - off;
+    float len = e - s;
+    if (!aligned) len = fmaxf(len, 1.0f);
+    const float bin = len / static_cast<float>(P);
+    int g;
+    if (S > 0) {
+        g = S;
+    } else if (!(bin > 0.0f)) {
+        g = 0;
+    } else {
+        const float cg = ceilf(bin);
+        g = cg > static_cast<float>(kGridCap) ? kGridCap : static_cast<int>(cg);
+    }
+    Axis a;
+    a.start = s;
+    a.bin = bin;
+    a.grid = g;
+    return a;
+}
+
+// Bilinear neighbours of one sample.  lo < 0 marks a sample outside [-1, size].
+struct Tap {
+    int lo;
+    int hi;
+    float wlo;
+    float whi;
+};
+
+__device__ __forceinline__ Tap axis_tap(const Axis &a, int p, int i, int size) {
+    const float t1 = static_cast<float>(p) * a.bin;
+    const float t2 = a.start + t1;
+    const float t3 = static_cast<float>(i) + 0.5f;
+    const float t4 = t3 * a.bin;
+    const float t5 = t4 / static_cast<float>(a.grid);
+    float v = t2 + t5;
+    Tap t;
+    if (v < -1.0f || v > static_cast<float>(size)) {
+        t.lo = -1;
+        t.hi = -1;
+        t.wlo = 0.0f;
+        t.whi = 0.0f;
+        return t;
+    }
+    v = fmaxf(v, 0.0f);
+    int lo = static_cast<int>(v);
+    int hi;
+    if (lo >= size - 1) {
+        lo = size - 1;
+        hi = size - 1;
+        v = static_cast<float>(lo);
+    } else {
+        hi = lo + 1;
+    }
+    const float frac = v - static_cast<float>(lo);
+    t.lo = lo;
+    t.hi = hi;
+    t.wlo = 1.0f - frac;
+    t.whi = frac;
+    return t;
+}
+
+// ---------------------------------------------------------------------------
+// Launch-order helpers
+// ---------------------------------------------------------------------------
+
+// Consecutive workgroup ids are dispatched round-robin over the 8 XCDs of an
+// MI355X.  Map them so XCD x receives one contiguous slice of the logical order,
+// which keeps neighbouring (plan-sorted) RoIs inside one XCD's L2.  Bijective on
+// [0, n) for any n.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t n) {
+    constexpr uint32_t X = 8;
+    const uint32_t q = n / X, r = n % X;
+    const uint32_t x = bid % X, i = bid / X;
+    return (x < r) ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+}
+
+// Orders LDS writes and later LDS reads of other lanes within one wavefront.
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ int uniform_i(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ float uniform_f(float v) {
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
+
+}  // namespace rex

@@ -1,0 +1,76 @@
+// internal.hpp -- argument blocks and launchers shared by the host API and the
+// kernel translation units.  Not part of the public ABI.
+#pragma once
+
+#include "common.hpp"
+
+namespace rex {
+
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanMaxBins = 15360;   // LDS histogram + scan scratch of the plan kernel = 64 KiB
+
+struct PlanArgs {
+    const float *rois;
+    int32_t *levels_out;
+    int32_t *keys;
+    int32_t *perm;
+    int32_t *offsets;      // [L + 1]
+    int32_t K;
+    int32_t L;
+    float finest_scale;
+    int32_t N;
+    int32_t nbins;
+    int32_t cell_shift;    // spatial cell = 2^cell_shift feature pixels
+    int32_t batch_in_key;
+    int32_t pad;
+    int32_t H[kMaxLevels], W[kMaxLevels];
+    int32_t ncx[kMaxLevels], ncy[kMaxLevels], base[kMaxLevels];
+    float scale[kMaxLevels];
+};
+
+struct FwdArgs {
+    LevelTable lv;
+    const float *rois;
+    const int32_t *roi_levels;   // may be null when lv.num == 1
+    const int32_t *perm;         // plan order or null
+    void *out;
+    int32_t K;
+    int32_t PH, PW, S;
+    int32_t aligned;
+    int32_t nslices;             // channel slices per RoI (fast kernels)
+    int32_t wg_per_roi;          // workgroups per RoI (fast kernels)
+    int32_t pad;
+};
+
+struct BwdArgs {
+    LevelTable lv;               // gradient levels (binary32, written with atomics)
+    const void *gout;
+    const float *rois;
+    const int32_t *roi_levels;
+    const int32_t *perm;
+    int32_t K;
+    int32_t PH, PW, S;
+    int32_t aligned;
+    int32_t nslices;
+    int32_t wg_per_roi;
+    int32_t pad;
+};
+
+hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float finest_scale,
+                            int32_t *out, hipStream_t stream);
+hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);
+
+// Forward: `fast` selects the channels-last kernels (every level stride_c == 1 and
+// (PH, PW, S) in the specialised set); otherwise the general strided kernel.
+bool fwd_fast_available(int PH, int PW, int S);
+hipError_t launch_fwd(FwdArgs a, int feat_dtype, int out_dtype, bool fast, hipStream_t stream);
+
+bool bwd_fast_available(int PH, int PW, int S);
+hipError_t launch_bwd(BwdArgs a, int gout_dtype, bool fast, hipStream_t stream);
+
+// Zero every element of the (binary32) levels in `lv`; `numel[l]` and `dense[l]`
+// describe each level (dense levels are cleared as flat arrays).
+hipError_t launch_zero(const LevelTable &lv, const int64_t *numel, const int *dense,
+                       hipStream_t stream);
+
+}  // namespace rex

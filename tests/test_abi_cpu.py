@@ -1,0 +1,166 @@
+"""The C ABI on the host: the library loads, exports every declared symbol, and
+rejects bad arguments with its documented status codes before enqueuing anything.
+
+No call here reaches a kernel launch, so these run without a GPU.  Device pointers
+are stand-in addresses that the library never dereferences on an error path.
+"""
+import ctypes
+import math
+import subprocess
+
+import pytest
+
+from paper_1906_07155_amd import binding as B
+
+OK, INVALID, UNSUPPORTED, WORKSPACE, DEVICE = range(5)
+FAKE = 0x10000          # a 64 KiB-aligned stand-in device address (never dereferenced)
+
+
+@pytest.fixture(scope="module")
+def L():
+    return B.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = B.header_functions()
+    assert len(names) >= 10
+    out = subprocess.check_output(["nm", "-D", "--defined-only", B.LIBRARY]).decode()
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for n in names:
+        assert n in exported, n
+        assert hasattr(L, n)
+
+
+def test_status_strings_and_version(L):
+    for s in range(5):
+        assert L.roi_extract_status_str(s)
+    assert b"unknown" in L.roi_extract_status_str(99)
+    assert b"gfx950" in L.roi_extract_version()
+
+
+def test_workspace_size(L):
+    n = ctypes.c_size_t(0)
+    assert L.roi_extract_workspace_size(0, 4, ctypes.byref(n)) == OK
+    base = n.value
+    assert L.roi_extract_workspace_size(1024, 4, ctypes.byref(n)) == OK
+    assert n.value >= base + 8 * 1024 and n.value % 256 == 0
+    assert L.roi_extract_workspace_size(-1, 4, ctypes.byref(n)) == INVALID
+    assert L.roi_extract_workspace_size(10, 0, ctypes.byref(n)) == INVALID
+    assert L.roi_extract_workspace_size(10, 9, ctypes.byref(n)) == INVALID
+    assert L.roi_extract_workspace_size(10, 4, None) == INVALID
+
+
+def _levels(n=2, c=8, hw=((16, 20), (8, 10)), dtype=0, scales=(0.25, 0.125), data=FAKE):
+    arr = (B.ReLevel * len(hw))()
+    for i, ((h, w), s) in enumerate(zip(hw, scales)):
+        # channels-last strides
+        arr[i] = B.ReLevel(data, dtype, 0, n, c, h, w, h * w * c, 1, w * c, c, s, 0.0)
+    return arr
+
+
+def _fwd(L, levels=None, nl=2, rois=FAKE, K=4, roi_levels=FAKE, oh=7, ow=7, sr=2, al=1,
+         out=FAKE, odt=0, plan=None, plan_bytes=0):
+    levels = levels if levels is not None else _levels()
+    return L.roi_align_fwd(levels, nl, rois, K, roi_levels, oh, ow, sr, al, out, odt, plan,
+                           plan_bytes, None)
+
+
+def _bwd(L, levels=None, nl=2, gout=FAKE, gdt=0, K=4, zero=0, sr=2, al=1, oh=7, ow=7,
+         plan=None, plan_bytes=0):
+    levels = levels if levels is not None else _levels()
+    return L.roi_align_bwd(gout, gdt, FAKE, K, FAKE, oh, ow, sr, al, levels, nl, zero, plan,
+                           plan_bytes, None)
+
+
+def test_level_map_validation(L):
+    assert L.fpn_level_map(FAKE, -1, 4, 56.0, FAKE, None) == INVALID
+    assert L.fpn_level_map(FAKE, 3, 0, 56.0, FAKE, None) == INVALID
+    assert L.fpn_level_map(FAKE, 3, 9, 56.0, FAKE, None) == INVALID
+    for s in (0.0, -1.0, math.inf, math.nan):
+        assert L.fpn_level_map(FAKE, 3, 4, s, FAKE, None) == INVALID
+    assert L.fpn_level_map(None, 3, 4, 56.0, FAKE, None) == INVALID
+    assert L.fpn_level_map(FAKE, 3, 4, 56.0, None, None) == INVALID
+    assert L.fpn_level_map(FAKE + 2, 3, 4, 56.0, FAKE, None) == INVALID
+    assert L.fpn_level_map(None, 0, 4, 56.0, None, None) == OK      # nothing to do
+
+
+def test_forward_validation(L):
+    assert _fwd(L, K=0) == OK                                      # nothing to do
+    assert _fwd(L, levels=None, nl=0) == INVALID
+    assert _fwd(L, nl=9) == INVALID
+    assert L.roi_align_fwd(None, 2, FAKE, 4, FAKE, 7, 7, 2, 1, FAKE, 0, None, 0, None) == INVALID
+    assert _fwd(L, K=-1) == INVALID
+    assert _fwd(L, K=(1 << 22) + 1) == INVALID
+    assert _fwd(L, rois=None) == INVALID
+    assert _fwd(L, rois=FAKE + 1) == INVALID
+    assert _fwd(L, roi_levels=None) == INVALID                     # several levels need them
+    assert _fwd(L, oh=0) == INVALID
+    assert _fwd(L, ow=257) == INVALID
+    assert _fwd(L, sr=-1) == INVALID
+    assert _fwd(L, sr=65) == INVALID
+    assert _fwd(L, al=2) == INVALID
+    assert _fwd(L, out=None) == INVALID
+    assert _fwd(L, odt=7) == INVALID
+    assert _fwd(L, odt=0, out=FAKE + 2) == INVALID                 # fp32 output misaligned
+    assert _fwd(L, plan=FAKE, plan_bytes=16) == WORKSPACE
+    assert _fwd(L, plan=FAKE + 64, plan_bytes=1 << 20) == WORKSPACE  # plan not 256-aligned
+
+
+@pytest.mark.parametrize("field,value", [
+    ("dtype", 5), ("reserved", 1), ("n", 0), ("c", 0), ("h", 0), ("w", 0), ("h", 1 << 24),
+    ("stride_h", -1), ("spatial_scale", 0.0), ("spatial_scale", -0.5),
+    ("spatial_scale", math.inf), ("spatial_scale", math.nan), ("data", None),
+    ("reserved2", 1.0)])
+def test_forward_rejects_bad_level(L, field, value):
+    lv = _levels()
+    setattr(lv[1], field, value)
+    assert _fwd(L, levels=lv) == INVALID
+
+
+def test_forward_rejects_mismatched_levels(L):
+    lv = _levels()
+    lv[1].n = 3
+    assert _fwd(L, levels=lv) == INVALID
+    lv = _levels()
+    lv[1].c = 16
+    assert _fwd(L, levels=lv) == INVALID
+    lv = _levels()
+    lv[1].dtype = 1
+    assert _fwd(L, levels=lv) == INVALID
+    lv = _levels(data=FAKE + 2)                                    # fp32 data misaligned
+    assert _fwd(L, levels=lv) == INVALID
+
+
+def test_backward_validation(L):
+    assert _bwd(L, levels=_levels(dtype=1)) == UNSUPPORTED         # gradient levels must be fp32
+    assert _bwd(L, zero=2) == INVALID
+    assert _bwd(L, gout=None) == INVALID
+    assert _bwd(L, gdt=3) == INVALID
+    assert _bwd(L, gdt=0, gout=FAKE + 2) == INVALID
+    assert _bwd(L, sr=-2) == INVALID
+    assert _bwd(L, plan=FAKE, plan_bytes=8) == WORKSPACE
+    assert _bwd(L, K=0, zero=0) == OK                              # nothing to do
+    assert L.roi_extract_zero_grad(_levels(dtype=1), 2, None) == UNSUPPORTED
+    assert L.roi_extract_zero_grad(None, 2, None) == INVALID
+
+
+def test_plan_validation(L):
+    lv = _levels()
+    n = ctypes.c_size_t(0)
+    assert L.roi_extract_workspace_size(4, 2, ctypes.byref(n)) == OK
+    assert L.roi_extract_plan(lv, 2, FAKE, 4, 56.0, FAKE, None, n.value, None) == WORKSPACE
+    assert L.roi_extract_plan(lv, 2, FAKE, 4, 56.0, FAKE, FAKE, n.value - 1, None) == WORKSPACE
+    assert L.roi_extract_plan(lv, 2, FAKE, 4, 0.0, FAKE, FAKE, n.value, None) == INVALID
+    assert L.roi_extract_plan(lv, 2, None, 4, 56.0, FAKE, FAKE, n.value, None) == INVALID
+    assert L.roi_extract_plan(lv, 0, FAKE, 4, 56.0, FAKE, FAKE, n.value, None) == INVALID
+    p = ctypes.c_void_p(0)
+    assert L.roi_extract_plan_perm(FAKE, n.value, 4, ctypes.byref(p)) == OK
+    assert p.value == FAKE + 256                                   # perm follows the header
+    assert L.roi_extract_plan_perm(FAKE, 16, 4, ctypes.byref(p)) == WORKSPACE
+    assert L.roi_extract_plan_perm(None, n.value, 4, ctypes.byref(p)) == INVALID
+    assert L.roi_extract_plan_offsets(FAKE, n.value, 4, 0, FAKE, None) == INVALID
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(RuntimeError):
+        B.lib(str(tmp_path / "missing.so"))

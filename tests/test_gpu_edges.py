@@ -1,0 +1,253 @@
+"""GPU edge cases and invariants, each against the CPU oracle.
+
+Small shapes that still span several channel slices with a ragged tail, every
+kernel family (channels-last fast path, general strided path), both dtypes, and
+the degenerate inputs the operator has.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1906_07155_amd as rex
+from paper_1906_07155_amd import workloads as W
+from gpu_helpers import as_f64, check_bwd, check_fwd, from_device, log, to_device
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rex.lib()
+
+
+def _feats(rng, shapes, fdt):
+    out = []
+    for s in shapes:
+        x = rng.standard_normal(s, dtype=np.float32)
+        out.append(W.f32_to_bf16_bits(x) if fdt == "bf16" else x)
+    return out
+
+
+def _device_levels(feats_np, fdt, layout):
+    if layout in ("cl", "nchw"):
+        return [to_device(f, fdt, layout) for f in feats_np]
+    # strided views into larger tensors: 'cl_view' keeps stride_c == 1, 'nchw_view' does not
+    views = []
+    for f in feats_np:
+        n, c, h, w = f.shape
+        big = np.zeros((n, c + 5, h + 2, w + 3), dtype=f.dtype)
+        big[:, 2:2 + c, 1:1 + h, :w] = f
+        t = to_device(big, fdt, "cl" if layout == "cl_view" else "nchw")
+        views.append(t[:, 2:2 + c, 1:1 + h, :w])
+    return views
+
+
+def _rois(rng, K, n_images, img_w, img_h, outside=0.2):
+    a = rng.uniform(-outside * img_w, (1 + outside) * img_w, (K, 2))
+    b = rng.uniform(-outside * img_h, (1 + outside) * img_h, (K, 2))
+    r = np.zeros((K, 5), np.float32)
+    r[:, 0] = rng.integers(0, n_images, K)
+    r[:, 1], r[:, 3] = a.min(1), a.max(1)
+    r[:, 2], r[:, 4] = b.min(1), b.max(1)
+    return r
+
+
+def run(name, shapes, scales, rois, out_hw=(7, 7), S=2, aligned=True, fdt="f32", odt="f32",
+        gdt="f32", layout="cl", roi_levels=None, use_plan=True, seed=0, backward=True):
+    log("edge case %s: shapes=%s K=%d out=%s S=%d aligned=%d %s->%s layout=%s" % (
+        name, shapes, rois.shape[0], out_hw, S, aligned, fdt, odt, layout))
+    rng = np.random.default_rng(seed)
+    feats_np = _feats(rng, shapes, fdt)
+    feats = _device_levels(feats_np, fdt, layout)
+    K = rois.shape[0]
+    C = shapes[0][1]
+    L = len(shapes)
+    r_dev = torch.from_numpy(rois).cuda()
+    ws = None
+    if roi_levels is None:
+        lv_dev, ws = rex.plan(feats, scales, r_dev, 56.0)
+        lv = oracle.level_map(rois, L, 56.0)
+        if not use_plan:
+            ws = None
+    else:
+        lv = np.asarray(roi_levels, np.int32)
+        lv_dev = torch.from_numpy(lv).cuda()
+    odt_t = torch.bfloat16 if odt == "bf16" else torch.float32
+    out = rex.roi_align_fwd(feats, scales, r_dev, lv_dev, out_hw, S, aligned, out_dtype=odt_t,
+                            workspace=ws)
+    torch.cuda.synchronize()
+    f64 = [as_f64(f, fdt) for f in feats_np]
+    ref = oracle.roi_align_fwd(f64, scales, rois, lv, out_hw[0], out_hw[1], S, aligned, "parity")
+    check_fwd(from_device(out), ref, fdt == "bf16" or odt == "bf16", name + " forward")
+    if not backward:
+        return out
+    g = rng.standard_normal((K, C) + tuple(out_hw), dtype=np.float32)
+    if gdt == "bf16":
+        g = W.f32_to_bf16_bits(g)
+    grads = [torch.full(s, 7.0, dtype=torch.float32, device="cuda") for s in shapes]
+    if layout in ("cl", "cl_view"):
+        grads = [x.contiguous(memory_format=torch.channels_last) for x in grads]
+    rex.roi_align_bwd(to_device(g, gdt, "nchw"), r_dev, lv_dev, out_hw, S, aligned, grads,
+                      scales, zero_init=True, workspace=ws)
+    torch.cuda.synchronize()
+    g64 = as_f64(g, gdt)
+    gref = oracle.roi_align_bwd(g64, shapes, scales, rois, lv, out_hw[0], out_hw[1], S, aligned,
+                                "parity")
+    aref = oracle.roi_align_bwd(np.abs(g64), shapes, scales, rois, lv, out_hw[0], out_hw[1], S,
+                                aligned, "parity")
+    for l in range(L):
+        check_bwd(from_device(grads[l]), gref[l], aref[l], False, "%s backward level %d" % (name, l))
+    return out
+
+
+PYR = [(2, 100, 24, 40), (2, 100, 12, 20), (2, 100, 6, 10), (2, 100, 3, 5)]
+SC = [0.25, 0.125, 0.0625, 0.03125]
+
+
+def _pyr(c):
+    return [(n, c, h, w) for (n, _, h, w) in PYR]
+
+
+@pytest.mark.parametrize("out_hw", [(7, 7), (14, 14)])
+@pytest.mark.parametrize("C", [1, 3, 100, 256, 320])
+def test_channels_ragged(out_hw, C):
+    rng = np.random.default_rng(C)
+    rois = W.draw_rois(rng, 2, 19, (96, 160), (4.0, 200.0))
+    run("C=%d %s" % (C, out_hw), _pyr(C), SC, rois, out_hw=out_hw)
+
+
+@pytest.mark.parametrize("S", [0, 1, 2, 3])
+@pytest.mark.parametrize("aligned", [True, False])
+def test_sampling_and_alignment(S, aligned):
+    rng = np.random.default_rng(10 + S)
+    rois = _rois(rng, 29, 2, 160, 96)
+    run("S=%d aligned=%d" % (S, aligned), _pyr(40), SC, rois, S=S, aligned=aligned)
+
+
+@pytest.mark.parametrize("layout", ["nchw", "cl_view", "nchw_view"])
+def test_layouts(layout):
+    rng = np.random.default_rng(20)
+    rois = _rois(rng, 23, 2, 160, 96)
+    run("layout %s" % layout, _pyr(70), SC, rois, layout=layout)
+    run("layout %s mask" % layout, _pyr(70), SC, rois, out_hw=(14, 14), layout=layout)
+
+
+@pytest.mark.parametrize("fdt,odt,gdt", [("bf16", "bf16", "bf16"), ("bf16", "f32", "f32"),
+                                         ("f32", "bf16", "bf16")])
+def test_dtypes(fdt, odt, gdt):
+    rng = np.random.default_rng(30)
+    rois = W.draw_rois(rng, 2, 21, (96, 160), (4.0, 200.0))
+    run("dtypes %s/%s/%s" % (fdt, odt, gdt), _pyr(130), SC, rois, fdt=fdt, odt=odt, gdt=gdt)
+    run("dtypes %s/%s/%s mask" % (fdt, odt, gdt), _pyr(130), SC, rois, out_hw=(14, 14),
+        fdt=fdt, odt=odt, gdt=gdt)
+
+
+def test_other_output_sizes():
+    rng = np.random.default_rng(40)
+    rois = _rois(rng, 17, 2, 160, 96)
+    run("out 5x3", _pyr(33), SC, rois, out_hw=(5, 3))
+    run("out 1x1", _pyr(33), SC, rois, out_hw=(1, 1), S=0)
+
+
+def test_degenerate_boxes_and_maps():
+    rng = np.random.default_rng(50)
+    shapes = [(2, 70, 1, 1), (2, 70, 2, 3)]
+    scales = [0.5, 0.25]
+    rois = np.array([[0, 0.0, 0.0, 0.0, 0.0],          # zero size
+                     [1, 0.5, 0.5, 0.5, 3.0],          # zero width
+                     [0, -50, -50, -10, -10],          # entirely outside, low side
+                     [1, 30, 30, 60, 60],              # entirely outside, high side
+                     [0, -3, -3, 5, 5],                # straddles the origin
+                     [1, 0, 0, 2, 2]], np.float32)
+    lv = np.array([0, 1, 0, 1, 0, 1], np.int32)
+    for S in (0, 2):
+        for out_hw in ((7, 7), (14, 14), (2, 2)):
+            run("degenerate S=%d %s" % (S, out_hw), shapes, scales, rois, out_hw=out_hw, S=S,
+                roi_levels=lv)
+
+
+def test_invalid_batch_and_level_indices():
+    rng = np.random.default_rng(60)
+    rois = W.draw_rois(rng, 2, 6, (96, 160), (8.0, 90.0))
+    rois[0, 0] = -1.0
+    rois[1, 0] = 2.0          # N = 2: names no image
+    rois[2, 0] = 1.9          # truncates to image 1
+    lv = np.array([0, 1, 2, 3, 7, -1, 0, 1, 2, 3, 0, 1], np.int32)
+    out = run("invalid indices", _pyr(64), SC, rois, roi_levels=lv)
+    o = out.cpu()
+    for k in (0, 1, 4, 5):
+        assert not o[k].any()
+
+
+def test_one_and_zero_rois():
+    rng = np.random.default_rng(70)
+    rois = W.draw_rois(rng, 1, 1, (96, 160), (30.0, 60.0))
+    run("K=1", [(1, 100, 24, 40), (1, 100, 12, 20)], SC[:2], rois)
+    shapes = [(1, 100, 24, 40), (1, 100, 12, 20)]
+    feats = [to_device(np.zeros(s, np.float32), "f32") for s in shapes]
+    empty = torch.zeros((0, 5), dtype=torch.float32, device="cuda")
+    lv, ws = rex.plan(feats, SC[:2], empty)
+    out = rex.roi_align_fwd(feats, SC[:2], empty, lv, (7, 7), 2, True, workspace=ws)
+    grads = [torch.ones(s, device="cuda") for s in shapes]
+    rex.roi_align_bwd(torch.zeros((0, 100, 7, 7), device="cuda"), empty, lv, (7, 7), 2, True,
+                      grads, SC[:2], zero_init=True, workspace=ws)
+    torch.cuda.synchronize()
+    assert out.shape == (0, 100, 7, 7)
+    assert all(not g.any() for g in grads)
+
+
+def test_plan_order_is_irrelevant_to_results():
+    rng = np.random.default_rng(80)
+    rois = W.draw_rois(rng, 2, 40, (96, 160), (4.0, 200.0))
+    a = run("with plan", _pyr(96), SC, rois, backward=False)
+    b = run("without plan", _pyr(96), SC, rois, use_plan=False, backward=False)
+    assert torch.equal(a, b)
+
+
+def test_threshold_boxes_bit_exact():
+    """Boxes whose areas sit at the level thresholds, one binary32 step either side."""
+    log("level map at thresholds")
+    rows = []
+    for side in (112.0, 224.0, 448.0):
+        s = np.float32(side)
+        for w in (np.nextafter(s, np.float32(0)), s, np.nextafter(s, np.float32(1e9))):
+            for h in (np.nextafter(s, np.float32(0)), s, np.nextafter(s, np.float32(1e9))):
+                for x in (0.0, 13.25, 300.5):
+                    rows.append([0, x, x, np.float32(x) + w, np.float32(x) + h])
+    rois = np.array(rows, np.float32)
+    ref = oracle.level_map(rois, 4, 56.0)
+    got = rex.fpn_level_map(torch.from_numpy(rois).cuda(), 4, 56.0).cpu().numpy()
+    assert np.array_equal(got, ref)
+    assert len(set(ref.tolist())) == 4
+
+
+def test_gpu_invariants():
+    """Constant maps give constants; the backward conserves mass and is the adjoint."""
+    log("invariants: constant, mass, adjoint (fp32 on the GPU)")
+    rng = np.random.default_rng(90)
+    shapes = _pyr(128)
+    scales = SC
+    rois = W.draw_rois(rng, 2, 50, (96, 160), (4.0, 150.0))
+    r_dev = torch.from_numpy(rois).cuda()
+    const = [torch.full(s, 1.5 + l, device="cuda").contiguous(memory_format=torch.channels_last)
+             for l, s in enumerate(shapes)]
+    lv, ws = rex.plan(const, scales, r_dev)
+    out = rex.roi_align_fwd(const, scales, r_dev, lv, (7, 7), 2, True, workspace=ws)
+    exp = (1.5 + lv.float())[:, None, None, None].expand_as(out)
+    assert torch.allclose(out, exp, rtol=1e-6, atol=1e-6)
+    g = torch.randn((rois.shape[0], 128, 7, 7), device="cuda")
+    grads = [torch.empty(s, device="cuda").contiguous(memory_format=torch.channels_last)
+             for s in shapes]
+    rex.roi_align_bwd(g, r_dev, lv, (7, 7), 2, True, grads, scales, zero_init=True, workspace=ws)
+    tot = sum(x.double().sum() for x in grads)
+    assert abs(tot.item() - g.double().sum().item()) <= 1e-4 * g.abs().sum().item()
+    x = [torch.randn(s, device="cuda").contiguous(memory_format=torch.channels_last)
+         for s in shapes]
+    y = rex.roi_align_fwd(x, scales, r_dev, lv, (7, 7), 2, True, workspace=ws)
+    lhs = (y.double() * g.double()).sum().item()
+    rhs = sum((a.double() * b.double()).sum().item() for a, b in zip(x, grads))
+    assert abs(lhs - rhs) <= 1e-5 * (y.double().abs() * g.double().abs()).sum().item()

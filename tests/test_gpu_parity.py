@@ -1,0 +1,175 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Full-size workloads run in the launch configuration the benchmark times (the
+plan-ordered channels-last kernels).  Workloads 1-4 are compared element by
+element in full; the batch-16 workload is compared on sampled RoIs and channels
+(forward rows are independent per RoI and channel; backward planes are independent
+per channel, so a channel subset of the oracle is exact).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1906_07155_amd as rex
+from paper_1906_07155_amd import workloads as W
+from gpu_helpers import Case, as_f64, check_bwd, check_fwd, from_device, log, to_device
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rex.lib()
+
+
+_CASES = {}
+
+
+def _case(idx, head=None, fdt=None):
+    key = (idx, head, fdt)
+    if key not in _CASES:
+        wl = W.config(idx, head=head, feat_dtype=fdt)
+        feats = None
+        if idx == 5:
+            other = [c for k, c in _CASES.items() if k[0] == 5]
+            if other:
+                feats = other[0].feats_np
+        _CASES[key] = Case(wl, feats=feats)
+    return _CASES[key]
+
+
+FULL = [(1, None, None), (2, None, None), (3, None, None), (4, None, "f32"), (4, None, "bf16")]
+SAMPLED = [(5, "box", None), (5, "mask", None)]
+
+
+def _run_fwd(c: Case, plan=True):
+    levels, ws = rex.plan(c.feats, c.scales, c.rois_dev, c.wl.finest_scale)
+    out = rex.roi_align_fwd(c.feats, c.scales, c.rois_dev, levels, c.wl.out_hw,
+                            c.wl.sampling_ratio, c.wl.aligned,
+                            out_dtype=torch.bfloat16 if c.wl.out_dtype == "bf16" else torch.float32,
+                            workspace=ws if plan else None)
+    torch.cuda.synchronize()
+    return levels, ws, out
+
+
+def _run_bwd(c: Case, levels, ws, g_np):
+    g = to_device(g_np, c.wl.grad_dtype, layout="nchw")
+    grads = [torch.empty(s, dtype=torch.float32, device="cuda",
+                         memory_format=torch.channels_last) for s in c.shapes]
+    rex.roi_align_bwd(g, c.rois_dev, levels, c.wl.out_hw, c.wl.sampling_ratio, c.wl.aligned,
+                      grads, c.scales, zero_init=True, workspace=ws)
+    torch.cuda.synchronize()
+    return grads
+
+
+@pytest.mark.parametrize("idx,head,fdt", FULL + SAMPLED)
+def test_level_map_and_plan(idx, head, fdt):
+    c = _case(idx, head, fdt)
+    log("level map + plan: workload %d %s %s, K=%d" % (idx, head, fdt, c.K))
+    ref = c.oracle_levels()
+    L = len(c.shapes)
+    lv1 = rex.fpn_level_map(c.rois_dev, L, c.wl.finest_scale)
+    levels, ws = rex.plan(c.feats, c.scales, c.rois_dev, c.wl.finest_scale)
+    offs = rex.plan_offsets(ws, c.K, L)
+    perm = rex.plan_perm(ws, c.K)
+    torch.cuda.synchronize()
+    assert np.array_equal(lv1.cpu().numpy(), ref)
+    assert np.array_equal(levels.cpu().numpy(), ref)
+    p = perm.cpu().numpy()
+    assert np.array_equal(np.sort(p), np.arange(c.K))
+    lv_sorted = ref[p]
+    assert np.all(np.diff(lv_sorted) >= 0)
+    counts = np.bincount(ref, minlength=L)
+    assert np.array_equal(offs.cpu().numpy(), np.concatenate([[0], np.cumsum(counts)]))
+    b = np.trunc(c.rois[p, 0]).astype(int)
+    for l in range(L):
+        seg = b[offs.cpu().numpy()[l]:offs.cpu().numpy()[l + 1]]
+        assert np.all(np.diff(seg) >= 0), "images not grouped within level %d" % l
+
+
+@pytest.mark.parametrize("idx,head,fdt", FULL)
+def test_forward_full(idx, head, fdt):
+    c = _case(idx, head, fdt)
+    log("forward full: workload %d %s, K=%d" % (idx, fdt, c.K))
+    levels, ws, out = _run_fwd(c)
+    ref_lv = c.oracle_levels()
+    ref = oracle.roi_align_fwd([as_f64(f, c.wl.feat_dtype) for f in c.feats_np], c.scales,
+                               c.rois, ref_lv, *c.wl.out_hw, c.wl.sampling_ratio,
+                               c.wl.aligned, "parity")
+    err = check_fwd(from_device(out), ref, c.bf16, "workload %d forward" % idx)
+    log("  max abs err %.3e" % err)
+
+
+@pytest.mark.parametrize("idx,head,fdt", [(2, None, None), (3, None, None)])
+def test_backward_full(idx, head, fdt):
+    c = _case(idx, head, fdt)
+    log("backward full: workload %d, K=%d" % (idx, c.K))
+    levels, ws, _ = _run_fwd(c)
+    g = c.wl.grad()
+    grads = _run_bwd(c, levels, ws, g)
+    ref_lv = c.oracle_levels()
+    g64 = as_f64(g, c.wl.grad_dtype)
+    ref = oracle.roi_align_bwd(g64, c.shapes, c.scales, c.rois, ref_lv, *c.wl.out_hw,
+                               c.wl.sampling_ratio, c.wl.aligned, "parity")
+    absref = oracle.roi_align_bwd(np.abs(g64), c.shapes, c.scales, c.rois, ref_lv,
+                                  *c.wl.out_hw, c.wl.sampling_ratio, c.wl.aligned, "parity")
+    for l in range(len(c.shapes)):
+        r = check_bwd(from_device(grads[l]), ref[l], absref[l], False,
+                      "workload %d backward level %d" % (idx, l))
+        log("  level %d rel norm err %.3e" % (l, r))
+
+
+@pytest.mark.parametrize("idx,head,fdt", SAMPLED)
+def test_batch16_sampled(idx, head, fdt):
+    c = _case(idx, head, fdt)
+    log("batch-16 %s head: fwd+bwd at full size, sampled comparison, K=%d" % (head, c.K))
+    levels, ws, out = _run_fwd(c)
+    g = c.wl.grad()
+    grads = _run_bwd(c, levels, ws, g)
+    rng = np.random.default_rng(5)
+    chans = np.sort(rng.choice(c.wl.channels, 6, replace=False))
+    sub = np.sort(rng.choice(c.K, 384, replace=False))
+    ref_lv = c.oracle_levels()
+    feats_sub = [as_f64(f[:, chans], "bf16") for f in c.feats_np]
+    ref = oracle.roi_align_fwd(feats_sub, c.scales, c.rois[sub], ref_lv[sub], *c.wl.out_hw,
+                               c.wl.sampling_ratio, c.wl.aligned, "parity")
+    got = from_device(out[torch.from_numpy(sub).cuda()][:, torch.from_numpy(chans).cuda()])
+    check_fwd(got, ref, True, "batch-16 %s forward (sampled)" % head)
+    g64 = as_f64(g, "bf16")[:, chans]
+    shapes = [(s[0], len(chans), s[2], s[3]) for s in c.shapes]
+    ref = oracle.roi_align_bwd(g64, shapes, c.scales, c.rois, ref_lv, *c.wl.out_hw,
+                               c.wl.sampling_ratio, c.wl.aligned, "parity")
+    absref = oracle.roi_align_bwd(np.abs(g64), shapes, c.scales, c.rois, ref_lv, *c.wl.out_hw,
+                                  c.wl.sampling_ratio, c.wl.aligned, "parity")
+    ch_dev = torch.from_numpy(chans).cuda()
+    for l in range(len(c.shapes)):
+        # the gradient pyramid is fp32 and the oracle reads the same bf16 values, so the
+        # fp32 backward tolerance applies
+        check_bwd(from_device(grads[l][:, ch_dev]), ref[l], absref[l], False,
+                  "batch-16 %s backward level %d (sampled channels)" % (head, l))
+
+
+def test_forward_is_deterministic_and_plan_independent():
+    c = _case(2)
+    log("determinism: workload 2 forward x3, with and without plan")
+    _, _, a = _run_fwd(c, plan=True)
+    _, _, b = _run_fwd(c, plan=True)
+    _, _, d = _run_fwd(c, plan=False)
+    assert torch.equal(a, b)
+    assert torch.equal(a, d)
+
+
+def test_backward_repeatable_within_tolerance():
+    c = _case(3)
+    log("repeatability: workload 3 backward x2")
+    levels, ws, _ = _run_fwd(c)
+    g = c.wl.grad()
+    g1 = _run_bwd(c, levels, ws, g)
+    g2 = _run_bwd(c, levels, ws, g)
+    for a, b in zip(g1, g2):
+        d = (a - b).abs().max().item()
+        assert d <= 1e-4 * max(a.abs().max().item(), 1e-30)
