@@ -1,0 +1,307 @@
+#!/usr/bin/env python3
+"""Benchmark: multi-level RoIAlign forward + backward on one MI355X.
+
+One step is one pass of the whole hot path over one batch of synthetic input:
+  roi_extract_plan   FPN level of every RoI + level/image/cell-bucketed launch order
+  roi_align_fwd      gather-average into [K, C, 7, 7]
+  roi_extract_zero_grad   clear the fp32 gradient pyramid
+  roi_align_bwd      scatter the upstream gradient back with fp32 atomics
+
+Default workload: the FPN box head (batch 2, 800x1344 images, P2-P5 with C=256 fp32,
+512 RoIs per image, 7x7, sampling ratio 2, aligned), inputs resident in HBM before
+timing starts.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload 2] [--layout cl|nchw]
+  python bench.py --calibrate-copy      # plain copy kernel for the counter scale
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "RoIAlign fwd+bwd RoIs/sec and achieved HBM GB/s vs peak, FPN Mask R-CNN shapes"
+HBM_PEAK_GBS = 8000.0
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--head", default="box", choices=["box", "mask"])
+    ap.add_argument("--feat-dtype", default=None, choices=[None, "f32", "bf16"])
+    ap.add_argument("--layout", default="cl", choices=["cl", "nchw"])
+    ap.add_argument("--no-plan", action="store_true", help="RoIs in index order (no sort)")
+    ap.add_argument("--cold-reps", type=int, default=10,
+                    help="extra steps each preceded by a 1 GiB cache flush (reported apart)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="target wall time of the oracle sample")
+    ap.add_argument("--calibrate-copy", action="store_true")
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "api.hip"):
+        with open(os.path.join(ROOT, "paper_1906_07155_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it was taken
+    on the current kernel sources (else None)."""
+    path = os.path.join(PROFILE_DIR, "traffic_%s_%s.txt" % (kernel, workload))
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def calibrate_copy():
+    import torch
+    n = 256 * 1024 * 1024          # 1 GiB of float32
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "reps": 5}))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (the operator shards by image with no "
+              "exchange; see the design notes). --gpus %d is not supported." % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+
+    import torch
+
+    import paper_1906_07155_amd as rex
+    from paper_1906_07155_amd import accounting, workloads
+
+    dev = torch.device("cuda:0")
+    wl = workloads.config(args.workload, head=args.head, feat_dtype=args.feat_dtype)
+    feats_np = wl.features()
+    rois_np = wl.rois()
+    K = rois_np.shape[0]
+    C = wl.channels
+    bf16 = wl.feat_dtype == "bf16"
+
+    def to_dev(a, dt, layout):
+        if dt == "bf16":
+            t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(a).to(dev)
+        return t.contiguous(memory_format=torch.channels_last) if layout == "cl" else t
+
+    feats = [to_dev(f, wl.feat_dtype, args.layout) for f in feats_np]
+    rois = torch.from_numpy(rois_np).to(dev)
+    odt = torch.bfloat16 if wl.out_dtype == "bf16" else torch.float32
+    out = torch.empty((K, C) + tuple(wl.out_hw), dtype=odt, device=dev)
+    backward = wl.backward
+    if backward:
+        gout = to_dev(wl.grad(), wl.grad_dtype, "nchw")
+        grads = [torch.empty(f.shape, dtype=torch.float32, device=dev) for f in feats]
+        if args.layout == "cl":
+            grads = [g.contiguous(memory_format=torch.channels_last) for g in grads]
+    L = len(feats)
+    levels = torch.empty(K, dtype=torch.int32, device=dev)
+    ws = torch.empty(rex.workspace_size(K, L), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    S, aligned, out_hw = wl.sampling_ratio, wl.aligned, wl.out_hw
+    plan_ws = None if args.no_plan else ws
+
+    names = ["plan", "fwd", "zero", "bwd"] if backward else ["plan", "fwd"]
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        rex.plan(feats, wl.scales, rois, wl.finest_scale, levels_out=levels, workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        rex.roi_align_fwd(feats, wl.scales, rois, levels, out_hw, S, aligned, out=out,
+                          workspace=plan_ws)
+        if ev is not None:
+            ev[2].record(stream)
+        if backward:
+            rex.zero_grad(grads, wl.scales)
+            if ev is not None:
+                ev[3].record(stream)
+            rex.roi_align_bwd(gout, rois, levels, out_hw, S, aligned, grads, wl.scales,
+                              zero_init=False, workspace=plan_ws)
+            if ev is not None:
+                ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    nev = len(names) + 1
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(events[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / args.steps
+    per_kernel = {}
+    for j, n in enumerate(names):
+        ts = [events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]
+        per_kernel[n] = float(np.mean(ts))
+
+    # cold: each step after a 1 GiB write that evicts L2 and the 256 MB MALL
+    cold = None
+    if args.cold_reps > 0:
+        flush = torch.empty(256 * 1024 * 1024, dtype=torch.float32, device=dev)
+        cts = {n: [] for n in names}
+        csteps = []
+        for _ in range(args.cold_reps):
+            flush.zero_()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(nev)]
+            step(ev)
+            torch.cuda.synchronize()
+            for j, n in enumerate(names):
+                cts[n].append(ev[j].elapsed_time(ev[j + 1]))
+            csteps.append(ev[0].elapsed_time(ev[-1]))
+        cold = {"ms_per_step": float(np.median(csteps)),
+                "kernel_ms": {n: float(np.median(v)) for n, v in cts.items()}}
+        del flush
+
+    # algorithmic bytes
+    lv_np = levels.cpu().numpy()
+    s_feat = 2 if bf16 else 4
+    s_out = 2 if wl.out_dtype == "bf16" else 4
+    s_gout = 2 if wl.grad_dtype == "bf16" else 4
+    by = accounting.count(rois_np, lv_np, wl.level_hw, wl.scales, wl.n_images, C, out_hw, S,
+                          aligned, s_feat, s_out, s_gout)
+    alg = {"plan": 24 * K + 4 * K * 3, "fwd": by.e_fwd}
+    if backward:
+        alg.update({"zero": by.zero, "bwd": by.e_bwd})
+    gbs = {n: alg[n] / (per_kernel[n] * 1e-3) / 1e9 for n in names}
+    dominant = max(["fwd", "bwd"] if backward else ["fwd"], key=lambda n: per_kernel[n])
+    wname = "cfg%d%s" % (args.workload, ("_" + args.head) if args.workload == 5 else
+                         ("_" + wl.feat_dtype if args.workload == 4 else ""))
+    traffic = stored_traffic(dominant, wname)
+    roofline = {"bound": "hbm", "achieved": round(gbs[dominant], 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(gbs[dominant] / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "kernel": "roi_align_" + dominant,
+                "bytes_per_launch": alg[dominant],
+                "launch_ms": round(per_kernel[dominant], 5)}
+
+    step_bytes = sum(alg[n] for n in names)
+    extra = {
+        "kernel_ms": {n: round(v, 5) for n, v in per_kernel.items()},
+        "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
+        "step_GBps_effective": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "bytes": {"E_fwd": by.e_fwd, "E_bwd": by.e_bwd, "U_fwd": by.u_fwd, "U_bwd": by.u_bwd,
+                  "T_fwd": by.t_fwd, "zero_fill": by.zero,
+                  "footprint_px": by.footprint_px, "union_px": by.union_px},
+        "fwd_bwd_GBps_effective_no_zero": (
+            round((by.e_fwd + by.e_bwd) / ((per_kernel["fwd"] + per_kernel["bwd"]) * 1e-3) / 1e9,
+                  1) if backward else None),
+        "fwd_bwd_GBps_unique_no_zero": (
+            round((by.u_fwd + by.u_bwd) / ((per_kernel["fwd"] + per_kernel["bwd"]) * 1e-3) / 1e9,
+                  1) if backward else None),
+        "cold": cold,
+        "layout": args.layout,
+        "plan": not args.no_plan,
+        "kernel_source_hash": kernel_source_hash(),
+    }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, feats_np, rois_np, lv_np, args.cpu_seconds)
+
+    result = {
+        "metric": METRIC,
+        "value": round(K / (ms_per_step * 1e-3), 1),
+        "unit": "RoIs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic (seeded normal features, log-uniform RoIs; no COCO)",
+        "config": {"workload": wl.name, "num_rois": K, "channels": C,
+                   "levels": [list(x) for x in wl.level_hw], "out": list(out_hw),
+                   "sampling_ratio": S, "aligned": aligned, "layout": args.layout,
+                   "backward": backward},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "extra": extra,
+    }
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(wl, feats_np, rois_np, lv_np, target_s):
+    """The CPU oracle (parity mode, as it stands) on a bounded sample of the same RoIs."""
+    import oracle
+    from paper_1906_07155_amd import workloads
+    lib = oracle.load()
+    if wl.feat_dtype == "bf16":
+        f64 = [workloads.bf16_bits_to_f32(f).astype(np.float64) for f in feats_np]
+    else:
+        f64 = [f.astype(np.float64) for f in feats_np]
+    shapes = [f.shape for f in f64]
+    rng = np.random.default_rng(0)
+    K = rois_np.shape[0]
+    n = min(K, 32)
+    elapsed = 0.0
+    while True:
+        sub = np.sort(rng.choice(K, n, replace=False))
+        g = np.zeros((n, wl.channels) + tuple(wl.out_hw))
+        if wl.backward:
+            g = rng.standard_normal(g.shape)
+        t0 = time.perf_counter()
+        oracle.roi_align_fwd(f64, wl.scales, rois_np[sub], lv_np[sub], *wl.out_hw,
+                             wl.sampling_ratio, wl.aligned, "parity", lib=lib)
+        if wl.backward:
+            oracle.roi_align_bwd(g, shapes, wl.scales, rois_np[sub], lv_np[sub], *wl.out_hw,
+                                 wl.sampling_ratio, wl.aligned, "parity", lib=lib)
+        elapsed = time.perf_counter() - t0
+        if elapsed >= target_s / 4 or n >= K:
+            break
+        n = min(K, n * 4)
+    return {"value": round(n / elapsed, 1), "unit": "RoIs/s", "cores": oracle.num_threads(lib),
+            "kind": "oracle",
+            "sample": "%d of %d RoIs (all %d channels), %s in %.2f s wall" % (
+                n, K, wl.channels, "fwd+bwd" if wl.backward else "fwd", elapsed)}
+
+
+if __name__ == "__main__":
+    main()
