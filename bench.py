@@ -2,10 +2,13 @@
 """Benchmark: multi-level RoIAlign forward + backward on one MI355X.
 
 One step is one pass of the whole hot path over one batch of synthetic input:
-  roi_extract_plan   FPN level of every RoI + level/image/cell-bucketed launch order
+  roi_extract_plan   FPN level of every RoI, level/image/cell-bucketed launch order,
+                     tile -> RoI lists
   roi_align_fwd      gather-average into [K, C, 7, 7]
-  roi_extract_zero_grad   clear the fp32 gradient pyramid
-  roi_align_bwd      scatter the upstream gradient back with fp32 atomics
+  roi_align_bwd      (default, --bwd gather) every 8x8 x 64-channel tile of the fp32
+                     gradient pyramid sums its RoIs and is written once, clearing included;
+                     (--bwd scatter) roi_extract_zero_grad, then per-RoI fp32 atomics.
+The other backward algorithm is timed separately and reported under extra.other_bwd.
 
 Default workload: the FPN box head (batch 2, 800x1344 images, P2-P5 with C=256 fp32,
 512 RoIs per image, 7x7, sampling ratio 2, aligned), inputs resident in HBM before
@@ -43,6 +46,10 @@ def parse():
     ap.add_argument("--feat-dtype", default=None, choices=[None, "f32", "bf16"])
     ap.add_argument("--layout", default="cl", choices=["cl", "nchw"])
     ap.add_argument("--no-plan", action="store_true", help="RoIs in index order (no sort)")
+    ap.add_argument("--bwd", default="gather", choices=["gather", "scatter"],
+                    help="backward algorithm of the timed step (the other is timed apart)")
+    ap.add_argument("--alt-steps", type=int, default=50,
+                    help="steps timed with the other backward algorithm (0: skip)")
     ap.add_argument("--cold-reps", type=int, default=10,
                     help="extra steps each preceded by a 1 GiB cache flush (reported apart)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -60,7 +67,7 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic(kernel: str, workload: str):
+def stored_traffic(kernel: str, workload: str):  # kernel: fwd | bwd_gather | bwd_scatter
     """HBM bytes per launch from a committed rocprofv3 counter summary, if it was taken
     on the current kernel sources (else None)."""
     path = os.path.join(PROFILE_DIR, "traffic_%s_%s.txt" % (kernel, workload))
@@ -134,63 +141,85 @@ def main():
             grads = [g.contiguous(memory_format=torch.channels_last) for g in grads]
     L = len(feats)
     levels = torch.empty(K, dtype=torch.int32, device=dev)
-    ws = torch.empty(rex.workspace_size(K, L), dtype=torch.uint8, device=dev)
+    ws = torch.empty(rex.workspace_size(feats, wl.scales, K), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
     S, aligned, out_hw = wl.sampling_ratio, wl.aligned, wl.out_hw
     plan_ws = None if args.no_plan else ws
 
-    names = ["plan", "fwd", "zero", "bwd"] if backward else ["plan", "fwd"]
+    def names_for(algo):
+        if not backward:
+            return ["plan", "fwd"]
+        return ["plan", "fwd", "bwd"] if algo == "gather" else ["plan", "fwd", "zero", "bwd"]
 
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
+    def step(algo, ev=None):
+        j = 0
+
+        def mark():
+            nonlocal j
+            if ev is not None:
+                ev[j].record(stream)
+            j += 1
+
+        mark()
         rex.plan(feats, wl.scales, rois, wl.finest_scale, levels_out=levels, workspace=ws)
-        if ev is not None:
-            ev[1].record(stream)
+        mark()
         rex.roi_align_fwd(feats, wl.scales, rois, levels, out_hw, S, aligned, out=out,
                           workspace=plan_ws)
-        if ev is not None:
-            ev[2].record(stream)
+        mark()
         if backward:
-            rex.zero_grad(grads, wl.scales)
-            if ev is not None:
-                ev[3].record(stream)
-            rex.roi_align_bwd(gout, rois, levels, out_hw, S, aligned, grads, wl.scales,
-                              zero_init=False, workspace=plan_ws)
-            if ev is not None:
-                ev[4].record(stream)
+            if algo == "scatter":
+                rex.zero_grad(grads, wl.scales)
+                mark()
+                rex.roi_align_bwd(gout, rois, levels, out_hw, S, aligned, grads, wl.scales,
+                                  zero_init=False, workspace=plan_ws, algorithm="scatter")
+            else:
+                rex.roi_align_bwd(gout, rois, levels, out_hw, S, aligned, grads, wl.scales,
+                                  zero_init=True, workspace=ws, algorithm="gather")
+            mark()
 
+    def timed(algo, nsteps):
+        names = names_for(algo)
+        nev = len(names) + 1
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(nsteps)]
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for i in range(nsteps):
+            step(algo, evs[i])
+        t1.record(stream)
+        torch.cuda.synchronize()
+        per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(nsteps)]))
+               for j, n in enumerate(names)}
+        return t0.elapsed_time(t1) / nsteps, per
+
+    algo = args.bwd
+    names = names_for(algo)
     for _ in range(args.warmup):
-        step()
+        step(algo)
     torch.cuda.synchronize()
+    ms_per_step, per_kernel = timed(algo, args.steps)
 
-    nev = len(names) + 1
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(events[i])
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_per_step = total_ms / args.steps
-    per_kernel = {}
-    for j, n in enumerate(names):
-        ts = [events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]
-        per_kernel[n] = float(np.mean(ts))
+    alt = None
+    if backward and args.alt_steps > 0:
+        other = "scatter" if algo == "gather" else "gather"
+        for _ in range(5):
+            step(other)
+        alt_ms, alt_per = timed(other, args.alt_steps)
+        alt = {"bwd": other, "ms_per_step": round(alt_ms, 5),
+               "kernel_ms": {n: round(v, 5) for n, v in alt_per.items()}}
 
     # cold: each step after a 1 GiB write that evicts L2 and the 256 MB MALL
     cold = None
     if args.cold_reps > 0:
         flush = torch.empty(256 * 1024 * 1024, dtype=torch.float32, device=dev)
+        nev = len(names) + 1
         cts = {n: [] for n in names}
         csteps = []
         for _ in range(args.cold_reps):
             flush.zero_()
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(nev)]
-            step(ev)
+            step(algo, ev)
             torch.cuda.synchronize()
             for j, n in enumerate(names):
                 cts[n].append(ev[j].elapsed_time(ev[j + 1]))
@@ -206,17 +235,22 @@ def main():
     s_gout = 2 if wl.grad_dtype == "bf16" else 4
     by = accounting.count(rois_np, lv_np, wl.level_hw, wl.scales, wl.n_images, C, out_hw, S,
                           aligned, s_feat, s_out, s_gout)
+    # bytes each kernel must move: the gather backward reads the upstream gradient once
+    # and writes every gradient element once (the clearing is part of it); the scatter
+    # backward does one fp32 read-modify-write per distinct (pixel, channel) of each RoI
+    gather_bytes = by.out_bytes // s_out * s_gout + by.zero + 24 * K
     alg = {"plan": 24 * K + 4 * K * 3, "fwd": by.e_fwd}
     if backward:
-        alg.update({"zero": by.zero, "bwd": by.e_bwd})
+        alg.update({"zero": by.zero, "bwd": gather_bytes if algo == "gather" else by.e_bwd})
     gbs = {n: alg[n] / (per_kernel[n] * 1e-3) / 1e9 for n in names}
     dominant = max(["fwd", "bwd"] if backward else ["fwd"], key=lambda n: per_kernel[n])
     wname = "cfg%d%s" % (args.workload, ("_" + args.head) if args.workload == 5 else
                          ("_" + wl.feat_dtype if args.workload == 4 else ""))
-    traffic = stored_traffic(dominant, wname)
+    kname = {"fwd": "fwd", "bwd": "bwd_" + algo}[dominant]
+    traffic = stored_traffic(kname, wname)
     roofline = {"bound": "hbm", "achieved": round(gbs[dominant], 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(gbs[dominant] / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "kernel": "roi_align_" + dominant,
+                "traffic": traffic, "kernel": "roi_align_" + kname,
                 "bytes_per_launch": alg[dominant],
                 "launch_ms": round(per_kernel[dominant], 5)}
 
@@ -228,12 +262,11 @@ def main():
         "bytes": {"E_fwd": by.e_fwd, "E_bwd": by.e_bwd, "U_fwd": by.u_fwd, "U_bwd": by.u_bwd,
                   "T_fwd": by.t_fwd, "zero_fill": by.zero,
                   "footprint_px": by.footprint_px, "union_px": by.union_px},
-        "fwd_bwd_GBps_effective_no_zero": (
+        "fwd_bwd_GBps_effective": (
             round((by.e_fwd + by.e_bwd) / ((per_kernel["fwd"] + per_kernel["bwd"]) * 1e-3) / 1e9,
                   1) if backward else None),
-        "fwd_bwd_GBps_unique_no_zero": (
-            round((by.u_fwd + by.u_bwd) / ((per_kernel["fwd"] + per_kernel["bwd"]) * 1e-3) / 1e9,
-                  1) if backward else None),
+        "bwd_algorithm": algo if backward else None,
+        "other_bwd": alt,
         "cold": cold,
         "layout": args.layout,
         "plan": not args.no_plan,

@@ -28,8 +28,9 @@
  *           hy*hx*F[yl,xl] + hy*lx*F[yl,xh] + ly*hx*F[yh,xl] + ly*lx*F[yh,xh],
  *       count = max(gh*gw, 1)   (invalid samples are counted).
  *   - Backward is the exact transpose: grad_F[b,c,y*,x*] += g[k,c,ph,pw]*w/count
- *     for every valid sample and corner, accumulated with fp32 atomics (the
- *     summation order, hence the last bits, vary from run to run).
+ *     for every valid sample and corner, summed in fp32 either by atomics (scatter)
+ *     or per output tile (gather); the summation order, hence the last bits, may
+ *     vary between runs and algorithms.
  *
  * Ownership and execution: the caller owns every buffer; all data pointers are
  * device pointers except the re_level_t arrays, which are read on the host during
@@ -90,14 +91,20 @@ typedef struct {
 re_status_t fpn_level_map(const float *rois, int64_t num_rois, int32_t num_levels,
                           float finest_scale, int32_t *levels_out, void *stream);
 
-/* Bytes of device workspace a plan for num_rois RoIs over num_levels levels needs
- * (a few bytes per RoI).  Host-only; writes *bytes. */
-re_status_t roi_extract_workspace_size(int64_t num_rois, int32_t num_levels, size_t *bytes);
+/* Bytes of device workspace a plan for num_rois RoIs over the pyramid `levels` needs
+ * (host array; only n, h and w are read).  It holds the launch permutation and the
+ * tile->RoI lists of the gather backward: 8 bytes per RoI, 4 per bin-tile, and 4 per
+ * RoI times the largest number of 16-pixel tiles of one image-level.  Host-only;
+ * writes *bytes. */
+re_status_t roi_extract_workspace_size(const re_level_t *levels, int32_t num_levels,
+                                       int64_t num_rois, size_t *bytes);
 
 /* a1 + a2 in one launch -- the level of every RoI (written to levels_out, as by
  * fpn_level_map) and the launch plan: a permutation of the RoIs ordered by
  * (level, image, coarse spatial cell of the box centre) plus per-level offsets,
- * stored in `workspace`.  The forward and backward walk the RoIs in plan order,
+ * stored in `workspace`; the same launch also lists, for every 16-pixel bin-tile of
+ * every (level, image), the RoIs whose footprint can reach it (used by the gather
+ * backward).  The forward and backward walk the RoIs in plan order,
  * so neighbouring work shares cache; any valid permutation gives the same
  * results, and RoIs with equal keys may come in any order.  The plan stays valid
  * for as long as rois, levels_out and the level shapes are unchanged, so one plan
@@ -146,19 +153,32 @@ re_status_t roi_align_fwd(const re_level_t *levels, int32_t num_levels,
 re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_levels,
                                   void *stream);
 
+/* Backward algorithms. */
+#define RE_BWD_AUTO 0       /* gather when eligible, else scatter */
+#define RE_BWD_SCATTER 1    /* per-RoI scatter, fp32 atomics (a7) */
+#define RE_BWD_GATHER 2     /* per-tile gather, plain stores (needs a plan, stride_c == 1,
+                               out 7x7 or 14x14 with sampling_ratio 2) */
+
 /* a6 + a7 -- RoIAlign backward: adds the transpose of the forward applied to
- * grad_out into the gradient pyramid.
+ * grad_out into the gradient pyramid (clears it first when zero_init != 0).
  *   grad_out: device [num_rois][c][out_h][out_w], dense, of grad_out_dtype;
  *   grad_levels: host array of num_levels descriptors, RE_DTYPE_F32, same n, c,
- *           h, w and spatial_scale as the forward's levels; accumulated into with
- *           fp32 atomics (cleared first when zero_init != 0);
+ *           h, w and spatial_scale as the forward's levels;
+ *   algorithm: RE_BWD_SCATTER adds every RoI's contributions with fp32 atomics, one
+ *           per distinct (pixel, channel) of the RoI, after an optional clearing
+ *           pass; RE_BWD_GATHER has each (8x8-pixel quadrant, 64 channels) of the
+ *           pyramid sum the RoIs the plan binned to it and write every element once
+ *           (no atomics; clearing is part of the same pass), which requires `plan`
+ *           built by roi_extract_plan for these RoIs with levels_out == roi_levels;
+ *           RE_BWD_AUTO picks gather when eligible.  RE_ERR_UNSUPPORTED if gather is
+ *           requested but not eligible;
  *   other arguments as roi_align_fwd. */
 re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype,
                           const float *rois, int64_t num_rois, const int32_t *roi_levels,
                           int32_t out_h, int32_t out_w, int32_t sampling_ratio,
                           int32_t aligned, const re_level_t *grad_levels, int32_t num_levels,
-                          int32_t zero_init, const void *plan, size_t plan_bytes,
-                          void *stream);
+                          int32_t zero_init, int32_t algorithm, const void *plan,
+                          size_t plan_bytes, void *stream);
 
 /* Static description of a status code. */
 const char *roi_extract_status_str(re_status_t status);

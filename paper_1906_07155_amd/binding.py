@@ -24,6 +24,8 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "roi_extract.h")
 
 RE_OK, RE_ERR_INVALID_ARG, RE_ERR_UNSUPPORTED, RE_ERR_WORKSPACE, RE_ERR_DEVICE = range(5)
 RE_DTYPE_F32, RE_DTYPE_BF16 = 0, 1
+BWD_AUTO, BWD_SCATTER, BWD_GATHER = 0, 1, 2
+_BWD_ALGOS = {"auto": BWD_AUTO, "scatter": BWD_SCATTER, "gather": BWD_GATHER}
 MAX_LEVELS = 8
 
 
@@ -48,7 +50,7 @@ _LEVELS = ctypes.POINTER(ReLevel)
 
 SIGNATURES = {
     "fpn_level_map": [_VP, _I64, _I32, _F32, _VP, _VP],
-    "roi_extract_workspace_size": [_I64, _I32, ctypes.POINTER(_SZ)],
+    "roi_extract_workspace_size": [_LEVELS, _I32, _I64, ctypes.POINTER(_SZ)],
     "roi_extract_plan": [_LEVELS, _I32, _VP, _I64, _F32, _VP, _VP, _SZ, _VP],
     "roi_extract_plan_offsets": [_VP, _SZ, _I64, _I32, _VP, _VP],
     "roi_extract_plan_perm": [_VP, _SZ, _I64, ctypes.POINTER(_VP)],
@@ -56,7 +58,7 @@ SIGNATURES = {
                       _SZ, _VP],
     "roi_extract_zero_grad": [_LEVELS, _I32, _VP],
     "roi_align_bwd": [_VP, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _LEVELS, _I32, _I32,
-                      _VP, _SZ, _VP],
+                      _I32, _VP, _SZ, _VP],
 }
 
 _lock = threading.Lock()
@@ -168,9 +170,11 @@ def fpn_level_map(rois, num_levels: int, finest_scale: float = 56.0, out=None, s
     return out
 
 
-def workspace_size(num_rois: int, num_levels: int) -> int:
+def workspace_size(features: Sequence, scales: Sequence[float], num_rois: int) -> int:
+    """Workspace bytes of a plan for `num_rois` RoIs over this pyramid."""
     n = ctypes.c_size_t(0)
-    check(lib().roi_extract_workspace_size(num_rois, num_levels, ctypes.byref(n)),
+    arr = level_array(features, scales)
+    check(lib().roi_extract_workspace_size(arr, len(features), num_rois, ctypes.byref(n)),
           "roi_extract_workspace_size")
     return int(n.value)
 
@@ -183,7 +187,7 @@ def plan(features: Sequence, scales: Sequence[float], rois, finest_scale: float 
     K, L = rois.shape[0], len(features)
     if levels_out is None:
         levels_out = torch.empty(K, dtype=torch.int32, device=rois.device)
-    nbytes = workspace_size(K, L)
+    nbytes = workspace_size(features, scales, K)
     if workspace is None:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=rois.device)
     arr = level_array(features, scales)
@@ -242,8 +246,11 @@ def zero_grad(grads: Sequence, scales: Sequence[float], stream=None):
 
 def roi_align_bwd(grad_out, rois, roi_levels, out_size: Tuple[int, int], sampling_ratio: int,
                   aligned: bool, grads: Sequence, scales: Sequence[float], zero_init: bool = True,
-                  workspace=None, stream=None):
-    """Accumulate the backward into `grads` (float32 levels, cleared first if zero_init)."""
+                  workspace=None, stream=None, algorithm: str = "auto"):
+    """Accumulate the backward into `grads` (float32 levels, cleared first if zero_init).
+
+    algorithm: 'scatter' (fp32 atomics), 'gather' (per-tile, needs the plan workspace) or
+    'auto' (gather when eligible)."""
     rois = _rois(rois)
     _need_cuda(grad_out, "grad_out")
     if not grad_out.is_contiguous():
@@ -256,6 +263,7 @@ def roi_align_bwd(grad_out, rois, roi_levels, out_size: Tuple[int, int], samplin
     wsb = workspace.numel() if workspace is not None else 0
     check(lib().roi_align_bwd(grad_out.data_ptr(), _dtype_code(grad_out), rois.data_ptr(), K, lv,
                               ph, pw, sampling_ratio, int(bool(aligned)), arr, L,
-                              int(bool(zero_init)), ws, wsb, stream_handle(stream)),
+                              int(bool(zero_init)), _BWD_ALGOS[algorithm], ws, wsb,
+                              stream_handle(stream)),
           "roi_align_bwd")
     return grads

@@ -4,6 +4,7 @@
 // HIP runtime call is made on an error path, so argument errors are reported the
 // same way with or without a GPU.  The library allocates nothing and keeps no
 // state: all scratch lives in the caller's workspace.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 
@@ -14,14 +15,70 @@ using namespace rex;
 
 namespace {
 
-// Workspace layout: [0, 256) per-level offsets, then perm[K], then keys[K], each
-// region aligned to 256 bytes.
+// Workspace layout: [0, 256) per-level offsets, then perm[K], keys[K],
+// tile_start[ntiles + 1], tile_order[ntiles] and tile_rois[capacity], each region
+// aligned to 256 bytes.
 constexpr size_t kHeader = 256;
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 size_t perm_offset() { return kHeader; }
 size_t keys_offset(int64_t K) { return kHeader + align256(static_cast<size_t>(K) * 4); }
-size_t workspace_bytes_for(int64_t K) {
-    return kHeader + 2 * align256(static_cast<size_t>(K) * 4);
+size_t tiles_offset(int64_t K) { return kHeader + 2 * align256(static_cast<size_t>(K) * 4); }
+size_t tile_order_offset(int64_t K, const TileLayout &t) {
+    return tiles_offset(K) + align256(static_cast<size_t>(t.ntiles + 1) * 4);
+}
+size_t tile_rois_offset(int64_t K, const TileLayout &t) {
+    return tile_order_offset(K, t) + align256(static_cast<size_t>(t.ntiles) * 4);
+}
+size_t workspace_bytes_for(int64_t K, const TileLayout &t) {
+    return tile_rois_offset(K, t) + align256(static_cast<size_t>(t.capacity) * 4);
+}
+
+// Bin-tiles of 2^shift pixels per (level, image): the smallest shift >= 4 whose tile
+// count fits the plan kernel's LDS histogram.  capacity bounds the number of
+// (tile, RoI) pairs: a RoI meets at most every tile of one image-level.  Binning is
+// switched off (ntiles = 0) when that bound would exceed 2^28 pairs.
+constexpr int64_t kMaxPairs = int64_t(1) << 28;
+TileLayout tile_layout(const LevelTable &t, int64_t K) {
+    TileLayout L{};
+    for (int shift = 4; shift <= 24; ++shift) {
+        int64_t n = 0, most = 1;
+        for (int l = 0; l < t.num; ++l) {
+            const int64_t nx = (t.l[l].W + (int64_t(1) << shift) - 1) >> shift;
+            const int64_t ny = (t.l[l].H + (int64_t(1) << shift) - 1) >> shift;
+            n += int64_t(t.N) * nx * ny;
+            most = std::max(most, nx * ny);
+        }
+        if (n > kPlanMaxBins) continue;
+        if (K * most > kMaxPairs) break;
+        L.shift = shift;
+        L.ntiles = static_cast<int32_t>(n);
+        L.capacity = std::max<int64_t>(1, K * most);
+        int32_t base = 0;
+        for (int l = 0; l < kMaxLevels; ++l) {
+            if (l < t.num) {
+                L.ntx[l] = static_cast<int32_t>((t.l[l].W + (1 << shift) - 1) >> shift);
+                L.nty[l] = static_cast<int32_t>((t.l[l].H + (1 << shift) - 1) >> shift);
+                L.tbase[l] = base;
+                base += t.N * L.ntx[l] * L.nty[l];
+            } else {
+                L.ntx[l] = 1;
+                L.nty[l] = 1;
+                L.tbase[l] = base;
+            }
+        }
+        L.tbase[kMaxLevels] = base;
+        return L;
+    }
+    TileLayout off{};
+    off.shift = 4;
+    for (int l = 0; l <= kMaxLevels; ++l) {
+        if (l < kMaxLevels) {
+            off.ntx[l] = 1;
+            off.nty[l] = 1;
+        }
+        off.tbase[l] = 0;
+    }
+    return off;   // ntiles = 0: no binning
 }
 
 constexpr int64_t kMaxRois = int64_t(1) << 22;
@@ -66,7 +123,7 @@ re_status_t check_levels(const re_level_t *levels, int32_t num_levels, bool need
         a.H = static_cast<int32_t>(v.h);
         a.W = static_cast<int32_t>(v.w);
         a.scale = v.spatial_scale;
-        if (v.stride_c != 1) cl = false;
+        if (v.stride_c != 1 && v.c != 1) cl = false;   // a single channel has no stride
         if (numel) numel[l] = v.n * v.c * v.h * v.w;
         if (dense) {
             // dense: the strides are those of a contiguous tensor for some order of dims
@@ -114,10 +171,10 @@ re_status_t check_common(const float *rois, int64_t K, const int32_t *roi_levels
     return RE_OK;
 }
 
-re_status_t check_plan(const void *plan, size_t plan_bytes, int64_t K) {
+re_status_t check_plan(const void *plan, size_t plan_bytes, int64_t K, const LevelTable &t) {
     if (!plan) return RE_OK;
     if (reinterpret_cast<uintptr_t>(plan) % 256 != 0) return RE_ERR_WORKSPACE;
-    if (plan_bytes < workspace_bytes_for(K)) return RE_ERR_WORKSPACE;
+    if (plan_bytes < workspace_bytes_for(K, tile_layout(t, K))) return RE_ERR_WORKSPACE;
     return RE_OK;
 }
 
@@ -140,10 +197,13 @@ const char *roi_extract_status_str(re_status_t s) {
     return "unknown status";
 }
 
-re_status_t roi_extract_workspace_size(int64_t num_rois, int32_t num_levels, size_t *bytes) {
+re_status_t roi_extract_workspace_size(const re_level_t *levels, int32_t num_levels,
+                                       int64_t num_rois, size_t *bytes) {
     if (!bytes || num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
-    if (num_levels < 1 || num_levels > RE_MAX_LEVELS) return RE_ERR_INVALID_ARG;
-    *bytes = workspace_bytes_for(num_rois);
+    LevelTable t;
+    re_status_t st = check_levels(levels, num_levels, false, &t, nullptr, nullptr, nullptr);
+    if (st != RE_OK) return st;
+    *bytes = workspace_bytes_for(num_rois, tile_layout(t, num_rois));
     return RE_OK;
 }
 
@@ -170,7 +230,7 @@ re_status_t roi_extract_plan(const re_level_t *levels, int32_t num_levels, const
     if (num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
     if (!std::isfinite(finest_scale) || !(finest_scale > 0.0f)) return RE_ERR_INVALID_ARG;
     if (!workspace) return RE_ERR_WORKSPACE;
-    if ((st = check_plan(workspace, workspace_bytes, num_rois)) != RE_OK) return st;
+    if ((st = check_plan(workspace, workspace_bytes, num_rois, t)) != RE_OK) return st;
     if (num_rois > 0 && (!rois || !levels_out)) return RE_ERR_INVALID_ARG;
     if (reinterpret_cast<uintptr_t>(rois) % 4 || reinterpret_cast<uintptr_t>(levels_out) % 4)
         return RE_ERR_INVALID_ARG;
@@ -216,6 +276,19 @@ re_status_t roi_extract_plan(const re_level_t *levels, int32_t num_levels, const
         a.base[l] = base;
         base += (a.batch_in_key ? t.N : 1) * a.ncx[l] * a.ncy[l];
     }
+    const TileLayout tl = tile_layout(t, num_rois);
+    a.tile_start = reinterpret_cast<int32_t *>(ws + tiles_offset(num_rois));
+    a.tile_rois = reinterpret_cast<int32_t *>(ws + tile_rois_offset(num_rois, tl));
+    a.tile_order = reinterpret_cast<int32_t *>(ws + tile_order_offset(num_rois, tl));
+    a.ntiles = tl.ntiles;
+    a.capacity = static_cast<int32_t>(tl.capacity);
+    a.tile_shift = tl.shift;
+    for (int l = 0; l < kMaxLevels; ++l) {
+        a.ntx[l] = tl.ntx[l];
+        a.nty[l] = tl.nty[l];
+        a.tbase[l] = tl.tbase[l];
+    }
+    a.tbase[kMaxLevels] = tl.tbase[kMaxLevels];
     return from_hip(launch_plan(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -223,8 +296,8 @@ re_status_t roi_extract_plan_perm(const void *workspace, size_t workspace_bytes,
                                   int64_t num_rois, const int32_t **perm_out) {
     if (!perm_out || !workspace) return RE_ERR_INVALID_ARG;
     if (num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
-    re_status_t st = check_plan(workspace, workspace_bytes, num_rois);
-    if (st != RE_OK) return st;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return RE_ERR_WORKSPACE;
+    if (workspace_bytes < tiles_offset(num_rois)) return RE_ERR_WORKSPACE;
     *perm_out = reinterpret_cast<const int32_t *>(static_cast<const char *>(workspace) +
                                                   perm_offset());
     return RE_OK;
@@ -236,8 +309,8 @@ re_status_t roi_extract_plan_offsets(const void *workspace, size_t workspace_byt
     if (!workspace || !offsets_out) return RE_ERR_INVALID_ARG;
     if (num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
     if (num_levels < 1 || num_levels > RE_MAX_LEVELS) return RE_ERR_INVALID_ARG;
-    re_status_t st = check_plan(workspace, workspace_bytes, num_rois);
-    if (st != RE_OK) return st;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return RE_ERR_WORKSPACE;
+    if (workspace_bytes < tiles_offset(num_rois)) return RE_ERR_WORKSPACE;
     return from_hip(hipMemcpyAsync(offsets_out, workspace, (num_levels + 1) * sizeof(int32_t),
                                    hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream)));
 }
@@ -257,7 +330,7 @@ re_status_t roi_align_fwd(const re_level_t *levels, int32_t num_levels, const fl
     if (!valid_dtype(out_dtype)) return RE_ERR_INVALID_ARG;
     if (num_rois > 0 && !out) return RE_ERR_INVALID_ARG;
     if (reinterpret_cast<uintptr_t>(out) % dtype_size(out_dtype)) return RE_ERR_INVALID_ARG;
-    if ((st = check_plan(plan, plan_bytes, num_rois)) != RE_OK) return st;
+    if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
     if (num_rois == 0) return RE_OK;
 
     FwdArgs a{};
@@ -294,7 +367,7 @@ re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype, const fl
                           int64_t num_rois, const int32_t *roi_levels, int32_t out_h,
                           int32_t out_w, int32_t sampling_ratio, int32_t aligned,
                           const re_level_t *grad_levels, int32_t num_levels, int32_t zero_init,
-                          const void *plan, size_t plan_bytes, void *stream) {
+                          int32_t algorithm, const void *plan, size_t plan_bytes, void *stream) {
     LevelTable t;
     bool cl = false;
     int64_t numel[RE_MAX_LEVELS] = {0};
@@ -311,9 +384,45 @@ re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype, const fl
     if (reinterpret_cast<uintptr_t>(grad_out) % dtype_size(grad_out_dtype))
         return RE_ERR_INVALID_ARG;
     if (zero_init != 0 && zero_init != 1) return RE_ERR_INVALID_ARG;
-    if ((st = check_plan(plan, plan_bytes, num_rois)) != RE_OK) return st;
+    if (algorithm != RE_BWD_AUTO && algorithm != RE_BWD_SCATTER && algorithm != RE_BWD_GATHER)
+        return RE_ERR_INVALID_ARG;
+    if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
+
+    const TileLayout tl = tile_layout(t, num_rois);
+    const bool gather_ok = plan && cl && tl.ntiles > 0 && num_rois > 0 &&
+                           gather_available(out_h, out_w, sampling_ratio);
+    if (algorithm == RE_BWD_GATHER && !gather_ok && num_rois > 0) return RE_ERR_UNSUPPORTED;
+    const bool gather = gather_ok && algorithm != RE_BWD_SCATTER;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (gather) {
+        GatherArgs g{};
+        g.lv = t;
+        g.gout = grad_out;
+        g.rois = rois;
+        g.roi_levels = roi_levels;
+        const char *ws = static_cast<const char *>(plan);
+        g.tile_start = reinterpret_cast<const int32_t *>(ws + tiles_offset(num_rois));
+        g.tile_rois = reinterpret_cast<const int32_t *>(ws + tile_rois_offset(num_rois, tl));
+        g.tile_order = reinterpret_cast<const int32_t *>(ws + tile_order_offset(num_rois, tl));
+        g.K = static_cast<int32_t>(num_rois);
+        g.PH = out_h;
+        g.PW = out_w;
+        g.S = sampling_ratio;
+        g.aligned = aligned;
+        g.zero_init = zero_init;
+        g.ntiles = tl.ntiles;
+        g.capacity = static_cast<int32_t>(tl.capacity);
+        g.tile_shift = tl.shift;
+        g.qside = 1 << (tl.shift - 3);
+        for (int l = 0; l < kMaxLevels; ++l) {
+            g.ntx[l] = tl.ntx[l];
+            g.nty[l] = tl.nty[l];
+            g.tbase[l] = tl.tbase[l];
+        }
+        g.tbase[kMaxLevels] = tl.tbase[kMaxLevels];
+        return from_hip(launch_gather(g, grad_out_dtype, s));
+    }
     if (zero_init) {
         if ((st = from_hip(launch_zero(t, numel, dense, s))) != RE_OK) return st;
     }

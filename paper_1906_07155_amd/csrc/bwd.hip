@@ -258,6 +258,315 @@ __global__ __launch_bounds__(256) void bwd_cl_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Tile-gather backward
+// ---------------------------------------------------------------------------
+//
+// Device-scope fp32 atomics are executed beyond the per-XCD L2 on this part and
+// saturate at about 1.2 TB/s of payload, so the scatter form of the backward is
+// bound by atomic transactions.  This kernel inverts the loop: a wavefront owns an
+// 8x8-pixel quadrant of one (level, image) for 64 channels, keeps its 64 sums in
+// registers, walks the RoIs the plan binned to the enclosing bin-tile, and stores
+// every pixel once with plain coalesced stores (which also replaces the zero fill).
+// For each RoI the quadrant's separable weights are built in LDS:
+//   Wy[ph][r] = sum over the samples of bin row ph of the bilinear weight they put on
+//               row R0 + r (divided by the sample count), likewise Wx[pw][q],
+// and the contribution is  acc[r][q] += sum_ph Wy[ph][r] * sum_pw Wx[pw][q] * g[ph][pw].
+
+template <typename TG, int PH, int PW, int S>
+__global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
+    constexpr int NR = PH * S;
+    constexpr int NCOL = PW * S;
+    constexpr int T = 8;                   // quadrant side
+    constexpr int NB = PH * PW;
+    constexpr int GB = 64 * NB;            // floats of one RoI's gradient block (64 channels)
+    constexpr int YP = (PH * T + 63) / 64;  // ballot passes for the row weights
+    constexpr int XP = (PW * T + 63) / 64;
+    // Double-buffer the staged gradient block (prefetching the next RoI's block into
+    // registers while the current one is consumed) when two blocks fit in 32 KiB.
+    constexpr bool kDouble = 2 * GB * 4 <= 32768;
+    constexpr int NBUF = kDouble ? 2 : 1;
+    constexpr int PF = kDouble ? (GB + 255) / 256 : 1;   // prefetch registers per thread
+    static_assert(NR + NCOL <= 256, "one tap per thread");
+    static_assert(PH <= 32 && PW <= 32, "bin masks are 32-bit");
+
+    __shared__ float s_g[NBUF][GB];
+    __shared__ Tap s_tap[NR + NCOL];
+    __shared__ __align__(16) float s_wy[4][PH * T];
+    __shared__ __align__(16) float s_wx[4][PW * T];
+    __shared__ int s_k[64], s_ok[64];
+    __shared__ float s_ax[64][4];
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    // Blocks in dispatch order walk the tiles longest list first (plan order); the
+    // channel groups and quadrant blocks of one tile are adjacent.
+    const int lid = static_cast<int>(blockIdx.x);
+    const int per_tile = a.ncg * a.wg_per_tile;
+    const int rank = lid / per_tile;
+    const int rem = lid - rank * per_tile;
+    const int cg = rem / a.wg_per_tile;
+    int t = a.tile_order[rank];
+    t = max(0, min(t, a.ntiles - 1));
+    const int quad = (rem - cg * a.wg_per_tile) * 4 + wave;
+
+    int l = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxLevels; ++i)
+        if (i < a.lv.num && t >= a.tbase[i]) l = i;
+    const LevelArg L = level_at(a.lv, l);
+    const int ntx = pick(a.ntx, l);
+    const int per_img = pick(a.nty, l) * ntx;
+    const int local = t - pick(a.tbase, l);
+    const int b = local / per_img;
+    const int rt = local - b * per_img;
+    const int ty = rt / ntx;
+    const int tx = rt - ty * ntx;
+    const int R0 = (ty << a.tile_shift) + (quad / a.qside) * T;
+    const int Q0 = (tx << a.tile_shift) + (quad % a.qside) * T;
+    // Waves whose quadrant is off the map still take part in staging and barriers.
+    const bool wave_on = quad < a.qside * a.qside && R0 < L.H && Q0 < L.W;
+
+    const int c = cg * 64 + lane;
+    const bool lane_on = c < a.lv.C;
+    const int nch = min(64, a.lv.C - cg * 64);
+    const int nvalid = nch * NB;                 // valid floats of a staged block
+    float acc[T][T];
+#pragma unroll
+    for (int r = 0; r < T; ++r)
+#pragma unroll
+        for (int q = 0; q < T; ++q) acc[r][q] = 0.0f;
+
+    int s0 = a.tile_start[t];
+    int s1 = a.tile_start[t + 1];
+    s0 = max(0, min(s0, a.capacity));
+    s1 = max(s0, min(s1, a.capacity));
+    constexpr float inv_count = 1.0f / static_cast<float>(S * S);
+    float *wy = s_wy[wave];
+    float *wx = s_wx[wave];
+    const gcptr<TG> gcg = as_global<TG>(a.gout) + static_cast<int64_t>(cg) * 64 * NB;
+    const int64_t kstride = static_cast<int64_t>(a.lv.C) * NB;
+
+    // Coalesced copy of RoI k's gradient block into registers / LDS.
+    float pf[PF];
+    auto fetch = [&](int k) {
+#pragma unroll
+        for (int m = 0; m < PF; ++m) {
+            const int e = tid + 256 * m;
+            pf[m] = e < nvalid ? load_f32(gcg + k * kstride + e) : 0.0f;
+        }
+    };
+    auto put = [&](int buf) {
+#pragma unroll
+        for (int m = 0; m < PF; ++m) {
+            const int e = tid + 256 * m;
+            if (e < GB) s_g[buf][e] = pf[m];
+        }
+    };
+
+    for (int base = s0; base < s1; base += 64) {
+        const int n = min(64, s1 - base);
+        __syncthreads();   // previous batch fully consumed
+        if (tid < n) {
+            int k = a.tile_rois[base + tid];
+            int ok = 0;
+            float ax_s = 0.0f, ax_b = 0.0f, ay_s = 0.0f, ay_b = 0.0f;
+            if (k >= 0 && k < a.K) {
+                const float *r = a.rois + 5 * static_cast<int64_t>(k);
+                const float r0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
+                const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
+                if (lvl == l && roi_batch(r0, a.lv.N) == b) {
+                    const Axis ax = axis_setup(x1, x2, L.scale, a.aligned, PW, S);
+                    const Axis ay = axis_setup(y1, y2, L.scale, a.aligned, PH, S);
+                    ax_s = ax.start;
+                    ax_b = ax.bin;
+                    ay_s = ay.start;
+                    ay_b = ay.bin;
+                    ok = 1;
+                }
+            } else {
+                k = 0;
+            }
+            s_k[tid] = k;
+            s_ok[tid] = ok;
+            s_ax[tid][0] = ax_s;
+            s_ax[tid][1] = ax_b;
+            s_ax[tid][2] = ay_s;
+            s_ax[tid][3] = ay_b;
+        }
+        __syncthreads();
+        if constexpr (kDouble) {
+            fetch(s_k[0]);
+            put(0);
+        }
+        for (int j = 0; j < n; ++j) {
+            const int buf = kDouble ? (j & 1) : 0;
+            if constexpr (kDouble) {
+                if (j + 1 < n) fetch(s_k[j + 1]);   // lands while RoI j is processed
+            } else {
+                for (int e = tid; e < GB; e += 256)
+                    s_g[0][e] = e < nvalid ? load_f32(gcg + s_k[j] * kstride + e) : 0.0f;
+            }
+            const bool ok = s_ok[j] != 0;
+            // Sample taps of RoI j, once for the workgroup.
+            if (ok && tid < NR + NCOL) {
+                Axis ax;
+                if (tid < NR) {
+                    ax.start = s_ax[j][2];
+                    ax.bin = s_ax[j][3];
+                } else {
+                    ax.start = s_ax[j][0];
+                    ax.bin = s_ax[j][1];
+                }
+                ax.grid = S;
+                s_tap[tid] = tid < NR ? axis_tap(ax, tid / S, tid % S, L.H)
+                                      : axis_tap(ax, (tid - NR) / S, (tid - NR) % S, L.W);
+            }
+            __syncthreads();   // taps (and the staged block) visible
+
+            if (ok && wave_on) {
+                // This quadrant's separable weights and which bin rows / columns reach it.
+                uint32_t ymask = 0, xmask = 0;
+#pragma unroll
+                for (int p = 0; p < YP; ++p) {
+                    const int u = p * 64 + lane;
+                    bool hit = false;
+                    if (u < PH * T) {
+                        const int ph = u / T;
+                        const int R = R0 + (u % T);
+                        float w = 0.0f;
+#pragma unroll
+                        for (int iy = 0; iy < S; ++iy) {
+                            const Tap tp = s_tap[ph * S + iy];
+                            if (tp.lo >= 0) {
+                                if (tp.lo == R) {
+                                    w += tp.wlo;
+                                    hit = true;
+                                }
+                                if (tp.hi == R) {
+                                    w += tp.whi;
+                                    hit = true;
+                                }
+                            }
+                        }
+                        wy[u] = w * inv_count;
+                    }
+                    const uint64_t bits = __ballot(hit);
+#pragma unroll
+                    for (int h = 0; h < 8; ++h)
+                        if ((bits >> (8 * h)) & 0xffu) ymask |= 1u << (p * 8 + h);
+                }
+#pragma unroll
+                for (int p = 0; p < XP; ++p) {
+                    const int u = p * 64 + lane;
+                    bool hit = false;
+                    if (u < PW * T) {
+                        const int pw = u / T;
+                        const int Q = Q0 + (u % T);
+                        float w = 0.0f;
+#pragma unroll
+                        for (int ix = 0; ix < S; ++ix) {
+                            const Tap tp = s_tap[NR + pw * S + ix];
+                            if (tp.lo >= 0) {
+                                if (tp.lo == Q) {
+                                    w += tp.wlo;
+                                    hit = true;
+                                }
+                                if (tp.hi == Q) {
+                                    w += tp.whi;
+                                    hit = true;
+                                }
+                            }
+                        }
+                        wx[u] = w;
+                    }
+                    const uint64_t bits = __ballot(hit);
+#pragma unroll
+                    for (int h = 0; h < 8; ++h)
+                        if ((bits >> (8 * h)) & 0xffu) xmask |= 1u << (p * 8 + h);
+                }
+                wave_sync();
+
+                const float *gl = s_g[buf] + lane * NB;   // this lane's channel, stride NB (odd)
+                for (uint32_t ym = ymask; ym; ym &= ym - 1) {
+                    const int ph = __builtin_ctz(ym);
+                    float X[T];
+#pragma unroll
+                    for (int q = 0; q < T; ++q) X[q] = 0.0f;
+                    for (uint32_t xm = xmask; xm; xm &= xm - 1) {
+                        const int pw = __builtin_ctz(xm);
+                        const float gv = gl[ph * PW + pw];
+                        const float4 w0 = *reinterpret_cast<const float4 *>(wx + pw * T);
+                        const float4 w1 = *reinterpret_cast<const float4 *>(wx + pw * T + 4);
+                        X[0] = fmaf(w0.x, gv, X[0]);
+                        X[1] = fmaf(w0.y, gv, X[1]);
+                        X[2] = fmaf(w0.z, gv, X[2]);
+                        X[3] = fmaf(w0.w, gv, X[3]);
+                        X[4] = fmaf(w1.x, gv, X[4]);
+                        X[5] = fmaf(w1.y, gv, X[5]);
+                        X[6] = fmaf(w1.z, gv, X[6]);
+                        X[7] = fmaf(w1.w, gv, X[7]);
+                    }
+                    const float4 y0 = *reinterpret_cast<const float4 *>(wy + ph * T);
+                    const float4 y1 = *reinterpret_cast<const float4 *>(wy + ph * T + 4);
+                    const float yr[T] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
+#pragma unroll
+                    for (int rr = 0; rr < T; ++rr)
+#pragma unroll
+                        for (int q = 0; q < T; ++q) acc[rr][q] = fmaf(yr[rr], X[q], acc[rr][q]);
+                }
+            }
+            if constexpr (kDouble) {
+                if (j + 1 < n) put(buf ^ 1);
+            }
+            __syncthreads();   // taps, weights and the consumed block are reused next
+        }
+    }
+
+    if (!wave_on || !lane_on) return;
+    const gptr<float> gb = as_global_mut<float>(const_cast<void *>(L.data)) + b * L.sn + c;
+#pragma unroll
+    for (int rr = 0; rr < T; ++rr) {
+        const int R = R0 + rr;
+        if (R >= L.H) break;
+#pragma unroll
+        for (int q = 0; q < T; ++q) {
+            const int Q = Q0 + q;
+            if (Q >= L.W) break;
+            const gptr<float> p = gb + R * L.sh + Q * L.sw;
+            float v = acc[rr][q];
+            if (!a.zero_init) v += *p;
+            *p = v;
+        }
+    }
+}
+
+bool gather_available(int PH, int PW, int S) {
+    return S == 2 && ((PH == 7 && PW == 7) || (PH == 14 && PW == 14));
+}
+
+hipError_t launch_gather(GatherArgs a, int gout_dtype, hipStream_t stream) {
+    a.ncg = (a.lv.C + 63) / 64;
+    a.wg_per_tile = (a.qside * a.qside + 3) / 4;
+    const int64_t grid = static_cast<int64_t>(a.ntiles) * a.wg_per_tile * a.ncg;
+    if (grid <= 0) return hipSuccess;
+    if (grid >= (int64_t(1) << 24)) return hipErrorInvalidConfiguration;
+    const uint32_t g = static_cast<uint32_t>(grid);
+    if (gout_dtype == kF32) {
+        if (a.PH == 7)
+            bwd_gather_kernel<float, 7, 7, 2><<<g, 256, 0, stream>>>(a);
+        else
+            bwd_gather_kernel<float, 14, 14, 2><<<g, 256, 0, stream>>>(a);
+    } else {
+        if (a.PH == 7)
+            bwd_gather_kernel<uint16_t, 7, 7, 2><<<g, 256, 0, stream>>>(a);
+        else
+            bwd_gather_kernel<uint16_t, 14, 14, 2><<<g, 256, 0, stream>>>(a);
+    }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Zero fill
 // ---------------------------------------------------------------------------
 

@@ -49,6 +49,23 @@ __device__ __forceinline__ LevelArg level_at(const LevelTable &t, int l) {
     }
 }
 
+// Element `l` (0 <= l < 8) of a small per-level array in the kernel arguments,
+// written with constant indices only, for the same reason as level_at.
+template <typename T, int N>
+__device__ __forceinline__ T pick(const T (&arr)[N], int l) {
+    static_assert(N >= kMaxLevels, "per-level array");
+    switch (l) {
+        case 1: return arr[1];
+        case 2: return arr[2];
+        case 3: return arr[3];
+        case 4: return arr[4];
+        case 5: return arr[5];
+        case 6: return arr[6];
+        case 7: return arr[7];
+        default: return arr[0];
+    }
+}
+
 // ---------------------------------------------------------------------------
 // bfloat16 <-> binary32
 // ---------------------------------------------------------------------------

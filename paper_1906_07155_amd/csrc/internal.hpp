@@ -26,6 +26,47 @@ struct PlanArgs {
     int32_t H[kMaxLevels], W[kMaxLevels];
     int32_t ncx[kMaxLevels], ncy[kMaxLevels], base[kMaxLevels];
     float scale[kMaxLevels];
+    // Tile binning for the gather backward: bin-tiles of 2^tile_shift pixels per
+    // (level, image); tile_start[ntiles + 1] / tile_rois[capacity] form a CSR list of
+    // the RoIs whose (conservative) footprint box meets each tile.
+    int32_t *tile_start;
+    int32_t *tile_rois;
+    int32_t *tile_order;   // [ntiles]: tiles by decreasing list length
+    int32_t ntiles;
+    int32_t capacity;
+    int32_t tile_shift;
+    int32_t pad2;
+    int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
+};
+
+// Tile layout shared by the plan and the gather backward (a function of the level
+// shapes and the batch size only).
+struct TileLayout {
+    int32_t shift;
+    int32_t ntiles;
+    int64_t capacity;
+    int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
+};
+
+struct GatherArgs {
+    LevelTable lv;               // gradient levels (binary32, channels-last)
+    const void *gout;
+    const float *rois;
+    const int32_t *roi_levels;
+    const int32_t *tile_start;
+    const int32_t *tile_rois;
+    const int32_t *tile_order;
+    int32_t K;
+    int32_t PH, PW, S;
+    int32_t aligned;
+    int32_t zero_init;
+    int32_t ntiles;
+    int32_t capacity;
+    int32_t tile_shift;
+    int32_t qside;               // 8x8 quadrants per bin-tile side
+    int32_t ncg;                 // 64-channel groups
+    int32_t wg_per_tile;
+    int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
 };
 
 struct FwdArgs {
@@ -67,6 +108,10 @@ hipError_t launch_fwd(FwdArgs a, int feat_dtype, int out_dtype, bool fast, hipSt
 
 bool bwd_fast_available(int PH, int PW, int S);
 hipError_t launch_bwd(BwdArgs a, int gout_dtype, bool fast, hipStream_t stream);
+
+// Tile-gather backward (channels-last levels, specialised grids, a plan with tiles).
+bool gather_available(int PH, int PW, int S);
+hipError_t launch_gather(GatherArgs a, int gout_dtype, hipStream_t stream);
 
 // Zero every element of the (binary32) levels in `lv`; `numel[l]` and `dense[l]`
 // describe each level (dense levels are cleared as flat arrays).

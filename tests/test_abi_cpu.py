@@ -39,15 +39,19 @@ def test_status_strings_and_version(L):
 
 
 def test_workspace_size(L):
+    lv = _levels()
     n = ctypes.c_size_t(0)
-    assert L.roi_extract_workspace_size(0, 4, ctypes.byref(n)) == OK
+    assert L.roi_extract_workspace_size(lv, 2, 0, ctypes.byref(n)) == OK
     base = n.value
-    assert L.roi_extract_workspace_size(1024, 4, ctypes.byref(n)) == OK
-    assert n.value >= base + 8 * 1024 and n.value % 256 == 0
-    assert L.roi_extract_workspace_size(-1, 4, ctypes.byref(n)) == INVALID
-    assert L.roi_extract_workspace_size(10, 0, ctypes.byref(n)) == INVALID
-    assert L.roi_extract_workspace_size(10, 9, ctypes.byref(n)) == INVALID
-    assert L.roi_extract_workspace_size(10, 4, None) == INVALID
+    assert L.roi_extract_workspace_size(lv, 2, 1024, ctypes.byref(n)) == OK
+    # perm + keys (8 B per RoI) + tile lists (4 B per RoI and tile of the largest map:
+    # 16x20 px in 16-px tiles = 2 tiles)
+    assert n.value >= 8 * 1024 + 4 * 1024 * 2 and n.value > base and n.value % 256 == 0
+    assert L.roi_extract_workspace_size(lv, 2, -1, ctypes.byref(n)) == INVALID
+    assert L.roi_extract_workspace_size(lv, 0, 10, ctypes.byref(n)) == INVALID
+    assert L.roi_extract_workspace_size(lv, 9, 10, ctypes.byref(n)) == INVALID
+    assert L.roi_extract_workspace_size(lv, 2, 10, None) == INVALID
+    assert L.roi_extract_workspace_size(None, 2, 10, ctypes.byref(n)) == INVALID
 
 
 def _levels(n=2, c=8, hw=((16, 20), (8, 10)), dtype=0, scales=(0.25, 0.125), data=FAKE):
@@ -66,10 +70,10 @@ def _fwd(L, levels=None, nl=2, rois=FAKE, K=4, roi_levels=FAKE, oh=7, ow=7, sr=2
 
 
 def _bwd(L, levels=None, nl=2, gout=FAKE, gdt=0, K=4, zero=0, sr=2, al=1, oh=7, ow=7,
-         plan=None, plan_bytes=0):
+         plan=None, plan_bytes=0, algo=0):
     levels = levels if levels is not None else _levels()
-    return L.roi_align_bwd(gout, gdt, FAKE, K, FAKE, oh, ow, sr, al, levels, nl, zero, plan,
-                           plan_bytes, None)
+    return L.roi_align_bwd(gout, gdt, FAKE, K, FAKE, oh, ow, sr, al, levels, nl, zero, algo,
+                           plan, plan_bytes, None)
 
 
 def test_level_map_validation(L):
@@ -140,6 +144,17 @@ def test_backward_validation(L):
     assert _bwd(L, sr=-2) == INVALID
     assert _bwd(L, plan=FAKE, plan_bytes=8) == WORKSPACE
     assert _bwd(L, K=0, zero=0) == OK                              # nothing to do
+    assert _bwd(L, algo=3) == INVALID
+    assert _bwd(L, algo=2) == UNSUPPORTED                          # gather needs a plan
+    n = ctypes.c_size_t(0)
+    assert L.roi_extract_workspace_size(_levels(), 2, 4, ctypes.byref(n)) == OK
+    assert _bwd(L, algo=2, plan=FAKE, plan_bytes=n.value, oh=5) == UNSUPPORTED   # 5x7 grid
+    assert _bwd(L, algo=2, plan=FAKE, plan_bytes=n.value, sr=0) == UNSUPPORTED   # adaptive
+    nchw = _levels()
+    for i in range(2):
+        nchw[i].stride_c, nchw[i].stride_h, nchw[i].stride_w = nchw[i].h * nchw[i].w, nchw[i].w, 1
+        nchw[i].stride_n = nchw[i].c * nchw[i].h * nchw[i].w
+    assert _bwd(L, levels=nchw, algo=2, plan=FAKE, plan_bytes=n.value) == UNSUPPORTED
     assert L.roi_extract_zero_grad(_levels(dtype=1), 2, None) == UNSUPPORTED
     assert L.roi_extract_zero_grad(None, 2, None) == INVALID
 
@@ -147,7 +162,7 @@ def test_backward_validation(L):
 def test_plan_validation(L):
     lv = _levels()
     n = ctypes.c_size_t(0)
-    assert L.roi_extract_workspace_size(4, 2, ctypes.byref(n)) == OK
+    assert L.roi_extract_workspace_size(lv, 2, 4, ctypes.byref(n)) == OK
     assert L.roi_extract_plan(lv, 2, FAKE, 4, 56.0, FAKE, None, n.value, None) == WORKSPACE
     assert L.roi_extract_plan(lv, 2, FAKE, 4, 56.0, FAKE, FAKE, n.value - 1, None) == WORKSPACE
     assert L.roi_extract_plan(lv, 2, FAKE, 4, 0.0, FAKE, FAKE, n.value, None) == INVALID

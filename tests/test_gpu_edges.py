@@ -57,7 +57,8 @@ def _rois(rng, K, n_images, img_w, img_h, outside=0.2):
 
 
 def run(name, shapes, scales, rois, out_hw=(7, 7), S=2, aligned=True, fdt="f32", odt="f32",
-        gdt="f32", layout="cl", roi_levels=None, use_plan=True, seed=0, backward=True):
+        gdt="f32", layout="cl", roi_levels=None, use_plan=True, seed=0, backward=True,
+        zero_init=True):
     log("edge case %s: shapes=%s K=%d out=%s S=%d aligned=%d %s->%s layout=%s" % (
         name, shapes, rois.shape[0], out_hw, S, aligned, fdt, odt, layout))
     rng = np.random.default_rng(seed)
@@ -88,19 +89,29 @@ def run(name, shapes, scales, rois, out_hw=(7, 7), S=2, aligned=True, fdt="f32",
     g = rng.standard_normal((K, C) + tuple(out_hw), dtype=np.float32)
     if gdt == "bf16":
         g = W.f32_to_bf16_bits(g)
-    grads = [torch.full(s, 7.0, dtype=torch.float32, device="cuda") for s in shapes]
-    if layout in ("cl", "cl_view"):
-        grads = [x.contiguous(memory_format=torch.channels_last) for x in grads]
-    rex.roi_align_bwd(to_device(g, gdt, "nchw"), r_dev, lv_dev, out_hw, S, aligned, grads,
-                      scales, zero_init=True, workspace=ws)
-    torch.cuda.synchronize()
     g64 = as_f64(g, gdt)
     gref = oracle.roi_align_bwd(g64, shapes, scales, rois, lv, out_hw[0], out_hw[1], S, aligned,
                                 "parity")
     aref = oracle.roi_align_bwd(np.abs(g64), shapes, scales, rois, lv, out_hw[0], out_hw[1], S,
                                 aligned, "parity")
-    for l in range(L):
-        check_bwd(from_device(grads[l]), gref[l], aref[l], False, "%s backward level %d" % (name, l))
+    # scatter always; the gather where it applies (plan, channels-last, 7x7 / 14x14, S = 2)
+    algos = ["scatter"]
+    if ws is not None and layout in ("cl", "cl_view") and S == 2 and tuple(out_hw) in (
+            (7, 7), (14, 14)):
+        algos.append("gather")
+    for algo in algos:
+        grads = [torch.full(s, 7.0, dtype=torch.float32, device="cuda") for s in shapes]
+        if layout in ("cl", "cl_view"):
+            grads = [x.contiguous(memory_format=torch.channels_last) for x in grads]
+        rex.roi_align_bwd(to_device(g, gdt, "nchw"), r_dev, lv_dev, out_hw, S, aligned, grads,
+                          scales, zero_init=zero_init, workspace=ws, algorithm=algo)
+        torch.cuda.synchronize()
+        base = 0.0 if zero_init else 7.0
+        for l in range(L):
+            # accumulating onto `base` adds one binary32 rounding of base + sum
+            scale = aref[l] + base * 2.0 ** -20 / 1e-4
+            check_bwd(from_device(grads[l]) - base, gref[l], scale, False,
+                      "%s backward (%s) level %d" % (name, algo, l))
     return out
 
 
@@ -198,6 +209,24 @@ def test_one_and_zero_rois():
     torch.cuda.synchronize()
     assert out.shape == (0, 100, 7, 7)
     assert all(not g.any() for g in grads)
+
+
+@pytest.mark.parametrize("out_hw", [(7, 7), (14, 14)])
+def test_backward_accumulates_without_zero_init(out_hw):
+    rng = np.random.default_rng(85)
+    rois = W.draw_rois(rng, 2, 33, (96, 160), (4.0, 200.0))
+    run("accumulate %s" % (out_hw,), _pyr(96), SC, rois, out_hw=out_hw, zero_init=False)
+
+
+def test_dense_rois_on_one_tile():
+    """Many RoIs on top of each other (long tile lists, heavy duplication)."""
+    rng = np.random.default_rng(86)
+    base = np.array([0, 20.0, 12.0, 60.0, 44.0], np.float32)
+    rois = np.tile(base, (150, 1))
+    rois[:, 1:] += rng.uniform(-3, 3, (150, 4)).astype(np.float32)
+    rois[:, 0] = rng.integers(0, 2, 150)
+    run("150 stacked RoIs", _pyr(64), SC, rois)
+    run("150 stacked RoIs mask", _pyr(64), SC, rois, out_hw=(14, 14))
 
 
 def test_plan_order_is_irrelevant_to_results():

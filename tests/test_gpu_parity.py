@@ -56,12 +56,12 @@ def _run_fwd(c: Case, plan=True):
     return levels, ws, out
 
 
-def _run_bwd(c: Case, levels, ws, g_np):
+def _run_bwd(c: Case, levels, ws, g_np, algorithm):
     g = to_device(g_np, c.wl.grad_dtype, layout="nchw")
-    grads = [torch.empty(s, dtype=torch.float32, device="cuda",
-                         memory_format=torch.channels_last) for s in c.shapes]
+    grads = [torch.full(s, 3.0, dtype=torch.float32, device="cuda").contiguous(
+        memory_format=torch.channels_last) for s in c.shapes]
     rex.roi_align_bwd(g, c.rois_dev, levels, c.wl.out_hw, c.wl.sampling_ratio, c.wl.aligned,
-                      grads, c.scales, zero_init=True, workspace=ws)
+                      grads, c.scales, zero_init=True, workspace=ws, algorithm=algorithm)
     torch.cuda.synchronize()
     return grads
 
@@ -104,13 +104,14 @@ def test_forward_full(idx, head, fdt):
     log("  max abs err %.3e" % err)
 
 
+@pytest.mark.parametrize("algorithm", ["scatter", "gather"])
 @pytest.mark.parametrize("idx,head,fdt", [(2, None, None), (3, None, None)])
-def test_backward_full(idx, head, fdt):
+def test_backward_full(idx, head, fdt, algorithm):
     c = _case(idx, head, fdt)
-    log("backward full: workload %d, K=%d" % (idx, c.K))
+    log("backward full (%s): workload %d, K=%d" % (algorithm, idx, c.K))
     levels, ws, _ = _run_fwd(c)
     g = c.wl.grad()
-    grads = _run_bwd(c, levels, ws, g)
+    grads = _run_bwd(c, levels, ws, g, algorithm)
     ref_lv = c.oracle_levels()
     g64 = as_f64(g, c.wl.grad_dtype)
     ref = oracle.roi_align_bwd(g64, c.shapes, c.scales, c.rois, ref_lv, *c.wl.out_hw,
@@ -123,13 +124,15 @@ def test_backward_full(idx, head, fdt):
         log("  level %d rel norm err %.3e" % (l, r))
 
 
+@pytest.mark.parametrize("algorithm", ["scatter", "gather"])
 @pytest.mark.parametrize("idx,head,fdt", SAMPLED)
-def test_batch16_sampled(idx, head, fdt):
+def test_batch16_sampled(idx, head, fdt, algorithm):
     c = _case(idx, head, fdt)
-    log("batch-16 %s head: fwd+bwd at full size, sampled comparison, K=%d" % (head, c.K))
+    log("batch-16 %s head (%s): fwd+bwd at full size, sampled comparison, K=%d" % (
+        head, algorithm, c.K))
     levels, ws, out = _run_fwd(c)
     g = c.wl.grad()
-    grads = _run_bwd(c, levels, ws, g)
+    grads = _run_bwd(c, levels, ws, g, algorithm)
     rng = np.random.default_rng(5)
     chans = np.sort(rng.choice(c.wl.channels, 6, replace=False))
     sub = np.sort(rng.choice(c.K, 384, replace=False))
@@ -163,13 +166,16 @@ def test_forward_is_deterministic_and_plan_independent():
     assert torch.equal(a, d)
 
 
-def test_backward_repeatable_within_tolerance():
+@pytest.mark.parametrize("algorithm", ["scatter", "gather"])
+def test_backward_repeatable_within_tolerance(algorithm):
     c = _case(3)
-    log("repeatability: workload 3 backward x2")
+    log("repeatability: workload 3 backward (%s) x2, and against the other algorithm" % algorithm)
     levels, ws, _ = _run_fwd(c)
     g = c.wl.grad()
-    g1 = _run_bwd(c, levels, ws, g)
-    g2 = _run_bwd(c, levels, ws, g)
-    for a, b in zip(g1, g2):
-        d = (a - b).abs().max().item()
-        assert d <= 1e-4 * max(a.abs().max().item(), 1e-30)
+    g1 = _run_bwd(c, levels, ws, g, algorithm)
+    g2 = _run_bwd(c, levels, ws, g, algorithm)
+    g3 = _run_bwd(c, levels, ws, g, "scatter" if algorithm == "gather" else "gather")
+    for a, b, d in zip(g1, g2, g3):
+        scale = max(a.abs().max().item(), 1e-30)
+        assert (a - b).abs().max().item() <= 1e-4 * scale
+        assert (a - d).abs().max().item() <= 1e-4 * scale
