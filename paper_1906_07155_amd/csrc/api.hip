@@ -124,6 +124,12 @@ re_status_t check_levels(const re_level_t *levels, int32_t num_levels, bool need
         a.W = static_cast<int32_t>(v.w);
         a.scale = v.spatial_scale;
         if (v.stride_c != 1 && v.c != 1) cl = false;   // a single channel has no stride
+        // the channels-last kernels address one image of a level with 32-bit byte
+        // offsets below 2^30
+        const double img = (double(v.c - 1) * v.stride_c + double(v.h - 1) * v.stride_h +
+                            double(v.w - 1) * v.stride_w + 1.0) * dtype_size(v.dtype);
+        if (img < double(kBufMaxBytes)) a.img_bytes = static_cast<uint32_t>(img);
+        else cl = false;
         if (numel) numel[l] = v.n * v.c * v.h * v.w;
         if (dense) {
             // dense: the strides are those of a contiguous tensor for some order of dims

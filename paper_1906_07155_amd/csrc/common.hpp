@@ -23,7 +23,7 @@ struct LevelArg {
     int64_t sn, sc, sh, sw;
     int32_t H, W;
     float scale;
-    int32_t pad;
+    uint32_t img_bytes;   // bytes spanned by one image (0: too large for buffer addressing)
 };
 
 struct LevelTable {
@@ -105,6 +105,44 @@ template <typename T> __device__ __forceinline__ void store_f32(gptr<T> p, float
 template <> __device__ __forceinline__ void store_f32<float>(gptr<float> p, float v) { *p = v; }
 template <> __device__ __forceinline__ void store_f32<uint16_t>(gptr<uint16_t> p, float v) {
     *p = f32_to_bf16(v);
+}
+
+// ---------------------------------------------------------------------------
+// Buffer-resource loads
+// ---------------------------------------------------------------------------
+// A raw buffer resource (stride 0) holds a base address and a byte range in
+// scalar registers; each lane then supplies one 32-bit byte offset, and the
+// hardware's range check makes an offset at or past the range read 0 without a
+// memory access.  Offsets inside one image of a level stay below 2^30 (checked on
+// the host), so adding kBufOOB to any term of an offset sum pushes it out of range
+// without wrapping, even when all three terms carry it.
+constexpr uint32_t kBufOOB = 0x40000000u;
+constexpr uint32_t kBufMaxBytes = 0x40000000u;
+constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, no swizzle (gfx9 family)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0,
+                                             static_cast<int>(bytes), kBufDword3);
+}
+
+// Raw element bits (fp32 bits, or bf16 bits zero-extended); the conversion is a
+// separate step so a batch of loads can be issued before any of them is waited on.
+template <typename T> __device__ __forceinline__ uint32_t buf_load_raw(__amdgpu_buffer_rsrc_t r,
+                                                                       uint32_t off);
+template <> __device__ __forceinline__ uint32_t buf_load_raw<float>(__amdgpu_buffer_rsrc_t r,
+                                                                    uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+template <> __device__ __forceinline__ uint32_t buf_load_raw<uint16_t>(__amdgpu_buffer_rsrc_t r,
+                                                                       uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+template <typename T> __device__ __forceinline__ float raw_to_f32(uint32_t v);
+template <> __device__ __forceinline__ float raw_to_f32<float>(uint32_t v) {
+    return __uint_as_float(v);
+}
+template <> __device__ __forceinline__ float raw_to_f32<uint16_t>(uint32_t v) {
+    return __uint_as_float(v << 16);
 }
 
 // ---------------------------------------------------------------------------

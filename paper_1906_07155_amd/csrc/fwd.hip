@@ -5,19 +5,32 @@
 //
 // Two kernels:
 //   fwd_cl_kernel       channels-last levels (stride_c == 1), specialised output
-//                       grids.  One workgroup = one RoI x up to 4 channel slices
-//                       (one wavefront each).  The RoI's sample geometry (bilinear
-//                       indices and weights of every sample row and column) is
-//                       computed once into LDS and shared by every channel; lanes
-//                       run over channels, so each corner tap is one coalesced,
-//                       channel-contiguous load.  Results are transposed through a
-//                       small per-wave LDS tile so the [C][PH][PW] block of the RoI is
-//                       stored contiguously at its original RoI index.
+//                       grids.  One workgroup = one RoI x one slice of 64 channels;
+//                       lanes run over channels, so every pixel read is one
+//                       coalesced, channel-contiguous load.  The RoI's sample
+//                       geometry is reduced once into LDS to its distinct tap rows
+//                       and columns with summed weights (the footprint), every
+//                       footprint pixel is loaded once, and the bins are formed as
+//                       two small separable products.  Results are transposed
+//                       through LDS so the [C][PH][PW] block of the RoI is stored
+//                       contiguously at its original RoI index.
 //   fwd_generic_kernel  any strides, output size and sampling ratio: one thread per
 //                       output element.
 #include "internal.hpp"
 
 namespace rex {
+
+// Units of footprint loads a forward wave keeps in flight ahead of the one it
+// reduces, and distinct columns per unit.
+#ifndef REX_FWD_DEPTH
+#define REX_FWD_DEPTH 2
+#endif
+#ifndef REX_FWD_CX
+#define REX_FWD_CX 8
+#endif
+constexpr int kFwdDepth = REX_FWD_DEPTH;
+constexpr int kFwdCX = REX_FWD_CX;
+
 
 // ---------------------------------------------------------------------------
 // General strided kernel
@@ -69,130 +82,363 @@ __global__ __launch_bounds__(256) void fwd_generic_kernel(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Channels-last kernel
+// Channels-last kernel: footprint-exact separable gather
 // ---------------------------------------------------------------------------
+//
+// With the sample geometry separable, the average over one bin is
+//     out[ph][pw] = sum_y sum_x Wy[ph][y] * Wx[pw][x] * F[y][x]
+// where y runs over the distinct tap rows and x over the distinct tap columns of
+// the RoI, and Wy[ph][y] (Wx[pw][x]) is the summed bilinear weight, divided by S,
+// that the samples of bin row ph (bin column pw) give to row y (column x).  Each
+// pixel of the footprint is therefore loaded exactly once per channel, however
+// many samples share it, and the weights are applied as two small dense products.
 
-// Channels per LDS transpose chunk: the largest divisor of CL whose chunk holds at
-// most 800 floats.
-__host__ __device__ constexpr int chunk_channels(int CL, int NB) {
-    int c = CL;
-    while (c > 1 && c * NB > 800) c /= 2;
-    return c;
+struct SampleTap {               // one sample row / column: taps and weights
+    int32_t lo;                  // -1: sample outside the map
+    int32_t hi;
+    float w_lo;
+    float w_hi;
+};
+
+// Distinct tap positions of `ns` consecutive samples (lane s < ns holds sample s;
+// S samples per bin), computed by one wavefront.  Sample coordinates are
+// non-decreasing, so the taps are too: a position is new exactly when it exceeds
+// the previous sample's upper tap, and its rank among the distinct positions
+// follows from two ballots.  If the taps are not monotone (a degenerate RoI whose
+// rounded coordinates step backwards), every tap simply gets a slot of its own.
+// Writes the byte offset of each distinct position to off[] and, for each bin b,
+// the summed weight (times wscale) of each position to w[rank][b]; both arrays
+// must be pre-set to the out-of-range offset and to zero.  Returns the count.
+template <int S, int NW>
+__device__ __forceinline__ int distinct_taps(const SampleTap *taps, int ns, int lane,
+                                             uint32_t stride_b, float wscale, uint32_t *off,
+                                             float (*w)[NW]) {
+    SampleTap st, pv;
+    st.lo = pv.lo = -1;
+    st.hi = pv.hi = -1;
+    st.w_lo = st.w_hi = pv.w_lo = pv.w_hi = 0.0f;
+    if (lane < ns) st = taps[lane];
+    if (lane < ns && lane > 0) pv = taps[lane - 1];
+    const bool valid = st.lo >= 0;
+    const bool pvalid = pv.lo >= 0;
+    const uint64_t vm = __builtin_amdgcn_ballot_w64(valid);
+    const bool down = valid && pvalid && (st.lo < pv.lo || st.hi < pv.hi);
+    const uint64_t run = vm ? (vm >> __builtin_ctzll(vm)) : 0;
+    const bool mono = __builtin_amdgcn_ballot_w64(down) == 0 && ((run + 1) & run) == 0;
+    int r_lo, r_hi, n;
+    if (mono) {
+        const bool new_lo = valid && (!pvalid || st.lo > pv.hi);
+        const bool new_hi = valid && st.hi > st.lo && (!pvalid || st.hi > pv.hi);
+        const uint64_t bl = __builtin_amdgcn_ballot_w64(new_lo);
+        const uint64_t bh = __builtin_amdgcn_ballot_w64(new_hi);
+        const int below = static_cast<int>(
+            __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(bl >> 32),
+                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bl), 0u)) +
+            __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(bh >> 32),
+                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bh), 0u)));
+        r_lo = new_lo ? below : below - 1 - (pv.hi - st.lo);
+        r_hi = r_lo + (st.hi - st.lo);
+        n = __builtin_popcountll(bl) + __builtin_popcountll(bh);
+        if (new_lo) off[r_lo] = static_cast<uint32_t>(st.lo) * stride_b;
+        if (new_hi) off[r_hi] = static_cast<uint32_t>(st.hi) * stride_b;
+    } else {
+        r_lo = 2 * lane;
+        r_hi = 2 * lane + 1;
+        n = 2 * ns;
+        if (valid) {
+            off[r_lo] = static_cast<uint32_t>(st.lo) * stride_b;
+            off[r_hi] = static_cast<uint32_t>(st.hi) * stride_b;
+        }
+    }
+    // Per bin, its first lane sums the weights of the bin's samples in sample order
+    // (lo before hi), so the result does not depend on scheduling.  The ranks one
+    // bin touches span at most 2S consecutive slots.
+    const float wl = valid ? st.w_lo * wscale : 0.0f;
+    const float wh = valid ? st.w_hi * wscale : 0.0f;
+    int rl[S], rh[S];
+    float fl[S], fh[S];
+    bool ok[S];
+#pragma unroll
+    for (int t = 0; t < S; ++t) {
+        const int src = min(lane + t, 63);
+        rl[t] = __shfl(r_lo, src);
+        rh[t] = __shfl(r_hi, src);
+        fl[t] = __shfl(wl, src);
+        fh[t] = __shfl(wh, src);
+        ok[t] = __shfl(valid ? 1 : 0, src) != 0 && lane + t < ns;
+    }
+    if (lane < ns && lane % S == 0) {
+        int base = INT32_MAX;
+#pragma unroll
+        for (int t = 0; t < S; ++t)
+            if (ok[t]) base = min(base, rl[t]);
+        if (base != INT32_MAX) {
+            float win[2 * S];
+#pragma unroll
+            for (int e = 0; e < 2 * S; ++e) win[e] = 0.0f;
+#pragma unroll
+            for (int t = 0; t < S; ++t) {
+                if (!ok[t]) continue;
+#pragma unroll
+                for (int e = 0; e < 2 * S; ++e) win[e] += (rl[t] - base == e) ? fl[t] : 0.0f;
+#pragma unroll
+                for (int e = 0; e < 2 * S; ++e) win[e] += (rh[t] - base == e) ? fh[t] : 0.0f;
+            }
+            const int bin = lane / S;
+#pragma unroll
+            for (int e = 0; e < 2 * S; ++e)
+                if (base + e < n) w[base + e][bin] = win[e];
+        }
+    }
+    return n;
 }
 
-template <typename T, typename TO, int PH, int PW, int S, int CL>
+// One workgroup per (RoI, slice of 64 channels); lane = channel.  Wave w owns bin
+// rows [w*RPW, min(PH, (w+1)*RPW)) and loads the distinct tap rows of those bin
+// rows times all distinct tap columns of the RoI, in chunks of CX columns, with
+// the next unit's loads issued before the current one is reduced.
+template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK>
 __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
-    constexpr int NG = 64 / CL;                 // bin groups per wavefront
     constexpr int NB = PH * PW;
-    constexpr int BPL = (NB + NG - 1) / NG;     // bins per lane
-    constexpr int NR = PH * S;
-    constexpr int NCOL = PW * S;
-    constexpr int CHK = chunk_channels(CL, NB);
-    static_assert(NR + NCOL <= 256, "geometry must fit one pass of the workgroup");
+    constexpr int NR = PH * S;                   // sample rows
+    constexpr int NCOL = PW * S;                 // sample columns
+    constexpr int RPW = (PH + 3) / 4;            // bin rows per wave
+    constexpr int RPWP = (RPW + 3) & ~3;
+    constexpr int MAXY = 2 * RPW * S;            // distinct tap rows per wave
+    constexpr int MAXX = ((2 * NCOL + CX - 1) / CX) * CX;   // distinct tap columns, padded
+    constexpr int PWP = (PW + 3) & ~3;           // padded for 16-byte LDS reads
+    static_assert(NR + NCOL <= 256 && NCOL <= 64 && RPW * S <= 64, "geometry sizes");
+    static_assert(64 % CHK == 0 && CX % 4 == 0, "tiling");
 
-    __shared__ Tap srow[NR];
-    __shared__ Tap scol[NCOL];
-    __shared__ float stile[4][CHK * NB];
+    __shared__ SampleTap srow[NR];
+    __shared__ SampleTap scol[NCOL];
+    __shared__ __align__(16) uint32_t s_xoff[MAXX];
+    __shared__ __align__(16) float s_wx[MAXX][PWP];
+    __shared__ uint32_t s_yoff[4][MAXY];
+    __shared__ __align__(16) float s_wy[4][MAXY][RPWP];
+    __shared__ int32_t s_nx;
+    __shared__ int32_t s_ny[4];
+    __shared__ float stile[CHK * NB];
 
-    // Which RoI: XCD-aware block order, then the plan's permutation.
+    // Which RoI and slice: XCD-aware block order, then the plan's permutation.
     const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
-    const int slot = static_cast<int>(lid / static_cast<uint32_t>(a.wg_per_roi));
-    const int sub = static_cast<int>(lid) - slot * a.wg_per_roi;
-    int k = a.perm ? a.perm[slot] : slot;
+    const int slot = static_cast<int>(lid / static_cast<uint32_t>(a.nslices));
+    const int slice = static_cast<int>(lid) - slot * a.nslices;
+    int k = uniform_i(a.perm ? a.perm[slot] : slot);
     const bool kvalid = k >= 0 && k < a.K;
     if (!kvalid) k = 0;
     const float *r = a.rois + 5 * static_cast<int64_t>(k);
     const float rb = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
-    const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
+    const int lvl = uniform_i(a.roi_levels ? a.roi_levels[k] : 0);
     const bool lvalid = lvl >= 0 && lvl < a.lv.num;
     const LevelArg L = level_at(a.lv, lvalid ? lvl : 0);
     const int b = roi_batch(rb, a.lv.N);
     const bool active = kvalid && lvalid && b >= 0;
 
-    // a3: sample geometry of the RoI, once, shared by every channel.
+    const int t = threadIdx.x;
+    const int wave = t >> 6;
+    const int lane = t & 63;
+    const int p0 = wave * RPW;
+    const int p1 = min(PH, p0 + RPW);
+    const uint32_t sh_b = static_cast<uint32_t>(L.sh * int64_t(sizeof(T)));
+    const uint32_t sw_b = static_cast<uint32_t>(L.sw * int64_t(sizeof(T)));
+
+    // a3: sample geometry, once per workgroup (an inactive RoI gets no valid
+    // sample, so its outputs are zero), and cleared footprint tables.
     {
         const Axis ax = axis_setup(x1, x2, L.scale, a.aligned, PW, S);
         const Axis ay = axis_setup(y1, y2, L.scale, a.aligned, PH, S);
-        const int t = threadIdx.x;
-        if (t < NR) {
-            srow[t] = axis_tap(ay, t / S, t % S, L.H);
-        } else if (t < NR + NCOL) {
-            const int u = t - NR;
-            scol[u] = axis_tap(ax, u / S, u % S, L.W);
+        if (t < NR + NCOL) {
+            const bool isrow = t < NR;
+            const int u = isrow ? t : t - NR;
+            const Tap tp = axis_tap(isrow ? ay : ax, u / S, u % S, isrow ? L.H : L.W);
+            SampleTap st;
+            st.lo = active ? tp.lo : -1;
+            st.hi = tp.hi;
+            st.w_lo = tp.wlo;
+            st.w_hi = tp.whi;
+            if (isrow) srow[u] = st;
+            else scol[u] = st;
+        }
+        for (int e = t; e < MAXX * PWP; e += 256) (&s_wx[0][0])[e] = 0.0f;
+        for (int e = t; e < 4 * MAXY * RPWP; e += 256) (&s_wy[0][0][0])[e] = 0.0f;
+        for (int e = t; e < MAXX; e += 256) s_xoff[e] = kBufOOB;
+        for (int e = t; e < 4 * MAXY; e += 256) (&s_yoff[0][0])[e] = kBufOOB;
+    }
+    __syncthreads();
+    // Footprint: distinct tap rows of each wave's bin rows, distinct tap columns of
+    // the RoI (wave 0); weights carry the 1/S of the sample average along their axis.
+    constexpr float kInvS = 1.0f / static_cast<float>(S);
+    {
+        const int ny = distinct_taps<S, RPWP>(srow + p0 * S, (p1 - p0) * S, lane, sh_b, kInvS,
+                                              s_yoff[wave], s_wy[wave]);
+        if (lane == 0) s_ny[wave] = ny;
+        if (wave == 0) {
+            const int nx = distinct_taps<S, PWP>(scol, NCOL, lane, sw_b, kInvS, s_xoff, s_wx);
+            if (lane == 0) s_nx = nx;
         }
     }
     __syncthreads();
 
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int slice = sub * 4 + wave;
-    const bool wave_on = slice < a.nslices;
-    const int cc = lane % CL;
-    const int bg = lane / CL;
-    const int c = slice * CL + cc;
-    const bool lane_on = active && wave_on && c < a.lv.C;
-    const gcptr<T> base = as_global<T>(L.data) + (lane_on ? (b * L.sn + c) : 0);
-    const int64_t sh = L.sh, sw = L.sw;
+    const int c = slice * 64 + lane;
+    const bool lane_on = active && c < a.lv.C;
+    // One buffer resource per image of the level; a lane with no channel reads out
+    // of range (zeros) instead of branching.
+    const char *img = static_cast<const char *>(L.data) +
+                      (active ? static_cast<int64_t>(b) * L.sn * int64_t(sizeof(T)) : 0);
+    const __amdgpu_buffer_rsrc_t res = make_rsrc(img, L.img_bytes);
+    const uint32_t vbase = lane_on ? static_cast<uint32_t>(c) * uint32_t(sizeof(T)) : kBufOOB;
 
-    // a4: gather and average.  Every load is issued unconditionally (an invalid
-    // sample reads pixel 0 and its contribution is discarded by a select), which
-    // keeps the body straight-line so many loads are in flight at once.
-    float acc[BPL];
-#pragma clang loop unroll(full)
-    for (int i = 0; i < BPL; ++i) {
-        const int j = bg + NG * i;
-        float s = 0.0f;
-        if (lane_on && j < NB) {
-            const int ph = j / PW;
-            const int pw = j - ph * PW;
+    // a4: gather.  Chunk-major over the footprint: for each chunk of CX distinct
+    // columns, every distinct row of the wave is loaded (work unit = (chunk, row))
+    // and reduced over rows first, H[x][p] = sum_y Wy[p][y] F[y][x]; at the end of
+    // the chunk the columns are reduced into the bins, acc[p][q] += Wx[q][x] H[x][p].
+    // Columns past the footprint read zeros (out-of-range offsets, zero weights).
+    const int ny = s_ny[wave];
+    const int nch = (s_nx + CX - 1) / CX;
+    float acc[RPW][PW];
 #pragma unroll
-            for (int iy = 0; iy < S; ++iy) {
-                const Tap ty = srow[ph * S + iy];
-                const bool vy = ty.lo >= 0;
-                const gcptr<T> p0 = base + (vy ? ty.lo : 0) * sh;
-                const gcptr<T> p1 = base + (vy ? ty.hi : 0) * sh;
+    for (int p = 0; p < RPW; ++p)
 #pragma unroll
-                for (int ix = 0; ix < S; ++ix) {
-                    const Tap tx = scol[pw * S + ix];
-                    const bool v = vy && tx.lo >= 0;
-                    const int64_t xl = (tx.lo >= 0 ? tx.lo : 0) * sw;
-                    const int64_t xh = (tx.lo >= 0 ? tx.hi : 0) * sw;
-                    const float v00 = load_f32(p0 + xl);
-                    const float v01 = load_f32(p0 + xh);
-                    const float v10 = load_f32(p1 + xl);
-                    const float v11 = load_f32(p1 + xh);
-                    float q = (ty.wlo * tx.wlo) * v00;
-                    q = fmaf(ty.wlo * tx.whi, v01, q);
-                    q = fmaf(ty.whi * tx.wlo, v10, q);
-                    q = fmaf(ty.whi * tx.whi, v11, q);
-                    s += v ? q : 0.0f;
-                }
-            }
-            s = s / static_cast<float>(S * S);
+        for (int q = 0; q < PW; ++q) acc[p][q] = 0.0f;
+    float H[CX][RPW];
+#pragma unroll
+    for (int x = 0; x < CX; ++x)
+#pragma unroll
+        for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
+
+    auto issue = [&](int ch, int yi, uint32_t (&v)[CX]) {
+        const uint32_t rowb = vbase + s_yoff[wave][yi];
+        const uint32_t *xo = s_xoff + ch * CX;
+#pragma unroll
+        for (int x = 0; x < CX; ++x) v[x] = buf_load_raw<T>(res, rowb + xo[x]);
+    };
+    auto consume = [&](int ch, int yi, const uint32_t (&v)[CX]) {
+        const float *wy = s_wy[wave][yi];
+#pragma unroll
+        for (int x = 0; x < CX; ++x) {
+            const float f = raw_to_f32<T>(v[x]);
+#pragma unroll
+            for (int p = 0; p < RPW; ++p) H[x][p] = fmaf(wy[p], f, H[x][p]);
         }
-        acc[i] = s;
+        if (yi == ny - 1) {
+#pragma unroll
+            for (int x = 0; x < CX; ++x) {
+                const float *wx = s_wx[ch * CX + x];
+#pragma unroll
+                for (int q = 0; q < PW; ++q)
+#pragma unroll
+                    for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+#pragma unroll
+                for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
+                // one column's weights live at a time
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    };
+
+    // Pipeline over the units in (chunk, row) order: the loads of units u+1 ..
+    // u+kFwdDepth are in flight while unit u is reduced.  The loop is unrolled by
+    // the ring size so every buffer index is a constant.
+    constexpr int D = kFwdDepth;
+    constexpr int NBUF = D + 1;
+    uint32_t v[NBUF][CX];
+    const int units = ny * nch;
+    int ic = 0, iy = 0;      // next unit to issue
+    int cc = 0, cy = 0;      // next unit to consume
+    auto step = [&](int &ch, int &y) {
+        if (++y == ny) {
+            y = 0;
+            ++ch;
+        }
+    };
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        if (d < units) {
+            issue(ic, iy, v[d]);
+            step(ic, iy);
+        }
+    }
+    for (int u0 = 0; u0 < units; u0 += NBUF) {
+#pragma unroll
+        for (int j = 0; j < NBUF; ++j) {
+            if (u0 + j >= units) break;
+            if (u0 + j + D < units) {
+                issue(ic, iy, v[(j + D) % NBUF]);
+                step(ic, iy);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            consume(cc, cy, v[j]);
+            step(cc, cy);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
 
-    // a5: transpose through LDS and store [CL][PH][PW] contiguously at RoI k.
-    const gptr<TO> out_blk = as_global_mut<TO>(a.out) +
-                        (static_cast<int64_t>(k) * a.lv.C + static_cast<int64_t>(slice) * CL) * NB;
-    const int nch = min(CL, a.lv.C - slice * CL);
-    float *tile = stile[wave];
+    // Every value the wave loaded reaches every one of its outputs through the
+    // dense products above, so a non-finite feature anywhere in the footprint shows
+    // up as a non-finite output.
+    uint32_t bad = 0;
 #pragma unroll
-    for (int c0 = 0; c0 < CL; c0 += CHK) {
-        if (cc >= c0 && cc < c0 + CHK) {
+    for (int p = 0; p < RPW; ++p)
 #pragma unroll
-            for (int i = 0; i < BPL; ++i) {
-                const int j = bg + NG * i;
-                if (j < NB) tile[(cc - c0) * NB + j] = acc[i];
+        for (int q = 0; q < PW; ++q) bad |= __builtin_isfinite(acc[p][q]) ? 0u : 1u;
+
+    // Then a zero weight times an infinity may have reached bins whose samples never
+    // touch that pixel, so this wave's bins are recomputed sample by sample, every
+    // product taken only where the definition takes it.
+    if (__builtin_amdgcn_ballot_w64(bad != 0) != 0) {
+#pragma unroll
+        for (int p = 0; p < RPW; ++p) {
+            if (p0 + p >= p1) continue;
+#pragma unroll 1
+            for (int q = 0; q < PW; ++q) {
+                float sum = 0.0f;
+                for (int iy2 = 0; iy2 < S; ++iy2) {
+                    const SampleTap ty = srow[(p0 + p) * S + iy2];
+                    if (ty.lo < 0) continue;
+                    const uint32_t r0 = vbase + static_cast<uint32_t>(ty.lo) * sh_b;
+                    const uint32_t r1 = vbase + static_cast<uint32_t>(ty.hi) * sh_b;
+                    for (int ix = 0; ix < S; ++ix) {
+                        const SampleTap tx = scol[q * S + ix];
+                        if (tx.lo < 0) continue;
+                        const uint32_t cl = static_cast<uint32_t>(tx.lo) * sw_b;
+                        const uint32_t chh = static_cast<uint32_t>(tx.hi) * sw_b;
+                        const float v00 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + cl));
+                        const float v01 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + chh));
+                        const float v10 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + cl));
+                        const float v11 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + chh));
+                        const float xl = fmaf(tx.w_hi, v01, tx.w_lo * v00);
+                        const float xh = fmaf(tx.w_hi, v11, tx.w_lo * v10);
+                        sum += fmaf(ty.w_hi, xh, ty.w_lo * xl);
+                    }
+                }
+                sum = sum / static_cast<float>(S * S);
+#pragma unroll
+                for (int qq = 0; qq < PW; ++qq) acc[p][qq] = (qq == q) ? sum : acc[p][qq];
             }
         }
-        wave_sync();
-        const int ne = max(0, min(CHK, nch - c0)) * NB;
-        if (kvalid && wave_on) {
-            for (int e = lane; e < ne; e += 64) store_f32(out_blk + c0 * NB + e, tile[e]);
+    }
+
+    // a5: the slice's [64][PH][PW] block is contiguous in the output at RoI k;
+    // transposed through LDS in rounds of CHK channels.
+    const int nchan = min(64, a.lv.C - slice * 64);
+    const gptr<TO> out_blk = as_global_mut<TO>(a.out) +
+                             (static_cast<int64_t>(k) * a.lv.C + static_cast<int64_t>(slice) * 64) * NB;
+#pragma unroll
+    for (int c0 = 0; c0 < 64; c0 += CHK) {
+        if (lane >= c0 && lane < c0 + CHK) {
+#pragma unroll
+            for (int p = 0; p < RPW; ++p) {
+                if (p0 + p >= p1) continue;
+#pragma unroll
+                for (int q = 0; q < PW; ++q) stile[(lane - c0) * NB + (p0 + p) * PW + q] = acc[p][q];
+            }
         }
-        wave_sync();
+        __syncthreads();
+        const int ne = max(0, min(CHK, nchan - c0)) * NB;
+        if (kvalid)
+            for (int e = t; e < ne; e += 256) store_f32(out_blk + c0 * NB + e, stile[e]);
+        if (c0 + CHK < 64) __syncthreads();
     }
 }
 
@@ -207,16 +453,15 @@ bool fwd_fast_available(int PH, int PW, int S) {
 template <typename T, typename TO>
 static hipError_t launch_fwd_typed(FwdArgs a, bool fast, hipStream_t stream) {
     if (fast) {
-        const int CL = (a.PH == 7) ? 64 : 16;
-        a.nslices = (a.lv.C + CL - 1) / CL;
-        a.wg_per_roi = (a.nslices + 3) / 4;
-        const int64_t grid = static_cast<int64_t>(a.K) * a.wg_per_roi;
+        a.nslices = (a.lv.C + 63) / 64;
+        a.wg_per_roi = a.nslices;
+        const int64_t grid = static_cast<int64_t>(a.K) * a.nslices;
         // a dispatch holds fewer than 2^32 work-items; beyond that, the strided kernel
         if (grid >= (int64_t(1) << 24)) return launch_fwd_typed<T, TO>(a, false, stream);
         if (a.PH == 7)
-            fwd_cl_kernel<T, TO, 7, 7, 2, 64><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
+            fwd_cl_kernel<T, TO, 7, 7, 2, kFwdCX, 64><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
         else
-            fwd_cl_kernel<T, TO, 14, 14, 2, 16><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
+            fwd_cl_kernel<T, TO, 14, 14, 2, 8, 16><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
     } else {
         const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * a.PH * a.PW;
         const int64_t blocks = std::min<int64_t>((total + 255) / 256, 16384);

@@ -280,3 +280,37 @@ def test_gpu_invariants():
     lhs = (y.double() * g.double()).sum().item()
     rhs = sum((a.double() * b.double()).sum().item() for a, b in zip(x, grads))
     assert abs(lhs - rhs) <= 1e-5 * (y.double().abs() * g.double().abs()).sum().item()
+
+
+@pytest.mark.parametrize("out_hw", [(7, 7), (14, 14)])
+def test_non_finite_features(out_hw):
+    """NaN and infinities in the footprint reach exactly the bins whose samples read
+    them (a zero bilinear weight times an infinity included), as in the definition."""
+    rng = np.random.default_rng(80)
+    shapes = _pyr(100)
+    rois = W.draw_rois(rng, 2, 12, (96, 160), (6.0, 120.0))
+    feats_np = _feats(rng, shapes, "f32")
+    lv = oracle.level_map(rois, len(shapes), 56.0)
+    planted = [np.nan, np.inf, -np.inf]
+    for i, k in enumerate(range(0, rois.shape[0], 3)):
+        l, b = lv[k], int(rois[k, 0])
+        _, _, H, Wd = shapes[l]
+        y = min(H - 1, max(0, int((rois[k, 2] + rois[k, 4]) * 0.5 * SC[l])))
+        x = min(Wd - 1, max(0, int((rois[k, 1] + rois[k, 3]) * 0.5 * SC[l])))
+        feats_np[l][b, (7 * i) % 100, y, x] = planted[i % 3]
+        feats_np[l][b, (7 * i + 50) % 100, y, min(Wd - 1, x + 1)] = planted[(i + 1) % 3]
+    log("non-finite features: %s, K=%d" % (out_hw, rois.shape[0]))
+    feats = [to_device(f, "f32", "cl") for f in feats_np]
+    r_dev = torch.from_numpy(rois).cuda()
+    lv_dev, ws = rex.plan(feats, SC, r_dev, 56.0)
+    out = rex.roi_align_fwd(feats, SC, r_dev, lv_dev, out_hw, 2, True, workspace=ws)
+    torch.cuda.synchronize()
+    got = from_device(out)
+    ref = oracle.roi_align_fwd([as_f64(f, "f32") for f in feats_np], SC, rois, lv, *out_hw, 2,
+                               True, "parity")
+    assert np.isnan(ref).any() and np.isinf(ref).any(), "the planted values reach the outputs"
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    assert np.array_equal(np.isposinf(got), np.isposinf(ref))
+    assert np.array_equal(np.isneginf(got), np.isneginf(ref))
+    fin = np.isfinite(ref)
+    check_fwd(np.where(fin, got, 0.0), np.where(fin, ref, 0.0), False, "non-finite features")
