@@ -272,6 +272,17 @@ __global__ __launch_bounds__(256) void bwd_cl_kernel(BwdArgs a) {
 //               row R0 + r (divided by the sample count), likewise Wx[pw][q],
 // and the contribution is  acc[r][q] += sum_ph Wy[ph][r] * sum_pw Wx[pw][q] * g[ph][pw].
 
+// Packs the nonzero bytes of a 64-bit ballot into 8 bits (bit h set iff byte h of
+// b has a set bit): OR-fold each byte onto its low bit, then gather the low bits
+// with one multiply (the partial products land on distinct bits, so nothing carries).
+__device__ __forceinline__ uint32_t byte_mask(uint64_t b) {
+    b |= b >> 4;
+    b |= b >> 2;
+    b |= b >> 1;
+    b &= 0x0101010101010101ull;
+    return static_cast<uint32_t>((b * 0x0102040810204080ull) >> 56);
+}
+
 template <typename TG, int PH, int PW, int S>
 __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     constexpr int NR = PH * S;
@@ -281,20 +292,23 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     constexpr int GB = 64 * NB;            // floats of one RoI's gradient block (64 channels)
     constexpr int YP = (PH * T + 63) / 64;  // ballot passes for the row weights
     constexpr int XP = (PW * T + 63) / 64;
-    // Double-buffer the staged gradient block (prefetching the next RoI's block into
+    // Double-buffer the staged gradient block (the next RoI's block travels in
     // registers while the current one is consumed) when two blocks fit in 32 KiB.
     constexpr bool kDouble = 2 * GB * 4 <= 32768;
     constexpr int NBUF = kDouble ? 2 : 1;
     constexpr int PF = kDouble ? (GB + 255) / 256 : 1;   // prefetch registers per thread
-    static_assert(NR + NCOL <= 256, "one tap per thread");
+    static_assert(NR + NCOL <= 64, "taps are computed by one wavefront");
     static_assert(PH <= 32 && PW <= 32, "bin masks are 32-bit");
 
     __shared__ float s_g[NBUF][GB];
-    __shared__ Tap s_tap[NR + NCOL];
+    __shared__ Tap s_tap[2][NR + NCOL];
     __shared__ __align__(16) float s_wy[4][PH * T];
     __shared__ __align__(16) float s_wx[4][PW * T];
-    __shared__ int s_k[64], s_ok[64];
+    __shared__ int s_k[64];
     __shared__ float s_ax[64][4];
+    // per kept RoI: tap extent ymin, ymax, xmin, xmax
+    __shared__ int s_rng[64][4];
+    __shared__ int s_n;
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
@@ -308,7 +322,8 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     const int cg = rem / a.wg_per_tile;
     int t = a.tile_order[rank];
     t = max(0, min(t, a.ntiles - 1));
-    const int quad = (rem - cg * a.wg_per_tile) * 4 + wave;
+    const int quad0 = (rem - cg * a.wg_per_tile) * 4;
+    const int quad = quad0 + wave;
 
     int l = 0;
 #pragma unroll
@@ -322,15 +337,21 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     const int rt = local - b * per_img;
     const int ty = rt / ntx;
     const int tx = rt - ty * ntx;
-    const int R0 = (ty << a.tile_shift) + (quad / a.qside) * T;
-    const int Q0 = (tx << a.tile_shift) + (quad % a.qside) * T;
+    const int qs = a.qside;
+    const int R0 = (ty << a.tile_shift) + (quad / qs) * T;
+    const int Q0 = (tx << a.tile_shift) + (quad % qs) * T;
     // Waves whose quadrant is off the map still take part in staging and barriers.
-    const bool wave_on = quad < a.qside * a.qside && R0 < L.H && Q0 < L.W;
+    const bool wave_on = quad < qs * qs && R0 < L.H && Q0 < L.W;
+    // The workgroup's region: the bounding box of its (up to 4) quadrants.
+    const int qlast = min(quad0 + 3, qs * qs - 1);
+    const int WR0 = (ty << a.tile_shift) + (quad0 / qs) * T;
+    const int WR1 = (ty << a.tile_shift) + (qlast / qs) * T + T;
+    const int WC0 = (tx << a.tile_shift) + ((qlast / qs > quad0 / qs) ? 0 : (quad0 % qs)) * T;
+    const int WC1 = (tx << a.tile_shift) + ((qlast / qs > quad0 / qs) ? qs : (qlast % qs) + 1) * T;
 
     const int c = cg * 64 + lane;
     const bool lane_on = c < a.lv.C;
     const int nch = min(64, a.lv.C - cg * 64);
-    const int nvalid = nch * NB;                 // valid floats of a staged block
     float acc[T][T];
 #pragma unroll
     for (int r = 0; r < T; ++r)
@@ -344,182 +365,240 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     constexpr float inv_count = 1.0f / static_cast<float>(S * S);
     float *wy = s_wy[wave];
     float *wx = s_wx[wave];
-    const gcptr<TG> gcg = as_global<TG>(a.gout) + static_cast<int64_t>(cg) * 64 * NB;
     const int64_t kstride = static_cast<int64_t>(a.lv.C) * NB;
 
-    // Coalesced copy of RoI k's gradient block into registers / LDS.
-    float pf[PF];
-    auto fetch = [&](int k) {
+    // Coalesced copy of kept RoI j's gradient block (nch x NB values) into
+    // registers / LDS through a buffer resource over exactly that block: element
+    // tid + 256 m sits at lane offset tid and a constant scalar offset, and the range
+    // check supplies the zeros past the valid channels.
+    const int nvalid = nch * NB;
+    auto block_rsrc = [&](int j) {
+        const char *src = static_cast<const char *>(a.gout) +
+                          (static_cast<int64_t>(cg) * 64 * NB + static_cast<int64_t>(s_k[j]) * kstride) *
+                              int64_t(sizeof(TG));
+        return make_rsrc(src, static_cast<uint32_t>(nvalid) * uint32_t(sizeof(TG)));
+    };
+    const uint32_t voff = static_cast<uint32_t>(tid) * uint32_t(sizeof(TG));
+    uint32_t pf[PF];
+    auto fetch = [&](int j) {
+        const __amdgpu_buffer_rsrc_t rs = block_rsrc(j);
 #pragma unroll
-        for (int m = 0; m < PF; ++m) {
-            const int e = tid + 256 * m;
-            pf[m] = e < nvalid ? load_f32(gcg + k * kstride + e) : 0.0f;
-        }
+        for (int m = 0; m < PF; ++m) pf[m] = buf_load_raw_s<TG>(rs, voff, 256 * m * sizeof(TG));
     };
     auto put = [&](int buf) {
 #pragma unroll
         for (int m = 0; m < PF; ++m) {
             const int e = tid + 256 * m;
-            if (e < GB) s_g[buf][e] = pf[m];
+            if (m < PF - 1 || e < GB) s_g[buf][e] = raw_to_f32<TG>(pf[m]);
         }
+    };
+    // Sample taps of kept RoI j into tap buffer tb (lanes of wave 0).
+    auto taps = [&](int j, int tb) {
+        if (tid < NR + NCOL) {
+            Axis ax;
+            ax.grid = S;
+            if (tid < NR) {
+                ax.start = s_ax[j][2];
+                ax.bin = s_ax[j][3];
+                s_tap[tb][tid] = axis_tap(ax, tid / S, tid % S, L.H);
+            } else {
+                ax.start = s_ax[j][0];
+                ax.bin = s_ax[j][1];
+                s_tap[tb][tid] = axis_tap(ax, (tid - NR) / S, (tid - NR) % S, L.W);
+            }
+        }
+    };
+    // Contribution of kept RoI j to this wave's quadrant.
+    auto consume = [&](int j, int buf, int tb) {
+        const int ymin = s_rng[j][0], ymax = s_rng[j][1];
+        const int xmin = s_rng[j][2], xmax = s_rng[j][3];
+        if (!wave_on || ymax < R0 || ymin >= R0 + T || xmax < Q0 || xmin >= Q0 + T) return;
+        // This quadrant's separable weights and which bin rows / columns reach it.
+        uint32_t ymask = 0, xmask = 0;
+#pragma unroll
+        for (int p = 0; p < YP; ++p) {
+            const int u = p * 64 + lane;
+            bool hit = false;
+            if (u < PH * T) {
+                const int ph = u / T;
+                const int R = R0 + (u % T);
+                float w = 0.0f;
+#pragma unroll
+                for (int iy = 0; iy < S; ++iy) {
+                    const Tap tp = s_tap[tb][ph * S + iy];
+                    if (tp.lo >= 0) {
+                        if (tp.lo == R) {
+                            w += tp.wlo;
+                            hit = true;
+                        }
+                        if (tp.hi == R) {
+                            w += tp.whi;
+                            hit = true;
+                        }
+                    }
+                }
+                wy[u] = w * inv_count;
+            }
+            ymask |= byte_mask(__ballot(hit)) << (p * 8);
+        }
+#pragma unroll
+        for (int p = 0; p < XP; ++p) {
+            const int u = p * 64 + lane;
+            bool hit = false;
+            if (u < PW * T) {
+                const int pw = u / T;
+                const int Q = Q0 + (u % T);
+                float w = 0.0f;
+#pragma unroll
+                for (int ix = 0; ix < S; ++ix) {
+                    const Tap tp = s_tap[tb][NR + pw * S + ix];
+                    if (tp.lo >= 0) {
+                        if (tp.lo == Q) {
+                            w += tp.wlo;
+                            hit = true;
+                        }
+                        if (tp.hi == Q) {
+                            w += tp.whi;
+                            hit = true;
+                        }
+                    }
+                }
+                wx[u] = w;
+            }
+            xmask |= byte_mask(__ballot(hit)) << (p * 8);
+        }
+        wave_sync();
+
+        const float *gl = s_g[buf] + lane * NB;   // this lane's channel, stride NB (odd)
+        for (uint32_t ym = ymask; ym; ym &= ym - 1) {
+            const int ph = __builtin_ctz(ym);
+            float X[T];
+#pragma unroll
+            for (int q = 0; q < T; ++q) X[q] = 0.0f;
+            for (uint32_t xm = xmask; xm; xm &= xm - 1) {
+                const int pw = __builtin_ctz(xm);
+                const float gv = gl[ph * PW + pw];
+                const float4 w0 = *reinterpret_cast<const float4 *>(wx + pw * T);
+                const float4 w1 = *reinterpret_cast<const float4 *>(wx + pw * T + 4);
+                X[0] = fmaf(w0.x, gv, X[0]);
+                X[1] = fmaf(w0.y, gv, X[1]);
+                X[2] = fmaf(w0.z, gv, X[2]);
+                X[3] = fmaf(w0.w, gv, X[3]);
+                X[4] = fmaf(w1.x, gv, X[4]);
+                X[5] = fmaf(w1.y, gv, X[5]);
+                X[6] = fmaf(w1.z, gv, X[6]);
+                X[7] = fmaf(w1.w, gv, X[7]);
+            }
+            const float4 y0 = *reinterpret_cast<const float4 *>(wy + ph * T);
+            const float4 y1 = *reinterpret_cast<const float4 *>(wy + ph * T + 4);
+            const float yr[T] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
+#pragma unroll
+            for (int rr = 0; rr < T; ++rr)
+#pragma unroll
+                for (int q = 0; q < T; ++q) acc[rr][q] = fmaf(yr[rr], X[q], acc[rr][q]);
+        }
+        // the weights are rewritten for the next RoI only after the next barrier
     };
 
     for (int base = s0; base < s1; base += 64) {
         const int n = min(64, s1 - base);
         __syncthreads();   // previous batch fully consumed
-        if (tid < n) {
-            int k = a.tile_rois[base + tid];
-            int ok = 0;
+        // RoI records of this batch (wave 0): validity, axis parameters and tap extent.
+        // RoIs whose tap extent misses the workgroup's region reach none of its pixels
+        // and are dropped; the rest are compacted.
+        if (wave == 0) {
+            bool keep = false;
+            int k = 0, ymin = INT32_MAX, ymax = -1, xmin = INT32_MAX, xmax = -1;
             float ax_s = 0.0f, ax_b = 0.0f, ay_s = 0.0f, ay_b = 0.0f;
-            if (k >= 0 && k < a.K) {
-                const float *r = a.rois + 5 * static_cast<int64_t>(k);
-                const float r0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
-                const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
-                if (lvl == l && roi_batch(r0, a.lv.N) == b) {
-                    const Axis ax = axis_setup(x1, x2, L.scale, a.aligned, PW, S);
-                    const Axis ay = axis_setup(y1, y2, L.scale, a.aligned, PH, S);
-                    ax_s = ax.start;
-                    ax_b = ax.bin;
-                    ay_s = ay.start;
-                    ay_b = ay.bin;
-                    ok = 1;
+            if (lane < n) {
+                k = a.tile_rois[base + lane];
+                if (k >= 0 && k < a.K) {
+                    const float *r = a.rois + 5 * static_cast<int64_t>(k);
+                    const float r0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
+                    const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
+                    if (lvl == l && roi_batch(r0, a.lv.N) == b) {
+                        const Axis ax = axis_setup(x1, x2, L.scale, a.aligned, PW, S);
+                        const Axis ay = axis_setup(y1, y2, L.scale, a.aligned, PH, S);
+                        ax_s = ax.start;
+                        ax_b = ax.bin;
+                        ay_s = ay.start;
+                        ay_b = ay.bin;
+                        // Tap extent from the first and last sample of each axis (taps
+                        // are monotone in the sample index); an end sample outside the
+                        // map widens the extent to the map edge, so it is a superset.
+                        const Tap fy = axis_tap(ay, 0, 0, L.H);
+                        const Tap ly = axis_tap(ay, PH - 1, S - 1, L.H);
+                        const Tap fx = axis_tap(ax, 0, 0, L.W);
+                        const Tap lx = axis_tap(ax, PW - 1, S - 1, L.W);
+                        ymin = fy.lo >= 0 ? fy.lo : 0;
+                        ymax = ly.lo >= 0 ? ly.hi : L.H - 1;
+                        xmin = fx.lo >= 0 ? fx.lo : 0;
+                        xmax = lx.lo >= 0 ? lx.hi : L.W - 1;
+                        const bool yhit = ymax >= WR0 && ymin < WR1;
+                        const bool xhit = xmax >= WC0 && xmin < WC1;
+                        keep = yhit && xhit;
+                    }
                 }
-            } else {
-                k = 0;
             }
-            s_k[tid] = k;
-            s_ok[tid] = ok;
-            s_ax[tid][0] = ax_s;
-            s_ax[tid][1] = ax_b;
-            s_ax[tid][2] = ay_s;
-            s_ax[tid][3] = ay_b;
+            const uint64_t km = __ballot(keep);
+            if (keep) {
+                const int pos = static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                    static_cast<uint32_t>(km >> 32),
+                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(km), 0u)));
+                s_k[pos] = k;
+                s_ax[pos][0] = ax_s;
+                s_ax[pos][1] = ax_b;
+                s_ax[pos][2] = ay_s;
+                s_ax[pos][3] = ay_b;
+                s_rng[pos][0] = ymin;
+                s_rng[pos][1] = ymax;
+                s_rng[pos][2] = xmin;
+                s_rng[pos][3] = xmax;
+            }
+            if (lane == 0) s_n = __builtin_popcountll(km);
         }
         __syncthreads();
+        const int nk = s_n;
+        if (nk == 0) continue;
         if constexpr (kDouble) {
-            fetch(s_k[0]);
+            fetch(0);
             put(0);
-        }
-        for (int j = 0; j < n; ++j) {
-            const int buf = kDouble ? (j & 1) : 0;
-            if constexpr (kDouble) {
-                if (j + 1 < n) fetch(s_k[j + 1]);   // lands while RoI j is processed
-            } else {
-                for (int e = tid; e < GB; e += 256)
-                    s_g[0][e] = e < nvalid ? load_f32(gcg + s_k[j] * kstride + e) : 0.0f;
-            }
-            const bool ok = s_ok[j] != 0;
-            // Sample taps of RoI j, once for the workgroup.
-            if (ok && tid < NR + NCOL) {
-                Axis ax;
-                if (tid < NR) {
-                    ax.start = s_ax[j][2];
-                    ax.bin = s_ax[j][3];
-                } else {
-                    ax.start = s_ax[j][0];
-                    ax.bin = s_ax[j][1];
+            taps(0, 0);
+            __syncthreads();
+            for (int j = 0; j < nk; ++j) {
+                const int buf = j & 1;
+                if (j + 1 < nk) {
+                    fetch(j + 1);           // lands while RoI j is processed
+                    taps(j + 1, buf ^ 1);   // the other tap buffer is idle
                 }
-                ax.grid = S;
-                s_tap[tid] = tid < NR ? axis_tap(ax, tid / S, tid % S, L.H)
-                                      : axis_tap(ax, (tid - NR) / S, (tid - NR) % S, L.W);
+                consume(j, buf, buf);
+                if (j + 1 < nk) put(buf ^ 1);
+                __syncthreads();   // staged block, taps and weights are reused next
             }
-            __syncthreads();   // taps (and the staged block) visible
-
-            if (ok && wave_on) {
-                // This quadrant's separable weights and which bin rows / columns reach it.
-                uint32_t ymask = 0, xmask = 0;
+        } else {
+            for (int j = 0; j < nk; ++j) {
+                if (j > 0) __syncthreads();   // the previous block is fully consumed
+                {
+                    const __amdgpu_buffer_rsrc_t rs = block_rsrc(j);
+                    constexpr int NE = (GB + 255) / 256;
+                    constexpr int U = 7;   // loads in flight per thread
 #pragma unroll
-                for (int p = 0; p < YP; ++p) {
-                    const int u = p * 64 + lane;
-                    bool hit = false;
-                    if (u < PH * T) {
-                        const int ph = u / T;
-                        const int R = R0 + (u % T);
-                        float w = 0.0f;
+                    for (int m0 = 0; m0 < NE; m0 += U) {
+                        uint32_t v[U];
 #pragma unroll
-                        for (int iy = 0; iy < S; ++iy) {
-                            const Tap tp = s_tap[ph * S + iy];
-                            if (tp.lo >= 0) {
-                                if (tp.lo == R) {
-                                    w += tp.wlo;
-                                    hit = true;
-                                }
-                                if (tp.hi == R) {
-                                    w += tp.whi;
-                                    hit = true;
-                                }
-                            }
+                        for (int u = 0; u < U; ++u)
+                            if (m0 + u < NE) v[u] = buf_load_raw_s<TG>(rs, voff, 256 * (m0 + u) * sizeof(TG));
+#pragma unroll
+                        for (int u = 0; u < U; ++u) {
+                            const int e = tid + 256 * (m0 + u);
+                            if (m0 + u < NE && e < GB) s_g[0][e] = raw_to_f32<TG>(v[u]);
                         }
-                        wy[u] = w * inv_count;
                     }
-                    const uint64_t bits = __ballot(hit);
-#pragma unroll
-                    for (int h = 0; h < 8; ++h)
-                        if ((bits >> (8 * h)) & 0xffu) ymask |= 1u << (p * 8 + h);
                 }
-#pragma unroll
-                for (int p = 0; p < XP; ++p) {
-                    const int u = p * 64 + lane;
-                    bool hit = false;
-                    if (u < PW * T) {
-                        const int pw = u / T;
-                        const int Q = Q0 + (u % T);
-                        float w = 0.0f;
-#pragma unroll
-                        for (int ix = 0; ix < S; ++ix) {
-                            const Tap tp = s_tap[NR + pw * S + ix];
-                            if (tp.lo >= 0) {
-                                if (tp.lo == Q) {
-                                    w += tp.wlo;
-                                    hit = true;
-                                }
-                                if (tp.hi == Q) {
-                                    w += tp.whi;
-                                    hit = true;
-                                }
-                            }
-                        }
-                        wx[u] = w;
-                    }
-                    const uint64_t bits = __ballot(hit);
-#pragma unroll
-                    for (int h = 0; h < 8; ++h)
-                        if ((bits >> (8 * h)) & 0xffu) xmask |= 1u << (p * 8 + h);
-                }
-                wave_sync();
-
-                const float *gl = s_g[buf] + lane * NB;   // this lane's channel, stride NB (odd)
-                for (uint32_t ym = ymask; ym; ym &= ym - 1) {
-                    const int ph = __builtin_ctz(ym);
-                    float X[T];
-#pragma unroll
-                    for (int q = 0; q < T; ++q) X[q] = 0.0f;
-                    for (uint32_t xm = xmask; xm; xm &= xm - 1) {
-                        const int pw = __builtin_ctz(xm);
-                        const float gv = gl[ph * PW + pw];
-                        const float4 w0 = *reinterpret_cast<const float4 *>(wx + pw * T);
-                        const float4 w1 = *reinterpret_cast<const float4 *>(wx + pw * T + 4);
-                        X[0] = fmaf(w0.x, gv, X[0]);
-                        X[1] = fmaf(w0.y, gv, X[1]);
-                        X[2] = fmaf(w0.z, gv, X[2]);
-                        X[3] = fmaf(w0.w, gv, X[3]);
-                        X[4] = fmaf(w1.x, gv, X[4]);
-                        X[5] = fmaf(w1.y, gv, X[5]);
-                        X[6] = fmaf(w1.z, gv, X[6]);
-                        X[7] = fmaf(w1.w, gv, X[7]);
-                    }
-                    const float4 y0 = *reinterpret_cast<const float4 *>(wy + ph * T);
-                    const float4 y1 = *reinterpret_cast<const float4 *>(wy + ph * T + 4);
-                    const float yr[T] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
-#pragma unroll
-                    for (int rr = 0; rr < T; ++rr)
-#pragma unroll
-                        for (int q = 0; q < T; ++q) acc[rr][q] = fmaf(yr[rr], X[q], acc[rr][q]);
-                }
+                taps(j, j & 1);
+                __syncthreads();
+                consume(j, 0, j & 1);
             }
-            if constexpr (kDouble) {
-                if (j + 1 < n) put(buf ^ 1);
-            }
-            __syncthreads();   // taps, weights and the consumed block are reused next
         }
     }
 

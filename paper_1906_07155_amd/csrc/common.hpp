@@ -137,6 +137,17 @@ template <> __device__ __forceinline__ uint32_t buf_load_raw<uint16_t>(__amdgpu_
                                                                        uint32_t off) {
     return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
+// Same, with a scalar byte offset added to every lane's offset.
+template <typename T> __device__ __forceinline__ uint32_t buf_load_raw_s(__amdgpu_buffer_rsrc_t r,
+                                                                         uint32_t off, uint32_t soff);
+template <> __device__ __forceinline__ uint32_t buf_load_raw_s<float>(__amdgpu_buffer_rsrc_t r,
+                                                                      uint32_t off, uint32_t soff) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, soff, 0);
+}
+template <> __device__ __forceinline__ uint32_t buf_load_raw_s<uint16_t>(__amdgpu_buffer_rsrc_t r,
+                                                                         uint32_t off, uint32_t soff) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, off, soff, 0);
+}
 template <typename T> __device__ __forceinline__ float raw_to_f32(uint32_t v);
 template <> __device__ __forceinline__ float raw_to_f32<float>(uint32_t v) {
     return __uint_as_float(v);
