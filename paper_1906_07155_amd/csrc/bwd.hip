@@ -311,7 +311,7 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     __shared__ int s_n;
 
     const int tid = threadIdx.x;
-    const int wave = tid >> 6;
+    const int wave = uniform_i(tid >> 6);
     const int lane = tid & 63;
     // Blocks in dispatch order walk the tiles longest list first (plan order); the
     // channel groups and quadrant blocks of one tile are adjacent.
@@ -373,8 +373,9 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     // check supplies the zeros past the valid channels.
     const int nvalid = nch * NB;
     auto block_rsrc = [&](int j) {
+        const int k = uniform_i(s_k[j]);   // one resource for the wave, no waterfall
         const char *src = static_cast<const char *>(a.gout) +
-                          (static_cast<int64_t>(cg) * 64 * NB + static_cast<int64_t>(s_k[j]) * kstride) *
+                          (static_cast<int64_t>(cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
                               int64_t(sizeof(TG));
         return make_rsrc(src, static_cast<uint32_t>(nvalid) * uint32_t(sizeof(TG)));
     };
@@ -602,20 +603,26 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
         }
     }
 
-    if (!wave_on || !lane_on) return;
-    const gptr<float> gb = as_global_mut<float>(const_cast<void *>(L.data)) + b * L.sn + c;
+    // Every pixel of the quadrant is written once (the clearing is fused).  The
+    // pixel offset is the same for the whole wave (scalar), the channel offset is the
+    // lane's; lanes past the last channel write out of range, which is dropped.
+    if (!wave_on) return;
+    const char *img = static_cast<const char *>(L.data) + static_cast<int64_t>(b) * L.sn * 4;
+    const __amdgpu_buffer_rsrc_t dst = make_rsrc(img, L.img_bytes);
+    const uint32_t vo = lane_on ? static_cast<uint32_t>(c) * 4u : kBufOOB;
+    const uint32_t sh4 = static_cast<uint32_t>(L.sh) * 4u;
+    const uint32_t sw4 = static_cast<uint32_t>(L.sw) * 4u;
 #pragma unroll
     for (int rr = 0; rr < T; ++rr) {
-        const int R = R0 + rr;
-        if (R >= L.H) break;
+        if (R0 + rr >= L.H) break;
+        const uint32_t rowo = static_cast<uint32_t>(R0 + rr) * sh4 + static_cast<uint32_t>(Q0) * sw4;
 #pragma unroll
         for (int q = 0; q < T; ++q) {
-            const int Q = Q0 + q;
-            if (Q >= L.W) break;
-            const gptr<float> p = gb + R * L.sh + Q * L.sw;
+            if (Q0 + q >= L.W) break;
+            const uint32_t so = rowo + static_cast<uint32_t>(q) * sw4;
             float v = acc[rr][q];
-            if (!a.zero_init) v += *p;
-            *p = v;
+            if (!a.zero_init) v += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dst, vo, so, 0));
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), dst, vo, so, 0);
         }
     }
 }
