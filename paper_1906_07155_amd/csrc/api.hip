@@ -16,7 +16,8 @@ using namespace rex;
 namespace {
 
 // Workspace layout: [0, 256) per-level offsets, then perm[K], keys[K],
-// tile_start[ntiles + 1], tile_order[ntiles] and tile_rois[capacity], each region
+// tile_start[ntiles + 1], tile_order[ntiles], tile_rois[capacity], and the plan's
+// scratch: bucket counters[kPlanMaxBins] and tile cursors[ntiles], each region
 // aligned to 256 bytes.
 constexpr size_t kHeader = 256;
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -29,8 +30,14 @@ size_t tile_order_offset(int64_t K, const TileLayout &t) {
 size_t tile_rois_offset(int64_t K, const TileLayout &t) {
     return tile_order_offset(K, t) + align256(static_cast<size_t>(t.ntiles) * 4);
 }
-size_t workspace_bytes_for(int64_t K, const TileLayout &t) {
+size_t key_count_offset(int64_t K, const TileLayout &t) {
     return tile_rois_offset(K, t) + align256(static_cast<size_t>(t.capacity) * 4);
+}
+size_t tile_cursor_offset(int64_t K, const TileLayout &t) {
+    return key_count_offset(K, t) + align256(static_cast<size_t>(kPlanMaxBins) * 4);
+}
+size_t workspace_bytes_for(int64_t K, const TileLayout &t) {
+    return tile_cursor_offset(K, t) + align256(static_cast<size_t>(t.ntiles) * 4);
 }
 
 // Bin-tiles of 2^shift pixels per (level, image): the smallest shift >= 4 whose tile
@@ -286,6 +293,8 @@ re_status_t roi_extract_plan(const re_level_t *levels, int32_t num_levels, const
     a.tile_start = reinterpret_cast<int32_t *>(ws + tiles_offset(num_rois));
     a.tile_rois = reinterpret_cast<int32_t *>(ws + tile_rois_offset(num_rois, tl));
     a.tile_order = reinterpret_cast<int32_t *>(ws + tile_order_offset(num_rois, tl));
+    a.key_count = reinterpret_cast<int32_t *>(ws + key_count_offset(num_rois, tl));
+    a.tile_cursor = reinterpret_cast<int32_t *>(ws + tile_cursor_offset(num_rois, tl));
     a.ntiles = tl.ntiles;
     a.capacity = static_cast<int32_t>(tl.capacity);
     a.tile_shift = tl.shift;

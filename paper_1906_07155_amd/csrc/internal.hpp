@@ -32,6 +32,9 @@ struct PlanArgs {
     int32_t *tile_start;
     int32_t *tile_rois;
     int32_t *tile_order;   // [ntiles]: tiles by decreasing list length
+    int32_t *key_count;    // [nbins] scratch: bucket counts, then cursors (the tile
+                           // counts live in tile_start until they are scanned)
+    int32_t *tile_cursor;  // [ntiles] scratch: next free slot of each tile's list
     int32_t ntiles;
     int32_t capacity;
     int32_t tile_shift;

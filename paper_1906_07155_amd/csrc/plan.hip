@@ -5,14 +5,13 @@
 // threshold form, see include/roi_extract.h.
 //
 // The plan is a counting sort of the RoIs by (level, image, spatial cell of the box
-// centre), done by one 1024-thread workgroup with an LDS histogram: RoIs that read
-// the same feature rows end up next to each other in launch order, and the
-// XCD-aware block mapping of the forward/backward then keeps them on one XCD's L2.
-// The order of RoIs with equal keys is whatever the LDS atomics give; only the
-// keys' order and the per-level offsets are defined.
+// centre): RoIs that read the same feature rows end up next to each other in launch
+// order, and the XCD-aware block mapping of the forward/backward then keeps them on
+// one XCD's L2.  The order of RoIs with equal keys is whatever the atomics give;
+// only the keys' order and the per-level offsets are defined.
 //
-// The same kernel also bins the RoIs into square bin-tiles of every (level, image)
-// for the gather backward: a CSR list of the RoIs whose footprint can reach each
+// The plan also bins the RoIs into square bin-tiles of every (level, image) for
+// the gather backward: a CSR list of the RoIs whose footprint can reach each
 // tile (a superset: a listed RoI may contribute nothing to the tile).
 #include "internal.hpp"
 
@@ -27,30 +26,46 @@ __global__ __launch_bounds__(256) void level_map_kernel(const float *__restrict_
     }
 }
 
-// Exclusive scan of hist[0, n) in place by the whole workgroup (per-thread chunk
-// sums, a block scan of the sums, then the chunk prefixes).  Returns the total.
+// Inclusive prefix sum across the 64 lanes of a wavefront.
+__device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int t = __shfl_up(v, off);
+        if (lane >= off) v += t;
+    }
+    return v;
+}
+
+// Exclusive scan of hist[0, n) in place by the whole workgroup: per-thread chunk
+// sums, a wavefront scan of the sums, a scan of the wavefront totals by wave 0,
+// then the chunk prefixes.  part[] holds the wavefront totals.  Returns the total.
 __device__ int block_exclusive_scan(int32_t *hist, int n, int32_t *part) {
+    constexpr int kWaves = kPlanThreads / 64;
     const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
     const int per = (n + kPlanThreads - 1) / kPlanThreads;
     const int lo = min(tid * per, n);
     const int hi = min(lo + per, n);
     int s = 0;
     for (int i = lo; i < hi; ++i) s += hist[i];
-    part[tid] = s;
+    const int incl = wave_inclusive_scan(s, lane);
+    if (lane == 63) part[wave] = incl;
     __syncthreads();
-    for (int off = 1; off < kPlanThreads; off <<= 1) {
-        const int v = tid >= off ? part[tid - off] : 0;
-        __syncthreads();
-        part[tid] += v;
-        __syncthreads();
+    if (wave == 0) {
+        const int w = lane < kWaves ? part[lane] : 0;
+        const int wi = wave_inclusive_scan(w, lane);
+        if (lane < kWaves) part[kWaves + lane] = wi - w;   // exclusive wave prefix
+        if (lane == kWaves - 1) part[2 * kWaves] = wi;     // total
     }
-    int run = tid == 0 ? 0 : part[tid - 1];
+    __syncthreads();
+    int run = part[kWaves + wave] + incl - s;
     for (int i = lo; i < hi; ++i) {
         const int c = hist[i];
         hist[i] = run;
         run += c;
     }
-    const int total = part[kPlanThreads - 1];
+    const int total = part[2 * kWaves];
     __syncthreads();
     return total;
 }
@@ -79,72 +94,64 @@ __device__ void roi_tile_box(const PlanArgs &a, int lvl, float x1, float y1, flo
     ty1 = min(ty1, a.nty[lvl] - 1);
 }
 
-// RoIs per thread kept in registers between the phases (K <= kPlanThreads * kCached);
-// larger K re-reads them from memory.
-constexpr int kCached = 8;
+// Sort key of a RoI: level bucket + image + spatial cell of the box centre.
+__device__ __forceinline__ int plan_key(const PlanArgs &a, float x1, float y1, float x2, float y2,
+                                        int lvl, int bb) {
+    const int b = (bb < 0 || !a.batch_in_key) ? 0 : bb;
+    float cx = (x1 + x2) * 0.5f * a.scale[lvl];
+    float cy = (y1 + y2) * 0.5f * a.scale[lvl];
+    cx = fminf(fmaxf(cx, 0.0f), static_cast<float>(a.W[lvl] - 1));   // NaN -> 0
+    cy = fminf(fmaxf(cy, 0.0f), static_cast<float>(a.H[lvl] - 1));
+    const int gx = min(static_cast<int>(cx) >> a.cell_shift, a.ncx[lvl] - 1);
+    const int gy = min(static_cast<int>(cy) >> a.cell_shift, a.ncy[lvl] - 1);
+    return a.base[lvl] + (b * a.ncy[lvl] + gy) * a.ncx[lvl] + gx;
+}
 
-template <bool CACHED>
-__global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
+// The tile phases give each RoI kPlanLanes consecutive lanes, which split its tiles,
+// so the atomics of one RoI are in flight together.
+constexpr int kPlanLanes = 16;
+constexpr int kPlanSmall = kPlanThreads * 2;
+
+// Small plans (K <= kPlanSmall) run in one 1024-thread workgroup with LDS
+// histograms, which avoids the launch latency of the four-kernel plan; each thread
+// keeps the keys of up to kCached RoIs in registers between the phases.
+constexpr int kCached = 2;
+
+__global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
     extern __shared__ int32_t smem[];
     int32_t *hist = smem;                           // [max(nbins, ntiles)]
-    int32_t *part = smem + max(a.nbins, a.ntiles);  // [kPlanThreads]
+    int32_t *part = hist + max(a.nbins, a.ntiles);  // [kPlanThreads]
+    int32_t *box = part + kPlanThreads;             // [3 * kPlanSmall]: tile box per RoI
     const int tid = threadIdx.x;
-    constexpr int R = CACHED ? kCached : 1;
-    float cx1[R], cy1[R], cx2[R], cy2[R];
-    int cb[R], clv[R], ckey[R];
-
-    // Loads RoI k: from the cache when CACHED (slot i), else from memory.
-    auto roi = [&](int i, int k, float &x1, float &y1, float &x2, float &y2, int &b, int &lvl) {
-        if constexpr (CACHED) {
-            x1 = cx1[i];
-            y1 = cy1[i];
-            x2 = cx2[i];
-            y2 = cy2[i];
-            b = cb[i];
-            lvl = clv[i];
-        } else {
-            const float *r = a.rois + 5 * static_cast<int64_t>(k);
-            x1 = r[1];
-            y1 = r[2];
-            x2 = r[3];
-            y2 = r[4];
-            b = roi_batch(r[0], a.N);
-            lvl = a.levels_out[k];
-        }
-    };
+    int ckey[kCached];
 
     for (int i = tid; i < a.nbins; i += kPlanThreads) hist[i] = 0;
     __syncthreads();
 
-    // a1: level of every RoI; key = level bucket + image + spatial cell.
+    // a1: level of every RoI; key = level bucket + image + spatial cell; the tile box
+    // of its footprint (first tile, packed x and y ranges; first tile -1: no tiles).
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-        for (int32_t k = tid + i * kPlanThreads; k < a.K; k += R * kPlanThreads) {
+    for (int i = 0; i < kCached; ++i) {
+        const int32_t k = tid + i * kPlanThreads;
+        if (k < a.K) {
             const float *r = a.rois + 5 * static_cast<int64_t>(k);
             const float b0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
             const int lvl = fpn_level(x1, y1, x2, y2, a.L, a.finest_scale);
             a.levels_out[k] = lvl;
             const int bb = roi_batch(b0, a.N);
-            const int b = (bb < 0 || !a.batch_in_key) ? 0 : bb;
-            float cx = (x1 + x2) * 0.5f * a.scale[lvl];
-            float cy = (y1 + y2) * 0.5f * a.scale[lvl];
-            cx = fminf(fmaxf(cx, 0.0f), static_cast<float>(a.W[lvl] - 1));   // NaN -> 0
-            cy = fminf(fmaxf(cy, 0.0f), static_cast<float>(a.H[lvl] - 1));
-            const int gx = min(static_cast<int>(cx) >> a.cell_shift, a.ncx[lvl] - 1);
-            const int gy = min(static_cast<int>(cy) >> a.cell_shift, a.ncy[lvl] - 1);
-            const int key = a.base[lvl] + (b * a.ncy[lvl] + gy) * a.ncx[lvl] + gx;
-            if constexpr (CACHED) {
-                cx1[i] = x1;
-                cy1[i] = y1;
-                cx2[i] = x2;
-                cy2[i] = y2;
-                cb[i] = bb;
-                clv[i] = lvl;
-                ckey[i] = key;
-            } else {
-                a.keys[k] = key;
+            ckey[i] = plan_key(a, x1, y1, x2, y2, lvl, bb);
+            atomicAdd(&hist[ckey[i]], 1);
+            int first = -1, xr = 0, yr = 0;
+            if (a.ntiles > 0 && bb >= 0) {
+                int tx0, tx1, ty0, ty1;
+                roi_tile_box(a, lvl, x1, y1, x2, y2, tx0, tx1, ty0, ty1);
+                first = a.tbase[lvl] + (bb * a.nty[lvl] + ty0) * a.ntx[lvl] + tx0;
+                xr = (tx1 - tx0 + 1) | (a.ntx[lvl] << 16);
+                yr = ty1 - ty0 + 1;
             }
-            atomicAdd(&hist[key], 1);
+            box[3 * k] = first;
+            box[3 * k + 1] = xr;
+            box[3 * k + 2] = yr;
         }
     }
     __syncthreads();
@@ -158,85 +165,171 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
 
     // a2: scatter RoI indices to their slots.
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-        for (int32_t k = tid + i * kPlanThreads; k < a.K; k += R * kPlanThreads) {
-            int key;
-            if constexpr (CACHED)
-                key = ckey[i];
-            else
-                key = a.keys[k];
-            const int pos = atomicAdd(&hist[key], 1);
-            a.perm[pos] = k;
-        }
+    for (int i = 0; i < kCached; ++i) {
+        const int32_t k = tid + i * kPlanThreads;
+        if (k < a.K) a.perm[atomicAdd(&hist[ckey[i]], 1)] = k;
     }
     if (a.ntiles <= 0) return;   // uniform
     __syncthreads();
 
-    // Tile binning: count the (tile, RoI) pairs, scan, then fill the CSR lists.
+    // Tile binning: count the (tile, RoI) pairs, scan, then fill the CSR lists.  Each
+    // RoI gets kSmallLanes consecutive lanes, which split its tiles.
+    constexpr int kSmallLanes = 4;
+    constexpr int kPer = kPlanThreads / kSmallLanes;   // RoIs per pass
+    const int sub = tid % kSmallLanes;
+    auto for_tiles = [&](auto &&fn) {
+        for (int32_t k = tid / kSmallLanes; k < a.K; k += kPer) {
+            const int first = box[3 * k];
+            if (first < 0) continue;
+            const int w = box[3 * k + 1] & 0xffff;
+            const int ntx = box[3 * k + 1] >> 16;
+            const int n = w * box[3 * k + 2];
+            for (int i = sub; i < n; i += kSmallLanes) {
+                const int dy = i / w;
+                fn(first + dy * ntx + (i - dy * w), k);
+            }
+        }
+    };
     for (int i = tid; i < a.ntiles; i += kPlanThreads) hist[i] = 0;
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < R; ++i) {
-        for (int32_t k = tid + i * kPlanThreads; k < a.K; k += R * kPlanThreads) {
-            float x1, y1, x2, y2;
-            int b, lvl;
-            roi(i, k, x1, y1, x2, y2, b, lvl);
-            if (b < 0) continue;
-            int tx0, tx1, ty0, ty1;
-            roi_tile_box(a, lvl, x1, y1, x2, y2, tx0, tx1, ty0, ty1);
-            const int base = a.tbase[lvl] + b * a.nty[lvl] * a.ntx[lvl];
-            for (int ty = ty0; ty <= ty1; ++ty)
-                for (int tx = tx0; tx <= tx1; ++tx) atomicAdd(&hist[base + ty * a.ntx[lvl] + tx], 1);
-        }
+    for_tiles([&](int t, int) { atomicAdd(&hist[t], 1); });
+    __syncthreads();
+    // Launch order of the tiles: longest lists first (counting sort on the list
+    // length, capped at 255), so the longest sequential chains start earliest.
+    constexpr int kLenBins = 256;
+    int32_t *lenh = part + 2 * (kPlanThreads / 64) + 1;   // [kLenBins], after the scan scratch
+    for (int i = tid; i < kLenBins; i += kPlanThreads) lenh[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < a.ntiles; i += kPlanThreads)
+        atomicAdd(&lenh[kLenBins - 1 - min(hist[i], kLenBins - 1)], 1);
+    __syncthreads();
+    block_exclusive_scan(lenh, kLenBins, part);
+    for (int i = tid; i < a.ntiles; i += kPlanThreads) {
+        const int pos = atomicAdd(&lenh[kLenBins - 1 - min(hist[i], kLenBins - 1)], 1);
+        a.tile_order[pos] = i;
     }
     __syncthreads();
     const int total = block_exclusive_scan(hist, a.ntiles, part);
     for (int i = tid; i < a.ntiles; i += kPlanThreads) a.tile_start[i] = hist[i];
     if (tid == 0) a.tile_start[a.ntiles] = total;
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < R; ++i) {
-        for (int32_t k = tid + i * kPlanThreads; k < a.K; k += R * kPlanThreads) {
-            float x1, y1, x2, y2;
-            int b, lvl;
-            roi(i, k, x1, y1, x2, y2, b, lvl);
-            if (b < 0) continue;
+    for_tiles([&](int t, int k) {
+        const int pos = atomicAdd(&hist[t], 1);
+        if (pos < a.capacity) a.tile_rois[pos] = k;
+    });
+}
+
+// Larger plans run as four short kernels over the whole GPU: clear the counters;
+// per RoI, its level, sort key and the tiles its footprint box meets, counted with
+// device-scope integer atomics; one workgroup turns the counts into bucket starts,
+// per-level offsets, tile list starts and the longest-first tile order; per RoI,
+// its slot in the permutation and in each of its tiles' lists.
+
+__global__ __launch_bounds__(256) void plan_clear_kernel(int32_t *__restrict__ a, int32_t na,
+                                                         int32_t *__restrict__ b, int32_t nb) {
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < na + nb;
+         i += gridDim.x * blockDim.x) {
+        if (i < na) a[i] = 0;
+        else b[i - na] = 0;
+    }
+}
+
+__global__ __launch_bounds__(256) void plan_count_kernel(PlanArgs a) {
+    const int sub = threadIdx.x % kPlanLanes;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * (256 / kPlanLanes);
+    for (int64_t k = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) / kPlanLanes; k < a.K;
+         k += stride) {
+        const float *r = a.rois + 5 * k;
+        const float b0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
+        const int lvl = fpn_level(x1, y1, x2, y2, a.L, a.finest_scale);
+        const int bb = roi_batch(b0, a.N);
+        if (sub == 0) {
+            a.levels_out[k] = lvl;
+            const int key = plan_key(a, x1, y1, x2, y2, lvl, bb);
+            a.keys[k] = key;
+            atomicAdd(&a.key_count[key], 1);
+        }
+        if (a.ntiles > 0 && bb >= 0) {
             int tx0, tx1, ty0, ty1;
             roi_tile_box(a, lvl, x1, y1, x2, y2, tx0, tx1, ty0, ty1);
-            const int base = a.tbase[lvl] + b * a.nty[lvl] * a.ntx[lvl];
-            for (int ty = ty0; ty <= ty1; ++ty)
-                for (int tx = tx0; tx <= tx1; ++tx) {
-                    const int pos = atomicAdd(&hist[base + ty * a.ntx[lvl] + tx], 1);
-                    if (pos < a.capacity) a.tile_rois[pos] = k;
-                }
+            const int w = tx1 - tx0 + 1;
+            const int n = w * (ty1 - ty0 + 1);
+            const int base = a.tbase[lvl] + bb * a.nty[lvl] * a.ntx[lvl];
+            for (int i = sub; i < n; i += kPlanLanes) {
+                const int dy = i / w;
+                atomicAdd(&a.tile_start[base + (ty0 + dy) * a.ntx[lvl] + tx0 + (i - dy * w)], 1);
+            }
         }
     }
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_scan_kernel(PlanArgs a) {
+    extern __shared__ int32_t smem[];
+    int32_t *hist = smem;                           // [max(nbins, ntiles)]
+    int32_t *part = smem + max(a.nbins, a.ntiles);  // [kPlanThreads]
+    const int tid = threadIdx.x;
+
+    // Bucket starts (the fill kernel's cursors) and per-level offsets.
+    for (int i = tid; i < a.nbins; i += kPlanThreads) hist[i] = a.key_count[i];
+    __syncthreads();
+    block_exclusive_scan(hist, a.nbins, part);
+    for (int i = tid; i < a.nbins; i += kPlanThreads) a.key_count[i] = hist[i];
+    if (tid < a.L) a.offsets[tid] = hist[a.base[tid]];
+    if (tid == 0) a.offsets[a.L] = a.K;
+    if (a.ntiles <= 0) return;   // uniform
     __syncthreads();
 
-    // Launch order of the tiles: longest lists first (counting sort on the list
-    // length, capped at 255), so the longest sequential chains start earliest.  After
-    // the fill, hist[i] is the end of tile i's list and hist[i - 1] its start.
+    // Tile list starts and cursors; launch order of the tiles: longest lists first
+    // (counting sort on the list length, capped at 255), so the longest sequential
+    // chains start earliest.
     constexpr int kLenBins = 256;
-    for (int i = tid; i < kLenBins; i += kPlanThreads) part[i] = 0;
+    int32_t *lenh = part + 2 * (kPlanThreads / 64) + 1;   // [kLenBins], after the scan scratch
+    for (int i = tid; i < kLenBins; i += kPlanThreads) lenh[i] = 0;
+    for (int i = tid; i < a.ntiles; i += kPlanThreads) hist[i] = a.tile_start[i];
     __syncthreads();
+    for (int i = tid; i < a.ntiles; i += kPlanThreads)
+        atomicAdd(&lenh[kLenBins - 1 - min(hist[i], kLenBins - 1)], 1);
+    __syncthreads();
+    block_exclusive_scan(lenh, kLenBins, part);
     for (int i = tid; i < a.ntiles; i += kPlanThreads) {
-        const int len = min(hist[i] - (i > 0 ? hist[i - 1] : 0), kLenBins - 1);
-        atomicAdd(&part[kLenBins - 1 - len], 1);
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int run = 0;
-        for (int i = 0; i < kLenBins; ++i) {
-            const int c = part[i];
-            part[i] = run;
-            run += c;
-        }
-    }
-    __syncthreads();
-    for (int i = tid; i < a.ntiles; i += kPlanThreads) {
-        const int len = min(hist[i] - (i > 0 ? hist[i - 1] : 0), kLenBins - 1);
-        const int pos = atomicAdd(&part[kLenBins - 1 - len], 1);
+        const int pos = atomicAdd(&lenh[kLenBins - 1 - min(hist[i], kLenBins - 1)], 1);
         a.tile_order[pos] = i;
+    }
+    __syncthreads();
+    const int total = block_exclusive_scan(hist, a.ntiles, part);
+    for (int i = tid; i < a.ntiles; i += kPlanThreads) {
+        a.tile_start[i] = hist[i];
+        a.tile_cursor[i] = hist[i];
+    }
+    if (tid == 0) a.tile_start[a.ntiles] = total;
+}
+
+__global__ __launch_bounds__(256) void plan_fill_kernel(PlanArgs a) {
+    const int sub = threadIdx.x % kPlanLanes;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * (256 / kPlanLanes);
+    for (int64_t k = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) / kPlanLanes; k < a.K;
+         k += stride) {
+        if (sub == 0) {
+            const int pos = atomicAdd(&a.key_count[a.keys[k]], 1);
+            a.perm[pos] = static_cast<int32_t>(k);
+        }
+        if (a.ntiles > 0) {
+            const float *r = a.rois + 5 * k;
+            const int bb = roi_batch(r[0], a.N);
+            if (bb < 0) continue;
+            const int lvl = a.levels_out[k];
+            int tx0, tx1, ty0, ty1;
+            roi_tile_box(a, lvl, r[1], r[2], r[3], r[4], tx0, tx1, ty0, ty1);
+            const int w = tx1 - tx0 + 1;
+            const int n = w * (ty1 - ty0 + 1);
+            const int base = a.tbase[lvl] + bb * a.nty[lvl] * a.ntx[lvl];
+            for (int i = sub; i < n; i += kPlanLanes) {
+                const int dy = i / w;
+                const int t = base + (ty0 + dy) * a.ntx[lvl] + tx0 + (i - dy * w);
+                const int p = atomicAdd(&a.tile_cursor[t], 1);
+                if (p < a.capacity) a.tile_rois[p] = static_cast<int32_t>(k);
+            }
+        }
     }
 }
 
@@ -248,12 +341,24 @@ hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float fines
 }
 
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream) {
+    if (a.K <= kPlanSmall) {
+        const size_t shmem =
+            static_cast<size_t>(max(a.nbins, a.ntiles) + kPlanThreads + 3 * kPlanSmall) *
+            sizeof(int32_t);
+        plan_small_kernel<<<1, kPlanThreads, shmem, stream>>>(a);
+        return hipGetLastError();
+    }
+    // key counts, and the tile counts that become tile_start
+    const int ntc = a.ntiles > 0 ? a.ntiles + 1 : 0;
+    const int nclear = a.nbins + ntc;
+    plan_clear_kernel<<<max(1, min((nclear + 255) / 256, 1024)), 256, 0, stream>>>(
+        a.key_count, a.nbins, a.tile_start, ntc);
+    const int blocks = max(1, min((a.K + 256 / kPlanLanes - 1) / (256 / kPlanLanes), 4096));
+    plan_count_kernel<<<blocks, 256, 0, stream>>>(a);
     const size_t shmem =
         static_cast<size_t>(max(a.nbins, a.ntiles) + kPlanThreads) * sizeof(int32_t);
-    if (a.K <= kPlanThreads * kCached)
-        plan_kernel<true><<<1, kPlanThreads, shmem, stream>>>(a);
-    else
-        plan_kernel<false><<<1, kPlanThreads, shmem, stream>>>(a);
+    plan_scan_kernel<<<1, kPlanThreads, shmem, stream>>>(a);
+    plan_fill_kernel<<<blocks, 256, 0, stream>>>(a);
     return hipGetLastError();
 }
 
