@@ -93,18 +93,19 @@ re_status_t fpn_level_map(const float *rois, int64_t num_rois, int32_t num_level
 
 /* Bytes of device workspace a plan for num_rois RoIs over the pyramid `levels` needs
  * (host array; only n, h and w are read).  It holds the launch permutation and the
- * tile->RoI lists of the gather backward: 8 bytes per RoI, 4 per bin-tile, and 4 per
- * RoI times the largest number of 16-pixel tiles of one image-level.  Host-only;
- * writes *bytes. */
+ * tile->RoI lists of the gather backward (8 bytes per RoI, 8 per bin-tile, and 4 per
+ * RoI times the largest number of bin-tiles of one image-level) and the plan's own
+ * counters (60 KiB).  Host-only; writes *bytes. */
 re_status_t roi_extract_workspace_size(const re_level_t *levels, int32_t num_levels,
                                        int64_t num_rois, size_t *bytes);
 
-/* a1 + a2 in one launch -- the level of every RoI (written to levels_out, as by
- * fpn_level_map) and the launch plan: a permutation of the RoIs ordered by
- * (level, image, coarse spatial cell of the box centre) plus per-level offsets,
- * stored in `workspace`; the same launch also lists, for every 16-pixel bin-tile of
- * every (level, image), the RoIs whose footprint can reach it (used by the gather
- * backward).  The forward and backward walk the RoIs in plan order,
+/* a1 + a2 -- the level of every RoI (written to levels_out, as by fpn_level_map)
+ * and the launch plan: a permutation of the RoIs ordered by (level, image, coarse
+ * spatial cell of the box centre) plus per-level offsets, stored in `workspace`; the
+ * plan also lists, for every bin-tile (16 pixels or more a side) of every
+ * (level, image), the RoIs whose footprint can reach it, and orders the tiles by
+ * decreasing list length (used by the gather backward).  Up to 2048 RoIs this is one
+ * kernel launch, above that four (all on `stream`, nothing allocated).  The forward and backward walk the RoIs in plan order,
  * so neighbouring work shares cache; any valid permutation gives the same
  * results, and RoIs with equal keys may come in any order.  The plan stays valid
  * for as long as rois, levels_out and the level shapes are unchanged, so one plan
