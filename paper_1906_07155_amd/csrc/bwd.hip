@@ -292,15 +292,19 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     constexpr int GB = 64 * NB;            // floats of one RoI's gradient block (64 channels)
     constexpr int YP = (PH * T + 63) / 64;  // ballot passes for the row weights
     constexpr int XP = (PW * T + 63) / 64;
-    // Double-buffer the staged gradient block (the next RoI's block travels in
-    // registers while the current one is consumed) when two blocks fit in 32 KiB.
-    constexpr bool kDouble = 2 * GB * 4 <= 32768;
-    constexpr int NBUF = kDouble ? 2 : 1;
-    constexpr int PF = kDouble ? (GB + 255) / 256 : 1;   // prefetch registers per thread
+    // The staged gradient blocks form a ring of NBUF: the next RoI's block is copied
+    // into the other slot by the buffer unit while the current one is consumed, when
+    // two blocks fit in 52 KiB.  The copy gives every lane a 32-bit LDS slot whatever
+    // the element size, so a block holds one 32-bit word per element (a bf16 value in
+    // its low half).
+    constexpr int GBYTES = GB * 4;
+    constexpr int NBUF = 2 * GBYTES <= 53248 ? 2 : 1;
+    constexpr int NDMA = GB / 64;           // 64-element runs of one block
+    static_assert(GB % 64 == 0, "a copy instruction moves whole 64-element runs");
     static_assert(NR + NCOL <= 64, "taps are computed by one wavefront");
     static_assert(PH <= 32 && PW <= 32, "bin masks are 32-bit");
 
-    __shared__ float s_g[NBUF][GB];
+    __shared__ __align__(16) uint32_t s_g[NBUF][GB];
     __shared__ Tap s_tap[2][NR + NCOL];
     __shared__ __align__(16) float s_wy[4][PH * T];
     __shared__ __align__(16) float s_wx[4][PW * T];
@@ -379,20 +383,26 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
                               int64_t(sizeof(TG));
         return make_rsrc(src, static_cast<uint32_t>(nvalid) * uint32_t(sizeof(TG)));
     };
-    const uint32_t voff = static_cast<uint32_t>(tid) * uint32_t(sizeof(TG));
-    uint32_t pf[PF];
-    auto fetch = [&](int j) {
+    // Direct buffer-to-LDS copy: run r = wave + 4 m of the block goes to LDS words
+    // [buf][64 r, 64 r + 64), lane i writing element 64 r + i (the LDS address is the
+    // uniform run base plus 4 bytes per lane, the global offset the lane's own).
+    auto fetch = [&](int j, int buf) {
         const __amdgpu_buffer_rsrc_t rs = block_rsrc(j);
 #pragma unroll
-        for (int m = 0; m < PF; ++m) pf[m] = buf_load_raw_s<TG>(rs, voff, 256 * m * sizeof(TG));
-    };
-    auto put = [&](int buf) {
-#pragma unroll
-        for (int m = 0; m < PF; ++m) {
-            const int e = tid + 256 * m;
-            if (m < PF - 1 || e < GB) s_g[buf][e] = raw_to_f32<TG>(pf[m]);
+        for (int m = 0; m < (NDMA + 3) / 4; ++m) {
+            const int run = wave + 4 * m;
+            if (m < NDMA / 4 || run < NDMA) {
+                auto *dst = (__attribute__((address_space(3))) void *)(&s_g[buf][64 * run]);
+                const uint32_t off = static_cast<uint32_t>(64 * run + lane) * uint32_t(sizeof(TG));
+                if constexpr (sizeof(TG) == 4)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 4, off, 0, 0, 0);
+                else
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 2, off, 0, 0, 0);
+            }
         }
     };
+    // The copies of this wave are complete (vmcnt 0); a barrier then publishes them.
+    auto fetch_wait = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };
     // Sample taps of kept RoI j into tap buffer tb (lanes of wave 0).
     auto taps = [&](int j, int tb) {
         if (tid < NR + NCOL) {
@@ -470,7 +480,7 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
         }
         wave_sync();
 
-        const float *gl = s_g[buf] + lane * NB;   // this lane's channel, stride NB (odd)
+        const uint32_t *gl = s_g[buf] + lane * NB;   // this lane's channel, stride NB (odd)
         for (uint32_t ym = ymask; ym; ym &= ym - 1) {
             const int ph = __builtin_ctz(ym);
             float X[T];
@@ -478,7 +488,7 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
             for (int q = 0; q < T; ++q) X[q] = 0.0f;
             for (uint32_t xm = xmask; xm; xm &= xm - 1) {
                 const int pw = __builtin_ctz(xm);
-                const float gv = gl[ph * PW + pw];
+                const float gv = raw_to_f32<TG>(gl[ph * PW + pw]);
                 const float4 w0 = *reinterpret_cast<const float4 *>(wx + pw * T);
                 const float4 w1 = *reinterpret_cast<const float4 *>(wx + pw * T + 4);
                 X[0] = fmaf(w0.x, gv, X[0]);
@@ -561,42 +571,27 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
         __syncthreads();
         const int nk = s_n;
         if (nk == 0) continue;
-        if constexpr (kDouble) {
-            fetch(0);
-            put(0);
+        if constexpr (NBUF == 2) {
+            fetch(0, 0);
             taps(0, 0);
+            fetch_wait();
             __syncthreads();
             for (int j = 0; j < nk; ++j) {
                 const int buf = j & 1;
                 if (j + 1 < nk) {
-                    fetch(j + 1);           // lands while RoI j is processed
-                    taps(j + 1, buf ^ 1);   // the other tap buffer is idle
+                    fetch(j + 1, buf ^ 1);   // lands while RoI j is processed
+                    taps(j + 1, buf ^ 1);    // the other tap buffer is idle
                 }
                 consume(j, buf, buf);
-                if (j + 1 < nk) put(buf ^ 1);
+                fetch_wait();
                 __syncthreads();   // staged block, taps and weights are reused next
             }
         } else {
             for (int j = 0; j < nk; ++j) {
                 if (j > 0) __syncthreads();   // the previous block is fully consumed
-                {
-                    const __amdgpu_buffer_rsrc_t rs = block_rsrc(j);
-                    constexpr int NE = (GB + 255) / 256;
-                    constexpr int U = 7;   // loads in flight per thread
-#pragma unroll
-                    for (int m0 = 0; m0 < NE; m0 += U) {
-                        uint32_t v[U];
-#pragma unroll
-                        for (int u = 0; u < U; ++u)
-                            if (m0 + u < NE) v[u] = buf_load_raw_s<TG>(rs, voff, 256 * (m0 + u) * sizeof(TG));
-#pragma unroll
-                        for (int u = 0; u < U; ++u) {
-                            const int e = tid + 256 * (m0 + u);
-                            if (m0 + u < NE && e < GB) s_g[0][e] = raw_to_f32<TG>(v[u]);
-                        }
-                    }
-                }
+                fetch(j, 0);
                 taps(j, j & 1);
+                fetch_wait();
                 __syncthreads();
                 consume(j, 0, j & 1);
             }
@@ -605,7 +600,10 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
 
     // Every pixel of the quadrant is written once (the clearing is fused).  The
     // pixel offset is the same for the whole wave (scalar), the channel offset is the
-    // lane's; lanes past the last channel write out of range, which is dropped.
+    // lane's; lanes past the last channel write out of range, which is dropped.  The
+    // gradient pyramid is far larger than the L2 and read only by a later pass, so
+    // the stores are non-temporal: they stream to memory instead of evicting cached
+    // data.
     if (!wave_on) return;
     const char *img = static_cast<const char *>(L.data) + static_cast<int64_t>(b) * L.sn * 4;
     const __amdgpu_buffer_rsrc_t dst = make_rsrc(img, L.img_bytes);
@@ -622,7 +620,7 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
             const uint32_t so = rowo + static_cast<uint32_t>(q) * sw4;
             float v = acc[rr][q];
             if (!a.zero_init) v += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dst, vo, so, 0));
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), dst, vo, so, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), dst, vo, so, kStoreNT);
         }
     }
 }
