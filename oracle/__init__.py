@@ -1,4 +1,4 @@
-"""CPU oracle for multi-level RoIAlign -- TEST INFRASTRUCTURE ONLY.
+"""CPU oracle for multi-level RoIAlign and RoI max pooling -- TEST INFRASTRUCTURE ONLY.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product path never does, and this
@@ -67,6 +67,16 @@ def _bind(lib):
                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                          ctypes.c_int32]
     lib.oracle_roi_align_bwd.restype = None
+    lib.oracle_roi_pool_fwd.argtypes = [f64pp, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_void_p, ctypes.c_void_p]
+    lib.oracle_roi_pool_fwd.restype = None
+    lib.oracle_roi_pool_bwd.argtypes = [ctypes.c_void_p, ctypes.c_void_p, f64pp,
+                                        ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                        ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32,
+                                        ctypes.c_int32]
+    lib.oracle_roi_pool_bwd.restype = None
     return lib
 
 
@@ -168,4 +178,41 @@ def roi_align_bwd(grad_out, shapes, scales, rois, roi_levels, out_h: int, out_w:
     lib.oracle_roi_align_bwd(_ptr(g), arr, _ptr(dims), _ptr(sc), len(grads), _ptr(r), K,
                              None if lv is None else _ptr(lv), int(out_h), int(out_w),
                              int(sampling_ratio), int(bool(aligned)), _MODES[mode])
+    return grads
+
+
+def roi_pool_fwd(features, scales, rois, roi_levels, out_h: int, out_w: int, lib=None):
+    """RoI max pooling.  Returns (float64 [K, C, out_h, out_w], int32 argmax of the
+    same shape: y * W + x within the RoI's (level, image, channel) plane, -1 for none)."""
+    lib = lib or load()
+    feats = [np.ascontiguousarray(f, dtype=np.float64) for f in features]
+    dims, sc = _level_args([f.shape for f in feats], scales)
+    r = _rois(rois)
+    K = r.shape[0]
+    C = feats[0].shape[1]
+    lv = None if roi_levels is None else np.ascontiguousarray(roi_levels, dtype=np.int32)
+    out = np.zeros((K, C, out_h, out_w), dtype=np.float64)
+    am = np.full((K, C, out_h, out_w), -1, dtype=np.int32)
+    arr = (ctypes.c_void_p * len(feats))(*[f.ctypes.data for f in feats])
+    lib.oracle_roi_pool_fwd(arr, _ptr(dims), _ptr(sc), len(feats), _ptr(r), K,
+                            None if lv is None else _ptr(lv), int(out_h), int(out_w),
+                            _ptr(out), _ptr(am))
+    return out, am
+
+
+def roi_pool_bwd(grad_out, argmax, shapes, rois, roi_levels, lib=None) -> list:
+    """Each output gradient added to its argmax pixel.  Returns float64 gradients."""
+    lib = lib or load()
+    g = np.ascontiguousarray(grad_out, dtype=np.float64)
+    am = np.ascontiguousarray(argmax, dtype=np.int32)
+    dims, _ = _level_args(shapes, [1.0] * len(shapes))
+    r = _rois(rois)
+    K = r.shape[0]
+    if g.shape != am.shape or g.shape[:2] != (K, shapes[0][1]):
+        raise ValueError("grad_out and argmax must be [K, C, out_h, out_w]")
+    lv = None if roi_levels is None else np.ascontiguousarray(roi_levels, dtype=np.int32)
+    grads = [np.zeros(tuple(s), dtype=np.float64) for s in shapes]
+    arr = (ctypes.c_void_p * len(grads))(*[x.ctypes.data for x in grads])
+    lib.oracle_roi_pool_bwd(_ptr(g), _ptr(am), arr, _ptr(dims), len(grads), _ptr(r), K,
+                            None if lv is None else _ptr(lv), int(g.shape[2]), int(g.shape[3]))
     return grads

@@ -1,5 +1,5 @@
 /*
- * roi_oracle.c -- plain CPU oracle for multi-level RoIAlign.
+ * roi_oracle.c -- plain CPU oracle for multi-level RoIAlign (and RoI max pooling).
  *
  * TEST INFRASTRUCTURE ONLY.  This library exists so that the GPU library can be
  * checked against something slow and obviously correct.  Only the test suite,
@@ -14,6 +14,9 @@
  *     by the Faster/Mask R-CNN + FPN detectors; §1 ("High efficiency") states the
  *     bbox and mask operations run on GPUs; §3.2 (training pipeline) runs forward
  *     and backward every iteration, so the backward (the transpose) is needed too.
+ *   - The same sections list RoIPool (Fast R-CNN's max pooling over quantized
+ *     bins) among the RoIPooling-like extractors; oracle_roi_pool_fwd/bwd below
+ *     follow its usual definition.
  *   The paper does not spell the operator out.  The definition below is the
  *   standard one (bilinear sampling on a regular grid inside each bin, averaged),
  *   and every convention the paper leaves open is fixed the same way as in the
@@ -346,6 +349,126 @@ void oracle_roi_align_bwd(const double *grad_out, double *const *grad_feats,
                         }
                     }
                 }
+            }
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* RoI max pooling -- the RoIPool of Fast R-CNN, the other RoIPooling-like     */
+/* extractor besides RoIAlign that the detectors of §2 / §3.1 use.             */
+/*                                                                             */
+/* Geometry, binary32, one rounding per operation in this order:               */
+/*   start_x = roundf(x1 * scale), end_x = roundf(x2 * scale)  (halves away    */
+/*   from zero); the box spans w = max(end_x - start_x + 1, 1) pixels (both    */
+/*   ends inclusive); bin width bw = w / PW.  Bin column pw covers pixels      */
+/*   [floor(pw * bw), ceil((pw + 1) * bw)) shifted by start_x and clipped to   */
+/*   [0, W]; rows likewise.                                                     */
+/* Output: the largest value in the bin; scanning rows top to bottom and each  */
+/* row left to right, a value replaces the current one only if strictly larger */
+/* (so the first maximum wins and a NaN is never chosen).  An empty bin gives  */
+/* 0 and argmax -1; a non-empty bin that holds no comparable value gives       */
+/* -FLT_MAX and argmax -1.  argmax = y * W + x of the chosen pixel.            */
+/* Backward: every output gradient is added to its argmax pixel (none for -1). */
+/* ------------------------------------------------------------------------- */
+
+#define ORACLE_FLT_MAX 3.4028234663852886e38
+
+typedef struct {
+    int lo, hi;   /* [lo, hi) after clipping */
+} pool_range;
+
+static pool_range pool_bin(float c1, float c2, float scale, int P, int p, int size)
+{
+    float s = roundf(c1 * scale);
+    float e = roundf(c2 * scale);
+    float len = e - s;
+    len = len + 1.0f;
+    if (len < 1.0f)
+        len = 1.0f;
+    float bin = len / (float)P;
+    float a = (float)p * bin;
+    float b = (float)(p + 1) * bin;
+    int lo = (int)floorf(a) + (int)s;
+    int hi = (int)ceilf(b) + (int)s;
+    pool_range r;
+    r.lo = lo < 0 ? 0 : (lo > size ? size : lo);
+    r.hi = hi < 0 ? 0 : (hi > size ? size : hi);
+    return r;
+}
+
+void oracle_roi_pool_fwd(const double *const *feats, const int64_t *dims,
+                         const float *scales, int32_t num_levels,
+                         const float *rois, int64_t K, const int32_t *roi_levels,
+                         int32_t PH, int32_t PW, double *out, int32_t *argmax)
+{
+    const int64_t C = dims[1];
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t k = 0; k < K; ++k) {
+        double *o = out + k * C * PH * PW;
+        int32_t *am = argmax + k * C * PH * PW;
+        for (int64_t e = 0; e < C * PH * PW; ++e) {
+            o[e] = 0.0;
+            am[e] = -1;
+        }
+        const float *r = rois + 5 * k;
+        int lvl = roi_levels ? roi_levels[k] : 0;
+        if (lvl < 0 || lvl >= num_levels)
+            continue;
+        const int64_t N = dims[4 * lvl + 0];
+        const int64_t H = dims[4 * lvl + 2];
+        const int64_t W = dims[4 * lvl + 3];
+        int b = roi_batch(r[0], N);
+        if (b < 0)
+            continue;
+        for (int64_t c = 0; c < C; ++c) {
+            const double *F = feats[lvl] + ((int64_t)b * C + c) * H * W;
+            for (int ph = 0; ph < PH; ++ph) {
+                pool_range ry = pool_bin(r[2], r[4], scales[lvl], PH, ph, (int)H);
+                for (int pw = 0; pw < PW; ++pw) {
+                    pool_range rx = pool_bin(r[1], r[3], scales[lvl], PW, pw, (int)W);
+                    const int64_t e = (c * PH + ph) * PW + pw;
+                    if (ry.hi <= ry.lo || rx.hi <= rx.lo)
+                        continue;   /* empty bin: 0, -1 */
+                    double best = -ORACLE_FLT_MAX;
+                    int32_t where = -1;
+                    for (int y = ry.lo; y < ry.hi; ++y)
+                        for (int x = rx.lo; x < rx.hi; ++x)
+                            if (F[y * W + x] > best) {
+                                best = F[y * W + x];
+                                where = (int32_t)(y * W + x);
+                            }
+                    o[e] = best;
+                    am[e] = where;
+                }
+            }
+        }
+    }
+}
+
+void oracle_roi_pool_bwd(const double *grad_out, const int32_t *argmax,
+                         double *const *grad_feats, const int64_t *dims,
+                         int32_t num_levels, const float *rois, int64_t K,
+                         const int32_t *roi_levels, int32_t PH, int32_t PW)
+{
+    const int64_t C = dims[1];
+#pragma omp parallel for schedule(static)
+    for (int64_t c = 0; c < C; ++c) {
+        for (int64_t k = 0; k < K; ++k) {
+            int lvl = roi_levels ? roi_levels[k] : 0;
+            if (lvl < 0 || lvl >= num_levels)
+                continue;
+            const int64_t N = dims[4 * lvl + 0];
+            const int64_t H = dims[4 * lvl + 2];
+            const int64_t W = dims[4 * lvl + 3];
+            int b = roi_batch(rois[5 * k], N);
+            if (b < 0)
+                continue;
+            double *G = grad_feats[lvl] + ((int64_t)b * C + c) * H * W;
+            for (int e = 0; e < PH * PW; ++e) {
+                const int64_t i = (k * C + c) * PH * PW + e;
+                if (argmax[i] >= 0 && argmax[i] < H * W)
+                    G[argmax[i]] += grad_out[i];
             }
         }
     }
