@@ -430,6 +430,7 @@ re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype, const fl
         g.capacity = static_cast<int32_t>(tl.capacity);
         g.tile_shift = tl.shift;
         g.qside = 1 << (tl.shift - 3);
+        g.cg_form = (out_h == 7 && grad_out_dtype == RE_DTYPE_BF16) ? 1 : 0;
         for (int l = 0; l < kMaxLevels; ++l) {
             g.ntx[l] = tl.ntx[l];
             g.nty[l] = tl.nty[l];

@@ -69,6 +69,8 @@ struct GatherArgs {
     int32_t qside;               // 8x8 quadrants per bin-tile side
     int32_t ncg;                 // 64-channel groups
     int32_t wg_per_tile;
+    int32_t cg_form;             // 1: workgroup = 4 channel groups of one quadrant
+                                 //    (bf16 upstream gradient, 7x7)
     int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
 };
 

@@ -123,12 +123,15 @@ def _pyr(c):
     return [(n, c, h, w) for (n, _, h, w) in PYR]
 
 
+@pytest.mark.parametrize("gdt", ["f32", "bf16"])
 @pytest.mark.parametrize("out_hw", [(7, 7), (14, 14)])
 @pytest.mark.parametrize("C", [1, 3, 100, 256, 320])
-def test_channels_ragged(out_hw, C):
+def test_channels_ragged(out_hw, C, gdt):
+    # a bf16 upstream gradient on the 7x7 grid takes the channel-group gather form,
+    # whose workgroups hold up to four channel groups (partial ones included)
     rng = np.random.default_rng(C)
     rois = W.draw_rois(rng, 2, 19, (96, 160), (4.0, 200.0))
-    run("C=%d %s" % (C, out_hw), _pyr(C), SC, rois, out_hw=out_hw)
+    run("C=%d %s g=%s" % (C, out_hw, gdt), _pyr(C), SC, rois, out_hw=out_hw, gdt=gdt)
 
 
 @pytest.mark.parametrize("S", [0, 1, 2, 3])
@@ -216,6 +219,8 @@ def test_backward_accumulates_without_zero_init(out_hw):
     rng = np.random.default_rng(85)
     rois = W.draw_rois(rng, 2, 33, (96, 160), (4.0, 200.0))
     run("accumulate %s" % (out_hw,), _pyr(96), SC, rois, out_hw=out_hw, zero_init=False)
+    run("accumulate %s bf16 grad" % (out_hw,), _pyr(96), SC, rois, out_hw=out_hw,
+        zero_init=False, gdt="bf16")
 
 
 def test_dense_rois_on_one_tile():
@@ -226,6 +231,7 @@ def test_dense_rois_on_one_tile():
     rois[:, 1:] += rng.uniform(-3, 3, (150, 4)).astype(np.float32)
     rois[:, 0] = rng.integers(0, 2, 150)
     run("150 stacked RoIs", _pyr(64), SC, rois)
+    run("150 stacked RoIs bf16 grad", _pyr(64), SC, rois, gdt="bf16")
     run("150 stacked RoIs mask", _pyr(64), SC, rois, out_hw=(14, 14))
 
 
