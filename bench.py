@@ -58,12 +58,16 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle work timed for the CPU baseline (seconds)")
     ap.add_argument("--calibrate-copy", action="store_true")
+    ap.add_argument("--op", default="align", choices=["align", "pool"],
+                    help="align: RoIAlign (the benchmark); pool: RoI max pooling on the same "
+                         "workload (plan, roi_pool_fwd, roi_pool_bwd with clearing)")
     return ap.parse_args()
 
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for name in ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "api.hip"):
+    for name in ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip",
+                 "api.hip"):
         with open(os.path.join(ROOT, "paper_1906_07155_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -109,6 +113,9 @@ def main():
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.op == "pool":
+        main_pool(args)
         return
 
     import torch
@@ -318,6 +325,119 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "extra": extra,
+    }
+    print(json.dumps(result), flush=True)
+
+
+def main_pool(args):
+    """RoI max pooling on a workload's pyramid and RoIs: one step is roi_extract_plan,
+    roi_pool_fwd and roi_pool_bwd (clearing included; fp32 atomics)."""
+    import torch
+
+    import oracle
+    import paper_1906_07155_amd as rex
+    from paper_1906_07155_amd import accounting, workloads
+
+    dev = torch.device("cuda:0")
+    wl = workloads.config(args.workload, head=args.head, feat_dtype=args.feat_dtype)
+    feats_np, rois_np = wl.features(), wl.rois()
+    K, C = rois_np.shape[0], wl.channels
+    bf16 = wl.feat_dtype == "bf16"
+
+    def to_dev(a, dt):
+        if dt == "bf16":
+            t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(a).to(dev)
+        return t.contiguous(memory_format=torch.channels_last)
+
+    feats = [to_dev(f, wl.feat_dtype) for f in feats_np]
+    rois = torch.from_numpy(rois_np).to(dev)
+    odt = torch.bfloat16 if wl.out_dtype == "bf16" else torch.float32
+    out = torch.empty((K, C) + tuple(wl.out_hw), dtype=odt, device=dev)
+    am = torch.empty((K, C) + tuple(wl.out_hw), dtype=torch.int32, device=dev)
+    gout = torch.from_numpy(np.ascontiguousarray(wl.grad()).view(
+        np.int16 if wl.grad_dtype == "bf16" else np.float32)).to(dev)
+    if wl.grad_dtype == "bf16":
+        gout = gout.view(torch.bfloat16)
+    grads = [torch.empty(f.shape, dtype=torch.float32, device=dev).contiguous(
+        memory_format=torch.channels_last) for f in feats]
+    levels = torch.empty(K, dtype=torch.int32, device=dev)
+    ws = torch.empty(rex.workspace_size(feats, wl.scales, K), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    names = ["plan", "fwd", "bwd"]
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        rex.plan(feats, wl.scales, rois, wl.finest_scale, levels_out=levels, workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        rex.roi_pool_fwd(feats, wl.scales, rois, levels, wl.out_hw, out=out, argmax=am,
+                         workspace=ws)
+        if ev is not None:
+            ev[2].record(stream)
+        rex.roi_pool_bwd(gout, am, rois, levels, grads, wl.scales, zero_init=True, workspace=ws)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
+           for j, n in enumerate(names)}
+    lv_np = levels.cpu().numpy()
+    by = accounting.count_pool(rois_np, lv_np, wl.level_hw, wl.scales, wl.n_images, C, wl.out_hw,
+                               2 if bf16 else 4, 2 if wl.out_dtype == "bf16" else 4,
+                               2 if wl.grad_dtype == "bf16" else 4)
+    alg = {"plan": 24 * K + 12 * K, "fwd": by.e_fwd, "bwd": by.e_bwd + by.zero}
+    gbs = {n: alg[n] / (per[n] * 1e-3) / 1e9 for n in names}
+    dominant = max(["fwd", "bwd"], key=lambda n: per[n])
+    roofline = {"bound": "hbm", "achieved": round(gbs[dominant], 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(gbs[dominant] / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "roi_pool_" + dominant, "bytes_per_launch": alg[dominant],
+                "launch_ms": round(per[dominant], 5)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        lib = oracle.load()
+        f64 = [(workloads.bf16_bits_to_f32(f) if bf16 else f).astype(np.float64) for f in feats_np]
+        g64 = np.random.default_rng(0).standard_normal((K, C) + tuple(wl.out_hw))
+        elapsed, passes = 0.0, 0
+        while elapsed < args.cpu_seconds:
+            c0 = time.perf_counter()
+            _, am_ref = oracle.roi_pool_fwd(f64, wl.scales, rois_np, lv_np, *wl.out_hw, lib=lib)
+            oracle.roi_pool_bwd(g64, am_ref, [f.shape for f in f64], rois_np, lv_np, lib=lib)
+            elapsed += time.perf_counter() - c0
+            passes += 1
+        cpu = {"value": round(K * passes / elapsed, 1), "unit": "RoIs/s",
+               "cores": oracle.num_threads(lib), "kind": "oracle",
+               "sample": "all %d RoIs (all %d channels), fwd+bwd, %d passes in %.1f s wall" % (
+                   K, C, passes, elapsed)}
+    result = {
+        "metric": "RoI max pooling fwd+bwd RoIs/sec and achieved HBM GB/s vs peak, FPN shapes",
+        "value": round(K / (ms_per_step * 1e-3), 1), "unit": "RoIs/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic (seeded normal features, log-uniform RoIs; no COCO)",
+        "config": {"workload": wl.name + ", RoI max pooling", "num_rois": K, "channels": C,
+                   "levels": [list(x) for x in wl.level_hw], "out": list(wl.out_hw),
+                   "layout": "cl", "backward": True},
+        "roofline": roofline, "cpu_baseline": cpu,
+        "extra": {"kernel_ms": {n: round(v, 5) for n, v in per.items()},
+                  "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
+                  "bytes": {"E_fwd": by.e_fwd, "E_bwd": by.e_bwd, "zero_fill": by.zero,
+                            "box_px": by.box_px},
+                  "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(result), flush=True)
 

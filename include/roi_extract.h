@@ -181,6 +181,44 @@ re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype,
                           int32_t zero_init, int32_t algorithm, const void *plan,
                           size_t plan_bytes, void *stream);
 
+/* f1 -- RoI max pooling, the RoIPool of Fast R-CNN (a two-stage method of §2),
+ * the other RoIPooling-like operator a RoIExtractor uses (§3.1).  On level l (scale
+ * s, H x W map), every operation rounded to binary32 in this order:
+ *   xs = roundf(x1*s), xe = roundf(x2*s)   (halves away from zero)
+ *   len = max(xe - xs + 1, 1)              (both end pixels belong to the box)
+ *   bin = len / out_w;  bin pw covers columns [floor(pw*bin) + xs, ceil((pw+1)*bin) + xs)
+ *   clipped to [0, W]; rows likewise with y1, y2, out_h, H.
+ * out[k,c,ph,pw] is the largest value of the bin: the pixels are scanned row by row,
+ * each row left to right, and a value replaces the running maximum only if it is
+ * strictly larger (so the first maximum wins and a NaN is never chosen; the running
+ * maximum starts at -FLT_MAX).  argmax[k,c,ph,pw] = y*W + x of the chosen pixel.
+ * An empty bin gives 0 and argmax -1; a non-empty bin without a value larger than
+ * -FLT_MAX (all NaN or -inf) gives -FLT_MAX (bf16 output: the most negative finite
+ * bf16) and argmax -1.  A RoI whose batch or level index is invalid gives 0 / -1.
+ *   levels, rois, roi_levels, plan: as roi_align_fwd (every H*W below 2^31);
+ *   out: device [num_rois][c][out_h][out_w] of out_dtype (bf16: features rounded to
+ *        nearest even, so bf16 features are stored exactly);
+ *   argmax: device int32 [num_rois][c][out_h][out_w].
+ * Writes every element of out and argmax once; results do not depend on the plan. */
+re_status_t roi_pool_fwd(const re_level_t *levels, int32_t num_levels, const float *rois,
+                         int64_t num_rois, const int32_t *roi_levels, int32_t out_h,
+                         int32_t out_w, void *out, int32_t out_dtype, int32_t *argmax,
+                         const void *plan, size_t plan_bytes, void *stream);
+
+/* f1 -- RoI max pooling backward: grad_F_l[b, c, argmax / W, argmax % W] +=
+ * grad_out[k, c, ph, pw] for every element whose argmax is in [0, H*W) (no gradient
+ * for -1), summed with fp32 atomics (the order, hence the last bits, may vary).  The
+ * gradient pyramid is cleared first when zero_init != 0.
+ *   grad_out: device [num_rois][c][out_h][out_w] of grad_out_dtype;
+ *   argmax: device int32, as written by roi_pool_fwd for the same RoIs and levels;
+ *   grad_levels: binary32 levels with the forward's n, c, h, w;
+ *   other arguments as roi_pool_fwd. */
+re_status_t roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype, const int32_t *argmax,
+                         const float *rois, int64_t num_rois, const int32_t *roi_levels,
+                         int32_t out_h, int32_t out_w, const re_level_t *grad_levels,
+                         int32_t num_levels, int32_t zero_init, const void *plan,
+                         size_t plan_bytes, void *stream);
+
 /* Static description of a status code. */
 const char *roi_extract_status_str(re_status_t status);
 

@@ -131,3 +131,54 @@ def count(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[int, in
         u_fwd=union_total * C * s_feat + out_elems * s_out + 24 * K,
         u_bwd=out_elems * s_gout + 2 * union_total * C * 4 + 24 * K,
         t_fwd=taps_total * C * s_feat, zero=zero, out_bytes=out_elems * s_out)
+
+
+def _round_half_away(x32: np.ndarray) -> np.ndarray:
+    """roundf of binary32 values (halves away from zero), exact in float64."""
+    x = x32.astype(np.float64)
+    return np.sign(x) * np.floor(np.abs(x) + 0.5)
+
+
+@dataclasses.dataclass
+class PoolBytes:
+    K: int
+    box_px: int              # sum over RoIs of the quantized box clipped to the map
+    e_fwd: int               # box pixels x C read, values and argmax written
+    e_bwd: int               # gradient and argmax read, one fp32 read-modify-write each
+    zero: int
+
+
+def count_pool(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[int, int]],
+               scales: Sequence[float], n_images: int, C: int, out_hw: Tuple[int, int],
+               s_feat: int, s_out: int, s_gout: int) -> PoolBytes:
+    """Effective bytes of RoI max pooling.  The bins of a RoI tile its quantized box
+    [round(x1 s), round(x2 s)] (both ends included) clipped to the map, so the forward
+    reads that box once per channel:
+
+      E_fwd = sum_r box_r*C*s_feat + K*C*PH*PW*(s_out + 4) + 24*K
+      E_bwd = K*C*PH*PW*(s_gout + 4) + K*C*PH*PW*8 + 24*K     (+ clearing, reported apart)
+    """
+    K = rois.shape[0]
+    PH, PW = out_hw
+    box = 0
+    for l, ((H, W), sc) in enumerate(zip(level_hw, scales)):
+        idx = np.flatnonzero(levels == l)
+        if idx.size == 0:
+            continue
+        r = rois[idx]
+        b = np.trunc(r[:, 0]).astype(np.int64)
+        ok = (b >= 0) & (b < n_images)
+        s = F32(sc)
+        xs = _round_half_away(r[:, 1].astype(F32) * s)
+        xe = _round_half_away(r[:, 3].astype(F32) * s)
+        ys = _round_half_away(r[:, 2].astype(F32) * s)
+        ye = _round_half_away(r[:, 4].astype(F32) * s)
+        w = np.maximum(xe - xs + 1, 1)
+        h = np.maximum(ye - ys + 1, 1)
+        cols = np.clip(xs + w, 0, W) - np.clip(xs, 0, W)
+        rows = np.clip(ys + h, 0, H) - np.clip(ys, 0, H)
+        box += int((cols * rows)[ok].sum())
+    elems = K * C * PH * PW
+    zero = sum(n_images * C * H * W * 4 for (H, W) in level_hw)
+    return PoolBytes(K=K, box_px=box, e_fwd=box * C * s_feat + elems * (s_out + 4) + 24 * K,
+                     e_bwd=elems * (s_gout + 4) + elems * 8 + 24 * K, zero=zero)

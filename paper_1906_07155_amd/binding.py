@@ -59,6 +59,9 @@ SIGNATURES = {
     "roi_extract_zero_grad": [_LEVELS, _I32, _VP],
     "roi_align_bwd": [_VP, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _LEVELS, _I32, _I32,
                       _I32, _VP, _SZ, _VP],
+    "roi_pool_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _VP, _I32, _VP, _VP, _SZ, _VP],
+    "roi_pool_bwd": [_VP, _I32, _VP, _VP, _I64, _VP, _I32, _I32, _LEVELS, _I32, _I32, _VP, _SZ,
+                     _VP],
 }
 
 _lock = threading.Lock()
@@ -266,4 +269,54 @@ def roi_align_bwd(grad_out, rois, roi_levels, out_size: Tuple[int, int], samplin
                               int(bool(zero_init)), _BWD_ALGOS[algorithm], ws, wsb,
                               stream_handle(stream)),
           "roi_align_bwd")
+    return grads
+
+
+def roi_pool_fwd(features: Sequence, scales: Sequence[float], rois, roi_levels,
+                 out_size: Tuple[int, int], out_dtype=None, workspace=None, out=None,
+                 argmax=None, stream=None):
+    """RoI max pooling.  Returns (out [K, C, out_h, out_w], argmax int32 of the same shape:
+    y * W + x of the chosen pixel in its level plane, -1 for none)."""
+    torch = _torch()
+    rois = _rois(rois)
+    K, L = rois.shape[0], len(features)
+    C = features[0].shape[1]
+    ph, pw = out_size
+    odt = out_dtype or features[0].dtype
+    if out is None:
+        out = torch.empty((K, C, ph, pw), dtype=odt, device=rois.device)
+    if argmax is None:
+        argmax = torch.empty((K, C, ph, pw), dtype=torch.int32, device=rois.device)
+    if not out.is_contiguous() or not argmax.is_contiguous() or argmax.dtype != torch.int32:
+        raise ValueError("out and argmax must be contiguous [K, C, out_h, out_w] (argmax int32)")
+    arr = level_array(features, scales)
+    lv = roi_levels.data_ptr() if roi_levels is not None else None
+    ws = workspace.data_ptr() if workspace is not None else None
+    wsb = workspace.numel() if workspace is not None else 0
+    check(lib().roi_pool_fwd(arr, L, rois.data_ptr(), K, lv, ph, pw, out.data_ptr(),
+                             _dtype_code(out), argmax.data_ptr(), ws, wsb, stream_handle(stream)),
+          "roi_pool_fwd")
+    return out, argmax
+
+
+def roi_pool_bwd(grad_out, argmax, rois, roi_levels, grads: Sequence, scales: Sequence[float],
+                 zero_init: bool = True, workspace=None, stream=None):
+    """Add every upstream gradient to its argmax pixel of `grads` (float32 levels, cleared
+    first if zero_init)."""
+    torch = _torch()
+    rois = _rois(rois)
+    _need_cuda(grad_out, "grad_out")
+    if not grad_out.is_contiguous() or not argmax.is_contiguous():
+        raise ValueError("grad_out and argmax must be contiguous [K, C, out_h, out_w]")
+    if argmax.dtype != torch.int32 or tuple(argmax.shape) != tuple(grad_out.shape):
+        raise ValueError("argmax must be int32 with grad_out's shape")
+    K, L = rois.shape[0], len(grads)
+    ph, pw = grad_out.shape[2], grad_out.shape[3]
+    arr = level_array(grads, scales)
+    lv = roi_levels.data_ptr() if roi_levels is not None else None
+    ws = workspace.data_ptr() if workspace is not None else None
+    wsb = workspace.numel() if workspace is not None else 0
+    check(lib().roi_pool_bwd(grad_out.data_ptr(), _dtype_code(grad_out), argmax.data_ptr(),
+                             rois.data_ptr(), K, lv, ph, pw, arr, L, int(bool(zero_init)), ws,
+                             wsb, stream_handle(stream)), "roi_pool_bwd")
     return grads

@@ -460,4 +460,97 @@ re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype, const fl
     return from_hip(launch_bwd(a, grad_out_dtype, fast, s));
 }
 
+// ---------------------------------------------------------------------------
+// RoI max pooling
+// ---------------------------------------------------------------------------
+
+namespace {
+// The argmax is a 32-bit index y * W + x into one (level, image, channel) plane.
+bool planes_fit_int32(const LevelTable &t) {
+    for (int l = 0; l < t.num; ++l)
+        if (int64_t(t.l[l].H) * t.l[l].W > INT32_MAX) return false;
+    return true;
+}
+}  // namespace
+
+re_status_t roi_pool_fwd(const re_level_t *levels, int32_t num_levels, const float *rois,
+                         int64_t num_rois, const int32_t *roi_levels, int32_t out_h,
+                         int32_t out_w, void *out, int32_t out_dtype, int32_t *argmax,
+                         const void *plan, size_t plan_bytes, void *stream) {
+    LevelTable t;
+    bool cl = false;
+    re_status_t st = check_levels(levels, num_levels, true, &t, &cl, nullptr, nullptr);
+    if (st != RE_OK) return st;
+    if ((st = check_common(rois, num_rois, roi_levels, num_levels, out_h, out_w, 0, 0)) != RE_OK)
+        return st;
+    if (!planes_fit_int32(t)) return RE_ERR_INVALID_ARG;
+    if (!valid_dtype(out_dtype)) return RE_ERR_INVALID_ARG;
+    if (num_rois > 0 && (!out || !argmax)) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(out) % dtype_size(out_dtype)) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(argmax) % 4) return RE_ERR_INVALID_ARG;
+    if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
+    if (num_rois == 0) return RE_OK;
+
+    PoolArgs a{};
+    a.lv = t;
+    a.rois = rois;
+    a.roi_levels = roi_levels;
+    a.perm = plan ? reinterpret_cast<const int32_t *>(static_cast<const char *>(plan) +
+                                                      perm_offset())
+                  : nullptr;
+    a.out = out;
+    a.argmax = argmax;
+    a.K = static_cast<int32_t>(num_rois);
+    a.PH = out_h;
+    a.PW = out_w;
+    const bool fast = cl && pool_fwd_fast_available(out_h, out_w);
+    return from_hip(launch_pool_fwd(a, levels[0].dtype, out_dtype, fast,
+                                    static_cast<hipStream_t>(stream)));
+}
+
+re_status_t roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype, const int32_t *argmax,
+                         const float *rois, int64_t num_rois, const int32_t *roi_levels,
+                         int32_t out_h, int32_t out_w, const re_level_t *grad_levels,
+                         int32_t num_levels, int32_t zero_init, const void *plan,
+                         size_t plan_bytes, void *stream) {
+    LevelTable t;
+    bool cl = false;
+    int64_t numel[RE_MAX_LEVELS] = {0};
+    int dense[RE_MAX_LEVELS] = {0};
+    re_status_t st = check_levels(grad_levels, num_levels, true, &t, &cl, numel, dense);
+    if (st != RE_OK) return st;
+    for (int l = 0; l < num_levels; ++l)
+        if (grad_levels[l].dtype != RE_DTYPE_F32) return RE_ERR_UNSUPPORTED;
+    if ((st = check_common(rois, num_rois, roi_levels, num_levels, out_h, out_w, 0, 0)) != RE_OK)
+        return st;
+    if (!planes_fit_int32(t)) return RE_ERR_INVALID_ARG;
+    if (!valid_dtype(grad_out_dtype)) return RE_ERR_INVALID_ARG;
+    if (num_rois > 0 && (!grad_out || !argmax)) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(grad_out) % dtype_size(grad_out_dtype))
+        return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(argmax) % 4) return RE_ERR_INVALID_ARG;
+    if (zero_init != 0 && zero_init != 1) return RE_ERR_INVALID_ARG;
+    if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (zero_init) {
+        if ((st = from_hip(launch_zero(t, numel, dense, s))) != RE_OK) return st;
+    }
+    if (num_rois == 0) return RE_OK;
+    PoolArgs a{};
+    a.lv = t;
+    a.rois = rois;
+    a.roi_levels = roi_levels;
+    a.perm = plan ? reinterpret_cast<const int32_t *>(static_cast<const char *>(plan) +
+                                                      perm_offset())
+                  : nullptr;
+    a.argmax = const_cast<int32_t *>(argmax);
+    a.gout = grad_out;
+    a.K = static_cast<int32_t>(num_rois);
+    a.PH = out_h;
+    a.PW = out_w;
+    const bool fast = cl && pool_fwd_fast_available(out_h, out_w);
+    return from_hip(launch_pool_bwd(a, grad_out_dtype, fast, s));
+}
+
 }  // extern "C"

@@ -102,6 +102,27 @@ struct BwdArgs {
     int32_t pad;
 };
 
+// RoI max pooling (forward and backward share the block).
+constexpr int kPoolFastBins = 96;   // largest out_h * out_w of the channels-last kernels
+
+struct PoolArgs {
+    LevelTable lv;               // features (forward) or binary32 gradients (backward)
+    const float *rois;
+    const int32_t *roi_levels;
+    const int32_t *perm;         // plan order or null
+    void *out;                   // forward: [K][C][PH][PW]
+    int32_t *argmax;             // [K][C][PH][PW]; read-only in the backward
+    const void *gout;            // backward: [K][C][PH][PW]
+    int32_t K;
+    int32_t PH, PW;
+    int32_t nslices;
+};
+
+bool pool_fwd_fast_available(int PH, int PW);
+hipError_t launch_pool_fwd(PoolArgs a, int feat_dtype, int out_dtype, bool fast,
+                           hipStream_t stream);
+hipError_t launch_pool_bwd(PoolArgs a, int gout_dtype, bool fast, hipStream_t stream);
+
 hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float finest_scale,
                             int32_t *out, hipStream_t stream);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);

@@ -179,3 +179,48 @@ def test_plan_validation(L):
 def test_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(RuntimeError):
         B.lib(str(tmp_path / "missing.so"))
+
+
+def _pfwd(L, levels=None, nl=2, K=4, oh=7, ow=7, out=FAKE, odt=0, am=FAKE, plan=None,
+          plan_bytes=0):
+    levels = levels if levels is not None else _levels()
+    return L.roi_pool_fwd(levels, nl, FAKE, K, FAKE, oh, ow, out, odt, am, plan, plan_bytes,
+                          None)
+
+
+def _pbwd(L, levels=None, nl=2, gout=FAKE, gdt=0, am=FAKE, K=4, zero=0, oh=7, ow=7, plan=None,
+          plan_bytes=0):
+    levels = levels if levels is not None else _levels()
+    return L.roi_pool_bwd(gout, gdt, am, FAKE, K, FAKE, oh, ow, levels, nl, zero, plan,
+                          plan_bytes, None)
+
+
+def test_pool_forward_validation(L):
+    assert _pfwd(L, K=0) == OK                                     # nothing to do
+    assert _pfwd(L, nl=0) == INVALID
+    assert _pfwd(L, K=-1) == INVALID
+    assert _pfwd(L, oh=0) == INVALID
+    assert _pfwd(L, ow=257) == INVALID
+    assert _pfwd(L, out=None) == INVALID
+    assert _pfwd(L, am=None) == INVALID
+    assert _pfwd(L, am=FAKE + 2) == INVALID                        # int32 argmax misaligned
+    assert _pfwd(L, odt=9) == INVALID
+    assert _pfwd(L, odt=0, out=FAKE + 2) == INVALID
+    assert _pfwd(L, plan=FAKE, plan_bytes=16) == WORKSPACE
+    big = _levels(hw=((1 << 16, 1 << 15), (8, 10)))                 # H*W = 2^31: argmax overflows
+    assert _pfwd(L, levels=big) == INVALID
+    assert L.roi_pool_fwd(_levels(), 2, FAKE, 4, None, 7, 7, FAKE, 0, FAKE, None, 0,
+                          None) == INVALID                         # several levels need indices
+
+
+def test_pool_backward_validation(L):
+    assert _pbwd(L, levels=_levels(dtype=1)) == UNSUPPORTED        # gradient levels must be fp32
+    assert _pbwd(L, zero=2) == INVALID
+    assert _pbwd(L, gout=None) == INVALID
+    assert _pbwd(L, am=None) == INVALID
+    assert _pbwd(L, am=FAKE + 1) == INVALID
+    assert _pbwd(L, gdt=4) == INVALID
+    assert _pbwd(L, gdt=0, gout=FAKE + 2) == INVALID
+    assert _pbwd(L, oh=0) == INVALID
+    assert _pbwd(L, plan=FAKE, plan_bytes=8) == WORKSPACE
+    assert _pbwd(L, K=0, zero=0) == OK                             # nothing to do
