@@ -58,9 +58,12 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle work timed for the CPU baseline (seconds)")
     ap.add_argument("--calibrate-copy", action="store_true")
-    ap.add_argument("--op", default="align", choices=["align", "pool"],
+    ap.add_argument("--op", default="align", choices=["align", "pool", "heads"],
                     help="align: RoIAlign (the benchmark); pool: RoI max pooling on the same "
-                         "workload (plan, roi_pool_fwd, roi_pool_bwd with clearing)")
+                         "workload (plan, roi_pool_fwd, roi_pool_bwd with clearing); heads: "
+                         "box and mask heads on one pyramid (workload 2: the batch-2 box and "
+                         "mask RoIs; workload 5: both heads of the batch-16 step), one fused "
+                         "backward, timed against two separate backward calls")
     return ap.parse_args()
 
 
@@ -116,6 +119,9 @@ def main():
         return
     if args.op == "pool":
         main_pool(args)
+        return
+    if args.op == "heads":
+        main_heads(args)
         return
 
     import torch
@@ -437,6 +443,125 @@ def main_pool(args):
                   "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
                   "bytes": {"E_fwd": by.e_fwd, "E_bwd": by.e_bwd, "zero_fill": by.zero,
                             "box_px": by.box_px},
+                  "kernel_source_hash": kernel_source_hash()},
+    }
+    print(json.dumps(result), flush=True)
+
+
+def main_heads(args):
+    """Box (7x7) and mask (14x14) heads on one pyramid: one step is a plan and a forward
+    per head, then roi_align_bwd_multi (both heads in one pass over the gradient
+    pyramid).  The same step with two roi_align_bwd calls is timed too."""
+    import torch
+
+    import oracle
+    import paper_1906_07155_amd as rex
+    from paper_1906_07155_amd import accounting, workloads
+
+    if args.workload == 5:
+        wb, wm = workloads.config(5, head="box"), workloads.config(5, head="mask")
+    elif args.workload == 2:
+        wb, wm = workloads.config(2), workloads.config(3)
+    else:
+        raise SystemExit("--op heads takes workload 2 or 5")
+    dev = torch.device("cuda:0")
+    bf16 = wb.feat_dtype == "bf16"
+
+    def to_dev(a, dt, cl=True):
+        if dt == "bf16":
+            t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        return t.contiguous(memory_format=torch.channels_last) if cl else t
+
+    feats_np = wb.features()
+    feats = [to_dev(f, wb.feat_dtype) for f in feats_np]
+    grads = [torch.empty(f.shape, dtype=torch.float32, device=dev).contiguous(
+        memory_format=torch.channels_last) for f in feats]
+    odt = torch.bfloat16 if wb.out_dtype == "bf16" else torch.float32
+    heads = []
+    for w in (wb, wm):
+        r_np = w.rois()
+        K = r_np.shape[0]
+        heads.append({
+            "wl": w, "rois_np": r_np, "rois": torch.from_numpy(r_np).to(dev),
+            "levels": torch.empty(K, dtype=torch.int32, device=dev),
+            "ws": torch.empty(rex.workspace_size(feats, wb.scales, K), dtype=torch.uint8,
+                              device=dev),
+            "out": torch.empty((K, wb.channels) + tuple(w.out_hw), dtype=odt, device=dev),
+            "gout": to_dev(w.grad(), w.grad_dtype, cl=False)})
+    stream = torch.cuda.current_stream()
+
+    def step(fused, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        for h in heads:
+            w = h["wl"]
+            rex.plan(feats, wb.scales, h["rois"], wb.finest_scale, levels_out=h["levels"],
+                     workspace=h["ws"])
+            rex.roi_align_fwd(feats, wb.scales, h["rois"], h["levels"], w.out_hw,
+                              w.sampling_ratio, w.aligned, out=h["out"], workspace=h["ws"])
+        if ev is not None:
+            ev[1].record(stream)
+        if fused:
+            rex.roi_align_bwd_multi(
+                [{"grad_out": h["gout"], "rois": h["rois"], "roi_levels": h["levels"],
+                  "out_size": h["wl"].out_hw, "workspace": h["ws"]} for h in heads],
+                grads, wb.scales, zero_init=True)
+        else:
+            for i, h in enumerate(heads):
+                w = h["wl"]
+                rex.roi_align_bwd(h["gout"], h["rois"], h["levels"], w.out_hw, w.sampling_ratio,
+                                  w.aligned, grads, wb.scales, zero_init=(i == 0),
+                                  workspace=h["ws"])
+        if ev is not None:
+            ev[2].record(stream)
+
+    def timed(fused, n):
+        for _ in range(max(1, args.warmup)):
+            step(fused)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for i in range(n):
+            step(fused, evs[i])
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return (t0.elapsed_time(t1) / n,
+                float(np.mean([evs[i][0].elapsed_time(evs[i][1]) for i in range(n)])),
+                float(np.mean([evs[i][1].elapsed_time(evs[i][2]) for i in range(n)])))
+
+    ms, ms_plan_fwd, ms_bwd = timed(True, args.steps)
+    alt = timed(False, max(1, args.alt_steps)) if args.alt_steps > 0 else None
+    Ktot = sum(h["rois_np"].shape[0] for h in heads)
+    s_g = 2 if wb.grad_dtype == "bf16" else 4
+    by = accounting.count(heads[0]["rois_np"], oracle.level_map(heads[0]["rois_np"], 4, 56.0),
+                          wb.level_hw, wb.scales, wb.n_images, wb.channels, (7, 7), 2, True,
+                          2 if bf16 else 4, 2 if wb.out_dtype == "bf16" else 4, s_g)
+    # the fused backward must read both upstream gradients and write every gradient once
+    gout_bytes = sum(h["gout"].numel() * s_g for h in heads)
+    bwd_bytes = gout_bytes + by.zero + 24 * Ktot
+    gbs = bwd_bytes / (ms_bwd * 1e-3) / 1e9
+    result = {
+        "metric": "RoIAlign box+mask heads fwd+bwd RoIs/sec and achieved HBM GB/s vs peak, FPN shapes",
+        "value": round(Ktot / (ms * 1e-3), 1), "unit": "RoIs/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic (seeded normal features, log-uniform RoIs; no COCO)",
+        "config": {"workload": "%s + %s on one pyramid" % (wb.name, wm.name),
+                   "num_rois": [h["rois_np"].shape[0] for h in heads], "channels": wb.channels,
+                   "levels": [list(x) for x in wb.level_hw], "out": [[7, 7], [14, 14]],
+                   "layout": "cl", "backward": True},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "roi_align_bwd_multi", "bytes_per_launch": bwd_bytes,
+                     "launch_ms": round(ms_bwd, 5)},
+        "cpu_baseline": None,
+        "extra": {"ms_plans_and_forwards": round(ms_plan_fwd, 5), "ms_fused_bwd": round(ms_bwd, 5),
+                  "separate_bwd": None if alt is None else {
+                      "ms_per_step": round(alt[0], 5), "ms_bwd": round(alt[2], 5)},
                   "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(result), flush=True)

@@ -181,6 +181,39 @@ re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype,
                           int32_t zero_init, int32_t algorithm, const void *plan,
                           size_t plan_bytes, void *stream);
 
+/* f2 -- several heads on one pyramid.  A two-stage detector extracts RoI features
+ * from the same FPN levels for more than one RoIHead (§3.1: BBoxHead and MaskHead;
+ * the cascaded heads of Cascade R-CNN and HTC, §2), and every head's backward adds
+ * into the same gradient pyramid.  One head is one upstream gradient and the RoIs
+ * it was extracted for: */
+#define RE_MAX_HEADS 8
+typedef struct {
+    const void *grad_out;     /* device [num_rois][c][out_h][out_w] of grad_out_dtype */
+    int32_t grad_out_dtype;   /* re_dtype_t */
+    int32_t out_h, out_w;
+    int32_t sampling_ratio;
+    int32_t aligned;
+    int32_t reserved;         /* must be 0 */
+    const float *rois;        /* device float[num_rois][5] */
+    int64_t num_rois;
+    const int32_t *roi_levels;/* device int32[num_rois]; NULL only with one level */
+    const void *plan;         /* roi_extract_plan workspace for these RoIs, or NULL */
+    size_t plan_bytes;
+} re_head_t;
+
+/* Backward of num_heads heads (1..RE_MAX_HEADS) into one gradient pyramid:
+ * grad_F += sum over heads of (head's transpose applied to its grad_out), after
+ * clearing when zero_init != 0; each head is defined as for roi_align_bwd.  Heads
+ * are taken in pairs: when both heads of a pair take the gather (plan, channels-last
+ * levels, 7x7 or 14x14 grid, sampling_ratio 2, one gradient dtype and one tile
+ * layout), the pair is a single pass in which every gradient element is written once;
+ * otherwise the heads run one after the other (gather or scatter, as roi_align_bwd
+ * with RE_BWD_AUTO).  Results equal the sum of the single-head calls up to the fp32
+ * summation order. */
+re_status_t roi_align_bwd_multi(const re_head_t *heads, int32_t num_heads,
+                                const re_level_t *grad_levels, int32_t num_levels,
+                                int32_t zero_init, void *stream);
+
 /* f1 -- RoI max pooling, the RoIPool of Fast R-CNN (a two-stage method of §2),
  * the other RoIPooling-like operator a RoIExtractor uses (§3.1).  On level l (scale
  * s, H x W map), every operation rounded to binary32 in this order:

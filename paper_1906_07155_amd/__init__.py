@@ -5,11 +5,11 @@ include/roi_extract.h (libroi_extract.so, built in-tree by `build.py`).  This
 package only marshals torch tensors into that ABI.
 """
 from .binding import (RoIExtractError, fpn_level_map, lib, plan, plan_offsets, plan_perm,
-                      roi_align_bwd, roi_align_fwd, roi_pool_bwd, roi_pool_fwd, workspace_size,
-                      zero_grad)
+                      roi_align_bwd, roi_align_bwd_multi, roi_align_fwd, roi_pool_bwd,
+                      roi_pool_fwd, workspace_size, zero_grad)
 
 __all__ = ["RoIExtractError", "fpn_level_map", "lib", "plan", "plan_offsets", "plan_perm",
-           "roi_align_bwd", "roi_align_fwd", "roi_pool_bwd", "roi_pool_fwd", "workspace_size",
+           "roi_align_bwd", "roi_align_bwd_multi", "roi_align_fwd", "roi_pool_bwd", "roi_pool_fwd", "workspace_size",
            "zero_grad", "roi_extract",
            "RoIAlignFunction"]
 

@@ -44,9 +44,19 @@ class ReLevel(ctypes.Structure):
                 ("reserved2", ctypes.c_float)]
 
 
+class ReHead(ctypes.Structure):
+    _fields_ = [("grad_out", ctypes.c_void_p), ("grad_out_dtype", ctypes.c_int32),
+                ("out_h", ctypes.c_int32), ("out_w", ctypes.c_int32),
+                ("sampling_ratio", ctypes.c_int32), ("aligned", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("rois", ctypes.c_void_p),
+                ("num_rois", ctypes.c_int64), ("roi_levels", ctypes.c_void_p),
+                ("plan", ctypes.c_void_p), ("plan_bytes", ctypes.c_size_t)]
+
+
 _VP, _I32, _I64, _F32, _SZ = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                               ctypes.c_size_t)
 _LEVELS = ctypes.POINTER(ReLevel)
+_HEADS = ctypes.POINTER(ReHead)
 
 SIGNATURES = {
     "fpn_level_map": [_VP, _I64, _I32, _F32, _VP, _VP],
@@ -59,6 +69,7 @@ SIGNATURES = {
     "roi_extract_zero_grad": [_LEVELS, _I32, _VP],
     "roi_align_bwd": [_VP, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _LEVELS, _I32, _I32,
                       _I32, _VP, _SZ, _VP],
+    "roi_align_bwd_multi": [_HEADS, _I32, _LEVELS, _I32, _I32, _VP],
     "roi_pool_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _VP, _I32, _VP, _VP, _SZ, _VP],
     "roi_pool_bwd": [_VP, _I32, _VP, _VP, _I64, _VP, _I32, _I32, _LEVELS, _I32, _I32, _VP, _SZ,
                      _VP],
@@ -319,4 +330,30 @@ def roi_pool_bwd(grad_out, argmax, rois, roi_levels, grads: Sequence, scales: Se
     check(lib().roi_pool_bwd(grad_out.data_ptr(), _dtype_code(grad_out), argmax.data_ptr(),
                              rois.data_ptr(), K, lv, ph, pw, arr, L, int(bool(zero_init)), ws,
                              wsb, stream_handle(stream)), "roi_pool_bwd")
+    return grads
+
+
+def roi_align_bwd_multi(heads: Sequence[dict], grads: Sequence, scales: Sequence[float],
+                        zero_init: bool = True, stream=None):
+    """Backward of several heads into one gradient pyramid (float32 levels, cleared first if
+    zero_init).  Each head is a dict with grad_out, rois, roi_levels, out_size and optionally
+    sampling_ratio (2), aligned (True) and workspace (its plan)."""
+    arr = (ReHead * max(1, len(heads)))()
+    for i, h in enumerate(heads):
+        rois = _rois(h["rois"])
+        g = h["grad_out"]
+        _need_cuda(g, "grad_out of head %d" % i)
+        if not g.is_contiguous():
+            raise ValueError("grad_out of head %d must be contiguous" % i)
+        ph, pw = h["out_size"]
+        lv = h.get("roi_levels")
+        ws = h.get("workspace")
+        arr[i] = ReHead(g.data_ptr(), _dtype_code(g), ph, pw, int(h.get("sampling_ratio", 2)),
+                        int(bool(h.get("aligned", True))), 0, rois.data_ptr(), rois.shape[0],
+                        lv.data_ptr() if lv is not None else None,
+                        ws.data_ptr() if ws is not None else None,
+                        ws.numel() if ws is not None else 0)
+    levels = level_array(grads, scales)
+    check(lib().roi_align_bwd_multi(arr, len(heads), levels, len(grads), int(bool(zero_init)),
+                                    stream_handle(stream)), "roi_align_bwd_multi")
     return grads

@@ -378,6 +378,122 @@ re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_lev
     return from_hip(launch_zero(t, numel, dense, static_cast<hipStream_t>(stream)));
 }
 
+}  // extern "C"
+
+namespace {
+
+// One head of a backward, validated.
+struct BwdHead {
+    const void *gout;
+    int32_t gdt;
+    const float *rois;
+    int64_t K;
+    const int32_t *roi_levels;
+    int32_t out_h, out_w, S, aligned;
+    const void *plan;
+    size_t plan_bytes;
+};
+
+re_status_t check_head(const BwdHead &h, int32_t num_levels, const LevelTable &t) {
+    re_status_t st;
+    if ((st = check_common(h.rois, h.K, h.roi_levels, num_levels, h.out_h, h.out_w, h.S,
+                           h.aligned)) != RE_OK)
+        return st;
+    if (!valid_dtype(h.gdt)) return RE_ERR_INVALID_ARG;
+    if (h.K > 0 && !h.gout) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(h.gout) % dtype_size(h.gdt)) return RE_ERR_INVALID_ARG;
+    return check_plan(h.plan, h.plan_bytes, h.K, t);
+}
+
+bool head_gather_ok(const BwdHead &h, const LevelTable &t, bool cl, const TileLayout &tl) {
+    return h.plan && cl && tl.ntiles > 0 && h.K > 0 && gather_available(h.out_h, h.out_w, h.S);
+}
+
+GatherHead gather_head(const BwdHead &h, const TileLayout &tl) {
+    GatherHead g{};
+    const char *ws = static_cast<const char *>(h.plan);
+    g.gout = h.gout;
+    g.rois = h.rois;
+    g.roi_levels = h.roi_levels;
+    g.tile_start = reinterpret_cast<const int32_t *>(ws + tiles_offset(h.K));
+    g.tile_rois = reinterpret_cast<const int32_t *>(ws + tile_rois_offset(h.K, tl));
+    g.K = static_cast<int32_t>(h.K);
+    g.aligned = h.aligned;
+    g.capacity = static_cast<int32_t>(tl.capacity);
+    g.PH = h.out_h;
+    g.PW = h.out_w;
+    return g;
+}
+
+GatherArgs gather_args(const LevelTable &t, const BwdHead &h0, const TileLayout &tl,
+                       int32_t zero_init) {
+    GatherArgs g{};
+    g.lv = t;
+    g.head[0] = gather_head(h0, tl);
+    g.tile_order = reinterpret_cast<const int32_t *>(static_cast<const char *>(h0.plan) +
+                                                     tile_order_offset(h0.K, tl));
+    g.nheads = 1;
+    g.PH = h0.out_h;
+    g.PW = h0.out_w;
+    g.S = h0.S;
+    g.zero_init = zero_init;
+    g.ntiles = tl.ntiles;
+    g.tile_shift = tl.shift;
+    g.qside = 1 << (tl.shift - 3);
+    g.cg_form = (h0.out_h == 7 && h0.gdt == RE_DTYPE_BF16) ? 1 : 0;
+    for (int l = 0; l < kMaxLevels; ++l) {
+        g.ntx[l] = tl.ntx[l];
+        g.nty[l] = tl.nty[l];
+        g.tbase[l] = tl.tbase[l];
+    }
+    g.tbase[kMaxLevels] = tl.tbase[kMaxLevels];
+    return g;
+}
+
+// One validated head: gather when eligible and not refused by `algorithm`, else the
+// scatter (after clearing when zero_init).
+re_status_t bwd_head(const BwdHead &h, const LevelTable &t, bool cl, const int64_t *numel,
+                     const int *dense, int32_t zero_init, int32_t algorithm, hipStream_t s) {
+    const TileLayout tl = tile_layout(t, h.K);
+    const bool gather_ok = head_gather_ok(h, t, cl, tl);
+    if (algorithm == RE_BWD_GATHER && !gather_ok && h.K > 0) return RE_ERR_UNSUPPORTED;
+    if (gather_ok && algorithm != RE_BWD_SCATTER)
+        return from_hip(launch_gather(gather_args(t, h, tl, zero_init), h.gdt, s));
+    re_status_t st;
+    if (zero_init) {
+        if ((st = from_hip(launch_zero(t, numel, dense, s))) != RE_OK) return st;
+    }
+    if (h.K == 0) return RE_OK;
+    BwdArgs a{};
+    a.lv = t;
+    a.gout = h.gout;
+    a.rois = h.rois;
+    a.roi_levels = h.roi_levels;
+    a.perm = h.plan ? reinterpret_cast<const int32_t *>(static_cast<const char *>(h.plan) +
+                                                        perm_offset())
+                    : nullptr;
+    a.K = static_cast<int32_t>(h.K);
+    a.PH = h.out_h;
+    a.PW = h.out_w;
+    a.S = h.S;
+    a.aligned = h.aligned;
+    const bool fast = cl && bwd_fast_available(h.out_h, h.out_w, h.S);
+    return from_hip(launch_bwd(a, h.gdt, fast, s));
+}
+
+re_status_t check_grad_levels(const re_level_t *grad_levels, int32_t num_levels, LevelTable *t,
+                              bool *cl, int64_t *numel, int *dense) {
+    re_status_t st = check_levels(grad_levels, num_levels, true, t, cl, numel, dense);
+    if (st != RE_OK) return st;
+    for (int l = 0; l < num_levels; ++l)
+        if (grad_levels[l].dtype != RE_DTYPE_F32) return RE_ERR_UNSUPPORTED;
+    return RE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype, const float *rois,
                           int64_t num_rois, const int32_t *roi_levels, int32_t out_h,
                           int32_t out_w, int32_t sampling_ratio, int32_t aligned,
@@ -387,77 +503,65 @@ re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype, const fl
     bool cl = false;
     int64_t numel[RE_MAX_LEVELS] = {0};
     int dense[RE_MAX_LEVELS] = {0};
-    re_status_t st = check_levels(grad_levels, num_levels, true, &t, &cl, numel, dense);
+    re_status_t st = check_grad_levels(grad_levels, num_levels, &t, &cl, numel, dense);
     if (st != RE_OK) return st;
-    for (int l = 0; l < num_levels; ++l)
-        if (grad_levels[l].dtype != RE_DTYPE_F32) return RE_ERR_UNSUPPORTED;
-    if ((st = check_common(rois, num_rois, roi_levels, num_levels, out_h, out_w,
-                           sampling_ratio, aligned)) != RE_OK)
-        return st;
-    if (!valid_dtype(grad_out_dtype)) return RE_ERR_INVALID_ARG;
-    if (num_rois > 0 && !grad_out) return RE_ERR_INVALID_ARG;
-    if (reinterpret_cast<uintptr_t>(grad_out) % dtype_size(grad_out_dtype))
-        return RE_ERR_INVALID_ARG;
+    const BwdHead h{grad_out, grad_out_dtype, rois,    num_rois, roi_levels, out_h,
+                    out_w,    sampling_ratio, aligned, plan,     plan_bytes};
+    if ((st = check_head(h, num_levels, t)) != RE_OK) return st;
     if (zero_init != 0 && zero_init != 1) return RE_ERR_INVALID_ARG;
     if (algorithm != RE_BWD_AUTO && algorithm != RE_BWD_SCATTER && algorithm != RE_BWD_GATHER)
         return RE_ERR_INVALID_ARG;
-    if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
+    return bwd_head(h, t, cl, numel, dense, zero_init, algorithm,
+                    static_cast<hipStream_t>(stream));
+}
 
-    const TileLayout tl = tile_layout(t, num_rois);
-    const bool gather_ok = plan && cl && tl.ntiles > 0 && num_rois > 0 &&
-                           gather_available(out_h, out_w, sampling_ratio);
-    if (algorithm == RE_BWD_GATHER && !gather_ok && num_rois > 0) return RE_ERR_UNSUPPORTED;
-    const bool gather = gather_ok && algorithm != RE_BWD_SCATTER;
-
+re_status_t roi_align_bwd_multi(const re_head_t *heads, int32_t num_heads,
+                                const re_level_t *grad_levels, int32_t num_levels,
+                                int32_t zero_init, void *stream) {
+    LevelTable t;
+    bool cl = false;
+    int64_t numel[RE_MAX_LEVELS] = {0};
+    int dense[RE_MAX_LEVELS] = {0};
+    re_status_t st = check_grad_levels(grad_levels, num_levels, &t, &cl, numel, dense);
+    if (st != RE_OK) return st;
+    if (!heads || num_heads < 1 || num_heads > RE_MAX_HEADS) return RE_ERR_INVALID_ARG;
+    if (zero_init != 0 && zero_init != 1) return RE_ERR_INVALID_ARG;
+    BwdHead hs[RE_MAX_HEADS];
+    for (int i = 0; i < num_heads; ++i) {
+        const re_head_t &u = heads[i];
+        if (u.reserved != 0) return RE_ERR_INVALID_ARG;
+        hs[i] = BwdHead{u.grad_out, u.grad_out_dtype, u.rois,    u.num_rois, u.roi_levels,
+                        u.out_h,    u.out_w,          u.sampling_ratio, u.aligned, u.plan,
+                        u.plan_bytes};
+        if ((st = check_head(hs[i], num_levels, t)) != RE_OK) return st;
+    }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (gather) {
-        GatherArgs g{};
-        g.lv = t;
-        g.gout = grad_out;
-        g.rois = rois;
-        g.roi_levels = roi_levels;
-        const char *ws = static_cast<const char *>(plan);
-        g.tile_start = reinterpret_cast<const int32_t *>(ws + tiles_offset(num_rois));
-        g.tile_rois = reinterpret_cast<const int32_t *>(ws + tile_rois_offset(num_rois, tl));
-        g.tile_order = reinterpret_cast<const int32_t *>(ws + tile_order_offset(num_rois, tl));
-        g.K = static_cast<int32_t>(num_rois);
-        g.PH = out_h;
-        g.PW = out_w;
-        g.S = sampling_ratio;
-        g.aligned = aligned;
-        g.zero_init = zero_init;
-        g.ntiles = tl.ntiles;
-        g.capacity = static_cast<int32_t>(tl.capacity);
-        g.tile_shift = tl.shift;
-        g.qside = 1 << (tl.shift - 3);
-        g.cg_form = (out_h == 7 && grad_out_dtype == RE_DTYPE_BF16) ? 1 : 0;
-        for (int l = 0; l < kMaxLevels; ++l) {
-            g.ntx[l] = tl.ntx[l];
-            g.nty[l] = tl.nty[l];
-            g.tbase[l] = tl.tbase[l];
+    // Heads in pairs: a pair whose heads both take the gather on the same tile layout
+    // (and one gradient dtype) is one pass over the pyramid; anything else runs head
+    // by head.  Only the first pass clears.
+    int32_t clear = zero_init;
+    for (int i = 0; i < num_heads;) {
+        if (i + 1 < num_heads) {
+            const BwdHead &a = hs[i], &b = hs[i + 1];
+            const TileLayout ta = tile_layout(t, a.K), tb = tile_layout(t, b.K);
+            if (head_gather_ok(a, t, cl, ta) && head_gather_ok(b, t, cl, tb) &&
+                ta.shift == tb.shift && ta.ntiles == tb.ntiles && a.gdt == b.gdt &&
+                a.S == b.S) {
+                GatherArgs g = gather_args(t, a, ta, clear);
+                g.head[1] = gather_head(b, tb);
+                g.nheads = 2;
+                g.gout_dtype1 = b.gdt;
+                if ((st = from_hip(launch_gather(g, a.gdt, s))) != RE_OK) return st;
+                clear = 0;
+                i += 2;
+                continue;
+            }
         }
-        g.tbase[kMaxLevels] = tl.tbase[kMaxLevels];
-        return from_hip(launch_gather(g, grad_out_dtype, s));
+        if ((st = bwd_head(hs[i], t, cl, numel, dense, clear, RE_BWD_AUTO, s)) != RE_OK) return st;
+        clear = 0;
+        ++i;
     }
-    if (zero_init) {
-        if ((st = from_hip(launch_zero(t, numel, dense, s))) != RE_OK) return st;
-    }
-    if (num_rois == 0) return RE_OK;
-    BwdArgs a{};
-    a.lv = t;
-    a.gout = grad_out;
-    a.rois = rois;
-    a.roi_levels = roi_levels;
-    a.perm = plan ? reinterpret_cast<const int32_t *>(static_cast<const char *>(plan) +
-                                                      perm_offset())
-                  : nullptr;
-    a.K = static_cast<int32_t>(num_rois);
-    a.PH = out_h;
-    a.PW = out_w;
-    a.S = sampling_ratio;
-    a.aligned = aligned;
-    const bool fast = cl && bwd_fast_available(out_h, out_w, sampling_ratio);
-    return from_hip(launch_bwd(a, grad_out_dtype, fast, s));
+    return RE_OK;
 }
 
 // ---------------------------------------------------------------------------

@@ -285,116 +285,89 @@ __device__ __forceinline__ uint32_t byte_mask(uint64_t b) {
     return static_cast<uint32_t>((b * 0x0102040810204080ull) >> 56);
 }
 
+// LDS of one head's pass over a tile (see gather_phase).
 template <typename TG, int PH, int PW, int S>
-__global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
-    constexpr int NR = PH * S;
-    constexpr int NCOL = PW * S;
-    constexpr int T = 8;                   // quadrant side
-    constexpr int NB = PH * PW;
-    constexpr int GB = 64 * NB;            // floats of one RoI's gradient block (64 channels)
-    constexpr int YP = (PH * T + 63) / 64;  // ballot passes for the row weights
-    constexpr int XP = (PW * T + 63) / 64;
+struct GatherSmem {
+    static constexpr int NR = PH * S;
+    static constexpr int NCOL = PW * S;
+    static constexpr int T = 8;
+    static constexpr int NB = PH * PW;
+    static constexpr int GB = 64 * NB;   // 32-bit words of one RoI's gradient block
     // The staged gradient blocks form a ring of NBUF: the next RoI's block is copied
     // into the other slot by the buffer unit while the current one is consumed, when
     // two blocks fit in 52 KiB.  The copy gives every lane a 32-bit LDS slot whatever
     // the element size, so a block holds one 32-bit word per element (a bf16 value in
     // its low half).
-    constexpr int GBYTES = GB * 4;
-    constexpr int NBUF = 2 * GBYTES <= 53248 ? 2 : 1;
-    constexpr int NDMA = GB / 64;           // 64-element runs of one block
+    static constexpr int NBUF = 2 * GB * 4 <= 53248 ? 2 : 1;
+    __align__(16) uint32_t g[NBUF][GB];
+    Tap tap[2][NR + NCOL];
+    __align__(16) float wy[4][PH * T];
+    __align__(16) float wx[4][PW * T];
+    int k[64];
+    float ax[64][4];
+    int rng[64][4];   // per kept RoI: tap extent ymin, ymax, xmin, xmax
+    int n;
+};
+
+// Where a workgroup of the quadrant-form gather sits: the tile's level and image,
+// its wave's quadrant and the bounding box of the workgroup's quadrants.
+struct GatherTile {
+    LevelArg L;
+    int l, b;
+    int R0, Q0;                 // this wave's quadrant
+    int WR0, WR1, WC0, WC1;     // the workgroup's region
+    int cg, nch;
+    bool wave_on;
+};
+
+// One head's RoIs binned to tile t, added into this wave's quadrant accumulators:
+//   acc[r][q] += sum over RoIs, bins: Wy[ph][r] * sum_pw Wx[pw][q] * g[ph][pw].
+// Every wave of the workgroup calls it (it holds workgroup barriers).
+template <typename TG, int PH, int PW, int S>
+__device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTable &lv, int t,
+                                             const GatherTile &x, float (&acc)[8][8],
+                                             GatherSmem<TG, PH, PW, S> &sm) {
+    using SM = GatherSmem<TG, PH, PW, S>;
+    constexpr int NR = SM::NR, NCOL = SM::NCOL, T = SM::T, NB = SM::NB, GB = SM::GB;
+    constexpr int NBUF = SM::NBUF;
+    constexpr int YP = (PH * T + 63) / 64;   // ballot passes for the row weights
+    constexpr int XP = (PW * T + 63) / 64;
+    constexpr int NDMA = GB / 64;            // 64-element runs of one block
     static_assert(GB % 64 == 0, "a copy instruction moves whole 64-element runs");
     static_assert(NR + NCOL <= 64, "taps are computed by one wavefront");
     static_assert(PH <= 32 && PW <= 32, "bin masks are 32-bit");
 
-    __shared__ __align__(16) uint32_t s_g[NBUF][GB];
-    __shared__ Tap s_tap[2][NR + NCOL];
-    __shared__ __align__(16) float s_wy[4][PH * T];
-    __shared__ __align__(16) float s_wx[4][PW * T];
-    __shared__ int s_k[64];
-    __shared__ float s_ax[64][4];
-    // per kept RoI: tap extent ymin, ymax, xmin, xmax
-    __shared__ int s_rng[64][4];
-    __shared__ int s_n;
-
     const int tid = threadIdx.x;
     const int wave = uniform_i(tid >> 6);
     const int lane = tid & 63;
-    // Blocks in dispatch order walk the tiles longest list first (plan order); the
-    // channel groups and quadrant blocks of one tile are adjacent.
-    const int lid = static_cast<int>(blockIdx.x);
-    const int per_tile = a.ncg * a.wg_per_tile;
-    const int rank = lid / per_tile;
-    const int rem = lid - rank * per_tile;
-    const int cg = rem / a.wg_per_tile;
-    int t = a.tile_order[rank];
-    t = max(0, min(t, a.ntiles - 1));
-    const int quad0 = (rem - cg * a.wg_per_tile) * 4;
-    const int quad = quad0 + wave;
-
-    int l = 0;
-#pragma unroll
-    for (int i = 1; i < kMaxLevels; ++i)
-        if (i < a.lv.num && t >= a.tbase[i]) l = i;
-    const LevelArg L = level_at(a.lv, l);
-    const int ntx = pick(a.ntx, l);
-    const int per_img = pick(a.nty, l) * ntx;
-    const int local = t - pick(a.tbase, l);
-    const int b = local / per_img;
-    const int rt = local - b * per_img;
-    const int ty = rt / ntx;
-    const int tx = rt - ty * ntx;
-    const int qs = a.qside;
-    const int R0 = (ty << a.tile_shift) + (quad / qs) * T;
-    const int Q0 = (tx << a.tile_shift) + (quad % qs) * T;
-    // Waves whose quadrant is off the map still take part in staging and barriers.
-    const bool wave_on = quad < qs * qs && R0 < L.H && Q0 < L.W;
-    // The workgroup's region: the bounding box of its (up to 4) quadrants.
-    const int qlast = min(quad0 + 3, qs * qs - 1);
-    const int WR0 = (ty << a.tile_shift) + (quad0 / qs) * T;
-    const int WR1 = (ty << a.tile_shift) + (qlast / qs) * T + T;
-    const int WC0 = (tx << a.tile_shift) + ((qlast / qs > quad0 / qs) ? 0 : (quad0 % qs)) * T;
-    const int WC1 = (tx << a.tile_shift) + ((qlast / qs > quad0 / qs) ? qs : (qlast % qs) + 1) * T;
-
-    const int c = cg * 64 + lane;
-    const bool lane_on = c < a.lv.C;
-    const int nch = min(64, a.lv.C - cg * 64);
-    float acc[T][T];
-#pragma unroll
-    for (int r = 0; r < T; ++r)
-#pragma unroll
-        for (int q = 0; q < T; ++q) acc[r][q] = 0.0f;
-
-    int s0 = a.tile_start[t];
-    int s1 = a.tile_start[t + 1];
-    s0 = max(0, min(s0, a.capacity));
-    s1 = max(s0, min(s1, a.capacity));
+    const LevelArg &L = x.L;
+    const int l = x.l, b = x.b, R0 = x.R0, Q0 = x.Q0;
+    int s0 = h.tile_start[t];
+    int s1 = h.tile_start[t + 1];
+    s0 = max(0, min(s0, h.capacity));
+    s1 = max(s0, min(s1, h.capacity));
     constexpr float inv_count = 1.0f / static_cast<float>(S * S);
-    float *wy = s_wy[wave];
-    float *wx = s_wx[wave];
-    const int64_t kstride = static_cast<int64_t>(a.lv.C) * NB;
+    float *wy = sm.wy[wave];
+    float *wx = sm.wx[wave];
+    const int64_t kstride = static_cast<int64_t>(lv.C) * NB;
 
-    // Coalesced copy of kept RoI j's gradient block (nch x NB values) into
-    // registers / LDS through a buffer resource over exactly that block: element
-    // tid + 256 m sits at lane offset tid and a constant scalar offset, and the range
-    // check supplies the zeros past the valid channels.
-    const int nvalid = nch * NB;
-    auto block_rsrc = [&](int j) {
-        const int k = uniform_i(s_k[j]);   // one resource for the wave, no waterfall
-        const char *src = static_cast<const char *>(a.gout) +
-                          (static_cast<int64_t>(cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
-                              int64_t(sizeof(TG));
-        return make_rsrc(src, static_cast<uint32_t>(nvalid) * uint32_t(sizeof(TG)));
-    };
-    // Direct buffer-to-LDS copy: run r = wave + 4 m of the block goes to LDS words
-    // [buf][64 r, 64 r + 64), lane i writing element 64 r + i (the LDS address is the
-    // uniform run base plus 4 bytes per lane, the global offset the lane's own).
+    // Coalesced copy of kept RoI j's gradient block (nch x NB values) into LDS
+    // through a buffer resource over exactly that block: run r = wave + 4 m goes to
+    // words [64 r, 64 r + 64), lane i writing element 64 r + i (the LDS address is the
+    // uniform run base plus 4 bytes per lane, the global offset the lane's own); the
+    // range check supplies the zeros past the valid channels.
+    const int nvalid = x.nch * NB;
     auto fetch = [&](int j, int buf) {
-        const __amdgpu_buffer_rsrc_t rs = block_rsrc(j);
+        const int k = uniform_i(sm.k[j]);   // one resource for the wave, no waterfall
+        const char *src = static_cast<const char *>(h.gout) +
+                          (static_cast<int64_t>(x.cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
+                              int64_t(sizeof(TG));
+        const __amdgpu_buffer_rsrc_t rs = make_rsrc(src, static_cast<uint32_t>(nvalid) * uint32_t(sizeof(TG)));
 #pragma unroll
         for (int m = 0; m < (NDMA + 3) / 4; ++m) {
             const int run = wave + 4 * m;
             if (m < NDMA / 4 || run < NDMA) {
-                auto *dst = (__attribute__((address_space(3))) void *)(&s_g[buf][64 * run]);
+                auto *dst = (__attribute__((address_space(3))) void *)(&sm.g[buf][64 * run]);
                 const uint32_t off = static_cast<uint32_t>(64 * run + lane) * uint32_t(sizeof(TG));
                 if constexpr (sizeof(TG) == 4)
                     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 4, off, 0, 0, 0);
@@ -411,21 +384,21 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
             Axis ax;
             ax.grid = S;
             if (tid < NR) {
-                ax.start = s_ax[j][2];
-                ax.bin = s_ax[j][3];
-                s_tap[tb][tid] = axis_tap(ax, tid / S, tid % S, L.H);
+                ax.start = sm.ax[j][2];
+                ax.bin = sm.ax[j][3];
+                sm.tap[tb][tid] = axis_tap(ax, tid / S, tid % S, L.H);
             } else {
-                ax.start = s_ax[j][0];
-                ax.bin = s_ax[j][1];
-                s_tap[tb][tid] = axis_tap(ax, (tid - NR) / S, (tid - NR) % S, L.W);
+                ax.start = sm.ax[j][0];
+                ax.bin = sm.ax[j][1];
+                sm.tap[tb][tid] = axis_tap(ax, (tid - NR) / S, (tid - NR) % S, L.W);
             }
         }
     };
     // Contribution of kept RoI j to this wave's quadrant.
     auto consume = [&](int j, int buf, int tb) {
-        const int ymin = s_rng[j][0], ymax = s_rng[j][1];
-        const int xmin = s_rng[j][2], xmax = s_rng[j][3];
-        if (!wave_on || ymax < R0 || ymin >= R0 + T || xmax < Q0 || xmin >= Q0 + T) return;
+        const int ymin = sm.rng[j][0], ymax = sm.rng[j][1];
+        const int xmin = sm.rng[j][2], xmax = sm.rng[j][3];
+        if (!x.wave_on || ymax < R0 || ymin >= R0 + T || xmax < Q0 || xmin >= Q0 + T) return;
         // This quadrant's separable weights and which bin rows / columns reach it.
         uint32_t ymask = 0, xmask = 0;
 #pragma unroll
@@ -438,7 +411,7 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
                 float w = 0.0f;
 #pragma unroll
                 for (int iy = 0; iy < S; ++iy) {
-                    const Tap tp = s_tap[tb][ph * S + iy];
+                    const Tap tp = sm.tap[tb][ph * S + iy];
                     if (tp.lo >= 0) {
                         if (tp.lo == R) {
                             w += tp.wlo;
@@ -464,7 +437,7 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
                 float w = 0.0f;
 #pragma unroll
                 for (int ix = 0; ix < S; ++ix) {
-                    const Tap tp = s_tap[tb][NR + pw * S + ix];
+                    const Tap tp = sm.tap[tb][NR + pw * S + ix];
                     if (tp.lo >= 0) {
                         if (tp.lo == Q) {
                             w += tp.wlo;
@@ -482,7 +455,7 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
         }
         wave_sync();
 
-        const uint32_t *gl = s_g[buf] + lane * NB;   // this lane's channel, stride NB (odd)
+        const uint32_t *gl = sm.g[buf] + lane * NB;   // this lane's channel, stride NB (odd)
         for (uint32_t ym = ymask; ym; ym &= ym - 1) {
             const int ph = __builtin_ctz(ym);
             float X[T];
@@ -524,14 +497,14 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
             int k = 0, ymin = INT32_MAX, ymax = -1, xmin = INT32_MAX, xmax = -1;
             float ax_s = 0.0f, ax_b = 0.0f, ay_s = 0.0f, ay_b = 0.0f;
             if (lane < n) {
-                k = a.tile_rois[base + lane];
-                if (k >= 0 && k < a.K) {
-                    const float *r = a.rois + 5 * static_cast<int64_t>(k);
+                k = h.tile_rois[base + lane];
+                if (k >= 0 && k < h.K) {
+                    const float *r = h.rois + 5 * static_cast<int64_t>(k);
                     const float r0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
-                    const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
-                    if (lvl == l && roi_batch(r0, a.lv.N) == b) {
-                        const Axis ax = axis_setup(x1, x2, L.scale, a.aligned, PW, S);
-                        const Axis ay = axis_setup(y1, y2, L.scale, a.aligned, PH, S);
+                    const int lvl = h.roi_levels ? h.roi_levels[k] : 0;
+                    if (lvl == l && roi_batch(r0, lv.N) == b) {
+                        const Axis ax = axis_setup(x1, x2, L.scale, h.aligned, PW, S);
+                        const Axis ay = axis_setup(y1, y2, L.scale, h.aligned, PH, S);
                         ax_s = ax.start;
                         ax_b = ax.bin;
                         ay_s = ay.start;
@@ -547,8 +520,8 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
                         ymax = ly.lo >= 0 ? ly.hi : L.H - 1;
                         xmin = fx.lo >= 0 ? fx.lo : 0;
                         xmax = lx.lo >= 0 ? lx.hi : L.W - 1;
-                        const bool yhit = ymax >= WR0 && ymin < WR1;
-                        const bool xhit = xmax >= WC0 && xmin < WC1;
+                        const bool yhit = ymax >= x.WR0 && ymin < x.WR1;
+                        const bool xhit = xmax >= x.WC0 && xmin < x.WC1;
                         keep = yhit && xhit;
                     }
                 }
@@ -558,20 +531,20 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
                 const int pos = static_cast<int>(__builtin_amdgcn_mbcnt_hi(
                     static_cast<uint32_t>(km >> 32),
                     __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(km), 0u)));
-                s_k[pos] = k;
-                s_ax[pos][0] = ax_s;
-                s_ax[pos][1] = ax_b;
-                s_ax[pos][2] = ay_s;
-                s_ax[pos][3] = ay_b;
-                s_rng[pos][0] = ymin;
-                s_rng[pos][1] = ymax;
-                s_rng[pos][2] = xmin;
-                s_rng[pos][3] = xmax;
+                sm.k[pos] = k;
+                sm.ax[pos][0] = ax_s;
+                sm.ax[pos][1] = ax_b;
+                sm.ax[pos][2] = ay_s;
+                sm.ax[pos][3] = ay_b;
+                sm.rng[pos][0] = ymin;
+                sm.rng[pos][1] = ymax;
+                sm.rng[pos][2] = xmin;
+                sm.rng[pos][3] = xmax;
             }
-            if (lane == 0) s_n = __builtin_popcountll(km);
+            if (lane == 0) sm.n = __builtin_popcountll(km);
         }
         __syncthreads();
-        const int nk = s_n;
+        const int nk = sm.n;
         if (nk == 0) continue;
         if constexpr (NBUF == 2) {
             fetch(0, 0);
@@ -599,32 +572,123 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
             }
         }
     }
+}
 
-    // Every pixel of the quadrant is written once (the clearing is fused).  The
-    // pixel offset is the same for the whole wave (scalar), the channel offset is the
-    // lane's; lanes past the last channel write out of range, which is dropped.  The
-    // gradient pyramid is far larger than the L2 and read only by a later pass, so
-    // the stores are non-temporal: they stream to memory instead of evicting cached
-    // data.
-    if (!wave_on) return;
-    const char *img = static_cast<const char *>(L.data) + static_cast<int64_t>(b) * L.sn * 4;
+// Decodes a quadrant-form workgroup: blocks in dispatch order walk the tiles in
+// `order` (longest list first); the channel groups and quadrant blocks of one tile
+// are adjacent.
+__device__ __forceinline__ int gather_tile(const GatherArgs &a, const int32_t *order,
+                                           GatherTile &x) {
+    const int tid = threadIdx.x;
+    const int wave = uniform_i(tid >> 6);
+    const int lid = static_cast<int>(blockIdx.x);
+    const int per_tile = a.ncg * a.wg_per_tile;
+    const int rank = lid / per_tile;
+    const int rem = lid - rank * per_tile;
+    const int cg = rem / a.wg_per_tile;
+    int t = order[rank];
+    t = max(0, min(t, a.ntiles - 1));
+    const int quad0 = (rem - cg * a.wg_per_tile) * 4;
+    const int quad = quad0 + wave;
+
+    int l = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxLevels; ++i)
+        if (i < a.lv.num && t >= a.tbase[i]) l = i;
+    x.L = level_at(a.lv, l);
+    x.l = l;
+    const int ntx = pick(a.ntx, l);
+    const int per_img = pick(a.nty, l) * ntx;
+    const int local = t - pick(a.tbase, l);
+    x.b = local / per_img;
+    const int rt = local - x.b * per_img;
+    const int ty = rt / ntx;
+    const int tx = rt - ty * ntx;
+    const int qs = a.qside;
+    x.R0 = (ty << a.tile_shift) + (quad / qs) * 8;
+    x.Q0 = (tx << a.tile_shift) + (quad % qs) * 8;
+    // Waves whose quadrant is off the map still take part in staging and barriers.
+    x.wave_on = quad < qs * qs && x.R0 < x.L.H && x.Q0 < x.L.W;
+    // The workgroup's region: the bounding box of its (up to 4) quadrants.
+    const int qlast = min(quad0 + 3, qs * qs - 1);
+    x.WR0 = (ty << a.tile_shift) + (quad0 / qs) * 8;
+    x.WR1 = (ty << a.tile_shift) + (qlast / qs) * 8 + 8;
+    x.WC0 = (tx << a.tile_shift) + ((qlast / qs > quad0 / qs) ? 0 : (quad0 % qs)) * 8;
+    x.WC1 = (tx << a.tile_shift) + ((qlast / qs > quad0 / qs) ? qs : (qlast % qs) + 1) * 8;
+    x.cg = cg;
+    x.nch = min(64, a.lv.C - cg * 64);
+    return t;
+}
+
+// Every pixel of this wave's quadrant is written once (the clearing is fused).  The
+// pixel offset is the same for the whole wave (scalar), the channel offset is the
+// lane's; lanes past the last channel write out of range, which is dropped.  The
+// gradient pyramid is far larger than the L2 and read only by a later pass, so the
+// stores are non-temporal: they stream to memory instead of evicting cached data.
+__device__ __forceinline__ void gather_store(const GatherTile &x, int zero_init,
+                                             const float (&acc)[8][8]) {
+    if (!x.wave_on) return;
+    const int lane = threadIdx.x & 63;
+    const int c = x.cg * 64 + lane;
+    const bool lane_on = lane < x.nch;
+    const LevelArg &L = x.L;
+    const char *img = static_cast<const char *>(L.data) + static_cast<int64_t>(x.b) * L.sn * 4;
     const __amdgpu_buffer_rsrc_t dst = make_rsrc(img, L.img_bytes);
     const uint32_t vo = lane_on ? static_cast<uint32_t>(c) * 4u : kBufOOB;
     const uint32_t sh4 = static_cast<uint32_t>(L.sh) * 4u;
     const uint32_t sw4 = static_cast<uint32_t>(L.sw) * 4u;
 #pragma unroll
-    for (int rr = 0; rr < T; ++rr) {
-        if (R0 + rr >= L.H) break;
-        const uint32_t rowo = static_cast<uint32_t>(R0 + rr) * sh4 + static_cast<uint32_t>(Q0) * sw4;
+    for (int rr = 0; rr < 8; ++rr) {
+        if (x.R0 + rr >= L.H) break;
+        const uint32_t rowo =
+            static_cast<uint32_t>(x.R0 + rr) * sh4 + static_cast<uint32_t>(x.Q0) * sw4;
 #pragma unroll
-        for (int q = 0; q < T; ++q) {
-            if (Q0 + q >= L.W) break;
+        for (int q = 0; q < 8; ++q) {
+            if (x.Q0 + q >= L.W) break;
             const uint32_t so = rowo + static_cast<uint32_t>(q) * sw4;
             float v = acc[rr][q];
-            if (!a.zero_init) v += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dst, vo, so, 0));
+            if (!zero_init) v += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dst, vo, so, 0));
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), dst, vo, so, kStoreNT);
         }
     }
+}
+
+template <typename TG, int PH, int PW, int S>
+__global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
+    __shared__ GatherSmem<TG, PH, PW, S> sm;
+    GatherTile x;
+    const int t = gather_tile(a, a.tile_order, x);
+    float acc[8][8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[r][q] = 0.0f;
+    gather_phase<TG, PH, PW, S>(a.head[0], a.lv, t, x, acc, sm);
+    gather_store(x, a.zero_init, acc);
+}
+
+// Two heads on one pyramid (e.g. the 7x7 box head and the 14x14 mask head of a Mask
+// R-CNN step): the workgroup walks head 0's RoIs of its tile, then head 1's, into the
+// same accumulators, and writes every gradient element once.  Tiles follow head 0's
+// order.
+template <typename TG, int PH0, int PW0, int PH1, int PW1>
+__global__ __launch_bounds__(256) void bwd_gather2_kernel(GatherArgs a) {
+    union Smem {
+        GatherSmem<TG, PH0, PW0, 2> h0;
+        GatherSmem<TG, PH1, PW1, 2> h1;
+    };
+    __shared__ Smem sm;
+    GatherTile x;
+    const int t = gather_tile(a, a.tile_order, x);
+    float acc[8][8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[r][q] = 0.0f;
+    gather_phase<TG, PH0, PW0, 2>(a.head[0], a.lv, t, x, acc, sm.h0);
+    __syncthreads();   // head 0's LDS is no longer read
+    gather_phase<TG, PH1, PW1, 2>(a.head[1], a.lv, t, x, acc, sm.h1);
+    gather_store(x, a.zero_init, acc);
 }
 
 // ---------------------------------------------------------------------------
@@ -716,10 +780,10 @@ __global__ __launch_bounds__(256) void bwd_gather_cg_kernel(GatherArgs a) {
 #pragma unroll
         for (int q = 0; q < T; ++q) acc[r][q] = 0.0f;
 
-    int s0 = a.tile_start[t];
-    int s1 = a.tile_start[t + 1];
-    s0 = max(0, min(s0, a.capacity));
-    s1 = max(s0, min(s1, a.capacity));
+    int s0 = a.head[0].tile_start[t];
+    int s1 = a.head[0].tile_start[t + 1];
+    s0 = max(0, min(s0, a.head[0].capacity));
+    s1 = max(s0, min(s1, a.head[0].capacity));
     constexpr float inv_count = 1.0f / static_cast<float>(S * S);
     const int64_t kstride = static_cast<int64_t>(a.lv.C) * NB;
     const uint32_t nvalid_bytes = static_cast<uint32_t>(nch * NB) * uint32_t(sizeof(TG));
@@ -736,7 +800,7 @@ __global__ __launch_bounds__(256) void bwd_gather_cg_kernel(GatherArgs a) {
     uint32_t pf_last = 0;
     auto fetch = [&](int j) {
         const int k = uniform_i(s_k[j]);
-        const char *src = static_cast<const char *>(a.gout) +
+        const char *src = static_cast<const char *>(a.head[0].gout) +
                           (static_cast<int64_t>(cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
                               int64_t(sizeof(TG));
         const __amdgpu_buffer_rsrc_t rs = make_rsrc(src, nvalid_bytes);
@@ -862,14 +926,14 @@ __global__ __launch_bounds__(256) void bwd_gather_cg_kernel(GatherArgs a) {
             int k = 0;
             float ax_s = 0.0f, ax_b = 0.0f, ay_s = 0.0f, ay_b = 0.0f;
             if (lane < n) {
-                k = a.tile_rois[base + lane];
-                if (k >= 0 && k < a.K) {
-                    const float *r = a.rois + 5 * static_cast<int64_t>(k);
+                k = a.head[0].tile_rois[base + lane];
+                if (k >= 0 && k < a.head[0].K) {
+                    const float *r = a.head[0].rois + 5 * static_cast<int64_t>(k);
                     const float r0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
-                    const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
+                    const int lvl = a.head[0].roi_levels ? a.head[0].roi_levels[k] : 0;
                     if (lvl == l && roi_batch(r0, a.lv.N) == b) {
-                        const Axis ax = axis_setup(x1, x2, L.scale, a.aligned, PW, S);
-                        const Axis ay = axis_setup(y1, y2, L.scale, a.aligned, PH, S);
+                        const Axis ax = axis_setup(x1, x2, L.scale, a.head[0].aligned, PW, S);
+                        const Axis ay = axis_setup(y1, y2, L.scale, a.head[0].aligned, PH, S);
                         ax_s = ax.start;
                         ax_b = ax.bin;
                         ay_s = ay.start;
@@ -946,6 +1010,19 @@ bool gather_available(int PH, int PW, int S) {
     return S == 2 && ((PH == 7 && PW == 7) || (PH == 14 && PW == 14));
 }
 
+template <typename TG>
+static void launch_gather2_typed(const GatherArgs &a, uint32_t g, hipStream_t stream) {
+    const bool b0 = a.PH == 7, b1 = a.head[1].PH == 7;
+    if (b0 && b1)
+        bwd_gather2_kernel<TG, 7, 7, 7, 7><<<g, 256, 0, stream>>>(a);
+    else if (b0)
+        bwd_gather2_kernel<TG, 7, 7, 14, 14><<<g, 256, 0, stream>>>(a);
+    else if (b1)
+        bwd_gather2_kernel<TG, 14, 14, 7, 7><<<g, 256, 0, stream>>>(a);
+    else
+        bwd_gather2_kernel<TG, 14, 14, 14, 14><<<g, 256, 0, stream>>>(a);
+}
+
 hipError_t launch_gather(GatherArgs a, int gout_dtype, hipStream_t stream) {
     a.ncg = (a.lv.C + 63) / 64;
     a.wg_per_tile = (a.qside * a.qside + 3) / 4;
@@ -953,6 +1030,14 @@ hipError_t launch_gather(GatherArgs a, int gout_dtype, hipStream_t stream) {
     if (grid <= 0) return hipSuccess;
     if (grid >= (int64_t(1) << 24)) return hipErrorInvalidConfiguration;
     const uint32_t g = static_cast<uint32_t>(grid);
+    if (a.nheads == 2) {
+        // both heads' gradients have one dtype here (the host checks it)
+        if (gout_dtype == kF32)
+            launch_gather2_typed<float>(a, g, stream);
+        else
+            launch_gather2_typed<uint16_t>(a, g, stream);
+        return hipGetLastError();
+    }
     if (a.PH == 7 && a.cg_form && gout_dtype == kBF16) {
         const int64_t gq = (static_cast<int64_t>(a.ntiles) + 7) / 8 * 8 * a.qside * a.qside *
                            ((a.ncg + 3) / 4);

@@ -51,26 +51,35 @@ struct TileLayout {
     int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
 };
 
-struct GatherArgs {
-    LevelTable lv;               // gradient levels (binary32, channels-last)
-    const void *gout;
+// One head's RoIs for the gather backward (its upstream gradient and its plan).
+struct GatherHead {
+    const void *gout;            // [K][C][PH][PW]
     const float *rois;
     const int32_t *roi_levels;
-    const int32_t *tile_start;
+    const int32_t *tile_start;   // the head's plan: CSR tile -> RoI lists
     const int32_t *tile_rois;
-    const int32_t *tile_order;
     int32_t K;
-    int32_t PH, PW, S;
     int32_t aligned;
+    int32_t capacity;
+    int32_t PH, PW;
+    int32_t pad;
+};
+
+struct GatherArgs {
+    LevelTable lv;               // gradient levels (binary32, channels-last)
+    GatherHead head[2];          // head 1 is used by the two-head kernel only
+    const int32_t *tile_order;   // head 0's plan: tiles by decreasing list length
+    int32_t nheads;
+    int32_t PH, PW, S;           // head 0's grid (both heads sample with S)
     int32_t zero_init;
     int32_t ntiles;
-    int32_t capacity;
     int32_t tile_shift;
     int32_t qside;               // 8x8 quadrants per bin-tile side
     int32_t ncg;                 // 64-channel groups
     int32_t wg_per_tile;
     int32_t cg_form;             // 1: workgroup = 4 channel groups of one quadrant
-                                 //    (bf16 upstream gradient, 7x7)
+                                 //    (bf16 upstream gradient, 7x7, one head)
+    int32_t gout_dtype1;         // head 1's upstream-gradient dtype
     int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
 };
 

@@ -224,3 +224,31 @@ def test_pool_backward_validation(L):
     assert _pbwd(L, oh=0) == INVALID
     assert _pbwd(L, plan=FAKE, plan_bytes=8) == WORKSPACE
     assert _pbwd(L, K=0, zero=0) == OK                             # nothing to do
+
+
+def _head(gout=FAKE, gdt=0, K=4, oh=7, ow=7, sr=2, al=1, reserved=0, plan=None, plan_bytes=0,
+          rois=FAKE, roi_levels=FAKE):
+    return B.ReHead(gout, gdt, oh, ow, sr, al, reserved, rois, K, roi_levels, plan, plan_bytes)
+
+
+def _multi(L, heads, nl=2, zero=0, levels=None, n=None):
+    levels = levels if levels is not None else _levels()
+    arr = (B.ReHead * max(1, len(heads)))(*heads)
+    return L.roi_align_bwd_multi(arr, len(heads) if n is None else n, levels, nl, zero, None)
+
+
+def test_multi_head_backward_validation(L):
+    assert _multi(L, [_head(K=0)]) == OK                           # nothing to do
+    assert _multi(L, [_head(K=0), _head(K=0, oh=14, ow=14)]) == OK
+    assert _multi(L, [_head()], n=0) == INVALID
+    assert _multi(L, [_head()] * 9) == INVALID                     # more than RE_MAX_HEADS
+    assert L.roi_align_bwd_multi(None, 1, _levels(), 2, 0, None) == INVALID
+    assert _multi(L, [_head(), _head(reserved=1)]) == INVALID
+    assert _multi(L, [_head(), _head(gout=None)]) == INVALID
+    assert _multi(L, [_head(), _head(gdt=5)]) == INVALID
+    assert _multi(L, [_head(), _head(oh=0)]) == INVALID
+    assert _multi(L, [_head(), _head(sr=-1)]) == INVALID
+    assert _multi(L, [_head(), _head(roi_levels=None)]) == INVALID  # several levels
+    assert _multi(L, [_head(plan=FAKE, plan_bytes=8)]) == WORKSPACE
+    assert _multi(L, [_head()], zero=3) == INVALID
+    assert _multi(L, [_head()], levels=_levels(dtype=1)) == UNSUPPORTED   # fp32 gradients only
