@@ -1,4 +1,5 @@
-"""CPU oracle for multi-level RoIAlign and RoI max pooling -- TEST INFRASTRUCTURE ONLY.
+"""CPU oracle for multi-level RoIAlign, RoI max pooling and deformable RoI pooling --
+TEST INFRASTRUCTURE ONLY.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product path never does, and this
@@ -77,6 +78,18 @@ def _bind(lib):
                                         ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32,
                                         ctypes.c_int32]
     lib.oracle_roi_pool_bwd.restype = None
+    lib.oracle_deform_roi_pool_fwd.argtypes = [
+        f64pp, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+        ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
+        ctypes.c_void_p]
+    lib.oracle_deform_roi_pool_fwd.restype = None
+    lib.oracle_deform_roi_pool_bwd.argtypes = [
+        ctypes.c_void_p, f64pp, f64pp, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
+        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.oracle_deform_roi_pool_bwd.restype = None
     return lib
 
 
@@ -216,3 +229,66 @@ def roi_pool_bwd(grad_out, argmax, shapes, rois, roi_levels, lib=None) -> list:
     lib.oracle_roi_pool_bwd(_ptr(g), _ptr(am), arr, _ptr(dims), len(grads), _ptr(r), K,
                             None if lv is None else _ptr(lv), int(g.shape[2]), int(g.shape[3]))
     return grads
+
+
+def _deform_args(rois, roi_levels, offset, mask, out_h, out_w):
+    r = _rois(rois)
+    K = r.shape[0]
+    off = np.ascontiguousarray(offset, dtype=np.float32)
+    if off.shape != (K, 2, out_h, out_w):
+        raise ValueError("offset must be [K, 2, out_h, out_w]")
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.float32)
+    if m is not None and m.shape != (K, out_h, out_w):
+        raise ValueError("mask must be [K, out_h, out_w]")
+    lv = None if roi_levels is None else np.ascontiguousarray(roi_levels, dtype=np.int32)
+    return r, K, off, m, lv
+
+
+def deform_roi_pool_fwd(features, scales, rois, roi_levels, out_h: int, out_w: int,
+                        sampling_ratio: int, aligned: bool, offset, mask=None,
+                        gamma: float = 0.1, mode: str = "parity", lib=None) -> np.ndarray:
+    """Deformable (modulated when `mask` is given) RoI pooling: RoIAlign bins shifted by
+    gamma * offset * box length and scaled by the mask.  offset [K, 2, out_h, out_w]
+    (x then y, normalized), mask [K, out_h, out_w] or None.  Returns float64 [K, C, ...]."""
+    lib = lib or load()
+    feats = [np.ascontiguousarray(f, dtype=np.float64) for f in features]
+    dims, sc = _level_args([f.shape for f in feats], scales)
+    r, K, off, m, lv = _deform_args(rois, roi_levels, offset, mask, out_h, out_w)
+    out = np.zeros((K, feats[0].shape[1], out_h, out_w), dtype=np.float64)
+    arr = (ctypes.c_void_p * len(feats))(*[f.ctypes.data for f in feats])
+    lib.oracle_deform_roi_pool_fwd(arr, _ptr(dims), _ptr(sc), len(feats), _ptr(r), K,
+                                   None if lv is None else _ptr(lv), int(out_h), int(out_w),
+                                   int(sampling_ratio), int(bool(aligned)), _ptr(off),
+                                   None if m is None else _ptr(m), float(gamma), _MODES[mode],
+                                   _ptr(out))
+    return out
+
+
+def deform_roi_pool_bwd(grad_out, features, scales, rois, roi_levels, out_h: int, out_w: int,
+                        sampling_ratio: int, aligned: bool, offset, mask=None,
+                        gamma: float = 0.1, mode: str = "parity", lib=None):
+    """Gradients of deform_roi_pool_fwd.  Returns (feature gradients per level, grad_offset
+    [K, 2, out_h, out_w], grad_mask [K, out_h, out_w] or None, and the absolute-value sums
+    scale_offset, scale_mask of the same shapes)."""
+    lib = lib or load()
+    feats = [np.ascontiguousarray(f, dtype=np.float64) for f in features]
+    shapes = [f.shape for f in feats]
+    dims, sc = _level_args(shapes, scales)
+    r, K, off, m, lv = _deform_args(rois, roi_levels, offset, mask, out_h, out_w)
+    g = np.ascontiguousarray(grad_out, dtype=np.float64)
+    if g.shape != (K, shapes[0][1], out_h, out_w):
+        raise ValueError("grad_out must be [K, C, out_h, out_w]")
+    grads = [np.zeros(s, dtype=np.float64) for s in shapes]
+    goff = np.zeros((K, 2, out_h, out_w), dtype=np.float64)
+    soff = np.zeros_like(goff)
+    gm = np.zeros((K, out_h, out_w), dtype=np.float64) if m is not None else None
+    sm = np.zeros((K, out_h, out_w), dtype=np.float64) if m is not None else None
+    farr = (ctypes.c_void_p * len(feats))(*[f.ctypes.data for f in feats])
+    garr = (ctypes.c_void_p * len(grads))(*[x.ctypes.data for x in grads])
+    lib.oracle_deform_roi_pool_bwd(_ptr(g), farr, garr, _ptr(dims), _ptr(sc), len(feats), _ptr(r),
+                                   K, None if lv is None else _ptr(lv), int(out_h), int(out_w),
+                                   int(sampling_ratio), int(bool(aligned)), _ptr(off),
+                                   None if m is None else _ptr(m), float(gamma), _MODES[mode],
+                                   _ptr(goff), None if gm is None else _ptr(gm), _ptr(soff),
+                                   None if sm is None else _ptr(sm))
+    return grads, goff, gm, soff, sm

@@ -1,5 +1,6 @@
 /*
- * roi_oracle.c -- plain CPU oracle for multi-level RoIAlign (and RoI max pooling).
+ * roi_oracle.c -- plain CPU oracle for multi-level RoIAlign (and RoI max pooling,
+ * deformable RoI pooling).
  *
  * TEST INFRASTRUCTURE ONLY.  This library exists so that the GPU library can be
  * checked against something slow and obviously correct.  Only the test suite,
@@ -17,6 +18,9 @@
  *   - The same sections list RoIPool (Fast R-CNN's max pooling over quantized
  *     bins) among the RoIPooling-like extractors; oracle_roi_pool_fwd/bwd below
  *     follow its usual definition.
+ *   - §2 also lists DCN (deformable RoI pooling) and DCNv2 (its modulated form):
+ *     oracle_deform_roi_pool_fwd/bwd move every RoIAlign bin by a learned offset
+ *     and scale it by a learned modulation; the definition is written above them.
  *   The paper does not spell the operator out.  The definition below is the
  *   standard one (bilinear sampling on a regular grid inside each bin, averaged),
  *   and every convention the paper leaves open is fixed the same way as in the
@@ -122,6 +126,8 @@ typedef struct {
     double start_d, bin_d;   /* MODE_MATH */
     float start_f, bin_f;    /* MODE_PARITY */
     int grid;                /* samples per bin along this axis */
+    double len_d;            /* box length on the level (after the minimum size) */
+    float len_f;
 } axis_geom;
 
 static int grid_from_bin(int sampling_ratio, double bin)
@@ -154,6 +160,8 @@ static axis_geom axis_setup(int mode, float c1, float c2, float scale, int align
         if (!aligned)
             len = fmaxf(len, 1.0f);
         float bin = len / (float)P;
+        g.len_f = len;
+        g.len_d = (double)len;
         g.start_f = s;
         g.bin_f = bin;
         g.start_d = (double)s;
@@ -167,6 +175,7 @@ static axis_geom axis_setup(int mode, float c1, float c2, float scale, int align
         if (!aligned)
             len = fmax(len, 1.0);
         double bin = len / (double)P;
+        g.len_d = len;
         g.start_d = s;
         g.bin_d = bin;
         g.grid = grid_from_bin(sampling_ratio, bin);
@@ -469,6 +478,320 @@ void oracle_roi_pool_bwd(const double *grad_out, const int32_t *argmax,
                 const int64_t i = (k * C + c) * PH * PW + e;
                 if (argmax[i] >= 0 && argmax[i] < H * W)
                     G[argmax[i]] += grad_out[i];
+            }
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Deformable RoI pooling -- DCN's deformable RoI pooling and its modulated    */
+/* form from DCNv2, listed among the general modules of §2.  Each bin of the   */
+/* RoIAlign grid above is moved by a learned offset, given normalized to the   */
+/* box size: the shift of bin (ph, pw) is                                      */
+/*   dx = (gamma * offset[k,0,ph,pw]) * len_x,  dy = (gamma * offset[k,1,ph,pw]) * len_y */
+/* (len = the box length on the level, as in the RoIAlign setup), and it is   */
+/* added to the bin start before the within-bin term:                          */
+/*   x = ((x0 + pw*bw) + dx) + ((ix + 1/2)*bw) / gw                            */
+/* (binary32, one rounding per operation, in parity mode).  Cut, clamp and     */
+/* bilinear weights are RoIAlign's.  The modulated form multiplies the bin     */
+/* average by mask[k,ph,pw]:  out = mask * (sum of weighted taps) / count.     */
+/*                                                                             */
+/* Gradients (the operator is piecewise bilinear in the shift):               */
+/*   feature: grad_F += g * mask / count * corner weight (as RoIAlign's);      */
+/*   offset x: sum over channels and valid samples of                          */
+/*       g * mask / count * dV/dx * gamma * len_x,                             */
+/*     dV/dx = hy*(F[yl,xh] - F[yl,xl]) + ly*(F[yh,xh] - F[yh,xl]) where the    */
+/*     sample is not clamped along x (0 <= x and xl < W-1), else 0;           */
+/*     offset y likewise with dV/dy = hx*(F[yh,xl] - F[yl,xl]) + lx*(F[yh,xh] - F[yl,xh]); */
+/*   mask: sum over channels of g * (sum of weighted taps) / count.           */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+    axis_tap t;
+    int slope;   /* 1 when the value is bilinear in this coordinate (not clamped) */
+} deform_tap;
+
+static deform_tap deform_sample(int mode, const axis_geom *g, float shift_f, double shift_d,
+                                int p, int i, int size)
+{
+    deform_tap d;
+    d.slope = 0;
+    d.t.valid = 0;
+    d.t.lo = d.t.hi = 0;
+    d.t.w_lo = d.t.w_hi = 0.0;
+    if (mode == MODE_PARITY) {
+        float a = (float)p * g->bin_f;
+        float b = g->start_f + a;
+        float b2 = b + shift_f;
+        float c = (float)i + 0.5f;
+        float e0 = c * g->bin_f;
+        float e = e0 / (float)g->grid;
+        float v = b2 + e;
+        if (v < -1.0f || v > (float)size)
+            return d;
+        d.slope = v >= 0.0f;
+        v = fmaxf(v, 0.0f);
+        int lo = (int)v;
+        int hi;
+        if (lo >= size - 1) {
+            lo = size - 1;
+            hi = size - 1;
+            v = (float)lo;
+            d.slope = 0;
+        } else {
+            hi = lo + 1;
+        }
+        float frac = v - (float)lo;
+        float rest = 1.0f - frac;
+        d.t.valid = 1;
+        d.t.lo = lo;
+        d.t.hi = hi;
+        d.t.w_lo = (double)rest;
+        d.t.w_hi = (double)frac;
+    } else {
+        double v = g->start_d + (double)p * g->bin_d + shift_d +
+                   ((double)i + 0.5) * g->bin_d / (double)g->grid;
+        if (v < -1.0 || v > (double)size)
+            return d;
+        d.slope = v >= 0.0;
+        v = fmax(v, 0.0);
+        int lo = (int)v;
+        int hi;
+        if (lo >= size - 1) {
+            lo = size - 1;
+            hi = size - 1;
+            v = (double)lo;
+            d.slope = 0;
+        } else {
+            hi = lo + 1;
+        }
+        double frac = v - (double)lo;
+        d.t.valid = 1;
+        d.t.lo = lo;
+        d.t.hi = hi;
+        d.t.w_lo = 1.0 - frac;
+        d.t.w_hi = frac;
+    }
+    return d;
+}
+
+/* Shift of one bin along one axis, in both precisions. */
+static void deform_shift(int mode, const axis_geom *g, float gamma, float off, float *sf,
+                         double *sd)
+{
+    if (mode == MODE_PARITY) {
+        float a = gamma * off;
+        float b = a * g->len_f;
+        *sf = b;
+        *sd = (double)b;
+    } else {
+        *sf = 0.0f;
+        *sd = (double)gamma * (double)off * g->len_d;
+    }
+}
+
+typedef struct {
+    int ok;              /* RoI names a valid level and image */
+    int lvl, b;
+    int64_t H, W;
+    axis_geom gx, gy;
+    int count;
+} deform_roi;
+
+static deform_roi deform_roi_setup(int mode, const int64_t *dims, const float *scales,
+                                   int32_t num_levels, const float *r, const int32_t *roi_levels,
+                                   int64_t k, int32_t PH, int32_t PW, int32_t sampling_ratio,
+                                   int32_t aligned)
+{
+    deform_roi d;
+    memset(&d, 0, sizeof(d));
+    d.lvl = roi_levels ? roi_levels[k] : 0;
+    if (d.lvl < 0 || d.lvl >= num_levels)
+        return d;
+    const int64_t N = dims[4 * d.lvl + 0];
+    d.H = dims[4 * d.lvl + 2];
+    d.W = dims[4 * d.lvl + 3];
+    d.b = roi_batch(r[0], N);
+    if (d.b < 0)
+        return d;
+    d.gx = axis_setup(mode, r[1], r[3], scales[d.lvl], aligned, PW, sampling_ratio);
+    d.gy = axis_setup(mode, r[2], r[4], scales[d.lvl], aligned, PH, sampling_ratio);
+    d.count = d.gy.grid * d.gx.grid;
+    if (d.count < 1)
+        d.count = 1;
+    d.ok = 1;
+    return d;
+}
+
+void oracle_deform_roi_pool_fwd(const double *const *feats, const int64_t *dims,
+                                const float *scales, int32_t num_levels,
+                                const float *rois, int64_t K, const int32_t *roi_levels,
+                                int32_t PH, int32_t PW, int32_t sampling_ratio,
+                                int32_t aligned, const float *offset, const float *mask,
+                                float gamma, int32_t mode, double *out)
+{
+    const int64_t C = dims[1];
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t k = 0; k < K; ++k) {
+        double *o = out + k * C * PH * PW;
+        for (int64_t e = 0; e < C * PH * PW; ++e)
+            o[e] = 0.0;
+        deform_roi d = deform_roi_setup(mode, dims, scales, num_levels, rois + 5 * k,
+                                        roi_levels, k, PH, PW, sampling_ratio, aligned);
+        if (!d.ok)
+            continue;
+        for (int ph = 0; ph < PH; ++ph) {
+            for (int pw = 0; pw < PW; ++pw) {
+                const int64_t bin = (int64_t)ph * PW + pw;
+                float sxf, syf;
+                double sxd, syd;
+                deform_shift(mode, &d.gx, gamma, offset[(k * 2 + 0) * PH * PW + bin], &sxf, &sxd);
+                deform_shift(mode, &d.gy, gamma, offset[(k * 2 + 1) * PH * PW + bin], &syf, &syd);
+                const double m = mask ? (double)mask[k * PH * PW + bin] : 1.0;
+                for (int64_t c = 0; c < C; ++c) {
+                    const double *F = feats[d.lvl] + ((int64_t)d.b * C + c) * d.H * d.W;
+                    double sum = 0.0;
+                    for (int iy = 0; iy < d.gy.grid; ++iy) {
+                        deform_tap ty = deform_sample(mode, &d.gy, syf, syd, ph, iy, (int)d.H);
+                        for (int ix = 0; ix < d.gx.grid; ++ix) {
+                            deform_tap tx = deform_sample(mode, &d.gx, sxf, sxd, pw, ix, (int)d.W);
+                            if (!ty.t.valid || !tx.t.valid)
+                                continue;
+                            sum += ty.t.w_lo * tx.t.w_lo * F[ty.t.lo * d.W + tx.t.lo];
+                            sum += ty.t.w_lo * tx.t.w_hi * F[ty.t.lo * d.W + tx.t.hi];
+                            sum += ty.t.w_hi * tx.t.w_lo * F[ty.t.hi * d.W + tx.t.lo];
+                            sum += ty.t.w_hi * tx.t.w_hi * F[ty.t.hi * d.W + tx.t.hi];
+                        }
+                    }
+                    o[c * PH * PW + bin] = m * (sum / (double)d.count);
+                }
+            }
+        }
+    }
+}
+
+/* Backward.  grad_feats (accumulated into; the caller clears them) in parallel over
+ * channels; grad_offset [K][2][PH][PW] and grad_mask [K][PH][PW] (written) in
+ * parallel over RoIs.  scale_offset / scale_mask (may be NULL) receive the same sums
+ * taken over the absolute values of every term, the scale of their rounding error. */
+void oracle_deform_roi_pool_bwd(const double *grad_out, const double *const *feats,
+                                double *const *grad_feats, const int64_t *dims,
+                                const float *scales, int32_t num_levels, const float *rois,
+                                int64_t K, const int32_t *roi_levels, int32_t PH, int32_t PW,
+                                int32_t sampling_ratio, int32_t aligned, const float *offset,
+                                const float *mask, float gamma, int32_t mode,
+                                double *grad_offset, double *grad_mask, double *scale_offset,
+                                double *scale_mask)
+{
+    const int64_t C = dims[1];
+#pragma omp parallel for schedule(static)
+    for (int64_t c = 0; c < C; ++c) {
+        for (int64_t k = 0; k < K; ++k) {
+            deform_roi d = deform_roi_setup(mode, dims, scales, num_levels, rois + 5 * k,
+                                            roi_levels, k, PH, PW, sampling_ratio, aligned);
+            if (!d.ok)
+                continue;
+            double *G = grad_feats[d.lvl] + ((int64_t)d.b * C + c) * d.H * d.W;
+            const double *g = grad_out + (k * C + c) * PH * PW;
+            for (int ph = 0; ph < PH; ++ph) {
+                for (int pw = 0; pw < PW; ++pw) {
+                    const int64_t bin = (int64_t)ph * PW + pw;
+                    float sxf, syf;
+                    double sxd, syd;
+                    deform_shift(mode, &d.gx, gamma, offset[(k * 2 + 0) * PH * PW + bin], &sxf, &sxd);
+                    deform_shift(mode, &d.gy, gamma, offset[(k * 2 + 1) * PH * PW + bin], &syf, &syd);
+                    const double m = mask ? (double)mask[k * PH * PW + bin] : 1.0;
+                    const double gv = g[bin] * m / (double)d.count;
+                    for (int iy = 0; iy < d.gy.grid; ++iy) {
+                        deform_tap ty = deform_sample(mode, &d.gy, syf, syd, ph, iy, (int)d.H);
+                        for (int ix = 0; ix < d.gx.grid; ++ix) {
+                            deform_tap tx = deform_sample(mode, &d.gx, sxf, sxd, pw, ix, (int)d.W);
+                            if (!ty.t.valid || !tx.t.valid)
+                                continue;
+                            G[ty.t.lo * d.W + tx.t.lo] += gv * ty.t.w_lo * tx.t.w_lo;
+                            G[ty.t.lo * d.W + tx.t.hi] += gv * ty.t.w_lo * tx.t.w_hi;
+                            G[ty.t.hi * d.W + tx.t.lo] += gv * ty.t.w_hi * tx.t.w_lo;
+                            G[ty.t.hi * d.W + tx.t.hi] += gv * ty.t.w_hi * tx.t.w_hi;
+                        }
+                    }
+                }
+            }
+        }
+    }
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t k = 0; k < K; ++k) {
+        for (int64_t e = 0; e < PH * PW; ++e) {
+            grad_offset[(k * 2 + 0) * PH * PW + e] = 0.0;
+            grad_offset[(k * 2 + 1) * PH * PW + e] = 0.0;
+            if (grad_mask)
+                grad_mask[k * PH * PW + e] = 0.0;
+            if (scale_offset) {
+                scale_offset[(k * 2 + 0) * PH * PW + e] = 0.0;
+                scale_offset[(k * 2 + 1) * PH * PW + e] = 0.0;
+            }
+            if (scale_mask)
+                scale_mask[k * PH * PW + e] = 0.0;
+        }
+        deform_roi d = deform_roi_setup(mode, dims, scales, num_levels, rois + 5 * k,
+                                        roi_levels, k, PH, PW, sampling_ratio, aligned);
+        if (!d.ok)
+            continue;
+        for (int ph = 0; ph < PH; ++ph) {
+            for (int pw = 0; pw < PW; ++pw) {
+                const int64_t bin = (int64_t)ph * PW + pw;
+                float sxf, syf;
+                double sxd, syd;
+                deform_shift(mode, &d.gx, gamma, offset[(k * 2 + 0) * PH * PW + bin], &sxf, &sxd);
+                deform_shift(mode, &d.gy, gamma, offset[(k * 2 + 1) * PH * PW + bin], &syf, &syd);
+                const double m = mask ? (double)mask[k * PH * PW + bin] : 1.0;
+                const double jx = (double)gamma * (mode == MODE_PARITY ? (double)d.gx.len_f : d.gx.len_d);
+                const double jy = (double)gamma * (mode == MODE_PARITY ? (double)d.gy.len_f : d.gy.len_d);
+                double ox = 0.0, oy = 0.0, om = 0.0, sx = 0.0, sy = 0.0, sm = 0.0;
+                for (int64_t c = 0; c < C; ++c) {
+                    const double *F = feats[d.lvl] + ((int64_t)d.b * C + c) * d.H * d.W;
+                    const double gc = grad_out[(k * C + c) * PH * PW + bin];
+                    double dvx = 0.0, dvy = 0.0, avx = 0.0, avy = 0.0, sum = 0.0, asum = 0.0;
+                    for (int iy = 0; iy < d.gy.grid; ++iy) {
+                        deform_tap ty = deform_sample(mode, &d.gy, syf, syd, ph, iy, (int)d.H);
+                        for (int ix = 0; ix < d.gx.grid; ++ix) {
+                            deform_tap tx = deform_sample(mode, &d.gx, sxf, sxd, pw, ix, (int)d.W);
+                            if (!ty.t.valid || !tx.t.valid)
+                                continue;
+                            const double v11 = F[ty.t.lo * d.W + tx.t.lo];
+                            const double v12 = F[ty.t.lo * d.W + tx.t.hi];
+                            const double v21 = F[ty.t.hi * d.W + tx.t.lo];
+                            const double v22 = F[ty.t.hi * d.W + tx.t.hi];
+                            sum += ty.t.w_lo * tx.t.w_lo * v11 + ty.t.w_lo * tx.t.w_hi * v12 +
+                                   ty.t.w_hi * tx.t.w_lo * v21 + ty.t.w_hi * tx.t.w_hi * v22;
+                            asum += fabs(ty.t.w_lo * tx.t.w_lo * v11) + fabs(ty.t.w_lo * tx.t.w_hi * v12) +
+                                    fabs(ty.t.w_hi * tx.t.w_lo * v21) + fabs(ty.t.w_hi * tx.t.w_hi * v22);
+                            if (tx.slope) {
+                                dvx += ty.t.w_lo * (v12 - v11) + ty.t.w_hi * (v22 - v21);
+                                avx += fabs(ty.t.w_lo * (v12 - v11)) + fabs(ty.t.w_hi * (v22 - v21));
+                            }
+                            if (ty.slope) {
+                                dvy += tx.t.w_lo * (v21 - v11) + tx.t.w_hi * (v22 - v12);
+                                avy += fabs(tx.t.w_lo * (v21 - v11)) + fabs(tx.t.w_hi * (v22 - v12));
+                            }
+                        }
+                    }
+                    ox += gc * m / (double)d.count * dvx * jx;
+                    oy += gc * m / (double)d.count * dvy * jy;
+                    om += gc * sum / (double)d.count;
+                    sx += fabs(gc * m / (double)d.count * jx) * avx;
+                    sy += fabs(gc * m / (double)d.count * jy) * avy;
+                    sm += fabs(gc) * asum / (double)d.count;
+                }
+                grad_offset[(k * 2 + 0) * PH * PW + bin] = ox;
+                grad_offset[(k * 2 + 1) * PH * PW + bin] = oy;
+                if (grad_mask)
+                    grad_mask[k * PH * PW + bin] = om;
+                if (scale_offset) {
+                    scale_offset[(k * 2 + 0) * PH * PW + bin] = sx;
+                    scale_offset[(k * 2 + 1) * PH * PW + bin] = sy;
+                }
+                if (scale_mask)
+                    scale_mask[k * PH * PW + bin] = sm;
             }
         }
     }
