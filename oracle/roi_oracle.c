@@ -520,14 +520,14 @@ static deform_tap deform_sample(int mode, const axis_geom *g, float shift_f, dou
     d.t.lo = d.t.hi = 0;
     d.t.w_lo = d.t.w_hi = 0.0;
     if (mode == MODE_PARITY) {
-        float a = (float)p * g->bin_f;
-        float b = g->start_f + a;
+        float pos = (float)p * g->bin_f;
+        float b = g->start_f + pos;
         float b2 = b + shift_f;
-        float c = (float)i + 0.5f;
-        float e0 = c * g->bin_f;
+        float half = (float)i + 0.5f;
+        float e0 = half * g->bin_f;
         float e = e0 / (float)g->grid;
         float v = b2 + e;
-        if (v < -1.0f || v > (float)size)
+        if (!(v >= -1.0f) || v > (float)size)
             return d;
         d.slope = v >= 0.0f;
         v = fmaxf(v, 0.0f);
@@ -549,9 +549,9 @@ static deform_tap deform_sample(int mode, const axis_geom *g, float shift_f, dou
         d.t.w_lo = (double)rest;
         d.t.w_hi = (double)frac;
     } else {
-        double v = g->start_d + (double)p * g->bin_d + shift_d +
-                   ((double)i + 0.5) * g->bin_d / (double)g->grid;
-        if (v < -1.0 || v > (double)size)
+        const double within = (0.5 + (double)i) * g->bin_d / (double)g->grid;
+        double v = g->start_d + (double)p * g->bin_d + shift_d + within;
+        if (!(v >= -1.0) || v > (double)size)
             return d;
         d.slope = v >= 0.0;
         v = fmax(v, 0.0);

@@ -25,7 +25,7 @@ def test_deform_pin_math_only(lib, pin):
 
 MUTANTS = [
     ("shift subtracted, binary32", "float b2 = b + shift_f;", "float b2 = b - shift_f;"),
-    ("shift subtracted, double", "g->bin_d + shift_d +", "g->bin_d - shift_d +"),
+    ("shift subtracted, double", "g->bin_d + shift_d + within;", "g->bin_d - shift_d + within;"),
     ("shift scaled by the bin instead of the box, binary32",
      "float b = a * g->len_f;", "float b = a * g->bin_f;"),
     ("shift scaled by the bin instead of the box, double",
