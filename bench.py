@@ -58,19 +58,21 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle work timed for the CPU baseline (seconds)")
     ap.add_argument("--calibrate-copy", action="store_true")
-    ap.add_argument("--op", default="align", choices=["align", "pool", "heads"],
+    ap.add_argument("--op", default="align", choices=["align", "pool", "heads", "deform"],
                     help="align: RoIAlign (the benchmark); pool: RoI max pooling on the same "
                          "workload (plan, roi_pool_fwd, roi_pool_bwd with clearing); heads: "
                          "box and mask heads on one pyramid (workload 2: the batch-2 box and "
                          "mask RoIs; workload 5: both heads of the batch-16 step), one fused "
-                         "backward, timed against two separate backward calls")
+                         "backward, timed against two separate backward calls; deform: "
+                         "modulated deformable RoI pooling on the workload (offsets "
+                         "N(0, 0.3^2), modulation U(0, 1), gamma 0.1)")
     return ap.parse_args()
 
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for name in ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip",
-                 "api.hip"):
+                 "deform.hip", "api.hip"):
         with open(os.path.join(ROOT, "paper_1906_07155_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -122,6 +124,9 @@ def main():
         return
     if args.op == "heads":
         main_heads(args)
+        return
+    if args.op == "deform":
+        main_deform(args)
         return
 
     import torch
@@ -563,6 +568,138 @@ def main_heads(args):
                   "separate_bwd": None if alt is None else {
                       "ms_per_step": round(alt[0], 5), "ms_bwd": round(alt[2], 5)},
                   "kernel_source_hash": kernel_source_hash()},
+    }
+    print(json.dumps(result), flush=True)
+
+
+def main_deform(args):
+    """Modulated deformable RoI pooling: one step is roi_extract_plan,
+    deform_roi_pool_fwd and deform_roi_pool_bwd (clearing included)."""
+    import torch
+
+    import oracle
+    import paper_1906_07155_amd as rex
+    from paper_1906_07155_amd import accounting, workloads
+
+    dev = torch.device("cuda:0")
+    wl = workloads.config(args.workload, head=args.head, feat_dtype=args.feat_dtype)
+    feats_np, rois_np = wl.features(), wl.rois()
+    K, C = rois_np.shape[0], wl.channels
+    PH, PW = wl.out_hw
+    bf16 = wl.feat_dtype == "bf16"
+    gamma = 0.1
+    rng = np.random.default_rng(workloads.BASE_SEED + 50)
+    off_np = (rng.standard_normal((K, 2, PH, PW)) * 0.3).astype(np.float32)
+    m_np = rng.uniform(0.0, 1.0, (K, PH, PW)).astype(np.float32)
+
+    def to_dev(a, dt, cl=True):
+        if dt == "bf16":
+            t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        return t.contiguous(memory_format=torch.channels_last) if cl else t
+
+    feats = [to_dev(f, wl.feat_dtype) for f in feats_np]
+    rois = torch.from_numpy(rois_np).to(dev)
+    off = torch.from_numpy(off_np).to(dev)
+    msk = torch.from_numpy(m_np).to(dev)
+    odt = torch.bfloat16 if wl.out_dtype == "bf16" else torch.float32
+    out = torch.empty((K, C, PH, PW), dtype=odt, device=dev)
+    gout = to_dev(wl.grad() if wl.backward else
+                  np.random.default_rng(1).standard_normal((K, C, PH, PW), dtype=np.float32),
+                  wl.grad_dtype, cl=False)
+    grads = [torch.empty(f.shape, dtype=torch.float32, device=dev).contiguous(
+        memory_format=torch.channels_last) for f in feats]
+    goff = torch.empty_like(off)
+    gmsk = torch.empty_like(msk)
+    levels = torch.empty(K, dtype=torch.int32, device=dev)
+    ws = torch.empty(rex.workspace_size(feats, wl.scales, K), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    names = ["plan", "fwd", "bwd"]
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        rex.plan(feats, wl.scales, rois, wl.finest_scale, levels_out=levels, workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        rex.deform_roi_pool_fwd(feats, wl.scales, rois, levels, wl.out_hw, off, msk, gamma,
+                                wl.sampling_ratio, wl.aligned, out=out, workspace=ws)
+        if ev is not None:
+            ev[2].record(stream)
+        rex.deform_roi_pool_bwd(gout, feats, rois, levels, off, msk, grads, wl.scales, gamma,
+                                wl.sampling_ratio, wl.aligned, zero_init=True, grad_offset=goff,
+                                grad_mask=gmsk, workspace=ws)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
+           for j, n in enumerate(names)}
+    lv_np = levels.cpu().numpy()
+    fp = accounting.deform_footprint(rois_np, lv_np, wl.level_hw, wl.scales, wl.n_images,
+                                     wl.out_hw, wl.sampling_ratio, wl.aligned, off_np, gamma)
+    s_f, s_o = (2 if bf16 else 4), (2 if wl.out_dtype == "bf16" else 4)
+    s_g = 2 if wl.grad_dtype == "bf16" else 4
+    elems = K * C * PH * PW
+    side = K * PH * PW * 3 * 4                       # offsets and modulation
+    zero = sum(wl.n_images * C * H * W * 4 for (H, W) in wl.level_hw)
+    alg = {"plan": 36 * K, "fwd": fp * C * s_f + elems * s_o + side + 24 * K,
+           "bwd": elems * s_g + fp * C * (s_f + 8) + 2 * side + zero + 24 * K}
+    gbs = {n: alg[n] / (per[n] * 1e-3) / 1e9 for n in names}
+    dominant = max(["fwd", "bwd"], key=lambda n: per[n])
+    cpu = None
+    if not args.no_cpu_baseline:
+        lib = oracle.load()
+        f64 = [(workloads.bf16_bits_to_f32(f) if bf16 else f).astype(np.float64) for f in feats_np]
+        g64 = np.random.default_rng(0).standard_normal((K, C, PH, PW))
+        n = min(K, 64)
+        sub = np.sort(np.random.default_rng(0).choice(K, n, replace=False))
+        elapsed, passes = 0.0, 0
+        while elapsed < args.cpu_seconds:
+            c0 = time.perf_counter()
+            oracle.deform_roi_pool_fwd(f64, wl.scales, rois_np[sub], lv_np[sub], PH, PW,
+                                       wl.sampling_ratio, wl.aligned, off_np[sub], m_np[sub],
+                                       gamma, lib=lib)
+            oracle.deform_roi_pool_bwd(g64[sub], f64, wl.scales, rois_np[sub], lv_np[sub], PH, PW,
+                                       wl.sampling_ratio, wl.aligned, off_np[sub], m_np[sub],
+                                       gamma, lib=lib)
+            elapsed += time.perf_counter() - c0
+            passes += 1
+        cpu = {"value": round(n * passes / elapsed, 1), "unit": "RoIs/s",
+               "cores": oracle.num_threads(lib), "kind": "oracle",
+               "sample": "%d of %d RoIs (all %d channels), fwd+bwd, %d passes in %.1f s wall" % (
+                   n, K, C, passes, elapsed)}
+    result = {
+        "metric": "modulated deformable RoI pooling fwd+bwd RoIs/sec and achieved HBM GB/s vs "
+                  "peak, FPN shapes",
+        "value": round(K / (ms_per_step * 1e-3), 1), "unit": "RoIs/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic (seeded normal features, log-uniform RoIs, normal offsets; no COCO)",
+        "config": {"workload": wl.name + ", modulated deformable RoI pooling", "num_rois": K,
+                   "channels": C, "out": [PH, PW], "gamma": gamma, "layout": "cl",
+                   "backward": True},
+        "roofline": {"bound": "hbm", "achieved": round(gbs[dominant], 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs[dominant] / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": "deform_roi_pool_" + dominant,
+                     "bytes_per_launch": alg[dominant], "launch_ms": round(per[dominant], 5)},
+        "cpu_baseline": cpu,
+        "extra": {"kernel_ms": {n: round(v, 5) for n, v in per.items()},
+                  "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
+                  "footprint_px": fp, "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(result), flush=True)
 

@@ -214,6 +214,48 @@ re_status_t roi_align_bwd_multi(const re_head_t *heads, int32_t num_heads,
                                 const re_level_t *grad_levels, int32_t num_levels,
                                 int32_t zero_init, void *stream);
 
+/* f3 -- deformable RoI pooling (DCN) and its modulated form (DCNv2), general modules
+ * of §2.  Every bin of the RoIAlign grid above is moved by a learned offset given
+ * normalized to the box size, and the bin average is scaled by a learned modulation:
+ *   dx = (gamma * offset[k,0,ph,pw]) * rw,  dy = (gamma * offset[k,1,ph,pw]) * rh
+ *   (rw, rh: the box length on the level, as in the RoIAlign definition)
+ *   sample (pw, ix):  x = ((x0 + pw*bw) + dx) + ((ix + 0.5)*bw) / gw   (y likewise)
+ * each operation rounded to binary32 in that order; a sample with x or y outside
+ * [-1, size] (or not a number) contributes zero but counts; cut, clamp, bilinear
+ * weights and count are RoIAlign's, and
+ *   out[k,c,ph,pw] = m * (sum of weighted taps) / count,  m = mask[k,ph,pw] (1 if NULL).
+ * With every offset 0 and no mask this is roi_align_fwd.
+ *   offset: device float[num_rois][2][out_h][out_w] (x then y);
+ *   mask: device float[num_rois][out_h][out_w] or NULL;  gamma: finite;
+ *   other arguments as roi_align_fwd (out of out_dtype, [num_rois][c][out_h][out_w]). */
+re_status_t deform_roi_pool_fwd(const re_level_t *levels, int32_t num_levels, const float *rois,
+                                int64_t num_rois, const int32_t *roi_levels, int32_t out_h,
+                                int32_t out_w, int32_t sampling_ratio, int32_t aligned,
+                                const float *offset, const float *mask, float gamma, void *out,
+                                int32_t out_dtype, const void *plan, size_t plan_bytes,
+                                void *stream);
+
+/* f3 -- gradients of deform_roi_pool_fwd for upstream gradient g:
+ *   features (added into grad_levels, cleared first when zero_init != 0):
+ *     g * m / count * corner weight, for every valid sample and corner;
+ *   grad_offset[k,0,ph,pw] (written) = sum over channels and valid samples of
+ *     g * m / count * dV/dx * gamma * rw, where dV/dx = hy*(F[yl,xh] - F[yl,xl]) +
+ *     ly*(F[yh,xh] - F[yh,xl]) for a sample not clamped along x (0 <= x and
+ *     xl < W-1) and 0 for a clamped one; grad_offset[k,1] likewise along y;
+ *   grad_mask[k,ph,pw] (written; NULL allowed, and required when mask is NULL) =
+ *     sum over channels of g * (sum of weighted taps) / count.
+ * Sums use fp32 atomics, so the last bits may vary between runs.
+ *   levels: the forward's features (read);  grad_levels: binary32 levels with the
+ *   features' n, c, h, w and spatial_scale;  grad_out: [num_rois][c][out_h][out_w]. */
+re_status_t deform_roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype,
+                                const re_level_t *levels, const re_level_t *grad_levels,
+                                int32_t num_levels, const float *rois, int64_t num_rois,
+                                const int32_t *roi_levels, int32_t out_h, int32_t out_w,
+                                int32_t sampling_ratio, int32_t aligned, const float *offset,
+                                const float *mask, float gamma, int32_t zero_init,
+                                float *grad_offset, float *grad_mask, const void *plan,
+                                size_t plan_bytes, void *stream);
+
 /* f1 -- RoI max pooling, the RoIPool of Fast R-CNN (a two-stage method of §2),
  * the other RoIPooling-like operator a RoIExtractor uses (§3.1).  On level l (scale
  * s, H x W map), every operation rounded to binary32 in this order:

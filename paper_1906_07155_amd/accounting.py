@@ -182,3 +182,47 @@ def count_pool(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[in
     zero = sum(n_images * C * H * W * 4 for (H, W) in level_hw)
     return PoolBytes(K=K, box_px=box, e_fwd=box * C * s_feat + elems * (s_out + 4) + 24 * K,
                      e_bwd=elems * (s_gout + 4) + elems * 8 + 24 * K, zero=zero)
+
+
+def deform_footprint(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[int, int]],
+                     scales: Sequence[float], n_images: int, out_hw: Tuple[int, int], S: int,
+                     aligned: bool, offset: np.ndarray, gamma: float) -> int:
+    """Sum over RoIs of the distinct pixels the bilinear corners of its shifted samples
+    touch (float64 geometry; used only for byte counts)."""
+    PH, PW = out_hw
+    total = 0
+    off_half = 0.5 if aligned else 0.0
+    for k in range(rois.shape[0]):
+        l = int(levels[k])
+        if l < 0 or l >= len(level_hw) or not (0 <= int(rois[k, 0]) < n_images):
+            continue
+        H, W = level_hw[l]
+        s = float(scales[l])
+        x0 = float(rois[k, 1]) * s - off_half
+        y0 = float(rois[k, 2]) * s - off_half
+        w = float(rois[k, 3]) * s - off_half - x0
+        h = float(rois[k, 4]) * s - off_half - y0
+        if not aligned:
+            w, h = max(w, 1.0), max(h, 1.0)
+        bw, bh = w / PW, h / PH
+        gx = S if S > 0 else max(1, min(64, int(np.ceil(bw))))
+        gy = S if S > 0 else max(1, min(64, int(np.ceil(bh))))
+        dx = gamma * offset[k, 0].astype(np.float64) * w
+        dy = gamma * offset[k, 1].astype(np.float64) * h
+        pw = np.arange(PW)[None, :, None, None]
+        ph = np.arange(PH)[:, None, None, None]
+        ix = np.arange(gx)[None, None, None, :]
+        iy = np.arange(gy)[None, None, :, None]
+        x = x0 + pw * bw + dx[:, :, None, None] + (ix + 0.5) * bw / gx
+        y = y0 + ph * bh + dy[:, :, None, None] + (iy + 0.5) * bh / gy
+        x, y = np.broadcast_arrays(x, y)
+        ok = (x >= -1) & (x <= W) & (y >= -1) & (y <= H)
+        xc = np.clip(x[ok], 0, W - 1)
+        yc = np.clip(y[ok], 0, H - 1)
+        xl = np.floor(xc).astype(np.int64)
+        yl = np.floor(yc).astype(np.int64)
+        xh = np.minimum(xl + 1, W - 1)
+        yh = np.minimum(yl + 1, H - 1)
+        px = np.concatenate([yl * W + xl, yl * W + xh, yh * W + xl, yh * W + xh])
+        total += int(np.unique(px).size)
+    return total

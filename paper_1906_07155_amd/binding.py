@@ -70,6 +70,10 @@ SIGNATURES = {
     "roi_align_bwd": [_VP, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _LEVELS, _I32, _I32,
                       _I32, _VP, _SZ, _VP],
     "roi_align_bwd_multi": [_HEADS, _I32, _LEVELS, _I32, _I32, _VP],
+    "deform_roi_pool_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _VP, _VP,
+                            _F32, _VP, _I32, _VP, _SZ, _VP],
+    "deform_roi_pool_bwd": [_VP, _I32, _LEVELS, _LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _I32,
+                            _I32, _VP, _VP, _F32, _I32, _VP, _VP, _VP, _SZ, _VP],
     "roi_pool_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _VP, _I32, _VP, _VP, _SZ, _VP],
     "roi_pool_bwd": [_VP, _I32, _VP, _VP, _I64, _VP, _I32, _I32, _LEVELS, _I32, _I32, _VP, _SZ,
                      _VP],
@@ -357,3 +361,76 @@ def roi_align_bwd_multi(heads: Sequence[dict], grads: Sequence, scales: Sequence
     check(lib().roi_align_bwd_multi(arr, len(heads), levels, len(grads), int(bool(zero_init)),
                                     stream_handle(stream)), "roi_align_bwd_multi")
     return grads
+
+
+def _f32_contig(t, name):
+    torch = _torch()
+    if t.dtype != torch.float32 or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous float32 tensor" % name)
+    _need_cuda(t, name)
+    return t
+
+
+def deform_roi_pool_fwd(features: Sequence, scales: Sequence[float], rois, roi_levels,
+                        out_size: Tuple[int, int], offset, mask=None, gamma: float = 0.1,
+                        sampling_ratio: int = 2, aligned: bool = True, out_dtype=None,
+                        workspace=None, out=None, stream=None):
+    """Deformable (modulated when `mask` is given) RoI pooling.  offset: float32
+    [K, 2, out_h, out_w] (x then y, normalized to the box size); mask: float32
+    [K, out_h, out_w] or None."""
+    torch = _torch()
+    rois = _rois(rois)
+    K, L = rois.shape[0], len(features)
+    C = features[0].shape[1]
+    ph, pw = out_size
+    _f32_contig(offset, "offset")
+    if mask is not None:
+        _f32_contig(mask, "mask")
+    odt = out_dtype or features[0].dtype
+    if out is None:
+        out = torch.empty((K, C, ph, pw), dtype=odt, device=rois.device)
+    arr = level_array(features, scales)
+    lv = roi_levels.data_ptr() if roi_levels is not None else None
+    ws = workspace.data_ptr() if workspace is not None else None
+    wsb = workspace.numel() if workspace is not None else 0
+    check(lib().deform_roi_pool_fwd(arr, L, rois.data_ptr(), K, lv, ph, pw, sampling_ratio,
+                                    int(bool(aligned)), offset.data_ptr(),
+                                    mask.data_ptr() if mask is not None else None, float(gamma),
+                                    out.data_ptr(), _dtype_code(out), ws, wsb,
+                                    stream_handle(stream)), "deform_roi_pool_fwd")
+    return out
+
+
+def deform_roi_pool_bwd(grad_out, features: Sequence, rois, roi_levels, offset, mask,
+                        grads: Sequence, scales: Sequence[float], gamma: float = 0.1,
+                        sampling_ratio: int = 2, aligned: bool = True, zero_init: bool = True,
+                        grad_offset=None, grad_mask=None, workspace=None, stream=None):
+    """Gradients of deform_roi_pool_fwd: feature gradients added into `grads` (float32
+    levels, cleared first if zero_init); returns (grads, grad_offset, grad_mask)."""
+    torch = _torch()
+    rois = _rois(rois)
+    _need_cuda(grad_out, "grad_out")
+    if not grad_out.is_contiguous():
+        raise ValueError("grad_out must be contiguous [K, C, out_h, out_w]")
+    K, L = rois.shape[0], len(grads)
+    ph, pw = grad_out.shape[2], grad_out.shape[3]
+    _f32_contig(offset, "offset")
+    if mask is not None:
+        _f32_contig(mask, "mask")
+    if grad_offset is None:
+        grad_offset = torch.empty((K, 2, ph, pw), dtype=torch.float32, device=rois.device)
+    if grad_mask is None and mask is not None:
+        grad_mask = torch.empty((K, ph, pw), dtype=torch.float32, device=rois.device)
+    farr = level_array(features, scales)
+    garr = level_array(grads, scales)
+    lv = roi_levels.data_ptr() if roi_levels is not None else None
+    ws = workspace.data_ptr() if workspace is not None else None
+    wsb = workspace.numel() if workspace is not None else 0
+    check(lib().deform_roi_pool_bwd(grad_out.data_ptr(), _dtype_code(grad_out), farr, garr, L,
+                                    rois.data_ptr(), K, lv, ph, pw, sampling_ratio,
+                                    int(bool(aligned)), offset.data_ptr(),
+                                    mask.data_ptr() if mask is not None else None, float(gamma),
+                                    int(bool(zero_init)), grad_offset.data_ptr(),
+                                    grad_mask.data_ptr() if grad_mask is not None else None,
+                                    ws, wsb, stream_handle(stream)), "deform_roi_pool_bwd")
+    return grads, grad_offset, grad_mask

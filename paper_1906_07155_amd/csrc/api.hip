@@ -657,4 +657,123 @@ re_status_t roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype, const int
     return from_hip(launch_pool_bwd(a, grad_out_dtype, fast, s));
 }
 
+// ---------------------------------------------------------------------------
+// Deformable (modulated) RoI pooling
+// ---------------------------------------------------------------------------
+
+namespace {
+constexpr int kDeformFastBins = 196;   // LDS of the channels-last kernels: 64 * bins * 4 bytes
+
+re_status_t check_deform(const float *offset, const float *mask, float gamma, int64_t K) {
+    if (K > 0 && !offset) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(offset) % 4 || reinterpret_cast<uintptr_t>(mask) % 4)
+        return RE_ERR_INVALID_ARG;
+    if (!std::isfinite(gamma)) return RE_ERR_INVALID_ARG;
+    return RE_OK;
+}
+}  // namespace
+
+re_status_t deform_roi_pool_fwd(const re_level_t *levels, int32_t num_levels, const float *rois,
+                                int64_t num_rois, const int32_t *roi_levels, int32_t out_h,
+                                int32_t out_w, int32_t sampling_ratio, int32_t aligned,
+                                const float *offset, const float *mask, float gamma, void *out,
+                                int32_t out_dtype, const void *plan, size_t plan_bytes,
+                                void *stream) {
+    LevelTable t;
+    bool cl = false;
+    re_status_t st = check_levels(levels, num_levels, true, &t, &cl, nullptr, nullptr);
+    if (st != RE_OK) return st;
+    if ((st = check_common(rois, num_rois, roi_levels, num_levels, out_h, out_w,
+                           sampling_ratio, aligned)) != RE_OK)
+        return st;
+    if ((st = check_deform(offset, mask, gamma, num_rois)) != RE_OK) return st;
+    if (!valid_dtype(out_dtype)) return RE_ERR_INVALID_ARG;
+    if (num_rois > 0 && !out) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(out) % dtype_size(out_dtype)) return RE_ERR_INVALID_ARG;
+    if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
+    if (num_rois == 0) return RE_OK;
+    DeformArgs a{};
+    a.lv = t;
+    a.rois = rois;
+    a.roi_levels = roi_levels;
+    a.perm = plan ? reinterpret_cast<const int32_t *>(static_cast<const char *>(plan) +
+                                                      perm_offset())
+                  : nullptr;
+    a.offset = offset;
+    a.mask = mask;
+    a.out = out;
+    a.gamma = gamma;
+    a.K = static_cast<int32_t>(num_rois);
+    a.PH = out_h;
+    a.PW = out_w;
+    a.S = sampling_ratio;
+    a.aligned = aligned;
+    const bool fast = cl && out_h * out_w <= kDeformFastBins;
+    return from_hip(launch_deform_fwd(a, levels[0].dtype, out_dtype, fast,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+re_status_t deform_roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype,
+                                const re_level_t *levels, const re_level_t *grad_levels,
+                                int32_t num_levels, const float *rois, int64_t num_rois,
+                                const int32_t *roi_levels, int32_t out_h, int32_t out_w,
+                                int32_t sampling_ratio, int32_t aligned, const float *offset,
+                                const float *mask, float gamma, int32_t zero_init,
+                                float *grad_offset, float *grad_mask, const void *plan,
+                                size_t plan_bytes, void *stream) {
+    LevelTable t, g;
+    bool cl = false, gcl = false;
+    int64_t numel[RE_MAX_LEVELS] = {0};
+    int dense[RE_MAX_LEVELS] = {0};
+    re_status_t st = check_levels(levels, num_levels, true, &t, &cl, nullptr, nullptr);
+    if (st != RE_OK) return st;
+    if ((st = check_levels(grad_levels, num_levels, true, &g, &gcl, numel, dense)) != RE_OK)
+        return st;
+    for (int l = 0; l < num_levels; ++l) {
+        if (grad_levels[l].dtype != RE_DTYPE_F32) return RE_ERR_UNSUPPORTED;
+        if (grad_levels[l].n != levels[l].n || grad_levels[l].c != levels[l].c ||
+            grad_levels[l].h != levels[l].h || grad_levels[l].w != levels[l].w ||
+            grad_levels[l].spatial_scale != levels[l].spatial_scale)
+            return RE_ERR_INVALID_ARG;
+    }
+    if ((st = check_common(rois, num_rois, roi_levels, num_levels, out_h, out_w,
+                           sampling_ratio, aligned)) != RE_OK)
+        return st;
+    if ((st = check_deform(offset, mask, gamma, num_rois)) != RE_OK) return st;
+    if (!valid_dtype(grad_out_dtype)) return RE_ERR_INVALID_ARG;
+    if (num_rois > 0 && (!grad_out || !grad_offset)) return RE_ERR_INVALID_ARG;
+    if (grad_mask && !mask) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(grad_out) % dtype_size(grad_out_dtype) ||
+        reinterpret_cast<uintptr_t>(grad_offset) % 4 || reinterpret_cast<uintptr_t>(grad_mask) % 4)
+        return RE_ERR_INVALID_ARG;
+    if (zero_init != 0 && zero_init != 1) return RE_ERR_INVALID_ARG;
+    if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (zero_init) {
+        if ((st = from_hip(launch_zero(g, numel, dense, s))) != RE_OK) return st;
+    }
+    if (num_rois == 0) return RE_OK;
+    DeformArgs a{};
+    a.lv = t;
+    a.glv = g;
+    a.rois = rois;
+    a.roi_levels = roi_levels;
+    a.perm = plan ? reinterpret_cast<const int32_t *>(static_cast<const char *>(plan) +
+                                                      perm_offset())
+                  : nullptr;
+    a.offset = offset;
+    a.mask = mask;
+    a.gout = grad_out;
+    a.grad_offset = grad_offset;
+    a.grad_mask = grad_mask;
+    a.gamma = gamma;
+    a.K = static_cast<int32_t>(num_rois);
+    a.PH = out_h;
+    a.PW = out_w;
+    a.S = sampling_ratio;
+    a.aligned = aligned;
+    const bool fast = cl && gcl && out_h * out_w <= kDeformFastBins;
+    return from_hip(launch_deform_bwd(a, levels[0].dtype, grad_out_dtype, fast, s));
+}
+
 }  // extern "C"

@@ -190,6 +190,7 @@ struct Axis {
     float start;
     float bin;
     int grid;
+    float len;   // box length on the level (after the minimum size)
 };
 
 __device__ __forceinline__ Axis axis_setup(float c1, float c2, float scale, int aligned, int P,
@@ -215,6 +216,7 @@ __device__ __forceinline__ Axis axis_setup(float c1, float c2, float scale, int 
     a.start = s;
     a.bin = bin;
     a.grid = g;
+    a.len = len;
     return a;
 }
 

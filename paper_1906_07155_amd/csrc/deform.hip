@@ -1,0 +1,476 @@
+// deform.hip -- deformable RoI pooling and its modulated form.
+//
+// DCN's deformable RoI pooling and DCNv2's modulated variant (general modules of
+// MMDetection, §2) move every bin of the RoIAlign grid by a learned offset,
+// normalized to the box size, and scale the bin average by a learned modulation.
+// Definition and gradients are stated in include/roi_extract.h.
+//
+// Kernels:
+//   deform_fwd_cl_kernel     channels-last features.  One workgroup = one RoI x one
+//                            slice of 64 channels; lanes run over channels, so every tap
+//                            is one coalesced load; the bins are dealt round-robin to
+//                            the four waves; results leave through an LDS transpose so
+//                            the [C][PH][PW] block is stored contiguously.
+//   deform_bwd_cl_kernel     channels-last features and gradients.  Same decomposition;
+//                            the slice's upstream gradient block is read through LDS,
+//                            feature gradients go out as no-return fp32 atomics (64
+//                            consecutive channels of one pixel per instruction), and the
+//                            offset and modulation gradients of a bin are summed over
+//                            the wave's channels with lane shuffles and added once per
+//                            wave.
+//   deform_*_generic_kernel  any strides: one thread per output element.
+#include "internal.hpp"
+
+namespace rex {
+
+// One sample of a shifted bin along one axis.  Binary32, one rounding per operation:
+//   x = ((start + p*bin) + shift) + ((i + 1/2)*bin) / grid.
+// A sample outside [-1, size] (or not a number) is invalid; otherwise it is clamped
+// like RoIAlign's, and `slope` says whether the value is bilinear in the coordinate
+// (not clamped), which is where the offset gradient is nonzero.
+struct DTap {
+    int lo, hi;
+    float wlo, whi;
+    bool valid;
+    bool slope;
+};
+
+__device__ __forceinline__ DTap deform_tap(const Axis &a, float shift, int p, int i, int size) {
+    const float pos = static_cast<float>(p) * a.bin;
+    const float b = a.start + pos;
+    const float b2 = b + shift;
+    const float half = static_cast<float>(i) + 0.5f;
+    const float e0 = half * a.bin;
+    const float e = e0 / static_cast<float>(a.grid);
+    float v = b2 + e;
+    DTap t;
+    t.lo = t.hi = 0;
+    t.wlo = t.whi = 0.0f;
+    t.valid = false;
+    t.slope = false;
+    if (!(v >= -1.0f) || v > static_cast<float>(size)) return t;
+    t.valid = true;
+    t.slope = v >= 0.0f;
+    v = fmaxf(v, 0.0f);
+    int lo = static_cast<int>(v);
+    int hi;
+    if (lo >= size - 1) {
+        lo = size - 1;
+        hi = size - 1;
+        v = static_cast<float>(lo);
+        t.slope = false;
+    } else {
+        hi = lo + 1;
+    }
+    const float frac = v - static_cast<float>(lo);
+    t.lo = lo;
+    t.hi = hi;
+    t.wlo = 1.0f - frac;
+    t.whi = frac;
+    return t;
+}
+
+// Shift of a bin along one axis: (gamma * offset) * box length.
+__device__ __forceinline__ float deform_shift(float gamma, float off, float len) {
+    const float t = gamma * off;
+    return t * len;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Gradient level `l` of the table, by constant indices only (as level_at).
+__device__ __forceinline__ void grad_level(const DeformArgs &a, int l, float *&data, int64_t &sn,
+                                           int64_t &sc, int64_t &sh, int64_t &sw) {
+#define REX_GRAD_LEVEL(i)                                              \
+    case i:                                                             \
+        data = static_cast<float *>(const_cast<void *>(a.glv.l[i].data)); \
+        sn = a.glv.l[i].sn;                                             \
+        sc = a.glv.l[i].sc;                                             \
+        sh = a.glv.l[i].sh;                                             \
+        sw = a.glv.l[i].sw;                                             \
+        break;
+    switch (l) {
+        REX_GRAD_LEVEL(1)
+        REX_GRAD_LEVEL(2)
+        REX_GRAD_LEVEL(3)
+        REX_GRAD_LEVEL(4)
+        REX_GRAD_LEVEL(5)
+        REX_GRAD_LEVEL(6)
+        REX_GRAD_LEVEL(7)
+        default:
+            data = static_cast<float *>(const_cast<void *>(a.glv.l[0].data));
+            sn = a.glv.l[0].sn;
+            sc = a.glv.l[0].sc;
+            sh = a.glv.l[0].sh;
+            sw = a.glv.l[0].sw;
+    }
+#undef REX_GRAD_LEVEL
+}
+
+// ---------------------------------------------------------------------------
+// General strided kernels
+// ---------------------------------------------------------------------------
+
+template <typename T, typename TO>
+__global__ __launch_bounds__(256) void deform_fwd_generic_kernel(DeformArgs a) {
+    const int PH = a.PH, PW = a.PW;
+    const int64_t NB = static_cast<int64_t>(PH) * PW;
+    const int64_t CNB = static_cast<int64_t>(a.lv.C) * NB;
+    const int64_t total = static_cast<int64_t>(a.K) * CNB;
+    for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < total;
+         e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t k = e / CNB;
+        const int64_t rem = e - k * CNB;
+        const int64_t c = rem / NB;
+        const int j = static_cast<int>(rem - c * NB);
+        const int ph = j / PW, pw = j - (j / PW) * PW;
+        float val = 0.0f;
+        const float *r = a.rois + 5 * k;
+        const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
+        if (lvl >= 0 && lvl < a.lv.num) {
+            const LevelArg L = level_at(a.lv, lvl);
+            const int b = roi_batch(r[0], a.lv.N);
+            if (b >= 0) {
+                const Axis ax = axis_setup(r[1], r[3], L.scale, a.aligned, PW, a.S);
+                const Axis ay = axis_setup(r[2], r[4], L.scale, a.aligned, PH, a.S);
+                const float sx = deform_shift(a.gamma, a.offset[(k * 2 + 0) * NB + j], ax.len);
+                const float sy = deform_shift(a.gamma, a.offset[(k * 2 + 1) * NB + j], ay.len);
+                const gcptr<T> base = as_global<T>(L.data) + b * L.sn + c * L.sc;
+                float sum = 0.0f;
+                for (int iy = 0; iy < ay.grid; ++iy) {
+                    const DTap ty = deform_tap(ay, sy, ph, iy, L.H);
+                    if (!ty.valid) continue;
+                    for (int ix = 0; ix < ax.grid; ++ix) {
+                        const DTap tx = deform_tap(ax, sx, pw, ix, L.W);
+                        if (!tx.valid) continue;
+                        sum = fmaf(ty.wlo * tx.wlo, load_f32(base + ty.lo * L.sh + tx.lo * L.sw), sum);
+                        sum = fmaf(ty.wlo * tx.whi, load_f32(base + ty.lo * L.sh + tx.hi * L.sw), sum);
+                        sum = fmaf(ty.whi * tx.wlo, load_f32(base + ty.hi * L.sh + tx.lo * L.sw), sum);
+                        sum = fmaf(ty.whi * tx.whi, load_f32(base + ty.hi * L.sh + tx.hi * L.sw), sum);
+                    }
+                }
+                const int count = max(ay.grid * ax.grid, 1);
+                const float m = a.mask ? a.mask[k * NB + j] : 1.0f;
+                val = m * (sum / static_cast<float>(count));
+            }
+        }
+        store_f32<TO>(as_global_mut<TO>(a.out) + e, val);
+    }
+}
+
+template <typename T, typename TG>
+__global__ __launch_bounds__(256) void deform_bwd_generic_kernel(DeformArgs a) {
+    const int PH = a.PH, PW = a.PW;
+    const int64_t NB = static_cast<int64_t>(PH) * PW;
+    const int64_t CNB = static_cast<int64_t>(a.lv.C) * NB;
+    const int64_t total = static_cast<int64_t>(a.K) * CNB;
+    for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < total;
+         e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t k = e / CNB;
+        const int64_t rem = e - k * CNB;
+        const int64_t c = rem / NB;
+        const int j = static_cast<int>(rem - c * NB);
+        const int ph = j / PW, pw = j - (j / PW) * PW;
+        const float *r = a.rois + 5 * k;
+        const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
+        if (lvl < 0 || lvl >= a.lv.num) continue;
+        const LevelArg L = level_at(a.lv, lvl);
+        float *gdata;
+        int64_t gsn, gsc, gsh, gsw;
+        grad_level(a, lvl, gdata, gsn, gsc, gsh, gsw);
+        const int b = roi_batch(r[0], a.lv.N);
+        if (b < 0) continue;
+        const Axis ax = axis_setup(r[1], r[3], L.scale, a.aligned, PW, a.S);
+        const Axis ay = axis_setup(r[2], r[4], L.scale, a.aligned, PH, a.S);
+        const float sx = deform_shift(a.gamma, a.offset[(k * 2 + 0) * NB + j], ax.len);
+        const float sy = deform_shift(a.gamma, a.offset[(k * 2 + 1) * NB + j], ay.len);
+        const int count = max(ay.grid * ax.grid, 1);
+        const float m = a.mask ? a.mask[k * NB + j] : 1.0f;
+        const float gv = load_f32(as_global<TG>(a.gout) + e);
+        const float gq = (gv * m) / static_cast<float>(count);
+        const gcptr<T> base = as_global<T>(L.data) + b * L.sn + c * L.sc;
+        float *const gbase = gdata + b * gsn + c * gsc;
+        float px = 0.0f, py = 0.0f, pm = 0.0f;
+        for (int iy = 0; iy < ay.grid; ++iy) {
+            const DTap ty = deform_tap(ay, sy, ph, iy, L.H);
+            if (!ty.valid) continue;
+            for (int ix = 0; ix < ax.grid; ++ix) {
+                const DTap tx = deform_tap(ax, sx, pw, ix, L.W);
+                if (!tx.valid) continue;
+                const float v11 = load_f32(base + ty.lo * L.sh + tx.lo * L.sw);
+                const float v12 = load_f32(base + ty.lo * L.sh + tx.hi * L.sw);
+                const float v21 = load_f32(base + ty.hi * L.sh + tx.lo * L.sw);
+                const float v22 = load_f32(base + ty.hi * L.sh + tx.hi * L.sw);
+                unsafeAtomicAdd(gbase + ty.lo * gsh + tx.lo * gsw, gq * (ty.wlo * tx.wlo));
+                unsafeAtomicAdd(gbase + ty.lo * gsh + tx.hi * gsw, gq * (ty.wlo * tx.whi));
+                unsafeAtomicAdd(gbase + ty.hi * gsh + tx.lo * gsw, gq * (ty.whi * tx.wlo));
+                unsafeAtomicAdd(gbase + ty.hi * gsh + tx.hi * gsw, gq * (ty.whi * tx.whi));
+                if (tx.slope) px += ty.wlo * (v12 - v11) + ty.whi * (v22 - v21);
+                if (ty.slope) py += tx.wlo * (v21 - v11) + tx.whi * (v22 - v12);
+                pm += ty.wlo * tx.wlo * v11 + ty.wlo * tx.whi * v12 + ty.whi * tx.wlo * v21 +
+                      ty.whi * tx.whi * v22;
+            }
+        }
+        unsafeAtomicAdd(a.grad_offset + (k * 2 + 0) * NB + j, gq * px * (a.gamma * ax.len));
+        unsafeAtomicAdd(a.grad_offset + (k * 2 + 1) * NB + j, gq * py * (a.gamma * ay.len));
+        if (a.grad_mask) unsafeAtomicAdd(a.grad_mask + k * NB + j, gv * pm / static_cast<float>(count));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Channels-last kernels
+// ---------------------------------------------------------------------------
+
+struct DeformRoi {
+    int k, slice, nch;
+    bool kvalid, active;
+    LevelArg L;
+    int b;
+    Axis ax, ay;
+};
+
+__device__ __forceinline__ DeformRoi deform_roi(const DeformArgs &a) {
+    DeformRoi d;
+    const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int slot = static_cast<int>(lid / static_cast<uint32_t>(a.nslices));
+    d.slice = static_cast<int>(lid) - slot * a.nslices;
+    int k = a.perm ? a.perm[slot] : slot;
+    d.kvalid = k >= 0 && k < a.K;
+    if (!d.kvalid) k = 0;
+    d.k = k;
+    const float *r = a.rois + 5 * static_cast<int64_t>(k);
+    const int lvl = a.roi_levels ? a.roi_levels[k] : 0;
+    const bool lvalid = lvl >= 0 && lvl < a.lv.num;
+    d.L = level_at(a.lv, lvalid ? lvl : 0);
+    d.b = roi_batch(r[0], a.lv.N);
+    d.active = d.kvalid && lvalid && d.b >= 0;
+    d.ax = axis_setup(r[1], r[3], d.L.scale, a.aligned, a.PW, a.S);
+    d.ay = axis_setup(r[2], r[4], d.L.scale, a.aligned, a.PH, a.S);
+    d.nch = min(64, a.lv.C - d.slice * 64);
+    return d;
+}
+
+template <typename T, typename TO>
+__global__ __launch_bounds__(256) void deform_fwd_cl_kernel(DeformArgs a) {
+    extern __shared__ __align__(16) float s_out[];   // [64][NB]
+    const int NB = a.PH * a.PW;
+    const DeformRoi d = deform_roi(a);
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const LevelArg &L = d.L;
+    const char *img = static_cast<const char *>(L.data) +
+                      static_cast<int64_t>(d.active ? d.b : 0) * L.sn * static_cast<int64_t>(sizeof(T));
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(img, L.img_bytes);
+    const uint32_t vo =
+        lane < d.nch ? static_cast<uint32_t>(d.slice * 64 + lane) * uint32_t(sizeof(T)) : kBufOOB;
+    const uint32_t sh = static_cast<uint32_t>(L.sh) * uint32_t(sizeof(T));
+    const uint32_t sw = static_cast<uint32_t>(L.sw) * uint32_t(sizeof(T));
+    const int count = max(d.ay.grid * d.ax.grid, 1);
+    for (int jb = wave; jb < NB; jb += 4) {
+        float val = 0.0f;
+        if (d.active) {
+            const int ph = jb / a.PW, pw = jb - (jb / a.PW) * a.PW;
+            const int64_t kb = static_cast<int64_t>(d.k) * NB + jb;
+            const float sx = deform_shift(a.gamma, a.offset[2 * static_cast<int64_t>(d.k) * NB + jb],
+                                          d.ax.len);
+            const float sy = deform_shift(
+                a.gamma, a.offset[(2 * static_cast<int64_t>(d.k) + 1) * NB + jb], d.ay.len);
+            float sum = 0.0f;
+            for (int iy = 0; iy < d.ay.grid; ++iy) {
+                const DTap ty = deform_tap(d.ay, sy, ph, iy, L.H);
+                if (!ty.valid) continue;
+                const uint32_t r0 = static_cast<uint32_t>(ty.lo) * sh;
+                const uint32_t r1 = static_cast<uint32_t>(ty.hi) * sh;
+                for (int ix = 0; ix < d.ax.grid; ++ix) {
+                    const DTap tx = deform_tap(d.ax, sx, pw, ix, L.W);
+                    if (!tx.valid) continue;
+                    const uint32_t c0 = static_cast<uint32_t>(tx.lo) * sw;
+                    const uint32_t c1 = static_cast<uint32_t>(tx.hi) * sw;
+                    const float v11 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r0 + c0));
+                    const float v12 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r0 + c1));
+                    const float v21 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c0));
+                    const float v22 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c1));
+                    sum = fmaf(ty.wlo * tx.wlo, v11, sum);
+                    sum = fmaf(ty.wlo * tx.whi, v12, sum);
+                    sum = fmaf(ty.whi * tx.wlo, v21, sum);
+                    sum = fmaf(ty.whi * tx.whi, v22, sum);
+                }
+            }
+            const float m = a.mask ? a.mask[kb] : 1.0f;
+            val = m * (sum / static_cast<float>(count));
+        }
+        s_out[lane * NB + jb] = val;
+    }
+    __syncthreads();
+    if (!d.kvalid) return;   // uniform over the workgroup, after the last barrier
+    const int64_t o0 =
+        (static_cast<int64_t>(d.k) * a.lv.C + static_cast<int64_t>(d.slice) * 64) * NB;
+    const gptr<TO> out = as_global_mut<TO>(a.out) + o0;
+    for (int e = threadIdx.x; e < d.nch * NB; e += 256) store_f32<TO>(out + e, s_out[e]);
+}
+
+template <typename T, typename TG>
+__global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
+    extern __shared__ __align__(16) float s_g[];   // [64][NB] upstream gradient of the slice
+    const int NB = a.PH * a.PW;
+    const DeformRoi d = deform_roi(a);
+    if (!d.active) return;   // uniform over the workgroup, before any barrier
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int64_t o0 =
+        (static_cast<int64_t>(d.k) * a.lv.C + static_cast<int64_t>(d.slice) * 64) * NB;
+    const gcptr<TG> gsrc = as_global<TG>(a.gout) + o0;
+    for (int e = threadIdx.x; e < d.nch * NB; e += 256) s_g[e] = load_f32(gsrc + e);
+    __syncthreads();
+
+    const bool lane_on = lane < d.nch;
+    const LevelArg &L = d.L;
+    float *gdata;
+    int64_t gsn, gsc, gsh, gsw;
+    grad_level(a, a.roi_levels ? a.roi_levels[d.k] : 0, gdata, gsn, gsc, gsh, gsw);
+    const char *img = static_cast<const char *>(L.data) +
+                      static_cast<int64_t>(d.b) * L.sn * static_cast<int64_t>(sizeof(T));
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(img, L.img_bytes);
+    const uint32_t vo =
+        lane_on ? static_cast<uint32_t>(d.slice * 64 + lane) * uint32_t(sizeof(T)) : kBufOOB;
+    const uint32_t sh = static_cast<uint32_t>(L.sh) * uint32_t(sizeof(T));
+    const uint32_t sw = static_cast<uint32_t>(L.sw) * uint32_t(sizeof(T));
+    float *const gbase = gdata + static_cast<int64_t>(d.b) * gsn + (d.slice * 64 + (lane_on ? lane : 0));
+    const int count = max(d.ay.grid * d.ax.grid, 1);
+    const float jx = a.gamma * d.ax.len, jy = a.gamma * d.ay.len;
+    for (int jb = wave; jb < NB; jb += 4) {
+        const int ph = jb / a.PW, pw = jb - (jb / a.PW) * a.PW;
+        const int64_t kb = static_cast<int64_t>(d.k) * NB + jb;
+        const float sx = deform_shift(a.gamma, a.offset[2 * static_cast<int64_t>(d.k) * NB + jb],
+                                      d.ax.len);
+        const float sy = deform_shift(
+            a.gamma, a.offset[(2 * static_cast<int64_t>(d.k) + 1) * NB + jb], d.ay.len);
+        const float m = a.mask ? a.mask[kb] : 1.0f;
+        const float gv = lane_on ? s_g[lane * NB + jb] : 0.0f;
+        const float gq = (gv * m) / static_cast<float>(count);
+        float px = 0.0f, py = 0.0f, pm = 0.0f;
+        for (int iy = 0; iy < d.ay.grid; ++iy) {
+            const DTap ty = deform_tap(d.ay, sy, ph, iy, L.H);
+            if (!ty.valid) continue;
+            const uint32_t r0 = static_cast<uint32_t>(ty.lo) * sh;
+            const uint32_t r1 = static_cast<uint32_t>(ty.hi) * sh;
+            for (int ix = 0; ix < d.ax.grid; ++ix) {
+                const DTap tx = deform_tap(d.ax, sx, pw, ix, L.W);
+                if (!tx.valid) continue;
+                const uint32_t c0 = static_cast<uint32_t>(tx.lo) * sw;
+                const uint32_t c1 = static_cast<uint32_t>(tx.hi) * sw;
+                const float v11 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r0 + c0));
+                const float v12 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r0 + c1));
+                const float v21 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c0));
+                const float v22 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c1));
+                if (lane_on) {
+                    unsafeAtomicAdd(gbase + ty.lo * gsh + tx.lo * gsw, gq * (ty.wlo * tx.wlo));
+                    unsafeAtomicAdd(gbase + ty.lo * gsh + tx.hi * gsw, gq * (ty.wlo * tx.whi));
+                    unsafeAtomicAdd(gbase + ty.hi * gsh + tx.lo * gsw, gq * (ty.whi * tx.wlo));
+                    unsafeAtomicAdd(gbase + ty.hi * gsh + tx.hi * gsw, gq * (ty.whi * tx.whi));
+                }
+                if (tx.slope) px += ty.wlo * (v12 - v11) + ty.whi * (v22 - v21);
+                if (ty.slope) py += tx.wlo * (v21 - v11) + tx.whi * (v22 - v12);
+                pm += ty.wlo * tx.wlo * v11 + ty.wlo * tx.whi * v12 + ty.whi * tx.wlo * v21 +
+                      ty.whi * tx.whi * v22;
+            }
+        }
+        // lanes past the last channel have gv = 0 and read zeros, so they add nothing
+        const float sx_sum = wave_sum(gq * px);
+        const float sy_sum = wave_sum(gq * py);
+        const float sm_sum = wave_sum(gv * pm);
+        if (lane == 0) {
+            unsafeAtomicAdd(a.grad_offset + 2 * static_cast<int64_t>(d.k) * NB + jb, sx_sum * jx);
+            unsafeAtomicAdd(a.grad_offset + (2 * static_cast<int64_t>(d.k) + 1) * NB + jb,
+                            sy_sum * jy);
+            if (a.grad_mask) unsafeAtomicAdd(a.grad_mask + kb, sm_sum / static_cast<float>(count));
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void deform_clear_kernel(float *p, int64_t n, float *q,
+                                                          int64_t m) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n + m;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        if (i < n)
+            p[i] = 0.0f;
+        else
+            q[i - n] = 0.0f;
+    }
+}
+
+template <typename T, typename TO>
+static void fwd_typed(const DeformArgs &a, bool fast, hipStream_t stream) {
+    const int NB = a.PH * a.PW;
+    if (fast) {
+        const uint32_t g = static_cast<uint32_t>(static_cast<int64_t>(a.K) * a.nslices);
+        deform_fwd_cl_kernel<T, TO><<<g, 256, static_cast<size_t>(64) * NB * 4, stream>>>(a);
+    } else {
+        const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * NB;
+        const uint32_t blocks = static_cast<uint32_t>(std::min<int64_t>((total + 255) / 256, 16384));
+        deform_fwd_generic_kernel<T, TO><<<blocks, 256, 0, stream>>>(a);
+    }
+}
+
+hipError_t launch_deform_fwd(DeformArgs a, int feat_dtype, int out_dtype, bool fast,
+                             hipStream_t stream) {
+    if (a.K == 0) return hipSuccess;
+    a.nslices = (a.lv.C + 63) / 64;
+    if (static_cast<int64_t>(a.K) * a.nslices >= (int64_t(1) << 24)) fast = false;
+    if (feat_dtype == kF32 && out_dtype == kF32)
+        fwd_typed<float, float>(a, fast, stream);
+    else if (feat_dtype == kF32)
+        fwd_typed<float, uint16_t>(a, fast, stream);
+    else if (out_dtype == kF32)
+        fwd_typed<uint16_t, float>(a, fast, stream);
+    else
+        fwd_typed<uint16_t, uint16_t>(a, fast, stream);
+    return hipGetLastError();
+}
+
+template <typename T, typename TG>
+static void bwd_typed(const DeformArgs &a, bool fast, hipStream_t stream) {
+    const int NB = a.PH * a.PW;
+    if (fast) {
+        const uint32_t g = static_cast<uint32_t>(static_cast<int64_t>(a.K) * a.nslices);
+        deform_bwd_cl_kernel<T, TG><<<g, 256, static_cast<size_t>(64) * NB * 4, stream>>>(a);
+    } else {
+        const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * NB;
+        const uint32_t blocks = static_cast<uint32_t>(std::min<int64_t>((total + 255) / 256, 16384));
+        deform_bwd_generic_kernel<T, TG><<<blocks, 256, 0, stream>>>(a);
+    }
+}
+
+hipError_t launch_deform_bwd(DeformArgs a, int feat_dtype, int gout_dtype, bool fast,
+                             hipStream_t stream) {
+    if (a.K == 0) return hipSuccess;
+    const int64_t NB = static_cast<int64_t>(a.PH) * a.PW;
+    const int64_t n_off = static_cast<int64_t>(a.K) * 2 * NB;
+    const int64_t n_mask = a.grad_mask ? static_cast<int64_t>(a.K) * NB : 0;
+    const uint32_t cb =
+        static_cast<uint32_t>(std::min<int64_t>((n_off + n_mask + 255) / 256, 4096));
+    deform_clear_kernel<<<cb, 256, 0, stream>>>(a.grad_offset, n_off, a.grad_mask, n_mask);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    a.nslices = (a.lv.C + 63) / 64;
+    if (static_cast<int64_t>(a.K) * a.nslices >= (int64_t(1) << 24)) fast = false;
+    if (feat_dtype == kF32 && gout_dtype == kF32)
+        bwd_typed<float, float>(a, fast, stream);
+    else if (feat_dtype == kF32)
+        bwd_typed<float, uint16_t>(a, fast, stream);
+    else if (gout_dtype == kF32)
+        bwd_typed<uint16_t, float>(a, fast, stream);
+    else
+        bwd_typed<uint16_t, uint16_t>(a, fast, stream);
+    return hipGetLastError();
+}
+
+}  // namespace rex

@@ -132,6 +132,33 @@ hipError_t launch_pool_fwd(PoolArgs a, int feat_dtype, int out_dtype, bool fast,
                            hipStream_t stream);
 hipError_t launch_pool_bwd(PoolArgs a, int gout_dtype, bool fast, hipStream_t stream);
 
+// Deformable (modulated) RoI pooling, forward and backward.
+struct DeformArgs {
+    LevelTable lv;               // features
+    LevelTable glv;              // backward: binary32 gradient levels
+    const float *rois;
+    const int32_t *roi_levels;
+    const int32_t *perm;         // plan order or null
+    const float *offset;         // [K][2][PH][PW]
+    const float *mask;           // [K][PH][PW] or null
+    void *out;                   // forward output [K][C][PH][PW]
+    const void *gout;            // backward upstream gradient [K][C][PH][PW]
+    float *grad_offset;          // backward, [K][2][PH][PW] (cleared first, then summed)
+    float *grad_mask;            // backward, [K][PH][PW] or null
+    float gamma;
+    int32_t K;
+    int32_t PH, PW, S;
+    int32_t aligned;
+    int32_t nslices;
+    int32_t pad;
+};
+
+hipError_t launch_deform_fwd(DeformArgs a, int feat_dtype, int out_dtype, bool fast,
+                             hipStream_t stream);
+// Clears grad_offset / grad_mask, then adds the gradients (features with atomics).
+hipError_t launch_deform_bwd(DeformArgs a, int feat_dtype, int gout_dtype, bool fast,
+                             hipStream_t stream);
+
 hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float finest_scale,
                             int32_t *out, hipStream_t stream);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);

@@ -252,3 +252,37 @@ def test_multi_head_backward_validation(L):
     assert _multi(L, [_head(plan=FAKE, plan_bytes=8)]) == WORKSPACE
     assert _multi(L, [_head()], zero=3) == INVALID
     assert _multi(L, [_head()], levels=_levels(dtype=1)) == UNSUPPORTED   # fp32 gradients only
+
+
+def test_deform_validation(L):
+    def fwd(levels=None, K=4, off=FAKE, mask=None, gamma=0.1, out=FAKE, odt=0, sr=2, oh=7):
+        lv = levels if levels is not None else _levels()
+        return L.deform_roi_pool_fwd(lv, 2, FAKE, K, FAKE, oh, 7, sr, 1, off, mask, gamma, out,
+                                     odt, None, 0, None)
+
+    def bwd(levels=None, glevels=None, K=4, off=FAKE, mask=None, goff=FAKE, gmask=None, zero=0,
+            gdt=0):
+        lv = levels if levels is not None else _levels()
+        gl = glevels if glevels is not None else _levels()
+        return L.deform_roi_pool_bwd(FAKE, gdt, lv, gl, 2, FAKE, K, FAKE, 7, 7, 2, 1, off, mask,
+                                     0.1, zero, goff, gmask, None, 0, None)
+
+    assert fwd(K=0) == OK
+    assert fwd(off=None) == INVALID
+    assert fwd(off=FAKE + 2) == INVALID
+    assert fwd(mask=FAKE + 1) == INVALID
+    assert fwd(gamma=math.inf) == INVALID
+    assert fwd(gamma=math.nan) == INVALID
+    assert fwd(out=None) == INVALID
+    assert fwd(odt=3) == INVALID
+    assert fwd(sr=-1) == INVALID
+    assert fwd(oh=0) == INVALID
+    assert bwd(K=0) == OK
+    assert bwd(glevels=_levels(dtype=1)) == UNSUPPORTED
+    assert bwd(glevels=_levels(hw=((16, 21), (8, 10)))) == INVALID      # shapes differ
+    assert bwd(glevels=_levels(scales=(0.5, 0.125))) == INVALID         # scales differ
+    assert bwd(goff=None) == INVALID
+    assert bwd(gmask=FAKE) == INVALID                                  # mask gradient, no mask
+    assert bwd(off=None) == INVALID
+    assert bwd(zero=5) == INVALID
+    assert bwd(gdt=2) == INVALID
