@@ -1,5 +1,5 @@
-"""CPU oracle for multi-level RoIAlign, RoI max pooling and deformable RoI pooling --
-TEST INFRASTRUCTURE ONLY.
+"""CPU oracle for multi-level RoIAlign, RoI max pooling, deformable RoI pooling and
+non-maximum suppression -- TEST INFRASTRUCTURE ONLY.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product path never does, and this
@@ -90,6 +90,11 @@ def _bind(lib):
         ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
         ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.oracle_deform_roi_pool_bwd.restype = None
+    lib.oracle_box_iou.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    lib.oracle_box_iou.restype = ctypes.c_float
+    lib.oracle_nms.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                               ctypes.c_float, ctypes.c_int32, ctypes.c_void_p]
+    lib.oracle_nms.restype = ctypes.c_int32
     return lib
 
 
@@ -292,3 +297,27 @@ def deform_roi_pool_bwd(grad_out, features, scales, rois, roi_levels, out_h: int
                                    _ptr(goff), None if gm is None else _ptr(gm), _ptr(soff),
                                    None if sm is None else _ptr(sm))
     return grads, goff, gm, soff, sm
+
+
+def box_iou(a, b, lib=None) -> float:
+    """Binary32 IoU of two boxes (x1, y1, x2, y2), one rounding per operation."""
+    lib = lib or load()
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    b = np.ascontiguousarray(b, dtype=np.float32)
+    return float(lib.oracle_box_iou(_ptr(a), _ptr(b)))
+
+
+def nms(boxes, scores, threshold: float, categories=None, max_keep: int | None = None,
+        lib=None) -> np.ndarray:
+    """Greedy NMS: kept box indices (int32) in rank order."""
+    lib = lib or load()
+    bx = np.ascontiguousarray(boxes, dtype=np.float32)
+    sc = np.ascontiguousarray(scores, dtype=np.float32)
+    N = sc.shape[0]
+    if bx.shape != (N, 4):
+        raise ValueError("boxes must be [N, 4]")
+    cats = None if categories is None else np.ascontiguousarray(categories, dtype=np.int32)
+    keep = np.zeros(max(N, 1), dtype=np.int32)
+    n = lib.oracle_nms(_ptr(bx), _ptr(sc), None if cats is None else _ptr(cats), N,
+                       float(threshold), N if max_keep is None else int(max_keep), _ptr(keep))
+    return keep[:n].copy()

@@ -1,6 +1,6 @@
 /*
  * roi_oracle.c -- plain CPU oracle for multi-level RoIAlign (and RoI max pooling,
- * deformable RoI pooling).
+ * deformable RoI pooling, non-maximum suppression).
  *
  * TEST INFRASTRUCTURE ONLY.  This library exists so that the GPU library can be
  * checked against something slow and obviously correct.  Only the test suite,
@@ -41,6 +41,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 #ifdef _OPENMP
 #include <omp.h>
@@ -795,4 +796,92 @@ void oracle_deform_roi_pool_bwd(const double *grad_out, const double *const *fea
             }
         }
     }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Non-maximum suppression -- the step that turns scored proposals into the    */
+/* RoIs above (the paper runs its bbox operations, NMS among them, on the GPU, */
+/* §1).  Greedy: boxes are ranked by score, highest first (IEEE total order of */
+/* the score bits, -0 below +0, NaN last; equal scores by index); in rank order */
+/* a box is kept unless a kept box of the same category overlaps it with       */
+/* IoU > threshold.  IoU is decided in binary32, one rounding per operation:   */
+/*   iw = max(min(x2a, x2b) - max(x1a, x1b), 0), ih likewise, inter = iw * ih, */
+/*   area = (x2 - x1) * (y2 - y1), uni = (area_a + area_b) - inter,            */
+/*   iou = inter / uni;  suppress iff iou > threshold                          */
+/* (a NaN IoU, e.g. two zero-area boxes, suppresses nothing).                 */
+/* ------------------------------------------------------------------------- */
+
+static uint32_t nms_rank_key(float s)
+{
+    uint32_t u;
+    memcpy(&u, &s, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u)
+        return 0xffffffffu;                    /* NaN: after every number */
+    uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ~asc;                               /* larger score, smaller key */
+}
+
+typedef struct {
+    uint32_t key;
+    int32_t idx;
+} nms_item;
+
+static int nms_item_cmp(const void *pa, const void *pb)
+{
+    const nms_item *a = (const nms_item *)pa, *b = (const nms_item *)pb;
+    if (a->key != b->key)
+        return a->key < b->key ? -1 : 1;
+    return a->idx < b->idx ? -1 : (a->idx > b->idx ? 1 : 0);
+}
+
+float oracle_box_iou(const float *a, const float *b)
+{
+    float ix1 = fmaxf(a[0], b[0]);
+    float iy1 = fmaxf(a[1], b[1]);
+    float ix2 = fminf(a[2], b[2]);
+    float iy2 = fminf(a[3], b[3]);
+    float iw = ix2 - ix1;
+    float ih = iy2 - iy1;
+    iw = fmaxf(iw, 0.0f);
+    ih = fmaxf(ih, 0.0f);
+    float inter = iw * ih;
+    float wa = a[2] - a[0];
+    float ha = a[3] - a[1];
+    float wb = b[2] - b[0];
+    float hb = b[3] - b[1];
+    float area_a = wa * ha;
+    float area_b = wb * hb;
+    float sum = area_a + area_b;
+    float uni = sum - inter;
+    return inter / uni;
+}
+
+/* Kept box indices in rank order (at most max_keep of them); returns their number. */
+int32_t oracle_nms(const float *boxes, const float *scores, const int32_t *cats, int32_t N,
+                   float threshold, int32_t max_keep, int32_t *keep_out)
+{
+    nms_item *it = (nms_item *)malloc(sizeof(nms_item) * (size_t)(N > 0 ? N : 1));
+    char *removed = (char *)calloc((size_t)(N > 0 ? N : 1), 1);
+    for (int32_t i = 0; i < N; ++i) {
+        it[i].key = nms_rank_key(scores[i]);
+        it[i].idx = i;
+    }
+    qsort(it, (size_t)N, sizeof(nms_item), nms_item_cmp);
+    int32_t n = 0;
+    for (int32_t r = 0; r < N && n < max_keep; ++r) {
+        if (removed[r])
+            continue;
+        const int32_t i = it[r].idx;
+        keep_out[n++] = i;
+        for (int32_t q = r + 1; q < N; ++q) {
+            const int32_t j = it[q].idx;
+            if (removed[q] || (cats && cats[j] != cats[i]))
+                continue;
+            if (oracle_box_iou(boxes + 4 * (int64_t)i, boxes + 4 * (int64_t)j) > threshold)
+                removed[q] = 1;
+        }
+    }
+    free(it);
+    free(removed);
+    return n;
 }
