@@ -58,21 +58,22 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle work timed for the CPU baseline (seconds)")
     ap.add_argument("--calibrate-copy", action="store_true")
-    ap.add_argument("--op", default="align", choices=["align", "pool", "heads", "deform"],
+    ap.add_argument("--op", default="align", choices=["align", "pool", "heads", "deform", "nms"],
                     help="align: RoIAlign (the benchmark); pool: RoI max pooling on the same "
                          "workload (plan, roi_pool_fwd, roi_pool_bwd with clearing); heads: "
                          "box and mask heads on one pyramid (workload 2: the batch-2 box and "
                          "mask RoIs; workload 5: both heads of the batch-16 step), one fused "
                          "backward, timed against two separate backward calls; deform: "
                          "modulated deformable RoI pooling on the workload (offsets "
-                         "N(0, 0.3^2), modulation U(0, 1), gamma 0.1)")
+                         "N(0, 0.3^2), modulation U(0, 1), gamma 0.1); nms: greedy NMS of "
+                         "two images of 4096 scored proposals in one call (IoU 0.7)")
     return ap.parse_args()
 
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for name in ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip",
-                 "deform.hip", "api.hip"):
+                 "deform.hip", "nms.hip", "api.hip"):
         with open(os.path.join(ROOT, "paper_1906_07155_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -127,6 +128,9 @@ def main():
         return
     if args.op == "deform":
         main_deform(args)
+        return
+    if args.op == "nms":
+        main_nms(args)
         return
 
     import torch
@@ -700,6 +704,85 @@ def main_deform(args):
         "extra": {"kernel_ms": {n: round(v, 5) for n, v in per.items()},
                   "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
                   "footprint_px": fp, "kernel_source_hash": kernel_source_hash()},
+    }
+    print(json.dumps(result), flush=True)
+
+
+def main_nms(args):
+    """Greedy NMS of RPN-like proposals: two images of 4096 scored boxes (centres uniform
+    in a 1333 x 800 image, sides log-uniform in [8, 600] px), the image as the category,
+    IoU threshold 0.7, every kept box returned.  One step is one box_nms call."""
+    import torch
+
+    import oracle
+    import paper_1906_07155_amd as rex
+    from paper_1906_07155_amd import workloads
+
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(workloads.BASE_SEED + 60)
+    per, n_img = 4096, 2
+    boxes = []
+    for _ in range(n_img):
+        cx, cy = rng.uniform(0, 1333, per), rng.uniform(0, 800, per)
+        w = np.exp(rng.uniform(np.log(8), np.log(600), per))
+        h = np.exp(rng.uniform(np.log(8), np.log(600), per))
+        boxes.append(np.stack([cx - w / 2, cy - h / 2, cx + w / 2, cy + h / 2], 1))
+    boxes_np = np.concatenate(boxes).astype(np.float32)
+    scores_np = rng.uniform(0, 1, n_img * per).astype(np.float32)
+    cats_np = np.repeat(np.arange(n_img, dtype=np.int32), per)
+    N = boxes_np.shape[0]
+    b = torch.from_numpy(boxes_np).to(dev)
+    sc = torch.from_numpy(scores_np).to(dev)
+    ct = torch.from_numpy(cats_np).to(dev)
+    keep, nk = rex.box_nms(b, sc, 0.7, ct)
+    import ctypes
+    n = ctypes.c_size_t(0)
+    rex.lib().box_nms_workspace_size(N, ctypes.byref(n))
+    ws = torch.empty(n.value, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        rex.box_nms(b, sc, 0.7, ct, workspace=ws, keep=keep, num_keep=nk)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        rex.box_nms(b, sc, 0.7, ct, workspace=ws, keep=keep, num_keep=nk)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    kept = int(nk.item())
+    # pairwise overlap tests of the upper triangle (every pair, also across categories),
+    # about 16 fp32 operations each: the arithmetic the mask kernel must do
+    pairs = N * (N - 1) // 2
+    flops = pairs * 16
+    achieved = flops / (ms * 1e-3) / 1e12
+    cpu = None
+    if not args.no_cpu_baseline:
+        lib = oracle.load()
+        elapsed, passes = 0.0, 0
+        while elapsed < args.cpu_seconds:
+            c0 = time.perf_counter()
+            oracle.nms(boxes_np, scores_np, 0.7, cats_np, lib=lib)
+            elapsed += time.perf_counter() - c0
+            passes += 1
+        cpu = {"value": round(N * passes / elapsed, 1), "unit": "boxes/s", "cores": 1,
+               "kind": "oracle", "sample": "all %d boxes, %d passes in %.1f s wall" % (
+                   N, passes, elapsed)}
+    result = {
+        "metric": "greedy NMS boxes/sec (proposal selection before the RoI extraction)",
+        "value": round(N / (ms * 1e-3), 1), "unit": "boxes/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (uniform centres, log-uniform sizes, uniform scores; no COCO)",
+        "config": {"workload": "NMS of 2 x 4096 proposals, IoU 0.7, image as category",
+                   "num_boxes": N, "kept": kept},
+        "roofline": {"bound": "alu", "achieved": round(achieved, 3), "peak": 157.3,
+                     "unit": "TFLOP/s", "frac": round(achieved / 157.3, 5), "traffic": None,
+                     "kernel": "box_nms (sort + overlap masks + scan)", "flops_per_launch": flops,
+                     "launch_ms": round(ms, 5)},
+        "cpu_baseline": cpu,
+        "extra": {"kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(result), flush=True)
 

@@ -294,6 +294,32 @@ re_status_t roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype, const int
                          int32_t num_levels, int32_t zero_init, const void *plan,
                          size_t plan_bytes, void *stream);
 
+/* f4 -- greedy non-maximum suppression, the step that turns a dense head's scored
+ * boxes into the proposals whose RoI features the functions above extract (the paper
+ * runs its bbox operations on the GPU, §1).  Boxes are ranked by score, highest first:
+ * scores compare by the IEEE total order of their bits (-0 below +0), NaN ranks after
+ * every number, equal scores rank by index.  In rank order a box is kept unless a kept
+ * box of the same category overlaps it with IoU > iou_threshold, IoU decided in binary32
+ * with one rounding per operation in this order:
+ *   iw = max(min(x2a, x2b) - max(x1a, x1b), 0), ih likewise, inter = iw * ih,
+ *   area = (x2 - x1) * (y2 - y1), union = (area_a + area_b) - inter, iou = inter / union
+ * (a NaN IoU, e.g. of two zero-area boxes, removes nothing).  Boxes of different
+ * categories never interact, so several images or classes go in one call by giving
+ * each its own category.
+ *   boxes: device float[num_boxes][4] (x1, y1, x2, y2);  scores: device float[num_boxes];
+ *   categories: device int32[num_boxes] or NULL (one category);
+ *   num_boxes in [0, RE_MAX_NMS_BOXES] (RE_ERR_UNSUPPORTED above);
+ *   keep_out: device int32[min(num_boxes, max_keep)]: the kept box indices in rank
+ *     order, then -1;  num_keep_out: device int32[1], the number kept (at most
+ *     max_keep >= 0);  iou_threshold: not NaN;
+ *   workspace: device, 256-byte aligned, box_nms_workspace_size() bytes. */
+#define RE_MAX_NMS_BOXES 8192
+re_status_t box_nms_workspace_size(int64_t num_boxes, size_t *bytes);
+re_status_t box_nms(const float *boxes, const float *scores, const int32_t *categories,
+                    int64_t num_boxes, float iou_threshold, int64_t max_keep, int32_t *keep_out,
+                    int32_t *num_keep_out, void *workspace, size_t workspace_bytes,
+                    void *stream);
+
 /* Static description of a status code. */
 const char *roi_extract_status_str(re_status_t status);
 

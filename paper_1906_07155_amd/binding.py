@@ -74,6 +74,8 @@ SIGNATURES = {
                             _F32, _VP, _I32, _VP, _SZ, _VP],
     "deform_roi_pool_bwd": [_VP, _I32, _LEVELS, _LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _I32,
                             _I32, _VP, _VP, _F32, _I32, _VP, _VP, _VP, _SZ, _VP],
+    "box_nms_workspace_size": [_I64, ctypes.POINTER(_SZ)],
+    "box_nms": [_VP, _VP, _VP, _I64, _F32, _I64, _VP, _VP, _VP, _SZ, _VP],
     "roi_pool_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _VP, _I32, _VP, _VP, _SZ, _VP],
     "roi_pool_bwd": [_VP, _I32, _VP, _VP, _I64, _VP, _I32, _I32, _LEVELS, _I32, _I32, _VP, _SZ,
                      _VP],
@@ -434,3 +436,33 @@ def deform_roi_pool_bwd(grad_out, features: Sequence, rois, roi_levels, offset, 
                                     grad_mask.data_ptr() if grad_mask is not None else None,
                                     ws, wsb, stream_handle(stream)), "deform_roi_pool_bwd")
     return grads, grad_offset, grad_mask
+
+
+def box_nms(boxes, scores, iou_threshold: float, categories=None, max_keep: int | None = None,
+            workspace=None, keep=None, num_keep=None, stream=None):
+    """Greedy NMS on the GPU.  Returns (keep int32 [min(N, max_keep)]: kept indices in rank
+    order then -1, num_keep int32 [1]); both stay on the device."""
+    torch = _torch()
+    _need_cuda(boxes, "boxes")
+    N = scores.shape[0]
+    if boxes.dtype != torch.float32 or tuple(boxes.shape) != (N, 4) or not boxes.is_contiguous():
+        raise ValueError("boxes must be a contiguous float32 [N, 4] tensor")
+    if scores.dtype != torch.float32 or not scores.is_contiguous():
+        raise ValueError("scores must be a contiguous float32 [N] tensor")
+    if categories is not None and (categories.dtype != torch.int32 or
+                                   not categories.is_contiguous()):
+        raise ValueError("categories must be a contiguous int32 [N] tensor")
+    mk = N if max_keep is None else int(max_keep)
+    n = ctypes.c_size_t(0)
+    check(lib().box_nms_workspace_size(N, ctypes.byref(n)), "box_nms_workspace_size")
+    if workspace is None:
+        workspace = torch.empty(n.value, dtype=torch.uint8, device=boxes.device)
+    if keep is None:
+        keep = torch.empty(max(min(N, mk), 1), dtype=torch.int32, device=boxes.device)
+    if num_keep is None:
+        num_keep = torch.empty(1, dtype=torch.int32, device=boxes.device)
+    check(lib().box_nms(boxes.data_ptr(), scores.data_ptr(),
+                        categories.data_ptr() if categories is not None else None, N,
+                        float(iou_threshold), mk, keep.data_ptr(), num_keep.data_ptr(),
+                        workspace.data_ptr(), workspace.numel(), stream_handle(stream)), "box_nms")
+    return keep[:min(N, mk)], num_keep

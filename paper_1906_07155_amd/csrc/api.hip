@@ -776,4 +776,68 @@ re_status_t deform_roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype,
     return from_hip(launch_deform_bwd(a, levels[0].dtype, grad_out_dtype, fast, s));
 }
 
+// ---------------------------------------------------------------------------
+// Non-maximum suppression
+// ---------------------------------------------------------------------------
+
+namespace {
+struct NmsLayout {
+    size_t order, sboxes, scats, mask, total;
+};
+NmsLayout nms_layout(int64_t N) {
+    NmsLayout L{};
+    const int64_t nw = (N + 63) / 64;
+    L.order = 0;
+    L.sboxes = align256(static_cast<size_t>(N) * 4);
+    L.scats = L.sboxes + align256(static_cast<size_t>(N) * 16);
+    L.mask = L.scats + align256(static_cast<size_t>(N) * 4);
+    L.total = L.mask + align256(static_cast<size_t>(N) * static_cast<size_t>(nw) * 8);
+    return L;
+}
+}  // namespace
+
+re_status_t box_nms_workspace_size(int64_t num_boxes, size_t *bytes) {
+    if (!bytes || num_boxes < 0 || num_boxes > kNmsMaxBoxes) return RE_ERR_INVALID_ARG;
+    *bytes = std::max<size_t>(nms_layout(num_boxes).total, 256);
+    return RE_OK;
+}
+
+re_status_t box_nms(const float *boxes, const float *scores, const int32_t *categories,
+                    int64_t num_boxes, float iou_threshold, int64_t max_keep, int32_t *keep_out,
+                    int32_t *num_keep_out, void *workspace, size_t workspace_bytes,
+                    void *stream) {
+    if (num_boxes < 0) return RE_ERR_INVALID_ARG;
+    if (num_boxes > kNmsMaxBoxes) return RE_ERR_UNSUPPORTED;
+    if (max_keep < 0 || !num_keep_out || std::isnan(iou_threshold)) return RE_ERR_INVALID_ARG;
+    if (num_boxes > 0 && (!boxes || !scores)) return RE_ERR_INVALID_ARG;
+    if (num_boxes > 0 && max_keep > 0 && !keep_out) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(boxes) % 4 || reinterpret_cast<uintptr_t>(scores) % 4 ||
+        reinterpret_cast<uintptr_t>(categories) % 4 || reinterpret_cast<uintptr_t>(keep_out) % 4 ||
+        reinterpret_cast<uintptr_t>(num_keep_out) % 4)
+        return RE_ERR_INVALID_ARG;
+    const NmsLayout lay = nms_layout(num_boxes);
+    if (num_boxes > 0) {
+        if (!workspace || reinterpret_cast<uintptr_t>(workspace) % 256) return RE_ERR_WORKSPACE;
+        if (workspace_bytes < lay.total) return RE_ERR_WORKSPACE;
+    }
+    char *ws = static_cast<char *>(workspace);
+    NmsArgs a{};
+    a.boxes = boxes;
+    a.scores = scores;
+    a.categories = categories;
+    if (num_boxes > 0) {
+        a.order = reinterpret_cast<int32_t *>(ws + lay.order);
+        a.sboxes = reinterpret_cast<float4 *>(ws + lay.sboxes);
+        a.scats = reinterpret_cast<int32_t *>(ws + lay.scats);
+        a.mask = reinterpret_cast<uint64_t *>(ws + lay.mask);
+    }
+    a.keep = keep_out;
+    a.num_keep = num_keep_out;
+    a.max_keep = max_keep;
+    a.threshold = iou_threshold;
+    a.N = static_cast<int32_t>(num_boxes);
+    a.nw = static_cast<int32_t>((num_boxes + 63) / 64);
+    return from_hip(launch_nms(a, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -159,6 +159,27 @@ hipError_t launch_deform_fwd(DeformArgs a, int feat_dtype, int out_dtype, bool f
 hipError_t launch_deform_bwd(DeformArgs a, int feat_dtype, int gout_dtype, bool fast,
                              hipStream_t stream);
 
+// Greedy non-maximum suppression.
+constexpr int kNmsMaxBoxes = 8192;   // boxes per call: the sort's 64-bit items fill 64 KiB of LDS
+
+struct NmsArgs {
+    const float *boxes;          // [N][4]
+    const float *scores;         // [N]
+    const int32_t *categories;   // [N] or null
+    int32_t *order;              // workspace: box index of every rank
+    float4 *sboxes;              // workspace: boxes in rank order
+    int32_t *scats;              // workspace: categories in rank order
+    uint64_t *mask;              // workspace: [N][nw] overlap bits of the upper triangle
+    int32_t *keep;               // [min(N, max_keep)]
+    int32_t *num_keep;           // [1]
+    int64_t max_keep;
+    float threshold;
+    int32_t N;
+    int32_t nw;                  // 64-box blocks
+};
+
+hipError_t launch_nms(NmsArgs a, hipStream_t stream);
+
 hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float finest_scale,
                             int32_t *out, hipStream_t stream);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);

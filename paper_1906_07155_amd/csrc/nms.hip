@@ -1,0 +1,235 @@
+// nms.hip -- greedy non-maximum suppression of scored boxes.
+//
+// The proposals a two-stage detector extracts RoI features for come out of NMS over
+// the dense head's scored boxes; MMDetection runs such bbox operations on the GPU (§1).
+// Definition (rank order, tie rules, binary32 IoU decision) in include/roi_extract.h.
+//
+// Three kernels on one stream:
+//   nms_sort_kernel   one 1024-thread workgroup: every box becomes a 64-bit item
+//                     (rank key << 32 | index), and a bitonic network in LDS sorts them
+//                     (key first, index second); the boxes and categories are then
+//                     gathered in rank order.
+//   nms_mask_kernel   one 64-lane workgroup per (row block, column block) of the upper
+//                     triangle: lane r of row block I tests its box against the 64 boxes
+//                     of column block J (staged in LDS) and writes the 64-bit mask of
+//                     later boxes of its category that it overlaps by IoU > threshold.
+//   nms_scan_kernel   one 1024-thread workgroup walks the row blocks in rank order: wave
+//                     0 resolves a block sequentially from its diagonal masks (one lane
+//                     read per box) and writes the kept indices; then every thread ORs the
+//                     kept rows of its group into its later words and adds them to the
+//                     removal words in LDS (lanes over words, so an atomic instruction
+//                     touches 64 different words), the rows having been loaded one block
+//                     ahead so their latency hides behind the resolution.
+#include "internal.hpp"
+
+namespace rex {
+
+constexpr int kNmsSortThreads = 1024;
+
+// Rank key of a score: IEEE total order of the bits, largest first; NaN after every
+// number.
+__device__ __forceinline__ uint32_t nms_key(float s) {
+    const uint32_t u = __float_as_uint(s);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0xffffffffu;
+    const uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ~asc;
+}
+
+// Binary32 IoU, one rounding per operation in the order of the definition.
+__device__ __forceinline__ float nms_iou(float4 a, float4 b) {
+    const float ix1 = fmaxf(a.x, b.x);
+    const float iy1 = fmaxf(a.y, b.y);
+    const float ix2 = fminf(a.z, b.z);
+    const float iy2 = fminf(a.w, b.w);
+    float iw = ix2 - ix1;
+    float ih = iy2 - iy1;
+    iw = fmaxf(iw, 0.0f);
+    ih = fmaxf(ih, 0.0f);
+    const float inter = iw * ih;
+    const float wa = a.z - a.x;
+    const float ha = a.w - a.y;
+    const float wb = b.z - b.x;
+    const float hb = b.w - b.y;
+    const float area_a = wa * ha;
+    const float area_b = wb * hb;
+    const float sum = area_a + area_b;
+    const float uni = sum - inter;
+    return inter / uni;
+}
+
+__global__ __launch_bounds__(kNmsSortThreads) void nms_sort_kernel(NmsArgs a) {
+    __shared__ uint64_t items[kNmsMaxBoxes];
+    const int N = a.N;
+    int P = 1;
+    while (P < N) P <<= 1;
+    for (int i = threadIdx.x; i < P; i += kNmsSortThreads) {
+        uint64_t v = (static_cast<uint64_t>(0xffffffffu) << 32) | 0x7fffffffu;   // pad: last
+        if (i < N) v = (static_cast<uint64_t>(nms_key(a.scores[i])) << 32) | static_cast<uint32_t>(i);
+        items[i] = v;
+    }
+    __syncthreads();
+    for (int k = 2; k <= P; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = threadIdx.x; i < P; i += kNmsSortThreads) {
+                const int p = i ^ j;
+                if (p > i) {
+                    const uint64_t x = items[i], y = items[p];
+                    const bool up = (i & k) == 0;
+                    if ((x > y) == up) {
+                        items[i] = y;
+                        items[p] = x;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int r = threadIdx.x; r < N; r += kNmsSortThreads) {
+        const int idx = static_cast<int>(static_cast<uint32_t>(items[r]));
+        a.order[r] = idx;
+        const float *b = a.boxes + 4 * static_cast<int64_t>(idx);
+        a.sboxes[r] = make_float4(b[0], b[1], b[2], b[3]);
+        a.scats[r] = a.categories ? a.categories[idx] : 0;
+    }
+}
+
+__global__ __launch_bounds__(64) void nms_mask_kernel(NmsArgs a) {
+    __shared__ float4 sb[64];
+    __shared__ int sc[64];
+    const int nb = a.nw;
+    const int ib = static_cast<int>(blockIdx.x) / nb;
+    const int jb = static_cast<int>(blockIdx.x) - ib * nb;
+    if (jb < ib) return;   // uniform over the workgroup: the lower triangle is never read
+    const int lane = threadIdx.x;
+    const int j0 = jb * 64;
+    if (j0 + lane < a.N) {
+        sb[lane] = a.sboxes[j0 + lane];
+        sc[lane] = a.scats[j0 + lane];
+    }
+    __syncthreads();
+    const int i = ib * 64 + lane;
+    if (i >= a.N) return;
+    const float4 bi = a.sboxes[i];
+    const int ci = a.scats[i];
+    const int jn = min(64, a.N - j0);
+    uint64_t bits = 0;
+    for (int jj = 0; jj < jn; ++jj) {
+        const int j = j0 + jj;
+        if (j > i && sc[jj] == ci && nms_iou(bi, sb[jj]) > a.threshold) bits |= uint64_t(1) << jj;
+    }
+    a.mask[static_cast<int64_t>(i) * nb + jb] = bits;
+}
+
+// A block's propagation over the scan workgroup: waves over groups of rows, lanes over
+// later words.
+constexpr int kNmsScanThreads = 1024;
+constexpr int kNmsRowsPerWave = 64 / (kNmsScanThreads / 64);           // 4
+constexpr int kNmsWordsPerLane = (kNmsMaxBoxes / 64 + 63) / 64;        // 2
+constexpr int kNmsPairs = kNmsRowsPerWave * kNmsWordsPerLane;
+
+__global__ __launch_bounds__(kNmsScanThreads) void nms_scan_kernel(NmsArgs a) {
+    __shared__ uint64_t removed[kNmsMaxBoxes / 64];
+    __shared__ uint64_t s_kept;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int nb = a.nw;
+    const int limit = static_cast<int>(min<int64_t>(a.max_keep, a.N));
+    for (int w = tid; w < nb; w += kNmsScanThreads) removed[w] = 0;
+
+    // Rows of a block as loaded ahead: wave 0 its diagonal words, every thread its share
+    // of the (row, later word) pairs.  Two blocks are in flight: the words of block b + 1
+    // are requested before block b is resolved, so their latency hides behind it.
+    auto load_diag = [&](int b) -> uint64_t {
+        const int i = b * 64 + lane;
+        return (b < nb && i < a.N) ? a.mask[static_cast<int64_t>(i) * nb + b] : 0;
+    };
+    // thread (wave, lane) holds rows 4 wave .. 4 wave + 3 of the block at the later words
+    // b + 1 + lane and b + 65 + lane: pf[4 j + r] = row 4 wave + r, word b + 1 + lane + 64 j
+    auto load_pairs = [&](int b, uint64_t (&pf)[kNmsPairs]) {
+#pragma unroll
+        for (int j = 0; j < kNmsWordsPerLane; ++j) {
+#pragma unroll
+            for (int r = 0; r < kNmsRowsPerWave; ++r) {
+                const int w = b + 1 + lane + 64 * j;
+                const int row = b * 64 + wave * kNmsRowsPerWave + r;
+                pf[j * kNmsRowsPerWave + r] =
+                    (b < nb && w < nb && row < a.N) ? a.mask[static_cast<int64_t>(row) * nb + w] : 0;
+            }
+        }
+    };
+    uint64_t pf_cur[kNmsPairs], pf_next[kNmsPairs];
+    uint64_t diag_cur = wave == 0 ? load_diag(0) : 0;
+    load_pairs(0, pf_cur);
+    __syncthreads();
+    int count = 0;   // the same in every thread
+    for (int b = 0; b < nb; ++b) {
+        uint64_t diag_next = 0;
+        if (wave == 0) diag_next = load_diag(b + 1);
+        load_pairs(b + 1, pf_next);
+        if (wave == 0) {
+            // sequential within the block: box t is kept unless a kept box of an earlier
+            // block or an earlier kept box of this block removed it
+            const int nrow = min(64, a.N - b * 64);
+            uint64_t rem = removed[b];
+            uint64_t kept = 0;
+            for (int t = 0; t < nrow; ++t) {
+                if (!((rem >> t) & 1)) {
+                    kept |= uint64_t(1) << t;
+                    const uint32_t lo =
+                        __builtin_amdgcn_readlane(static_cast<uint32_t>(diag_cur), t);
+                    const uint32_t hi =
+                        __builtin_amdgcn_readlane(static_cast<uint32_t>(diag_cur >> 32), t);
+                    rem |= (static_cast<uint64_t>(hi) << 32) | lo;
+                }
+            }
+            if ((kept >> lane) & 1) {
+                const int rank = count + __popcll(kept & ((uint64_t(1) << lane) - 1));
+                if (rank < limit) a.keep[rank] = a.order[b * 64 + lane];
+            }
+            if (lane == 0) s_kept = kept;
+        }
+        __syncthreads();
+        const uint64_t kept = s_kept;
+        count += __popcll(kept);
+        if (count >= limit) break;   // uniform over the workgroup
+        // the kept rows remove boxes of later blocks: each thread ORs its kept rows of a
+        // word, then adds them to the word in LDS (the 64 lanes of an atomic instruction
+        // address 64 different words)
+#pragma unroll
+        for (int j = 0; j < kNmsWordsPerLane; ++j) {
+            uint64_t v = 0;
+#pragma unroll
+            for (int r = 0; r < kNmsRowsPerWave; ++r)
+                if ((kept >> (wave * kNmsRowsPerWave + r)) & 1) v |= pf_cur[j * kNmsRowsPerWave + r];
+            const int w = b + 1 + lane + 64 * j;
+            if (v != 0 && w < nb)
+                atomicOr(reinterpret_cast<unsigned long long *>(&removed[w]),
+                         static_cast<unsigned long long>(v));
+        }
+#pragma unroll
+        for (int m = 0; m < kNmsPairs; ++m) pf_cur[m] = pf_next[m];
+        diag_cur = diag_next;
+        __syncthreads();   // removal words final before block b + 1 is resolved
+    }
+    const int n = min(count, limit);
+    for (int r = n + tid; r < limit; r += kNmsScanThreads) a.keep[r] = -1;
+    if (tid == 0) a.num_keep[0] = n;
+}
+
+hipError_t launch_nms(NmsArgs a, hipStream_t stream) {
+    if (a.N == 0) {
+        // nothing kept: the count is written by the scan with an empty loop
+        nms_scan_kernel<<<1, kNmsScanThreads, 0, stream>>>(a);
+        return hipGetLastError();
+    }
+    nms_sort_kernel<<<1, kNmsSortThreads, 0, stream>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    nms_mask_kernel<<<static_cast<uint32_t>(a.nw * a.nw), 64, 0, stream>>>(a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    nms_scan_kernel<<<1, kNmsScanThreads, 0, stream>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace rex

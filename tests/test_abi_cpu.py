@@ -286,3 +286,31 @@ def test_deform_validation(L):
     assert bwd(off=None) == INVALID
     assert bwd(zero=5) == INVALID
     assert bwd(gdt=2) == INVALID
+
+
+def test_nms_validation(L):
+    n = ctypes.c_size_t(0)
+    assert L.box_nms_workspace_size(100, ctypes.byref(n)) == OK and n.value >= 100 * (4 + 16 + 4 + 16)
+    assert L.box_nms_workspace_size(-1, ctypes.byref(n)) == INVALID
+    assert L.box_nms_workspace_size(8193, ctypes.byref(n)) == INVALID
+    assert L.box_nms_workspace_size(10, None) == INVALID
+
+    def nms(N=100, boxes=FAKE, scores=FAKE, cats=None, thr=0.5, mk=100, keep=FAKE, nk=FAKE,
+            ws=FAKE, wsb=None):
+        return L.box_nms(boxes, scores, cats, N, thr, mk, keep, nk, ws,
+                         n.value if wsb is None else wsb, None)
+
+    assert L.box_nms_workspace_size(100, ctypes.byref(n)) == OK
+    assert nms(N=8193) == UNSUPPORTED
+    assert nms(N=-1) == INVALID
+    assert nms(thr=math.nan) == INVALID
+    assert nms(mk=-1) == INVALID
+    assert nms(nk=None) == INVALID
+    assert nms(boxes=None) == INVALID
+    assert nms(scores=None) == INVALID
+    assert nms(keep=None) == INVALID
+    assert nms(boxes=FAKE + 2) == INVALID
+    assert nms(cats=FAKE + 1) == INVALID
+    assert nms(ws=None) == WORKSPACE
+    assert nms(ws=FAKE + 64) == WORKSPACE
+    assert nms(wsb=16) == WORKSPACE
