@@ -285,6 +285,78 @@ __device__ __forceinline__ uint32_t byte_mask(uint64_t b) {
     return static_cast<uint32_t>((b * 0x0102040810204080ull) >> 56);
 }
 
+// First / last set bit of a multi-word ballot, -1 if none (uniform scalar values).
+template <int P>
+__device__ __forceinline__ int first_set(const uint64_t (&b)[P]) {
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+        if (b[p]) return p * 64 + __builtin_ctzll(b[p]);
+    return -1;
+}
+template <int P>
+__device__ __forceinline__ int last_set(const uint64_t (&b)[P]) {
+#pragma unroll
+    for (int p = P - 1; p >= 0; --p)
+        if (b[p]) return p * 64 + 63 - __builtin_clzll(b[p]);
+    return -1;
+}
+
+// acc[r][q] += yrow[r] * X[q] for the rows r0 .. r0 + NR - 1 of the quadrant.
+template <int R0, int NR>
+__device__ __forceinline__ void outer_rows(float (&acc)[8][8], const float *yrow,
+                                           const float (&X)[8]) {
+    static_assert(R0 % 4 == 0 && NR % 4 == 0, "rows in aligned groups of 4");
+    float yr[8];
+#pragma unroll
+    for (int h = R0 / 4; h < (R0 + NR) / 4; ++h) {
+        const float4 y = *reinterpret_cast<const float4 *>(yrow + 4 * h);
+        yr[4 * h] = y.x;
+        yr[4 * h + 1] = y.y;
+        yr[4 * h + 2] = y.z;
+        yr[4 * h + 3] = y.w;
+    }
+#pragma unroll
+    for (int rr = R0; rr < R0 + NR; ++rr)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[rr][q] = fmaf(yr[rr], X[q], acc[rr][q]);
+}
+
+// One RoI's contribution to a wave's 8x8 quadrant, for the bin rows pha..phb that
+// reach the quadrant's rows and the npw bin columns pwa.. that reach its columns:
+//   X[q] = sum over pw of Wx[pw][q] * g[ph][pw]
+//   acc[r][q] += Wy[ph][r] * X[q]
+// gl points at g[0][pwa] of this lane's channel, wxa at Wx[pwa][0], wy at Wy[0][0];
+// yb holds the nonzero pattern of Wy (bit ph * 8 + r), which decides the half
+// quadrants (rows 0-3, 4-7) a bin row updates.
+template <typename TG, int PW, int YP>
+__device__ __forceinline__ void gather_rows(float (&acc)[8][8], const uint32_t *gl,
+                                            const float *wxa, const float *wy,
+                                            const uint64_t (&yb)[YP], int pha, int phb, int npw) {
+    for (int ph = pha; ph <= phb; ++ph) {
+        const uint32_t rb = static_cast<uint32_t>(yb[YP == 1 ? 0 : ph >> 3] >> ((ph & 7) * 8)) & 0xffu;
+        if (rb == 0) continue;
+        const uint32_t *gr = gl + ph * PW;
+        // The run of bins is unrolled up to its longest possible length, so every
+        // LDS address is a fixed offset from gr / wxa (no loop-carried pointers, which
+        // would hide from the compiler that these reads do not touch the slot being
+        // filled by the copy in flight).
+        float X[8];
+#pragma unroll
+        for (int i = 0; i < PW; ++i) {
+            if (i >= npw) break;
+            const float gv = raw_to_f32<TG>(gr[i]);
+            const float4 w0 = *reinterpret_cast<const float4 *>(wxa + i * 8);
+            const float4 w1 = *reinterpret_cast<const float4 *>(wxa + i * 8 + 4);
+            const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+            for (int q = 0; q < 8; ++q) X[q] = i == 0 ? w[q] * gv : fmaf(w[q], gv, X[q]);
+        }
+        // rows 0-3 and 4-7 of the quadrant are updated only if the bin row reaches them
+        if (rb & 0x0fu) outer_rows<0, 4>(acc, wy + ph * 8, X);
+        if (rb & 0xf0u) outer_rows<4, 4>(acc, wy + ph * 8, X);
+    }
+}
+
 // LDS of one head's pass over a tile (see gather_phase).
 template <typename TG, int PH, int PW, int S>
 struct GatherSmem {
@@ -299,7 +371,6 @@ struct GatherSmem {
     // the element size, so a block holds one 32-bit word per element (a bf16 value in
     // its low half).
     static constexpr int NBUF = 2 * GB * 4 <= 53248 ? 2 : 1;
-    __align__(16) uint32_t g[NBUF][GB];
     Tap tap[2][NR + NCOL];
     __align__(16) float wy[4][PH * T];
     __align__(16) float wx[4][PW * T];
@@ -307,6 +378,13 @@ struct GatherSmem {
     float ax[64][4];
     int rng[64][4];   // per kept RoI: tap extent ymin, ymax, xmin, xmax
     int n;
+};
+
+// One staged gradient block.  The ring's slots are separate LDS variables, so the
+// compiler can tell that reading one slot does not depend on the copy into the other.
+template <typename TG, int PH, int PW, int S>
+struct GatherBlock {
+    __align__(16) uint32_t g[GatherSmem<TG, PH, PW, S>::GB];
 };
 
 // Where a workgroup of the quadrant-form gather sits: the tile's level and image,
@@ -326,7 +404,8 @@ struct GatherTile {
 template <typename TG, int PH, int PW, int S>
 __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTable &lv, int t,
                                              const GatherTile &x, float (&acc)[8][8],
-                                             GatherSmem<TG, PH, PW, S> &sm) {
+                                             GatherSmem<TG, PH, PW, S> &sm, uint32_t *slot0,
+                                             uint32_t *slot1) {
     using SM = GatherSmem<TG, PH, PW, S>;
     constexpr int NR = SM::NR, NCOL = SM::NCOL, T = SM::T, NB = SM::NB, GB = SM::GB;
     constexpr int NBUF = SM::NBUF;
@@ -357,7 +436,7 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
     // uniform run base plus 4 bytes per lane, the global offset the lane's own); the
     // range check supplies the zeros past the valid channels.
     const int nvalid = x.nch * NB;
-    auto fetch = [&](int j, int buf) {
+    auto fetch = [&](int j, uint32_t *gdst) {
         const int k = uniform_i(sm.k[j]);   // one resource for the wave, no waterfall
         const char *src = static_cast<const char *>(h.gout) +
                           (static_cast<int64_t>(x.cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
@@ -367,7 +446,7 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
         for (int m = 0; m < (NDMA + 3) / 4; ++m) {
             const int run = wave + 4 * m;
             if (m < NDMA / 4 || run < NDMA) {
-                auto *dst = (__attribute__((address_space(3))) void *)(&sm.g[buf][64 * run]);
+                auto *dst = (__attribute__((address_space(3))) void *)(gdst + 64 * run);
                 const uint32_t off = static_cast<uint32_t>(64 * run + lane) * uint32_t(sizeof(TG));
                 if constexpr (sizeof(TG) == 4)
                     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 4, off, 0, 0, 0);
@@ -395,12 +474,14 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
         }
     };
     // Contribution of kept RoI j to this wave's quadrant.
-    auto consume = [&](int j, int buf, int tb) {
+    auto consume = [&](int j, const uint32_t *gsrc, int tb) {
         const int ymin = sm.rng[j][0], ymax = sm.rng[j][1];
         const int xmin = sm.rng[j][2], xmax = sm.rng[j][3];
         if (!x.wave_on || ymax < R0 || ymin >= R0 + T || xmax < Q0 || xmin >= Q0 + T) return;
         // This quadrant's separable weights and which bin rows / columns reach it.
-        uint32_t ymask = 0, xmask = 0;
+        // Ballot bit p * 64 + i marks a nonzero weight of lane u = p * 64 + i
+        // (u = bin * 8 + row or column of the quadrant).
+        uint64_t yb[YP], xb[XP];
 #pragma unroll
         for (int p = 0; p < YP; ++p) {
             const int u = p * 64 + lane;
@@ -411,21 +492,16 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
                 float w = 0.0f;
 #pragma unroll
                 for (int iy = 0; iy < S; ++iy) {
+                    // branch-free: an invalid tap has lo = hi = -1 and matches no row
                     const Tap tp = sm.tap[tb][ph * S + iy];
-                    if (tp.lo >= 0) {
-                        if (tp.lo == R) {
-                            w += tp.wlo;
-                            hit = true;
-                        }
-                        if (tp.hi == R) {
-                            w += tp.whi;
-                            hit = true;
-                        }
-                    }
+                    const bool a = tp.lo == R, c = tp.hi == R;
+                    w += a ? tp.wlo : 0.0f;
+                    w += c ? tp.whi : 0.0f;
+                    hit = hit || a || c;
                 }
                 wy[u] = w * inv_count;
             }
-            ymask |= byte_mask(__ballot(hit)) << (p * 8);
+            yb[p] = __ballot(hit);
         }
 #pragma unroll
         for (int p = 0; p < XP; ++p) {
@@ -438,51 +514,25 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
 #pragma unroll
                 for (int ix = 0; ix < S; ++ix) {
                     const Tap tp = sm.tap[tb][NR + pw * S + ix];
-                    if (tp.lo >= 0) {
-                        if (tp.lo == Q) {
-                            w += tp.wlo;
-                            hit = true;
-                        }
-                        if (tp.hi == Q) {
-                            w += tp.whi;
-                            hit = true;
-                        }
-                    }
+                    const bool a = tp.lo == Q, c = tp.hi == Q;
+                    w += a ? tp.wlo : 0.0f;
+                    w += c ? tp.whi : 0.0f;
+                    hit = hit || a || c;
                 }
                 wx[u] = w;
             }
-            xmask |= byte_mask(__ballot(hit)) << (p * 8);
+            xb[p] = __ballot(hit);
         }
+        // Sample positions grow with the bin index, so the bins reaching the quadrant's
+        // rows (columns) form one run [pha, phb] ([pwa, pwb]).
+        const int pha = first_set(yb) / T, phb = last_set(yb) / T;
+        const int pwa = first_set(xb) / T, pwb = last_set(xb) / T;
+        if (pha < 0 || pwa < 0) return;
         wave_sync();
 
-        const uint32_t *gl = sm.g[buf] + lane * NB;   // this lane's channel, stride NB (odd)
-        for (uint32_t ym = ymask; ym; ym &= ym - 1) {
-            const int ph = __builtin_ctz(ym);
-            float X[T];
-#pragma unroll
-            for (int q = 0; q < T; ++q) X[q] = 0.0f;
-            for (uint32_t xm = xmask; xm; xm &= xm - 1) {
-                const int pw = __builtin_ctz(xm);
-                const float gv = raw_to_f32<TG>(gl[ph * PW + pw]);
-                const float4 w0 = *reinterpret_cast<const float4 *>(wx + pw * T);
-                const float4 w1 = *reinterpret_cast<const float4 *>(wx + pw * T + 4);
-                X[0] = fmaf(w0.x, gv, X[0]);
-                X[1] = fmaf(w0.y, gv, X[1]);
-                X[2] = fmaf(w0.z, gv, X[2]);
-                X[3] = fmaf(w0.w, gv, X[3]);
-                X[4] = fmaf(w1.x, gv, X[4]);
-                X[5] = fmaf(w1.y, gv, X[5]);
-                X[6] = fmaf(w1.z, gv, X[6]);
-                X[7] = fmaf(w1.w, gv, X[7]);
-            }
-            const float4 y0 = *reinterpret_cast<const float4 *>(wy + ph * T);
-            const float4 y1 = *reinterpret_cast<const float4 *>(wy + ph * T + 4);
-            const float yr[T] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
-#pragma unroll
-            for (int rr = 0; rr < T; ++rr)
-#pragma unroll
-                for (int q = 0; q < T; ++q) acc[rr][q] = fmaf(yr[rr], X[q], acc[rr][q]);
-        }
+        const uint32_t *gl = gsrc + lane * NB + pwa;   // this lane's channel, stride NB (odd)
+        const float *wxa = wx + pwa * T;
+        gather_rows<TG, PW>(acc, gl, wxa, wy, yb, pha, phb, pwb - pwa + 1);
         // the weights are rewritten for the next RoI only after the next barrier
     };
 
@@ -547,28 +597,37 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
         const int nk = sm.n;
         if (nk == 0) continue;
         if constexpr (NBUF == 2) {
-            fetch(0, 0);
+            // Unrolled by two so that each slot is named statically: the copy of RoI
+            // j + 1 into one slot lands while RoI j is read from the other.
+            fetch(0, slot0);
             taps(0, 0);
             fetch_wait();
             __syncthreads();
-            for (int j = 0; j < nk; ++j) {
-                const int buf = j & 1;
+            for (int j = 0; j < nk; j += 2) {
                 if (j + 1 < nk) {
-                    fetch(j + 1, buf ^ 1);   // lands while RoI j is processed
-                    taps(j + 1, buf ^ 1);    // the other tap buffer is idle
+                    fetch(j + 1, slot1);
+                    taps(j + 1, 1);   // the other tap buffer is idle
                 }
-                consume(j, buf, buf);
+                consume(j, slot0, 0);
                 fetch_wait();
                 __syncthreads();   // staged block, taps and weights are reused next
+                if (j + 1 >= nk) break;
+                if (j + 2 < nk) {
+                    fetch(j + 2, slot0);
+                    taps(j + 2, 0);
+                }
+                consume(j + 1, slot1, 1);
+                fetch_wait();
+                __syncthreads();
             }
         } else {
             for (int j = 0; j < nk; ++j) {
                 if (j > 0) __syncthreads();   // the previous block is fully consumed
-                fetch(j, 0);
+                fetch(j, slot0);
                 taps(j, j & 1);
                 fetch_wait();
                 __syncthreads();
-                consume(j, 0, j & 1);
+                consume(j, slot0, j & 1);
             }
         }
     }
@@ -656,6 +715,9 @@ __device__ __forceinline__ void gather_store(const GatherTile &x, int zero_init,
 template <typename TG, int PH, int PW, int S>
 __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     __shared__ GatherSmem<TG, PH, PW, S> sm;
+    __shared__ GatherBlock<TG, PH, PW, S> blk0;
+    constexpr bool two = GatherSmem<TG, PH, PW, S>::NBUF == 2;
+    __shared__ GatherBlock<TG, two ? PH : 1, two ? PW : 1, S> blk1;
     GatherTile x;
     const int t = gather_tile(a, a.tile_order, x);
     float acc[8][8];
@@ -663,7 +725,8 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
     for (int r = 0; r < 8; ++r)
 #pragma unroll
         for (int q = 0; q < 8; ++q) acc[r][q] = 0.0f;
-    gather_phase<TG, PH, PW, S>(a.head[0], a.lv, t, x, acc, sm);
+    gather_phase<TG, PH, PW, S>(a.head[0], a.lv, t, x, acc, sm, blk0.g,
+                                two ? blk1.g : nullptr);
     gather_store(x, a.zero_init, acc);
 }
 
@@ -673,11 +736,16 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
 // order.
 template <typename TG, int PH0, int PW0, int PH1, int PW1>
 __global__ __launch_bounds__(256) void bwd_gather2_kernel(GatherArgs a) {
+    using SM0 = GatherSmem<TG, PH0, PW0, 2>;
+    using SM1 = GatherSmem<TG, PH1, PW1, 2>;
     union Smem {
-        GatherSmem<TG, PH0, PW0, 2> h0;
-        GatherSmem<TG, PH1, PW1, 2> h1;
+        SM0 h0;
+        SM1 h1;
     };
     __shared__ Smem sm;
+    // the staging ring of whichever head is being walked
+    constexpr int kStage0 = SM0::NBUF * SM0::GB, kStage1 = SM1::NBUF * SM1::GB;
+    __shared__ __align__(16) uint32_t stage[kStage0 > kStage1 ? kStage0 : kStage1];
     GatherTile x;
     const int t = gather_tile(a, a.tile_order, x);
     float acc[8][8];
@@ -685,9 +753,11 @@ __global__ __launch_bounds__(256) void bwd_gather2_kernel(GatherArgs a) {
     for (int r = 0; r < 8; ++r)
 #pragma unroll
         for (int q = 0; q < 8; ++q) acc[r][q] = 0.0f;
-    gather_phase<TG, PH0, PW0, 2>(a.head[0], a.lv, t, x, acc, sm.h0);
+    gather_phase<TG, PH0, PW0, 2>(a.head[0], a.lv, t, x, acc, sm.h0, stage,
+                                  SM0::NBUF == 2 ? stage + SM0::GB : nullptr);
     __syncthreads();   // head 0's LDS is no longer read
-    gather_phase<TG, PH1, PW1, 2>(a.head[1], a.lv, t, x, acc, sm.h1);
+    gather_phase<TG, PH1, PW1, 2>(a.head[1], a.lv, t, x, acc, sm.h1, stage,
+                                  SM1::NBUF == 2 ? stage + SM1::GB : nullptr);
     gather_store(x, a.zero_init, acc);
 }
 
