@@ -19,6 +19,7 @@
 //   bwd_generic_kernel  any strides / sizes: one thread per gradient element, four
 //                       atomics per valid sample.
 //   zero kernels        clear the gradient pyramid.
+#include <algorithm>
 #include <type_traits>
 
 #include "internal.hpp"
@@ -640,14 +641,14 @@ __device__ __forceinline__ int gather_tile(const GatherArgs &a, const int32_t *o
                                            GatherTile &x) {
     const int tid = threadIdx.x;
     const int wave = uniform_i(tid >> 6);
-    const int lid = static_cast<int>(blockIdx.x);
+    const uint32_t lid = blockIdx.x;
     const int per_tile = a.ncg * a.wg_per_tile;
-    const int rank = lid / per_tile;
-    const int rem = lid - rank * per_tile;
-    const int cg = rem / a.wg_per_tile;
+    const int rank = static_cast<int>(fdiv(lid, a.div_tile));
+    const int rem = static_cast<int>(lid) - rank * per_tile;
+    const int cg = rem >> a.wgpt_shift;   // wg_per_tile is a power of two
     int t = order[rank];
     t = max(0, min(t, a.ntiles - 1));
-    const int quad0 = (rem - cg * a.wg_per_tile) * 4;
+    const int quad0 = (rem & (a.wg_per_tile - 1)) * 4;
     const int quad = quad0 + wave;
 
     int l = 0;
@@ -659,21 +660,21 @@ __device__ __forceinline__ int gather_tile(const GatherArgs &a, const int32_t *o
     const int ntx = pick(a.ntx, l);
     const int per_img = pick(a.nty, l) * ntx;
     const int local = t - pick(a.tbase, l);
-    x.b = local / per_img;
+    x.b = static_cast<int>(fdiv(static_cast<uint32_t>(local), pick(a.img_m, l), pick(a.img_sh, l)));
     const int rt = local - x.b * per_img;
-    const int ty = rt / ntx;
+    const int ty = static_cast<int>(fdiv(static_cast<uint32_t>(rt), pick(a.row_m, l), pick(a.row_sh, l)));
     const int tx = rt - ty * ntx;
-    const int qs = a.qside;
-    x.R0 = (ty << a.tile_shift) + (quad / qs) * 8;
-    x.Q0 = (tx << a.tile_shift) + (quad % qs) * 8;
+    const int qs = a.qside, qsh = a.qs_shift;   // qside is a power of two
+    x.R0 = (ty << a.tile_shift) + (quad >> qsh) * 8;
+    x.Q0 = (tx << a.tile_shift) + (quad & (qs - 1)) * 8;
     // Waves whose quadrant is off the map still take part in staging and barriers.
     x.wave_on = quad < qs * qs && x.R0 < x.L.H && x.Q0 < x.L.W;
     // The workgroup's region: the bounding box of its (up to 4) quadrants.
     const int qlast = min(quad0 + 3, qs * qs - 1);
-    x.WR0 = (ty << a.tile_shift) + (quad0 / qs) * 8;
-    x.WR1 = (ty << a.tile_shift) + (qlast / qs) * 8 + 8;
-    x.WC0 = (tx << a.tile_shift) + ((qlast / qs > quad0 / qs) ? 0 : (quad0 % qs)) * 8;
-    x.WC1 = (tx << a.tile_shift) + ((qlast / qs > quad0 / qs) ? qs : (qlast % qs) + 1) * 8;
+    x.WR0 = (ty << a.tile_shift) + (quad0 >> qsh) * 8;
+    x.WR1 = (ty << a.tile_shift) + (qlast >> qsh) * 8 + 8;
+    x.WC0 = (tx << a.tile_shift) + ((qlast >> qsh > quad0 >> qsh) ? 0 : (quad0 & (qs - 1))) * 8;
+    x.WC1 = (tx << a.tile_shift) + ((qlast >> qsh > quad0 >> qsh) ? qs : (qlast & (qs - 1)) + 1) * 8;
     x.cg = cg;
     x.nch = min(64, a.lv.C - cg * 64);
     return t;
@@ -696,19 +697,43 @@ __device__ __forceinline__ void gather_store(const GatherTile &x, int zero_init,
     const uint32_t vo = lane_on ? static_cast<uint32_t>(c) * 4u : kBufOOB;
     const uint32_t sh4 = static_cast<uint32_t>(L.sh) * 4u;
     const uint32_t sw4 = static_cast<uint32_t>(L.sw) * 4u;
+    const uint32_t base = static_cast<uint32_t>(x.R0) * sh4 + static_cast<uint32_t>(x.Q0) * sw4;
+    if (zero_init && x.R0 + 8 <= L.H && x.Q0 + 8 <= L.W) {
+        // a whole quadrant inside the map: 64 plain stores, no per-pixel checks
+#pragma unroll
+        for (int rr = 0; rr < 8; ++rr)
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[rr][q]), dst, vo,
+                                                      base + rr * sh4 + q * sw4, kStoreNT);
+        return;
+    }
+    // Quadrants cut by the map edge, or accumulation: pixels off the map take an
+    // out-of-range offset (loads read 0, stores are dropped), so there are no branches.
+    // When accumulating, a row's old values are loaded together before it is stored,
+    // one row at a time (the empty asm keeps the compiler from hoisting every row's
+    // loads, which would cost registers).
 #pragma unroll
     for (int rr = 0; rr < 8; ++rr) {
-        if (x.R0 + rr >= L.H) break;
-        const uint32_t rowo =
-            static_cast<uint32_t>(x.R0 + rr) * sh4 + static_cast<uint32_t>(x.Q0) * sw4;
+        const bool row_on = x.R0 + rr < L.H;
+        uint32_t vq[8];
+        float v[8];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            if (x.Q0 + q >= L.W) break;
-            const uint32_t so = rowo + static_cast<uint32_t>(q) * sw4;
-            float v = acc[rr][q];
-            if (!zero_init) v += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dst, vo, so, 0));
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), dst, vo, so, kStoreNT);
+            vq[q] = (row_on && x.Q0 + q < L.W) ? vo : kBufOOB;
+            v[q] = acc[rr][q];
         }
+        if (!zero_init) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                v[q] += __uint_as_float(
+                    __builtin_amdgcn_raw_buffer_load_b32(dst, vq[q], base + rr * sh4 + q * sw4, 0));
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[q]), dst, vq[q],
+                                                  base + rr * sh4 + q * sw4, kStoreNT);
+        asm volatile("" ::: "memory");
     }
 }
 
@@ -813,12 +838,13 @@ __global__ __launch_bounds__(256) void bwd_gather_cg_kernel(GatherArgs a) {
     const int ncgg = (a.ncg + 3) >> 2;
     const int qs = a.qside;
     const int per_tile = qs * qs * ncgg;
-    const int lid = static_cast<int>(blockIdx.x);
-    const int slot = lid >> 3;
-    const int rank = (slot / per_tile) * 8 + (lid & 7);
+    const uint32_t lid = blockIdx.x;
+    const uint32_t slot = lid >> 3;
+    const int tq = static_cast<int>(fdiv(slot, a.div_tile_cg));
+    const int rank = tq * 8 + static_cast<int>(lid & 7);
     if (rank >= a.ntiles) return;   // uniform over the workgroup, before any barrier
-    const int rem = slot - (slot / per_tile) * per_tile;
-    const int quad = rem / ncgg;
+    const int rem = static_cast<int>(slot) - tq * per_tile;
+    const int quad = static_cast<int>(fdiv(static_cast<uint32_t>(rem), a.div_ncgg));
     const int cgg = rem - quad * ncgg;
     int t = a.tile_order[rank];
     t = max(0, min(t, a.ntiles - 1));
@@ -831,12 +857,12 @@ __global__ __launch_bounds__(256) void bwd_gather_cg_kernel(GatherArgs a) {
     const int ntx = pick(a.ntx, l);
     const int per_img = pick(a.nty, l) * ntx;
     const int local = t - pick(a.tbase, l);
-    const int b = local / per_img;
+    const int b = static_cast<int>(fdiv(static_cast<uint32_t>(local), pick(a.img_m, l), pick(a.img_sh, l)));
     const int rt = local - b * per_img;
-    const int ty = rt / ntx;
+    const int ty = static_cast<int>(fdiv(static_cast<uint32_t>(rt), pick(a.row_m, l), pick(a.row_sh, l)));
     const int tx = rt - ty * ntx;
-    const int R0 = (ty << a.tile_shift) + (quad / qs) * T;
-    const int Q0 = (tx << a.tile_shift) + (quad % qs) * T;
+    const int R0 = (ty << a.tile_shift) + (quad >> a.qs_shift) * T;
+    const int Q0 = (tx << a.tile_shift) + (quad & (qs - 1)) * T;
     if (R0 >= L.H || Q0 >= L.W) return;   // uniform over the workgroup, before any barrier
 
     const int cg = cgg * 4 + wave;
@@ -1099,6 +1125,23 @@ hipError_t launch_gather(GatherArgs a, int gout_dtype, hipStream_t stream) {
     const int64_t grid = static_cast<int64_t>(a.ntiles) * a.wg_per_tile * a.ncg;
     if (grid <= 0) return hipSuccess;
     if (grid >= (int64_t(1) << 24)) return hipErrorInvalidConfiguration;
+    // qside = 2^(tile_shift - 3) with tile_shift >= 4, so qside and wg_per_tile are
+    // powers of two
+    a.qs_shift = a.tile_shift - 3;
+    a.wgpt_shift = 2 * a.qs_shift - 2;
+    if (a.qs_shift < 1 || a.qside != (1 << a.qs_shift) || a.wg_per_tile != (1 << a.wgpt_shift))
+        return hipErrorInvalidConfiguration;
+    a.div_tile = make_fastdiv(static_cast<uint32_t>(a.ncg * a.wg_per_tile));
+    a.div_ncgg = make_fastdiv(static_cast<uint32_t>((a.ncg + 3) / 4));
+    a.div_tile_cg = make_fastdiv(static_cast<uint32_t>(a.qside * a.qside * ((a.ncg + 3) / 4)));
+    for (int l = 0; l < kMaxLevels; ++l) {
+        const FastDiv di = make_fastdiv(static_cast<uint32_t>(std::max(1, a.ntx[l] * a.nty[l])));
+        const FastDiv dr = make_fastdiv(static_cast<uint32_t>(std::max(1, a.ntx[l])));
+        a.img_m[l] = di.m;
+        a.img_sh[l] = di.sh;
+        a.row_m[l] = dr.m;
+        a.row_sh[l] = dr.sh;
+    }
     const uint32_t g = static_cast<uint32_t>(grid);
     if (a.nheads == 2) {
         // both heads' gradients have one dtype here (the host checks it)

@@ -65,6 +65,31 @@ struct GatherHead {
     int32_t pad;
 };
 
+// Division by a divisor fixed at launch, for the block-id decoding of the gather
+// kernels: n / d = (t + ((n - t) >> s1)) >> s2 with t = umulhi(n, m), exact for every
+// 32-bit n (Granlund and Montgomery, division by invariant integers, 1994).  The
+// scalar unit has no divide instruction; this takes five scalar operations.
+// The two shifts are packed as s1 | s2 << 8.  Per-level divisors are kept as plain
+// integer arrays (a switch over a struct array in the kernel arguments can make the
+// compiler copy the arguments to scratch memory to index them).
+struct FastDiv {
+    uint32_t m;
+    int32_t sh;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {   // d >= 1
+    int l = 0;
+    while ((uint64_t(1) << l) < d) ++l;   // ceil(log2 d)
+    const uint64_t m = ((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1;
+    return FastDiv{static_cast<uint32_t>(m), (l < 1 ? l : 1) | (l > 1 ? l - 1 : 0) << 8};
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, uint32_t m, int32_t sh) {
+    const uint32_t t = __umulhi(n, m);
+    return (t + ((n - t) >> (sh & 0xff))) >> (sh >> 8);
+}
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) { return fdiv(n, f.m, f.sh); }
+
 struct GatherArgs {
     LevelTable lv;               // gradient levels (binary32, channels-last)
     GatherHead head[2];          // head 1 is used by the two-head kernel only
@@ -81,6 +106,16 @@ struct GatherArgs {
                                  //    (bf16 upstream gradient, 7x7, one head)
     int32_t gout_dtype1;         // head 1's upstream-gradient dtype
     int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
+    // set at launch: block-id decoding without integer division
+    int32_t qs_shift;            // log2 qside
+    int32_t wgpt_shift;          // log2 wg_per_tile
+    FastDiv div_tile;            // by ncg * wg_per_tile (quadrant form)
+    FastDiv div_tile_cg;         // by qside^2 * ceil(ncg / 4) (channel-group form)
+    FastDiv div_ncgg;            // by ceil(ncg / 4)
+    uint32_t img_m[kMaxLevels];  // by the tiles of one image of a level
+    int32_t img_sh[kMaxLevels];
+    uint32_t row_m[kMaxLevels];  // by the tiles of one row of a level
+    int32_t row_sh[kMaxLevels];
 };
 
 struct FwdArgs {
