@@ -366,12 +366,18 @@ struct GatherSmem {
     static constexpr int T = 8;
     static constexpr int NB = PH * PW;
     static constexpr int GB = 64 * NB;   // 32-bit words of one RoI's gradient block
+    // The block is copied in runs of RUN elements, one copy instruction per run:
+    // 16 bytes per lane for binary32, one element per lane for bf16.  A slot holds
+    // whole runs (GBP words); the words past the block are never read.
+    static constexpr int RUN = sizeof(TG) == 4 ? 256 : 64;
+    static constexpr int NRUN = (GB + RUN - 1) / RUN;
+    static constexpr int GBP = NRUN * RUN;
     // The staged gradient blocks form a ring of NBUF: the next RoI's block is copied
     // into the other slot by the buffer unit while the current one is consumed, when
     // two blocks fit in 52 KiB.  The copy gives every lane a 32-bit LDS slot whatever
     // the element size, so a block holds one 32-bit word per element (a bf16 value in
     // its low half).
-    static constexpr int NBUF = 2 * GB * 4 <= 53248 ? 2 : 1;
+    static constexpr int NBUF = 2 * GBP * 4 <= 53248 ? 2 : 1;
     Tap tap[2][NR + NCOL];
     __align__(16) float wy[4][PH * T];
     __align__(16) float wx[4][PW * T];
@@ -385,7 +391,7 @@ struct GatherSmem {
 // compiler can tell that reading one slot does not depend on the copy into the other.
 template <typename TG, int PH, int PW, int S>
 struct GatherBlock {
-    __align__(16) uint32_t g[GatherSmem<TG, PH, PW, S>::GB];
+    __align__(16) uint32_t g[GatherSmem<TG, PH, PW, S>::GBP];
 };
 
 // Where a workgroup of the quadrant-form gather sits: the tile's level and image,
@@ -412,8 +418,6 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
     constexpr int NBUF = SM::NBUF;
     constexpr int YP = (PH * T + 63) / 64;   // ballot passes for the row weights
     constexpr int XP = (PW * T + 63) / 64;
-    constexpr int NDMA = GB / 64;            // 64-element runs of one block
-    static_assert(GB % 64 == 0, "a copy instruction moves whole 64-element runs");
     static_assert(NR + NCOL <= 64, "taps are computed by one wavefront");
     static_assert(PH <= 32 && PW <= 32, "bin masks are 32-bit");
 
@@ -433,26 +437,46 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
 
     // Coalesced copy of kept RoI j's gradient block (nch x NB values) into LDS
     // through a buffer resource over exactly that block: run r = wave + 4 m goes to
-    // words [64 r, 64 r + 64), lane i writing element 64 r + i (the LDS address is the
-    // uniform run base plus 4 bytes per lane, the global offset the lane's own); the
-    // range check supplies the zeros past the valid channels.
+    // words [RUN r, RUN r + RUN), lane i writing the RUN / 64 elements from RUN r +
+    // i RUN / 64 on (the LDS address is the uniform run base plus the lane's bytes, in
+    // lane order; the global offset is the lane's own); the range check, which works
+    // per dword, supplies the zeros past the valid channels.
     const int nvalid = x.nch * NB;
+    // 16-byte copies need every block 16-byte aligned: a multiple of 4 channels and an
+    // aligned gradient (binary32 only)
+    const bool wide = sizeof(TG) == 4 && (lv.C & 3) == 0 &&
+                      (reinterpret_cast<uintptr_t>(h.gout) & 15u) == 0;
     auto fetch = [&](int j, uint32_t *gdst) {
         const int k = uniform_i(sm.k[j]);   // one resource for the wave, no waterfall
         const char *src = static_cast<const char *>(h.gout) +
                           (static_cast<int64_t>(x.cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
                               int64_t(sizeof(TG));
         const __amdgpu_buffer_rsrc_t rs = make_rsrc(src, static_cast<uint32_t>(nvalid) * uint32_t(sizeof(TG)));
+        constexpr int RUN = SM::RUN, NRUN = SM::NRUN;
+        if (RUN == 256 && wide) {
 #pragma unroll
-        for (int m = 0; m < (NDMA + 3) / 4; ++m) {
-            const int run = wave + 4 * m;
-            if (m < NDMA / 4 || run < NDMA) {
-                auto *dst = (__attribute__((address_space(3))) void *)(gdst + 64 * run);
-                const uint32_t off = static_cast<uint32_t>(64 * run + lane) * uint32_t(sizeof(TG));
-                if constexpr (sizeof(TG) == 4)
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 4, off, 0, 0, 0);
-                else
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 2, off, 0, 0, 0);
+            for (int m = 0; m < (NRUN + 3) / 4; ++m) {
+                const int run = wave + 4 * m;
+                if (m < NRUN / 4 || run < NRUN) {
+                    auto *dst = (__attribute__((address_space(3))) void *)(gdst + RUN * run);
+                    const uint32_t off = static_cast<uint32_t>(RUN * run + lane * 4) * 4u;
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 16, off, 0, 0, 0);
+                }
+            }
+        } else {
+            // one element per lane and instruction (bf16, or blocks not 16-byte aligned)
+            constexpr int NR64 = GB / 64;
+#pragma unroll
+            for (int m = 0; m < (NR64 + 3) / 4; ++m) {
+                const int run = wave + 4 * m;
+                if (m < NR64 / 4 || run < NR64) {
+                    auto *dst = (__attribute__((address_space(3))) void *)(gdst + 64 * run);
+                    const uint32_t off = static_cast<uint32_t>(64 * run + lane) * uint32_t(sizeof(TG));
+                    if constexpr (sizeof(TG) == 4)
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 4, off, 0, 0, 0);
+                    else
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 2, off, 0, 0, 0);
+                }
             }
         }
     };
@@ -769,7 +793,7 @@ __global__ __launch_bounds__(256) void bwd_gather2_kernel(GatherArgs a) {
     };
     __shared__ Smem sm;
     // the staging ring of whichever head is being walked
-    constexpr int kStage0 = SM0::NBUF * SM0::GB, kStage1 = SM1::NBUF * SM1::GB;
+    constexpr int kStage0 = SM0::NBUF * SM0::GBP, kStage1 = SM1::NBUF * SM1::GBP;
     __shared__ __align__(16) uint32_t stage[kStage0 > kStage1 ? kStage0 : kStage1];
     GatherTile x;
     const int t = gather_tile(a, a.tile_order, x);
@@ -779,10 +803,10 @@ __global__ __launch_bounds__(256) void bwd_gather2_kernel(GatherArgs a) {
 #pragma unroll
         for (int q = 0; q < 8; ++q) acc[r][q] = 0.0f;
     gather_phase<TG, PH0, PW0, 2>(a.head[0], a.lv, t, x, acc, sm.h0, stage,
-                                  SM0::NBUF == 2 ? stage + SM0::GB : nullptr);
+                                  SM0::NBUF == 2 ? stage + SM0::GBP : nullptr);
     __syncthreads();   // head 0's LDS is no longer read
     gather_phase<TG, PH1, PW1, 2>(a.head[1], a.lv, t, x, acc, sm.h1, stage,
-                                  SM1::NBUF == 2 ? stage + SM1::GB : nullptr);
+                                  SM1::NBUF == 2 ? stage + SM1::GBP : nullptr);
     gather_store(x, a.zero_init, acc);
 }
 
