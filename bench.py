@@ -286,8 +286,7 @@ def main():
         alg.update({"zero": by.zero, "bwd": gather_bytes if algo == "gather" else by.e_bwd})
     gbs = {n: alg[n] / (per_kernel[n] * 1e-3) / 1e9 for n in names}
     dominant = max(["fwd", "bwd"] if backward else ["fwd"], key=lambda n: per_kernel[n])
-    wname = "cfg%d%s" % (args.workload, ("_" + args.head) if args.workload == 5 else
-                         ("_" + wl.feat_dtype if args.workload == 4 else ""))
+    wname = wl.tag
     kname = {"fwd": "fwd", "bwd": "bwd_" + algo}[dominant]
     traffic = stored_traffic(kname, wname)
     roofline = {"bound": "hbm", "achieved": round(gbs[dominant], 1), "peak": HBM_PEAK_GBS,

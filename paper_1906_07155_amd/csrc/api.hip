@@ -440,7 +440,6 @@ GatherArgs gather_args(const LevelTable &t, const BwdHead &h0, const TileLayout 
     g.ntiles = tl.ntiles;
     g.tile_shift = tl.shift;
     g.qside = 1 << (tl.shift - 3);
-    g.cg_form = (h0.out_h == 7 && h0.gdt == RE_DTYPE_BF16) ? 1 : 0;
     for (int l = 0; l < kMaxLevels; ++l) {
         g.ntx[l] = tl.ntx[l];
         g.nty[l] = tl.nty[l];

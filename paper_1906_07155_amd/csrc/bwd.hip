@@ -20,7 +20,6 @@
 //                       atomics per valid sample.
 //   zero kernels        clear the gradient pyramid.
 #include <algorithm>
-#include <type_traits>
 
 #include "internal.hpp"
 
@@ -274,17 +273,6 @@ __global__ __launch_bounds__(256) void bwd_cl_kernel(BwdArgs a) {
 //   Wy[ph][r] = sum over the samples of bin row ph of the bilinear weight they put on
 //               row R0 + r (divided by the sample count), likewise Wx[pw][q],
 // and the contribution is  acc[r][q] += sum_ph Wy[ph][r] * sum_pw Wx[pw][q] * g[ph][pw].
-
-// Packs the nonzero bytes of a 64-bit ballot into 8 bits (bit h set iff byte h of
-// b has a set bit): OR-fold each byte onto its low bit, then gather the low bits
-// with one multiply (the partial products land on distinct bits, so nothing carries).
-__device__ __forceinline__ uint32_t byte_mask(uint64_t b) {
-    b |= b >> 4;
-    b |= b >> 2;
-    b |= b >> 1;
-    b &= 0x0101010101010101ull;
-    return static_cast<uint32_t>((b * 0x0102040810204080ull) >> 56);
-}
 
 // First / last set bit of a multi-word ballot, -1 if none (uniform scalar values).
 template <int P>
@@ -810,322 +798,6 @@ __global__ __launch_bounds__(256) void bwd_gather2_kernel(GatherArgs a) {
     gather_store(x, a.zero_init, acc);
 }
 
-// ---------------------------------------------------------------------------
-// Tile-gather backward, channel-group form
-// ---------------------------------------------------------------------------
-// Same sums as bwd_gather_kernel, with the work of a workgroup arranged the other
-// way round: its four wavefronts own four 64-channel groups of ONE 8x8-pixel
-// quadrant (instead of four quadrants of one channel group).  Every RoI the
-// quadrant receives then costs all four waves the same work, so no wave idles at
-// the per-RoI barrier while another finishes a RoI that only reaches its own
-// quadrant, and the separable weights are built once for all four waves.  Each
-// wave stages its own channel group's gradient block; the four blocks of a RoI
-// are the full 1 KiB of every (bin, channel) row it needs, and every pixel's 256
-// channels are stored by one workgroup.  The blocks are staged one RoI ahead through
-// registers.  Staging four blocks per quadrant (instead of one per 16x16 tile) moves
-// about twice the gradient bytes through L2 and LDS; with bf16 upstream gradients
-// that costs less than the idle waves it removes, with fp32 it does not (measured on
-// the batch-2 and batch-16 box heads), so the library uses this form for bf16
-// gradients on the 7x7 grid only.
-template <typename TG, int PH, int PW, int S>
-__global__ __launch_bounds__(256) void bwd_gather_cg_kernel(GatherArgs a) {
-    constexpr int NR = PH * S;
-    constexpr int NCOL = PW * S;
-    constexpr int T = 8;                    // quadrant side
-    constexpr int NB = PH * PW;
-    constexpr int GBYTES = 64 * NB * int(sizeof(TG));   // one staged block
-    constexpr int NPF = (GBYTES + 1023) / 1024;          // 16-byte loads per lane
-    constexpr int YP = (PH * T + 63) / 64;  // ballot passes for the row weights
-    constexpr int XP = (PW * T + 63) / 64;
-    static_assert(4 * GBYTES <= 56 * 1024, "four staged blocks must fit LDS");
-    static_assert(GBYTES % 16 == 0, "blocks move in 16-byte pieces");
-    static_assert(NR <= 64 && NCOL <= 64, "taps of an axis are computed by one wavefront");
-    static_assert(PH <= 32 && PW <= 32, "bin masks are 32-bit");
-
-    __shared__ __align__(16) unsigned char s_g[4][GBYTES];
-    __shared__ Tap s_tap[NR + NCOL];
-    __shared__ __align__(16) float s_wy[PH * T];
-    __shared__ __align__(16) float s_wx[PW * T];
-    __shared__ uint64_t s_yb[YP];
-    __shared__ uint64_t s_xb[XP];
-    __shared__ int s_k[64];
-    __shared__ float s_ax[64][4];
-    __shared__ int s_n;
-
-    const int tid = threadIdx.x;
-    const int wave = uniform_i(tid >> 6);
-    const int lane = tid & 63;
-    // Workgroup ids are dealt round-robin to the 8 XCDs.  Tile rank r (plan order:
-    // longest list first) goes to XCD r % 8, where its quadrants and channel-group
-    // quartets take consecutive dispatch slots, so the RoI blocks the quadrants of a
-    // tile share are fetched into one L2.  Ids past the last tile exit at once.
-    const int ncgg = (a.ncg + 3) >> 2;
-    const int qs = a.qside;
-    const int per_tile = qs * qs * ncgg;
-    const uint32_t lid = blockIdx.x;
-    const uint32_t slot = lid >> 3;
-    const int tq = static_cast<int>(fdiv(slot, a.div_tile_cg));
-    const int rank = tq * 8 + static_cast<int>(lid & 7);
-    if (rank >= a.ntiles) return;   // uniform over the workgroup, before any barrier
-    const int rem = static_cast<int>(slot) - tq * per_tile;
-    const int quad = static_cast<int>(fdiv(static_cast<uint32_t>(rem), a.div_ncgg));
-    const int cgg = rem - quad * ncgg;
-    int t = a.tile_order[rank];
-    t = max(0, min(t, a.ntiles - 1));
-
-    int l = 0;
-#pragma unroll
-    for (int i = 1; i < kMaxLevels; ++i)
-        if (i < a.lv.num && t >= a.tbase[i]) l = i;
-    const LevelArg L = level_at(a.lv, l);
-    const int ntx = pick(a.ntx, l);
-    const int per_img = pick(a.nty, l) * ntx;
-    const int local = t - pick(a.tbase, l);
-    const int b = static_cast<int>(fdiv(static_cast<uint32_t>(local), pick(a.img_m, l), pick(a.img_sh, l)));
-    const int rt = local - b * per_img;
-    const int ty = static_cast<int>(fdiv(static_cast<uint32_t>(rt), pick(a.row_m, l), pick(a.row_sh, l)));
-    const int tx = rt - ty * ntx;
-    const int R0 = (ty << a.tile_shift) + (quad >> a.qs_shift) * T;
-    const int Q0 = (tx << a.tile_shift) + (quad & (qs - 1)) * T;
-    if (R0 >= L.H || Q0 >= L.W) return;   // uniform over the workgroup, before any barrier
-
-    const int cg = cgg * 4 + wave;
-    const bool wave_on = cg < a.ncg;        // uniform over the wavefront
-    const int c = cg * 64 + lane;
-    const bool lane_on = c < a.lv.C;
-    const int nch = wave_on ? min(64, a.lv.C - cg * 64) : 0;
-    float acc[T][T];
-#pragma unroll
-    for (int r = 0; r < T; ++r)
-#pragma unroll
-        for (int q = 0; q < T; ++q) acc[r][q] = 0.0f;
-
-    int s0 = a.head[0].tile_start[t];
-    int s1 = a.head[0].tile_start[t + 1];
-    s0 = max(0, min(s0, a.head[0].capacity));
-    s1 = max(s0, min(s1, a.head[0].capacity));
-    constexpr float inv_count = 1.0f / static_cast<float>(S * S);
-    const int64_t kstride = static_cast<int64_t>(a.lv.C) * NB;
-    const uint32_t nvalid_bytes = static_cast<uint32_t>(nch * NB) * uint32_t(sizeof(TG));
-
-    // This wave's channel group of kept RoI j is loaded into registers one RoI ahead
-    // (16 bytes per lane and load, coalesced) and written to the wave's LDS block
-    // when its turn comes; the resource covers exactly the valid channels, so the
-    // range check reads zeros past them.
-    // The range check works per dword: when the valid bytes end inside a dword (bf16
-    // with an odd channel count), the 16-byte loads return that dword as zero, so the
-    // last element is loaded on its own (2 bytes) and patched into LDS after staging.
-    const bool odd_tail = (nvalid_bytes & 3u) != 0;
-    uint4 pf[NPF];
-    uint32_t pf_last = 0;
-    auto fetch = [&](int j) {
-        const int k = uniform_i(s_k[j]);
-        const char *src = static_cast<const char *>(a.head[0].gout) +
-                          (static_cast<int64_t>(cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
-                              int64_t(sizeof(TG));
-        const __amdgpu_buffer_rsrc_t rs = make_rsrc(src, nvalid_bytes);
-        const uint32_t voff = static_cast<uint32_t>(lane) * 16u;
-#pragma unroll
-        for (int m = 0; m < NPF; ++m) {
-            const uint32_t soff = static_cast<uint32_t>(m) * 1024u;
-            if (m * 1024 + 1024 <= GBYTES || static_cast<int>(voff + soff) < GBYTES) {
-                const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
-                pf[m] = make_uint4(v[0], v[1], v[2], v[3]);
-            }
-        }
-        if (odd_tail) pf_last = __builtin_amdgcn_raw_buffer_load_b16(rs, 0u, nvalid_bytes - 2u, 0);
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int m = 0; m < NPF; ++m) {
-            const int off = m * 1024 + lane * 16;
-            if (m * 1024 + 1024 <= GBYTES || off < GBYTES)
-                *reinterpret_cast<uint4 *>(&s_g[wave][off]) = pf[m];
-        }
-        if (odd_tail && lane == 0)
-            *reinterpret_cast<uint16_t *>(&s_g[wave][nvalid_bytes - 2u]) =
-                static_cast<uint16_t>(pf_last);
-    };
-    // Wave 0 builds the row side, wave 1 the column side: the sample taps of kept
-    // RoI j along that axis, then the quadrant's summed weight of every (bin, pixel)
-    // and the ballot of which bins reach which of its 8 pixels (bit 8 * bin + pixel).
-    auto axis_weights = [&](int j, bool rows) {
-        Axis ax;
-        ax.grid = S;
-        ax.start = s_ax[j][rows ? 2 : 0];
-        ax.bin = s_ax[j][rows ? 3 : 1];
-        const int nt = rows ? NR : NCOL;
-        const int P = rows ? PH : PW;
-        const int size = rows ? L.H : L.W;
-        const int base = rows ? 0 : NR;
-        if (lane < nt) s_tap[base + lane] = axis_tap(ax, lane / S, lane % S, size);
-        wave_sync();
-        const int origin = rows ? R0 : Q0;
-        float *wdst = rows ? s_wy : s_wx;
-        const float scale = rows ? inv_count : 1.0f;
-#pragma unroll
-        for (int p = 0; p < (rows ? YP : XP); ++p) {
-            const int u = p * 64 + lane;
-            bool hit = false;
-            if (u < P * T) {
-                const int bin = u / T;
-                const int pix = origin + (u % T);
-                float w = 0.0f;
-#pragma unroll
-                for (int i = 0; i < S; ++i) {
-                    const Tap tp = s_tap[base + bin * S + i];
-                    if (tp.lo >= 0) {
-                        if (tp.lo == pix) {
-                            w += tp.wlo;
-                            hit = true;
-                        }
-                        if (tp.hi == pix) {
-                            w += tp.whi;
-                            hit = true;
-                        }
-                    }
-                }
-                wdst[u] = w * scale;
-            }
-            const uint64_t bal = __ballot(hit);
-            if (lane == 0) {
-                if (rows)
-                    s_yb[p] = bal;
-                else
-                    s_xb[p] = bal;
-            }
-        }
-    };
-    auto consume = [&]() {
-        uint32_t ymask = 0, xmask = 0;
-#pragma unroll
-        for (int p = 0; p < YP; ++p) ymask |= byte_mask(s_yb[p]) << (p * 8);
-#pragma unroll
-        for (int p = 0; p < XP; ++p) xmask |= byte_mask(s_xb[p]) << (p * 8);
-        ymask = static_cast<uint32_t>(uniform_i(static_cast<int>(ymask)));
-        xmask = static_cast<uint32_t>(uniform_i(static_cast<int>(xmask)));
-        // this lane's channel: NB raw elements (fp32 bits, or bf16 bits)
-        using Raw = typename std::conditional<sizeof(TG) == 4, uint32_t, uint16_t>::type;
-        const Raw *gl = reinterpret_cast<const Raw *>(s_g[wave]) + lane * NB;
-        for (uint32_t ym = ymask; ym; ym &= ym - 1) {
-            const int ph = __builtin_ctz(ym);
-            float X[T];
-#pragma unroll
-            for (int q = 0; q < T; ++q) X[q] = 0.0f;
-            for (uint32_t xm = xmask; xm; xm &= xm - 1) {
-                const int pw = __builtin_ctz(xm);
-                const float gv = raw_to_f32<TG>(static_cast<uint32_t>(gl[ph * PW + pw]));
-                const float4 w0 = *reinterpret_cast<const float4 *>(s_wx + pw * T);
-                const float4 w1 = *reinterpret_cast<const float4 *>(s_wx + pw * T + 4);
-                X[0] = fmaf(w0.x, gv, X[0]);
-                X[1] = fmaf(w0.y, gv, X[1]);
-                X[2] = fmaf(w0.z, gv, X[2]);
-                X[3] = fmaf(w0.w, gv, X[3]);
-                X[4] = fmaf(w1.x, gv, X[4]);
-                X[5] = fmaf(w1.y, gv, X[5]);
-                X[6] = fmaf(w1.z, gv, X[6]);
-                X[7] = fmaf(w1.w, gv, X[7]);
-            }
-            const float4 y0 = *reinterpret_cast<const float4 *>(s_wy + ph * T);
-            const float4 y1 = *reinterpret_cast<const float4 *>(s_wy + ph * T + 4);
-            const float yr[T] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
-#pragma unroll
-            for (int rr = 0; rr < T; ++rr)
-#pragma unroll
-                for (int q = 0; q < T; ++q) acc[rr][q] = fmaf(yr[rr], X[q], acc[rr][q]);
-        }
-    };
-
-    for (int base = s0; base < s1; base += 64) {
-        const int n = min(64, s1 - base);
-        __syncthreads();   // the previous batch's records are no longer read
-        // RoI records of this batch (wave 0): RoIs whose tap extent misses the
-        // quadrant reach none of its pixels and are dropped; the rest are compacted.
-        if (wave == 0) {
-            bool keep = false;
-            int k = 0;
-            float ax_s = 0.0f, ax_b = 0.0f, ay_s = 0.0f, ay_b = 0.0f;
-            if (lane < n) {
-                k = a.head[0].tile_rois[base + lane];
-                if (k >= 0 && k < a.head[0].K) {
-                    const float *r = a.head[0].rois + 5 * static_cast<int64_t>(k);
-                    const float r0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
-                    const int lvl = a.head[0].roi_levels ? a.head[0].roi_levels[k] : 0;
-                    if (lvl == l && roi_batch(r0, a.lv.N) == b) {
-                        const Axis ax = axis_setup(x1, x2, L.scale, a.head[0].aligned, PW, S);
-                        const Axis ay = axis_setup(y1, y2, L.scale, a.head[0].aligned, PH, S);
-                        ax_s = ax.start;
-                        ax_b = ax.bin;
-                        ay_s = ay.start;
-                        ay_b = ay.bin;
-                        // Tap extent from the first and last sample of each axis (taps
-                        // are monotone in the sample index); an end sample outside the
-                        // map widens the extent to the map edge, so it is a superset.
-                        const Tap fy = axis_tap(ay, 0, 0, L.H);
-                        const Tap ly = axis_tap(ay, PH - 1, S - 1, L.H);
-                        const Tap fx = axis_tap(ax, 0, 0, L.W);
-                        const Tap lx = axis_tap(ax, PW - 1, S - 1, L.W);
-                        const int ymin = fy.lo >= 0 ? fy.lo : 0;
-                        const int ymax = ly.lo >= 0 ? ly.hi : L.H - 1;
-                        const int xmin = fx.lo >= 0 ? fx.lo : 0;
-                        const int xmax = lx.lo >= 0 ? lx.hi : L.W - 1;
-                        keep = ymax >= R0 && ymin < R0 + T && xmax >= Q0 && xmin < Q0 + T;
-                    }
-                }
-            }
-            const uint64_t km = __ballot(keep);
-            if (keep) {
-                const int pos = static_cast<int>(__builtin_amdgcn_mbcnt_hi(
-                    static_cast<uint32_t>(km >> 32),
-                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(km), 0u)));
-                s_k[pos] = k;
-                s_ax[pos][0] = ax_s;
-                s_ax[pos][1] = ax_b;
-                s_ax[pos][2] = ay_s;
-                s_ax[pos][3] = ay_b;
-            }
-            if (lane == 0) s_n = __builtin_popcountll(km);
-        }
-        __syncthreads();
-        const int nk = s_n;
-        if (nk > 0 && wave_on) fetch(0);
-        for (int j = 0; j < nk; ++j) {
-            if (j > 0) __syncthreads();   // RoI j-1 fully consumed by every wave
-            if (wave_on) {
-                __builtin_amdgcn_s_waitcnt(0x0F70);   // block j is in registers
-                stage();
-                if (j + 1 < nk) fetch(j + 1);   // in flight while RoI j is processed
-            }
-            if (wave == 0) axis_weights(j, true);
-            if (wave == 1) axis_weights(j, false);
-            __syncthreads();
-            if (wave_on) consume();
-        }
-    }
-
-    // Every pixel of the quadrant is written once (the clearing is fused), with
-    // non-temporal buffer stores: pixel offset scalar, channel offset per lane.
-    if (!wave_on) return;
-    const char *img = static_cast<const char *>(L.data) + static_cast<int64_t>(b) * L.sn * 4;
-    const __amdgpu_buffer_rsrc_t dst = make_rsrc(img, L.img_bytes);
-    const uint32_t vo = lane_on ? static_cast<uint32_t>(c) * 4u : kBufOOB;
-    const uint32_t sh4 = static_cast<uint32_t>(L.sh) * 4u;
-    const uint32_t sw4 = static_cast<uint32_t>(L.sw) * 4u;
-#pragma unroll
-    for (int rr = 0; rr < T; ++rr) {
-        if (R0 + rr >= L.H) break;
-        const uint32_t rowo = static_cast<uint32_t>(R0 + rr) * sh4 + static_cast<uint32_t>(Q0) * sw4;
-#pragma unroll
-        for (int q = 0; q < T; ++q) {
-            if (Q0 + q >= L.W) break;
-            const uint32_t so = rowo + static_cast<uint32_t>(q) * sw4;
-            float v = acc[rr][q];
-            if (!a.zero_init) v += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dst, vo, so, 0));
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), dst, vo, so, kStoreNT);
-        }
-    }
-}
-
 bool gather_available(int PH, int PW, int S) {
     return S == 2 && ((PH == 7 && PW == 7) || (PH == 14 && PW == 14));
 }
@@ -1156,8 +828,6 @@ hipError_t launch_gather(GatherArgs a, int gout_dtype, hipStream_t stream) {
     if (a.qs_shift < 1 || a.qside != (1 << a.qs_shift) || a.wg_per_tile != (1 << a.wgpt_shift))
         return hipErrorInvalidConfiguration;
     a.div_tile = make_fastdiv(static_cast<uint32_t>(a.ncg * a.wg_per_tile));
-    a.div_ncgg = make_fastdiv(static_cast<uint32_t>((a.ncg + 3) / 4));
-    a.div_tile_cg = make_fastdiv(static_cast<uint32_t>(a.qside * a.qside * ((a.ncg + 3) / 4)));
     for (int l = 0; l < kMaxLevels; ++l) {
         const FastDiv di = make_fastdiv(static_cast<uint32_t>(std::max(1, a.ntx[l] * a.nty[l])));
         const FastDiv dr = make_fastdiv(static_cast<uint32_t>(std::max(1, a.ntx[l])));
@@ -1173,13 +843,6 @@ hipError_t launch_gather(GatherArgs a, int gout_dtype, hipStream_t stream) {
             launch_gather2_typed<float>(a, g, stream);
         else
             launch_gather2_typed<uint16_t>(a, g, stream);
-        return hipGetLastError();
-    }
-    if (a.PH == 7 && a.cg_form && gout_dtype == kBF16) {
-        const int64_t gq = (static_cast<int64_t>(a.ntiles) + 7) / 8 * 8 * a.qside * a.qside *
-                           ((a.ncg + 3) / 4);
-        if (gq >= (int64_t(1) << 24)) return hipErrorInvalidConfiguration;
-        bwd_gather_cg_kernel<uint16_t, 7, 7, 2><<<static_cast<uint32_t>(gq), 256, 0, stream>>>(a);
         return hipGetLastError();
     }
     if (gout_dtype == kF32) {

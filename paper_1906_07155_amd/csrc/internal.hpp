@@ -102,16 +102,12 @@ struct GatherArgs {
     int32_t qside;               // 8x8 quadrants per bin-tile side
     int32_t ncg;                 // 64-channel groups
     int32_t wg_per_tile;
-    int32_t cg_form;             // 1: workgroup = 4 channel groups of one quadrant
-                                 //    (bf16 upstream gradient, 7x7, one head)
     int32_t gout_dtype1;         // head 1's upstream-gradient dtype
     int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
     // set at launch: block-id decoding without integer division
     int32_t qs_shift;            // log2 qside
     int32_t wgpt_shift;          // log2 wg_per_tile
-    FastDiv div_tile;            // by ncg * wg_per_tile (quadrant form)
-    FastDiv div_tile_cg;         // by qside^2 * ceil(ncg / 4) (channel-group form)
-    FastDiv div_ncgg;            // by ceil(ncg / 4)
+    FastDiv div_tile;            // by ncg * wg_per_tile
     uint32_t img_m[kMaxLevels];  // by the tiles of one image of a level
     int32_t img_sh[kMaxLevels];
     uint32_t row_m[kMaxLevels];  // by the tiles of one row of a level

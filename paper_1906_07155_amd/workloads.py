@@ -155,6 +155,17 @@ class Workload:
         return len(self.level_hw)
 
     @property
+    def tag(self) -> str:
+        """Short file-name tag: head, batch and dtype (e.g. box_batch2_fp32)."""
+        if not self.fpn:
+            return "single_level_batch%d" % self.n_images
+        head = "box" if self.out_hw == (7, 7) else "mask"
+        if not self.backward:
+            head = "infer"
+        dt = {"f32": "fp32", "bf16": "bf16"}[self.feat_dtype]
+        return "%s_batch%d_%s" % (head, self.n_images, dt)
+
+    @property
     def num_rois(self) -> int:
         return self.n_images * self.per_image
 
@@ -185,8 +196,8 @@ def _pyramid(img_hw):
 
 
 def config(index: int, head: Optional[str] = None, feat_dtype: Optional[str] = None) -> Workload:
-    """Workload `index` (1..5).  cfg4 takes feat_dtype 'f32' or 'bf16'; cfg5 takes head
-    'box' or 'mask'."""
+    """Workload `index` (1..5).  The batch-1 inference workload (4) takes feat_dtype 'f32'
+    or 'bf16'; the batch-16 workload (5) takes head 'box' or 'mask'."""
     seed = BASE_SEED + index
     if index == 1:
         return Workload("single-level 1x256x50x68 fwd, 128 RoIs, 7x7", 1, 256, [(50, 68)],
