@@ -51,10 +51,10 @@ def _bind(lib):
     f64pp = ctypes.POINTER(ctypes.c_void_p)
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_level_map.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
-                                     ctypes.c_float, ctypes.c_void_p]
+                                     ctypes.c_float, ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_level_map.restype = None
     lib.oracle_level_map_log2.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
-                                          ctypes.c_double, ctypes.c_void_p]
+                                          ctypes.c_double, ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_level_map_log2.restype = None
     lib.oracle_roi_align_fwd.argtypes = [f64pp, ctypes.c_void_p, ctypes.c_void_p,
                                          ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
@@ -127,22 +127,26 @@ def _rois(rois) -> np.ndarray:
     return r
 
 
-def level_map(rois, num_levels: int, finest_scale: float = 56.0, lib=None) -> np.ndarray:
-    """Threshold form of the FPN level rule (binary32 area and thresholds)."""
+def level_map(rois, num_levels: int, finest_scale: float = 56.0, box_plus1: bool = False,
+              lib=None) -> np.ndarray:
+    """Threshold form of the FPN level rule (binary32 area and thresholds); with
+    box_plus1 the sides are (x2 - x1) + 1 (boxes as inclusive pixel ranges)."""
     lib = lib or load()
     r = _rois(rois)
     out = np.zeros(r.shape[0], dtype=np.int32)
-    lib.oracle_level_map(_ptr(r), r.shape[0], int(num_levels), float(finest_scale), _ptr(out))
+    lib.oracle_level_map(_ptr(r), r.shape[0], int(num_levels), float(finest_scale),
+                         int(bool(box_plus1)), _ptr(out))
     return out
 
 
-def level_map_log2(rois, num_levels: int, finest_scale: float = 56.0, lib=None) -> np.ndarray:
+def level_map_log2(rois, num_levels: int, finest_scale: float = 56.0, box_plus1: bool = False,
+                   lib=None) -> np.ndarray:
     """floor(log2(sqrt(area)/finest_scale)) clamped, in double precision."""
     lib = lib or load()
     r = _rois(rois)
     out = np.zeros(r.shape[0], dtype=np.int32)
     lib.oracle_level_map_log2(_ptr(r), r.shape[0], int(num_levels), float(finest_scale),
-                              _ptr(out))
+                              int(bool(box_plus1)), _ptr(out))
     return out
 
 

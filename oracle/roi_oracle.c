@@ -69,14 +69,21 @@ int oracle_num_threads(void)
 
 /* Threshold form of the FPN rule: the level is the number of thresholds
  * (finest_scale * 2^j)^2, j = 1 .. L-1, that the box area reaches.  Area and
- * thresholds are binary32 values, one rounding per operation. */
+ * thresholds are binary32 values, one rounding per operation.  With box_plus1 the
+ * box is a range of whole pixels with both ends inside (the convention of the
+ * pre-"aligned" detectors): each side is (x2 - x1) + 1, the difference rounded
+ * first. */
 void oracle_level_map(const float *rois, int64_t K, int32_t num_levels,
-                      float finest_scale, int32_t *out)
+                      float finest_scale, int32_t box_plus1, int32_t *out)
 {
     for (int64_t k = 0; k < K; ++k) {
         const float *r = rois + 5 * k;
         float w = r[3] - r[1];
         float h = r[4] - r[2];
+        if (box_plus1) {
+            w = w + 1.0f;
+            h = h + 1.0f;
+        }
         float area = w * h;
         int32_t lvl = 0;
         for (int32_t j = 1; j < num_levels; ++j) {
@@ -93,12 +100,12 @@ void oracle_level_map(const float *rois, int64_t K, int32_t num_levels,
  * floor(log2(sqrt(w*h) / finest_scale)), clamped to [0, L-1].  Agrees with the
  * threshold form everywhere except within rounding distance of a threshold. */
 void oracle_level_map_log2(const float *rois, int64_t K, int32_t num_levels,
-                           double finest_scale, int32_t *out)
+                           double finest_scale, int32_t box_plus1, int32_t *out)
 {
     for (int64_t k = 0; k < K; ++k) {
         const float *r = rois + 5 * k;
-        double w = (double)r[3] - (double)r[1];
-        double h = (double)r[4] - (double)r[2];
+        double w = (double)r[3] - (double)r[1] + (box_plus1 ? 1.0 : 0.0);
+        double h = (double)r[4] - (double)r[2] + (box_plus1 ? 1.0 : 0.0);
         double a = w * h;
         int32_t lvl = 0;
         if (a > 0.0) {

@@ -79,14 +79,35 @@ def load_level_cases():
             if not line:
                 continue
             v = line.split()
-            rows.append(([0.0] + [float(x) for x in v[:4]], int(v[4]), float(v[5]), int(v[6])))
+            plus1 = bool(int(v[7])) if len(v) > 7 else False
+            rows.append(([0.0] + [float(x) for x in v[:4]], int(v[4]), float(v[5]), int(v[6]),
+                         plus1))
     return rows
 
 
 def pin_level_cases(lib, mode=None):
-    for roi, L, fs, exp in load_level_cases():
-        got = oracle.level_map(np.array([roi], np.float32), L, fs, lib=lib)[0]
-        assert got == exp, (roi, L, fs, got, exp)
+    for roi, L, fs, exp, plus1 in load_level_cases():
+        got = oracle.level_map(np.array([roi], np.float32), L, fs, box_plus1=plus1, lib=lib)[0]
+        assert got == exp, (roi, L, fs, plus1, got, exp)
+
+
+def pin_level_plus1_is_shifted_box(lib, mode=None):
+    """Inclusive pixel boxes: on integer coordinates (where every difference is
+    exact) the level of (x1, y1, x2, y2) with box_plus1 is the level of the continuous
+    box (x1, y1, x2 + 1, y2 + 1)."""
+    rng = np.random.default_rng(11)
+    K = 3000
+    xy = rng.integers(0, 1000, (K, 2))
+    wh = rng.integers(0, 700, (K, 2))
+    rois = np.zeros((K, 5), np.float32)
+    rois[:, 1:3] = xy
+    rois[:, 3:5] = xy + wh
+    shifted = rois.copy()
+    shifted[:, 3:5] += 1
+    a = oracle.level_map(rois, 4, 56.0, box_plus1=True, lib=lib)
+    b = oracle.level_map(shifted, 4, 56.0, lib=lib)
+    assert np.array_equal(a, b)
+    assert set(np.unique(a)) == {0, 1, 2, 3}
 
 
 def pin_level_log2_agrees(lib, mode=None):
@@ -98,16 +119,17 @@ def pin_level_log2_agrees(lib, mode=None):
     rois = np.zeros((K, 5), np.float32)
     rois[:, 1:3] = xy
     rois[:, 3:5] = xy + wh
-    a = oracle.level_map(rois, 4, 56.0, lib=lib)
-    b = oracle.level_map_log2(rois, 4, 56.0, lib=lib)
-    w = rois[:, 3].astype(np.float64) - rois[:, 1]
-    h = rois[:, 4].astype(np.float64) - rois[:, 2]
-    s = np.sqrt(w * h)
-    near = np.zeros(K, bool)
-    for t in (112.0, 224.0, 448.0):
-        near |= np.abs(s / t - 1.0) < 1e-5
-    assert np.array_equal(a[~near], b[~near])
-    assert set(np.unique(a)) == {0, 1, 2, 3}
+    for plus1 in (False, True):
+        a = oracle.level_map(rois, 4, 56.0, box_plus1=plus1, lib=lib)
+        b = oracle.level_map_log2(rois, 4, 56.0, box_plus1=plus1, lib=lib)
+        w = rois[:, 3].astype(np.float64) - rois[:, 1] + plus1
+        h = rois[:, 4].astype(np.float64) - rois[:, 2] + plus1
+        s = np.sqrt(w * h)
+        near = np.zeros(K, bool)
+        for t in (112.0, 224.0, 448.0):
+            near |= np.abs(s / t - 1.0) < 1e-5
+        assert np.array_equal(a[~near], b[~near])
+        assert set(np.unique(a)) == {0, 1, 2, 3}
 
 
 # ---------------------------------------------------------------------------
@@ -382,7 +404,8 @@ def pin_guards(lib, mode):
     assert not grads[0].any()
 
 
-ALL_PINS = [pin_hand_cases, pin_level_cases, pin_level_log2_agrees, pin_constant, pin_affine,
+ALL_PINS = [pin_hand_cases, pin_level_cases, pin_level_log2_agrees, pin_level_plus1_is_shifted_box,
+            pin_constant, pin_affine,
             pin_adjoint, pin_tent, pin_dense_matrix, pin_textbook, pin_mass, pin_guards]
 MATH_ONLY_PINS = [pin_mirror]
 

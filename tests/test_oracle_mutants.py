@@ -40,6 +40,10 @@ MUTANTS = [
      "sum += ty.w_hi * tx.w_hi * F[ty.hi * W + tx.hi];", ""),
     ("level threshold compared with >",
      "if (area >= thr)", "if (area > thr)"),
+    ("inclusive pixel boxes: +1 dropped on one side",
+     "            h = h + 1.0f;\n", ""),
+    ("inclusive pixel boxes: +1 applied to the continuous rule too",
+     "        if (box_plus1) {\n            w = w + 1.0f;", "        if (1) {\n            w = w + 1.0f;"),
     ("level thresholds from finest_scale*2^(j-1)",
      "float side = finest_scale * (float)(1 << j);",
      "float side = finest_scale * (float)(1 << (j - 1));"),
