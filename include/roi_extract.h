@@ -14,7 +14,8 @@
  *     level index is outside the valid range yields zeros and no gradient.
  *   - Level rule (threshold form of the FPN rule floor(log2(sqrt(wh)/s0))):
  *     level = #{ j in 1..L-1 : (x2-x1)*(y2-y1) >= (s0*2^j)^2 }, every product and
- *     difference rounded to binary32, s0 = finest_scale (56 for P2..P5).
+ *     difference rounded to binary32, s0 = finest_scale (56 for P2..P5); the _ex
+ *     entry points can measure boxes in whole pixels instead (RE_BOX_PIXELS).
  *   - On level l with scale s, H x W map, output PH x PW, sampling ratio S:
  *       off = aligned ? 0.5 : 0
  *       x0 = x1*s - off,  xe = x2*s - off,  rw = xe - x0 (>= 1 if !aligned)
@@ -91,6 +92,23 @@ typedef struct {
 re_status_t fpn_level_map(const float *rois, int64_t num_rois, int32_t num_levels,
                           float finest_scale, int32_t *levels_out, void *stream);
 
+/* Box conventions of the level rule (the paper does not fix one; the legacy
+ * detectors of its era, e.g. Fast R-CNN and the first MMDetection releases, §2,
+ * measured boxes in whole pixels):
+ *   RE_BOX_CONTINUOUS  sides x2 - x1, y2 - y1 (the default above);
+ *   RE_BOX_PIXELS      boxes are inclusive pixel ranges: sides (x2 - x1) + 1 and
+ *                      (y2 - y1) + 1, the difference rounded to binary32 first.
+ * Only the level rule changes; the sampling geometry is chosen by `aligned`. */
+#define RE_BOX_CONTINUOUS 0
+#define RE_BOX_PIXELS 1
+
+/* a1 with a box convention: as fpn_level_map, the sides measured by box_convention
+ * (RE_BOX_CONTINUOUS or RE_BOX_PIXELS; anything else is RE_ERR_INVALID_ARG, nothing
+ * enqueued). */
+re_status_t fpn_level_map_ex(const float *rois, int64_t num_rois, int32_t num_levels,
+                             float finest_scale, int32_t box_convention, int32_t *levels_out,
+                             void *stream);
+
 /* Bytes of device workspace a plan for num_rois RoIs over the pyramid `levels` needs
  * (host array; only n, h and w are read).  It holds the launch permutation and the
  * tile->RoI lists of the gather backward (8 bytes per RoI, 8 per bin-tile, and 4 per
@@ -118,6 +136,13 @@ re_status_t roi_extract_plan(const re_level_t *levels, int32_t num_levels,
                              const float *rois, int64_t num_rois, float finest_scale,
                              int32_t *levels_out, void *workspace, size_t workspace_bytes,
                              void *stream);
+
+/* a1 + a2 with a box convention for the level rule (see fpn_level_map_ex); otherwise
+ * as roi_extract_plan. */
+re_status_t roi_extract_plan_ex(const re_level_t *levels, int32_t num_levels,
+                                const float *rois, int64_t num_rois, float finest_scale,
+                                int32_t box_convention, int32_t *levels_out, void *workspace,
+                                size_t workspace_bytes, void *stream);
 
 /* Copy of the plan's per-level offsets: a device int32[num_levels + 1] array
  * (offsets[l] = first position of level l in plan order; offsets[num_levels] =

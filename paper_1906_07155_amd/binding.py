@@ -60,8 +60,10 @@ _HEADS = ctypes.POINTER(ReHead)
 
 SIGNATURES = {
     "fpn_level_map": [_VP, _I64, _I32, _F32, _VP, _VP],
+    "fpn_level_map_ex": [_VP, _I64, _I32, _F32, _I32, _VP, _VP],
     "roi_extract_workspace_size": [_LEVELS, _I32, _I64, ctypes.POINTER(_SZ)],
     "roi_extract_plan": [_LEVELS, _I32, _VP, _I64, _F32, _VP, _VP, _SZ, _VP],
+    "roi_extract_plan_ex": [_LEVELS, _I32, _VP, _I64, _F32, _I32, _VP, _VP, _SZ, _VP],
     "roi_extract_plan_offsets": [_VP, _SZ, _I64, _I32, _VP, _VP],
     "roi_extract_plan_perm": [_VP, _SZ, _I64, ctypes.POINTER(_VP)],
     "roi_align_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _VP, _I32, _VP,
@@ -179,14 +181,24 @@ def _rois(rois):
 # The C ABI, one function each
 # ---------------------------------------------------------------------------
 
-def fpn_level_map(rois, num_levels: int, finest_scale: float = 56.0, out=None, stream=None):
+BOX_CONTINUOUS, BOX_PIXELS = 0, 1   # RE_BOX_CONTINUOUS, RE_BOX_PIXELS
+
+
+def fpn_level_map(rois, num_levels: int, finest_scale: float = 56.0, out=None, stream=None,
+                  box_pixels: bool = False):
+    """Level of every RoI; box_pixels measures boxes as inclusive pixel ranges
+    (fpn_level_map_ex with RE_BOX_PIXELS)."""
     torch = _torch()
     rois = _rois(rois)
     K = rois.shape[0]
     if out is None:
         out = torch.empty(K, dtype=torch.int32, device=rois.device)
-    check(lib().fpn_level_map(rois.data_ptr(), K, num_levels, finest_scale, out.data_ptr(),
-                              stream_handle(stream)), "fpn_level_map")
+    if box_pixels:
+        check(lib().fpn_level_map_ex(rois.data_ptr(), K, num_levels, finest_scale, BOX_PIXELS,
+                                     out.data_ptr(), stream_handle(stream)), "fpn_level_map_ex")
+    else:
+        check(lib().fpn_level_map(rois.data_ptr(), K, num_levels, finest_scale, out.data_ptr(),
+                                  stream_handle(stream)), "fpn_level_map")
     return out
 
 
@@ -200,8 +212,11 @@ def workspace_size(features: Sequence, scales: Sequence[float], num_rois: int) -
 
 
 def plan(features: Sequence, scales: Sequence[float], rois, finest_scale: float = 56.0,
-         levels_out=None, workspace=None, stream=None) -> Tuple[object, object]:
-    """Level of every RoI plus the launch plan.  Returns (roi_levels, workspace)."""
+         levels_out=None, workspace=None, stream=None,
+         box_pixels: bool = False) -> Tuple[object, object]:
+    """Level of every RoI plus the launch plan.  Returns (roi_levels, workspace).
+    box_pixels: the level rule measures boxes as inclusive pixel ranges
+    (roi_extract_plan_ex with RE_BOX_PIXELS)."""
     torch = _torch()
     rois = _rois(rois)
     K, L = rois.shape[0], len(features)
@@ -211,9 +226,15 @@ def plan(features: Sequence, scales: Sequence[float], rois, finest_scale: float 
     if workspace is None:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=rois.device)
     arr = level_array(features, scales)
-    check(lib().roi_extract_plan(arr, L, rois.data_ptr(), K, finest_scale,
-                                 levels_out.data_ptr(), workspace.data_ptr(), workspace.numel(),
-                                 stream_handle(stream)), "roi_extract_plan")
+    if box_pixels:
+        check(lib().roi_extract_plan_ex(arr, L, rois.data_ptr(), K, finest_scale, BOX_PIXELS,
+                                        levels_out.data_ptr(), workspace.data_ptr(),
+                                        workspace.numel(), stream_handle(stream)),
+              "roi_extract_plan_ex")
+    else:
+        check(lib().roi_extract_plan(arr, L, rois.data_ptr(), K, finest_scale,
+                                     levels_out.data_ptr(), workspace.data_ptr(),
+                                     workspace.numel(), stream_handle(stream)), "roi_extract_plan")
     return levels_out, workspace
 
 

@@ -222,6 +222,15 @@ re_status_t roi_extract_workspace_size(const re_level_t *levels, int32_t num_lev
 
 re_status_t fpn_level_map(const float *rois, int64_t num_rois, int32_t num_levels,
                           float finest_scale, int32_t *levels_out, void *stream) {
+    return fpn_level_map_ex(rois, num_rois, num_levels, finest_scale, RE_BOX_CONTINUOUS,
+                            levels_out, stream);
+}
+
+re_status_t fpn_level_map_ex(const float *rois, int64_t num_rois, int32_t num_levels,
+                             float finest_scale, int32_t box_convention, int32_t *levels_out,
+                             void *stream) {
+    if (box_convention != RE_BOX_CONTINUOUS && box_convention != RE_BOX_PIXELS)
+        return RE_ERR_INVALID_ARG;
     if (num_rois < 0 || num_rois > kMaxRois) return RE_ERR_INVALID_ARG;
     if (num_levels < 1 || num_levels > RE_MAX_LEVELS) return RE_ERR_INVALID_ARG;
     if (!std::isfinite(finest_scale) || !(finest_scale > 0.0f)) return RE_ERR_INVALID_ARG;
@@ -230,13 +239,23 @@ re_status_t fpn_level_map(const float *rois, int64_t num_rois, int32_t num_level
     if (reinterpret_cast<uintptr_t>(rois) % 4 || reinterpret_cast<uintptr_t>(levels_out) % 4)
         return RE_ERR_INVALID_ARG;
     return from_hip(launch_level_map(rois, static_cast<int32_t>(num_rois), num_levels,
-                                     finest_scale, levels_out,
-                                     static_cast<hipStream_t>(stream)));
+                                     finest_scale, box_convention == RE_BOX_PIXELS ? 1 : 0,
+                                     levels_out, static_cast<hipStream_t>(stream)));
 }
 
 re_status_t roi_extract_plan(const re_level_t *levels, int32_t num_levels, const float *rois,
                              int64_t num_rois, float finest_scale, int32_t *levels_out,
                              void *workspace, size_t workspace_bytes, void *stream) {
+    return roi_extract_plan_ex(levels, num_levels, rois, num_rois, finest_scale,
+                               RE_BOX_CONTINUOUS, levels_out, workspace, workspace_bytes, stream);
+}
+
+re_status_t roi_extract_plan_ex(const re_level_t *levels, int32_t num_levels, const float *rois,
+                                int64_t num_rois, float finest_scale, int32_t box_convention,
+                                int32_t *levels_out, void *workspace, size_t workspace_bytes,
+                                void *stream) {
+    if (box_convention != RE_BOX_CONTINUOUS && box_convention != RE_BOX_PIXELS)
+        return RE_ERR_INVALID_ARG;
     LevelTable t;
     re_status_t st = check_levels(levels, num_levels, false, &t, nullptr, nullptr, nullptr);
     if (st != RE_OK) return st;
@@ -258,6 +277,7 @@ re_status_t roi_extract_plan(const re_level_t *levels, int32_t num_levels, const
     a.K = static_cast<int32_t>(num_rois);
     a.L = num_levels;
     a.finest_scale = finest_scale;
+    a.box_plus1 = box_convention == RE_BOX_PIXELS ? 1 : 0;
     a.N = t.N;
     // Cell size 2^shift feature pixels: the smallest shift >= 4 whose bucket count fits.
     a.batch_in_key = 1;

@@ -161,10 +161,15 @@ template <> __device__ __forceinline__ float raw_to_f32<uint16_t>(uint32_t v) {
 // FPN level (threshold form), binary32
 // ---------------------------------------------------------------------------
 
+// box_plus1: boxes are inclusive pixel ranges, each side (x2 - x1) + 1.
 __device__ __forceinline__ int fpn_level(float x1, float y1, float x2, float y2, int num_levels,
-                                         float finest_scale) {
-    const float w = x2 - x1;
-    const float h = y2 - y1;
+                                         float finest_scale, int box_plus1) {
+    float w = x2 - x1;
+    float h = y2 - y1;
+    if (box_plus1) {
+        w = w + 1.0f;
+        h = h + 1.0f;
+    }
     const float area = w * h;
     int lvl = 0;
     for (int j = 1; j < num_levels; ++j) {

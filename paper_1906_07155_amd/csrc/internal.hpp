@@ -22,7 +22,7 @@ struct PlanArgs {
     int32_t nbins;
     int32_t cell_shift;    // spatial cell = 2^cell_shift feature pixels
     int32_t batch_in_key;
-    int32_t pad;
+    int32_t box_plus1;     // level rule on inclusive pixel boxes
     int32_t H[kMaxLevels], W[kMaxLevels];
     int32_t ncx[kMaxLevels], ncy[kMaxLevels], base[kMaxLevels];
     float scale[kMaxLevels];
@@ -212,7 +212,7 @@ struct NmsArgs {
 hipError_t launch_nms(NmsArgs a, hipStream_t stream);
 
 hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float finest_scale,
-                            int32_t *out, hipStream_t stream);
+                            int32_t box_plus1, int32_t *out, hipStream_t stream);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);
 
 // Forward: `fast` selects the channels-last kernels (every level stride_c == 1 and

@@ -19,10 +19,11 @@ namespace rex {
 
 __global__ __launch_bounds__(256) void level_map_kernel(const float *__restrict__ rois,
                                                         int32_t K, int32_t L, float finest_scale,
+                                                        int32_t box_plus1,
                                                         int32_t *__restrict__ out) {
     for (int32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < K; k += gridDim.x * blockDim.x) {
         const float *r = rois + 5 * static_cast<int64_t>(k);
-        out[k] = fpn_level(r[1], r[2], r[3], r[4], L, finest_scale);
+        out[k] = fpn_level(r[1], r[2], r[3], r[4], L, finest_scale, box_plus1);
     }
 }
 
@@ -136,7 +137,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
         if (k < a.K) {
             const float *r = a.rois + 5 * static_cast<int64_t>(k);
             const float b0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
-            const int lvl = fpn_level(x1, y1, x2, y2, a.L, a.finest_scale);
+            const int lvl = fpn_level(x1, y1, x2, y2, a.L, a.finest_scale, a.box_plus1);
             a.levels_out[k] = lvl;
             const int bb = roi_batch(b0, a.N);
             ckey[i] = plan_key(a, x1, y1, x2, y2, lvl, bb);
@@ -241,7 +242,7 @@ __global__ __launch_bounds__(256) void plan_count_kernel(PlanArgs a) {
          k += stride) {
         const float *r = a.rois + 5 * k;
         const float b0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
-        const int lvl = fpn_level(x1, y1, x2, y2, a.L, a.finest_scale);
+        const int lvl = fpn_level(x1, y1, x2, y2, a.L, a.finest_scale, a.box_plus1);
         const int bb = roi_batch(b0, a.N);
         if (sub == 0) {
             a.levels_out[k] = lvl;
@@ -334,9 +335,9 @@ __global__ __launch_bounds__(256) void plan_fill_kernel(PlanArgs a) {
 }
 
 hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float finest_scale,
-                            int32_t *out, hipStream_t stream) {
+                            int32_t box_plus1, int32_t *out, hipStream_t stream) {
     const int blocks = min((K + 255) / 256, 4096);
-    level_map_kernel<<<blocks, 256, 0, stream>>>(rois, K, L, finest_scale, out);
+    level_map_kernel<<<blocks, 256, 0, stream>>>(rois, K, L, finest_scale, box_plus1, out);
     return hipGetLastError();
 }
 

@@ -88,6 +88,15 @@ def test_level_map_validation(L):
     assert L.fpn_level_map(None, 0, 4, 56.0, None, None) == OK      # nothing to do
 
 
+def test_level_map_box_convention_validation(L):
+    # only RE_BOX_CONTINUOUS (0) and RE_BOX_PIXELS (1); checked before anything else
+    for conv in (-1, 2, 7):
+        assert L.fpn_level_map_ex(FAKE, 3, 4, 56.0, conv, FAKE, None) == INVALID
+        assert L.fpn_level_map_ex(None, 0, 4, 56.0, conv, None, None) == INVALID
+    assert L.fpn_level_map_ex(None, 0, 4, 56.0, 1, None, None) == OK
+    assert L.fpn_level_map_ex(FAKE, 3, 0, 56.0, 1, FAKE, None) == INVALID
+
+
 def test_forward_validation(L):
     assert _fwd(L, K=0) == OK                                      # nothing to do
     assert _fwd(L, levels=None, nl=0) == INVALID
@@ -168,6 +177,10 @@ def test_plan_validation(L):
     assert L.roi_extract_plan(lv, 2, FAKE, 4, 0.0, FAKE, FAKE, n.value, None) == INVALID
     assert L.roi_extract_plan(lv, 2, None, 4, 56.0, FAKE, FAKE, n.value, None) == INVALID
     assert L.roi_extract_plan(lv, 0, FAKE, 4, 56.0, FAKE, FAKE, n.value, None) == INVALID
+    for conv in (-1, 2):
+        assert L.roi_extract_plan_ex(lv, 2, FAKE, 4, 56.0, conv, FAKE, FAKE, n.value,
+                                     None) == INVALID
+    assert L.roi_extract_plan_ex(lv, 2, FAKE, 4, 56.0, 1, FAKE, None, n.value, None) == WORKSPACE
     p = ctypes.c_void_p(0)
     assert L.roi_extract_plan_perm(FAKE, n.value, 4, ctypes.byref(p)) == OK
     assert p.value == FAKE + 256                                   # perm follows the header

@@ -260,6 +260,44 @@ def test_threshold_boxes_bit_exact():
     assert len(set(ref.tolist())) == 4
 
 
+def test_level_map_pixel_boxes():
+    """Boxes as inclusive pixel ranges (RE_BOX_PIXELS): the level map, the plan's
+    levels and a forward on them, against the oracle with box_plus1; thresholds hit
+    exactly (sides one below, at and one binary32 step around 112, 224, 448 minus 1)
+    and random boxes with fractional corners."""
+    log("level map, inclusive pixel boxes: threshold neighbourhoods and random boxes")
+    rows = []
+    for side in (111.0, 223.0, 447.0):
+        s = np.float32(side)
+        for w in (np.nextafter(s, np.float32(0)), s, np.nextafter(s, np.float32(1e9))):
+            for h in (np.float32(side - 1), s, np.nextafter(s, np.float32(1e9))):
+                for x in (0.0, 13.25, 300.5):
+                    rows.append([0, x, x, np.float32(x) + w, np.float32(x) + h])
+    rng = np.random.default_rng(91)
+    rows += W.draw_rois(rng, 2, 300, (800, 1344), (4.0, 800.0)).tolist()
+    rois = np.array(rows, np.float32)
+    rois[:, 0] = np.minimum(rois[:, 0], 1)
+    ref = oracle.level_map(rois, 4, 56.0, box_plus1=True)
+    r_dev = torch.from_numpy(rois).cuda()
+    got = rex.fpn_level_map(r_dev, 4, 56.0, box_pixels=True).cpu().numpy()
+    assert np.array_equal(got, ref)
+    assert len(set(ref.tolist())) == 4
+    assert not np.array_equal(ref, oracle.level_map(rois, 4, 56.0))   # the convention matters
+    # the plan computes the same levels, and the forward reads the level they name
+    shapes = [(2, 16, 200, 336), (2, 16, 100, 168), (2, 16, 50, 84), (2, 16, 25, 42)]
+    scales = [0.25, 0.125, 0.0625, 0.03125]
+    feats_np = [rng.standard_normal(sh, dtype=np.float32) for sh in shapes]
+    feats = [torch.from_numpy(f).cuda().contiguous(memory_format=torch.channels_last)
+             for f in feats_np]
+    lv, ws = rex.plan(feats, scales, r_dev, 56.0, box_pixels=True)
+    assert np.array_equal(lv.cpu().numpy(), ref)
+    out = rex.roi_align_fwd(feats, scales, r_dev, lv, (7, 7), 2, True, workspace=ws)
+    torch.cuda.synchronize()
+    exp = oracle.roi_align_fwd([f.astype(np.float64) for f in feats_np], scales, rois, ref,
+                               7, 7, 2, True)
+    check_fwd(from_device(out), exp, False, "forward on pixel-box levels")
+
+
 def test_gpu_invariants():
     """Constant maps give constants; the backward conserves mass and is the adjoint."""
     log("invariants: constant, mass, adjoint (fp32 on the GPU)")
