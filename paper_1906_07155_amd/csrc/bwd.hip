@@ -5,6 +5,11 @@
 // g[k,c,ph,pw] * w / count into the four pixels the forward read.
 //
 // Kernels:
+//   bwd_gather_kernel   the default: per (bin-tile, 64 channels), the RoIs binned to the
+//                       tile are gathered into register accumulators and every gradient
+//                       element is stored once (no atomics, clearing included); see
+//                       "Tile-gather backward" below.
+//   bwd_gather2_kernel  the same for two heads on one pyramid in one pass.
 //   bwd_cl_kernel       channels-last gradient levels, specialised grids.  Lanes run
 //                       over channels, so the 64 lanes of one atomic instruction hit
 //                       64 consecutive floats of one pixel.  Contributions of one RoI
