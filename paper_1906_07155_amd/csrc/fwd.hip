@@ -207,7 +207,9 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     constexpr int MAXY = 2 * RPW * S;            // distinct tap rows per wave
     constexpr int MAXX = ((2 * NCOL + CX - 1) / CX) * CX;   // distinct tap columns, padded
     constexpr int PWP = (PW + 3) & ~3;           // padded for 16-byte LDS reads
-    static_assert(NR + NCOL <= 256 && NCOL <= 64 && RPW * S <= 64, "geometry sizes");
+    constexpr int QH = (PW + 1) / 2;             // the bin columns' first half
+    constexpr bool kHalves = PW >= 12;           // skip the halves a column misses
+    static_assert(NR + NCOL <= 256 && NCOL <= 64 && RPW * S <= 64 && MAXX <= 64, "geometry sizes");
     static_assert(64 % CHK == 0 && CX % 4 == 0, "tiling");
 
     __shared__ SampleTap srow[NR];
@@ -218,6 +220,7 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     __shared__ __align__(16) float s_wy[4][MAXY][RPWP];
     __shared__ int32_t s_nx;
     __shared__ int32_t s_ny[4];
+    __shared__ uint64_t s_xhalf[2];   // bit x: column x weighs on bins [0, QH) / [QH, PW)
     __shared__ float stile[CHK * NB];
 
     // Which RoI and slice: XCD-aware block order, then the plan's permutation.
@@ -276,6 +279,25 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
         if (wave == 0) {
             const int nx = distinct_taps<S, PWP>(scol, NCOL, lane, sw_b, kInvS, s_xoff, s_wx);
             if (lane == 0) s_nx = nx;
+            // Which half of the bin columns each distinct column reaches (a column is
+            // reached by a run of at most a few adjacent bins, mostly inside one half);
+            // padding columns reach none.
+            wave_sync();
+            bool lo = false, hi = false;
+            if (lane < MAXX) {
+#pragma unroll
+                for (int q = 0; q < PW; ++q) {
+                    const bool nz = s_wx[lane][q] != 0.0f;
+                    if (q < QH) lo = lo || nz;
+                    else hi = hi || nz;
+                }
+            }
+            const uint64_t blo = __builtin_amdgcn_ballot_w64(lo);
+            const uint64_t bhi = __builtin_amdgcn_ballot_w64(hi);
+            if (lane == 0) {
+                s_xhalf[0] = blo;
+                s_xhalf[1] = bhi;
+            }
         }
     }
     __syncthreads();
@@ -296,6 +318,10 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     // Columns past the footprint read zeros (out-of-range offsets, zero weights).
     const int ny = s_ny[wave];
     const int nch = (s_nx + CX - 1) / CX;
+    const uint64_t xlo = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[0] >> 32))) << 32) |
+                         static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[0])));
+    const uint64_t xhi = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[1] >> 32))) << 32) |
+                         static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[1])));
     float acc[RPW][PW];
 #pragma unroll
     for (int p = 0; p < RPW; ++p)
@@ -324,11 +350,23 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
         if (yi == ny - 1) {
 #pragma unroll
             for (int x = 0; x < CX; ++x) {
-                const float *wx = s_wx[ch * CX + x];
+                const int col = ch * CX + x;
+                const float *wx = s_wx[col];
+                // each half of the bins only where the column reaches it (the other
+                // weights are zero); on the 7-wide grid the test costs more than the
+                // few products it saves
+                if (!kHalves || ((xlo >> col) & 1)) {
 #pragma unroll
-                for (int q = 0; q < PW; ++q)
+                    for (int q = 0; q < QH; ++q)
 #pragma unroll
-                    for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+                        for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+                }
+                if (!kHalves || ((xhi >> col) & 1)) {
+#pragma unroll
+                    for (int q = QH; q < PW; ++q)
+#pragma unroll
+                        for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+                }
 #pragma unroll
                 for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
                 // one column's weights live at a time
