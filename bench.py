@@ -99,6 +99,39 @@ def stored_traffic(kernel: str, workload: str):  # kernel: fwd | bwd_gather | bw
         return None
 
 
+def time_two_passes(step, names, nsteps, stream):
+    """Step time and per-call durations over `nsteps` steps of `step(ev)`.
+
+    An event recorded between two kernels on the stream leaves the GPU idle for about
+    5 us, so the step time comes from a pass with events only at its two ends, and the
+    per-call durations from a second pass of as many steps in which `step` records
+    ev[j] before call j and ev[len(names)] after the last.  Returns (ms per step,
+    {name: ms per call}, ms per step of the pass with events)."""
+    import torch
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    torch.cuda.synchronize()
+    t0, t1 = ev(), ev()
+    t0.record(stream)
+    for _ in range(nsteps):
+        step(None)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / nsteps
+    evs = [[ev() for _ in range(len(names) + 1)] for _ in range(nsteps)]
+    t0, t1 = ev(), ev()
+    t0.record(stream)
+    for i in range(nsteps):
+        step(evs[i])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(nsteps)]))
+           for j, n in enumerate(names)}
+    return ms, per, t0.elapsed_time(t1) / nsteps
+
+
 def calibrate_copy():
     import torch
     n = 256 * 1024 * 1024          # 1 GiB of float32
@@ -202,34 +235,21 @@ def main():
             mark()
 
     def timed(algo, nsteps):
-        names = names_for(algo)
-        nev = len(names) + 1
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(nsteps)]
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t0.record(stream)
-        for i in range(nsteps):
-            step(algo, evs[i])
-        t1.record(stream)
-        torch.cuda.synchronize()
-        per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(nsteps)]))
-               for j, n in enumerate(names)}
-        return t0.elapsed_time(t1) / nsteps, per
+        return time_two_passes(lambda ev: step(algo, ev), names_for(algo), nsteps, stream)
 
     algo = args.bwd
     names = names_for(algo)
     for _ in range(args.warmup):
         step(algo)
     torch.cuda.synchronize()
-    ms_per_step, per_kernel = timed(algo, args.steps)
+    ms_per_step, per_kernel, ms_with_events = timed(algo, args.steps)
 
     alt = None
     if backward and args.alt_steps > 0:
         other = "scatter" if algo == "gather" else "gather"
         for _ in range(5):
             step(other)
-        alt_ms, alt_per = timed(other, args.alt_steps)
+        alt_ms, alt_per, _ = timed(other, args.alt_steps)
         alt = {"bwd": other, "ms_per_step": round(alt_ms, 5),
                "kernel_ms": {n: round(v, 5) for n, v in alt_per.items()}}
 
@@ -300,6 +320,7 @@ def main():
         "kernel_ms": {n: round(v, 5) for n, v in per_kernel.items()},
         "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
         "step_GBps_effective": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "ms_per_step_with_kernel_events": round(ms_with_events, 5),
         "copy_GBps_measured": copy_gbs,
         "bytes": {"E_fwd": by.e_fwd, "E_bwd": by.e_bwd, "U_fwd": by.u_fwd, "U_bwd": by.u_bwd,
                   "T_fwd": by.t_fwd, "zero_fill": by.zero,
@@ -398,17 +419,7 @@ def main_pool(args):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
-    for i in range(args.steps):
-        step(evs[i])
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = t0.elapsed_time(t1) / args.steps
-    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
-           for j, n in enumerate(names)}
+    ms_per_step, per, ms_with_events = time_two_passes(step, names, args.steps, stream)
     lv_np = levels.cpu().numpy()
     by = accounting.count_pool(rois_np, lv_np, wl.level_hw, wl.scales, wl.n_images, C, wl.out_hw,
                                2 if bf16 else 4, 2 if wl.out_dtype == "bf16" else 4,
@@ -448,6 +459,7 @@ def main_pool(args):
                    "layout": "cl", "backward": True},
         "roofline": roofline, "cpu_baseline": cpu,
         "extra": {"kernel_ms": {n: round(v, 5) for n, v in per.items()},
+                  "ms_per_step_with_kernel_events": round(ms_with_events, 5),
                   "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
                   "bytes": {"E_fwd": by.e_fwd, "E_bwd": by.e_bwd, "zero_fill": by.zero,
                             "box_px": by.box_px},
@@ -528,18 +540,8 @@ def main_heads(args):
     def timed(fused, n):
         for _ in range(max(1, args.warmup)):
             step(fused)
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t0.record(stream)
-        for i in range(n):
-            step(fused, evs[i])
-        t1.record(stream)
-        torch.cuda.synchronize()
-        return (t0.elapsed_time(t1) / n,
-                float(np.mean([evs[i][0].elapsed_time(evs[i][1]) for i in range(n)])),
-                float(np.mean([evs[i][1].elapsed_time(evs[i][2]) for i in range(n)])))
+        ms, per, _ = time_two_passes(lambda ev: step(fused, ev), ["plan_fwd", "bwd"], n, stream)
+        return ms, per["plan_fwd"], per["bwd"]
 
     ms, ms_plan_fwd, ms_bwd = timed(True, args.steps)
     alt = timed(False, max(1, args.alt_steps)) if args.alt_steps > 0 else None
@@ -639,17 +641,7 @@ def main_deform(args):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
-    for i in range(args.steps):
-        step(evs[i])
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = t0.elapsed_time(t1) / args.steps
-    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
-           for j, n in enumerate(names)}
+    ms_per_step, per, ms_with_events = time_two_passes(step, names, args.steps, stream)
     lv_np = levels.cpu().numpy()
     fp = accounting.deform_footprint(rois_np, lv_np, wl.level_hw, wl.scales, wl.n_images,
                                      wl.out_hw, wl.sampling_ratio, wl.aligned, off_np, gamma)
@@ -701,6 +693,7 @@ def main_deform(args):
                      "bytes_per_launch": alg[dominant], "launch_ms": round(per[dominant], 5)},
         "cpu_baseline": cpu,
         "extra": {"kernel_ms": {n: round(v, 5) for n, v in per.items()},
+                  "ms_per_step_with_kernel_events": round(ms_with_events, 5),
                   "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
                   "footprint_px": fp, "kernel_source_hash": kernel_source_hash()},
     }

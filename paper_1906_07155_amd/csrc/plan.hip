@@ -27,6 +27,32 @@ __global__ __launch_bounds__(256) void level_map_kernel(const float *__restrict_
     }
 }
 
+// Per-level tables of the plan arguments, staged in LDS at kernel start: indexing the
+// argument arrays with a per-lane level would make every lane load from the
+// kernel-argument segment after its RoI's level is known; the staging loads are issued
+// at once, alongside the first RoI loads.
+struct LevelTab {
+    float scale[kMaxLevels];
+    int32_t W[kMaxLevels], H[kMaxLevels], ncx[kMaxLevels], ncy[kMaxLevels], base[kMaxLevels];
+    int32_t tbase[kMaxLevels], ntx[kMaxLevels], nty[kMaxLevels];
+};
+
+// Threads 0..kMaxLevels-1 fill the table; a barrier must follow before it is read.
+__device__ __forceinline__ void load_tab(const PlanArgs &a, LevelTab &t) {
+    const int i = threadIdx.x;
+    if (i < kMaxLevels) {
+        t.scale[i] = a.scale[i];
+        t.W[i] = a.W[i];
+        t.H[i] = a.H[i];
+        t.ncx[i] = a.ncx[i];
+        t.ncy[i] = a.ncy[i];
+        t.base[i] = a.base[i];
+        t.tbase[i] = a.tbase[i];
+        t.ntx[i] = a.ntx[i];
+        t.nty[i] = a.nty[i];
+    }
+}
+
 // Inclusive prefix sum across the 64 lanes of a wavefront.
 __device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
 #pragma unroll
@@ -75,11 +101,11 @@ __device__ int block_exclusive_scan(int32_t *hist, int n, int32_t *part) {
 // Every sample of the RoI lies between the (shifted) box edges for any output size,
 // sampling ratio and alignment; taps add one pixel, and a 1.5-pixel margin absorbs
 // rounding.  Non-finite boxes cover the whole map.
-__device__ void roi_tile_box(const PlanArgs &a, int lvl, float x1, float y1, float x2, float y2,
+__device__ void roi_tile_box(const PlanArgs &a, const LevelTab &tb, int lvl, float x1, float y1, float x2, float y2,
                              int &tx0, int &tx1, int &ty0, int &ty1) {
-    const float s = a.scale[lvl];
-    const float W = static_cast<float>(a.W[lvl] - 1);
-    const float H = static_cast<float>(a.H[lvl] - 1);
+    const float s = tb.scale[lvl];
+    const float W = static_cast<float>(tb.W[lvl] - 1);
+    const float H = static_cast<float>(tb.H[lvl] - 1);
     float lx = 0.0f, hx = W, ly = 0.0f, hy = H;
     if (isfinite(x1) && isfinite(x2) && isfinite(y1) && isfinite(y2)) {
         lx = fminf(fmaxf(fminf(x1, x2) * s - 1.5f, 0.0f), W);
@@ -91,21 +117,21 @@ __device__ void roi_tile_box(const PlanArgs &a, int lvl, float x1, float y1, flo
     tx1 = max(static_cast<int>(hx) >> a.tile_shift, tx0);
     ty0 = static_cast<int>(ly) >> a.tile_shift;
     ty1 = max(static_cast<int>(hy) >> a.tile_shift, ty0);
-    tx1 = min(tx1, a.ntx[lvl] - 1);
-    ty1 = min(ty1, a.nty[lvl] - 1);
+    tx1 = min(tx1, tb.ntx[lvl] - 1);
+    ty1 = min(ty1, tb.nty[lvl] - 1);
 }
 
 // Sort key of a RoI: level bucket + image + spatial cell of the box centre.
-__device__ __forceinline__ int plan_key(const PlanArgs &a, float x1, float y1, float x2, float y2,
+__device__ __forceinline__ int plan_key(const PlanArgs &a, const LevelTab &tb, float x1, float y1, float x2, float y2,
                                         int lvl, int bb) {
     const int b = (bb < 0 || !a.batch_in_key) ? 0 : bb;
-    float cx = (x1 + x2) * 0.5f * a.scale[lvl];
-    float cy = (y1 + y2) * 0.5f * a.scale[lvl];
-    cx = fminf(fmaxf(cx, 0.0f), static_cast<float>(a.W[lvl] - 1));   // NaN -> 0
-    cy = fminf(fmaxf(cy, 0.0f), static_cast<float>(a.H[lvl] - 1));
-    const int gx = min(static_cast<int>(cx) >> a.cell_shift, a.ncx[lvl] - 1);
-    const int gy = min(static_cast<int>(cy) >> a.cell_shift, a.ncy[lvl] - 1);
-    return a.base[lvl] + (b * a.ncy[lvl] + gy) * a.ncx[lvl] + gx;
+    float cx = (x1 + x2) * 0.5f * tb.scale[lvl];
+    float cy = (y1 + y2) * 0.5f * tb.scale[lvl];
+    cx = fminf(fmaxf(cx, 0.0f), static_cast<float>(tb.W[lvl] - 1));   // NaN -> 0
+    cy = fminf(fmaxf(cy, 0.0f), static_cast<float>(tb.H[lvl] - 1));
+    const int gx = min(static_cast<int>(cx) >> a.cell_shift, tb.ncx[lvl] - 1);
+    const int gy = min(static_cast<int>(cy) >> a.cell_shift, tb.ncy[lvl] - 1);
+    return tb.base[lvl] + (b * tb.ncy[lvl] + gy) * tb.ncx[lvl] + gx;
 }
 
 // The tile phases give each RoI kPlanLanes consecutive lanes, which split its tiles,
@@ -123,9 +149,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
     int32_t *hist = smem;                           // [max(nbins, ntiles)]
     int32_t *part = hist + max(a.nbins, a.ntiles);  // [kPlanThreads]
     int32_t *box = part + kPlanThreads;             // [3 * kPlanSmall]: tile box per RoI
+    __shared__ LevelTab tb;
     const int tid = threadIdx.x;
     int ckey[kCached];
 
+    // the RoIs are loaded before the first barrier, alongside the level tables
+    float rv[kCached][5];
+#pragma unroll
+    for (int i = 0; i < kCached; ++i) {
+        const int32_t k = tid + i * kPlanThreads;
+        if (k < a.K) {
+            const float *r = a.rois + 5 * static_cast<int64_t>(k);
+#pragma unroll
+            for (int j = 0; j < 5; ++j) rv[i][j] = r[j];
+        }
+    }
+    load_tab(a, tb);
     for (int i = tid; i < a.nbins; i += kPlanThreads) hist[i] = 0;
     __syncthreads();
 
@@ -135,19 +174,18 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
     for (int i = 0; i < kCached; ++i) {
         const int32_t k = tid + i * kPlanThreads;
         if (k < a.K) {
-            const float *r = a.rois + 5 * static_cast<int64_t>(k);
-            const float b0 = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
+            const float b0 = rv[i][0], x1 = rv[i][1], y1 = rv[i][2], x2 = rv[i][3], y2 = rv[i][4];
             const int lvl = fpn_level(x1, y1, x2, y2, a.L, a.finest_scale, a.box_plus1);
             a.levels_out[k] = lvl;
             const int bb = roi_batch(b0, a.N);
-            ckey[i] = plan_key(a, x1, y1, x2, y2, lvl, bb);
+            ckey[i] = plan_key(a, tb, x1, y1, x2, y2, lvl, bb);
             atomicAdd(&hist[ckey[i]], 1);
             int first = -1, xr = 0, yr = 0;
             if (a.ntiles > 0 && bb >= 0) {
                 int tx0, tx1, ty0, ty1;
-                roi_tile_box(a, lvl, x1, y1, x2, y2, tx0, tx1, ty0, ty1);
-                first = a.tbase[lvl] + (bb * a.nty[lvl] + ty0) * a.ntx[lvl] + tx0;
-                xr = (tx1 - tx0 + 1) | (a.ntx[lvl] << 16);
+                roi_tile_box(a, tb, lvl, x1, y1, x2, y2, tx0, tx1, ty0, ty1);
+                first = tb.tbase[lvl] + (bb * tb.nty[lvl] + ty0) * tb.ntx[lvl] + tx0;
+                xr = (tx1 - tx0 + 1) | (tb.ntx[lvl] << 16);
                 yr = ty1 - ty0 + 1;
             }
             box[3 * k] = first;
@@ -160,7 +198,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
     block_exclusive_scan(hist, a.nbins, part);
 
     // Per-level offsets: the first slot of each level's bucket range.
-    if (tid < a.L) a.offsets[tid] = hist[a.base[tid]];
+    if (tid < a.L) a.offsets[tid] = hist[tb.base[tid]];
     if (tid == 0) a.offsets[a.L] = a.K;
     __syncthreads();
 
@@ -236,6 +274,9 @@ __global__ __launch_bounds__(256) void plan_clear_kernel(int32_t *__restrict__ a
 }
 
 __global__ __launch_bounds__(256) void plan_count_kernel(PlanArgs a) {
+    __shared__ LevelTab tb;
+    load_tab(a, tb);
+    __syncthreads();
     const int sub = threadIdx.x % kPlanLanes;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * (256 / kPlanLanes);
     for (int64_t k = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) / kPlanLanes; k < a.K;
@@ -246,19 +287,19 @@ __global__ __launch_bounds__(256) void plan_count_kernel(PlanArgs a) {
         const int bb = roi_batch(b0, a.N);
         if (sub == 0) {
             a.levels_out[k] = lvl;
-            const int key = plan_key(a, x1, y1, x2, y2, lvl, bb);
+            const int key = plan_key(a, tb, x1, y1, x2, y2, lvl, bb);
             a.keys[k] = key;
             atomicAdd(&a.key_count[key], 1);
         }
         if (a.ntiles > 0 && bb >= 0) {
             int tx0, tx1, ty0, ty1;
-            roi_tile_box(a, lvl, x1, y1, x2, y2, tx0, tx1, ty0, ty1);
+            roi_tile_box(a, tb, lvl, x1, y1, x2, y2, tx0, tx1, ty0, ty1);
             const int w = tx1 - tx0 + 1;
             const int n = w * (ty1 - ty0 + 1);
-            const int base = a.tbase[lvl] + bb * a.nty[lvl] * a.ntx[lvl];
+            const int base = tb.tbase[lvl] + bb * tb.nty[lvl] * tb.ntx[lvl];
             for (int i = sub; i < n; i += kPlanLanes) {
                 const int dy = i / w;
-                atomicAdd(&a.tile_start[base + (ty0 + dy) * a.ntx[lvl] + tx0 + (i - dy * w)], 1);
+                atomicAdd(&a.tile_start[base + (ty0 + dy) * tb.ntx[lvl] + tx0 + (i - dy * w)], 1);
             }
         }
     }
@@ -306,6 +347,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_scan_kernel(PlanArgs a) {
 }
 
 __global__ __launch_bounds__(256) void plan_fill_kernel(PlanArgs a) {
+    __shared__ LevelTab tb;
+    load_tab(a, tb);
+    __syncthreads();
     const int sub = threadIdx.x % kPlanLanes;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * (256 / kPlanLanes);
     for (int64_t k = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) / kPlanLanes; k < a.K;
@@ -320,13 +364,13 @@ __global__ __launch_bounds__(256) void plan_fill_kernel(PlanArgs a) {
             if (bb < 0) continue;
             const int lvl = a.levels_out[k];
             int tx0, tx1, ty0, ty1;
-            roi_tile_box(a, lvl, r[1], r[2], r[3], r[4], tx0, tx1, ty0, ty1);
+            roi_tile_box(a, tb, lvl, r[1], r[2], r[3], r[4], tx0, tx1, ty0, ty1);
             const int w = tx1 - tx0 + 1;
             const int n = w * (ty1 - ty0 + 1);
-            const int base = a.tbase[lvl] + bb * a.nty[lvl] * a.ntx[lvl];
+            const int base = tb.tbase[lvl] + bb * tb.nty[lvl] * tb.ntx[lvl];
             for (int i = sub; i < n; i += kPlanLanes) {
                 const int dy = i / w;
-                const int t = base + (ty0 + dy) * a.ntx[lvl] + tx0 + (i - dy * w);
+                const int t = base + (ty0 + dy) * tb.ntx[lvl] + tx0 + (i - dy * w);
                 const int p = atomicAdd(&a.tile_cursor[t], 1);
                 if (p < a.capacity) a.tile_rois[p] = static_cast<int32_t>(k);
             }

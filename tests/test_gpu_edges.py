@@ -233,6 +233,31 @@ def test_dense_rois_on_one_tile():
     run("150 stacked RoIs", _pyr(64), SC, rois)
     run("150 stacked RoIs bf16 grad", _pyr(64), SC, rois, gdt="bf16")
     run("150 stacked RoIs mask", _pyr(64), SC, rois, out_hw=(14, 14))
+    # the cut lists' partial sums added onto existing gradients
+    run("150 stacked RoIs accumulate", _pyr(64), SC, rois, zero_init=False)
+    run("150 stacked RoIs mask accumulate bf16 grad", _pyr(64), SC, rois, out_hw=(14, 14),
+        zero_init=False, gdt="bf16")
+
+
+def test_many_long_tile_lists():
+    """40 hot spots of 40 RoIs each: more long tile lists than the plan has partial slots
+    for, so only the longest are cut into parts and the rest run whole."""
+    rng = np.random.default_rng(87)
+    shapes = [(1, 64, 128, 128), (1, 64, 64, 64), (1, 64, 32, 32), (1, 64, 16, 16)]
+    centres = rng.uniform(40, 472, (40, 2))
+    rows = []
+    for cx, cy in centres:
+        half = rng.uniform(8, 24, (40, 2))
+        jit = rng.uniform(-6, 6, (40, 2))
+        x1 = np.clip(cx + jit[:, 0] - half[:, 0], 0, 512)
+        x2 = np.clip(cx + jit[:, 0] + half[:, 0], 0, 512)
+        y1 = np.clip(cy + jit[:, 1] - half[:, 1], 0, 512)
+        y2 = np.clip(cy + jit[:, 1] + half[:, 1], 0, 512)
+        rows.append(np.stack([np.zeros(40), x1, y1, x2, y2], 1))
+    rois = np.concatenate(rows).astype(np.float32)
+    run("40 hot spots", shapes, SC, rois)
+    run("40 hot spots accumulate", shapes, SC, rois, zero_init=False)
+    run("40 hot spots mask bf16 grad", shapes, SC, rois, out_hw=(14, 14), gdt="bf16")
 
 
 def test_plan_order_is_irrelevant_to_results():
