@@ -70,10 +70,18 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_source_hash() -> str:
+ALL_SOURCES = ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip",
+               "deform.hip", "nms.hip", "api.hip")
+# the sources a kernel's code comes from (its device code and the shared headers)
+KERNEL_SOURCES = {"fwd": ("common.hpp", "internal.hpp", "fwd.hip"),
+                  "bwd_gather": ("common.hpp", "internal.hpp", "bwd.hip"),
+                  "bwd_scatter": ("common.hpp", "internal.hpp", "bwd.hip")}
+
+
+def kernel_source_hash(kernel: str = None) -> str:
+    """Hash of the sources of `kernel` (a KERNEL_SOURCES key), or of every source."""
     h = hashlib.sha256()
-    for name in ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip",
-                 "deform.hip", "nms.hip", "api.hip"):
+    for name in KERNEL_SOURCES[kernel] if kernel else ALL_SOURCES:
         with open(os.path.join(ROOT, "paper_1906_07155_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -81,7 +89,7 @@ def kernel_source_hash() -> str:
 
 def stored_traffic(kernel: str, workload: str):  # kernel: fwd | bwd_gather | bwd_scatter
     """HBM bytes per launch from a committed rocprofv3 counter summary, if it was taken
-    on the current kernel sources (else None)."""
+    on the current sources of that kernel (else None)."""
     path = os.path.join(PROFILE_DIR, "traffic_%s_%s.txt" % (kernel, workload))
     if not os.path.exists(path):
         return None
@@ -91,7 +99,7 @@ def stored_traffic(kernel: str, workload: str):  # kernel: fwd | bwd_gather | bw
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("kernel_source_hash") != kernel_source_hash():
+    if vals.get("kernel_source_hash") != kernel_source_hash(kernel):
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
@@ -334,6 +342,7 @@ def main():
         "layout": args.layout,
         "plan": not args.no_plan,
         "kernel_source_hash": kernel_source_hash(),
+        "kernel_source_hashes": {k: kernel_source_hash(k) for k in KERNEL_SOURCES},
     }
 
     cpu = None
