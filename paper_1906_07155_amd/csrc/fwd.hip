@@ -5,7 +5,7 @@
 //
 // Two kernels:
 //   fwd_cl_kernel       channels-last levels (stride_c == 1), specialised output
-//                       grids.  One workgroup = one RoI x one slice of 64 channels;
+//                       grids.  One workgroup = one RoI x 1-4 slices of 64 channels;
 //                       lanes run over channels, so every pixel read is one
 //                       coalesced, channel-contiguous load.  The RoI's sample
 //                       geometry is reduced once into LDS to its distinct tap rows
@@ -193,7 +193,7 @@ __device__ __forceinline__ int distinct_taps(const SampleTap *taps, int ns, int 
     return n;
 }
 
-// One workgroup per (RoI, slice of 64 channels); lane = channel.  Wave w owns bin
+// One workgroup per (RoI, run of spw slices of 64 channels); lane = channel.  Wave w owns bin
 // rows [w*RPW, min(PH, (w+1)*RPW)) and loads the distinct tap rows of those bin
 // rows times all distinct tap columns of the RoI, in chunks of CX columns, with
 // the next unit's loads issued before the current one is reduced.
@@ -225,8 +225,10 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
 
     // Which RoI and slice: XCD-aware block order, then the plan's permutation.
     const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
-    const int slot = static_cast<int>(lid / static_cast<uint32_t>(a.nslices));
-    const int slice = static_cast<int>(lid) - slot * a.nslices;
+    const int slot = static_cast<int>(lid / static_cast<uint32_t>(a.wg_per_roi));
+    const int sub = static_cast<int>(lid) - slot * a.wg_per_roi;
+    const int slice0 = sub * a.spw;                          // this workgroup's slices
+    const int slice1 = min(a.nslices, slice0 + a.spw);
     int k = uniform_i(a.perm ? a.perm[slot] : slot);
     const bool kvalid = k >= 0 && k < a.K;
     if (!kvalid) k = 0;
@@ -302,6 +304,15 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     }
     __syncthreads();
 
+    const int ny = s_ny[wave];
+    const int nch = (s_nx + CX - 1) / CX;
+    const uint64_t xlo = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[0] >> 32))) << 32) |
+                         static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[0])));
+    const uint64_t xhi = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[1] >> 32))) << 32) |
+                         static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[1])));
+    // The geometry above serves every slice of the workgroup.
+    for (int slice = slice0; slice < slice1; ++slice) {
+    if (slice > slice0) __syncthreads();   // the previous slice's output tile is stored
     const int c = slice * 64 + lane;
     const bool lane_on = active && c < a.lv.C;
     // One buffer resource per image of the level; a lane with no channel reads out
@@ -316,12 +327,6 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     // and reduced over rows first, H[x][p] = sum_y Wy[p][y] F[y][x]; at the end of
     // the chunk the columns are reduced into the bins, acc[p][q] += Wx[q][x] H[x][p].
     // Columns past the footprint read zeros (out-of-range offsets, zero weights).
-    const int ny = s_ny[wave];
-    const int nch = (s_nx + CX - 1) / CX;
-    const uint64_t xlo = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[0] >> 32))) << 32) |
-                         static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[0])));
-    const uint64_t xhi = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[1] >> 32))) << 32) |
-                         static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[1])));
     float acc[RPW][PW];
 #pragma unroll
     for (int p = 0; p < RPW; ++p)
@@ -478,6 +483,7 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
             for (int e = t; e < ne; e += 256) store_f32(out_blk + c0 * NB + e, stile[e]);
         if (c0 + CHK < 64) __syncthreads();
     }
+    }   // slices
 }
 
 // ---------------------------------------------------------------------------
@@ -492,8 +498,19 @@ template <typename T, typename TO>
 static hipError_t launch_fwd_typed(FwdArgs a, bool fast, hipStream_t stream) {
     if (fast) {
         a.nslices = (a.lv.C + 63) / 64;
-        a.wg_per_roi = a.nslices;
-        const int64_t grid = static_cast<int64_t>(a.K) * a.nslices;
+        // Slices per workgroup: the RoI's geometry (two IEEE divisions, the distinct-tap
+        // reductions) is built once per workgroup, so a workgroup takes up to 4 slices
+        // while the grid keeps at least 32 workgroups per CU; below that the longest
+        // workgroups would set the kernel's tail (measured, 1024 RoIs x 256 channels:
+        // 53 us with one slice, 56 with two; 8192 RoIs: 361 us with one, 328 with four).
+        a.spw = 1;
+        for (int spw = 4; spw > 1; spw /= 2)
+            if (static_cast<int64_t>(a.K) * ((a.nslices + spw - 1) / spw) >= 8192) {
+                a.spw = spw;
+                break;
+            }
+        a.wg_per_roi = (a.nslices + a.spw - 1) / a.spw;
+        const int64_t grid = static_cast<int64_t>(a.K) * a.wg_per_roi;
         // a dispatch holds fewer than 2^32 work-items; beyond that, the strided kernel
         if (grid >= (int64_t(1) << 24)) return launch_fwd_typed<T, TO>(a, false, stream);
         if (a.PH == 7)

@@ -125,7 +125,7 @@ struct FwdArgs {
     int32_t aligned;
     int32_t nslices;             // channel slices per RoI (fast kernels)
     int32_t wg_per_roi;          // workgroups per RoI (fast kernels)
-    int32_t pad;
+    int32_t spw;                 // slices per workgroup (channels-last forward)
 };
 
 struct BwdArgs {

@@ -260,6 +260,14 @@ def test_many_long_tile_lists():
     run("40 hot spots mask bf16 grad", shapes, SC, rois, out_hw=(14, 14), gdt="bf16")
 
 
+def test_forward_many_rois_ragged_slices():
+    """Enough RoIs that a forward workgroup takes several 64-channel slices of its RoI:
+    300 channels = 4 slices + one of 44, so RoIs split 4 + 1 across two workgroups."""
+    rng = np.random.default_rng(88)
+    rois = W.draw_rois(rng, 2, 2048, (96, 160), (4.0, 200.0))
+    run("4096 RoIs, 300 channels", _pyr(300), SC, rois, backward=False)
+
+
 def test_plan_order_is_irrelevant_to_results():
     rng = np.random.default_rng(80)
     rois = W.draw_rois(rng, 2, 40, (96, 160), (4.0, 200.0))
