@@ -353,30 +353,90 @@ __global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
         const float gv = lane_on ? s_g[lane * NB + jb] : 0.0f;
         const float gq = (gv * m) / static_cast<float>(count);
         float px = 0.0f, py = 0.0f, pm = 0.0f;
-        for (int iy = 0; iy < d.ay.grid; ++iy) {
-            const DTap ty = deform_tap(d.ay, sy, ph, iy, L.H);
-            if (!ty.valid) continue;
+        // One sample: its four taps feed the offset and modulation gradients, and, when
+        // `scatter`, its four feature-gradient atomics.
+        auto sample = [&](const DTap &ty, const DTap &tx, bool scatter) {
             const uint32_t r0 = static_cast<uint32_t>(ty.lo) * sh;
             const uint32_t r1 = static_cast<uint32_t>(ty.hi) * sh;
-            for (int ix = 0; ix < d.ax.grid; ++ix) {
-                const DTap tx = deform_tap(d.ax, sx, pw, ix, L.W);
-                if (!tx.valid) continue;
-                const uint32_t c0 = static_cast<uint32_t>(tx.lo) * sw;
-                const uint32_t c1 = static_cast<uint32_t>(tx.hi) * sw;
-                const float v11 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r0 + c0));
-                const float v12 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r0 + c1));
-                const float v21 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c0));
-                const float v22 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c1));
-                if (lane_on) {
-                    unsafeAtomicAdd(gbase + ty.lo * gsh + tx.lo * gsw, gq * (ty.wlo * tx.wlo));
-                    unsafeAtomicAdd(gbase + ty.lo * gsh + tx.hi * gsw, gq * (ty.wlo * tx.whi));
-                    unsafeAtomicAdd(gbase + ty.hi * gsh + tx.lo * gsw, gq * (ty.whi * tx.wlo));
-                    unsafeAtomicAdd(gbase + ty.hi * gsh + tx.hi * gsw, gq * (ty.whi * tx.whi));
+            const uint32_t c0 = static_cast<uint32_t>(tx.lo) * sw;
+            const uint32_t c1 = static_cast<uint32_t>(tx.hi) * sw;
+            const float v11 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r0 + c0));
+            const float v12 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r0 + c1));
+            const float v21 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c0));
+            const float v22 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c1));
+            if (scatter && lane_on) {
+                unsafeAtomicAdd(gbase + ty.lo * gsh + tx.lo * gsw, gq * (ty.wlo * tx.wlo));
+                unsafeAtomicAdd(gbase + ty.lo * gsh + tx.hi * gsw, gq * (ty.wlo * tx.whi));
+                unsafeAtomicAdd(gbase + ty.hi * gsh + tx.lo * gsw, gq * (ty.whi * tx.wlo));
+                unsafeAtomicAdd(gbase + ty.hi * gsh + tx.hi * gsw, gq * (ty.whi * tx.whi));
+            }
+            if (tx.slope) px += ty.wlo * (v12 - v11) + ty.whi * (v22 - v21);
+            if (ty.slope) py += tx.wlo * (v21 - v11) + tx.whi * (v22 - v12);
+            pm += ty.wlo * tx.wlo * v11 + ty.wlo * tx.whi * v12 + ty.whi * tx.wlo * v21 +
+                  ty.whi * tx.whi * v22;
+        };
+        if (d.ay.grid <= 2 && d.ax.grid <= 2) {
+            // At most two samples per axis.  Validity and weights are separable, so the
+            // bin's feature gradient is gq * Wy[y] * Wx[x], Wy / Wx summing the tap weights
+            // of the valid samples per pixel row / column.  Sample taps are monotone, so
+            // they fit a window of 4 pixels from the first valid sample's low tap unless
+            // the samples are more than 2 pixels apart (then per-sample atomics).  A window
+            // slot any valid sample taps is `present` even with weight zero, so a
+            // non-finite gradient reaches exactly the pixels of the definition.
+            DTap ty[2], tx[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                ty[i] = deform_tap(d.ay, sy, ph, i, L.H);
+                tx[i] = deform_tap(d.ax, sx, pw, i, L.W);
+                if (i >= d.ay.grid) ty[i].valid = false;
+                if (i >= d.ax.grid) tx[i].valid = false;
+            }
+            float wy[4] = {0.0f, 0.0f, 0.0f, 0.0f}, wx[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            bool hy[4] = {false, false, false, false}, hx[4] = {false, false, false, false};
+            const int by = ty[0].valid ? ty[0].lo : ty[1].lo;
+            const int bx = tx[0].valid ? tx[0].lo : tx[1].lo;
+            bool fits = true;
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int ylo = ty[i].lo - by, yhi = ty[i].hi - by;
+                const int xlo = tx[i].lo - bx, xhi = tx[i].hi - bx;
+                if (ty[i].valid) fits = fits && ylo >= 0 && yhi <= 3;
+                if (tx[i].valid) fits = fits && xlo >= 0 && xhi <= 3;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if (ty[i].valid) {
+                        wy[e] += (ylo == e ? ty[i].wlo : 0.0f) + (yhi == e ? ty[i].whi : 0.0f);
+                        hy[e] = hy[e] || ylo == e || yhi == e;
+                    }
+                    if (tx[i].valid) {
+                        wx[e] += (xlo == e ? tx[i].wlo : 0.0f) + (xhi == e ? tx[i].whi : 0.0f);
+                        hx[e] = hx[e] || xlo == e || xhi == e;
+                    }
                 }
-                if (tx.slope) px += ty.wlo * (v12 - v11) + ty.whi * (v22 - v21);
-                if (ty.slope) py += tx.wlo * (v21 - v11) + tx.whi * (v22 - v12);
-                pm += ty.wlo * tx.wlo * v11 + ty.wlo * tx.whi * v12 + ty.whi * tx.wlo * v21 +
-                      ty.whi * tx.whi * v22;
+            }
+#pragma unroll
+            for (int iy = 0; iy < 2; ++iy)
+#pragma unroll
+                for (int ix = 0; ix < 2; ++ix)
+                    if (ty[iy].valid && tx[ix].valid) sample(ty[iy], tx[ix], !fits);
+            if (fits && lane_on) {
+#pragma unroll
+                for (int ey = 0; ey < 4; ++ey)
+#pragma unroll
+                    for (int ex = 0; ex < 4; ++ex)
+                        if (hy[ey] && hx[ex])
+                            unsafeAtomicAdd(gbase + (by + ey) * gsh + (bx + ex) * gsw,
+                                            gq * (wy[ey] * wx[ex]));
+            }
+        } else {
+            for (int iy = 0; iy < d.ay.grid; ++iy) {
+                const DTap ty = deform_tap(d.ay, sy, ph, iy, L.H);
+                if (!ty.valid) continue;
+                for (int ix = 0; ix < d.ax.grid; ++ix) {
+                    const DTap tx = deform_tap(d.ax, sx, pw, ix, L.W);
+                    if (!tx.valid) continue;
+                    sample(ty, tx, true);
+                }
             }
         }
         // lanes past the last channel have gv = 0 and read zeros, so they add nothing

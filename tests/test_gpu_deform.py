@@ -148,6 +148,19 @@ def test_deform_large_offsets_and_degenerate_inputs():
     run("invalid indices", f, SC, rois, roi_levels=[0, 0, 1, 5])
 
 
+def test_deform_wide_bins():
+    """RoIs spanning most of the finest map: bins wider than 4 pixels put a bin's two
+    samples more than 2 pixels apart along x, so their taps do not fit one 4-pixel
+    window (per-sample atomics); along y they do."""
+    rng = np.random.default_rng(250)
+    f = _pyr(rng, 24)
+    rois = np.array([[0, 0, 0, 150, 90], [1, 10, 5, 140, 95], [0, 30, 20, 100, 80],
+                     [1, 0, 0, 20, 20]], np.float32)
+    run("wide bins", f, SC, rois, roi_levels=[0, 0, 0, 0])
+    run("wide bins S=1", f, SC, rois, roi_levels=[0, 0, 0, 0], S=1)
+    run("wide bins 14x14", f, SC, rois, roi_levels=[0, 0, 0, 0], out_hw=(14, 14))
+
+
 def test_deform_full_box_head_workload():
     """The FPN box head workload (batch 2, P2-P5 with 256 channels, 1024 RoIs, 7x7) with
     offsets ~ N(0, 0.3^2) and modulation ~ U(0, 1)."""
