@@ -18,8 +18,8 @@
 //                     read per box) and writes the kept indices; then every thread ORs the
 //                     kept rows of its group into its later words and adds them to the
 //                     removal words in LDS (lanes over words, so an atomic instruction
-//                     touches 64 different words), the rows having been loaded one block
-//                     ahead so their latency hides behind the resolution.
+//                     touches 64 different words), the rows having been loaded three
+//                     blocks ahead so their latency hides behind the resolution.
 #include "internal.hpp"
 
 namespace rex {
@@ -126,10 +126,11 @@ constexpr int kNmsScanThreads = 1024;
 constexpr int kNmsRowsPerWave = 64 / (kNmsScanThreads / 64);           // 4
 constexpr int kNmsWordsPerLane = (kNmsMaxBoxes / 64 + 63) / 64;        // 2
 constexpr int kNmsPairs = kNmsRowsPerWave * kNmsWordsPerLane;
+constexpr int kNmsAhead = 3;   // blocks of mask rows in flight ahead of the one resolved
 
 __global__ __launch_bounds__(kNmsScanThreads) void nms_scan_kernel(NmsArgs a) {
     __shared__ uint64_t removed[kNmsMaxBoxes / 64];
-    __shared__ uint64_t s_kept;
+    __shared__ uint64_t s_keptm[kNmsMaxBoxes / 64];   // kept boxes of every resolved block
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -138,8 +139,7 @@ __global__ __launch_bounds__(kNmsScanThreads) void nms_scan_kernel(NmsArgs a) {
     for (int w = tid; w < nb; w += kNmsScanThreads) removed[w] = 0;
 
     // Rows of a block as loaded ahead: wave 0 its diagonal words, every thread its share
-    // of the (row, later word) pairs.  Two blocks are in flight: the words of block b + 1
-    // are requested before block b is resolved, so their latency hides behind it.
+    // of the (row, later word) pairs.
     auto load_diag = [&](int b) -> uint64_t {
         const int i = b * 64 + lane;
         return (b < nb && i < a.N) ? a.mask[static_cast<int64_t>(i) * nb + b] : 0;
@@ -158,40 +158,52 @@ __global__ __launch_bounds__(kNmsScanThreads) void nms_scan_kernel(NmsArgs a) {
             }
         }
     };
-    uint64_t pf_cur[kNmsPairs], pf_next[kNmsPairs];
-    uint64_t diag_cur = wave == 0 ? load_diag(0) : 0;
-    load_pairs(0, pf_cur);
+    // Rows of the next kNmsAhead blocks are in flight: slot 0 holds block b, the loads
+    // of block b + kNmsAhead are issued as block b starts.
+    uint64_t pf[kNmsAhead][kNmsPairs];
+    uint64_t dg[kNmsAhead];
+#pragma unroll
+    for (int d = 0; d < kNmsAhead; ++d) {
+        dg[d] = wave == 0 ? load_diag(d) : 0;
+        load_pairs(d, pf[d]);
+    }
     __syncthreads();
     int count = 0;   // the same in every thread
+    int nres = 0;    // blocks resolved
     for (int b = 0; b < nb; ++b) {
-        uint64_t diag_next = 0;
-        if (wave == 0) diag_next = load_diag(b + 1);
-        load_pairs(b + 1, pf_next);
+        const uint64_t dg_new = wave == 0 ? load_diag(b + kNmsAhead) : 0;
+        uint64_t pf_new[kNmsPairs];
+        load_pairs(b + kNmsAhead, pf_new);
         if (wave == 0) {
             // sequential within the block: box t is kept unless a kept box of an earlier
-            // block or an earlier kept box of this block removed it
+            // block or an earlier kept box of this block removed it.  The removal word is
+            // the same in every lane; held in scalar registers, each step is a scalar
+            // branch instead of a masked vector one.
             const int nrow = min(64, a.N - b * 64);
-            uint64_t rem = removed[b];
+            const uint64_t rw = removed[b];
+            // (readfirstlane returns a signed int: both halves go through uint32_t, so
+            // the low half is not sign-extended into the high one)
+            const uint32_t rlo = static_cast<uint32_t>(
+                __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(rw)));
+            const uint32_t rhi = static_cast<uint32_t>(
+                __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(rw >> 32)));
+            uint64_t rem = (static_cast<uint64_t>(rhi) << 32) | rlo;
             uint64_t kept = 0;
             for (int t = 0; t < nrow; ++t) {
                 if (!((rem >> t) & 1)) {
                     kept |= uint64_t(1) << t;
-                    const uint32_t lo =
-                        __builtin_amdgcn_readlane(static_cast<uint32_t>(diag_cur), t);
+                    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(dg[0]), t);
                     const uint32_t hi =
-                        __builtin_amdgcn_readlane(static_cast<uint32_t>(diag_cur >> 32), t);
+                        __builtin_amdgcn_readlane(static_cast<uint32_t>(dg[0] >> 32), t);
                     rem |= (static_cast<uint64_t>(hi) << 32) | lo;
                 }
             }
-            if ((kept >> lane) & 1) {
-                const int rank = count + __popcll(kept & ((uint64_t(1) << lane) - 1));
-                if (rank < limit) a.keep[rank] = a.order[b * 64 + lane];
-            }
-            if (lane == 0) s_kept = kept;
+            if (lane == 0) s_keptm[b] = kept;   // indices are written after the loop
         }
         __syncthreads();
-        const uint64_t kept = s_kept;
+        const uint64_t kept = s_keptm[b];
         count += __popcll(kept);
+        nres = b + 1;
         if (count >= limit) break;   // uniform over the workgroup
         // the kept rows remove boxes of later blocks: each thread ORs its kept rows of a
         // word, then adds them to the word in LDS (the 64 lanes of an atomic instruction
@@ -201,16 +213,36 @@ __global__ __launch_bounds__(kNmsScanThreads) void nms_scan_kernel(NmsArgs a) {
             uint64_t v = 0;
 #pragma unroll
             for (int r = 0; r < kNmsRowsPerWave; ++r)
-                if ((kept >> (wave * kNmsRowsPerWave + r)) & 1) v |= pf_cur[j * kNmsRowsPerWave + r];
+                if ((kept >> (wave * kNmsRowsPerWave + r)) & 1) v |= pf[0][j * kNmsRowsPerWave + r];
             const int w = b + 1 + lane + 64 * j;
             if (v != 0 && w < nb)
                 atomicOr(reinterpret_cast<unsigned long long *>(&removed[w]),
                          static_cast<unsigned long long>(v));
         }
 #pragma unroll
-        for (int m = 0; m < kNmsPairs; ++m) pf_cur[m] = pf_next[m];
-        diag_cur = diag_next;
+        for (int d = 0; d + 1 < kNmsAhead; ++d) {
+            dg[d] = dg[d + 1];
+#pragma unroll
+            for (int m = 0; m < kNmsPairs; ++m) pf[d][m] = pf[d + 1][m];
+        }
+        dg[kNmsAhead - 1] = dg_new;
+#pragma unroll
+        for (int m = 0; m < kNmsPairs; ++m) pf[kNmsAhead - 1][m] = pf_new[m];
         __syncthreads();   // removal words final before block b + 1 is resolved
+    }
+    // Kept indices in rank order, off the sequential path: wave w writes blocks w,
+    // w + 16, ...; a block's first rank is the kept count of the blocks before it.
+    __syncthreads();
+    for (int b = wave; b < nres; b += kNmsScanThreads / 64) {
+        int before = 0;
+        for (int c = lane; c < b; c += 64) before += __popcll(s_keptm[c]);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) before += __shfl_xor(before, o, 64);
+        const uint64_t kept = s_keptm[b];
+        if ((kept >> lane) & 1) {
+            const int rank = before + __popcll(kept & ((uint64_t(1) << lane) - 1));
+            if (rank < limit) a.keep[rank] = a.order[b * 64 + lane];
+        }
     }
     const int n = min(count, limit);
     for (int r = n + tid; r < limit; r += kNmsScanThreads) a.keep[r] = -1;
