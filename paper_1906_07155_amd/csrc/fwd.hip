@@ -304,8 +304,9 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     }
     __syncthreads();
 
-    const int ny = s_ny[wave];
-    const int nch = (s_nx + CX - 1) / CX;
+    // wave-uniform counts in scalar registers: the pipeline below branches on them
+    const int ny = uniform_i(s_ny[wave]);
+    const int nch = uniform_i((s_nx + CX - 1) / CX);
     const uint64_t xlo = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[0] >> 32))) << 32) |
                          static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[0])));
     const uint64_t xhi = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[1] >> 32))) << 32) |
