@@ -517,7 +517,10 @@ static hipError_t launch_fwd_typed(FwdArgs a, bool fast, hipStream_t stream) {
         if (a.PH == 7)
             fwd_cl_kernel<T, TO, 7, 7, 2, kFwdCX, 64><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
         else
-            fwd_cl_kernel<T, TO, 14, 14, 2, 8, 16><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
+            // 4 columns per unit keep the 14x14 kernel at 124 registers, four workgroups
+            // per CU (8 columns: 164 registers, three; mask head batch 2: 44 vs 51 us);
+            // the 7x7 kernel is fastest with 8 (4: 60 registers, 336 vs 321 us batch 16)
+            fwd_cl_kernel<T, TO, 14, 14, 2, 4, 16><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
     } else {
         const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * a.PH * a.PW;
         const int64_t blocks = std::min<int64_t>((total + 255) / 256, 16384);
