@@ -313,177 +313,177 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
                          static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[1])));
     // The geometry above serves every slice of the workgroup.
     for (int slice = slice0; slice < slice1; ++slice) {
-    if (slice > slice0) __syncthreads();   // the previous slice's output tile is stored
-    const int c = slice * 64 + lane;
-    const bool lane_on = active && c < a.lv.C;
-    // One buffer resource per image of the level; a lane with no channel reads out
-    // of range (zeros) instead of branching.
-    const char *img = static_cast<const char *>(L.data) +
-                      (active ? static_cast<int64_t>(b) * L.sn * int64_t(sizeof(T)) : 0);
-    const __amdgpu_buffer_rsrc_t res = make_rsrc(img, L.img_bytes);
-    const uint32_t vbase = lane_on ? static_cast<uint32_t>(c) * uint32_t(sizeof(T)) : kBufOOB;
+        if (slice > slice0) __syncthreads();   // the previous slice's output tile is stored
+        const int c = slice * 64 + lane;
+        const bool lane_on = active && c < a.lv.C;
+        // One buffer resource per image of the level; a lane with no channel reads out
+        // of range (zeros) instead of branching.
+        const char *img = static_cast<const char *>(L.data) +
+                          (active ? static_cast<int64_t>(b) * L.sn * int64_t(sizeof(T)) : 0);
+        const __amdgpu_buffer_rsrc_t res = make_rsrc(img, L.img_bytes);
+        const uint32_t vbase = lane_on ? static_cast<uint32_t>(c) * uint32_t(sizeof(T)) : kBufOOB;
 
-    // a4: gather.  Chunk-major over the footprint: for each chunk of CX distinct
-    // columns, every distinct row of the wave is loaded (work unit = (chunk, row))
-    // and reduced over rows first, H[x][p] = sum_y Wy[p][y] F[y][x]; at the end of
-    // the chunk the columns are reduced into the bins, acc[p][q] += Wx[q][x] H[x][p].
-    // Columns past the footprint read zeros (out-of-range offsets, zero weights).
-    float acc[RPW][PW];
-#pragma unroll
-    for (int p = 0; p < RPW; ++p)
-#pragma unroll
-        for (int q = 0; q < PW; ++q) acc[p][q] = 0.0f;
-    float H[CX][RPW];
-#pragma unroll
-    for (int x = 0; x < CX; ++x)
-#pragma unroll
-        for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
+        // a4: gather.  Chunk-major over the footprint: for each chunk of CX distinct
+        // columns, every distinct row of the wave is loaded (work unit = (chunk, row))
+        // and reduced over rows first, H[x][p] = sum_y Wy[p][y] F[y][x]; at the end of
+        // the chunk the columns are reduced into the bins, acc[p][q] += Wx[q][x] H[x][p].
+        // Columns past the footprint read zeros (out-of-range offsets, zero weights).
+        float acc[RPW][PW];
+    #pragma unroll
+        for (int p = 0; p < RPW; ++p)
+    #pragma unroll
+            for (int q = 0; q < PW; ++q) acc[p][q] = 0.0f;
+        float H[CX][RPW];
+    #pragma unroll
+        for (int x = 0; x < CX; ++x)
+    #pragma unroll
+            for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
 
-    auto issue = [&](int ch, int yi, uint32_t (&v)[CX]) {
-        const uint32_t rowb = vbase + s_yoff[wave][yi];
-        const uint32_t *xo = s_xoff + ch * CX;
-#pragma unroll
-        for (int x = 0; x < CX; ++x) v[x] = buf_load_raw<T>(res, rowb + xo[x]);
-    };
-    auto consume = [&](int ch, int yi, const uint32_t (&v)[CX]) {
-        const float *wy = s_wy[wave][yi];
-#pragma unroll
-        for (int x = 0; x < CX; ++x) {
-            const float f = raw_to_f32<T>(v[x]);
-#pragma unroll
-            for (int p = 0; p < RPW; ++p) H[x][p] = fmaf(wy[p], f, H[x][p]);
-        }
-        if (yi == ny - 1) {
-#pragma unroll
+        auto issue = [&](int ch, int yi, uint32_t (&v)[CX]) {
+            const uint32_t rowb = vbase + s_yoff[wave][yi];
+            const uint32_t *xo = s_xoff + ch * CX;
+    #pragma unroll
+            for (int x = 0; x < CX; ++x) v[x] = buf_load_raw<T>(res, rowb + xo[x]);
+        };
+        auto consume = [&](int ch, int yi, const uint32_t (&v)[CX]) {
+            const float *wy = s_wy[wave][yi];
+    #pragma unroll
             for (int x = 0; x < CX; ++x) {
-                const int col = ch * CX + x;
-                const float *wx = s_wx[col];
-                // each half of the bins only where the column reaches it (the other
-                // weights are zero); on the 7-wide grid the test costs more than the
-                // few products it saves
-                if (!kHalves || ((xlo >> col) & 1)) {
-#pragma unroll
-                    for (int q = 0; q < QH; ++q)
-#pragma unroll
-                        for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+                const float f = raw_to_f32<T>(v[x]);
+    #pragma unroll
+                for (int p = 0; p < RPW; ++p) H[x][p] = fmaf(wy[p], f, H[x][p]);
+            }
+            if (yi == ny - 1) {
+    #pragma unroll
+                for (int x = 0; x < CX; ++x) {
+                    const int col = ch * CX + x;
+                    const float *wx = s_wx[col];
+                    // each half of the bins only where the column reaches it (the other
+                    // weights are zero); on the 7-wide grid the test costs more than the
+                    // few products it saves
+                    if (!kHalves || ((xlo >> col) & 1)) {
+    #pragma unroll
+                        for (int q = 0; q < QH; ++q)
+    #pragma unroll
+                            for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+                    }
+                    if (!kHalves || ((xhi >> col) & 1)) {
+    #pragma unroll
+                        for (int q = QH; q < PW; ++q)
+    #pragma unroll
+                            for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+                    }
+    #pragma unroll
+                    for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
+                    // one column's weights live at a time
+                    __builtin_amdgcn_sched_barrier(0);
                 }
-                if (!kHalves || ((xhi >> col) & 1)) {
-#pragma unroll
-                    for (int q = QH; q < PW; ++q)
-#pragma unroll
-                        for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+            }
+        };
+
+        // Pipeline over the units in (chunk, row) order: the loads of units u+1 ..
+        // u+kFwdDepth are in flight while unit u is reduced.  The loop is unrolled by
+        // the ring size so every buffer index is a constant.
+        constexpr int D = kFwdDepth;
+        constexpr int NBUF = D + 1;
+        uint32_t v[NBUF][CX];
+        const int units = ny * nch;
+        int ic = 0, iy = 0;      // next unit to issue
+        int cc = 0, cy = 0;      // next unit to consume
+        auto step = [&](int &ch, int &y) {
+            if (++y == ny) {
+                y = 0;
+                ++ch;
+            }
+        };
+    #pragma unroll
+        for (int d = 0; d < D; ++d) {
+            if (d < units) {
+                issue(ic, iy, v[d]);
+                step(ic, iy);
+            }
+        }
+        for (int u0 = 0; u0 < units; u0 += NBUF) {
+    #pragma unroll
+            for (int j = 0; j < NBUF; ++j) {
+                if (u0 + j >= units) break;
+                if (u0 + j + D < units) {
+                    issue(ic, iy, v[(j + D) % NBUF]);
+                    step(ic, iy);
                 }
-#pragma unroll
-                for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
-                // one column's weights live at a time
+                __builtin_amdgcn_sched_barrier(0);
+                consume(cc, cy, v[j]);
+                step(cc, cy);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
-    };
 
-    // Pipeline over the units in (chunk, row) order: the loads of units u+1 ..
-    // u+kFwdDepth are in flight while unit u is reduced.  The loop is unrolled by
-    // the ring size so every buffer index is a constant.
-    constexpr int D = kFwdDepth;
-    constexpr int NBUF = D + 1;
-    uint32_t v[NBUF][CX];
-    const int units = ny * nch;
-    int ic = 0, iy = 0;      // next unit to issue
-    int cc = 0, cy = 0;      // next unit to consume
-    auto step = [&](int &ch, int &y) {
-        if (++y == ny) {
-            y = 0;
-            ++ch;
-        }
-    };
-#pragma unroll
-    for (int d = 0; d < D; ++d) {
-        if (d < units) {
-            issue(ic, iy, v[d]);
-            step(ic, iy);
-        }
-    }
-    for (int u0 = 0; u0 < units; u0 += NBUF) {
-#pragma unroll
-        for (int j = 0; j < NBUF; ++j) {
-            if (u0 + j >= units) break;
-            if (u0 + j + D < units) {
-                issue(ic, iy, v[(j + D) % NBUF]);
-                step(ic, iy);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            consume(cc, cy, v[j]);
-            step(cc, cy);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    }
+        // Every value the wave loaded reaches every one of its outputs through the
+        // dense products above, so a non-finite feature anywhere in the footprint shows
+        // up as a non-finite output.
+        uint32_t bad = 0;
+    #pragma unroll
+        for (int p = 0; p < RPW; ++p)
+    #pragma unroll
+            for (int q = 0; q < PW; ++q) bad |= __builtin_isfinite(acc[p][q]) ? 0u : 1u;
 
-    // Every value the wave loaded reaches every one of its outputs through the
-    // dense products above, so a non-finite feature anywhere in the footprint shows
-    // up as a non-finite output.
-    uint32_t bad = 0;
-#pragma unroll
-    for (int p = 0; p < RPW; ++p)
-#pragma unroll
-        for (int q = 0; q < PW; ++q) bad |= __builtin_isfinite(acc[p][q]) ? 0u : 1u;
-
-    // Then a zero weight times an infinity may have reached bins whose samples never
-    // touch that pixel, so this wave's bins are recomputed sample by sample, every
-    // product taken only where the definition takes it.
-    if (__builtin_amdgcn_ballot_w64(bad != 0) != 0) {
-#pragma unroll
-        for (int p = 0; p < RPW; ++p) {
-            if (p0 + p >= p1) continue;
-#pragma unroll 1
-            for (int q = 0; q < PW; ++q) {
-                float sum = 0.0f;
-                for (int iy2 = 0; iy2 < S; ++iy2) {
-                    const SampleTap ty = srow[(p0 + p) * S + iy2];
-                    if (ty.lo < 0) continue;
-                    const uint32_t r0 = vbase + static_cast<uint32_t>(ty.lo) * sh_b;
-                    const uint32_t r1 = vbase + static_cast<uint32_t>(ty.hi) * sh_b;
-                    for (int ix = 0; ix < S; ++ix) {
-                        const SampleTap tx = scol[q * S + ix];
-                        if (tx.lo < 0) continue;
-                        const uint32_t cl = static_cast<uint32_t>(tx.lo) * sw_b;
-                        const uint32_t chh = static_cast<uint32_t>(tx.hi) * sw_b;
-                        const float v00 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + cl));
-                        const float v01 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + chh));
-                        const float v10 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + cl));
-                        const float v11 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + chh));
-                        const float xl = fmaf(tx.w_hi, v01, tx.w_lo * v00);
-                        const float xh = fmaf(tx.w_hi, v11, tx.w_lo * v10);
-                        sum += fmaf(ty.w_hi, xh, ty.w_lo * xl);
-                    }
-                }
-                sum = sum / static_cast<float>(S * S);
-#pragma unroll
-                for (int qq = 0; qq < PW; ++qq) acc[p][qq] = (qq == q) ? sum : acc[p][qq];
-            }
-        }
-    }
-
-    // a5: the slice's [64][PH][PW] block is contiguous in the output at RoI k;
-    // transposed through LDS in rounds of CHK channels.
-    const int nchan = min(64, a.lv.C - slice * 64);
-    const gptr<TO> out_blk = as_global_mut<TO>(a.out) +
-                             (static_cast<int64_t>(k) * a.lv.C + static_cast<int64_t>(slice) * 64) * NB;
-#pragma unroll
-    for (int c0 = 0; c0 < 64; c0 += CHK) {
-        if (lane >= c0 && lane < c0 + CHK) {
-#pragma unroll
+        // Then a zero weight times an infinity may have reached bins whose samples never
+        // touch that pixel, so this wave's bins are recomputed sample by sample, every
+        // product taken only where the definition takes it.
+        if (__builtin_amdgcn_ballot_w64(bad != 0) != 0) {
+    #pragma unroll
             for (int p = 0; p < RPW; ++p) {
                 if (p0 + p >= p1) continue;
-#pragma unroll
-                for (int q = 0; q < PW; ++q) stile[(lane - c0) * NB + (p0 + p) * PW + q] = acc[p][q];
+    #pragma unroll 1
+                for (int q = 0; q < PW; ++q) {
+                    float sum = 0.0f;
+                    for (int iy2 = 0; iy2 < S; ++iy2) {
+                        const SampleTap ty = srow[(p0 + p) * S + iy2];
+                        if (ty.lo < 0) continue;
+                        const uint32_t r0 = vbase + static_cast<uint32_t>(ty.lo) * sh_b;
+                        const uint32_t r1 = vbase + static_cast<uint32_t>(ty.hi) * sh_b;
+                        for (int ix = 0; ix < S; ++ix) {
+                            const SampleTap tx = scol[q * S + ix];
+                            if (tx.lo < 0) continue;
+                            const uint32_t cl = static_cast<uint32_t>(tx.lo) * sw_b;
+                            const uint32_t chh = static_cast<uint32_t>(tx.hi) * sw_b;
+                            const float v00 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + cl));
+                            const float v01 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + chh));
+                            const float v10 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + cl));
+                            const float v11 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + chh));
+                            const float xl = fmaf(tx.w_hi, v01, tx.w_lo * v00);
+                            const float xh = fmaf(tx.w_hi, v11, tx.w_lo * v10);
+                            sum += fmaf(ty.w_hi, xh, ty.w_lo * xl);
+                        }
+                    }
+                    sum = sum / static_cast<float>(S * S);
+    #pragma unroll
+                    for (int qq = 0; qq < PW; ++qq) acc[p][qq] = (qq == q) ? sum : acc[p][qq];
+                }
             }
         }
-        __syncthreads();
-        const int ne = max(0, min(CHK, nchan - c0)) * NB;
-        if (kvalid)
-            for (int e = t; e < ne; e += 256) store_f32(out_blk + c0 * NB + e, stile[e]);
-        if (c0 + CHK < 64) __syncthreads();
-    }
+
+        // a5: the slice's [64][PH][PW] block is contiguous in the output at RoI k;
+        // transposed through LDS in rounds of CHK channels.
+        const int nchan = min(64, a.lv.C - slice * 64);
+        const gptr<TO> out_blk = as_global_mut<TO>(a.out) +
+                                 (static_cast<int64_t>(k) * a.lv.C + static_cast<int64_t>(slice) * 64) * NB;
+    #pragma unroll
+        for (int c0 = 0; c0 < 64; c0 += CHK) {
+            if (lane >= c0 && lane < c0 + CHK) {
+    #pragma unroll
+                for (int p = 0; p < RPW; ++p) {
+                    if (p0 + p >= p1) continue;
+    #pragma unroll
+                    for (int q = 0; q < PW; ++q) stile[(lane - c0) * NB + (p0 + p) * PW + q] = acc[p][q];
+                }
+            }
+            __syncthreads();
+            const int ne = max(0, min(CHK, nchan - c0)) * NB;
+            if (kvalid)
+                for (int e = t; e < ne; e += 256) store_f32(out_blk + c0 * NB + e, stile[e]);
+            if (c0 + CHK < 64) __syncthreads();
+        }
     }   // slices
 }
 
