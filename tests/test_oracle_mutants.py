@@ -7,7 +7,6 @@ one pin in tests/oracle_pins.py to fail.  All planted mistakes keep every memory
 access in bounds (indices stay clamped), so the broken copies are safe to run
 in-process.  CPU only.
 """
-import os
 
 import pytest
 
