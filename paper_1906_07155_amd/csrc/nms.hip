@@ -70,15 +70,15 @@ __global__ __launch_bounds__(kNmsSortThreads) void nms_sort_kernel(NmsArgs a) {
     __syncthreads();
     for (int k = 2; k <= P; k <<= 1) {
         for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = threadIdx.x; i < P; i += kNmsSortThreads) {
-                const int p = i ^ j;
-                if (p > i) {
-                    const uint64_t x = items[i], y = items[p];
-                    const bool up = (i & k) == 0;
-                    if ((x > y) == up) {
-                        items[i] = y;
-                        items[p] = x;
-                    }
+            // the P / 2 compare-exchange pairs (i, i + j), i with bit j clear
+            for (int q = threadIdx.x; q < P / 2; q += kNmsSortThreads) {
+                const int i = ((q & ~(j - 1)) << 1) | (q & (j - 1));
+                const int p = i + j;
+                const uint64_t x = items[i], y = items[p];
+                const bool up = (i & k) == 0;
+                if ((x > y) == up) {
+                    items[i] = y;
+                    items[p] = x;
                 }
             }
             __syncthreads();
