@@ -81,7 +81,16 @@ __global__ __launch_bounds__(kNmsSortThreads) void nms_sort_kernel(NmsArgs a) {
                     items[p] = x;
                 }
             }
-            __syncthreads();
+            // With j <= 64 the 64 pairs of a wave (64 consecutive q) cover one aligned
+            // block of 128 items, the same block for every such j: between two such
+            // stages each wave only reads what it wrote, so a wave-level sync suffices.
+            // Any stage with partners 128 or more apart, and the end of the sort (the
+            // gather below reads every item), needs the workgroup barrier.
+            const int jn = j > 1 ? j >> 1 : k;   // next stage's distance
+            if (j <= 64 && jn <= 64 && !(k == P && j == 1))
+                wave_sync();
+            else
+                __syncthreads();
         }
     }
     for (int r = threadIdx.x; r < N; r += kNmsSortThreads) {
