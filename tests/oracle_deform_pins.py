@@ -21,6 +21,8 @@ the oracle's deformable code.
                    2 pixels (math mode)
   parity vs math   the binary32-geometry gradients follow the finite-difference pinned
                    math-mode ones within the rounding scale, clamped samples included
+  binary32 order   hand-derived binary32 sample coordinates on a ramp map fix where the
+                   shift enters the rounded sum (tests/golden/deform_binary32_cases.json)
 """
 from __future__ import annotations
 
@@ -299,8 +301,33 @@ def pin_parity_gradients_follow_math(lib, mode):
     assert np.all(np.abs(mp - mm) <= 1e-4 * (sm + 1e-12)), "parity mask gradient"
 
 
+def pin_binary32_shift_order(lib, mode):
+    """Hand-derived binary32 sample coordinates (tests/golden/deform_binary32_cases.json)
+    that fix where the bin shift enters the rounded sum: after the bin start is rounded
+    and before the within-bin offset.  A ramp map returns the sample coordinate, so one
+    ulp of difference shows; the comparison is exact."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                        "deform_binary32_cases.json")
+    with open(path) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
+        shape = tuple(case["shape"])
+        feat = np.broadcast_to(np.arange(shape[3], dtype=np.float64), shape).copy()
+        ph, pw = case["out"]
+        out = oracle.deform_roi_pool_fwd([feat], [case["scale"]],
+                                         np.array(case["rois"], np.float32), None, ph, pw,
+                                         case["sampling_ratio"], case["aligned"],
+                                         np.array(case["offset"], np.float32),
+                                         gamma=case["gamma"], mode=mode, lib=lib)
+        exp = np.array(case["expected_parity" if mode == "parity" else "expected_math"])
+        rtol = 0.0 if mode == "parity" else 1e-12
+        assert np.allclose(out, exp, rtol=rtol, atol=0.0), (case["name"], mode, out.ravel())
+
+
 ALL_DEFORM_PINS = [pin_zero_offsets_are_roialign, pin_constant_map, pin_mask_linearity,
-                   pin_adjoint]
+                   pin_adjoint, pin_binary32_shift_order]
 AFFINE_PINS = [pin_affine_closed_form]
 MATH_ONLY_DEFORM_PINS = [pin_finite_differences, pin_brute_force_tent, pin_integer_shift,
                          pin_parity_gradients_follow_math]

@@ -6,6 +6,8 @@ operator and by mathematics:
 
   hand cases      values derived by hand (tests/golden/), incl. the -1/size cut,
                   the divisor that counts invalid samples, clamping, adaptive grid
+  binary32 order  hand-derived binary32 sample coordinates on ramp maps: the order
+                  and association of every rounding step of the geometry, the grid cap
   level cases     hand-derived FPN level thresholds, bit-exact (golden)
   constant        a constant map returns the constant (weights sum to one)
   affine          on an affine map a bin average is the affine value at the bin centre
@@ -51,6 +53,8 @@ def _case_levels(case):
         shape = tuple(lv["shape"])
         if "fill" in lv:
             f = np.full(shape, lv["fill"], dtype=np.float64)
+        elif lv.get("ramp_x"):
+            f = np.broadcast_to(np.arange(shape[3], dtype=np.float64), shape).copy()
         else:
             f = np.array(lv["values"], dtype=np.float64).reshape(shape)
         feats.append(f)
@@ -69,6 +73,31 @@ def pin_hand_cases(lib, mode):
         assert out.shape == exp.shape, case["name"]
         tol = _tol(mode, 1e-12, 2e-6)
         assert np.allclose(out, exp, rtol=tol, atol=tol), (case["name"], out, exp)
+
+
+def load_binary32_cases():
+    with open(os.path.join(GOLDEN, "roi_align_binary32_cases.json")) as f:
+        return json.load(f)["cases"]
+
+
+def pin_binary32_order(lib, mode):
+    """Hand-derived sample coordinates that fix the binary32 order of the geometry (which
+    association of the bin start and the within-bin offset, where the division by the
+    grid comes, IEEE division for the bin size) and the adaptive-grid cap.  A ramp map
+    returns the sample coordinate itself, so one ulp of difference in any rounding step
+    shows; the comparison is therefore exact up to double rounding of the final mean."""
+    for case in load_binary32_cases():
+        feats, scales = _case_levels(case)
+        ph, pw = case["out"]
+        out = oracle.roi_align_fwd(feats, scales, np.array(case["rois"], np.float32),
+                                   np.array(case["roi_levels"], np.int32), ph, pw,
+                                   case["sampling_ratio"], case["aligned"], mode, lib=lib)
+        exp = np.array(case["expected_parity" if mode == "parity" else "expected_math"],
+                       dtype=np.float64)
+        assert out.shape == exp.shape, case["name"]
+        rtol = 1e-14 if mode == "parity" else 1e-12
+        assert np.allclose(out, exp, rtol=rtol, atol=0.0), (case["name"], mode, out.ravel(),
+                                                            exp.ravel())
 
 
 def load_level_cases():
@@ -404,7 +433,7 @@ def pin_guards(lib, mode):
     assert not grads[0].any()
 
 
-ALL_PINS = [pin_hand_cases, pin_level_cases, pin_level_log2_agrees, pin_level_plus1_is_shifted_box,
+ALL_PINS = [pin_hand_cases, pin_binary32_order, pin_level_cases, pin_level_log2_agrees, pin_level_plus1_is_shifted_box,
             pin_constant, pin_affine,
             pin_adjoint, pin_tent, pin_dense_matrix, pin_textbook, pin_mass, pin_guards]
 MATH_ONLY_PINS = [pin_mirror]

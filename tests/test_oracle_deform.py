@@ -67,6 +67,16 @@ MUTANTS = [
      "        d.slope = 1;\n        v = fmaxf(v, 0.0f);"),
     ("shift added after the within-bin term is rounded away, binary32",
      "float v = b2 + e;", "float v = b + e;"),
+    ("shift added to the within-bin offset first, binary32",
+     "float b2 = b + shift_f;\n        float half = (float)i + 0.5f;\n"
+     "        float e0 = half * g->bin_f;\n        float e = e0 / (float)g->grid;\n"
+     "        float v = b2 + e;",
+     "float b2 = b;\n        float half = (float)i + 0.5f;\n"
+     "        float e0 = half * g->bin_f;\n        float e = e0 / (float)g->grid;\n"
+     "        float v = b2 + (shift_f + e);"),
+    ("shift added to the bin position first, binary32",
+     "float b = g->start_f + pos;\n        float b2 = b + shift_f;",
+     "float b = g->start_f + (pos + shift_f);\n        float b2 = b;"),
 ]
 
 

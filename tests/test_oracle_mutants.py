@@ -70,6 +70,22 @@ MUTANTS = [
      "double g = ceil(bin);", "double g = floor(bin);"),
     ("scale applied after the shift",
      "float s = c1 * scale;\n        s = s - off;", "float s = c1 - off;\n        s = s * scale;"),
+    ("bin start and within-bin offset summed first, binary32",
+     "float b = g->start_f + a;\n        float c = (float)i + 0.5f;\n"
+     "        float d = c * g->bin_f;\n        float e = d / (float)g->grid;\n"
+     "        float v = b + e;",
+     "float b = a;\n        float c = (float)i + 0.5f;\n"
+     "        float d = c * g->bin_f;\n        float e = d / (float)g->grid;\n"
+     "        float v = g->start_f + (b + e);"),
+    ("within-bin offset as (i + 1/2) * (bin / grid), binary32",
+     "float d = c * g->bin_f;\n        float e = d / (float)g->grid;",
+     "float d = g->bin_f / (float)g->grid;\n        float e = c * d;"),
+    ("bin size by the reciprocal of the bin count, binary32",
+     "float bin = len / (float)P;\n        g.len_f = len;",
+     "float bin = len * (1.0f / (float)P);\n        g.len_f = len;"),
+    ("adaptive grid cap raised", "#define ADAPTIVE_GRID_CAP 64", "#define ADAPTIVE_GRID_CAP 128"),
+    ("adaptive grid uncapped",
+     "    if (g > (double)ADAPTIVE_GRID_CAP)\n        g = (double)ADAPTIVE_GRID_CAP;\n", ""),
 ]
 
 
