@@ -491,7 +491,6 @@ def main_heads(args):
     pyramid).  The same step with two roi_align_bwd calls is timed too."""
     import torch
 
-    import oracle
     import paper_1906_07155_amd as rex
     from paper_1906_07155_amd import accounting, workloads
 
@@ -564,7 +563,7 @@ def main_heads(args):
     alt = timed(False, max(1, args.alt_steps)) if args.alt_steps > 0 else None
     Ktot = sum(h["rois_np"].shape[0] for h in heads)
     s_g = 2 if wb.grad_dtype == "bf16" else 4
-    by = accounting.count(heads[0]["rois_np"], oracle.level_map(heads[0]["rois_np"], 4, 56.0),
+    by = accounting.count(heads[0]["rois_np"], heads[0]["levels"].cpu().numpy(),
                           wb.level_hw, wb.scales, wb.n_images, wb.channels, (7, 7), 2, True,
                           2 if bf16 else 4, 2 if wb.out_dtype == "bf16" else 4, s_g)
     # the fused backward must read both upstream gradients and write every gradient once

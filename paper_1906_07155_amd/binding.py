@@ -140,9 +140,60 @@ def _dtype_code(t) -> int:
     raise TypeError("only float32 and bfloat16 tensors are supported, got %s" % t.dtype)
 
 
-def _need_cuda(t, name: str):
+def _need_cuda(t, name: str, like=None):
     if not t.is_cuda:
         raise ValueError("%s must be a GPU tensor" % name)
+    if like is not None and t.device != like.device:
+        raise ValueError("%s must be on %s (got %s)" % (name, like.device, t.device))
+
+
+def _on_device(rois, **tensors):
+    """After the shape checks: the RoIs and every given tensor (None skipped) are GPU
+    tensors on one device."""
+    _need_cuda(rois, "rois")
+    for name, t in tensors.items():
+        if t is not None:
+            _need_cuda(t, name, rois)
+
+
+def _roi_levels(roi_levels, rois, num_levels: int):
+    """Device pointer of the per-RoI level array: a contiguous int32 [K] tensor (the
+    library reads K int32 values), or None with a single level."""
+    torch = _torch()
+    if roi_levels is None:
+        if num_levels > 1:
+            raise ValueError("roi_levels is required with more than one level")
+        return None
+    K = rois.shape[0]
+    if (roi_levels.dtype != torch.int32 or roi_levels.dim() != 1 or roi_levels.numel() != K
+            or not roi_levels.is_contiguous()):
+        raise ValueError("roi_levels must be a contiguous int32 tensor of shape [%d] (got %s %s)"
+                         % (K, roi_levels.dtype, tuple(roi_levels.shape)))
+    return roi_levels.data_ptr()
+
+
+def _block(t, shape, name: str, rois, dtypes=None):
+    """A dense [K, C, out_h, out_w] tensor (out, grad_out, argmax) of the expected shape,
+    checked before its pointer goes to the library."""
+    torch = _torch()
+    if tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous tensor of shape %s (got %s)"
+                         % (name, tuple(shape), tuple(t.shape)))
+    if dtypes is None:
+        _dtype_code(t)
+    elif t.dtype not in dtypes:
+        raise ValueError("%s must be %s (got %s)" % (name, " or ".join(map(str, dtypes)), t.dtype))
+    return t
+
+
+def _workspace(workspace, rois):
+    """(pointer, bytes) of a workspace tensor: contiguous 1-D uint8."""
+    torch = _torch()
+    if workspace is None:
+        return None, 0
+    if workspace.dtype != torch.uint8 or workspace.dim() != 1 or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous 1-D uint8 tensor")
+    return workspace.data_ptr(), workspace.numel()
 
 
 def stream_handle(stream=None) -> int:
@@ -151,15 +202,19 @@ def stream_handle(stream=None) -> int:
     return int(s.cuda_stream)
 
 
-def level_array(tensors: Sequence, scales: Sequence[float]):
-    """re_level_t[] describing logically-NCHW tensors (any strides)."""
+def level_array(tensors: Sequence, scales: Sequence[float], like=None):
+    """re_level_t[] describing logically-NCHW tensors (any strides), all on the device of
+    `like` when it is given."""
     if len(tensors) != len(scales):
         raise ValueError("one spatial scale per level")
+    if not 1 <= len(tensors) <= MAX_LEVELS:
+        raise ValueError("between 1 and %d levels" % MAX_LEVELS)
     arr = (ReLevel * max(1, len(tensors)))()
     for i, (t, s) in enumerate(zip(tensors, scales)):
         if t.dim() != 4:
             raise ValueError("feature level %d must be 4-D [N, C, H, W]" % i)
-        _need_cuda(t, "feature level %d" % i)
+        _dtype_code(t)
+        _need_cuda(t, "feature level %d" % i, like if like is not None else tensors[0])
         n, c, h, w = t.shape
         sn, sc, sh, sw = t.stride()
         arr[i] = ReLevel(t.data_ptr(), _dtype_code(t), 0, n, c, h, w, sn, sc, sh, sw, float(s),
@@ -171,10 +226,15 @@ def _rois(rois):
     torch = _torch()
     if rois.dim() != 2 or rois.shape[1] != 5 or rois.dtype != torch.float32:
         raise ValueError("rois must be a float32 [K, 5] tensor")
-    _need_cuda(rois, "rois")
     if not rois.is_contiguous():
         raise ValueError("rois must be contiguous")
-    return rois
+    return rois   # its device is checked after the shapes, before the first pointer is taken
+
+
+def _channels(features: Sequence) -> int:
+    if not features or features[0].dim() != 4:
+        raise ValueError("features must be a non-empty list of 4-D [N, C, H, W] tensors")
+    return int(features[0].shape[1])
 
 
 # ---------------------------------------------------------------------------
@@ -193,11 +253,13 @@ def fpn_level_map(rois, num_levels: int, finest_scale: float = 56.0, out=None, s
     K = rois.shape[0]
     if out is None:
         out = torch.empty(K, dtype=torch.int32, device=rois.device)
+    out_ptr = _roi_levels(out, rois, 2)
+    _on_device(rois, levels_out=out)
     if box_pixels:
         check(lib().fpn_level_map_ex(rois.data_ptr(), K, num_levels, finest_scale, BOX_PIXELS,
-                                     out.data_ptr(), stream_handle(stream)), "fpn_level_map_ex")
+                                     out_ptr, stream_handle(stream)), "fpn_level_map_ex")
     else:
-        check(lib().fpn_level_map(rois.data_ptr(), K, num_levels, finest_scale, out.data_ptr(),
+        check(lib().fpn_level_map(rois.data_ptr(), K, num_levels, finest_scale, out_ptr,
                                   stream_handle(stream)), "fpn_level_map")
     return out
 
@@ -222,36 +284,40 @@ def plan(features: Sequence, scales: Sequence[float], rois, finest_scale: float 
     K, L = rois.shape[0], len(features)
     if levels_out is None:
         levels_out = torch.empty(K, dtype=torch.int32, device=rois.device)
+    lv = _roi_levels(levels_out, rois, 2)
+    if workspace is not None:
+        _workspace(workspace, rois)
+    _on_device(rois, levels_out=levels_out, workspace=workspace)
     nbytes = workspace_size(features, scales, K)
     if workspace is None:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=rois.device)
-    arr = level_array(features, scales)
+    ws, wsb = _workspace(workspace, rois)
+    arr = level_array(features, scales, rois)
     if box_pixels:
         check(lib().roi_extract_plan_ex(arr, L, rois.data_ptr(), K, finest_scale, BOX_PIXELS,
-                                        levels_out.data_ptr(), workspace.data_ptr(),
-                                        workspace.numel(), stream_handle(stream)),
+                                        lv, ws, wsb, stream_handle(stream)),
               "roi_extract_plan_ex")
     else:
-        check(lib().roi_extract_plan(arr, L, rois.data_ptr(), K, finest_scale,
-                                     levels_out.data_ptr(), workspace.data_ptr(),
-                                     workspace.numel(), stream_handle(stream)), "roi_extract_plan")
+        check(lib().roi_extract_plan(arr, L, rois.data_ptr(), K, finest_scale, lv, ws, wsb,
+                                     stream_handle(stream)), "roi_extract_plan")
     return levels_out, workspace
 
 
 def plan_offsets(workspace, num_rois: int, num_levels: int, stream=None):
     torch = _torch()
+    ws, wsb = _workspace(workspace, workspace)
     out = torch.empty(num_levels + 1, dtype=torch.int32, device=workspace.device)
-    check(lib().roi_extract_plan_offsets(workspace.data_ptr(), workspace.numel(), num_rois,
-                                         num_levels, out.data_ptr(), stream_handle(stream)),
-          "roi_extract_plan_offsets")
+    check(lib().roi_extract_plan_offsets(ws, wsb, num_rois, num_levels, out.data_ptr(),
+                                         stream_handle(stream)), "roi_extract_plan_offsets")
     return out
 
 
 def plan_perm(workspace, num_rois: int):
     """The plan's permutation (a view into the workspace)."""
+    ws, wsb = _workspace(workspace, workspace)
     ptr = ctypes.c_void_p(0)
-    check(lib().roi_extract_plan_perm(workspace.data_ptr(), workspace.numel(), num_rois,
-                                      ctypes.byref(ptr)), "roi_extract_plan_perm")
+    check(lib().roi_extract_plan_perm(ws, wsb, num_rois, ctypes.byref(ptr)),
+          "roi_extract_plan_perm")
     off = (ptr.value or 0) - workspace.data_ptr()
     return workspace[off:off + 4 * num_rois].view(_torch().int32)
 
@@ -262,17 +328,16 @@ def roi_align_fwd(features: Sequence, scales: Sequence[float], rois, roi_levels,
     torch = _torch()
     rois = _rois(rois)
     K, L = rois.shape[0], len(features)
-    C = features[0].shape[1]
+    C = _channels(features)
     ph, pw = out_size
-    odt = out_dtype or features[0].dtype
+    lv = _roi_levels(roi_levels, rois, L)
     if out is None:
-        out = torch.empty((K, C, ph, pw), dtype=odt, device=rois.device)
-    if not out.is_contiguous():
-        raise ValueError("out must be contiguous [K, C, out_h, out_w]")
-    arr = level_array(features, scales)
-    lv = roi_levels.data_ptr() if roi_levels is not None else None
-    ws = workspace.data_ptr() if workspace is not None else None
-    wsb = workspace.numel() if workspace is not None else 0
+        out = torch.empty((K, C, ph, pw), dtype=out_dtype or features[0].dtype,
+                          device=rois.device)
+    _block(out, (K, C, ph, pw), "out", rois)
+    ws, wsb = _workspace(workspace, rois)
+    _on_device(rois, roi_levels=roi_levels, out=out, workspace=workspace)
+    arr = level_array(features, scales, rois)
     check(lib().roi_align_fwd(arr, L, rois.data_ptr(), K, lv, ph, pw, sampling_ratio,
                               int(bool(aligned)), out.data_ptr(), _dtype_code(out), ws, wsb,
                               stream_handle(stream)), "roi_align_fwd")
@@ -293,15 +358,16 @@ def roi_align_bwd(grad_out, rois, roi_levels, out_size: Tuple[int, int], samplin
     algorithm: 'scatter' (fp32 atomics), 'gather' (per-tile, needs the plan workspace) or
     'auto' (gather when eligible)."""
     rois = _rois(rois)
-    _need_cuda(grad_out, "grad_out")
-    if not grad_out.is_contiguous():
-        raise ValueError("grad_out must be contiguous [K, C, out_h, out_w]")
     K, L = rois.shape[0], len(grads)
+    C = _channels(grads)
     ph, pw = out_size
-    arr = level_array(grads, scales)
-    lv = roi_levels.data_ptr() if roi_levels is not None else None
-    ws = workspace.data_ptr() if workspace is not None else None
-    wsb = workspace.numel() if workspace is not None else 0
+    if algorithm not in _BWD_ALGOS:
+        raise ValueError("algorithm must be one of %s" % sorted(_BWD_ALGOS))
+    lv = _roi_levels(roi_levels, rois, L)
+    _block(grad_out, (K, C, ph, pw), "grad_out", rois)
+    ws, wsb = _workspace(workspace, rois)
+    _on_device(rois, roi_levels=roi_levels, grad_out=grad_out, workspace=workspace)
+    arr = level_array(grads, scales, rois)
     check(lib().roi_align_bwd(grad_out.data_ptr(), _dtype_code(grad_out), rois.data_ptr(), K, lv,
                               ph, pw, sampling_ratio, int(bool(aligned)), arr, L,
                               int(bool(zero_init)), _BWD_ALGOS[algorithm], ws, wsb,
@@ -318,19 +384,19 @@ def roi_pool_fwd(features: Sequence, scales: Sequence[float], rois, roi_levels,
     torch = _torch()
     rois = _rois(rois)
     K, L = rois.shape[0], len(features)
-    C = features[0].shape[1]
+    C = _channels(features)
     ph, pw = out_size
-    odt = out_dtype or features[0].dtype
+    lv = _roi_levels(roi_levels, rois, L)
     if out is None:
-        out = torch.empty((K, C, ph, pw), dtype=odt, device=rois.device)
+        out = torch.empty((K, C, ph, pw), dtype=out_dtype or features[0].dtype,
+                          device=rois.device)
     if argmax is None:
         argmax = torch.empty((K, C, ph, pw), dtype=torch.int32, device=rois.device)
-    if not out.is_contiguous() or not argmax.is_contiguous() or argmax.dtype != torch.int32:
-        raise ValueError("out and argmax must be contiguous [K, C, out_h, out_w] (argmax int32)")
-    arr = level_array(features, scales)
-    lv = roi_levels.data_ptr() if roi_levels is not None else None
-    ws = workspace.data_ptr() if workspace is not None else None
-    wsb = workspace.numel() if workspace is not None else 0
+    _block(out, (K, C, ph, pw), "out", rois)
+    _block(argmax, (K, C, ph, pw), "argmax", rois, (torch.int32,))
+    ws, wsb = _workspace(workspace, rois)
+    _on_device(rois, roi_levels=roi_levels, out=out, argmax=argmax, workspace=workspace)
+    arr = level_array(features, scales, rois)
     check(lib().roi_pool_fwd(arr, L, rois.data_ptr(), K, lv, ph, pw, out.data_ptr(),
                              _dtype_code(out), argmax.data_ptr(), ws, wsb, stream_handle(stream)),
           "roi_pool_fwd")
@@ -343,17 +409,18 @@ def roi_pool_bwd(grad_out, argmax, rois, roi_levels, grads: Sequence, scales: Se
     first if zero_init)."""
     torch = _torch()
     rois = _rois(rois)
-    _need_cuda(grad_out, "grad_out")
-    if not grad_out.is_contiguous() or not argmax.is_contiguous():
-        raise ValueError("grad_out and argmax must be contiguous [K, C, out_h, out_w]")
-    if argmax.dtype != torch.int32 or tuple(argmax.shape) != tuple(grad_out.shape):
-        raise ValueError("argmax must be int32 with grad_out's shape")
     K, L = rois.shape[0], len(grads)
+    C = _channels(grads)
+    if grad_out.dim() != 4:
+        raise ValueError("grad_out must be 4-D [K, C, out_h, out_w]")
     ph, pw = grad_out.shape[2], grad_out.shape[3]
-    arr = level_array(grads, scales)
-    lv = roi_levels.data_ptr() if roi_levels is not None else None
-    ws = workspace.data_ptr() if workspace is not None else None
-    wsb = workspace.numel() if workspace is not None else 0
+    lv = _roi_levels(roi_levels, rois, L)
+    _block(grad_out, (K, C, ph, pw), "grad_out", rois)
+    _block(argmax, (K, C, ph, pw), "argmax", rois, (torch.int32,))
+    ws, wsb = _workspace(workspace, rois)
+    _on_device(rois, roi_levels=roi_levels, grad_out=grad_out, argmax=argmax,
+               workspace=workspace)
+    arr = level_array(grads, scales, rois)
     check(lib().roi_pool_bwd(grad_out.data_ptr(), _dtype_code(grad_out), argmax.data_ptr(),
                              rois.data_ptr(), K, lv, ph, pw, arr, L, int(bool(zero_init)), ws,
                              wsb, stream_handle(stream)), "roi_pool_bwd")
@@ -365,32 +432,31 @@ def roi_align_bwd_multi(heads: Sequence[dict], grads: Sequence, scales: Sequence
     """Backward of several heads into one gradient pyramid (float32 levels, cleared first if
     zero_init).  Each head is a dict with grad_out, rois, roi_levels, out_size and optionally
     sampling_ratio (2), aligned (True) and workspace (its plan)."""
+    C, L = _channels(grads), len(grads)
     arr = (ReHead * max(1, len(heads)))()
     for i, h in enumerate(heads):
         rois = _rois(h["rois"])
-        g = h["grad_out"]
-        _need_cuda(g, "grad_out of head %d" % i)
-        if not g.is_contiguous():
-            raise ValueError("grad_out of head %d must be contiguous" % i)
+        K = rois.shape[0]
         ph, pw = h["out_size"]
-        lv = h.get("roi_levels")
-        ws = h.get("workspace")
+        g = _block(h["grad_out"], (K, C, ph, pw), "grad_out of head %d" % i, rois)
+        lv = _roi_levels(h.get("roi_levels"), rois, L)
+        ws, wsb = _workspace(h.get("workspace"), rois)
+        _on_device(rois, roi_levels=h.get("roi_levels"), grad_out=g,
+                   workspace=h.get("workspace"))
         arr[i] = ReHead(g.data_ptr(), _dtype_code(g), ph, pw, int(h.get("sampling_ratio", 2)),
-                        int(bool(h.get("aligned", True))), 0, rois.data_ptr(), rois.shape[0],
-                        lv.data_ptr() if lv is not None else None,
-                        ws.data_ptr() if ws is not None else None,
-                        ws.numel() if ws is not None else 0)
+                        int(bool(h.get("aligned", True))), 0, rois.data_ptr(), K, lv, ws, wsb)
     levels = level_array(grads, scales)
     check(lib().roi_align_bwd_multi(arr, len(heads), levels, len(grads), int(bool(zero_init)),
                                     stream_handle(stream)), "roi_align_bwd_multi")
     return grads
 
 
-def _f32_contig(t, name):
+def _f32_contig(t, name, shape=None, like=None):
     torch = _torch()
     if t.dtype != torch.float32 or not t.is_contiguous():
         raise ValueError("%s must be a contiguous float32 tensor" % name)
-    _need_cuda(t, name)
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s (got %s)" % (name, tuple(shape), tuple(t.shape)))
     return t
 
 
@@ -404,18 +470,20 @@ def deform_roi_pool_fwd(features: Sequence, scales: Sequence[float], rois, roi_l
     torch = _torch()
     rois = _rois(rois)
     K, L = rois.shape[0], len(features)
-    C = features[0].shape[1]
+    C = _channels(features)
     ph, pw = out_size
-    _f32_contig(offset, "offset")
+    lv = _roi_levels(roi_levels, rois, L)
+    _f32_contig(offset, "offset", (K, 2, ph, pw), rois)
     if mask is not None:
-        _f32_contig(mask, "mask")
-    odt = out_dtype or features[0].dtype
+        _f32_contig(mask, "mask", (K, ph, pw), rois)
     if out is None:
-        out = torch.empty((K, C, ph, pw), dtype=odt, device=rois.device)
-    arr = level_array(features, scales)
-    lv = roi_levels.data_ptr() if roi_levels is not None else None
-    ws = workspace.data_ptr() if workspace is not None else None
-    wsb = workspace.numel() if workspace is not None else 0
+        out = torch.empty((K, C, ph, pw), dtype=out_dtype or features[0].dtype,
+                          device=rois.device)
+    _block(out, (K, C, ph, pw), "out", rois)
+    ws, wsb = _workspace(workspace, rois)
+    _on_device(rois, roi_levels=roi_levels, offset=offset, mask=mask, out=out,
+               workspace=workspace)
+    arr = level_array(features, scales, rois)
     check(lib().deform_roi_pool_fwd(arr, L, rois.data_ptr(), K, lv, ph, pw, sampling_ratio,
                                     int(bool(aligned)), offset.data_ptr(),
                                     mask.data_ptr() if mask is not None else None, float(gamma),
@@ -432,23 +500,28 @@ def deform_roi_pool_bwd(grad_out, features: Sequence, rois, roi_levels, offset, 
     levels, cleared first if zero_init); returns (grads, grad_offset, grad_mask)."""
     torch = _torch()
     rois = _rois(rois)
-    _need_cuda(grad_out, "grad_out")
-    if not grad_out.is_contiguous():
-        raise ValueError("grad_out must be contiguous [K, C, out_h, out_w]")
     K, L = rois.shape[0], len(grads)
+    C = _channels(grads)
+    if grad_out.dim() != 4:
+        raise ValueError("grad_out must be 4-D [K, C, out_h, out_w]")
     ph, pw = grad_out.shape[2], grad_out.shape[3]
-    _f32_contig(offset, "offset")
+    lv = _roi_levels(roi_levels, rois, L)
+    _block(grad_out, (K, C, ph, pw), "grad_out", rois)
+    _f32_contig(offset, "offset", (K, 2, ph, pw), rois)
     if mask is not None:
-        _f32_contig(mask, "mask")
+        _f32_contig(mask, "mask", (K, ph, pw), rois)
     if grad_offset is None:
         grad_offset = torch.empty((K, 2, ph, pw), dtype=torch.float32, device=rois.device)
+    _f32_contig(grad_offset, "grad_offset", (K, 2, ph, pw), rois)
     if grad_mask is None and mask is not None:
         grad_mask = torch.empty((K, ph, pw), dtype=torch.float32, device=rois.device)
-    farr = level_array(features, scales)
-    garr = level_array(grads, scales)
-    lv = roi_levels.data_ptr() if roi_levels is not None else None
-    ws = workspace.data_ptr() if workspace is not None else None
-    wsb = workspace.numel() if workspace is not None else 0
+    if grad_mask is not None:
+        _f32_contig(grad_mask, "grad_mask", (K, ph, pw), rois)
+    ws, wsb = _workspace(workspace, rois)
+    _on_device(rois, roi_levels=roi_levels, grad_out=grad_out, offset=offset, mask=mask,
+               grad_offset=grad_offset, grad_mask=grad_mask, workspace=workspace)
+    farr = level_array(features, scales, rois)
+    garr = level_array(grads, scales, rois)
     check(lib().deform_roi_pool_bwd(grad_out.data_ptr(), _dtype_code(grad_out), farr, garr, L,
                                     rois.data_ptr(), K, lv, ph, pw, sampling_ratio,
                                     int(bool(aligned)), offset.data_ptr(),
@@ -464,16 +537,28 @@ def box_nms(boxes, scores, iou_threshold: float, categories=None, max_keep: int 
     """Greedy NMS on the GPU.  Returns (keep int32 [min(N, max_keep)]: kept indices in rank
     order then -1, num_keep int32 [1]); both stay on the device."""
     torch = _torch()
-    _need_cuda(boxes, "boxes")
+    if scores.dtype != torch.float32 or scores.dim() != 1 or not scores.is_contiguous():
+        raise ValueError("scores must be a contiguous float32 [N] tensor")
     N = scores.shape[0]
     if boxes.dtype != torch.float32 or tuple(boxes.shape) != (N, 4) or not boxes.is_contiguous():
         raise ValueError("boxes must be a contiguous float32 [N, 4] tensor")
-    if scores.dtype != torch.float32 or not scores.is_contiguous():
-        raise ValueError("scores must be a contiguous float32 [N] tensor")
     if categories is not None and (categories.dtype != torch.int32 or
+                                   tuple(categories.shape) != (N,) or
                                    not categories.is_contiguous()):
         raise ValueError("categories must be a contiguous int32 [N] tensor")
     mk = N if max_keep is None else int(max_keep)
+    if mk < 0:
+        raise ValueError("max_keep must be >= 0")
+    if keep is not None and (keep.dtype != torch.int32 or not keep.is_contiguous() or
+                             keep.numel() < min(N, mk)):
+        raise ValueError("keep must be a contiguous int32 tensor of at least %d elements"
+                         % min(N, mk))
+    if num_keep is not None and (num_keep.dtype != torch.int32 or num_keep.numel() < 1):
+        raise ValueError("num_keep must be an int32 tensor of at least 1 element")
+    _need_cuda(boxes, "boxes")
+    _need_cuda(scores, "scores", boxes)
+    if categories is not None:
+        _need_cuda(categories, "categories", boxes)
     n = ctypes.c_size_t(0)
     check(lib().box_nms_workspace_size(N, ctypes.byref(n)), "box_nms_workspace_size")
     if workspace is None:
@@ -482,8 +567,11 @@ def box_nms(boxes, scores, iou_threshold: float, categories=None, max_keep: int 
         keep = torch.empty(max(min(N, mk), 1), dtype=torch.int32, device=boxes.device)
     if num_keep is None:
         num_keep = torch.empty(1, dtype=torch.int32, device=boxes.device)
+    _need_cuda(keep, "keep", boxes)
+    _need_cuda(num_keep, "num_keep", boxes)
+    ws, wsb = _workspace(workspace, boxes)
     check(lib().box_nms(boxes.data_ptr(), scores.data_ptr(),
                         categories.data_ptr() if categories is not None else None, N,
                         float(iou_threshold), mk, keep.data_ptr(), num_keep.data_ptr(),
-                        workspace.data_ptr(), workspace.numel(), stream_handle(stream)), "box_nms")
+                        ws, wsb, stream_handle(stream)), "box_nms")
     return keep[:min(N, mk)], num_keep

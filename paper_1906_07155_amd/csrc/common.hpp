@@ -114,8 +114,9 @@ template <> __device__ __forceinline__ void store_f32<uint16_t>(gptr<uint16_t> p
 // scalar registers; each lane then supplies one 32-bit byte offset, and the
 // hardware's range check makes an offset at or past the range read 0 without a
 // memory access.  Offsets inside one image of a level stay below 2^30 (checked on
-// the host), so adding kBufOOB to any term of an offset sum pushes it out of range
-// without wrapping, even when all three terms carry it.
+// the host), so adding kBufOOB to any term of a lane-offset sum pushes it out of
+// range without wrapping, even when all three terms carry it.  The check covers the
+// lane offset only: a scalar offset added by the instruction is not checked.
 constexpr uint32_t kBufOOB = 0x40000000u;
 constexpr uint32_t kBufMaxBytes = 0x40000000u;
 constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, no swizzle (gfx9 family)
@@ -138,7 +139,10 @@ template <> __device__ __forceinline__ uint32_t buf_load_raw<uint16_t>(__amdgpu_
                                                                        uint32_t off) {
     return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
-// Same, with a scalar byte offset added to every lane's offset.
+// Same, with a scalar byte offset added to every lane's offset.  The range check
+// sees the lane offset only: the scalar offset must itself keep the access inside
+// the range (mark an access out of range through the lane offset, never through
+// the scalar one).
 template <typename T> __device__ __forceinline__ uint32_t buf_load_raw_s(__amdgpu_buffer_rsrc_t r,
                                                                          uint32_t off, uint32_t soff);
 template <> __device__ __forceinline__ uint32_t buf_load_raw_s<float>(__amdgpu_buffer_rsrc_t r,

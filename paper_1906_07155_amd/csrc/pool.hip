@@ -160,8 +160,11 @@ __global__ __launch_bounds__(256) void pool_fwd_cl_kernel(PoolArgs a) {
             if (active && ry.hi > ry.lo && rx.hi > rx.lo) {
                 best = -FLT_MAX;
                 // The bin's pixels in row-major order, kPoolBatch loads in flight at a
-                // time (positions past the bin read out of range and are skipped), then
-                // compared in order so the first maximum wins.
+                // time, then compared in order so the first maximum wins.  A position
+                // past the bin takes the out-of-range lane offset and reads zero without
+                // a memory access (the hardware range check covers the lane offset only,
+                // never the scalar one, so the scalar offset is always an in-map pixel);
+                // its value is skipped.
                 const int nx = rx.hi - rx.lo;
                 const int n = (ry.hi - ry.lo) * nx;
                 int y = ry.lo, x = rx.lo;
@@ -170,10 +173,11 @@ __global__ __launch_bounds__(256) void pool_fwd_cl_kernel(PoolArgs a) {
                     int yy = y, xx = x;
 #pragma unroll
                     for (int j = 0; j < kPoolBatch; ++j) {
-                        const uint32_t off = i0 + j < n ? static_cast<uint32_t>(yy) * sh +
-                                                              static_cast<uint32_t>(xx) * sw
-                                                        : kBufOOB;
-                        v[j] = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, off));
+                        const bool in_bin = i0 + j < n;
+                        const uint32_t off = in_bin ? static_cast<uint32_t>(yy) * sh +
+                                                          static_cast<uint32_t>(xx) * sw
+                                                    : 0u;
+                        v[j] = raw_to_f32<T>(buf_load_raw_s<T>(rs, in_bin ? vo : kBufOOB, off));
                         if (++xx == rx.hi) {
                             xx = rx.lo;
                             ++yy;

@@ -1,9 +1,11 @@
 """SingleRoIExtractor-style entry point with autograd (MMDetection §3.1, §3.2).
 
 `roi_extract` assigns every RoI to its FPN level, builds the launch plan and runs
-the RoIAlign forward; the backward (the transpose, scattered into the feature
-pyramid with fp32 atomics) reuses the same levels and plan.  All arithmetic runs
-in the HIP library; this module only wires it into torch.autograd.
+the RoIAlign forward; the backward (the transpose) reuses the same levels and plan:
+by default every tile of the gradient pyramid gathers the RoIs the plan binned to it
+and is written once with plain stores (the fp32-atomic scatter serves the cases the
+gather does not cover).  All arithmetic runs in the HIP library; this module only
+wires it into torch.autograd.
 """
 from __future__ import annotations
 

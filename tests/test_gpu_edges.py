@@ -127,8 +127,8 @@ def _pyr(c):
 @pytest.mark.parametrize("out_hw", [(7, 7), (14, 14)])
 @pytest.mark.parametrize("C", [1, 3, 100, 256, 320])
 def test_channels_ragged(out_hw, C, gdt):
-    # a bf16 upstream gradient on the 7x7 grid takes the channel-group gather form,
-    # whose workgroups hold up to four channel groups (partial ones included)
+    # channel counts that leave the last 64-channel group partial (or make it the only
+    # one): the lanes past the last channel must neither read nor write
     rng = np.random.default_rng(C)
     rois = W.draw_rois(rng, 2, 19, (96, 160), (4.0, 200.0))
     run("C=%d %s g=%s" % (C, out_hw, gdt), _pyr(C), SC, rois, out_hw=out_hw, gdt=gdt)
