@@ -37,7 +37,9 @@
  * device pointers except the re_level_t arrays, which are read on the host during
  * the call.  Calls enqueue work on `stream` (a hipStream_t; NULL = the null
  * stream) and return without synchronizing.  The library never allocates device
- * memory and keeps no state between calls.  Argument errors are detected on the
+ * memory and keeps no state between calls (one exception: roi_align_fwd_noalloc keeps
+ * its plan in a fixed array of the library's device code, see there).  Argument
+ * errors are detected on the
  * host before anything is enqueued; a launch failure is reported as
  * RE_ERR_DEVICE.  Device-side content (RoI coordinates, level indices, plan
  * contents) is never reported as an error: out-of-range values are clamped or
@@ -173,6 +175,28 @@ re_status_t roi_align_fwd(const re_level_t *levels, int32_t num_levels,
                           int32_t out_h, int32_t out_w, int32_t sampling_ratio,
                           int32_t aligned, void *out, int32_t out_dtype,
                           const void *plan, size_t plan_bytes, void *stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): roi_extract_plan's level map and
+ * launch order without the tile lists, then roi_align_fwd in that order, with the plan
+ * kept in a fixed array of RE_NOALLOC_SCRATCH_BYTES inside the library's device code
+ * instead of a caller workspace.  Nothing is allocated (no hipMalloc or hipFree, no
+ * allocating library routine); each GPU the library runs on holds its own copy of the
+ * array until the process ends.  The copy of the current device is used (`stream` must
+ * belong to it); its address is looked up on the first call on each device.
+ *   num_rois <= RE_NOALLOC_MAX_ROIS (RE_ERR_UNSUPPORTED above, nothing enqueued);
+ *   levels_out: device int32[num_rois], written as by roi_extract_plan (RE_BOX_CONTINUOUS);
+ *   the other arguments as roi_extract_plan and roi_align_fwd.
+ * Results equal roi_align_fwd's.  Every call on one GPU shares that GPU's array (each
+ * call rebuilds the plan in it), so calls that overlap on one GPU -- on two streams or
+ * from two host threads -- race and must be serialised by the caller. */
+#define RE_NOALLOC_MAX_ROIS 65536
+#define RE_NOALLOC_SCRATCH_BYTES 589824   /* 576 KiB per GPU */
+re_status_t roi_align_fwd_noalloc(const re_level_t *levels, int32_t num_levels,
+                                  const float *rois, int64_t num_rois, float finest_scale,
+                                  int32_t *levels_out, int32_t out_h, int32_t out_w,
+                                  int32_t sampling_ratio, int32_t aligned, void *out,
+                                  int32_t out_dtype, void *stream);
 
 /* a6 -- clear the gradient pyramid (every element of every level set to +0.0).
  * grad_levels: host array; every level RE_DTYPE_F32. */

@@ -69,6 +69,8 @@ SIGNATURES = {
     "roi_align_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _VP, _I32, _VP,
                       _SZ, _VP],
     "roi_extract_zero_grad": [_LEVELS, _I32, _VP],
+    "roi_align_fwd_noalloc": [_LEVELS, _I32, _VP, _I64, _F32, _VP, _I32, _I32, _I32, _I32, _VP,
+                              _I32, _VP],
     "roi_align_bwd": [_VP, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _LEVELS, _I32, _I32,
                       _I32, _VP, _SZ, _VP],
     "roi_align_bwd_multi": [_HEADS, _I32, _LEVELS, _I32, _I32, _VP],
@@ -342,6 +344,35 @@ def roi_align_fwd(features: Sequence, scales: Sequence[float], rois, roi_levels,
                               int(bool(aligned)), out.data_ptr(), _dtype_code(out), ws, wsb,
                               stream_handle(stream)), "roi_align_fwd")
     return out
+
+
+def roi_align_fwd_noalloc(features: Sequence, scales: Sequence[float], rois,
+                          out_size: Tuple[int, int], sampling_ratio: int = 2,
+                          aligned: bool = True, finest_scale: float = 56.0, levels_out=None,
+                          out=None, out_dtype=None, stream=None):
+    """Level map, launch plan and forward in one call that allocates no device memory in
+    the library (the plan lives in the library's fixed per-GPU array; calls overlapping
+    on one GPU race).  Returns (out, levels_out); pass preallocated `out` and
+    `levels_out` for a call that allocates nothing at all."""
+    torch = _torch()
+    rois = _rois(rois)
+    K, L = rois.shape[0], len(features)
+    C = _channels(features)
+    ph, pw = out_size
+    if levels_out is None:
+        levels_out = torch.empty(K, dtype=torch.int32, device=rois.device)
+    lv = _roi_levels(levels_out, rois, 2)
+    if out is None:
+        out = torch.empty((K, C, ph, pw), dtype=out_dtype or features[0].dtype,
+                          device=rois.device)
+    _block(out, (K, C, ph, pw), "out", rois)
+    _on_device(rois, levels_out=levels_out, out=out)
+    arr = level_array(features, scales, rois)
+    check(lib().roi_align_fwd_noalloc(arr, L, rois.data_ptr(), K, finest_scale, lv, ph, pw,
+                                      sampling_ratio, int(bool(aligned)), out.data_ptr(),
+                                      _dtype_code(out), stream_handle(stream)),
+          "roi_align_fwd_noalloc")
+    return out, levels_out
 
 
 def zero_grad(grads: Sequence, scales: Sequence[float], stream=None):

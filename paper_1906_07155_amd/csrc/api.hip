@@ -7,6 +7,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "internal.hpp"
 #include "roi_extract.h"
@@ -45,6 +46,21 @@ size_t workspace_bytes_for(int64_t K, const TileLayout &t) {
 // (tile, RoI) pairs: a RoI meets at most every tile of one image-level.  Binning is
 // switched off (ntiles = 0) when that bound would exceed 2^28 pairs.
 constexpr int64_t kMaxPairs = int64_t(1) << 28;
+
+// No bin-tiles: the plan is the forward's launch order only.
+TileLayout no_tiles() {
+    TileLayout off{};
+    off.shift = 4;
+    for (int l = 0; l <= kMaxLevels; ++l) {
+        if (l < kMaxLevels) {
+            off.ntx[l] = 1;
+            off.nty[l] = 1;
+        }
+        off.tbase[l] = 0;
+    }
+    return off;
+}
+
 TileLayout tile_layout(const LevelTable &t, int64_t K) {
     TileLayout L{};
     for (int shift = 4; shift <= 24; ++shift) {
@@ -76,16 +92,7 @@ TileLayout tile_layout(const LevelTable &t, int64_t K) {
         L.tbase[kMaxLevels] = base;
         return L;
     }
-    TileLayout off{};
-    off.shift = 4;
-    for (int l = 0; l <= kMaxLevels; ++l) {
-        if (l < kMaxLevels) {
-            off.ntx[l] = 1;
-            off.nty[l] = 1;
-        }
-        off.tbase[l] = 0;
-    }
-    return off;   // ntiles = 0: no binning
+    return no_tiles();   // ntiles = 0: no binning
 }
 
 constexpr int64_t kMaxRois = int64_t(1) << 22;
@@ -193,6 +200,71 @@ re_status_t check_plan(const void *plan, size_t plan_bytes, int64_t K, const Lev
 
 re_status_t from_hip(hipError_t e) { return e == hipSuccess ? RE_OK : RE_ERR_DEVICE; }
 
+// Plan arguments for the RoIs over pyramid t, the plan stored in `ws` with the tile
+// layout tl (ntiles = 0: no tile lists, the forward's launch order only).
+re_status_t plan_args(const LevelTable &t, const float *rois, int64_t num_rois, float finest_scale,
+                      int32_t box_convention, int32_t *levels_out, char *ws, const TileLayout &tl,
+                      PlanArgs *out) {
+    const int32_t num_levels = t.num;
+    PlanArgs a{};
+    a.rois = rois;
+    a.levels_out = levels_out;
+    a.offsets = reinterpret_cast<int32_t *>(ws);
+    a.perm = reinterpret_cast<int32_t *>(ws + perm_offset());
+    a.keys = reinterpret_cast<int32_t *>(ws + keys_offset(num_rois));
+    a.K = static_cast<int32_t>(num_rois);
+    a.L = num_levels;
+    a.finest_scale = finest_scale;
+    a.box_plus1 = box_convention == RE_BOX_PIXELS ? 1 : 0;
+    a.N = t.N;
+    // Cell size 2^shift feature pixels: the smallest shift >= 4 whose bucket count fits.
+    a.batch_in_key = 1;
+    int shift = 4;
+    int64_t nbins = 0;
+    for (;; ++shift) {
+        nbins = 0;
+        for (int l = 0; l < num_levels; ++l) {
+            const int64_t ncx = (t.l[l].W + (int64_t(1) << shift) - 1) >> shift;
+            const int64_t ncy = (t.l[l].H + (int64_t(1) << shift) - 1) >> shift;
+            nbins += (a.batch_in_key ? t.N : 1) * ncx * ncy;
+        }
+        if (nbins <= kPlanMaxBins) break;
+        if (shift >= 24) {
+            if (!a.batch_in_key) return RE_ERR_UNSUPPORTED;
+            a.batch_in_key = 0;   // very large batches: bucket by level and cell only
+            shift = 3;
+        }
+    }
+    a.cell_shift = shift;
+    a.nbins = static_cast<int32_t>(nbins);
+    int32_t base = 0;
+    for (int l = 0; l < num_levels; ++l) {
+        a.H[l] = t.l[l].H;
+        a.W[l] = t.l[l].W;
+        a.scale[l] = t.l[l].scale;
+        a.ncx[l] = static_cast<int32_t>((t.l[l].W + (1 << shift) - 1) >> shift);
+        a.ncy[l] = static_cast<int32_t>((t.l[l].H + (1 << shift) - 1) >> shift);
+        a.base[l] = base;
+        base += (a.batch_in_key ? t.N : 1) * a.ncx[l] * a.ncy[l];
+    }
+    a.tile_start = reinterpret_cast<int32_t *>(ws + tiles_offset(num_rois));
+    a.tile_rois = reinterpret_cast<int32_t *>(ws + tile_rois_offset(num_rois, tl));
+    a.tile_order = reinterpret_cast<int32_t *>(ws + tile_order_offset(num_rois, tl));
+    a.key_count = reinterpret_cast<int32_t *>(ws + key_count_offset(num_rois, tl));
+    a.tile_cursor = reinterpret_cast<int32_t *>(ws + tile_cursor_offset(num_rois, tl));
+    a.ntiles = tl.ntiles;
+    a.capacity = static_cast<int32_t>(tl.capacity);
+    a.tile_shift = tl.shift;
+    for (int l = 0; l < kMaxLevels; ++l) {
+        a.ntx[l] = tl.ntx[l];
+        a.nty[l] = tl.nty[l];
+        a.tbase[l] = tl.tbase[l];
+    }
+    a.tbase[kMaxLevels] = tl.tbase[kMaxLevels];
+    *out = a;
+    return RE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -267,63 +339,10 @@ re_status_t roi_extract_plan_ex(const re_level_t *levels, int32_t num_levels, co
     if (reinterpret_cast<uintptr_t>(rois) % 4 || reinterpret_cast<uintptr_t>(levels_out) % 4)
         return RE_ERR_INVALID_ARG;
 
-    PlanArgs a{};
-    char *ws = static_cast<char *>(workspace);
-    a.rois = rois;
-    a.levels_out = levels_out;
-    a.offsets = reinterpret_cast<int32_t *>(ws);
-    a.perm = reinterpret_cast<int32_t *>(ws + perm_offset());
-    a.keys = reinterpret_cast<int32_t *>(ws + keys_offset(num_rois));
-    a.K = static_cast<int32_t>(num_rois);
-    a.L = num_levels;
-    a.finest_scale = finest_scale;
-    a.box_plus1 = box_convention == RE_BOX_PIXELS ? 1 : 0;
-    a.N = t.N;
-    // Cell size 2^shift feature pixels: the smallest shift >= 4 whose bucket count fits.
-    a.batch_in_key = 1;
-    int shift = 4;
-    int64_t nbins = 0;
-    for (;; ++shift) {
-        nbins = 0;
-        for (int l = 0; l < num_levels; ++l) {
-            const int64_t ncx = (t.l[l].W + (int64_t(1) << shift) - 1) >> shift;
-            const int64_t ncy = (t.l[l].H + (int64_t(1) << shift) - 1) >> shift;
-            nbins += (a.batch_in_key ? t.N : 1) * ncx * ncy;
-        }
-        if (nbins <= kPlanMaxBins) break;
-        if (shift >= 24) {
-            if (!a.batch_in_key) return RE_ERR_UNSUPPORTED;
-            a.batch_in_key = 0;   // very large batches: bucket by level and cell only
-            shift = 3;
-        }
-    }
-    a.cell_shift = shift;
-    a.nbins = static_cast<int32_t>(nbins);
-    int32_t base = 0;
-    for (int l = 0; l < num_levels; ++l) {
-        a.H[l] = t.l[l].H;
-        a.W[l] = t.l[l].W;
-        a.scale[l] = t.l[l].scale;
-        a.ncx[l] = static_cast<int32_t>((t.l[l].W + (1 << shift) - 1) >> shift);
-        a.ncy[l] = static_cast<int32_t>((t.l[l].H + (1 << shift) - 1) >> shift);
-        a.base[l] = base;
-        base += (a.batch_in_key ? t.N : 1) * a.ncx[l] * a.ncy[l];
-    }
-    const TileLayout tl = tile_layout(t, num_rois);
-    a.tile_start = reinterpret_cast<int32_t *>(ws + tiles_offset(num_rois));
-    a.tile_rois = reinterpret_cast<int32_t *>(ws + tile_rois_offset(num_rois, tl));
-    a.tile_order = reinterpret_cast<int32_t *>(ws + tile_order_offset(num_rois, tl));
-    a.key_count = reinterpret_cast<int32_t *>(ws + key_count_offset(num_rois, tl));
-    a.tile_cursor = reinterpret_cast<int32_t *>(ws + tile_cursor_offset(num_rois, tl));
-    a.ntiles = tl.ntiles;
-    a.capacity = static_cast<int32_t>(tl.capacity);
-    a.tile_shift = tl.shift;
-    for (int l = 0; l < kMaxLevels; ++l) {
-        a.ntx[l] = tl.ntx[l];
-        a.nty[l] = tl.nty[l];
-        a.tbase[l] = tl.tbase[l];
-    }
-    a.tbase[kMaxLevels] = tl.tbase[kMaxLevels];
+    PlanArgs a;
+    if ((st = plan_args(t, rois, num_rois, finest_scale, box_convention, levels_out,
+                        static_cast<char *>(workspace), tile_layout(t, num_rois), &a)) != RE_OK)
+        return st;
     return from_hip(launch_plan(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -384,6 +403,88 @@ re_status_t roi_align_fwd(const re_level_t *levels, int32_t num_levels, const fl
     const bool fast = cl && fwd_fast_available(out_h, out_w, sampling_ratio);
     return from_hip(launch_fwd(a, levels[0].dtype, out_dtype, fast,
                                static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free forward
+// ---------------------------------------------------------------------------
+//
+// roi_align_fwd_noalloc keeps its launch plan in `scratch`, a fixed array in the
+// library's device code instead of a caller workspace.  In host code the name
+// `scratch` only stands in for the symbol: the device address of each GPU's copy is
+// looked up once per device (hipGetSymbolAddress with that device current) and only
+// that address is passed to kernels.  The plan kernels clear every counter they use
+// themselves (no memset), so the array's previous contents do not matter.
+
+static_assert(RE_NOALLOC_SCRATCH_BYTES % 256 == 0, "scratch size");
+static __device__ __align__(256) unsigned char scratch[RE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (looked up on first use).
+re_status_t scratch_address(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return RE_ERR_DEVICE;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return RE_ERR_DEVICE;
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return RE_OK;
+}
+}  // namespace
+
+extern "C" {
+
+re_status_t roi_align_fwd_noalloc(const re_level_t *levels, int32_t num_levels, const float *rois,
+                                  int64_t num_rois, float finest_scale, int32_t *levels_out,
+                                  int32_t out_h, int32_t out_w, int32_t sampling_ratio,
+                                  int32_t aligned, void *out, int32_t out_dtype, void *stream) {
+    LevelTable t;
+    bool cl = false;
+    re_status_t st = check_levels(levels, num_levels, true, &t, &cl, nullptr, nullptr);
+    if (st != RE_OK) return st;
+    if (num_rois > RE_NOALLOC_MAX_ROIS) return RE_ERR_UNSUPPORTED;
+    if ((st = check_common(rois, num_rois, levels_out, 2, out_h, out_w, sampling_ratio,
+                           aligned)) != RE_OK)
+        return st;
+    if (!std::isfinite(finest_scale) || !(finest_scale > 0.0f)) return RE_ERR_INVALID_ARG;
+    if (!valid_dtype(out_dtype)) return RE_ERR_INVALID_ARG;
+    if (num_rois > 0 && !out) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(out) % dtype_size(out_dtype)) return RE_ERR_INVALID_ARG;
+    if (num_rois == 0) return RE_OK;
+    const TileLayout tl = no_tiles();
+    if (workspace_bytes_for(num_rois, tl) > RE_NOALLOC_SCRATCH_BYTES) return RE_ERR_UNSUPPORTED;
+
+    void *ws = nullptr;
+    if ((st = scratch_address(&ws)) != RE_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    PlanArgs pa;
+    if ((st = plan_args(t, rois, num_rois, finest_scale, RE_BOX_CONTINUOUS, levels_out,
+                        static_cast<char *>(ws), tl, &pa)) != RE_OK)
+        return st;
+    if ((st = from_hip(launch_plan(pa, s))) != RE_OK) return st;
+
+    FwdArgs a{};
+    a.lv = t;
+    a.rois = rois;
+    a.roi_levels = levels_out;
+    a.perm = reinterpret_cast<const int32_t *>(static_cast<const char *>(ws) + perm_offset());
+    a.out = out;
+    a.K = static_cast<int32_t>(num_rois);
+    a.PH = out_h;
+    a.PW = out_w;
+    a.S = sampling_ratio;
+    a.aligned = aligned;
+    const bool fast = cl && fwd_fast_available(out_h, out_w, sampling_ratio);
+    return from_hip(launch_fwd(a, levels[0].dtype, out_dtype, fast, s));
 }
 
 re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_levels,
