@@ -95,6 +95,14 @@ def _bind(lib):
     lib.oracle_nms.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                ctypes.c_float, ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_nms.restype = ctypes.c_int32
+    lib.oracle_soft_gauss_weight.argtypes = [ctypes.c_float, ctypes.c_float]
+    lib.oracle_soft_gauss_weight.restype = ctypes.c_float
+    lib.oracle_nms_batched.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                       ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                       ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p]
+    lib.oracle_nms_batched.restype = None
     return lib
 
 
@@ -325,3 +333,38 @@ def nms(boxes, scores, threshold: float, categories=None, max_keep: int | None =
     n = lib.oracle_nms(_ptr(bx), _ptr(sc), None if cats is None else _ptr(cats), N,
                        float(threshold), N if max_keep is None else int(max_keep), _ptr(keep))
     return keep[:n].copy()
+
+
+NMS_METHODS = {"hard": 0, "linear": 1, "gaussian": 2}
+
+
+def soft_gauss_weight(iou: float, sigma: float, lib=None) -> float:
+    """Binary32 Gaussian decay weight exp(-iou^2 / sigma) of Soft-NMS (1 for iou <= 0 or
+    NaN)."""
+    lib = lib or load()
+    return float(lib.oracle_soft_gauss_weight(float(iou), float(sigma)))
+
+
+def nms_batched(boxes, scores, categories, num_categories: int, method: str = "hard",
+                iou_threshold: float = 0.5, sigma: float = 0.5,
+                score_threshold: float = float("-inf"), max_keep: int | None = None, lib=None):
+    """Per-category proposal selection: greedy NMS ("hard") or Soft-NMS with linear or
+    Gaussian decay.  Returns (keep [C, max_keep] int32 padded with -1, scores
+    [C, max_keep] float32 padded with 0, num_keep [C] int32)."""
+    lib = lib or load()
+    bx = np.ascontiguousarray(boxes, dtype=np.float32)
+    sc = np.ascontiguousarray(scores, dtype=np.float32)
+    N = sc.shape[0]
+    if bx.shape != (N, 4):
+        raise ValueError("boxes must be [N, 4]")
+    cats = None if categories is None else np.ascontiguousarray(categories, dtype=np.int32)
+    mk = N if max_keep is None else int(max_keep)
+    C = int(num_categories)
+    keep = np.zeros((C, max(mk, 1)), dtype=np.int32)
+    kept_scores = np.zeros((C, max(mk, 1)), dtype=np.float32)
+    num = np.zeros(C, dtype=np.int32)
+    lib.oracle_nms_batched(_ptr(bx), _ptr(sc), None if cats is None else _ptr(cats), N, C,
+                           NMS_METHODS[method], float(iou_threshold), float(sigma),
+                           float(score_threshold), mk, _ptr(keep), _ptr(kept_scores),
+                           _ptr(num))
+    return keep[:, :mk].copy(), kept_scores[:, :mk].copy(), num

@@ -21,6 +21,9 @@
  *   - §2 also lists DCN (deformable RoI pooling) and DCNv2 (its modulated form):
  *     oracle_deform_roi_pool_fwd/bwd move every RoIAlign bin by a learned offset
  *     and scale it by a learned modulation; the definition is written above them.
+ *   - §1 runs the bbox operations on the GPU and §2 lists Soft-NMS next to greedy
+ *     NMS: oracle_nms (greedy) and oracle_nms_batched (per-category greedy or
+ *     Soft-NMS with linear or Gaussian decay) select the proposals.
  *   The paper does not spell the operator out.  The definition below is the
  *   standard one (bilinear sampling on a regular grid inside each bin, averaged),
  *   and every convention the paper leaves open is fixed the same way as in the
@@ -891,4 +894,146 @@ int32_t oracle_nms(const float *boxes, const float *scores, const int32_t *cats,
     free(it);
     free(removed);
     return n;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Batched proposal selection and Soft-NMS.  The paper lists Soft-NMS among     */
+/* its general modules (§2) next to greedy NMS; a batch of images (or of        */
+/* classes) is one call with one category per image (class).  Per category c:  */
+/*   candidates: the boxes of category c whose score is >= score_threshold     */
+/*   (a NaN score never is); ranked as in greedy NMS (total order of the score */
+/*   bits, highest first, equal scores by index).                              */
+/*   hard (method 0): greedy NMS over the candidates in rank order, a box      */
+/*     removed when IoU > iou_threshold with a kept box;                       */
+/*   soft (methods 1, 2), repeated while candidates remain and fewer than      */
+/*     max_keep are kept: select the candidate with the largest current score  */
+/*     (same total order; equal current scores by rank), output it with that   */
+/*     score and remove it; every remaining candidate of the category is       */
+/*     decayed, s = fl(s * w(iou)), iou = oracle_box_iou(selected, candidate): */
+/*       linear (1):   w = fl(1 - iou) if iou > iou_threshold, else s is kept; */
+/*       gaussian (2): w = soft_gauss_weight(iou, sigma);                      */
+/*     a NaN iou leaves s unchanged; a candidate whose new score is below      */
+/*     score_threshold is dropped.                                             */
+/*   At most max_keep per category; the output of category c is its kept box   */
+/*   indices in selection order (for hard: rank order) with their score at     */
+/*   selection (hard: the input score), then -1 / 0 padding.                   */
+/* ------------------------------------------------------------------------- */
+
+/* The Gaussian decay exp(-iou^2 / sigma), rounded to binary32.  exp is evaluated */
+/* in double by scaling and squaring (halve the argument until it is in [-1/2, 0], */
+/* a degree-16 Taylor polynomial in Horner form, square back), one double rounding */
+/* per operation in the written order, so that the CPU and the GPU library, each  */
+/* implementing the same method, obtain the same binary32 weight (a score decides */
+/* which box is selected next, so both must hold it in the same precision).       */
+float oracle_soft_gauss_weight(float iou, float sigma)
+{
+    if (!(iou > 0.0f))
+        return 1.0f;
+    double x = -((double)iou * (double)iou) / (double)sigma;
+    if (!(x >= -128.0))
+        return 0.0f;   /* exp(x) < 2^-184 rounds to +0 (also an infinite IoU) */
+    int k = 0;
+    while (x < -0.5) {
+        x = x * 0.5;
+        ++k;
+    }
+    double e = 1.0;
+    for (int n = 16; n >= 1; --n)
+        e = 1.0 + (x * e) / (double)n;
+    for (int i = 0; i < k; ++i)
+        e = e * e;
+    return (float)e;
+}
+
+/* keep_out / scores_out: [num_categories][max_keep]; num_keep_out: [num_categories]. */
+void oracle_nms_batched(const float *boxes, const float *scores, const int32_t *cats,
+                        int32_t N, int32_t num_categories, int32_t method,
+                        float iou_threshold, float sigma, float score_threshold,
+                        int32_t max_keep, int32_t *keep_out, float *scores_out,
+                        int32_t *num_keep_out)
+{
+    nms_item *it = (nms_item *)malloc(sizeof(nms_item) * (size_t)(N > 0 ? N : 1));
+    float *cur = (float *)malloc(sizeof(float) * (size_t)(N > 0 ? N : 1));
+    char *alive = (char *)malloc((size_t)(N > 0 ? N : 1));
+    for (int32_t c = 0; c < num_categories; ++c) {
+        int32_t *ko = keep_out + (int64_t)c * max_keep;
+        float *so = scores_out + (int64_t)c * max_keep;
+        for (int32_t q = 0; q < max_keep; ++q) {
+            ko[q] = -1;
+            so[q] = 0.0f;
+        }
+        /* the candidates of category c, in rank order */
+        int32_t n = 0;
+        for (int32_t i = 0; i < N; ++i) {
+            const int32_t ci = cats ? cats[i] : 0;
+            if (ci != c || !(scores[i] >= score_threshold))
+                continue;
+            it[n].key = nms_rank_key(scores[i]);
+            it[n].idx = i;
+            ++n;
+        }
+        qsort(it, (size_t)n, sizeof(nms_item), nms_item_cmp);
+        int32_t kept = 0;
+        if (method == 0) {
+            for (int32_t r = 0; r < n; ++r)
+                alive[r] = 1;
+            for (int32_t r = 0; r < n && kept < max_keep; ++r) {
+                if (!alive[r])
+                    continue;
+                const int32_t i = it[r].idx;
+                ko[kept] = i;
+                so[kept] = scores[i];
+                ++kept;
+                for (int32_t q = r + 1; q < n; ++q) {
+                    if (alive[q] && oracle_box_iou(boxes + 4 * (int64_t)i,
+                                                   boxes + 4 * (int64_t)it[q].idx) > iou_threshold)
+                        alive[q] = 0;
+                }
+            }
+        } else {
+            for (int32_t r = 0; r < n; ++r) {
+                alive[r] = 1;
+                cur[r] = scores[it[r].idx];
+            }
+            while (kept < max_keep) {
+                /* the candidate with the largest current score; equal scores by rank */
+                int32_t best = -1;
+                for (int32_t r = 0; r < n; ++r) {
+                    if (!alive[r])
+                        continue;
+                    if (best < 0 || nms_rank_key(cur[r]) < nms_rank_key(cur[best]))
+                        best = r;
+                }
+                if (best < 0)
+                    break;
+                const int32_t m = it[best].idx;
+                ko[kept] = m;
+                so[kept] = cur[best];
+                ++kept;
+                alive[best] = 0;
+                for (int32_t r = 0; r < n; ++r) {
+                    if (!alive[r])
+                        continue;
+                    const float iou = oracle_box_iou(boxes + 4 * (int64_t)m,
+                                                     boxes + 4 * (int64_t)it[r].idx);
+                    if (iou != iou)
+                        continue;                  /* NaN IoU: no decay */
+                    if (method == 1) {
+                        if (iou > iou_threshold) {
+                            const float w = 1.0f - iou;
+                            cur[r] = cur[r] * w;
+                        }
+                    } else {
+                        cur[r] = cur[r] * oracle_soft_gauss_weight(iou, sigma);
+                    }
+                    if (cur[r] < score_threshold)
+                        alive[r] = 0;
+                }
+            }
+        }
+        num_keep_out[c] = kept;
+    }
+    free(it);
+    free(cur);
+    free(alive);
 }

@@ -33,6 +33,38 @@ MUTANTS = [
      "        return 0u;"),
     ("one box too many", "for (int32_t r = 0; r < N && n < max_keep; ++r) {",
      "for (int32_t r = 0; r < N && n <= max_keep; ++r) {"),
+    ("soft: linear decay at IoU equal to the threshold",
+     "                        if (iou > iou_threshold) {\n                            const float w",
+     "                        if (iou >= iou_threshold) {\n                            const float w"),
+    ("soft: linear weight iou instead of 1 - iou",
+     "const float w = 1.0f - iou;", "const float w = iou;"),
+    ("soft: gaussian without the square",
+     "double x = -((double)iou * (double)iou) / (double)sigma;",
+     "double x = -((double)iou) / (double)sigma;"),
+    ("soft: gaussian multiplied by sigma",
+     "double x = -((double)iou * (double)iou) / (double)sigma;",
+     "double x = -((double)iou * (double)iou) * (double)sigma;"),
+    ("soft: exp series cut to three terms",
+     "for (int n = 16; n >= 1; --n)", "for (int n = 3; n >= 1; --n)"),
+    ("soft: exp without squaring back",
+     "    for (int i = 0; i < k; ++i)\n        e = e * e;\n", ""),
+    ("soft: equal current scores go to the later rank",
+     "nms_rank_key(cur[r]) < nms_rank_key(cur[best])",
+     "nms_rank_key(cur[r]) <= nms_rank_key(cur[best])"),
+    ("soft: output score is the input score",
+     "so[kept] = cur[best];", "so[kept] = scores[m];"),
+    ("soft: a score equal to the threshold is dropped",
+     "if (cur[r] < score_threshold)", "if (cur[r] <= score_threshold)"),
+    ("batched: categories ignored",
+     "if (ci != c || !(scores[i] >= score_threshold))", "if (!(scores[i] >= score_threshold))"),
+    ("batched: no score threshold",
+     "if (ci != c || !(scores[i] >= score_threshold))", "if (ci != c)"),
+    ("batched hard: suppression at IoU equal to the threshold",
+     "boxes + 4 * (int64_t)it[q].idx) > iou_threshold)",
+     "boxes + 4 * (int64_t)it[q].idx) >= iou_threshold)"),
+    ("batched hard: removed boxes still suppress",
+     "            for (int32_t r = 0; r < n && kept < max_keep; ++r) {\n                if (!alive[r])\n                    continue;\n",
+     "            for (int32_t r = 0; r < n && kept < max_keep; ++r) {\n                if (!alive[r] && r < 0)\n                    continue;\n"),
 ]
 
 
