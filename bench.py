@@ -58,7 +58,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle work timed for the CPU baseline (seconds)")
     ap.add_argument("--calibrate-copy", action="store_true")
-    ap.add_argument("--op", default="align", choices=["align", "pool", "heads", "deform", "nms"],
+    ap.add_argument("--op", default="align",
+                    choices=["align", "pool", "heads", "deform", "nms", "select"],
                     help="align: RoIAlign (the benchmark); pool: RoI max pooling on the same "
                          "workload (plan, roi_pool_fwd, roi_pool_bwd with clearing); heads: "
                          "box and mask heads on one pyramid (workload 2: the batch-2 box and "
@@ -66,12 +67,15 @@ def parse():
                          "backward, timed against two separate backward calls; deform: "
                          "modulated deformable RoI pooling on the workload (offsets "
                          "N(0, 0.3^2), modulation U(0, 1), gamma 0.1); nms: greedy NMS of "
-                         "two images of 4096 scored proposals in one call (IoU 0.7)")
+                         "two images of 4096 scored proposals in one call (IoU 0.7); "
+                         "select: per-image proposal selection of a batch of 16 images x "
+                         "2000 proposals in one call (greedy NMS at IoU 0.7 keeping up to "
+                         "1000 per image; Soft-NMS linear and Gaussian timed beside it)")
     return ap.parse_args()
 
 
 ALL_SOURCES = ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip",
-               "deform.hip", "nms.hip", "api.hip")
+               "deform.hip", "nms.hip", "select.hip", "api.hip")
 # the sources a kernel's code comes from (its device code and the shared headers)
 KERNEL_SOURCES = {"fwd": ("common.hpp", "internal.hpp", "fwd.hip"),
                   "bwd_gather": ("common.hpp", "internal.hpp", "bwd.hip"),
@@ -172,6 +176,9 @@ def main():
         return
     if args.op == "nms":
         main_nms(args)
+        return
+    if args.op == "select":
+        main_select(args)
         return
 
     import torch
@@ -791,6 +798,111 @@ def main_nms(args):
                      "launch_ms": round(ms, 5)},
         "cpu_baseline": cpu,
         "extra": {"kernel_source_hash": kernel_source_hash()},
+    }
+    print(json.dumps(result), flush=True)
+
+
+def select_pair_tests(scores, cats, keep, num_keep, n_categories):
+    """Box pairs the greedy selection tests: per category, each block of 64 candidates
+    (rank order) against the boxes kept before it, plus the pairs inside the block."""
+    total = 0
+    for c in range(n_categories):
+        idx = np.flatnonzero(cats == c)
+        u = scores[idx].view(np.uint32).astype(np.uint64)
+        asc = np.where(u & 0x80000000, (~u) & 0xFFFFFFFF, u | 0x80000000)
+        order = idx[np.lexsort((idx, (~asc) & 0xFFFFFFFF))]
+        pos = {int(i): r for r, i in enumerate(order)}
+        kept_pos = np.sort([pos[int(i)] for i in keep[c, :num_keep[c]]])
+        for b0 in range(0, len(order), 64):
+            nb = min(64, len(order) - b0)
+            total += nb * int(np.searchsorted(kept_pos, b0)) + nb * (nb - 1) // 2
+            if np.searchsorted(kept_pos, b0 + nb) >= len(kept_pos) and \
+                    len(kept_pos) == keep.shape[1]:
+                break
+    return total
+
+
+def main_select(args):
+    """Per-image proposal selection of a training batch: 16 images x 2000 scored
+    proposals (synthetic RPN output: uniform centres, log-uniform sides, 30% jittered
+    duplicates) in one box_nms_batched call, greedy NMS at IoU 0.7 keeping up to 1000
+    per image (the RPN's post-NMS count); Soft-NMS (linear at 0.3, Gaussian sigma 0.5,
+    score threshold 0.05, 100 per image) timed beside it.  One step is one call."""
+    import torch
+
+    import oracle
+    import paper_1906_07155_amd as rex
+    from paper_1906_07155_amd import workloads
+
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(workloads.BASE_SEED + 70)
+    n_img, per = 16, 2000
+    boxes_np, scores_np, cats_np = workloads.draw_proposals(rng, n_img, per)
+    perm = rng.permutation(boxes_np.shape[0])        # images interleaved in the input
+    boxes_np, scores_np, cats_np = boxes_np[perm], scores_np[perm], cats_np[perm]
+    N = boxes_np.shape[0]
+    b = torch.from_numpy(boxes_np).to(dev)
+    sc = torch.from_numpy(scores_np).to(dev)
+    ct = torch.from_numpy(cats_np).to(dev)
+    stream = torch.cuda.current_stream()
+    cfgs = {"hard": dict(method="hard", iou_threshold=0.7, max_keep=1000),
+            "linear": dict(method="linear", iou_threshold=0.3, score_threshold=0.05,
+                           max_keep=100),
+            "gaussian": dict(method="gaussian", sigma=0.5, score_threshold=0.05, max_keep=100)}
+
+    def timed(cfg, steps):
+        out = rex.box_nms_batched(b, sc, ct, n_img, **cfg)
+        for _ in range(args.warmup):
+            rex.box_nms_batched(b, sc, ct, n_img, keep=out[0], kept_scores=out[1],
+                                num_keep=out[2], **cfg)
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(steps):
+            rex.box_nms_batched(b, sc, ct, n_img, keep=out[0], kept_scores=out[1],
+                                num_keep=out[2], **cfg)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / steps, [o.cpu().numpy() for o in out]
+
+    ms, (keep, ks, nk) = timed(cfgs["hard"], args.steps)
+    soft = {}
+    for name in ("linear", "gaussian"):
+        m, (k2, s2, n2) = timed(cfgs[name], max(1, args.steps // 4))
+        soft[name] = {"ms_per_call": round(m, 5), "boxes_per_s": round(N / (m * 1e-3), 1),
+                      "kept_per_image": int(n2.mean())}
+    pairs = select_pair_tests(scores_np, cats_np, keep, nk, n_img)
+    flops = pairs * 16          # about 16 fp32 operations per IoU test
+    achieved = flops / (ms * 1e-3) / 1e12
+    cpu = None
+    if not args.no_cpu_baseline:
+        lib = oracle.load()
+        elapsed, passes = 0.0, 0
+        while elapsed < args.cpu_seconds:
+            c0 = time.perf_counter()
+            oracle.nms_batched(boxes_np, scores_np, cats_np, n_img, "hard", 0.7, max_keep=1000,
+                               lib=lib)
+            elapsed += time.perf_counter() - c0
+            passes += 1
+        cpu = {"value": round(N * passes / elapsed, 1), "unit": "boxes/s", "cores": 1,
+               "kind": "oracle", "sample": "all %d boxes (greedy, IoU 0.7), %d passes in %.1f s "
+               "wall" % (N, passes, elapsed)}
+    result = {
+        "metric": "per-image proposal selection boxes/sec (greedy NMS, batch of 16 images)",
+        "value": round(N / (ms * 1e-3), 1), "unit": "boxes/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (uniform centres, log-uniform sizes, jittered duplicates, uniform "
+                "scores; no COCO)",
+        "config": {"workload": "16 images x 2000 proposals, greedy NMS IoU 0.7, up to 1000 "
+                               "per image", "num_boxes": N, "kept_per_image": int(nk.mean())},
+        "roofline": {"bound": "alu", "achieved": round(achieved, 4), "peak": 157.3,
+                     "unit": "TFLOP/s", "frac": round(achieved / 157.3, 6), "traffic": None,
+                     "kernel": "box_nms_batched (5 launches)", "flops_per_launch": flops,
+                     "iou_tests": pairs, "launch_ms": round(ms, 5)},
+        "cpu_baseline": cpu,
+        "extra": {"soft_nms": soft, "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(result), flush=True)
 

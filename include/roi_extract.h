@@ -369,6 +369,56 @@ re_status_t box_nms(const float *boxes, const float *scores, const int32_t *cate
                     int32_t *num_keep_out, void *workspace, size_t workspace_bytes,
                     void *stream);
 
+/* f4 -- per-category proposal selection: greedy NMS or Soft-NMS over a batch in one
+ * call.  A two-stage detector selects proposals per image (and detections per class)
+ * with NMS before extracting their RoI features; the paper runs these bbox operations
+ * on the GPU (§1) and lists Soft-NMS among its general modules (§2).  Each box belongs
+ * to one category (an image, or an image and class), and categories never interact.
+ * For every category c in [0, num_categories):
+ *   candidates: the boxes of category c whose score is >= score_threshold (a NaN score,
+ *     or a category outside the range, never is), ranked by score as in box_nms (IEEE
+ *     total order of the bits, highest first; equal scores by index);
+ *   RE_NMS_HARD: greedy NMS over the candidates in rank order -- a box is kept unless
+ *     a kept box overlaps it with IoU > iou_threshold (IoU as in box_nms);
+ *   RE_NMS_LINEAR / RE_NMS_GAUSSIAN (Soft-NMS): while candidates remain and fewer than
+ *     max_keep are kept, the candidate with the largest current score (same order;
+ *     equal current scores by rank) is output with that score and removed, and every
+ *     remaining candidate is decayed, s = s * w rounded to binary32, with
+ *       linear:   w = 1 - iou when iou > iou_threshold (else s is unchanged),
+ *       gaussian: w = exp(-iou^2 / sigma) evaluated in double by scaling and squaring
+ *                 (halve the argument into [-1/2, 0], degree-16 Taylor polynomial in
+ *                 Horner form, square back; 0 below -128), rounded to binary32;
+ *     a NaN IoU leaves s unchanged; a candidate whose score falls below
+ *     score_threshold is dropped.
+ * Outputs (dense, [num_categories][max_keep]): keep_out = the kept box indices of each
+ * category in selection order (RE_NMS_HARD: rank order), then -1; scores_out = the
+ * score of each at its selection (RE_NMS_HARD: its input score), then 0; num_keep_out
+ * [num_categories] = the number kept (<= max_keep).
+ *   boxes: device float[num_boxes][4] (x1, y1, x2, y2); scores: device float[num_boxes];
+ *   categories: device int32[num_boxes], or NULL with num_categories == 1;
+ *   num_boxes in [0, RE_MAX_NMS_BATCH_BOXES]; num_categories in [1, RE_MAX_NMS_CATEGORIES];
+ *   iou_threshold, score_threshold not NaN; sigma finite > 0 (RE_NMS_GAUSSIAN);
+ *   max_keep >= 0 with max_keep * num_categories < 2^31;
+ *   workspace: device, 256-byte aligned, box_nms_batched_workspace_size() bytes (about
+ *   48 bytes per box).
+ * A category is handled by one workgroup: its candidates are sorted in LDS up to 8192
+ * (above that in the workspace, slower); greedy selection tests blocks of 64 candidates
+ * against the growing kept list, Soft-NMS runs one workgroup-wide iteration per
+ * selection. */
+#define RE_NMS_HARD 0
+#define RE_NMS_LINEAR 1
+#define RE_NMS_GAUSSIAN 2
+#define RE_MAX_NMS_BATCH_BOXES (1 << 24)
+#define RE_MAX_NMS_CATEGORIES 8192
+re_status_t box_nms_batched_workspace_size(int64_t num_boxes, int32_t num_categories,
+                                           size_t *bytes);
+re_status_t box_nms_batched(const float *boxes, const float *scores, const int32_t *categories,
+                            int64_t num_boxes, int32_t num_categories, int32_t method,
+                            float iou_threshold, float sigma, float score_threshold,
+                            int32_t max_keep, int32_t *keep_out, float *scores_out,
+                            int32_t *num_keep_out, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
 /* Static description of a status code. */
 const char *roi_extract_status_str(re_status_t status);
 

@@ -25,6 +25,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "roi_extract.h")
 RE_OK, RE_ERR_INVALID_ARG, RE_ERR_UNSUPPORTED, RE_ERR_WORKSPACE, RE_ERR_DEVICE = range(5)
 RE_DTYPE_F32, RE_DTYPE_BF16 = 0, 1
 BWD_AUTO, BWD_SCATTER, BWD_GATHER = 0, 1, 2
+NMS_METHODS = {"hard": 0, "linear": 1, "gaussian": 2}   # RE_NMS_HARD / _LINEAR / _GAUSSIAN
 _BWD_ALGOS = {"auto": BWD_AUTO, "scatter": BWD_SCATTER, "gather": BWD_GATHER}
 MAX_LEVELS = 8
 
@@ -80,6 +81,9 @@ SIGNATURES = {
                             _I32, _VP, _VP, _F32, _I32, _VP, _VP, _VP, _SZ, _VP],
     "box_nms_workspace_size": [_I64, ctypes.POINTER(_SZ)],
     "box_nms": [_VP, _VP, _VP, _I64, _F32, _I64, _VP, _VP, _VP, _SZ, _VP],
+    "box_nms_batched_workspace_size": [_I64, _I32, ctypes.POINTER(_SZ)],
+    "box_nms_batched": [_VP, _VP, _VP, _I64, _I32, _I32, _F32, _F32, _F32, _I32, _VP, _VP, _VP,
+                        _VP, _SZ, _VP],
     "roi_pool_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _VP, _I32, _VP, _VP, _SZ, _VP],
     "roi_pool_bwd": [_VP, _I32, _VP, _VP, _I64, _VP, _I32, _I32, _LEVELS, _I32, _I32, _VP, _SZ,
                      _VP],
@@ -606,3 +610,64 @@ def box_nms(boxes, scores, iou_threshold: float, categories=None, max_keep: int 
                         float(iou_threshold), mk, keep.data_ptr(), num_keep.data_ptr(),
                         ws, wsb, stream_handle(stream)), "box_nms")
     return keep[:min(N, mk)], num_keep
+
+
+def box_nms_batched(boxes, scores, categories=None, num_categories: int = 1,
+                    method: str = "hard", iou_threshold: float = 0.5, sigma: float = 0.5,
+                    score_threshold: float = float("-inf"), max_keep: int | None = None,
+                    workspace=None, keep=None, kept_scores=None, num_keep=None, stream=None):
+    """Per-category proposal selection on the GPU: greedy NMS ("hard") or Soft-NMS
+    ("linear", "gaussian").  Returns (keep int32 [C, max_keep]: kept indices of each
+    category in selection order then -1, kept_scores float32 [C, max_keep]: score at
+    selection then 0, num_keep int32 [C]); all stay on the device."""
+    torch = _torch()
+    if method not in NMS_METHODS:
+        raise ValueError("method must be one of %s" % sorted(NMS_METHODS))
+    if scores.dtype != torch.float32 or scores.dim() != 1 or not scores.is_contiguous():
+        raise ValueError("scores must be a contiguous float32 [N] tensor")
+    N = scores.shape[0]
+    if boxes.dtype != torch.float32 or tuple(boxes.shape) != (N, 4) or not boxes.is_contiguous():
+        raise ValueError("boxes must be a contiguous float32 [N, 4] tensor")
+    if categories is not None and (categories.dtype != torch.int32 or
+                                   tuple(categories.shape) != (N,) or
+                                   not categories.is_contiguous()):
+        raise ValueError("categories must be a contiguous int32 [N] tensor")
+    C = int(num_categories)
+    mk = N if max_keep is None else int(max_keep)
+    if mk < 0:
+        raise ValueError("max_keep must be >= 0")
+    for t, name, dt, shape in ((keep, "keep", torch.int32, (C, mk)),
+                               (kept_scores, "kept_scores", torch.float32, (C, mk)),
+                               (num_keep, "num_keep", torch.int32, (C,))):
+        if t is not None and (t.dtype != dt or tuple(t.shape) != shape or not t.is_contiguous()):
+            raise ValueError("%s must be a contiguous %s tensor of shape %s" % (name, dt, shape))
+    if workspace is not None:
+        _workspace(workspace, boxes)
+    _need_cuda(boxes, "boxes")
+    for t, name in ((scores, "scores"), (categories, "categories"), (keep, "keep"),
+                    (kept_scores, "kept_scores"), (num_keep, "num_keep"),
+                    (workspace, "workspace")):
+        if t is not None:
+            _need_cuda(t, name, boxes)
+    n = ctypes.c_size_t(0)
+    check(lib().box_nms_batched_workspace_size(N, C, ctypes.byref(n)),
+          "box_nms_batched_workspace_size")
+    dev = boxes.device
+    if workspace is None:
+        workspace = torch.empty(n.value, dtype=torch.uint8, device=dev)
+    if keep is None:
+        keep = torch.empty((C, mk), dtype=torch.int32, device=dev)
+    if kept_scores is None:
+        kept_scores = torch.empty((C, mk), dtype=torch.float32, device=dev)
+    if num_keep is None:
+        num_keep = torch.empty(C, dtype=torch.int32, device=dev)
+    ws, wsb = _workspace(workspace, boxes)
+    check(lib().box_nms_batched(boxes.data_ptr(), scores.data_ptr(),
+                                categories.data_ptr() if categories is not None else None, N, C,
+                                NMS_METHODS[method], float(iou_threshold), float(sigma),
+                                float(score_threshold), mk,
+                                keep.data_ptr() if mk * C > 0 else None,
+                                kept_scores.data_ptr() if mk * C > 0 else None,
+                                num_keep.data_ptr(), ws, wsb, stream_handle(stream)),
+          "box_nms_batched")
+    return keep, kept_scores, num_keep

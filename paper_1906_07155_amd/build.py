@@ -18,7 +18,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIBRARY = os.path.join(HERE, "libroi_extract.so")
-SOURCES = ["api.hip", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip", "deform.hip", "nms.hip"]
+SOURCES = ["api.hip", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip", "deform.hip", "nms.hip",
+           "select.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",

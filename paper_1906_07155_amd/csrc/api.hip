@@ -904,7 +904,7 @@ namespace {
 struct NmsLayout {
     size_t order, sboxes, scats, mask, total;
 };
-NmsLayout nms_layout(int64_t N) {
+static NmsLayout nms_layout(int64_t N) {
     NmsLayout L{};
     const int64_t nw = (N + 63) / 64;
     L.order = 0;
@@ -958,6 +958,88 @@ re_status_t box_nms(const float *boxes, const float *scores, const int32_t *cate
     a.N = static_cast<int32_t>(num_boxes);
     a.nw = static_cast<int32_t>((num_boxes + 63) / 64);
     return from_hip(launch_nms(a, static_cast<hipStream_t>(stream)));
+}
+
+// ---------------------------------------------------------------------------
+// Per-category proposal selection
+// ---------------------------------------------------------------------------
+
+namespace {
+struct NmsBatchLayout {
+    size_t count, start, sidx, skey, sbox, sscore, kbox, total;
+};
+static NmsBatchLayout nmsb_layout(int64_t N, int32_t C) {
+    NmsBatchLayout L{};
+    const size_t n = static_cast<size_t>(std::max<int64_t>(N, 1));
+    L.count = 0;
+    L.start = align256(static_cast<size_t>(C) * 4);
+    L.sidx = L.start + align256(static_cast<size_t>(C + 1) * 4);
+    L.skey = L.sidx + align256(n * 4);
+    L.sbox = L.skey + align256(n * 8);
+    L.sscore = L.sbox + align256(n * 16);
+    L.kbox = L.sscore + align256(n * 4);
+    L.total = L.kbox + align256(n * 16);
+    return L;
+}
+static bool nmsb_sizes_ok(int64_t N, int32_t C) {
+    return N >= 0 && N <= RE_MAX_NMS_BATCH_BOXES && C >= 1 && C <= RE_MAX_NMS_CATEGORIES;
+}
+}  // namespace
+
+re_status_t box_nms_batched_workspace_size(int64_t num_boxes, int32_t num_categories,
+                                           size_t *bytes) {
+    if (!bytes || !nmsb_sizes_ok(num_boxes, num_categories)) return RE_ERR_INVALID_ARG;
+    *bytes = nmsb_layout(num_boxes, num_categories).total;
+    return RE_OK;
+}
+
+re_status_t box_nms_batched(const float *boxes, const float *scores, const int32_t *categories,
+                            int64_t num_boxes, int32_t num_categories, int32_t method,
+                            float iou_threshold, float sigma, float score_threshold,
+                            int32_t max_keep, int32_t *keep_out, float *scores_out,
+                            int32_t *num_keep_out, void *workspace, size_t workspace_bytes,
+                            void *stream) {
+    if (!nmsb_sizes_ok(num_boxes, num_categories)) return RE_ERR_INVALID_ARG;
+    if (!categories && num_categories != 1) return RE_ERR_INVALID_ARG;
+    if (method != RE_NMS_HARD && method != RE_NMS_LINEAR && method != RE_NMS_GAUSSIAN)
+        return RE_ERR_INVALID_ARG;
+    if (std::isnan(iou_threshold) || std::isnan(score_threshold)) return RE_ERR_INVALID_ARG;
+    if (method == RE_NMS_GAUSSIAN && (!std::isfinite(sigma) || !(sigma > 0.0f)))
+        return RE_ERR_INVALID_ARG;
+    if (max_keep < 0 || int64_t(max_keep) * num_categories > INT32_MAX) return RE_ERR_INVALID_ARG;
+    if (!num_keep_out) return RE_ERR_INVALID_ARG;
+    if (max_keep > 0 && (!keep_out || !scores_out)) return RE_ERR_INVALID_ARG;
+    if (num_boxes > 0 && (!boxes || !scores)) return RE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(boxes) % 4 || reinterpret_cast<uintptr_t>(scores) % 4 ||
+        reinterpret_cast<uintptr_t>(categories) % 4 || reinterpret_cast<uintptr_t>(keep_out) % 4 ||
+        reinterpret_cast<uintptr_t>(scores_out) % 4 || reinterpret_cast<uintptr_t>(num_keep_out) % 4)
+        return RE_ERR_INVALID_ARG;
+    const NmsBatchLayout lay = nmsb_layout(num_boxes, num_categories);
+    if (!workspace || reinterpret_cast<uintptr_t>(workspace) % 256) return RE_ERR_WORKSPACE;
+    if (workspace_bytes < lay.total) return RE_ERR_WORKSPACE;
+    char *ws = static_cast<char *>(workspace);
+    NmsBatchArgs a{};
+    a.boxes = boxes;
+    a.scores = scores;
+    a.categories = categories;
+    a.keep = keep_out;
+    a.kept_scores = scores_out;
+    a.num_keep = num_keep_out;
+    a.count = reinterpret_cast<int32_t *>(ws + lay.count);
+    a.start = reinterpret_cast<int32_t *>(ws + lay.start);
+    a.sidx = reinterpret_cast<int32_t *>(ws + lay.sidx);
+    a.skey = reinterpret_cast<uint64_t *>(ws + lay.skey);
+    a.sbox = reinterpret_cast<float4 *>(ws + lay.sbox);
+    a.sscore = reinterpret_cast<float *>(ws + lay.sscore);
+    a.kbox = reinterpret_cast<float4 *>(ws + lay.kbox);
+    a.N = static_cast<int32_t>(num_boxes);
+    a.C = num_categories;
+    a.method = method;
+    a.max_keep = max_keep;
+    a.iou_threshold = iou_threshold;
+    a.sigma = sigma;
+    a.score_threshold = score_threshold;
+    return from_hip(launch_nms_batched(a, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

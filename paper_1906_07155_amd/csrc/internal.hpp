@@ -211,6 +211,108 @@ struct NmsArgs {
 
 hipError_t launch_nms(NmsArgs a, hipStream_t stream);
 
+// Rank key of a score: IEEE total order of the bits, largest first; NaN after every
+// number.
+__device__ __forceinline__ uint32_t nms_key(float s) {
+    const uint32_t u = __float_as_uint(s);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0xffffffffu;
+    const uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ~asc;
+}
+
+// Binary32 IoU, one rounding per operation in the order of the definition.
+__device__ __forceinline__ float nms_iou(float4 a, float4 b) {
+    const float ix1 = fmaxf(a.x, b.x);
+    const float iy1 = fmaxf(a.y, b.y);
+    const float ix2 = fminf(a.z, b.z);
+    const float iy2 = fminf(a.w, b.w);
+    float iw = ix2 - ix1;
+    float ih = iy2 - iy1;
+    iw = fmaxf(iw, 0.0f);
+    ih = fmaxf(ih, 0.0f);
+    const float inter = iw * ih;
+    const float wa = a.z - a.x;
+    const float ha = a.w - a.y;
+    const float wb = b.z - b.x;
+    const float hb = b.w - b.y;
+    const float area_a = wa * ha;
+    const float area_b = wb * hb;
+    const float sum = area_a + area_b;
+    const float uni = sum - inter;
+    return inter / uni;
+}
+
+// Per-category proposal selection (greedy NMS or Soft-NMS), many categories per call.
+constexpr int kNmsHard = 0, kNmsLinear = 1, kNmsGaussian = 2;
+
+struct NmsBatchArgs {
+    const float *boxes;          // [N][4]
+    const float *scores;         // [N]
+    const int32_t *categories;   // [N] or null (one category)
+    int32_t *keep;               // [C][max_keep]
+    float *kept_scores;          // [C][max_keep]
+    int32_t *num_keep;           // [C]
+    // workspace
+    int32_t *count;              // [C] candidates per category, then the placement cursor
+    int32_t *start;              // [C + 1] first sorted position of each category
+    int32_t *sidx;               // [N] box index of every sorted position
+    uint64_t *skey;              // [N] sort keys (categories too long for LDS)
+    float4 *sbox;                // [N] boxes in sorted order
+    float *sscore;               // [N] scores in sorted order (Soft-NMS: current scores)
+    float4 *kbox;                // [N] kept boxes of each category (greedy)
+    int32_t N, C;
+    int32_t method;
+    int32_t max_keep;
+    float iou_threshold, sigma, score_threshold;
+    int32_t pad;
+};
+
+hipError_t launch_nms_batched(const NmsBatchArgs &a, hipStream_t stream);
+
+// Inclusive prefix sum across the 64 lanes of a wavefront.
+__device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int t = __shfl_up(v, off);
+        if (lane >= off) v += t;
+    }
+    return v;
+}
+
+// Exclusive scan of hist[0, n) in place by the whole workgroup: per-thread chunk
+// sums, a wavefront scan of the sums, a scan of the wavefront totals by wave 0,
+// then the chunk prefixes.  part[] holds the wavefront totals.  Returns the total.
+__device__ __forceinline__ int block_exclusive_scan(int32_t *hist, int n, int32_t *part) {
+    constexpr int kWaves = kPlanThreads / 64;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int per = (n + kPlanThreads - 1) / kPlanThreads;
+    const int lo = min(tid * per, n);
+    const int hi = min(lo + per, n);
+    int s = 0;
+    for (int i = lo; i < hi; ++i) s += hist[i];
+    const int incl = wave_inclusive_scan(s, lane);
+    if (lane == 63) part[wave] = incl;
+    __syncthreads();
+    if (wave == 0) {
+        const int w = lane < kWaves ? part[lane] : 0;
+        const int wi = wave_inclusive_scan(w, lane);
+        if (lane < kWaves) part[kWaves + lane] = wi - w;   // exclusive wave prefix
+        if (lane == kWaves - 1) part[2 * kWaves] = wi;     // total
+    }
+    __syncthreads();
+    int run = part[kWaves + wave] + incl - s;
+    for (int i = lo; i < hi; ++i) {
+        const int c = hist[i];
+        hist[i] = run;
+        run += c;
+    }
+    const int total = part[2 * kWaves];
+    __syncthreads();
+    return total;
+}
+
 hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float finest_scale,
                             int32_t box_plus1, int32_t *out, hipStream_t stream);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);

@@ -26,37 +26,6 @@ namespace rex {
 
 constexpr int kNmsSortThreads = 1024;
 
-// Rank key of a score: IEEE total order of the bits, largest first; NaN after every
-// number.
-__device__ __forceinline__ uint32_t nms_key(float s) {
-    const uint32_t u = __float_as_uint(s);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0xffffffffu;
-    const uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-    return ~asc;
-}
-
-// Binary32 IoU, one rounding per operation in the order of the definition.
-__device__ __forceinline__ float nms_iou(float4 a, float4 b) {
-    const float ix1 = fmaxf(a.x, b.x);
-    const float iy1 = fmaxf(a.y, b.y);
-    const float ix2 = fminf(a.z, b.z);
-    const float iy2 = fminf(a.w, b.w);
-    float iw = ix2 - ix1;
-    float ih = iy2 - iy1;
-    iw = fmaxf(iw, 0.0f);
-    ih = fmaxf(ih, 0.0f);
-    const float inter = iw * ih;
-    const float wa = a.z - a.x;
-    const float ha = a.w - a.y;
-    const float wb = b.z - b.x;
-    const float hb = b.w - b.y;
-    const float area_a = wa * ha;
-    const float area_b = wb * hb;
-    const float sum = area_a + area_b;
-    const float uni = sum - inter;
-    return inter / uni;
-}
-
 __global__ __launch_bounds__(kNmsSortThreads) void nms_sort_kernel(NmsArgs a) {
     __shared__ uint64_t items[kNmsMaxBoxes];
     const int N = a.N;

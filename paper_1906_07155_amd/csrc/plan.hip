@@ -53,50 +53,6 @@ __device__ __forceinline__ void load_tab(const PlanArgs &a, LevelTab &t) {
     }
 }
 
-// Inclusive prefix sum across the 64 lanes of a wavefront.
-__device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int t = __shfl_up(v, off);
-        if (lane >= off) v += t;
-    }
-    return v;
-}
-
-// Exclusive scan of hist[0, n) in place by the whole workgroup: per-thread chunk
-// sums, a wavefront scan of the sums, a scan of the wavefront totals by wave 0,
-// then the chunk prefixes.  part[] holds the wavefront totals.  Returns the total.
-__device__ int block_exclusive_scan(int32_t *hist, int n, int32_t *part) {
-    constexpr int kWaves = kPlanThreads / 64;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int per = (n + kPlanThreads - 1) / kPlanThreads;
-    const int lo = min(tid * per, n);
-    const int hi = min(lo + per, n);
-    int s = 0;
-    for (int i = lo; i < hi; ++i) s += hist[i];
-    const int incl = wave_inclusive_scan(s, lane);
-    if (lane == 63) part[wave] = incl;
-    __syncthreads();
-    if (wave == 0) {
-        const int w = lane < kWaves ? part[lane] : 0;
-        const int wi = wave_inclusive_scan(w, lane);
-        if (lane < kWaves) part[kWaves + lane] = wi - w;   // exclusive wave prefix
-        if (lane == kWaves - 1) part[2 * kWaves] = wi;     // total
-    }
-    __syncthreads();
-    int run = part[kWaves + wave] + incl - s;
-    for (int i = lo; i < hi; ++i) {
-        const int c = hist[i];
-        hist[i] = run;
-        run += c;
-    }
-    const int total = part[2 * kWaves];
-    __syncthreads();
-    return total;
-}
-
 // Bin-tiles met by a conservative box around the footprint of a RoI on its level.
 // Every sample of the RoI lies between the (shifted) box edges for any output size,
 // sampling ratio and alignment; taps add one pixel, and a 1.5-pixel margin absorbs

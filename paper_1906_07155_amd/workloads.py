@@ -107,6 +107,32 @@ def add_duplicates(rng: np.random.Generator, rois: np.ndarray, frac: float,
     return r
 
 
+def draw_proposals(rng: np.random.Generator, n_images: int, per_image: int,
+                   img_hw: Tuple[int, int] = (800, 1333), size_range=(8.0, 600.0),
+                   dup: float = 0.3):
+    """Scored proposals of a batch, the input of NMS (a synthetic stand-in for a dense
+    head's output): centres uniform in the image, log-uniform sides, a share `dup` of
+    slots overwritten with copies of other boxes jittered by up to 10% of their size
+    (the heavy overlaps NMS exists for), clipped to the image; scores uniform in [0, 1).
+    Returns (boxes float32 [N, 4], scores float32 [N], image index int32 [N]), the
+    images' boxes contiguous."""
+    H, W = img_hw
+    lo, hi = size_range
+    N = n_images * per_image
+    cx, cy = rng.uniform(0, W, N), rng.uniform(0, H, N)
+    w = np.exp(rng.uniform(np.log(lo), np.log(hi), N))
+    h = np.exp(rng.uniform(np.log(lo), np.log(hi), N))
+    boxes = np.stack([cx - w / 2, cy - h / 2, cx + w / 2, cy + h / 2], 1)
+    nd = int(dup * N)
+    src = rng.integers(0, N, nd)
+    dst = rng.choice(N, nd, replace=False)
+    boxes[dst] = boxes[src] + rng.uniform(-0.1, 0.1, (nd, 4)) * np.stack([w[src], h[src]] * 2, 1)
+    boxes = np.clip(boxes, 0, [W, H, W, H]).astype(np.float32)
+    scores = rng.uniform(0, 1, N).astype(np.float32)
+    images = np.repeat(np.arange(n_images, dtype=np.int32), per_image)
+    return boxes, scores, images
+
+
 def draw_features(rng: np.random.Generator, n: int, c: int,
                   level_hw: List[Tuple[int, int]], dtype: str) -> List[np.ndarray]:
     """Standard-normal NCHW maps.  dtype 'f32' -> float32, 'bf16' -> uint16 bf16 bits."""

@@ -327,3 +327,38 @@ def test_nms_validation(L):
     assert nms(ws=None) == WORKSPACE
     assert nms(ws=FAKE + 64) == WORKSPACE
     assert nms(wsb=16) == WORKSPACE
+
+
+def test_nms_batched_validation(L):
+    n = ctypes.c_size_t(0)
+    assert L.box_nms_batched_workspace_size(1000, 16, ctypes.byref(n)) == OK
+    assert n.value >= 1000 * 48 and n.value % 256 == 0
+    assert L.box_nms_batched_workspace_size(-1, 16, ctypes.byref(n)) == INVALID
+    assert L.box_nms_batched_workspace_size(10, 0, ctypes.byref(n)) == INVALID
+    assert L.box_nms_batched_workspace_size(10, 8193, ctypes.byref(n)) == INVALID
+    assert L.box_nms_batched_workspace_size((1 << 24) + 1, 1, ctypes.byref(n)) == INVALID
+    assert L.box_nms_batched_workspace_size(10, 4, None) == INVALID
+    assert L.box_nms_batched_workspace_size(1000, 16, ctypes.byref(n)) == OK
+
+    def call(N=1000, C=16, boxes=FAKE, scores=FAKE, cats=FAKE, method=0, thr=0.5, sigma=0.5,
+             st=-math.inf, mk=100, keep=FAKE, ks=FAKE, nk=FAKE, ws=FAKE, wsb=None):
+        return L.box_nms_batched(boxes, scores, cats, N, C, method, thr, sigma, st, mk, keep, ks,
+                                 nk, ws, n.value if wsb is None else wsb, None)
+
+    assert call(C=0) == INVALID
+    assert call(cats=None) == INVALID               # several categories need the array
+    assert call(method=3) == INVALID
+    assert call(thr=math.nan) == INVALID
+    assert call(st=math.nan) == INVALID
+    assert call(method=2, sigma=0.0) == INVALID
+    assert call(method=2, sigma=math.inf) == INVALID
+    assert call(mk=-1) == INVALID
+    assert call(mk=1 << 28) == INVALID              # max_keep * categories >= 2^31
+    assert call(nk=None) == INVALID
+    assert call(keep=None) == INVALID
+    assert call(ks=None) == INVALID
+    assert call(boxes=None) == INVALID
+    assert call(scores=FAKE + 2) == INVALID
+    assert call(ws=None) == WORKSPACE
+    assert call(ws=FAKE + 64) == WORKSPACE
+    assert call(wsb=256) == WORKSPACE
