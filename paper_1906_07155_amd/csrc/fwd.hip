@@ -5,9 +5,10 @@
 //
 // Two kernels:
 //   fwd_cl_kernel       channels-last levels (stride_c == 1), specialised output
-//                       grids.  One workgroup = one RoI x 1-4 slices of 64 channels;
-//                       lanes run over channels, so every pixel read is one
-//                       coalesced, channel-contiguous load.  The RoI's sample
+//                       grids.  One workgroup = one RoI x 1-4 slices of 64 channels
+//                       (128 for bf16 on the 7x7 grid, two channels per lane); lanes
+//                       run over channels, so every pixel read is one coalesced,
+//                       channel-contiguous load.  The RoI's sample
 //                       geometry is reduced once into LDS to its distinct tap rows
 //                       and columns with summed weights (the footprint), every
 //                       footprint pixel is loaded once, and the bins are formed as
@@ -28,6 +29,11 @@ namespace rex {
 #ifndef REX_FWD_CX
 #define REX_FWD_CX 8
 #endif
+// columns per load unit with two bf16 channels per lane (7x7 grid)
+#ifndef REX_FWD_CX2_BF16
+#define REX_FWD_CX2_BF16 8
+#endif
+
 constexpr int kFwdDepth = REX_FWD_DEPTH;
 constexpr int kFwdCX = REX_FWD_CX;
 
@@ -193,11 +199,47 @@ __device__ __forceinline__ int distinct_taps(const SampleTap *taps, int ns, int 
     return n;
 }
 
-// One workgroup per (RoI, run of spw slices of 64 channels); lane = channel.  Wave w owns bin
-// rows [w*RPW, min(PH, (w+1)*RPW)) and loads the distinct tap rows of those bin
-// rows times all distinct tap columns of the RoI, in chunks of CX columns, with
-// the next unit's loads issued before the current one is reduced.
-template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK>
+// Raw bits of CPL adjacent channels of one pixel: one load per pixel and lane (32 bits
+// for one binary32 or one or two bf16 values, 64 bits for two binary32 values), then
+// unpacked to binary32 when consumed.
+template <typename T, int CPL>
+struct RawPix {
+    static constexpr int W = (static_cast<int>(sizeof(T)) * CPL + 3) / 4;
+    uint32_t w[W];
+};
+
+template <typename T, int CPL>
+__device__ __forceinline__ void load_pix(__amdgpu_buffer_rsrc_t r, uint32_t off, RawPix<T, CPL> &p) {
+    if constexpr (sizeof(T) * CPL == 8) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+        p.w[0] = v[0];
+        p.w[1] = v[1];
+    } else if constexpr (sizeof(T) * CPL == 4) {
+        p.w[0] = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+    } else {
+        p.w[0] = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+    }
+}
+
+// Channel j of the pixel (the element at the lower address is channel 0).
+template <typename T, int CPL>
+__device__ __forceinline__ float unpack_pix(const RawPix<T, CPL> &p, int j) {
+    if constexpr (sizeof(T) == 4) {
+        return __uint_as_float(p.w[j]);
+    } else if constexpr (CPL == 1) {
+        return __uint_as_float(p.w[0] << 16);
+    } else {
+        return __uint_as_float(j == 0 ? (p.w[0] << 16) : (p.w[0] & 0xffff0000u));
+    }
+}
+
+// One workgroup per (RoI, run of spw slices of 64 * CPL channels); lane i holds channels
+// CPL*i .. CPL*i + CPL - 1 of the slice, adjacent in memory, so every pixel read is one
+// coalesced load per lane.  Wave w owns bin rows [w*RPW, min(PH, (w+1)*RPW)) and loads
+// the distinct tap rows of those bin rows times all distinct tap columns of the RoI, in
+// chunks of CX columns, with the next unit's loads issued before the current one is
+// reduced.
+template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK, int CPL>
 __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     constexpr int NB = PH * PW;
     constexpr int NR = PH * S;                   // sample rows
@@ -209,8 +251,9 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     constexpr int PWP = (PW + 3) & ~3;           // padded for 16-byte LDS reads
     constexpr int QH = (PW + 1) / 2;             // the bin columns' first half
     constexpr bool kHalves = PW >= 12;           // skip the halves a column misses
+    constexpr int SLICE = 64 * CPL;              // channels of one slice
     static_assert(NR + NCOL <= 256 && NCOL <= 64 && RPW * S <= 64 && MAXX <= 64, "geometry sizes");
-    static_assert(64 % CHK == 0 && CX % 4 == 0, "tiling");
+    static_assert(SLICE % CHK == 0 && CHK % CPL == 0 && CX % 4 == 0, "tiling");
 
     __shared__ SampleTap srow[NR];
     __shared__ SampleTap scol[NCOL];
@@ -314,7 +357,9 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     // The geometry above serves every slice of the workgroup.
     for (int slice = slice0; slice < slice1; ++slice) {
         if (slice > slice0) __syncthreads();   // the previous slice's output tile is stored
-        const int c = slice * 64 + lane;
+        // the lane's first channel; with CPL > 1 the channel count is a multiple of CPL,
+        // so a lane holds either all of its channels or none
+        const int c = slice * SLICE + lane * CPL;
         const bool lane_on = active && c < a.lv.C;
         // One buffer resource per image of the level; a lane with no channel reads out
         // of range (zeros) instead of branching.
@@ -328,33 +373,40 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
         // and reduced over rows first, H[x][p] = sum_y Wy[p][y] F[y][x]; at the end of
         // the chunk the columns are reduced into the bins, acc[p][q] += Wx[q][x] H[x][p].
         // Columns past the footprint read zeros (out-of-range offsets, zero weights).
-        float acc[RPW][PW];
-    #pragma unroll
-        for (int p = 0; p < RPW; ++p)
-    #pragma unroll
-            for (int q = 0; q < PW; ++q) acc[p][q] = 0.0f;
-        float H[CX][RPW];
-    #pragma unroll
-        for (int x = 0; x < CX; ++x)
-    #pragma unroll
-            for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
+        float acc[CPL][RPW][PW];
+#pragma unroll
+        for (int j = 0; j < CPL; ++j)
+#pragma unroll
+            for (int p = 0; p < RPW; ++p)
+#pragma unroll
+                for (int q = 0; q < PW; ++q) acc[j][p][q] = 0.0f;
+        float H[CPL][CX][RPW];
+#pragma unroll
+        for (int j = 0; j < CPL; ++j)
+#pragma unroll
+            for (int x = 0; x < CX; ++x)
+#pragma unroll
+                for (int p = 0; p < RPW; ++p) H[j][x][p] = 0.0f;
 
-        auto issue = [&](int ch, int yi, uint32_t (&v)[CX]) {
+        auto issue = [&](int ch, int yi, RawPix<T, CPL> (&v)[CX]) {
             const uint32_t rowb = vbase + s_yoff[wave][yi];
             const uint32_t *xo = s_xoff + ch * CX;
-    #pragma unroll
-            for (int x = 0; x < CX; ++x) v[x] = buf_load_raw<T>(res, rowb + xo[x]);
+#pragma unroll
+            for (int x = 0; x < CX; ++x) load_pix<T, CPL>(res, rowb + xo[x], v[x]);
         };
-        auto consume = [&](int ch, int yi, const uint32_t (&v)[CX]) {
+        auto consume = [&](int ch, int yi, const RawPix<T, CPL> (&v)[CX]) {
             const float *wy = s_wy[wave][yi];
-    #pragma unroll
+#pragma unroll
             for (int x = 0; x < CX; ++x) {
-                const float f = raw_to_f32<T>(v[x]);
-    #pragma unroll
-                for (int p = 0; p < RPW; ++p) H[x][p] = fmaf(wy[p], f, H[x][p]);
+#pragma unroll
+                for (int j = 0; j < CPL; ++j) {
+                    const float f = unpack_pix<T, CPL>(v[x], j);
+#pragma unroll
+                    for (int p = 0; p < RPW; ++p) H[j][x][p] = fmaf(wy[p], f, H[j][x][p]);
+                }
             }
             if (yi == ny - 1) {
-    #pragma unroll
+#pragma unroll
                 for (int x = 0; x < CX; ++x) {
                     const int col = ch * CX + x;
                     const float *wx = s_wx[col];
@@ -362,19 +414,27 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
                     // weights are zero); on the 7-wide grid the test costs more than the
                     // few products it saves
                     if (!kHalves || ((xlo >> col) & 1)) {
-    #pragma unroll
+#pragma unroll
                         for (int q = 0; q < QH; ++q)
-    #pragma unroll
-                            for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+#pragma unroll
+                            for (int j = 0; j < CPL; ++j)
+#pragma unroll
+                                for (int p = 0; p < RPW; ++p)
+                                    acc[j][p][q] = fmaf(wx[q], H[j][x][p], acc[j][p][q]);
                     }
                     if (!kHalves || ((xhi >> col) & 1)) {
-    #pragma unroll
+#pragma unroll
                         for (int q = QH; q < PW; ++q)
-    #pragma unroll
-                            for (int p = 0; p < RPW; ++p) acc[p][q] = fmaf(wx[q], H[x][p], acc[p][q]);
+#pragma unroll
+                            for (int j = 0; j < CPL; ++j)
+#pragma unroll
+                                for (int p = 0; p < RPW; ++p)
+                                    acc[j][p][q] = fmaf(wx[q], H[j][x][p], acc[j][p][q]);
                     }
-    #pragma unroll
-                    for (int p = 0; p < RPW; ++p) H[x][p] = 0.0f;
+#pragma unroll
+                    for (int j = 0; j < CPL; ++j)
+#pragma unroll
+                        for (int p = 0; p < RPW; ++p) H[j][x][p] = 0.0f;
                     // one column's weights live at a time
                     __builtin_amdgcn_sched_barrier(0);
                 }
@@ -386,7 +446,7 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
         // the ring size so every buffer index is a constant.
         constexpr int D = kFwdDepth;
         constexpr int NBUF = D + 1;
-        uint32_t v[NBUF][CX];
+        RawPix<T, CPL> v[NBUF][CX];
         const int units = ny * nch;
         int ic = 0, iy = 0;      // next unit to issue
         int cc = 0, cy = 0;      // next unit to consume
@@ -396,7 +456,7 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
                 ++ch;
             }
         };
-    #pragma unroll
+#pragma unroll
         for (int d = 0; d < D; ++d) {
             if (d < units) {
                 issue(ic, iy, v[d]);
@@ -404,15 +464,15 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
             }
         }
         for (int u0 = 0; u0 < units; u0 += NBUF) {
-    #pragma unroll
-            for (int j = 0; j < NBUF; ++j) {
-                if (u0 + j >= units) break;
-                if (u0 + j + D < units) {
-                    issue(ic, iy, v[(j + D) % NBUF]);
+#pragma unroll
+            for (int jj = 0; jj < NBUF; ++jj) {
+                if (u0 + jj >= units) break;
+                if (u0 + jj + D < units) {
+                    issue(ic, iy, v[(jj + D) % NBUF]);
                     step(ic, iy);
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                consume(cc, cy, v[j]);
+                consume(cc, cy, v[jj]);
                 step(cc, cy);
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -422,67 +482,76 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
         // dense products above, so a non-finite feature anywhere in the footprint shows
         // up as a non-finite output.
         uint32_t bad = 0;
-    #pragma unroll
-        for (int p = 0; p < RPW; ++p)
-    #pragma unroll
-            for (int q = 0; q < PW; ++q) bad |= __builtin_isfinite(acc[p][q]) ? 0u : 1u;
+#pragma unroll
+        for (int j = 0; j < CPL; ++j)
+#pragma unroll
+            for (int p = 0; p < RPW; ++p)
+#pragma unroll
+                for (int q = 0; q < PW; ++q) bad |= __builtin_isfinite(acc[j][p][q]) ? 0u : 1u;
 
         // Then a zero weight times an infinity may have reached bins whose samples never
         // touch that pixel, so this wave's bins are recomputed sample by sample, every
         // product taken only where the definition takes it.
         if (__builtin_amdgcn_ballot_w64(bad != 0) != 0) {
-    #pragma unroll
-            for (int p = 0; p < RPW; ++p) {
-                if (p0 + p >= p1) continue;
-    #pragma unroll 1
-                for (int q = 0; q < PW; ++q) {
-                    float sum = 0.0f;
-                    for (int iy2 = 0; iy2 < S; ++iy2) {
-                        const SampleTap ty = srow[(p0 + p) * S + iy2];
-                        if (ty.lo < 0) continue;
-                        const uint32_t r0 = vbase + static_cast<uint32_t>(ty.lo) * sh_b;
-                        const uint32_t r1 = vbase + static_cast<uint32_t>(ty.hi) * sh_b;
-                        for (int ix = 0; ix < S; ++ix) {
-                            const SampleTap tx = scol[q * S + ix];
-                            if (tx.lo < 0) continue;
-                            const uint32_t cl = static_cast<uint32_t>(tx.lo) * sw_b;
-                            const uint32_t chh = static_cast<uint32_t>(tx.hi) * sw_b;
-                            const float v00 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + cl));
-                            const float v01 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + chh));
-                            const float v10 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + cl));
-                            const float v11 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + chh));
-                            const float xl = fmaf(tx.w_hi, v01, tx.w_lo * v00);
-                            const float xh = fmaf(tx.w_hi, v11, tx.w_lo * v10);
-                            sum += fmaf(ty.w_hi, xh, ty.w_lo * xl);
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) {
+                const uint32_t vb = vbase + static_cast<uint32_t>(j) * uint32_t(sizeof(T));
+#pragma unroll
+                for (int p = 0; p < RPW; ++p) {
+                    if (p0 + p >= p1) continue;
+#pragma unroll 1
+                    for (int q = 0; q < PW; ++q) {
+                        float sum = 0.0f;
+                        for (int iy2 = 0; iy2 < S; ++iy2) {
+                            const SampleTap ty = srow[(p0 + p) * S + iy2];
+                            if (ty.lo < 0) continue;
+                            const uint32_t r0 = vb + static_cast<uint32_t>(ty.lo) * sh_b;
+                            const uint32_t r1 = vb + static_cast<uint32_t>(ty.hi) * sh_b;
+                            for (int ix = 0; ix < S; ++ix) {
+                                const SampleTap tx = scol[q * S + ix];
+                                if (tx.lo < 0) continue;
+                                const uint32_t cl = static_cast<uint32_t>(tx.lo) * sw_b;
+                                const uint32_t chh = static_cast<uint32_t>(tx.hi) * sw_b;
+                                const float v00 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + cl));
+                                const float v01 = raw_to_f32<T>(buf_load_raw<T>(res, r0 + chh));
+                                const float v10 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + cl));
+                                const float v11 = raw_to_f32<T>(buf_load_raw<T>(res, r1 + chh));
+                                const float xl = fmaf(tx.w_hi, v01, tx.w_lo * v00);
+                                const float xh = fmaf(tx.w_hi, v11, tx.w_lo * v10);
+                                sum += fmaf(ty.w_hi, xh, ty.w_lo * xl);
+                            }
                         }
+                        sum = sum / static_cast<float>(S * S);
+#pragma unroll
+                        for (int qq = 0; qq < PW; ++qq) acc[j][p][qq] = (qq == q) ? sum : acc[j][p][qq];
                     }
-                    sum = sum / static_cast<float>(S * S);
-    #pragma unroll
-                    for (int qq = 0; qq < PW; ++qq) acc[p][qq] = (qq == q) ? sum : acc[p][qq];
                 }
             }
         }
 
-        // a5: the slice's [64][PH][PW] block is contiguous in the output at RoI k;
+        // a5: the slice's [SLICE][PH][PW] block is contiguous in the output at RoI k;
         // transposed through LDS in rounds of CHK channels.
-        const int nchan = min(64, a.lv.C - slice * 64);
+        const int nchan = min(SLICE, a.lv.C - slice * SLICE);
         const gptr<TO> out_blk = as_global_mut<TO>(a.out) +
-                                 (static_cast<int64_t>(k) * a.lv.C + static_cast<int64_t>(slice) * 64) * NB;
-    #pragma unroll
-        for (int c0 = 0; c0 < 64; c0 += CHK) {
-            if (lane >= c0 && lane < c0 + CHK) {
-    #pragma unroll
-                for (int p = 0; p < RPW; ++p) {
-                    if (p0 + p >= p1) continue;
-    #pragma unroll
-                    for (int q = 0; q < PW; ++q) stile[(lane - c0) * NB + (p0 + p) * PW + q] = acc[p][q];
-                }
+                                 (static_cast<int64_t>(k) * a.lv.C + static_cast<int64_t>(slice) * SLICE) * NB;
+#pragma unroll
+        for (int c0 = 0; c0 < SLICE; c0 += CHK) {
+            if (lane * CPL >= c0 && lane * CPL < c0 + CHK) {
+#pragma unroll
+                for (int j = 0; j < CPL; ++j)
+#pragma unroll
+                    for (int p = 0; p < RPW; ++p) {
+                        if (p0 + p >= p1) continue;
+#pragma unroll
+                        for (int q = 0; q < PW; ++q)
+                            stile[(lane * CPL + j - c0) * NB + (p0 + p) * PW + q] = acc[j][p][q];
+                    }
             }
             __syncthreads();
             const int ne = max(0, min(CHK, nchan - c0)) * NB;
             if (kvalid)
                 for (int e = t; e < ne; e += 256) store_f32(out_blk + c0 * NB + e, stile[e]);
-            if (c0 + CHK < 64) __syncthreads();
+            if (c0 + CHK < SLICE) __syncthreads();
         }
     }   // slices
 }
@@ -495,37 +564,55 @@ bool fwd_fast_available(int PH, int PW, int S) {
     return S == 2 && ((PH == 7 && PW == 7) || (PH == 14 && PW == 14));
 }
 
+template <typename T, typename TO, int PH, int PW, int CX, int CHK, int CPL>
+static hipError_t launch_fwd_cl(FwdArgs a, hipStream_t stream) {
+    a.nslices = (a.lv.C + 64 * CPL - 1) / (64 * CPL);
+    // Slices per workgroup: the RoI's geometry (two IEEE divisions, the distinct-tap
+    // reductions) is built once per workgroup, so a workgroup takes up to 4 slices
+    // while the grid keeps at least 32 workgroups per CU; below that the longest
+    // workgroups would set the kernel's tail (measured, 1024 RoIs x 256 channels:
+    // 53 us with one slice, 56 with two; 8192 RoIs: 361 us with one, 328 with four).
+    a.spw = 1;
+    for (int spw = 4; spw > 1; spw /= 2)
+        if (static_cast<int64_t>(a.K) * ((a.nslices + spw - 1) / spw) >= 8192) {
+            a.spw = spw;
+            break;
+        }
+    a.wg_per_roi = (a.nslices + a.spw - 1) / a.spw;
+    const int64_t grid = static_cast<int64_t>(a.K) * a.wg_per_roi;
+    if (grid >= (int64_t(1) << 24)) return hipErrorInvalidConfiguration;
+    fwd_cl_kernel<T, TO, PH, PW, 2, CX, CHK, CPL><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
+    return hipGetLastError();
+}
+
 template <typename T, typename TO>
 static hipError_t launch_fwd_typed(FwdArgs a, bool fast, hipStream_t stream) {
+    // a dispatch holds fewer than 2^32 work-items; beyond that, the strided kernel
+    if (fast && static_cast<int64_t>(a.K) * ((a.lv.C + 63) / 64) >= (int64_t(1) << 24)) fast = false;
     if (fast) {
-        a.nslices = (a.lv.C + 63) / 64;
-        // Slices per workgroup: the RoI's geometry (two IEEE divisions, the distinct-tap
-        // reductions) is built once per workgroup, so a workgroup takes up to 4 slices
-        // while the grid keeps at least 32 workgroups per CU; below that the longest
-        // workgroups would set the kernel's tail (measured, 1024 RoIs x 256 channels:
-        // 53 us with one slice, 56 with two; 8192 RoIs: 361 us with one, 328 with four).
-        a.spw = 1;
-        for (int spw = 4; spw > 1; spw /= 2)
-            if (static_cast<int64_t>(a.K) * ((a.nslices + spw - 1) / spw) >= 8192) {
-                a.spw = spw;
-                break;
-            }
-        a.wg_per_roi = (a.nslices + a.spw - 1) / a.spw;
-        const int64_t grid = static_cast<int64_t>(a.K) * a.wg_per_roi;
-        // a dispatch holds fewer than 2^32 work-items; beyond that, the strided kernel
-        if (grid >= (int64_t(1) << 24)) return launch_fwd_typed<T, TO>(a, false, stream);
-        if (a.PH == 7)
-            fwd_cl_kernel<T, TO, 7, 7, 2, kFwdCX, 64><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
-        else
-            // 4 columns per unit keep the 14x14 kernel at 124 registers, four workgroups
-            // per CU (8 columns: 164 registers, three; mask head batch 2: 44 vs 51 us);
-            // the 7x7 kernel is fastest with 8 (4: 60 registers, 336 vs 321 us batch 16)
-            fwd_cl_kernel<T, TO, 14, 14, 2, 4, 16><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
-    } else {
-        const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * a.PH * a.PW;
-        const int64_t blocks = std::min<int64_t>((total + 255) / 256, 16384);
-        fwd_generic_kernel<T, TO><<<static_cast<uint32_t>(blocks), 256, 0, stream>>>(a);
+        if (a.PH == 7) {
+            // bf16 features: two adjacent channels per lane (one 32-bit load per pixel)
+            // when the channel count is even -- half the load and address instructions of
+            // one channel per lane, and twice the bytes in flight per load (batch-1
+            // inference, 1000 RoIs: 49.3 -> 41.9 us; batch 16: 316 -> 268 us).  For
+            // binary32 (64-bit loads) the same layout is slower (1024 RoIs: 51.0 -> 54.6
+            // us): the grid halves and occupancy drops from six to four waves, so fewer
+            // bytes are in flight per SIMD; so is sharing one geometry between two slices
+            // taken at once by an 8-wave workgroup (53.5 -> 59.8 us).
+            if constexpr (sizeof(T) == 2)
+                if (a.lv.C % 2 == 0)
+                    return launch_fwd_cl<T, TO, 7, 7, REX_FWD_CX2_BF16, 64, 2>(a, stream);
+            return launch_fwd_cl<T, TO, 7, 7, kFwdCX, 64, 1>(a, stream);
+        }
+        // 4 columns per unit keep the 14x14 kernel at 124 registers, four workgroups
+        // per CU (8 columns: 164 registers, three; mask head batch 2: 44 vs 51 us);
+        // the 7x7 kernel with one channel per lane is fastest with 8 (4: 60 registers,
+        // 336 vs 321 us batch 16)
+        return launch_fwd_cl<T, TO, 14, 14, 4, 16, 1>(a, stream);
     }
+    const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * a.PH * a.PW;
+    const int64_t blocks = std::min<int64_t>((total + 255) / 256, 16384);
+    fwd_generic_kernel<T, TO><<<static_cast<uint32_t>(blocks), 256, 0, stream>>>(a);
     return hipGetLastError();
 }
 
