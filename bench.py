@@ -328,7 +328,24 @@ def main():
                 "unit": "GB/s", "frac": round(gbs[dominant] / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "kernel": "roi_align_" + kname,
                 "bytes_per_launch": alg[dominant],
+                "bytes_model": ("bytes the kernel must move: for the gather backward the "
+                                "upstream gradient read once and every gradient element "
+                                "written once; for the forward E_fwd (each RoI's distinct "
+                                "footprint read once per channel plus the output)"),
                 "launch_ms": round(per_kernel[dominant], 5)}
+    if traffic is not None:
+        roofline["traffic_kind"] = ("L2 egress: rocprofv3 FETCH_SIZE + WRITE_SIZE per launch, "
+                                    "scaled by a plain copy; hits in the 256 MB MALL are not "
+                                    "seen by these counters")
+    if dominant == "bwd":
+        # the same kernel against the effective-byte model of the workload (E_bwd: the
+        # upstream gradient plus one fp32 read-modify-write per distinct (pixel, channel)
+        # of every RoI, the traffic of a scatter with atomics).  The gather performs no
+        # read-modify-write (it accumulates in registers and writes each element once),
+        # so E_bwd is not a bound for it and this fraction can exceed 1.
+        roofline["frac_effective"] = round(by.e_bwd / (per_kernel["bwd"] * 1e-3) / 1e9
+                                           / HBM_PEAK_GBS, 4)
+        roofline["effective_bytes_per_launch"] = by.e_bwd
 
     step_bytes = sum(alg[n] for n in names)
     extra = {
@@ -364,6 +381,27 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, feats_np, rois_np, lv_np, args.cpu_seconds)
 
+    # cold step (each step after a 1 GiB write that evicts L2 and the MALL), with the
+    # headline measure of the effective-byte model: (E_fwd + E_bwd) over the forward and
+    # backward times, the plan included in the forward, zero-fill not counted
+    cold_line = None
+    if cold is not None:
+        ck = cold["kernel_ms"]
+        t_fb = ck["plan"] + ck["fwd"] + (ck["bwd"] if backward else 0.0)
+        cold_line = {
+            "ms_per_step": round(cold["ms_per_step"], 5),
+            "value": round(K / (cold["ms_per_step"] * 1e-3), 1), "unit": "RoIs/s",
+            "kernel_ms": {n: round(v, 5) for n, v in ck.items()},
+            "frac_effective_fwd_bwd": round((by.e_fwd + (by.e_bwd if backward else 0))
+                                            / (t_fb * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "reps": args.cold_reps}
+    warm_fb = per_kernel["plan"] + per_kernel["fwd"] + (per_kernel["bwd"] if backward else 0.0)
+    warm_line = {
+        "ms_per_step": round(ms_per_step, 5), "value": round(K / (ms_per_step * 1e-3), 1),
+        "unit": "RoIs/s",
+        "frac_effective_fwd_bwd": round((by.e_fwd + (by.e_bwd if backward else 0))
+                                        / (warm_fb * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
     result = {
         "metric": METRIC,
         "value": round(K / (ms_per_step * 1e-3), 1),
@@ -383,6 +421,8 @@ def main():
                    "backward": backward},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "warm": warm_line,
+        "cold": cold_line,
         "extra": extra,
     }
     print(json.dumps(result), flush=True)
@@ -493,9 +533,10 @@ def main_pool(args):
 
 
 def main_heads(args):
-    """Box (7x7) and mask (14x14) heads on one pyramid: one step is a plan and a forward
-    per head, then roi_align_bwd_multi (both heads in one pass over the gradient
-    pyramid).  The same step with two roi_align_bwd calls is timed too."""
+    """Box (7x7) and mask (14x14) heads on one pyramid: one step is a plan per head,
+    roi_align_fwd_multi (both heads' forwards in one launch) and roi_align_bwd_multi
+    (both heads in one pass over the gradient pyramid).  The same step with one
+    roi_align_fwd and one roi_align_bwd call per head is timed too."""
     import torch
 
     import paper_1906_07155_amd as rex
@@ -535,17 +576,27 @@ def main_heads(args):
             "gout": to_dev(w.grad(), w.grad_dtype, cl=False)})
     stream = torch.cuda.current_stream()
 
+    fwd_heads = [{"rois": h["rois"], "roi_levels": h["levels"], "out_size": h["wl"].out_hw,
+                  "sampling_ratio": h["wl"].sampling_ratio, "aligned": h["wl"].aligned,
+                  "workspace": h["ws"], "out": h["out"]} for h in heads]
+
     def step(fused, ev=None):
         if ev is not None:
             ev[0].record(stream)
         for h in heads:
-            w = h["wl"]
             rex.plan(feats, wb.scales, h["rois"], wb.finest_scale, levels_out=h["levels"],
                      workspace=h["ws"])
-            rex.roi_align_fwd(feats, wb.scales, h["rois"], h["levels"], w.out_hw,
-                              w.sampling_ratio, w.aligned, out=h["out"], workspace=h["ws"])
         if ev is not None:
             ev[1].record(stream)
+        if fused:
+            rex.roi_align_fwd_multi(feats, wb.scales, fwd_heads, out_dtype=odt)
+        else:
+            for h in heads:
+                w = h["wl"]
+                rex.roi_align_fwd(feats, wb.scales, h["rois"], h["levels"], w.out_hw,
+                                  w.sampling_ratio, w.aligned, out=h["out"], workspace=h["ws"])
+        if ev is not None:
+            ev[2].record(stream)
         if fused:
             rex.roi_align_bwd_multi(
                 [{"grad_out": h["gout"], "rois": h["rois"], "roi_levels": h["levels"],
@@ -558,15 +609,16 @@ def main_heads(args):
                                   w.aligned, grads, wb.scales, zero_init=(i == 0),
                                   workspace=h["ws"])
         if ev is not None:
-            ev[2].record(stream)
+            ev[3].record(stream)
 
     def timed(fused, n):
         for _ in range(max(1, args.warmup)):
             step(fused)
-        ms, per, _ = time_two_passes(lambda ev: step(fused, ev), ["plan_fwd", "bwd"], n, stream)
-        return ms, per["plan_fwd"], per["bwd"]
+        ms, per, _ = time_two_passes(lambda ev: step(fused, ev), ["plan", "fwd", "bwd"], n,
+                                     stream)
+        return ms, per["plan"], per["fwd"], per["bwd"]
 
-    ms, ms_plan_fwd, ms_bwd = timed(True, args.steps)
+    ms, ms_plan, ms_fwd, ms_bwd = timed(True, args.steps)
     alt = timed(False, max(1, args.alt_steps)) if args.alt_steps > 0 else None
     Ktot = sum(h["rois_np"].shape[0] for h in heads)
     s_g = 2 if wb.grad_dtype == "bf16" else 4
@@ -592,9 +644,11 @@ def main_heads(args):
                      "kernel": "roi_align_bwd_multi", "bytes_per_launch": bwd_bytes,
                      "launch_ms": round(ms_bwd, 5)},
         "cpu_baseline": None,
-        "extra": {"ms_plans_and_forwards": round(ms_plan_fwd, 5), "ms_fused_bwd": round(ms_bwd, 5),
-                  "separate_bwd": None if alt is None else {
-                      "ms_per_step": round(alt[0], 5), "ms_bwd": round(alt[2], 5)},
+        "extra": {"ms_plans": round(ms_plan, 5), "ms_fused_fwd": round(ms_fwd, 5),
+                  "ms_fused_bwd": round(ms_bwd, 5),
+                  "separate_fwd_and_bwd": None if alt is None else {
+                      "ms_per_step": round(alt[0], 5), "ms_plans": round(alt[1], 5),
+                      "ms_fwd": round(alt[2], 5), "ms_bwd": round(alt[3], 5)},
                   "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(result), flush=True)

@@ -263,6 +263,35 @@ re_status_t roi_align_bwd_multi(const re_head_t *heads, int32_t num_heads,
                                 const re_level_t *grad_levels, int32_t num_levels,
                                 int32_t zero_init, void *stream);
 
+/* f2 -- the forward of several heads in one launch.  The RoIHeads of a two-stage
+ * detector extract features from the same pyramid (§3.1: BBoxHead and MaskHead; the
+ * cascaded stages of Cascade R-CNN and HTC, §2, extract again from refined boxes): each
+ * head has its own RoIs, grid and output, and the forward of all of them is one kernel
+ * launch whose workgroups are the heads' (RoI, channel slice) pairs, every head's in its
+ * own plan order.  Heads on the channels-last fast path (7x7 or 14x14 grid, sampling
+ * ratio 2, every level with stride_c == 1) share the launch, 14x14 heads first; with
+ * fp32 features (or an odd channel count) the 7x7 and the 14x14 heads take one launch
+ * each, since the 14x14 kernel's register count would lower the 7x7 heads' occupancy.
+ * Other heads run one after the other as roi_align_fwd.  Results equal roi_align_fwd's
+ * for every head, bit for bit. */
+typedef struct {
+    const float *rois;        /* device float[num_rois][5] */
+    int64_t num_rois;
+    const int32_t *roi_levels;/* device int32[num_rois]; NULL only with one level */
+    int32_t out_h, out_w;
+    int32_t sampling_ratio;
+    int32_t aligned;
+    void *out;                /* device [num_rois][c][out_h][out_w] of the call's out_dtype */
+    const void *plan;         /* roi_extract_plan workspace for these RoIs, or NULL */
+    size_t plan_bytes;
+} re_fwd_head_t;
+
+/* num_heads in [1, RE_MAX_HEADS]; levels and out_dtype as roi_align_fwd, each head's
+ * fields as the arguments of roi_align_fwd. */
+re_status_t roi_align_fwd_multi(const re_level_t *levels, int32_t num_levels,
+                                const re_fwd_head_t *heads, int32_t num_heads, int32_t out_dtype,
+                                void *stream);
+
 /* f3 -- deformable RoI pooling (DCN) and its modulated form (DCNv2), general modules
  * of §2.  Every bin of the RoIAlign grid above is moved by a learned offset given
  * normalized to the box size, and the bin average is scaled by a learned modulation:

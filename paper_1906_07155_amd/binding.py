@@ -28,6 +28,7 @@ BWD_AUTO, BWD_SCATTER, BWD_GATHER = 0, 1, 2
 NMS_METHODS = {"hard": 0, "linear": 1, "gaussian": 2}   # RE_NMS_HARD / _LINEAR / _GAUSSIAN
 _BWD_ALGOS = {"auto": BWD_AUTO, "scatter": BWD_SCATTER, "gather": BWD_GATHER}
 MAX_LEVELS = 8
+MAX_HEADS = 8
 
 
 class RoIExtractError(RuntimeError):
@@ -54,6 +55,14 @@ class ReHead(ctypes.Structure):
                 ("plan", ctypes.c_void_p), ("plan_bytes", ctypes.c_size_t)]
 
 
+class ReFwdHead(ctypes.Structure):
+    _fields_ = [("rois", ctypes.c_void_p), ("num_rois", ctypes.c_int64),
+                ("roi_levels", ctypes.c_void_p), ("out_h", ctypes.c_int32),
+                ("out_w", ctypes.c_int32), ("sampling_ratio", ctypes.c_int32),
+                ("aligned", ctypes.c_int32), ("out", ctypes.c_void_p), ("plan", ctypes.c_void_p),
+                ("plan_bytes", ctypes.c_size_t)]
+
+
 _VP, _I32, _I64, _F32, _SZ = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                               ctypes.c_size_t)
 _LEVELS = ctypes.POINTER(ReLevel)
@@ -70,6 +79,7 @@ SIGNATURES = {
     "roi_align_fwd": [_LEVELS, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _VP, _I32, _VP,
                       _SZ, _VP],
     "roi_extract_zero_grad": [_LEVELS, _I32, _VP],
+    "roi_align_fwd_multi": [_LEVELS, _I32, ctypes.POINTER(ReFwdHead), _I32, _I32, _VP],
     "roi_align_fwd_noalloc": [_LEVELS, _I32, _VP, _I64, _F32, _VP, _I32, _I32, _I32, _I32, _VP,
                               _I32, _VP],
     "roi_align_bwd": [_VP, _I32, _VP, _I64, _VP, _I32, _I32, _I32, _I32, _LEVELS, _I32, _I32,
@@ -377,6 +387,48 @@ def roi_align_fwd_noalloc(features: Sequence, scales: Sequence[float], rois,
                                       _dtype_code(out), stream_handle(stream)),
           "roi_align_fwd_noalloc")
     return out, levels_out
+
+
+def roi_align_fwd_multi(features: Sequence, scales: Sequence[float], heads: Sequence[dict],
+                        out_dtype=None, stream=None):
+    """Forward of several heads in one launch.  Each head is a dict with rois, roi_levels,
+    out_size and optionally sampling_ratio (2), aligned (True), workspace (its plan) and
+    out.  Returns the list of outputs ([K_h, C, out_h, out_w] of out_dtype, default the
+    features' dtype)."""
+    torch = _torch()
+    C, L = _channels(features), len(features)
+    odt = out_dtype or features[0].dtype
+    if odt not in (torch.float32, torch.bfloat16):
+        raise TypeError("out_dtype must be float32 or bfloat16 (got %s)" % odt)
+    if not 1 <= len(heads) <= MAX_HEADS:
+        raise ValueError("between 1 and %d heads" % MAX_HEADS)
+    arr = (ReFwdHead * len(heads))()
+    outs, fields = [], []
+    for i, h in enumerate(heads):          # every head's shapes first, then the devices
+        rois = _rois(h["rois"])
+        K = rois.shape[0]
+        ph, pw = h["out_size"]
+        lv = _roi_levels(h.get("roi_levels"), rois, L)
+        out = h.get("out")
+        if out is not None:
+            _block(out, (K, C, ph, pw), "out of head %d" % i, rois, (odt,))
+        ws, wsb = _workspace(h.get("workspace"), rois)
+        fields.append((rois, K, lv, ph, pw, ws, wsb))
+    for i, h in enumerate(heads):
+        rois, K, lv, ph, pw, ws, wsb = fields[i]
+        _on_device(rois, roi_levels=h.get("roi_levels"), out=h.get("out"),
+                   workspace=h.get("workspace"))
+        out = h.get("out")
+        if out is None:
+            out = torch.empty((K, C, ph, pw), dtype=odt, device=rois.device)
+        arr[i] = ReFwdHead(rois.data_ptr(), K, lv, ph, pw, int(h.get("sampling_ratio", 2)),
+                           int(bool(h.get("aligned", True))), out.data_ptr(), ws, wsb)
+        outs.append(out)
+    levels = level_array(features, scales, heads[0]["rois"] if heads else None)
+    check(lib().roi_align_fwd_multi(levels, L, arr, len(heads),
+                                    RE_DTYPE_BF16 if odt == torch.bfloat16 else RE_DTYPE_F32,
+                                    stream_handle(stream)), "roi_align_fwd_multi")
+    return outs
 
 
 def zero_grad(grads: Sequence, scales: Sequence[float], stream=None):

@@ -487,6 +487,69 @@ re_status_t roi_align_fwd_noalloc(const re_level_t *levels, int32_t num_levels, 
     return from_hip(launch_fwd(a, levels[0].dtype, out_dtype, fast, s));
 }
 
+re_status_t roi_align_fwd_multi(const re_level_t *levels, int32_t num_levels,
+                                const re_fwd_head_t *heads, int32_t num_heads, int32_t out_dtype,
+                                void *stream) {
+    LevelTable t;
+    bool cl = false;
+    re_status_t st = check_levels(levels, num_levels, true, &t, &cl, nullptr, nullptr);
+    if (st != RE_OK) return st;
+    if (!heads || num_heads < 1 || num_heads > RE_MAX_HEADS) return RE_ERR_INVALID_ARG;
+    if (!valid_dtype(out_dtype)) return RE_ERR_INVALID_ARG;
+    for (int i = 0; i < num_heads; ++i) {
+        const re_fwd_head_t &h = heads[i];
+        if ((st = check_common(h.rois, h.num_rois, h.roi_levels, num_levels, h.out_h, h.out_w,
+                               h.sampling_ratio, h.aligned)) != RE_OK)
+            return st;
+        if (h.num_rois > 0 && !h.out) return RE_ERR_INVALID_ARG;
+        if (reinterpret_cast<uintptr_t>(h.out) % dtype_size(out_dtype)) return RE_ERR_INVALID_ARG;
+        if ((st = check_plan(h.plan, h.plan_bytes, h.num_rois, t)) != RE_OK) return st;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    FwdMultiArgs m{};
+    m.lv = t;
+    int64_t fused_wgs = 0;   // upper bound of the shared launch's workgroups
+    for (int i = 0; i < num_heads; ++i) {
+        const re_fwd_head_t &h = heads[i];
+        if (h.num_rois == 0) continue;
+        const int32_t *perm = h.plan ? reinterpret_cast<const int32_t *>(
+                                           static_cast<const char *>(h.plan) + perm_offset())
+                                     : nullptr;
+        // fast-path heads share the launch while its grid stays within one dispatch
+        const int64_t wgs = h.num_rois * ((t.C + 63) / 64);
+        if (cl && fwd_fast_available(h.out_h, h.out_w, h.sampling_ratio) &&
+            fused_wgs + wgs < (int64_t(1) << 24)) {
+            fused_wgs += wgs;
+            FwdHeadArgs &a = m.head[m.nheads++];
+            a.rois = h.rois;
+            a.roi_levels = h.roi_levels;
+            a.perm = perm;
+            a.out = h.out;
+            a.K = static_cast<int32_t>(h.num_rois);
+            a.PH = h.out_h;
+            a.PW = h.out_w;
+            a.S = h.sampling_ratio;
+            a.aligned = h.aligned;
+            continue;
+        }
+        FwdArgs a{};
+        a.lv = t;
+        a.rois = h.rois;
+        a.roi_levels = h.roi_levels;
+        a.perm = perm;
+        a.out = h.out;
+        a.K = static_cast<int32_t>(h.num_rois);
+        a.PH = h.out_h;
+        a.PW = h.out_w;
+        a.S = h.sampling_ratio;
+        a.aligned = h.aligned;
+        const bool fast = cl && fwd_fast_available(h.out_h, h.out_w, h.sampling_ratio);
+        if ((st = from_hip(launch_fwd(a, levels[0].dtype, out_dtype, fast, s))) != RE_OK) return st;
+    }
+    if (m.nheads == 0) return RE_OK;
+    return from_hip(launch_fwd_multi(m, levels[0].dtype, out_dtype, s));
+}
+
 re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_levels,
                                   void *stream) {
     LevelTable t;

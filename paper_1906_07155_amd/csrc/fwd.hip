@@ -239,35 +239,57 @@ __device__ __forceinline__ float unpack_pix(const RawPix<T, CPL> &p, int j) {
 // the distinct tap rows of those bin rows times all distinct tap columns of the RoI, in
 // chunks of CX columns, with the next unit's loads issued before the current one is
 // reduced.
-template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK, int CPL>
-__global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
-    constexpr int NB = PH * PW;
-    constexpr int NR = PH * S;                   // sample rows
-    constexpr int NCOL = PW * S;                 // sample columns
-    constexpr int RPW = (PH + 3) / 4;            // bin rows per wave
-    constexpr int RPWP = (RPW + 3) & ~3;
-    constexpr int MAXY = 2 * RPW * S;            // distinct tap rows per wave
-    constexpr int MAXX = ((2 * NCOL + CX - 1) / CX) * CX;   // distinct tap columns, padded
-    constexpr int PWP = (PW + 3) & ~3;           // padded for 16-byte LDS reads
+// LDS of one forward workgroup.
+template <int PH, int PW, int S, int CX, int CHK>
+struct FwdSmem {
+    static constexpr int NB = PH * PW;
+    static constexpr int NR = PH * S;
+    static constexpr int NCOL = PW * S;
+    static constexpr int RPW = (PH + 3) / 4;
+    static constexpr int RPWP = (RPW + 3) & ~3;
+    static constexpr int MAXY = 2 * RPW * S;
+    static constexpr int MAXX = ((2 * NCOL + CX - 1) / CX) * CX;
+    static constexpr int PWP = (PW + 3) & ~3;
+    SampleTap srow[NR];
+    SampleTap scol[NCOL];
+    __align__(16) uint32_t s_xoff[MAXX];
+    __align__(16) float s_wx[MAXX][PWP];
+    uint32_t s_yoff[4][MAXY];
+    __align__(16) float s_wy[4][MAXY][RPWP];
+    int32_t s_nx;
+    int32_t s_ny[4];
+    uint64_t s_xhalf[2];   // bit x: column x weighs on bins [0, QH) / [QH, PW)
+    __align__(16) float stile[CHK * NB];
+};
+
+// The forward of workgroup `lid` (in logical order) of a launch over the RoIs of `a`
+// (FwdArgs or FwdHeadArgs: RoIs, levels, plan order, output and slicing) on pyramid lv.
+template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK, int CPL, typename A>
+__device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, uint32_t lid,
+                                            FwdSmem<PH, PW, S, CX, CHK> &sm) {
+    using SM = FwdSmem<PH, PW, S, CX, CHK>;
+    constexpr int NB = SM::NB;
+    constexpr int NR = SM::NR;                   // sample rows
+    constexpr int NCOL = SM::NCOL;               // sample columns
+    constexpr int RPW = SM::RPW;                 // bin rows per wave
+    constexpr int RPWP = SM::RPWP;
+    constexpr int MAXY = SM::MAXY;               // distinct tap rows per wave
+    constexpr int MAXX = SM::MAXX;               // distinct tap columns, padded
+    constexpr int PWP = SM::PWP;                 // padded for 16-byte LDS reads
     constexpr int QH = (PW + 1) / 2;             // the bin columns' first half
     constexpr bool kHalves = PW >= 12;           // skip the halves a column misses
     constexpr int SLICE = 64 * CPL;              // channels of one slice
     static_assert(NR + NCOL <= 256 && NCOL <= 64 && RPW * S <= 64 && MAXX <= 64, "geometry sizes");
     static_assert(SLICE % CHK == 0 && CHK % CPL == 0 && CX % 4 == 0, "tiling");
+    SampleTap *const srow = sm.srow;
+    SampleTap *const scol = sm.scol;
+    uint32_t *const s_xoff = sm.s_xoff;
+    float (*const s_wx)[PWP] = sm.s_wx;
+    uint32_t (*const s_yoff)[MAXY] = sm.s_yoff;
+    float (*const s_wy)[MAXY][RPWP] = sm.s_wy;
+    float *const stile = sm.stile;
 
-    __shared__ SampleTap srow[NR];
-    __shared__ SampleTap scol[NCOL];
-    __shared__ __align__(16) uint32_t s_xoff[MAXX];
-    __shared__ __align__(16) float s_wx[MAXX][PWP];
-    __shared__ uint32_t s_yoff[4][MAXY];
-    __shared__ __align__(16) float s_wy[4][MAXY][RPWP];
-    __shared__ int32_t s_nx;
-    __shared__ int32_t s_ny[4];
-    __shared__ uint64_t s_xhalf[2];   // bit x: column x weighs on bins [0, QH) / [QH, PW)
-    __shared__ float stile[CHK * NB];
-
-    // Which RoI and slice: XCD-aware block order, then the plan's permutation.
-    const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
+    // Which RoI and slice: the logical block id, then the plan's permutation.
     const int slot = static_cast<int>(lid / static_cast<uint32_t>(a.wg_per_roi));
     const int sub = static_cast<int>(lid) - slot * a.wg_per_roi;
     const int slice0 = sub * a.spw;                          // this workgroup's slices
@@ -278,9 +300,9 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     const float *r = a.rois + 5 * static_cast<int64_t>(k);
     const float rb = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
     const int lvl = uniform_i(a.roi_levels ? a.roi_levels[k] : 0);
-    const bool lvalid = lvl >= 0 && lvl < a.lv.num;
-    const LevelArg L = level_at(a.lv, lvalid ? lvl : 0);
-    const int b = roi_batch(rb, a.lv.N);
+    const bool lvalid = lvl >= 0 && lvl < lv.num;
+    const LevelArg L = level_at(lv, lvalid ? lvl : 0);
+    const int b = roi_batch(rb, lv.N);
     const bool active = kvalid && lvalid && b >= 0;
 
     const int t = threadIdx.x;
@@ -320,10 +342,10 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     {
         const int ny = distinct_taps<S, RPWP>(srow + p0 * S, (p1 - p0) * S, lane, sh_b, kInvS,
                                               s_yoff[wave], s_wy[wave]);
-        if (lane == 0) s_ny[wave] = ny;
+        if (lane == 0) sm.s_ny[wave] = ny;
         if (wave == 0) {
             const int nx = distinct_taps<S, PWP>(scol, NCOL, lane, sw_b, kInvS, s_xoff, s_wx);
-            if (lane == 0) s_nx = nx;
+            if (lane == 0) sm.s_nx = nx;
             // Which half of the bin columns each distinct column reaches (a column is
             // reached by a run of at most a few adjacent bins, mostly inside one half);
             // padding columns reach none.
@@ -340,27 +362,27 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
             const uint64_t blo = __builtin_amdgcn_ballot_w64(lo);
             const uint64_t bhi = __builtin_amdgcn_ballot_w64(hi);
             if (lane == 0) {
-                s_xhalf[0] = blo;
-                s_xhalf[1] = bhi;
+                sm.s_xhalf[0] = blo;
+                sm.s_xhalf[1] = bhi;
             }
         }
     }
     __syncthreads();
 
     // wave-uniform counts in scalar registers: the pipeline below branches on them
-    const int ny = uniform_i(s_ny[wave]);
-    const int nch = uniform_i((s_nx + CX - 1) / CX);
-    const uint64_t xlo = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[0] >> 32))) << 32) |
-                         static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[0])));
-    const uint64_t xhi = (static_cast<uint64_t>(uniform_i(static_cast<int>(s_xhalf[1] >> 32))) << 32) |
-                         static_cast<uint32_t>(uniform_i(static_cast<int>(s_xhalf[1])));
+    const int ny = uniform_i(sm.s_ny[wave]);
+    const int nch = uniform_i((sm.s_nx + CX - 1) / CX);
+    const uint64_t xlo = (static_cast<uint64_t>(uniform_i(static_cast<int>(sm.s_xhalf[0] >> 32))) << 32) |
+                         static_cast<uint32_t>(uniform_i(static_cast<int>(sm.s_xhalf[0])));
+    const uint64_t xhi = (static_cast<uint64_t>(uniform_i(static_cast<int>(sm.s_xhalf[1] >> 32))) << 32) |
+                         static_cast<uint32_t>(uniform_i(static_cast<int>(sm.s_xhalf[1])));
     // The geometry above serves every slice of the workgroup.
     for (int slice = slice0; slice < slice1; ++slice) {
         if (slice > slice0) __syncthreads();   // the previous slice's output tile is stored
         // the lane's first channel; with CPL > 1 the channel count is a multiple of CPL,
         // so a lane holds either all of its channels or none
         const int c = slice * SLICE + lane * CPL;
-        const bool lane_on = active && c < a.lv.C;
+        const bool lane_on = active && c < lv.C;
         // One buffer resource per image of the level; a lane with no channel reads out
         // of range (zeros) instead of branching.
         const char *img = static_cast<const char *>(L.data) +
@@ -531,9 +553,9 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
 
         // a5: the slice's [SLICE][PH][PW] block is contiguous in the output at RoI k;
         // transposed through LDS in rounds of CHK channels.
-        const int nchan = min(SLICE, a.lv.C - slice * SLICE);
+        const int nchan = min(SLICE, lv.C - slice * SLICE);
         const gptr<TO> out_blk = as_global_mut<TO>(a.out) +
-                                 (static_cast<int64_t>(k) * a.lv.C + static_cast<int64_t>(slice) * SLICE) * NB;
+                                 (static_cast<int64_t>(k) * lv.C + static_cast<int64_t>(slice) * SLICE) * NB;
 #pragma unroll
         for (int c0 = 0; c0 < SLICE; c0 += CHK) {
             if (lane * CPL >= c0 && lane * CPL < c0 + CHK) {
@@ -554,6 +576,18 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
             if (c0 + CHK < SLICE) __syncthreads();
         }
     }   // slices
+}
+
+template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK, int CPL>
+__global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
+    __shared__ FwdSmem<PH, PW, S, CX, CHK> sm;
+    // The arguments are read in place from the kernel-argument segment (a reference to
+    // the by-value parameter would make the compiler copy the level table to private
+    // memory to index it by the RoI's level).
+    const FwdArgs &ka = *(const FwdArgs *)__builtin_amdgcn_kernarg_segment_ptr();
+    // XCD-aware block order: consecutive logical ids (neighbouring RoIs of the plan
+    // order) land on one XCD
+    fwd_cl_body<T, TO, PH, PW, S, CX, CHK, CPL>(ka, ka.lv, xcd_remap(blockIdx.x, gridDim.x), sm);
 }
 
 // ---------------------------------------------------------------------------
@@ -614,6 +648,127 @@ static hipError_t launch_fwd_typed(FwdArgs a, bool fast, hipStream_t stream) {
     const int64_t blocks = std::min<int64_t>((total + 255) / 256, 16384);
     fwd_generic_kernel<T, TO><<<static_cast<uint32_t>(blocks), 256, 0, stream>>>(a);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Several heads in one launch
+// ---------------------------------------------------------------------------
+//
+// The workgroups of every head form one grid: logical block ids [first_h, first_{h+1})
+// belong to head h (each head's blocks in its own plan order), and the XCD-aware
+// remapping runs over the whole grid.  A head takes the 7x7 or the 14x14 body; the
+// kernel holds the LDS of both as a union and the registers of the larger, so a launch
+// that mixes the two grids runs the 7x7 heads at the 14x14 occupancy.
+template <typename T, typename TO, bool H7, bool H14, int CPL7>
+__global__ __launch_bounds__(256, 4) void fwd_multi_kernel(FwdMultiArgs m) {
+    using S7 = FwdSmem<7, 7, 2, kFwdCX, 64>;
+    using S14 = FwdSmem<14, 14, 2, 4, 16>;
+    union Smem {
+        S7 s7;
+        S14 s14;
+    };
+    __shared__ Smem sm;
+    const FwdMultiArgs &ka = *(const FwdMultiArgs *)__builtin_amdgcn_kernarg_segment_ptr();
+    const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
+    int h = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxFwdHeads; ++i)
+        if (i < ka.nheads && lid >= static_cast<uint32_t>(ka.head[i].first)) h = i;
+    const FwdHeadArgs &a = ka.head[h];
+    const uint32_t local = lid - static_cast<uint32_t>(a.first);
+    if constexpr (H7 && H14) {
+        if (a.PH == 7)
+            fwd_cl_body<T, TO, 7, 7, 2, kFwdCX, 64, CPL7>(a, ka.lv, local, sm.s7);
+        else
+            fwd_cl_body<T, TO, 14, 14, 2, 4, 16, 1>(a, ka.lv, local, sm.s14);
+    } else if constexpr (H7) {
+        fwd_cl_body<T, TO, 7, 7, 2, kFwdCX, 64, CPL7>(a, ka.lv, local, sm.s7);
+    } else {
+        fwd_cl_body<T, TO, 14, 14, 2, 4, 16, 1>(a, ka.lv, local, sm.s14);
+    }
+}
+
+#ifndef REX_FWD_MULTI_ORDER
+#define REX_FWD_MULTI_ORDER 1
+#endif
+// One channel per lane (fp32 features, or an odd channel count): the 7x7 body needs 78
+// registers and the 14x14 one 124, so a kernel holding both runs the 7x7 heads at four
+// workgroups per CU instead of six; there the two grids go in two launches, 14x14 first
+// (batch 2, box 1024 + mask 256 RoIs, fp32: 100 us, against 145 in one mixed launch
+// and 110 as two roi_align_fwd calls).  Two bf16 channels per lane already take 116
+// registers on the 7x7 grid, and one mixed launch is fastest (batch 16, box 8192 +
+// mask 2048 RoIs: 503 us, against 536 as two calls).
+#ifndef REX_FWD_MULTI_MIX1
+#define REX_FWD_MULTI_MIX1 0
+#endif
+
+template <typename T, typename TO>
+static hipError_t launch_fwd_multi_typed(FwdMultiArgs m, hipStream_t stream) {
+    // two bf16 channels per lane on the 7x7 grid, as in the single-head launch
+    const int cpl7 = (sizeof(T) == 2 && m.lv.C % 2 == 0) ? 2 : 1;
+    if (REX_FWD_MULTI_ORDER) {
+        // 14x14 heads first: their workgroups are the longest, and the short 7x7 ones
+        // then fill the tail of the grid
+        FwdMultiArgs o = m;
+        int n = 0;
+        for (int pass = 0; pass < 2; ++pass)
+            for (int i = 0; i < m.nheads; ++i)
+                if ((m.head[i].PH == 14) == (pass == 0)) o.head[n++] = m.head[i];
+        m = o;
+    }
+    if (!REX_FWD_MULTI_MIX1 && cpl7 == 1) {
+        int n14 = 0;
+        while (n14 < m.nheads && m.head[n14].PH == 14) ++n14;
+        if (REX_FWD_MULTI_ORDER && n14 > 0 && n14 < m.nheads) {
+            FwdMultiArgs a = m, b = m;
+            a.nheads = n14;
+            b.nheads = m.nheads - n14;
+            for (int i = 0; i < b.nheads; ++i) b.head[i] = m.head[n14 + i];
+            hipError_t e = launch_fwd_multi_typed<T, TO>(a, stream);
+            return e != hipSuccess ? e : launch_fwd_multi_typed<T, TO>(b, stream);
+        }
+    }
+    bool h7 = false, h14 = false;
+    int64_t first = 0;
+    for (int i = 0; i < m.nheads; ++i) {
+        FwdHeadArgs &a = m.head[i];
+        const int cpl = a.PH == 7 ? cpl7 : 1;
+        (a.PH == 7 ? h7 : h14) = true;
+        a.nslices = (m.lv.C + 64 * cpl - 1) / (64 * cpl);
+        a.spw = 1;
+        for (int spw = 4; spw > 1; spw /= 2)
+            if (static_cast<int64_t>(a.K) * ((a.nslices + spw - 1) / spw) >= 8192) {
+                a.spw = spw;
+                break;
+            }
+        a.wg_per_roi = (a.nslices + a.spw - 1) / a.spw;
+        a.first = static_cast<int32_t>(first);
+        first += static_cast<int64_t>(a.K) * a.wg_per_roi;
+        if (first >= (int64_t(1) << 24)) return hipErrorInvalidConfiguration;
+    }
+    if (first == 0) return hipSuccess;
+    const uint32_t g = static_cast<uint32_t>(first);
+    if (cpl7 == 2) {
+        if constexpr (sizeof(T) == 2) {
+            if (h7 && h14) fwd_multi_kernel<T, TO, true, true, 2><<<g, 256, 0, stream>>>(m);
+            else if (h7) fwd_multi_kernel<T, TO, true, false, 2><<<g, 256, 0, stream>>>(m);
+            else fwd_multi_kernel<T, TO, false, true, 2><<<g, 256, 0, stream>>>(m);
+        }
+    } else {
+        if (h7 && h14) fwd_multi_kernel<T, TO, true, true, 1><<<g, 256, 0, stream>>>(m);
+        else if (h7) fwd_multi_kernel<T, TO, true, false, 1><<<g, 256, 0, stream>>>(m);
+        else fwd_multi_kernel<T, TO, false, true, 1><<<g, 256, 0, stream>>>(m);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_fwd_multi(FwdMultiArgs m, int feat_dtype, int out_dtype, hipStream_t stream) {
+    if (feat_dtype == kF32 && out_dtype == kF32) return launch_fwd_multi_typed<float, float>(m, stream);
+    if (feat_dtype == kF32 && out_dtype == kBF16)
+        return launch_fwd_multi_typed<float, uint16_t>(m, stream);
+    if (feat_dtype == kBF16 && out_dtype == kF32)
+        return launch_fwd_multi_typed<uint16_t, float>(m, stream);
+    return launch_fwd_multi_typed<uint16_t, uint16_t>(m, stream);
 }
 
 hipError_t launch_fwd(FwdArgs a, int feat_dtype, int out_dtype, bool fast, hipStream_t stream) {

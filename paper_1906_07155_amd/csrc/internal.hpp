@@ -128,6 +128,35 @@ struct FwdArgs {
     int32_t spw;                 // slices per workgroup (channels-last forward)
 };
 
+// One head of a multi-head forward (the pyramid is shared): its RoIs, output and the
+// slicing of its channels, and the first logical block id of its workgroups.
+constexpr int kMaxFwdHeads = 8;
+struct FwdHeadArgs {
+    const float *rois;
+    const int32_t *roi_levels;
+    const int32_t *perm;         // plan order or null
+    void *out;
+    int32_t K;
+    int32_t PH, PW, S;
+    int32_t aligned;
+    int32_t nslices;
+    int32_t wg_per_roi;
+    int32_t spw;
+    int32_t first;               // first logical block of the head
+    int32_t pad;
+};
+
+struct FwdMultiArgs {
+    LevelTable lv;
+    FwdHeadArgs head[kMaxFwdHeads];
+    int32_t nheads;
+    int32_t pad;
+};
+
+// Heads on the channels-last fast path (fwd_fast_available grids) in one launch; the
+// heads' K, PH, PW, S, aligned, rois, roi_levels, perm and out must be set.
+hipError_t launch_fwd_multi(FwdMultiArgs m, int feat_dtype, int out_dtype, hipStream_t stream);
+
 struct BwdArgs {
     LevelTable lv;               // gradient levels (binary32, written with atomics)
     const void *gout;

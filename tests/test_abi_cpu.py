@@ -267,6 +267,37 @@ def test_multi_head_backward_validation(L):
     assert _multi(L, [_head()], levels=_levels(dtype=1)) == UNSUPPORTED   # fp32 gradients only
 
 
+def _fhead(K=4, oh=7, ow=7, sr=2, al=1, out=FAKE, plan=None, plan_bytes=0, rois=FAKE,
+           roi_levels=FAKE):
+    return B.ReFwdHead(rois, K, roi_levels, oh, ow, sr, al, out, plan, plan_bytes)
+
+
+def _fmulti(L, heads, nl=2, odt=0, levels=None, n=None):
+    levels = levels if levels is not None else _levels()
+    arr = (B.ReFwdHead * max(1, len(heads)))(*heads)
+    return L.roi_align_fwd_multi(levels, nl, arr, len(heads) if n is None else n, odt, None)
+
+
+def test_multi_head_forward_validation(L):
+    assert _fmulti(L, [_fhead(K=0)]) == OK                         # nothing to do
+    assert _fmulti(L, [_fhead(K=0), _fhead(K=0, oh=14, ow=14, out=None)]) == OK
+    assert _fmulti(L, [_fhead()], n=0) == INVALID
+    assert _fmulti(L, [_fhead()] * 9) == INVALID                   # more than RE_MAX_HEADS
+    assert L.roi_align_fwd_multi(_levels(), 2, None, 1, 0, None) == INVALID
+    assert _fmulti(L, [_fhead()], levels=None, nl=0) == INVALID
+    assert _fmulti(L, [_fhead()], odt=7) == INVALID
+    # a bad head anywhere in the list is refused before any head is launched
+    assert _fmulti(L, [_fhead(), _fhead(out=None)]) == INVALID
+    assert _fmulti(L, [_fhead(), _fhead(out=FAKE + 2)]) == INVALID   # fp32 output misaligned
+    assert _fmulti(L, [_fhead(), _fhead(oh=0)]) == INVALID
+    assert _fmulti(L, [_fhead(), _fhead(sr=65)]) == INVALID
+    assert _fmulti(L, [_fhead(), _fhead(al=2)]) == INVALID
+    assert _fmulti(L, [_fhead(), _fhead(K=-1)]) == INVALID
+    assert _fmulti(L, [_fhead(), _fhead(rois=None)]) == INVALID
+    assert _fmulti(L, [_fhead(), _fhead(roi_levels=None)]) == INVALID  # several levels
+    assert _fmulti(L, [_fhead(), _fhead(plan=FAKE, plan_bytes=8)]) == WORKSPACE
+
+
 def test_deform_validation(L):
     def fwd(levels=None, K=4, off=FAKE, mask=None, gamma=0.1, out=FAKE, odt=0, sr=2, oh=7):
         lv = levels if levels is not None else _levels()

@@ -115,3 +115,17 @@ def test_nms_shapes():
         B.box_nms(boxes, scores, 0.5, keep=torch.zeros(5, dtype=torch.int32))
     with pytest.raises(ValueError, match="GPU tensor"):
         B.box_nms(boxes, scores, 0.5)
+
+
+def test_multi_head_forward_blocks():
+    heads = [dict(rois=_rois(), roi_levels=_levels(), out_size=(7, 7)),
+             dict(rois=_rois(), roi_levels=_levels(n=K - 1), out_size=(14, 14))]
+    with pytest.raises(ValueError, match="roi_levels"):
+        B.roi_align_fwd_multi(_feats(), SCALES, heads)
+    heads[1]["roi_levels"] = _levels()
+    heads[1]["out"] = torch.zeros(K, C, 7, 7)
+    with pytest.raises(ValueError, match="out of head 1"):
+        B.roi_align_fwd_multi(_feats(), SCALES, heads)
+    del heads[1]["out"]
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.roi_align_fwd_multi(_feats(), SCALES, heads)

@@ -19,7 +19,7 @@ def test_bench_json_line():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     cmd = [sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--steps", "3", "--warmup", "1",
-           "--alt-steps", "0", "--cold-reps", "0", "--no-copy-ceiling", "--cpu-seconds", "0.5"]
+           "--alt-steps", "0", "--cold-reps", "2", "--no-copy-ceiling", "--cpu-seconds", "0.5"]
     log("bench: " + " ".join(cmd[2:]))
     res = subprocess.run(cmd, cwd=ROOT, capture_output=True, text=True, timeout=110)
     assert res.returncode == 0, res.stderr[-2000:]
@@ -43,6 +43,18 @@ def test_bench_json_line():
     assert abs(r["frac"] - r["achieved"] / r["peak"]) <= 1e-3
     assert r["achieved"] == pytest.approx(r["bytes_per_launch"] / (r["launch_ms"] * 1e-3) / 1e9,
                                           rel=1e-3)
+    if r["kernel"] == "roi_align_bwd_gather":
+        # the same kernel against the effective bytes of the workload (a scatter's
+        # read-modify-write included): larger bytes, the same launch time
+        assert r["frac_effective"] == pytest.approx(
+            r["effective_bytes_per_launch"] / (r["launch_ms"] * 1e-3) / 1e9 / 8000.0, rel=1e-3)
+        assert r["effective_bytes_per_launch"] > r["bytes_per_launch"]
+    for kind in ("warm", "cold"):
+        w = d[kind]
+        assert w["unit"] == "RoIs/s" and w["ms_per_step"] > 0
+        assert abs(w["value"] - K / (w["ms_per_step"] * 1e-3)) <= 1e-3 * w["value"]
+        assert 0 < w["frac_effective_fwd_bwd"] < 2
+    assert d["warm"]["ms_per_step"] == d["ms_per_step"]
     c = d["cpu_baseline"]
     for key in ("value", "unit", "cores", "kind", "sample"):
         assert key in c, key
