@@ -113,9 +113,10 @@ re_status_t fpn_level_map_ex(const float *rois, int64_t num_rois, int32_t num_le
 
 /* Bytes of device workspace a plan for num_rois RoIs over the pyramid `levels` needs
  * (host array; only n, h and w are read).  It holds the launch permutation and the
- * tile->RoI lists of the gather backward (8 bytes per RoI, 8 per bin-tile, and 4 per
+ * tile->RoI lists of the gather backward (8 bytes per RoI, 12 per bin-tile, and 4 per
  * RoI times the largest number of bin-tiles of one image-level) and the plan's own
- * counters (60 KiB).  Host-only; writes *bytes. */
+ * counters (60 KiB).  Host-only; writes *bytes.  (A plan needs the level shapes, not
+ * only the RoI and level counts, to size its tile lists, hence the level array.) */
 re_status_t roi_extract_workspace_size(const re_level_t *levels, int32_t num_levels,
                                        int64_t num_rois, size_t *bytes);
 
@@ -124,8 +125,9 @@ re_status_t roi_extract_workspace_size(const re_level_t *levels, int32_t num_lev
  * spatial cell of the box centre) plus per-level offsets, stored in `workspace`; the
  * plan also lists, for every bin-tile (16 pixels or more a side) of every
  * (level, image), the RoIs whose footprint can reach it, and orders the tiles by
- * decreasing list length (used by the gather backward).  Up to 2048 RoIs this is one
- * kernel launch, above that four (all on `stream`, nothing allocated).  The forward and backward walk the RoIs in plan order,
+ * decreasing list length (used by the gather backward).  Up to 2048 RoIs (and bucket
+ * and tile tables that fit one workgroup's LDS) this is one kernel launch, otherwise
+ * five (all on `stream`, nothing allocated).  The forward and backward walk the RoIs in plan order,
  * so neighbouring work shares cache; any valid permutation gives the same
  * results, and RoIs with equal keys may come in any order.  The plan stays valid
  * for as long as rois, levels_out and the level shapes are unchanged, so one plan

@@ -17,16 +17,18 @@ using namespace rex;
 namespace {
 
 // Workspace layout: [0, 256) per-level offsets, then perm[K], keys[K],
-// tile_start[ntiles + 1], tile_order[ntiles], tile_rois[capacity], and the plan's
-// scratch: bucket counters[kPlanMaxBins] and tile cursors[ntiles], each region
-// aligned to 256 bytes.
+// tile_start[ntiles], tile_end[ntiles], tile_order[ntiles], tile_rois[capacity], and
+// the plan's scratch: bucket counters[kPlanMaxBins], each region aligned to 256 bytes.
 constexpr size_t kHeader = 256;
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 size_t perm_offset() { return kHeader; }
 size_t keys_offset(int64_t K) { return kHeader + align256(static_cast<size_t>(K) * 4); }
 size_t tiles_offset(int64_t K) { return kHeader + 2 * align256(static_cast<size_t>(K) * 4); }
+size_t tile_end_offset(int64_t K, const TileLayout &t) {
+    return tiles_offset(K) + align256(static_cast<size_t>(t.ntiles) * 4);
+}
 size_t tile_order_offset(int64_t K, const TileLayout &t) {
-    return tiles_offset(K) + align256(static_cast<size_t>(t.ntiles + 1) * 4);
+    return tile_end_offset(K, t) + align256(static_cast<size_t>(t.ntiles) * 4);
 }
 size_t tile_rois_offset(int64_t K, const TileLayout &t) {
     return tile_order_offset(K, t) + align256(static_cast<size_t>(t.ntiles) * 4);
@@ -34,16 +36,14 @@ size_t tile_rois_offset(int64_t K, const TileLayout &t) {
 size_t key_count_offset(int64_t K, const TileLayout &t) {
     return tile_rois_offset(K, t) + align256(static_cast<size_t>(t.capacity) * 4);
 }
-size_t tile_cursor_offset(int64_t K, const TileLayout &t) {
-    return key_count_offset(K, t) + align256(static_cast<size_t>(kPlanMaxBins) * 4);
-}
 size_t workspace_bytes_for(int64_t K, const TileLayout &t) {
-    return tile_cursor_offset(K, t) + align256(static_cast<size_t>(t.ntiles) * 4);
+    return key_count_offset(K, t) + align256(static_cast<size_t>(kPlanMaxBins) * 4);
 }
 
 // Bin-tiles of 2^shift pixels per (level, image): the smallest shift >= 4 whose tile
-// count fits the plan kernel's LDS histogram.  capacity bounds the number of
-// (tile, RoI) pairs: a RoI meets at most every tile of one image-level.  Binning is
+// count fits the plan kernel's LDS histogram.  capacity bounds the slots of the tile
+// lists: the lists of the RoIs of one (level, image) take that bucket's RoI count
+// times its tiles, at most K times the most tiles of one image-level.  Binning is
 // switched off (ntiles = 0) when that bound would exceed 2^28 pairs.
 constexpr int64_t kMaxPairs = int64_t(1) << 28;
 
@@ -248,10 +248,13 @@ re_status_t plan_args(const LevelTable &t, const float *rois, int64_t num_rois, 
         base += (a.batch_in_key ? t.N : 1) * a.ncx[l] * a.ncy[l];
     }
     a.tile_start = reinterpret_cast<int32_t *>(ws + tiles_offset(num_rois));
+    a.tile_end = reinterpret_cast<int32_t *>(ws + tile_end_offset(num_rois, tl));
     a.tile_rois = reinterpret_cast<int32_t *>(ws + tile_rois_offset(num_rois, tl));
     a.tile_order = reinterpret_cast<int32_t *>(ws + tile_order_offset(num_rois, tl));
     a.key_count = reinterpret_cast<int32_t *>(ws + key_count_offset(num_rois, tl));
-    a.tile_cursor = reinterpret_cast<int32_t *>(ws + tile_cursor_offset(num_rois, tl));
+    // the tile lists are bucketed by (level, image): every tile's bucket must be one
+    // key range (always so when the tiles fit: cells then fit at a shift no larger)
+    if (tl.ntiles > 0 && !a.batch_in_key) return RE_ERR_UNSUPPORTED;
     a.ntiles = tl.ntiles;
     a.capacity = static_cast<int32_t>(tl.capacity);
     a.tile_shift = tl.shift;
@@ -261,6 +264,7 @@ re_status_t plan_args(const LevelTable &t, const float *rois, int64_t num_rois, 
         a.tbase[l] = tl.tbase[l];
     }
     a.tbase[kMaxLevels] = tl.tbase[kMaxLevels];
+    plan_bands(a);
     *out = a;
     return RE_OK;
 }
@@ -600,6 +604,7 @@ GatherHead gather_head(const BwdHead &h, const TileLayout &tl) {
     g.rois = h.rois;
     g.roi_levels = h.roi_levels;
     g.tile_start = reinterpret_cast<const int32_t *>(ws + tiles_offset(h.K));
+    g.tile_end = reinterpret_cast<const int32_t *>(ws + tile_end_offset(h.K, tl));
     g.tile_rois = reinterpret_cast<const int32_t *>(ws + tile_rois_offset(h.K, tl));
     g.K = static_cast<int32_t>(h.K);
     g.aligned = h.aligned;

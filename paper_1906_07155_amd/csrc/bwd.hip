@@ -420,7 +420,7 @@ __device__ __forceinline__ void gather_phase(const GatherHead &h, const LevelTab
     const LevelArg &L = x.L;
     const int l = x.l, b = x.b, R0 = x.R0, Q0 = x.Q0;
     int s0 = h.tile_start[t];
-    int s1 = h.tile_start[t + 1];
+    int s1 = h.tile_end[t];
     s0 = max(0, min(s0, h.capacity));
     s1 = max(s0, min(s1, h.capacity));
     constexpr float inv_count = 1.0f / static_cast<float>(S * S);

@@ -27,19 +27,26 @@ struct PlanArgs {
     int32_t ncx[kMaxLevels], ncy[kMaxLevels], base[kMaxLevels];
     float scale[kMaxLevels];
     // Tile binning for the gather backward: bin-tiles of 2^tile_shift pixels per
-    // (level, image); tile_start[ntiles + 1] / tile_rois[capacity] form a CSR list of
-    // the RoIs whose (conservative) footprint box meets each tile.
-    int32_t *tile_start;
-    int32_t *tile_rois;
+    // (level, image); tile_rois[tile_start[t], tile_end[t]) lists the RoIs whose
+    // (conservative) footprint box meets tile t.
+    int32_t *tile_start;   // [ntiles]
+    int32_t *tile_end;     // [ntiles] (the fill's cursors until the lists are done)
+    int32_t *tile_rois;    // [capacity]
     int32_t *tile_order;   // [ntiles]: tiles by decreasing list length
-    int32_t *key_count;    // [nbins] scratch: bucket counts, then cursors (the tile
-                           // counts live in tile_start until they are scanned)
-    int32_t *tile_cursor;  // [ntiles] scratch: next free slot of each tile's list
+    int32_t *key_count;    // [nbins] scratch: bucket counts, then cursors
     int32_t ntiles;
     int32_t capacity;
     int32_t tile_shift;
     int32_t pad2;
     int32_t ntx[kMaxLevels], nty[kMaxLevels], tbase[kMaxLevels + 1];
+    // One-launch plan: bands of band_rows[l] tile rows of one (level, image), band ids
+    // [band_base[l], band_base[l + 1]) on level l; the list-length difference grids,
+    // (nty + 1) x (ntx + 1) per (level, image), level l's from dbase[l], ndiff in all.
+    int32_t nbands;
+    int32_t ndiff;
+    int32_t band_base[kMaxLevels + 1];
+    int32_t band_rows[kMaxLevels];
+    int32_t dbase[kMaxLevels];
 };
 
 // Tile layout shared by the plan and the gather backward (a function of the level
@@ -56,7 +63,8 @@ struct GatherHead {
     const void *gout;            // [K][C][PH][PW]
     const float *rois;
     const int32_t *roi_levels;
-    const int32_t *tile_start;   // the head's plan: CSR tile -> RoI lists
+    const int32_t *tile_start;   // the head's plan: tile -> RoI lists
+    const int32_t *tile_end;
     const int32_t *tile_rois;
     int32_t K;
     int32_t aligned;
@@ -298,13 +306,17 @@ struct NmsBatchArgs {
 
 hipError_t launch_nms_batched(const NmsBatchArgs &a, hipStream_t stream);
 
-// Inclusive prefix sum across the 64 lanes of a wavefront.
-__device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int t = __shfl_up(v, off);
-        if (lane >= off) v += t;
-    }
+// Inclusive prefix sum across the 64 lanes of a wavefront, in DPP moves: shifts by
+// 1, 2, 4 and 8 lanes inside each row of 16 (lanes shifted in from outside the row
+// add the old value, 0), then the last lane of row 0 (and of row 2) broadcast into
+// row 1 (and row 3), then the last lane of row 1 into rows 2 and 3.
+__device__ __forceinline__ int wave_inclusive_scan(int v, int /*lane*/) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31
     return v;
 }
 
@@ -345,6 +357,7 @@ __device__ __forceinline__ int block_exclusive_scan(int32_t *hist, int n, int32_
 hipError_t launch_level_map(const float *rois, int32_t K, int32_t L, float finest_scale,
                             int32_t box_plus1, int32_t *out, hipStream_t stream);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);
+void plan_bands(PlanArgs &a);   // fills nbands, ndiff, band_base, band_rows, dbase
 
 // Forward: `fast` selects the channels-last kernels (every level stride_c == 1 and
 // (PH, PW, S) in the specialised set); otherwise the general strided kernel.
