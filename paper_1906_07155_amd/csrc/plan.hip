@@ -187,8 +187,14 @@ constexpr int kPlanLanes = 16;
 // ---------------------------------------------------------------------------
 constexpr int kPlanOne = 8192;
 constexpr int kBandTiles = 2048;   // LDS cursors of one band
-constexpr int kBandCand = 4096;    // RoIs of one band kept in LDS (beyond: a second scan)
-constexpr int kBandTarget = 128;   // tiles per band aimed at
+#ifndef REX_BAND_CAND
+#define REX_BAND_CAND 2048
+#endif
+constexpr int kBandCand = REX_BAND_CAND;   // RoIs of one band kept in LDS (beyond: a second scan)
+#ifndef REX_BAND_TARGET
+#define REX_BAND_TARGET 64
+#endif
+constexpr int kBandTarget = REX_BAND_TARGET;   // tiles per band aimed at
 constexpr int kPlanWords = 24576;  // 96 KiB of LDS per workgroup
 
 // fn(k, roi) for every RoI, each thread's RoIs loaded kRoiBatch at a time.
