@@ -268,6 +268,40 @@ def main():
         alt = {"bwd": other, "ms_per_step": round(alt_ms, 5),
                "kernel_ms": {n: round(v, 5) for n, v in alt_per.items()}}
 
+    # NCHW levels: the same step with the pyramid converted to channels-last first and
+    # the gradients converted back (torch copies), for callers choosing between them
+    via_cl = None
+    if args.layout == "nchw" and backward:
+        cl_feats = [f.contiguous(memory_format=torch.channels_last) for f in feats]
+        cl_grads = [torch.empty(f.shape, dtype=torch.float32, device=dev).contiguous(
+            memory_format=torch.channels_last) for f in feats]
+
+        def step_cl(ev=None):
+            if ev is not None:
+                ev[0].record(stream)
+            for d, f in zip(cl_feats, feats):
+                d.copy_(f)
+            if ev is not None:
+                ev[1].record(stream)
+            rex.plan(cl_feats, wl.scales, rois, wl.finest_scale, levels_out=levels, workspace=ws)
+            rex.roi_align_fwd(cl_feats, wl.scales, rois, levels, out_hw, S, aligned, out=out,
+                              workspace=ws)
+            rex.roi_align_bwd(gout, rois, levels, out_hw, S, aligned, cl_grads, wl.scales,
+                              zero_init=True, workspace=ws, algorithm="gather")
+            if ev is not None:
+                ev[2].record(stream)
+            for d, g in zip(grads, cl_grads):
+                d.copy_(g)
+            if ev is not None:
+                ev[3].record(stream)
+
+        for _ in range(3):
+            step_cl()
+        vms, vper, _ = time_two_passes(step_cl, ["to_channels_last", "plan_fwd_bwd",
+                                                 "grads_to_nchw"], max(3, args.steps // 2), stream)
+        via_cl = {"ms_per_step": round(vms, 5), "kernel_ms": {n: round(v, 5) for n, v in vper.items()}}
+        del cl_feats, cl_grads
+
     # cold: each step after a 1 GiB write that evicts L2 and the 256 MB MALL
     cold = None
     if args.cold_reps > 0:
@@ -372,6 +406,7 @@ def main():
         "other_bwd": alt,
         "cold": cold,
         "layout": args.layout,
+        "nchw_via_channels_last": via_cl,
         "plan": not args.no_plan,
         "kernel_source_hash": kernel_source_hash(),
         "kernel_source_hashes": {k: kernel_source_hash(k) for k in KERNEL_SOURCES},

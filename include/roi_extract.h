@@ -208,8 +208,10 @@ re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_lev
 /* Backward algorithms. */
 #define RE_BWD_AUTO 0       /* gather when eligible, else scatter */
 #define RE_BWD_SCATTER 1    /* per-RoI scatter, fp32 atomics (a7) */
-#define RE_BWD_GATHER 2     /* per-tile gather, plain stores (needs a plan, stride_c == 1,
-                               out 7x7 or 14x14 with sampling_ratio 2) */
+#define RE_BWD_GATHER 2     /* per-tile gather, plain stores (needs a plan, gradient
+                               levels whose images span less than 2^30 bytes -- channels-
+                               last or contiguous NCHW alike -- and out 7x7 or 14x14 with
+                               sampling_ratio 2) */
 
 /* a6 + a7 -- RoIAlign backward: adds the transpose of the forward applied to
  * grad_out into the gradient pyramid (clears it first when zero_init != 0).
@@ -255,8 +257,8 @@ typedef struct {
 /* Backward of num_heads heads (1..RE_MAX_HEADS) into one gradient pyramid:
  * grad_F += sum over heads of (head's transpose applied to its grad_out), after
  * clearing when zero_init != 0; each head is defined as for roi_align_bwd.  Heads
- * are taken in pairs: when both heads of a pair take the gather (plan, channels-last
- * levels, 7x7 or 14x14 grid, sampling_ratio 2, one gradient dtype and one tile
+ * are taken in pairs: when both heads of a pair take the gather (plan, levels the
+ * gather can address, 7x7 or 14x14 grid, sampling_ratio 2, one gradient dtype and one tile
  * layout), the pair is a single pass in which every gradient element is written once;
  * otherwise the heads run one after the other (gather or scatter, as roi_align_bwd
  * with RE_BWD_AUTO).  Results equal the sum of the single-head calls up to the fp32

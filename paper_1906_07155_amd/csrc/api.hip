@@ -593,8 +593,18 @@ re_status_t check_head(const BwdHead &h, int32_t num_levels, const LevelTable &t
     return check_plan(h.plan, h.plan_bytes, h.K, t);
 }
 
-bool head_gather_ok(const BwdHead &h, const LevelTable &t, bool cl, const TileLayout &tl) {
-    return h.plan && cl && tl.ntiles > 0 && h.K > 0 && gather_available(h.out_h, h.out_w, h.S);
+// The gather stores through a buffer resource over one image of a level, so it takes
+// any strides for which an image spans less than 2^30 bytes (img_bytes != 0): the
+// channels-last pyramid and contiguous NCHW alike.
+bool levels_buffered(const LevelTable &t) {
+    for (int l = 0; l < t.num; ++l)
+        if (t.l[l].img_bytes == 0) return false;
+    return true;
+}
+
+bool head_gather_ok(const BwdHead &h, const LevelTable &t, const TileLayout &tl) {
+    return h.plan && levels_buffered(t) && tl.ntiles > 0 && h.K > 0 &&
+           gather_available(h.out_h, h.out_w, h.S);
 }
 
 GatherHead gather_head(const BwdHead &h, const TileLayout &tl) {
@@ -643,7 +653,7 @@ GatherArgs gather_args(const LevelTable &t, const BwdHead &h0, const TileLayout 
 re_status_t bwd_head(const BwdHead &h, const LevelTable &t, bool cl, const int64_t *numel,
                      const int *dense, int32_t zero_init, int32_t algorithm, hipStream_t s) {
     const TileLayout tl = tile_layout(t, h.K);
-    const bool gather_ok = head_gather_ok(h, t, cl, tl);
+    const bool gather_ok = head_gather_ok(h, t, tl);
     if (algorithm == RE_BWD_GATHER && !gather_ok && h.K > 0) return RE_ERR_UNSUPPORTED;
     if (gather_ok && algorithm != RE_BWD_SCATTER)
         return from_hip(launch_gather(gather_args(t, h, tl, zero_init), h.gdt, s));
@@ -732,7 +742,7 @@ re_status_t roi_align_bwd_multi(const re_head_t *heads, int32_t num_heads,
         if (i + 1 < num_heads) {
             const BwdHead &a = hs[i], &b = hs[i + 1];
             const TileLayout ta = tile_layout(t, a.K), tb = tile_layout(t, b.K);
-            if (head_gather_ok(a, t, cl, ta) && head_gather_ok(b, t, cl, tb) &&
+            if (head_gather_ok(a, t, ta) && head_gather_ok(b, t, tb) &&
                 ta.shift == tb.shift && ta.ntiles == tb.ntiles && a.gdt == b.gdt &&
                 a.S == b.S) {
                 GatherArgs g = gather_args(t, a, ta, clear);

@@ -711,18 +711,42 @@ __device__ __forceinline__ void gather_store(const GatherTile &x, int zero_init,
     const LevelArg &L = x.L;
     const char *img = static_cast<const char *>(L.data) + static_cast<int64_t>(x.b) * L.sn * 4;
     const __amdgpu_buffer_rsrc_t dst = make_rsrc(img, L.img_bytes);
-    const uint32_t vo = lane_on ? static_cast<uint32_t>(c) * 4u : kBufOOB;
+    // the lane's channel: stride_c elements apart (1 for channels-last levels)
+    const uint32_t vo = lane_on ? static_cast<uint32_t>(c) * static_cast<uint32_t>(L.sc) * 4u
+                                : kBufOOB;
     const uint32_t sh4 = static_cast<uint32_t>(L.sh) * 4u;
     const uint32_t sw4 = static_cast<uint32_t>(L.sw) * 4u;
     const uint32_t base = static_cast<uint32_t>(x.R0) * sh4 + static_cast<uint32_t>(x.Q0) * sw4;
+    if (L.sc != 1 && L.sw == 1 && zero_init && x.R0 + 8 <= L.H && x.Q0 + 8 <= L.W) {
+        // Channels in separate planes (NCHW): a lane's row of 8 pixels is 32 contiguous
+        // bytes, written as two 16-byte stores, and the neighbouring quadrant's wave
+        // writes the other half of the 64-byte run; ordinary stores, so the L2 merges
+        // the halves before they go to memory.
+#pragma unroll
+        for (int rr = 0; rr < 8; ++rr) {
+            const uint32_t o = base + rr * sh4;
+            const u32x4 lo = {__float_as_uint(acc[rr][0]), __float_as_uint(acc[rr][1]),
+                              __float_as_uint(acc[rr][2]), __float_as_uint(acc[rr][3])};
+            const u32x4 hi = {__float_as_uint(acc[rr][4]), __float_as_uint(acc[rr][5]),
+                              __float_as_uint(acc[rr][6]), __float_as_uint(acc[rr][7])};
+            __builtin_amdgcn_raw_buffer_store_b128(lo, dst, vo, o, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(hi, dst, vo, o + 16u, 0);
+        }
+        return;
+    }
+    // channel-contiguous lanes stream past the L2; strided channels go through it
+    const bool nt = L.sc == 1;
+    auto st32 = [&](float v, uint32_t lane_off, uint32_t off) {
+        if (nt) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), dst, lane_off, off, kStoreNT);
+        else __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), dst, lane_off, off, 0);
+    };
     if (zero_init && x.R0 + 8 <= L.H && x.Q0 + 8 <= L.W) {
         // a whole quadrant inside the map: 64 plain stores, no per-pixel checks
 #pragma unroll
         for (int rr = 0; rr < 8; ++rr)
 #pragma unroll
             for (int q = 0; q < 8; ++q)
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[rr][q]), dst, vo,
-                                                      base + rr * sh4 + q * sw4, kStoreNT);
+                st32(acc[rr][q], vo, base + rr * sh4 + q * sw4);
         return;
     }
     // Quadrants cut by the map edge, or accumulation: pixels off the map take an
@@ -748,8 +772,7 @@ __device__ __forceinline__ void gather_store(const GatherTile &x, int zero_init,
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q)
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[q]), dst, vq[q],
-                                                  base + rr * sh4 + q * sw4, kStoreNT);
+            st32(v[q], vq[q], base + rr * sh4 + q * sw4);
         asm volatile("" ::: "memory");
     }
 }

@@ -121,6 +121,7 @@ constexpr uint32_t kBufOOB = 0x40000000u;
 constexpr uint32_t kBufMaxBytes = 0x40000000u;
 constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, no swizzle (gfx9 family)
 constexpr int kStoreNT = 2;              // buffer store cache policy: non-temporal
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // a 16-byte buffer store
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0,

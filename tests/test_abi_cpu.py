@@ -159,11 +159,13 @@ def test_backward_validation(L):
     assert L.roi_extract_workspace_size(_levels(), 2, 4, ctypes.byref(n)) == OK
     assert _bwd(L, algo=2, plan=FAKE, plan_bytes=n.value, oh=5) == UNSUPPORTED   # 5x7 grid
     assert _bwd(L, algo=2, plan=FAKE, plan_bytes=n.value, sr=0) == UNSUPPORTED   # adaptive
-    nchw = _levels()
+    # the gather stores through 32-bit buffer offsets: levels whose images span 2^30
+    # bytes or more (here a channel stride of 2^28 elements) take the scatter only
+    wide = _levels()
     for i in range(2):
-        nchw[i].stride_c, nchw[i].stride_h, nchw[i].stride_w = nchw[i].h * nchw[i].w, nchw[i].w, 1
-        nchw[i].stride_n = nchw[i].c * nchw[i].h * nchw[i].w
-    assert _bwd(L, levels=nchw, algo=2, plan=FAKE, plan_bytes=n.value) == UNSUPPORTED
+        wide[i].stride_c, wide[i].stride_h, wide[i].stride_w = 1 << 28, wide[i].w, 1
+        wide[i].stride_n = wide[i].c << 28
+    assert _bwd(L, levels=wide, algo=2, plan=FAKE, plan_bytes=n.value) == UNSUPPORTED
     assert L.roi_extract_zero_grad(_levels(dtype=1), 2, None) == UNSUPPORTED
     assert L.roi_extract_zero_grad(None, 2, None) == INVALID
 

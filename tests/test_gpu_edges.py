@@ -94,10 +94,10 @@ def run(name, shapes, scales, rois, out_hw=(7, 7), S=2, aligned=True, fdt="f32",
                                 "parity")
     aref = oracle.roi_align_bwd(np.abs(g64), shapes, scales, rois, lv, out_hw[0], out_hw[1], S,
                                 aligned, "parity")
-    # scatter always; the gather where it applies (plan, channels-last, 7x7 / 14x14, S = 2)
+    # scatter always; the gather where it applies (plan, 7x7 / 14x14, S = 2; any level
+    # layout whose images span less than 2^30 bytes, channels-last or NCHW)
     algos = ["scatter"]
-    if ws is not None and layout in ("cl", "cl_view") and S == 2 and tuple(out_hw) in (
-            (7, 7), (14, 14)):
+    if ws is not None and S == 2 and tuple(out_hw) in ((7, 7), (14, 14)):
         algos.append("gather")
     for algo in algos:
         grads = [torch.full(s, 7.0, dtype=torch.float32, device="cuda") for s in shapes]

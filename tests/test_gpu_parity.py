@@ -54,10 +54,11 @@ def _run_fwd(c: Case, plan=True):
     return levels, ws, out
 
 
-def _run_bwd(c: Case, levels, ws, g_np, algorithm):
+def _run_bwd(c: Case, levels, ws, g_np, algorithm, layout="cl"):
     g = to_device(g_np, c.wl.grad_dtype, layout="nchw")
-    grads = [torch.full(s, 3.0, dtype=torch.float32, device="cuda").contiguous(
-        memory_format=torch.channels_last) for s in c.shapes]
+    grads = [torch.full(s, 3.0, dtype=torch.float32, device="cuda") for s in c.shapes]
+    if layout == "cl":
+        grads = [x.contiguous(memory_format=torch.channels_last) for x in grads]
     rex.roi_align_bwd(g, c.rois_dev, levels, c.wl.out_hw, c.wl.sampling_ratio, c.wl.aligned,
                       grads, c.scales, zero_init=True, workspace=ws, algorithm=algorithm)
     torch.cuda.synchronize()
@@ -102,14 +103,33 @@ def test_forward_full(idx, head, fdt):
     log("  max abs err %.3e" % err)
 
 
-@pytest.mark.parametrize("algorithm", ["scatter", "gather"])
+def test_forward_full_nchw():
+    """Workload 2 forward on contiguous NCHW levels (the general strided kernel), every
+    element against the oracle."""
+    c = _case(2)
+    log("forward full, NCHW levels: workload 2, K=%d" % c.K)
+    feats = [to_device(f, c.wl.feat_dtype, "nchw") for f in c.feats_np]
+    levels, ws = rex.plan(feats, c.scales, c.rois_dev, c.wl.finest_scale)
+    out = rex.roi_align_fwd(feats, c.scales, c.rois_dev, levels, c.wl.out_hw,
+                            c.wl.sampling_ratio, c.wl.aligned, workspace=ws)
+    torch.cuda.synchronize()
+    ref = oracle.roi_align_fwd([as_f64(f, c.wl.feat_dtype) for f in c.feats_np], c.scales,
+                               c.rois, c.oracle_levels(), *c.wl.out_hw, c.wl.sampling_ratio,
+                               c.wl.aligned, "parity")
+    check_fwd(from_device(out), ref, False, "workload 2 NCHW forward")
+
+
+@pytest.mark.parametrize("algorithm,layout", [("scatter", "cl"), ("gather", "cl"),
+                                              ("gather", "nchw")])
 @pytest.mark.parametrize("idx,head,fdt", [(2, None, None), (3, None, None)])
-def test_backward_full(idx, head, fdt, algorithm):
+def test_backward_full(idx, head, fdt, algorithm, layout):
+    """Full-size backward; the gather also into contiguous NCHW gradients (the RoIs are
+    planned on the channels-last features, the plan does not depend on the layout)."""
     c = _case(idx, head, fdt)
-    log("backward full (%s): workload %d, K=%d" % (algorithm, idx, c.K))
+    log("backward full (%s, %s gradients): workload %d, K=%d" % (algorithm, layout, idx, c.K))
     levels, ws, _ = _run_fwd(c)
     g = c.wl.grad()
-    grads = _run_bwd(c, levels, ws, g, algorithm)
+    grads = _run_bwd(c, levels, ws, g, algorithm, layout)
     ref_lv = c.oracle_levels()
     g64 = as_f64(g, c.wl.grad_dtype)
     ref = oracle.roi_align_bwd(g64, c.shapes, c.scales, c.rois, ref_lv, *c.wl.out_hw,
