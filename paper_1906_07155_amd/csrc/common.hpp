@@ -293,6 +293,14 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// n / d for 0 <= n < 2^21 - 1 and d >= 1, exactly: (n + 1/2) times the hardware
+// reciprocal of d (1 ulp) is within (n + 1/2) 2^-22 / d < 1 / (2d) of (n + 1/2) / d,
+// closer than the nearest integer.
+__device__ __forceinline__ int small_div_exact(int n, int d) {
+    return static_cast<int>((static_cast<float>(n) + 0.5f) *
+                            __builtin_amdgcn_rcpf(static_cast<float>(d)));
+}
+
 __device__ __forceinline__ int uniform_i(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ float uniform_f(float v) {
     return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));

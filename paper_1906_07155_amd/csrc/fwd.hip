@@ -15,6 +15,9 @@
 //                       two small separable products.  Results are transposed
 //                       through LDS so the [C][PH][PW] block of the RoI is stored
 //                       contiguously at its original RoI index.
+//   fwd_nchw_kernel     other strides (channels in separate planes), 7x7 / 14x14 with
+//                       sampling ratio 2: a RoI's distinct tap rows x columns staged in
+//                       LDS per channel, lanes along x.
 //   fwd_generic_kernel  any strides, output size and sampling ratio: one thread per
 //                       output element.
 #include "internal.hpp"
@@ -28,6 +31,16 @@ namespace rex {
 #endif
 #ifndef REX_FWD_CX
 #define REX_FWD_CX 8
+#endif
+// channels per workgroup of the NCHW kernel (7x7, 14x14 grids): the kernel waits on
+// dependent loads, so more resident workgroups (less LDS each) beat fewer, fuller ones
+// (batch-2 box head: 2 channels 244 us, 4: 164, 8: 183, 16: 260; mask head 1 or 2: 138,
+// 146)
+#ifndef REX_NCHW_CC7
+#define REX_NCHW_CC7 4
+#endif
+#ifndef REX_NCHW_CC14
+#define REX_NCHW_CC14 1
 #endif
 // columns per load unit with two bf16 channels per lane (7x7 grid)
 #ifndef REX_FWD_CX2_BF16
@@ -644,9 +657,214 @@ static hipError_t launch_fwd_typed(FwdArgs a, bool fast, hipStream_t stream) {
         // 336 vs 321 us batch 16)
         return launch_fwd_cl<T, TO, 14, 14, 4, 16, 1>(a, stream);
     }
+    // other layouts (channels in separate planes): the staged kernel on the same grids
+    if (fwd_fast_available(a.PH, a.PW, a.S) && static_cast<int64_t>(a.K) * a.lv.C < (int64_t(1) << 30)) {
+        if (a.PH == 7) return launch_fwd_nchw<T, TO, 7, 7, REX_NCHW_CC7>(a, stream);
+        return launch_fwd_nchw<T, TO, 14, 14, REX_NCHW_CC14>(a, stream);
+    }
     const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * a.PH * a.PW;
     const int64_t blocks = std::min<int64_t>((total + 255) / 256, 16384);
     fwd_generic_kernel<T, TO><<<static_cast<uint32_t>(blocks), 256, 0, stream>>>(a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Channels in separate planes (NCHW): staged footprint, lanes along x
+// ---------------------------------------------------------------------------
+//
+// One workgroup per (RoI, CC channels).  The sample positions of an axis grow with
+// the sample index, so the tap rows (columns) form runs of equal `lo`, each adding
+// `lo` and, unless it is the next run's `lo` or the map edge, `lo + 1` to the
+// distinct set: one wave lists the distinct rows and gives every sample the indices
+// of its two taps in the list (a scan over the run ends).  The workgroup then loads
+// every channel's distinct rows x distinct columns into LDS with consecutive lanes
+// on consecutive columns (a RoI's columns are a contiguous run unless its bins are
+// wider than a pixel), reduces each tap row along x per bin column, and the tap
+// rows along y per bin.  Any other grid, or a RoI whose taps are not monotone, takes
+// the per-output path.
+template <int N>
+struct NchwAxis {
+    int idx_lo[N], idx_hi[N];   // per sample: its taps' positions in the distinct list
+    float w_lo[N], w_hi[N];     // bilinear weights (0 for a sample off the map)
+    int list[2 * N];            // distinct tap rows (columns)
+    int n;                      // their count
+    int bad;                    // taps not monotone in the sample index
+};
+
+// Lanes 0..N-1 of one wave: sample u of axis `ax` on a map of `size` pixels.
+template <int N, int S>
+__device__ __forceinline__ void nchw_axis(const Axis &ax, int size, bool active,
+                                          NchwAxis<N> &o) {
+    const int lane = threadIdx.x & 63;
+    Tap tp{-1, -1, 0.0f, 0.0f};
+    if (lane < N && active) tp = axis_tap(ax, lane / S, lane % S, size);
+    const bool valid = tp.lo >= 0;
+    const int nlo = __shfl_down(tp.lo, 1);      // the next sample's lo (-1 past the last)
+    const bool next_valid = lane + 1 < N && nlo >= 0;
+    const bool run_end = valid && (!next_valid || nlo != tp.lo);
+    const bool extra = run_end && tp.hi != tp.lo && !(next_valid && nlo == tp.lo + 1);
+    const int contrib = run_end ? 1 + (extra ? 1 : 0) : 0;
+    const int incl = wave_inclusive_scan(contrib, lane);
+    const int pos = incl - contrib;             // the run's position (every sample of it)
+    const uint64_t bad = __ballot(valid && next_valid && nlo < tp.lo);
+    if (lane < N) {
+        o.idx_lo[lane] = valid ? pos : -1;   // -1: the sample is off the map
+        o.idx_hi[lane] = valid ? (tp.hi == tp.lo ? pos : pos + 1) : -1;
+        o.w_lo[lane] = tp.wlo;
+        o.w_hi[lane] = tp.whi;
+    }
+    if (run_end) {
+        o.list[pos] = tp.lo;
+        if (extra) o.list[pos + 1] = tp.lo + 1;
+    }
+    if (lane == 63) {
+        o.n = incl;
+        o.bad = bad != 0;
+    }
+}
+
+template <int PH, int PW, int CC>
+struct NchwSmem {
+    static constexpr int S = 2;
+    static constexpr int NR = PH * S, NCOL = PW * S;
+    NchwAxis<NR> y;
+    NchwAxis<NCOL> x;
+    float fw[CC * 2 * NR * 2 * NCOL];   // [channel][distinct row][distinct column]
+    float rw[CC * 2 * NR * PW];         // [channel][distinct row][bin column]
+};
+
+template <typename T, typename TO, int PH, int PW, int CC>
+__global__ __launch_bounds__(256) void fwd_nchw_kernel(FwdArgs a) {
+    constexpr int S = 2;
+    using SM = NchwSmem<PH, PW, CC>;
+    constexpr int NR = SM::NR, NCOL = SM::NCOL;
+    __shared__ SM sm;
+    const FwdArgs &ka = *(const FwdArgs *)__builtin_amdgcn_kernarg_segment_ptr();
+    const LevelTable &lv = ka.lv;
+    // channel chunk outer, plan order inner: neighbouring workgroups read the same
+    // planes around neighbouring RoIs
+    const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int chunk = static_cast<int>(lid / static_cast<uint32_t>(ka.K));
+    const int slot = static_cast<int>(lid) - chunk * ka.K;
+    const int c0 = chunk * CC;
+    int k = uniform_i(ka.perm ? ka.perm[slot] : slot);
+    const bool kvalid = k >= 0 && k < ka.K;
+    if (!kvalid) k = 0;
+    const float *r = ka.rois + 5 * static_cast<int64_t>(k);
+    const float rb = r[0], x1 = r[1], y1 = r[2], x2 = r[3], y2 = r[4];
+    const int lvl = uniform_i(ka.roi_levels ? ka.roi_levels[k] : 0);
+    const bool lvalid = lvl >= 0 && lvl < lv.num;
+    const LevelArg L = level_at(lv, lvalid ? lvl : 0);
+    const int b = roi_batch(rb, lv.N);
+    const bool active = kvalid && lvalid && b >= 0;
+    const int t = threadIdx.x;
+    const int wave = t >> 6;
+    const Axis ax = axis_setup(x1, x2, L.scale, ka.aligned, PW, S);
+    const Axis ay = axis_setup(y1, y2, L.scale, ka.aligned, PH, S);
+    if (wave == 0) nchw_axis<NR, S>(ay, L.H, active, sm.y);
+    else if (wave == 1) nchw_axis<NCOL, S>(ax, L.W, active, sm.x);
+    __syncthreads();
+    const int nr = sm.y.n, nc = sm.x.n;
+    const int nch = min(CC, lv.C - c0);
+    const int64_t kout = static_cast<int64_t>(k) * lv.C * PH * PW;
+    constexpr float inv_count = 1.0f / static_cast<float>(S * S);
+    if (!kvalid) return;   // a plan slot past the RoIs (never with a valid plan)
+
+    if (sm.y.bad || sm.x.bad) {
+        // taps out of order (binary32 ties): each output from its own samples
+        for (int e = t; e < nch * PH * PW; e += 256) {
+            const int c = e / (PH * PW), j = e - c * (PH * PW);
+            const int ph = j / PW, pw = j - ph * PW;
+            float sum = 0.0f;
+            if (active) {
+                const gcptr<T> base = as_global<T>(L.data) + b * L.sn + (c0 + c) * L.sc;
+                for (int iy = 0; iy < S; ++iy) {
+                    const Tap ty = axis_tap(ay, ph, iy, L.H);
+                    if (ty.lo < 0) continue;
+                    for (int ix = 0; ix < S; ++ix) {
+                        const Tap tx = axis_tap(ax, pw, ix, L.W);
+                        if (tx.lo < 0) continue;
+                        sum = fmaf(ty.wlo * tx.wlo, load_f32(base + ty.lo * L.sh + tx.lo * L.sw), sum);
+                        sum = fmaf(ty.wlo * tx.whi, load_f32(base + ty.lo * L.sh + tx.hi * L.sw), sum);
+                        sum = fmaf(ty.whi * tx.wlo, load_f32(base + ty.hi * L.sh + tx.lo * L.sw), sum);
+                        sum = fmaf(ty.whi * tx.whi, load_f32(base + ty.hi * L.sh + tx.hi * L.sw), sum);
+                    }
+                }
+            }
+            store_f32(as_global_mut<TO>(ka.out) + kout + static_cast<int64_t>(c0) * PH * PW + e,
+                      sum * inv_count);
+        }
+        return;
+    }
+
+    // a4: the footprint of every channel of the chunk, eight loads in flight per lane
+    const int per_c = nr * nc;
+    const int nload = nch * per_c;
+    const gcptr<T> img = as_global<T>(L.data) + b * L.sn + static_cast<int64_t>(c0) * L.sc;
+    for (int e0 = t; e0 < nload; e0 += 8 * 256) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int e = e0 + u * 256;
+            v[u] = 0.0f;
+            if (e < nload) {
+                const int c = small_div_exact(e, per_c);
+                const int rem = e - c * per_c;
+                const int j = small_div_exact(rem, nc);
+                const int i = rem - j * nc;
+                v[u] = load_f32(img + c * L.sc + sm.y.list[j] * L.sh + sm.x.list[i] * L.sw);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (e0 + u * 256 < nload) sm.fw[e0 + u * 256] = v[u];
+    }
+    __syncthreads();
+    // along x: every distinct tap row of every channel, per bin column
+    const int nx = nch * nr * PW;
+    for (int e = t; e < nx; e += 256) {
+        const int cj = small_div_exact(e, PW);          // channel * nr + row
+        const int pw = e - cj * PW;
+        const float *row = sm.fw + cj * nc;
+        float acc = 0.0f;
+#pragma unroll
+        for (int ix = 0; ix < S; ++ix) {
+            const int u = pw * S + ix;
+            const int il = sm.x.idx_lo[u];
+            if (il < 0) continue;   // off the map: no contribution
+            acc = fmaf(sm.x.w_lo[u], row[il], acc);
+            acc = fmaf(sm.x.w_hi[u], row[sm.x.idx_hi[u]], acc);
+        }
+        sm.rw[e] = acc;
+    }
+    __syncthreads();
+    // along y: every bin, then the output (written in order, one channel's bins
+    // contiguous)
+    for (int e = t; e < nch * PH * PW; e += 256) {
+        const int c = small_div_exact(e, PH * PW);
+        const int jj = e - c * (PH * PW);
+        const int ph = small_div_exact(jj, PW);
+        const int pw = jj - ph * PW;
+        const float *col = sm.rw + c * nr * PW + pw;
+        float acc = 0.0f;
+#pragma unroll
+        for (int iy = 0; iy < S; ++iy) {
+            const int u = ph * S + iy;
+            const int il = sm.y.idx_lo[u];
+            if (il < 0) continue;
+            acc = fmaf(sm.y.w_lo[u], col[il * PW], acc);
+            acc = fmaf(sm.y.w_hi[u], col[sm.y.idx_hi[u] * PW], acc);
+        }
+        store_f32(as_global_mut<TO>(ka.out) + kout + static_cast<int64_t>(c0) * PH * PW + e,
+                  acc * inv_count);
+    }
+}
+
+template <typename T, typename TO, int PH, int PW, int CC>
+static hipError_t launch_fwd_nchw(const FwdArgs &a, hipStream_t stream) {
+    const int64_t grid = static_cast<int64_t>(a.K) * ((a.lv.C + CC - 1) / CC);
+    if (grid >= (int64_t(1) << 31)) return hipErrorInvalidConfiguration;
+    fwd_nchw_kernel<T, TO, PH, PW, CC><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
     return hipGetLastError();
 }
 

@@ -220,11 +220,8 @@ __device__ __forceinline__ void for_rois(const PlanArgs &a, F &&fn) {
     }
 }
 
-// Exact quotient of non-negative integers n < 2^21 - 1 and d >= 1 (see box_row).
-__device__ __forceinline__ int small_div(int n, int d) {
-    return static_cast<int>((static_cast<float>(n) + 0.5f) *
-                            __builtin_amdgcn_rcpf(static_cast<float>(d)));
-}
+// Exact quotient of non-negative integers n < 2^21 - 1 and d >= 1.
+__device__ __forceinline__ int small_div(int n, int d) { return small_div_exact(n, d); }
 
 __device__ void plan_sort_role(const PlanArgs &a, const LevelTab &tb, int32_t *smem) {
     int32_t *hist = smem;                  // [nbins]
