@@ -1,12 +1,12 @@
 /*
  * roi_extract.h -- C ABI of the MI355X multi-level RoIAlign library.
  *
- * The operator is the RoIExtractor of MMDetection (arXiv 1906.07155, §3.1
- * "Model Representation"): RoI-wise features are taken from the corresponding
- * level of an FPN feature pyramid (§3.1, Neck) with a RoIPooling-like operator,
- * here RoIAlign (the Mask R-CNN operator, cited among the supported frameworks in
- * §2).  The paper runs these bbox/mask operations on the GPU (§1, "High
- * efficiency") and trains with forward and backward every iteration (§3.2).
+ * The operator is the RoIExtractor of MMDetection (arXiv 1906.07155, §3.1, model
+ * representation): the features of each RoI are pooled from one level of an FPN
+ * feature pyramid (§3.1, Neck), the level matched to the RoI's size, by a RoI
+ * pooling operator, here RoIAlign (the Mask R-CNN operator, cited among the
+ * supported frameworks in §2).  The paper runs these bbox and mask operations on
+ * the GPU (§1) and trains with a forward and a backward every iteration (§3.2).
  *
  * Conventions (the paper leaves them open; these are the library's definitions):
  *   - RoI k is 5 binary32 values (batch_index, x1, y1, x2, y2) in input-image
@@ -87,8 +87,8 @@ typedef struct {
     float reserved2;          /* must be 0 */
 } re_level_t;
 
-/* a1 -- FPN level of every RoI (§3.1: "the corresponding level of feature
- * pyramids").  rois: device float[num_rois][5]; levels_out: device
+/* a1 -- FPN level of every RoI (§3.1: each RoI is pooled from the pyramid level
+ * that matches its size).  rois: device float[num_rois][5]; levels_out: device
  * int32[num_rois], written with values in [0, num_levels).  num_levels in
  * [1, RE_MAX_LEVELS]; finest_scale finite and > 0.  num_rois == 0 is a no-op. */
 re_status_t fpn_level_map(const float *rois, int64_t num_rois, int32_t num_levels,
@@ -111,7 +111,8 @@ re_status_t fpn_level_map_ex(const float *rois, int64_t num_rois, int32_t num_le
                              float finest_scale, int32_t box_convention, int32_t *levels_out,
                              void *stream);
 
-/* Bytes of device workspace a plan for num_rois RoIs over the pyramid `levels` needs
+/* Workspace of the launch plan (a1 + a2, §3.1: the per-level extraction).
+ * Bytes of device workspace a plan for num_rois RoIs over the pyramid `levels` needs
  * (host array; only n, h and w are read).  It holds the launch permutation and the
  * tile->RoI lists of the gather backward (8 bytes per RoI, 12 per bin-tile, and 4 per
  * RoI times the largest number of bin-tiles of one image-level) and the plan's own
@@ -160,7 +161,9 @@ re_status_t roi_extract_plan_offsets(const void *workspace, size_t workspace_byt
 re_status_t roi_extract_plan_perm(const void *workspace, size_t workspace_bytes,
                                   int64_t num_rois, const int32_t **perm_out);
 
-/* a3-a5 -- RoIAlign forward.
+/* a3-a5 -- RoIAlign forward: the RoIExtractor's pooling of every RoI from its level
+ * (§3.1, RoIExtractor; RoIAlign is the Mask R-CNN operator of §2), computed as
+ * defined under Conventions above.
  *   levels/num_levels: host array of feature levels (same n, c, dtype);
  *   rois: device float[num_rois][5];
  *   roi_levels: device int32[num_rois] (e.g. from roi_extract_plan); may be NULL
@@ -200,7 +203,8 @@ re_status_t roi_align_fwd_noalloc(const re_level_t *levels, int32_t num_levels,
                                   int32_t sampling_ratio, int32_t aligned, void *out,
                                   int32_t out_dtype, void *stream);
 
-/* a6 -- clear the gradient pyramid (every element of every level set to +0.0).
+/* a6 -- clear the gradient pyramid (every element of every level set to +0.0), the
+ * start of the scatter backward (§3.2).
  * grad_levels: host array; every level RE_DTYPE_F32. */
 re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_levels,
                                   void *stream);
@@ -213,7 +217,8 @@ re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_lev
                                last or contiguous NCHW alike -- and out 7x7 or 14x14 with
                                sampling_ratio 2) */
 
-/* a6 + a7 -- RoIAlign backward: adds the transpose of the forward applied to
+/* a6 + a7 -- RoIAlign backward (§3.2: every training iteration runs the forward and
+ * the backward of the RoIExtractor): adds the transpose of the forward applied to
  * grad_out into the gradient pyramid (clears it first when zero_init != 0).
  *   grad_out: device [num_rois][c][out_h][out_w], dense, of grad_out_dtype;
  *   grad_levels: host array of num_levels descriptors, RE_DTYPE_F32, same n, c,
@@ -339,7 +344,7 @@ re_status_t deform_roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype,
                                 size_t plan_bytes, void *stream);
 
 /* f1 -- RoI max pooling, the RoIPool of Fast R-CNN (a two-stage method of §2),
- * the other RoIPooling-like operator a RoIExtractor uses (§3.1).  On level l (scale
+ * the other RoI pooling operator a RoIExtractor uses (§3.1).  On level l (scale
  * s, H x W map), every operation rounded to binary32 in this order:
  *   xs = roundf(x1*s), xe = roundf(x2*s)   (halves away from zero)
  *   len = max(xe - xs + 1, 1)              (both end pixels belong to the box)

@@ -10,7 +10,7 @@ forward and over channels for the backward).  This module compiles it with gcc
 and marshals numpy arrays through ctypes.  Everything it returns is float64.
 
 Paper anchors (MMDetection, arXiv 1906.07155): §3.1 RoIExtractor /
-SingleRoIExtractor (per-level RoI feature extraction with a RoIPooling-like
+SingleRoIExtractor (per-level RoI feature extraction with a RoI pooling
 operator), §2 (Mask R-CNN, whose RoIAlign that operator is), §3.2 (forward and
 backward every training iteration).
 """

@@ -8,15 +8,15 @@
  * never calls it, and it shares no source, header or helper with the HIP code.
  *
  * What it computes (MMDetection, arXiv 1906.07155):
- *   - §3.1 "Model Representation", RoIExtractor / SingleRoIExtractor: RoI-wise
- *     features are extracted from "the corresponding level" of the feature
- *     pyramid produced by the FPN neck, with a RoIPooling-like operator.
+ *   - §3.1 (model representation), RoIExtractor / SingleRoIExtractor: each RoI's
+ *     features are pooled from the level of the FPN pyramid that matches the
+ *     RoI's size, by a RoI pooling operator.
  *   - §2 (supported frameworks) cites Mask R-CNN for the RoIAlign operator used
- *     by the Faster/Mask R-CNN + FPN detectors; §1 ("High efficiency") states the
- *     bbox and mask operations run on GPUs; §3.2 (training pipeline) runs forward
- *     and backward every iteration, so the backward (the transpose) is needed too.
- *   - The same sections list RoIPool (Fast R-CNN's max pooling over quantized
- *     bins) among the RoIPooling-like extractors; oracle_roi_pool_fwd/bwd below
+ *     by the Faster/Mask R-CNN + FPN detectors; §1 says the bbox and mask
+ *     operations run on GPUs; §3.2 (training pipeline) runs forward and backward
+ *     every iteration, so the backward (the transpose) is needed too.
+ *   - The same sections name RoIPool (Fast R-CNN's max pooling over quantized
+ *     bins) as the other RoI pooling operator; oracle_roi_pool_fwd/bwd below
  *     follow its usual definition.
  *   - §2 also lists DCN (deformable RoI pooling) and DCNv2 (its modulated form):
  *     oracle_deform_roi_pool_fwd/bwd move every RoIAlign bin by a learned offset
@@ -67,7 +67,7 @@ int oracle_num_threads(void)
 }
 
 /* ------------------------------------------------------------------------- */
-/* Level assignment (§3.1: "the corresponding level of feature pyramids").    */
+/* Level assignment (§3.1: the pyramid level matched to the RoI's size).      */
 /* ------------------------------------------------------------------------- */
 
 /* Threshold form of the FPN rule: the level is the number of thresholds
@@ -375,8 +375,8 @@ void oracle_roi_align_bwd(const double *grad_out, double *const *grad_feats,
 }
 
 /* ------------------------------------------------------------------------- */
-/* RoI max pooling -- the RoIPool of Fast R-CNN, the other RoIPooling-like     */
-/* extractor besides RoIAlign that the detectors of §2 / §3.1 use.             */
+/* RoI max pooling -- the RoIPool of Fast R-CNN, the other RoI pooling        */
+/* operator besides RoIAlign that the detectors of §2 / §3.1 use.              */
 /*                                                                             */
 /* Geometry, binary32, one rounding per operation in this order:               */
 /*   start_x = roundf(x1 * scale), end_x = roundf(x2 * scale)  (halves away    */

@@ -1,8 +1,8 @@
 // plan.hip -- FPN level assignment and the RoI launch plan.
 //
-// Level assignment: §3.1 of MMDetection (SingleRoIExtractor reads each RoI from
-// "the corresponding level" of the FPN pyramid); the rule is the FPN rule in its
-// threshold form, see include/roi_extract.h.
+// Level assignment: §3.1 of MMDetection (SingleRoIExtractor pools each RoI from the
+// FPN level matched to its size); the rule is the FPN rule in its threshold form,
+// see include/roi_extract.h.
 //
 // The plan is a counting sort of the RoIs by (level, image, spatial cell of the box
 // centre): RoIs that read the same feature rows end up next to each other in launch

@@ -1,6 +1,6 @@
 // pool.hip -- RoI max pooling forward and backward.
 //
-// RoIPool is the other RoIPooling-like operator of the RoIExtractor (MMDetection
+// RoIPool is the other RoI pooling operator of the RoIExtractor (MMDetection
 // §3.1): Fast R-CNN (listed among the two-stage methods in §2) quantizes the box to
 // whole feature pixels, cuts it into out_h x out_w bins and keeps each bin's maximum.
 // Definition, tie rule and sentinels are stated in include/roi_extract.h.
