@@ -12,6 +12,32 @@
 #include "internal.hpp"
 #include "roi_extract.h"
 
+namespace rex {
+
+// Bands and difference grids of the one-launch plan (nbands = 0 when a level is wider
+// than one band's cursors).
+void plan_bands(PlanArgs &a) {
+    a.nbands = 0;
+    a.ndiff = 0;
+    int nb = 0, nd = 0;
+    for (int l = 0; l < kMaxLevels; ++l) {
+        a.band_base[l] = nb;
+        a.dbase[l] = nd;
+        a.band_rows[l] = 1;
+        if (l >= a.L || a.ntiles <= 0) continue;
+        if (a.ntx[l] > kBandTiles) return;
+        const int rows = std::min(a.nty[l], std::max(1, kBandTarget / a.ntx[l]));
+        a.band_rows[l] = rows;
+        nb += a.N * ((a.nty[l] + rows - 1) / rows);
+        nd += a.N * (a.nty[l] + 1) * (a.ntx[l] + 1);
+    }
+    a.band_base[kMaxLevels] = nb;
+    a.nbands = nb;
+    a.ndiff = nd;
+}
+
+}  // namespace rex
+
 using namespace rex;
 
 namespace {

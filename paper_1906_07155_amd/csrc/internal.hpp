@@ -7,6 +7,17 @@
 namespace rex {
 
 constexpr int kPlanThreads = 1024;
+// The one-launch plan's bands of tile rows (see plan.hip): at most kBandTiles tiles
+// (LDS cursors), about kBandTarget aimed at; kBandCand RoIs of a band kept in LDS.
+constexpr int kBandTiles = 2048;   // LDS cursors of one band
+#ifndef REX_BAND_CAND
+#define REX_BAND_CAND 2048
+#endif
+constexpr int kBandCand = REX_BAND_CAND;   // RoIs of one band kept in LDS (beyond: a second scan)
+#ifndef REX_BAND_TARGET
+#define REX_BAND_TARGET 64
+#endif
+constexpr int kBandTarget = REX_BAND_TARGET;   // tiles per band aimed at
 constexpr int kPlanMaxBins = 15360;   // LDS histogram + scan scratch of the plan kernel = 64 KiB
 
 struct PlanArgs {

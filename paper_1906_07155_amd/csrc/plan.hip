@@ -186,15 +186,7 @@ constexpr int kPlanLanes = 16;
 // bands keeps every role to a few instructions per RoI.
 // ---------------------------------------------------------------------------
 constexpr int kPlanOne = 8192;
-constexpr int kBandTiles = 2048;   // LDS cursors of one band
-#ifndef REX_BAND_CAND
-#define REX_BAND_CAND 2048
-#endif
-constexpr int kBandCand = REX_BAND_CAND;   // RoIs of one band kept in LDS (beyond: a second scan)
-#ifndef REX_BAND_TARGET
-#define REX_BAND_TARGET 64
-#endif
-constexpr int kBandTarget = REX_BAND_TARGET;   // tiles per band aimed at
+
 constexpr int kPlanWords = 24576;  // 96 KiB of LDS per workgroup
 
 // fn(k, roi) for every RoI, each thread's RoIs loaded kRoiBatch at a time.
@@ -603,28 +595,6 @@ hipError_t launch_plan(const PlanArgs &a, hipStream_t stream) {
     plan_fill_kernel<<<blocks, 256, 0, stream>>>(a);
     if (a.ntiles > 0) plan_order_kernel<<<1, kPlanThreads, 0, stream>>>(a);
     return hipGetLastError();
-}
-
-// Bands and difference grids of the one-launch plan (nbands = 0 when a level is wider
-// than one band's cursors).
-void plan_bands(PlanArgs &a) {
-    a.nbands = 0;
-    a.ndiff = 0;
-    int nb = 0, nd = 0;
-    for (int l = 0; l < kMaxLevels; ++l) {
-        a.band_base[l] = nb;
-        a.dbase[l] = nd;
-        a.band_rows[l] = 1;
-        if (l >= a.L || a.ntiles <= 0) continue;
-        if (a.ntx[l] > kBandTiles) return;
-        const int rows = std::min(a.nty[l], std::max(1, kBandTarget / a.ntx[l]));
-        a.band_rows[l] = rows;
-        nb += a.N * ((a.nty[l] + rows - 1) / rows);
-        nd += a.N * (a.nty[l] + 1) * (a.ntx[l] + 1);
-    }
-    a.band_base[kMaxLevels] = nb;
-    a.nbands = nb;
-    a.ndiff = nd;
 }
 
 }  // namespace rex
