@@ -116,7 +116,8 @@ re_status_t fpn_level_map_ex(const float *rois, int64_t num_rois, int32_t num_le
  * (host array; only n, h and w are read).  It holds the launch permutation and the
  * tile->RoI lists of the gather backward (8 bytes per RoI, 12 per bin-tile, and 4 per
  * RoI times the largest number of bin-tiles of one image-level) and the plan's own
- * counters (60 KiB).  Host-only; writes *bytes.  (A plan needs the level shapes, not
+ * counters (60 KiB).  Where that product exceeds 2^28 the plan keeps no tile lists
+ * (the gather backward is then not eligible).  Host-only; writes *bytes.  (A plan needs the level shapes, not
  * only the RoI and level counts, to size its tile lists, hence the level array.) */
 re_status_t roi_extract_workspace_size(const re_level_t *levels, int32_t num_levels,
                                        int64_t num_rois, size_t *bytes);
@@ -214,8 +215,8 @@ re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_lev
 #define RE_BWD_SCATTER 1    /* per-RoI scatter, fp32 atomics (a7) */
 #define RE_BWD_GATHER 2     /* per-tile gather, plain stores (needs a plan, gradient
                                levels whose images span less than 2^30 bytes -- channels-
-                               last or contiguous NCHW alike -- and out 7x7 or 14x14 with
-                               sampling_ratio 2) */
+                               last or contiguous NCHW alike -- out 7x7 or 14x14 with
+                               sampling_ratio 2, and a plan with tile lists) */
 
 /* a6 + a7 -- RoIAlign backward (§3.2: every training iteration runs the forward and
  * the backward of the RoIExtractor): adds the transpose of the forward applied to

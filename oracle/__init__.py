@@ -112,6 +112,9 @@ def load(path: str | None = None):
     with _lock:
         if path is not None:
             return _bind(ctypes.CDLL(path))
+        if _lib is None and os.environ.get("ORACLE_LIBRARY"):
+            # a prebuilt copy (the sanitizer build), loaded as it is
+            _lib = _bind(ctypes.CDLL(os.environ["ORACLE_LIBRARY"]))
         if _lib is None:
             if not os.path.exists(LIBRARY) or (
                     os.path.getmtime(LIBRARY) < os.path.getmtime(SOURCE)):

@@ -19,7 +19,9 @@ import threading
 from typing import List, Optional, Sequence, Tuple
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIBRARY = os.path.join(HERE, "libroi_extract.so")
+# REX_LIBRARY names another build of the same library (the host-code build that the
+# sanitizer tests load); unset, the in-tree library is loaded.
+LIBRARY = os.environ.get("REX_LIBRARY") or os.path.join(HERE, "libroi_extract.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "roi_extract.h")
 
 RE_OK, RE_ERR_INVALID_ARG, RE_ERR_UNSUPPORTED, RE_ERR_WORKSPACE, RE_ERR_DEVICE = range(5)
