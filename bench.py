@@ -92,8 +92,9 @@ def kernel_source_hash(kernel: str = None) -> str:
 
 
 def stored_traffic(kernel: str, workload: str):  # kernel: fwd | bwd_gather | bwd_scatter
-    """HBM bytes per launch from a committed rocprofv3 counter summary, if it was taken
-    on the current sources of that kernel (else None)."""
+    """Bytes per launch between the L2 and memory (rocprofv3 FETCH_SIZE + WRITE_SIZE,
+    scaled by a plain copy) from a committed counter summary, if it was taken on the
+    current sources of that kernel (else None)."""
     path = os.path.join(PROFILE_DIR, "traffic_%s_%s.txt" % (kernel, workload))
     if not os.path.exists(path):
         return None
@@ -106,7 +107,7 @@ def stored_traffic(kernel: str, workload: str):  # kernel: fwd | bwd_gather | bw
     if vals.get("kernel_source_hash") != kernel_source_hash(kernel):
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals["bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 

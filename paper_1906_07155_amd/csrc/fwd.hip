@@ -126,12 +126,14 @@ struct SampleTap {               // one sample row / column: taps and weights
 // follows from two ballots.  If the taps are not monotone (a degenerate RoI whose
 // rounded coordinates step backwards), every tap simply gets a slot of its own.
 // Writes the byte offset of each distinct position to off[] and, for each bin b,
-// the summed weight (times wscale) of each position to w[rank][b]; both arrays
-// must be pre-set to the out-of-range offset and to zero.  Returns the count.
-template <int S, int NW>
+// the summed weight (times wscale) of each position to w[rank * RS + b * BS]; both
+// arrays must be pre-set to the out-of-range offset and to zero.  With `touch`, also
+// sets bit b of touch[rank] for every bin b one of whose samples has the position as
+// a tap, whatever its weight (touch pre-set to zero).  Returns the count.
+template <int S, int RS, int BS>
 __device__ __forceinline__ int distinct_taps(const SampleTap *taps, int ns, int lane,
                                              uint32_t stride_b, float wscale, uint32_t *off,
-                                             float (*w)[NW]) {
+                                             float *w, uint32_t *touch) {
     SampleTap st, pv;
     st.lo = pv.lo = -1;
     st.hi = pv.hi = -1;
@@ -168,6 +170,10 @@ __device__ __forceinline__ int distinct_taps(const SampleTap *taps, int ns, int 
             off[r_lo] = static_cast<uint32_t>(st.lo) * stride_b;
             off[r_hi] = static_cast<uint32_t>(st.hi) * stride_b;
         }
+    }
+    if (touch && valid) {
+        atomicOr(&touch[r_lo], 1u << (lane / S));
+        if (r_hi != r_lo) atomicOr(&touch[r_hi], 1u << (lane / S));
     }
     // Per bin, its first lane sums the weights of the bin's samples in sample order
     // (lo before hi), so the result does not depend on scheduling.  The ranks one
@@ -206,7 +212,7 @@ __device__ __forceinline__ int distinct_taps(const SampleTap *taps, int ns, int 
             const int bin = lane / S;
 #pragma unroll
             for (int e = 0; e < 2 * S; ++e)
-                if (base + e < n) w[base + e][bin] = win[e];
+                if (base + e < n) w[(base + e) * RS + bin * BS] = win[e];
         }
     }
     return n;
@@ -266,12 +272,13 @@ struct FwdSmem {
     SampleTap srow[NR];
     SampleTap scol[NCOL];
     __align__(16) uint32_t s_xoff[MAXX];
-    __align__(16) float s_wx[MAXX][PWP];
+    __align__(16) float s_wx[PWP][MAXX];   // [bin column][distinct column]
     uint32_t s_yoff[4][MAXY];
     __align__(16) float s_wy[4][MAXY][RPWP];
     int32_t s_nx;
     int32_t s_ny[4];
-    uint64_t s_xhalf[2];   // bit x: column x weighs on bins [0, QH) / [QH, PW)
+    uint32_t s_xbins[MAXX];        // bit q: a sample of bin column q has this tap column
+    uint32_t s_cmask[MAXX / CX];   // the same, over each chunk of CX columns
     __align__(16) float stile[CHK * NB];
 };
 
@@ -289,15 +296,13 @@ __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, ui
     constexpr int MAXY = SM::MAXY;               // distinct tap rows per wave
     constexpr int MAXX = SM::MAXX;               // distinct tap columns, padded
     constexpr int PWP = SM::PWP;                 // padded for 16-byte LDS reads
-    constexpr int QH = (PW + 1) / 2;             // the bin columns' first half
-    constexpr bool kHalves = PW >= 12;           // skip the halves a column misses
     constexpr int SLICE = 64 * CPL;              // channels of one slice
     static_assert(NR + NCOL <= 256 && NCOL <= 64 && RPW * S <= 64 && MAXX <= 64, "geometry sizes");
     static_assert(SLICE % CHK == 0 && CHK % CPL == 0 && CX % 4 == 0, "tiling");
     SampleTap *const srow = sm.srow;
     SampleTap *const scol = sm.scol;
     uint32_t *const s_xoff = sm.s_xoff;
-    float (*const s_wx)[PWP] = sm.s_wx;
+    float (*const s_wx)[MAXX] = sm.s_wx;
     uint32_t (*const s_yoff)[MAXY] = sm.s_yoff;
     float (*const s_wy)[MAXY][RPWP] = sm.s_wy;
     float *const stile = sm.stile;
@@ -344,6 +349,7 @@ __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, ui
             else scol[u] = st;
         }
         for (int e = t; e < MAXX * PWP; e += 256) (&s_wx[0][0])[e] = 0.0f;
+        for (int e = t; e < MAXX; e += 256) sm.s_xbins[e] = 0u;
         for (int e = t; e < 4 * MAXY * RPWP; e += 256) (&s_wy[0][0][0])[e] = 0.0f;
         for (int e = t; e < MAXX; e += 256) s_xoff[e] = kBufOOB;
         for (int e = t; e < 4 * MAXY; e += 256) (&s_yoff[0][0])[e] = kBufOOB;
@@ -353,30 +359,22 @@ __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, ui
     // the RoI (wave 0); weights carry the 1/S of the sample average along their axis.
     constexpr float kInvS = 1.0f / static_cast<float>(S);
     {
-        const int ny = distinct_taps<S, RPWP>(srow + p0 * S, (p1 - p0) * S, lane, sh_b, kInvS,
-                                              s_yoff[wave], s_wy[wave]);
+        const int ny = distinct_taps<S, RPWP, 1>(srow + p0 * S, (p1 - p0) * S, lane, sh_b, kInvS,
+                                                 s_yoff[wave], &s_wy[wave][0][0], nullptr);
         if (lane == 0) sm.s_ny[wave] = ny;
         if (wave == 0) {
-            const int nx = distinct_taps<S, PWP>(scol, NCOL, lane, sw_b, kInvS, s_xoff, s_wx);
+            const int nx = distinct_taps<S, 1, MAXX>(scol, NCOL, lane, sw_b, kInvS, s_xoff,
+                                                     &s_wx[0][0], sm.s_xbins);
             if (lane == 0) sm.s_nx = nx;
-            // Which half of the bin columns each distinct column reaches (a column is
-            // reached by a run of at most a few adjacent bins, mostly inside one half);
-            // padding columns reach none.
+            // Which bin columns each chunk of CX distinct columns reaches (a column is a
+            // tap of a run of at most a few adjacent bins): the column reduction skips
+            // the others, whose products the definition never takes.
             wave_sync();
-            bool lo = false, hi = false;
-            if (lane < MAXX) {
+            if (lane < MAXX / CX) {
+                uint32_t m = 0;
 #pragma unroll
-                for (int q = 0; q < PW; ++q) {
-                    const bool nz = s_wx[lane][q] != 0.0f;
-                    if (q < QH) lo = lo || nz;
-                    else hi = hi || nz;
-                }
-            }
-            const uint64_t blo = __builtin_amdgcn_ballot_w64(lo);
-            const uint64_t bhi = __builtin_amdgcn_ballot_w64(hi);
-            if (lane == 0) {
-                sm.s_xhalf[0] = blo;
-                sm.s_xhalf[1] = bhi;
+                for (int x = 0; x < CX; ++x) m |= sm.s_xbins[lane * CX + x];
+                sm.s_cmask[lane] = m;
             }
         }
     }
@@ -385,10 +383,6 @@ __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, ui
     // wave-uniform counts in scalar registers: the pipeline below branches on them
     const int ny = uniform_i(sm.s_ny[wave]);
     const int nch = uniform_i((sm.s_nx + CX - 1) / CX);
-    const uint64_t xlo = (static_cast<uint64_t>(uniform_i(static_cast<int>(sm.s_xhalf[0] >> 32))) << 32) |
-                         static_cast<uint32_t>(uniform_i(static_cast<int>(sm.s_xhalf[0])));
-    const uint64_t xhi = (static_cast<uint64_t>(uniform_i(static_cast<int>(sm.s_xhalf[1] >> 32))) << 32) |
-                         static_cast<uint32_t>(uniform_i(static_cast<int>(sm.s_xhalf[1])));
     // The geometry above serves every slice of the workgroup.
     for (int slice = slice0; slice < slice1; ++slice) {
         if (slice > slice0) __syncthreads();   // the previous slice's output tile is stored
@@ -441,38 +435,38 @@ __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, ui
                 }
             }
             if (yi == ny - 1) {
+                // acc[p][q] += sum over the chunk's columns x of Wx[q][x] H[x][p], for the
+                // bin columns q the chunk reaches (uniform mask); the sum over x runs in
+                // column order, chunk after chunk, for every bin
+                const uint32_t m = static_cast<uint32_t>(uniform_i(static_cast<int>(sm.s_cmask[ch])));
 #pragma unroll
-                for (int x = 0; x < CX; ++x) {
-                    const int col = ch * CX + x;
-                    const float *wx = s_wx[col];
-                    // each half of the bins only where the column reaches it (the other
-                    // weights are zero); on the 7-wide grid the test costs more than the
-                    // few products it saves
-                    if (!kHalves || ((xlo >> col) & 1)) {
+                for (int q = 0; q < PW; ++q) {
+                    if (!((m >> q) & 1u)) continue;
+                    float wq[CX];
 #pragma unroll
-                        for (int q = 0; q < QH; ++q)
-#pragma unroll
-                            for (int j = 0; j < CPL; ++j)
-#pragma unroll
-                                for (int p = 0; p < RPW; ++p)
-                                    acc[j][p][q] = fmaf(wx[q], H[j][x][p], acc[j][p][q]);
+                    for (int x4 = 0; x4 < CX; x4 += 4) {
+                        const float4 w4 = *reinterpret_cast<const float4 *>(&s_wx[q][ch * CX + x4]);
+                        wq[x4] = w4.x;
+                        wq[x4 + 1] = w4.y;
+                        wq[x4 + 2] = w4.z;
+                        wq[x4 + 3] = w4.w;
                     }
-                    if (!kHalves || ((xhi >> col) & 1)) {
 #pragma unroll
-                        for (int q = QH; q < PW; ++q)
+                    for (int x = 0; x < CX; ++x)
 #pragma unroll
-                            for (int j = 0; j < CPL; ++j)
+                        for (int j = 0; j < CPL; ++j)
 #pragma unroll
-                                for (int p = 0; p < RPW; ++p)
-                                    acc[j][p][q] = fmaf(wx[q], H[j][x][p], acc[j][p][q]);
-                    }
+                            for (int p = 0; p < RPW; ++p)
+                                acc[j][p][q] = fmaf(wq[x], H[j][x][p], acc[j][p][q]);
+                    // one bin column's weights live at a time
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+#pragma unroll
+                for (int x = 0; x < CX; ++x)
 #pragma unroll
                     for (int j = 0; j < CPL; ++j)
 #pragma unroll
                         for (int p = 0; p < RPW; ++p) H[j][x][p] = 0.0f;
-                    // one column's weights live at a time
-                    __builtin_amdgcn_sched_barrier(0);
-                }
             }
         };
 
