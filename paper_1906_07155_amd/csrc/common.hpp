@@ -107,6 +107,7 @@ template <> __device__ __forceinline__ void store_f32<uint16_t>(gptr<uint16_t> p
     *p = f32_to_bf16(v);
 }
 
+
 // ---------------------------------------------------------------------------
 // Buffer-resource loads
 // ---------------------------------------------------------------------------
@@ -122,6 +123,33 @@ constexpr uint32_t kBufMaxBytes = 0x40000000u;
 constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, no swizzle (gfx9 family)
 constexpr int kStoreNT = 2;              // buffer store cache policy: non-temporal
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // a 16-byte buffer store
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// n contiguous values from src (16-byte aligned) to dst, 4 per store where dst is
+// aligned to 4 elements (one 16-byte or 8-byte store), the rest one at a time; every
+// thread i of `nt` takes groups i, i + nt, ...
+template <typename T>
+__device__ __forceinline__ void store_run_f32(gptr<T> dst, const float *src, int n, int i, int nt) {
+    int done = 0;
+    if ((reinterpret_cast<uintptr_t>(dst) & (4 * sizeof(T) - 1)) == 0) {
+        const int nv = n >> 2;
+        for (int v = i; v < nv; v += nt) {
+            const float4 f = *reinterpret_cast<const float4 *>(src + 4 * v);
+            if constexpr (sizeof(T) == 4) {
+                const u32x4 w = {__float_as_uint(f.x), __float_as_uint(f.y), __float_as_uint(f.z),
+                                 __float_as_uint(f.w)};
+                *reinterpret_cast<REX_GLOBAL u32x4 *>(dst + 4 * v) = w;
+            } else {
+                const u32x2 w = {
+                    static_cast<uint32_t>(f32_to_bf16(f.x)) | (static_cast<uint32_t>(f32_to_bf16(f.y)) << 16),
+                    static_cast<uint32_t>(f32_to_bf16(f.z)) | (static_cast<uint32_t>(f32_to_bf16(f.w)) << 16)};
+                *reinterpret_cast<REX_GLOBAL u32x2 *>(dst + 4 * v) = w;
+            }
+        }
+        done = nv << 2;
+    }
+    for (int e = done + i; e < n; e += nt) store_f32<T>(dst + e, src[e]);
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0,

@@ -579,7 +579,7 @@ __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, ui
             __syncthreads();
             const int ne = max(0, min(CHK, nchan - c0)) * NB;
             if (kvalid)
-                for (int e = t; e < ne; e += 256) store_f32(out_blk + c0 * NB + e, stile[e]);
+                store_run_f32<TO>(out_blk + c0 * NB, stile, ne, t, 256);
             if (c0 + CHK < SLICE) __syncthreads();
         }
     }   // slices
