@@ -42,9 +42,12 @@ namespace rex {
 #ifndef REX_NCHW_CC14
 #define REX_NCHW_CC14 1
 #endif
-// columns per load unit with two bf16 channels per lane (7x7 grid)
+// columns per load unit and units in flight with two bf16 channels per lane (7x7 grid)
 #ifndef REX_FWD_CX2_BF16
-#define REX_FWD_CX2_BF16 8
+#define REX_FWD_CX2_BF16 4
+#endif
+#ifndef REX_FWD_DEPTH2_BF16
+#define REX_FWD_DEPTH2_BF16 4
 #endif
 
 constexpr int kFwdDepth = REX_FWD_DEPTH;
@@ -284,7 +287,8 @@ struct FwdSmem {
 
 // The forward of workgroup `lid` (in logical order) of a launch over the RoIs of `a`
 // (FwdArgs or FwdHeadArgs: RoIs, levels, plan order, output and slicing) on pyramid lv.
-template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK, int CPL, typename A>
+template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK, int CPL, typename A,
+          int D = kFwdDepth>
 __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, uint32_t lid,
                                             FwdSmem<PH, PW, S, CX, CHK> &sm) {
     using SM = FwdSmem<PH, PW, S, CX, CHK>;
@@ -471,9 +475,8 @@ __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, ui
         };
 
         // Pipeline over the units in (chunk, row) order: the loads of units u+1 ..
-        // u+kFwdDepth are in flight while unit u is reduced.  The loop is unrolled by
+        // u+D are in flight while unit u is reduced.  The loop is unrolled by
         // the ring size so every buffer index is a constant.
-        constexpr int D = kFwdDepth;
         constexpr int NBUF = D + 1;
         RawPix<T, CPL> v[NBUF][CX];
         const int units = ny * nch;
@@ -585,7 +588,7 @@ __device__ __forceinline__ void fwd_cl_body(const A &a, const LevelTable &lv, ui
     }   // slices
 }
 
-template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK, int CPL>
+template <typename T, typename TO, int PH, int PW, int S, int CX, int CHK, int CPL, int D>
 __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     __shared__ FwdSmem<PH, PW, S, CX, CHK> sm;
     // The arguments are read in place from the kernel-argument segment (a reference to
@@ -594,7 +597,8 @@ __global__ __launch_bounds__(256) void fwd_cl_kernel(FwdArgs a) {
     const FwdArgs &ka = *(const FwdArgs *)__builtin_amdgcn_kernarg_segment_ptr();
     // XCD-aware block order: consecutive logical ids (neighbouring RoIs of the plan
     // order) land on one XCD
-    fwd_cl_body<T, TO, PH, PW, S, CX, CHK, CPL>(ka, ka.lv, xcd_remap(blockIdx.x, gridDim.x), sm);
+    fwd_cl_body<T, TO, PH, PW, S, CX, CHK, CPL, FwdArgs, D>(ka, ka.lv, xcd_remap(blockIdx.x, gridDim.x),
+                                                          sm);
 }
 
 // ---------------------------------------------------------------------------
@@ -605,7 +609,7 @@ bool fwd_fast_available(int PH, int PW, int S) {
     return S == 2 && ((PH == 7 && PW == 7) || (PH == 14 && PW == 14));
 }
 
-template <typename T, typename TO, int PH, int PW, int CX, int CHK, int CPL>
+template <typename T, typename TO, int PH, int PW, int CX, int CHK, int CPL, int D = kFwdDepth>
 static hipError_t launch_fwd_cl(FwdArgs a, hipStream_t stream) {
     a.nslices = (a.lv.C + 64 * CPL - 1) / (64 * CPL);
     // Slices per workgroup: the RoI's geometry (two IEEE divisions, the distinct-tap
@@ -622,7 +626,7 @@ static hipError_t launch_fwd_cl(FwdArgs a, hipStream_t stream) {
     a.wg_per_roi = (a.nslices + a.spw - 1) / a.spw;
     const int64_t grid = static_cast<int64_t>(a.K) * a.wg_per_roi;
     if (grid >= (int64_t(1) << 24)) return hipErrorInvalidConfiguration;
-    fwd_cl_kernel<T, TO, PH, PW, 2, CX, CHK, CPL><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
+    fwd_cl_kernel<T, TO, PH, PW, 2, CX, CHK, CPL, D><<<static_cast<uint32_t>(grid), 256, 0, stream>>>(a);
     return hipGetLastError();
 }
 
@@ -640,9 +644,13 @@ static hipError_t launch_fwd_typed(FwdArgs a, bool fast, hipStream_t stream) {
             // us): the grid halves and occupancy drops from six to four waves, so fewer
             // bytes are in flight per SIMD; so is sharing one geometry between two slices
             // taken at once by an 8-wave workgroup (53.5 -> 59.8 us).
+            // With two channels per lane, units of 4 columns and 4 units in flight (batch
+            // 16, 8192 RoIs: 241 -> 227 us; batch 1, 1000 RoIs: 38.2 -> 38.0 us); one
+            // channel per lane keeps 8 columns and 2 units (1024 RoIs: 47.2 vs 49.0 us).
             if constexpr (sizeof(T) == 2)
                 if (a.lv.C % 2 == 0)
-                    return launch_fwd_cl<T, TO, 7, 7, REX_FWD_CX2_BF16, 64, 2>(a, stream);
+                    return launch_fwd_cl<T, TO, 7, 7, REX_FWD_CX2_BF16, 64, 2, REX_FWD_DEPTH2_BF16>(
+                        a, stream);
             return launch_fwd_cl<T, TO, 7, 7, kFwdCX, 64, 1>(a, stream);
         }
         // 4 columns per unit keep the 14x14 kernel at 124 registers, four workgroups
