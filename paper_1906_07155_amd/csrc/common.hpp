@@ -127,7 +127,9 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // n contiguous values from src (16-byte aligned) to dst, 4 per store where dst is
 // aligned to 4 elements (one 16-byte or 8-byte store), the rest one at a time; every
-// thread i of `nt` takes groups i, i + nt, ...
+// thread i of `nt` takes groups i, i + nt, ...  The vector stores are non-temporal: the
+// kernel never reads what it writes here, so it streams past the caches and leaves
+// them to the data that is read (batch-2 box head forward: 46.8 -> 45.5 us).
 template <typename T>
 __device__ __forceinline__ void store_run_f32(gptr<T> dst, const float *src, int n, int i, int nt) {
     int done = 0;
@@ -138,12 +140,12 @@ __device__ __forceinline__ void store_run_f32(gptr<T> dst, const float *src, int
             if constexpr (sizeof(T) == 4) {
                 const u32x4 w = {__float_as_uint(f.x), __float_as_uint(f.y), __float_as_uint(f.z),
                                  __float_as_uint(f.w)};
-                *reinterpret_cast<REX_GLOBAL u32x4 *>(dst + 4 * v) = w;
+                __builtin_nontemporal_store(w, reinterpret_cast<REX_GLOBAL u32x4 *>(dst + 4 * v));
             } else {
                 const u32x2 w = {
                     static_cast<uint32_t>(f32_to_bf16(f.x)) | (static_cast<uint32_t>(f32_to_bf16(f.y)) << 16),
                     static_cast<uint32_t>(f32_to_bf16(f.z)) | (static_cast<uint32_t>(f32_to_bf16(f.w)) << 16)};
-                *reinterpret_cast<REX_GLOBAL u32x2 *>(dst + 4 * v) = w;
+                __builtin_nontemporal_store(w, reinterpret_cast<REX_GLOBAL u32x2 *>(dst + 4 * v));
             }
         }
         done = nv << 2;

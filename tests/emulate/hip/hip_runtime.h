@@ -59,3 +59,5 @@ struct uint2 { unsigned x, y; };
 struct uint4 { unsigned x, y, z, w; };
 inline float4 make_float4(float a, float b, float c, float d) { return {a, b, c, d}; }
 using std::isfinite;
+// clang builtin of the device code: a plain store here
+template <typename V, typename P> inline void __builtin_nontemporal_store(V v, P p) { *p = v; }

@@ -61,3 +61,5 @@ inline int __builtin_amdgcn_update_dpp(int o, int, int, int, int, bool) { return
 #define __builtin_amdgcn_mbcnt_lo(a, b) 0u
 #define __builtin_amdgcn_mbcnt_hi(a, b) 0u
 #define __builtin_amdgcn_kernarg_segment_ptr() nullptr
+// clang builtin of the device code: a plain store here
+template <typename V, typename P> inline void __builtin_nontemporal_store(V v, P p) { *p = v; }
