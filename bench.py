@@ -356,7 +356,7 @@ def main():
         alg.update({"zero": by.zero, "bwd": gather_bytes if algo == "gather" else by.e_bwd})
     gbs = {n: alg[n] / (per_kernel[n] * 1e-3) / 1e9 for n in names}
     dominant = max(["fwd", "bwd"] if backward else ["fwd"], key=lambda n: per_kernel[n])
-    wname = wl.tag
+    wname = wl.tag + ("_nchw" if args.layout == "nchw" else "")
     kname = {"fwd": "fwd", "bwd": "bwd_" + algo}[dominant]
     traffic = stored_traffic(kname, wname)
     roofline = {"bound": "hbm", "achieved": round(gbs[dominant], 1), "peak": HBM_PEAK_GBS,
