@@ -160,6 +160,19 @@ def test_dtypes(fdt, odt, gdt):
         fdt=fdt, odt=odt, gdt=gdt)
 
 
+@pytest.mark.parametrize("layout", ["nchw", "nchw_view"])
+@pytest.mark.parametrize("fdt,odt,gdt", [("bf16", "bf16", "bf16"), ("f32", "bf16", "f32")])
+def test_layouts_dtypes(layout, fdt, odt, gdt):
+    """Levels in separate channel planes with bf16 features, outputs or upstream
+    gradients, on both specialised grids; 70 channels leave a partial last channel
+    group."""
+    rng = np.random.default_rng(35)
+    rois = W.draw_rois(rng, 2, 19, (96, 160), (4.0, 200.0))
+    for out_hw in ((7, 7), (14, 14)):
+        run("layout %s dtypes %s/%s/%s %s" % (layout, fdt, odt, gdt, out_hw), _pyr(70), SC,
+            rois, out_hw=out_hw, fdt=fdt, odt=odt, gdt=gdt, layout=layout)
+
+
 def test_other_output_sizes():
     rng = np.random.default_rng(40)
     rois = _rois(rng, 17, 2, 160, 96)
