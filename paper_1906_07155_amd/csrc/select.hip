@@ -43,11 +43,32 @@ __device__ __forceinline__ int nmsb_category(const NmsBatchArgs &a, int32_t i) {
     return (c >= 0 && c < a.C && a.scores[i] >= a.score_threshold) ? c : -1;
 }
 
-__global__ __launch_bounds__(256) void nmsb_count_kernel(NmsBatchArgs a) {
-    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.N; i += gridDim.x * blockDim.x) {
+// Candidate counting and placement work on contiguous ranges of kPlaceRange boxes per
+// workgroup: the workgroup counts its boxes per category in LDS and touches each
+// category's device counter once.  Device-scope atomics to one address are serialised
+// beyond the per-XCD L2 (about 0.2 us each), so one per box and category -- thousands
+// on each of a few counters -- would dominate the selection.
+constexpr int kPlaceThreads = 256;
+constexpr int kPlaceRange = 4096;
+
+__device__ __forceinline__ void nmsb_range(const NmsBatchArgs &a, int32_t &i0, int32_t &i1) {
+    i0 = static_cast<int32_t>(blockIdx.x) * kPlaceRange;
+    i1 = min(a.N, i0 + kPlaceRange);
+}
+
+__global__ __launch_bounds__(kPlaceThreads) void nmsb_count_kernel(NmsBatchArgs a) {
+    extern __shared__ int32_t hist[];   // [C]
+    for (int c = threadIdx.x; c < a.C; c += kPlaceThreads) hist[c] = 0;
+    __syncthreads();
+    int32_t i0, i1;
+    nmsb_range(a, i0, i1);
+    for (int32_t i = i0 + threadIdx.x; i < i1; i += kPlaceThreads) {
         const int c = nmsb_category(a, i);
-        if (c >= 0) atomicAdd(&a.count[c], 1);
+        if (c >= 0) atomicAdd(&hist[c], 1);
     }
+    __syncthreads();
+    for (int c = threadIdx.x; c < a.C; c += kPlaceThreads)
+        if (hist[c] > 0) atomicAdd(&a.count[c], hist[c]);
 }
 
 __global__ __launch_bounds__(kSelThreads) void nmsb_scan_kernel(NmsBatchArgs a) {
@@ -64,10 +85,28 @@ __global__ __launch_bounds__(kSelThreads) void nmsb_scan_kernel(NmsBatchArgs a) 
     if (threadIdx.x == 0) a.start[a.C] = total;
 }
 
-__global__ __launch_bounds__(256) void nmsb_place_kernel(NmsBatchArgs a) {
-    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.N; i += gridDim.x * blockDim.x) {
+// Every candidate of the workgroup's range to a slot of its category: the range's count
+// per category reserves a run of slots with one device atomic, then LDS cursors deal the
+// run out.  The order inside a category is free (the selection sorts it).
+__global__ __launch_bounds__(kPlaceThreads) void nmsb_place_kernel(NmsBatchArgs a) {
+    extern __shared__ int32_t cur[];   // [C]: counts, then cursors
+    for (int c = threadIdx.x; c < a.C; c += kPlaceThreads) cur[c] = 0;
+    __syncthreads();
+    int32_t i0, i1;
+    nmsb_range(a, i0, i1);
+    for (int32_t i = i0 + threadIdx.x; i < i1; i += kPlaceThreads) {
         const int c = nmsb_category(a, i);
-        if (c >= 0) a.sidx[atomicAdd(&a.count[c], 1)] = i;
+        if (c >= 0) atomicAdd(&cur[c], 1);
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < a.C; c += kPlaceThreads)
+        if (cur[c] > 0) cur[c] = atomicAdd(&a.count[c], cur[c]);
+    __syncthreads();
+    for (int32_t i = i0 + threadIdx.x; i < i1; i += kPlaceThreads) {
+        const int c = nmsb_category(a, i);
+        if (c < 0) continue;
+        const int slot = atomicAdd(&cur[c], 1);
+        if (slot >= 0 && slot < a.N) a.sidx[slot] = i;
     }
 }
 
@@ -358,16 +397,18 @@ hipError_t launch_nms_batched(const NmsBatchArgs &a, hipStream_t stream) {
                                                                                          a.C);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int blocks = std::max(1, std::min((a.N + 255) / 256, 4096));
+    // contiguous ranges of kPlaceRange boxes, one workgroup each (N <= 2^24: at most 4096)
+    const int blocks = static_cast<int>((static_cast<int64_t>(a.N) + kPlaceRange - 1) / kPlaceRange);
+    const size_t hist_bytes = static_cast<size_t>(a.C) * sizeof(int32_t);
     if (a.N > 0) {
-        nmsb_count_kernel<<<blocks, 256, 0, stream>>>(a);
+        nmsb_count_kernel<<<blocks, kPlaceThreads, hist_bytes, stream>>>(a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     const size_t shmem = static_cast<size_t>(a.C + kSelThreads) * sizeof(int32_t);
     nmsb_scan_kernel<<<1, kSelThreads, shmem, stream>>>(a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.N > 0) {
-        nmsb_place_kernel<<<blocks, 256, 0, stream>>>(a);
+        nmsb_place_kernel<<<blocks, kPlaceThreads, hist_bytes, stream>>>(a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     nmsb_select_kernel<<<std::min(a.C, 4096), kSelThreads, 0, stream>>>(a);
