@@ -253,8 +253,8 @@ def test_dense_rois_on_one_tile():
 
 
 def test_many_long_tile_lists():
-    """40 hot spots of 40 RoIs each: more long tile lists than the plan has partial slots
-    for, so only the longest are cut into parts and the rest run whole."""
+    """40 hot spots of 40 RoIs each on one image: many long tile lists, whose workgroups
+    run first (longest-first tile order)."""
     rng = np.random.default_rng(87)
     shapes = [(1, 64, 128, 128), (1, 64, 64, 64), (1, 64, 32, 32), (1, 64, 16, 16)]
     centres = rng.uniform(40, 472, (40, 2))
@@ -271,6 +271,16 @@ def test_many_long_tile_lists():
     run("40 hot spots", shapes, SC, rois)
     run("40 hot spots accumulate", shapes, SC, rois, zero_init=False)
     run("40 hot spots mask bf16 grad", shapes, SC, rois, out_hw=(14, 14), gdt="bf16")
+
+
+def test_plan_five_kernel_path():
+    """More RoIs than the one-launch plan takes (8192): the plan runs as five kernels
+    (device-wide counting, scan, fill, tile order), and the forward and the gather
+    backward use its order and tile lists."""
+    rng = np.random.default_rng(89)
+    rois = W.draw_rois(rng, 2, 4700, (96, 160), (4.0, 200.0))
+    run("9400 RoIs (five-kernel plan)", _pyr(16), SC, rois)
+    run("9400 RoIs (five-kernel plan) mask", _pyr(16), SC, rois, out_hw=(14, 14))
 
 
 def test_forward_many_rois_ragged_slices():
