@@ -703,7 +703,7 @@ __device__ __forceinline__ int gather_tile(const GatherArgs &a, const int32_t *o
 // gradient pyramid is far larger than the L2 and read only by a later pass, so the
 // stores are non-temporal: they stream to memory instead of evicting cached data.
 __device__ __forceinline__ void gather_store(const GatherTile &x, int zero_init,
-                                             const float (&acc)[8][8]) {
+                                             const float (&acc)[8][8], float *scratch) {
     if (!x.wave_on) return;
     const int lane = threadIdx.x & 63;
     const int c = x.cg * 64 + lane;
@@ -731,6 +731,32 @@ __device__ __forceinline__ void gather_store(const GatherTile &x, int zero_init,
                               __float_as_uint(acc[rr][6]), __float_as_uint(acc[rr][7])};
             __builtin_amdgcn_raw_buffer_store_b128(lo, dst, vo, o, 0);
             __builtin_amdgcn_raw_buffer_store_b128(hi, dst, vo, o + 16u, 0);
+        }
+        return;
+    }
+    if (L.sc == 1 && zero_init && x.nch == 64 && x.R0 + 8 <= L.H && x.Q0 + 8 <= L.W) {
+        // Channels-last, a whole quadrant inside the map and a full channel group: each
+        // row of 8 pixels is turned around in this wave's 2 KiB of LDS so a lane holds 4
+        // adjacent channels of one pixel, and leaves as two 16-byte stores per lane (1
+        // KiB per instruction instead of 256 bytes: 16 store instructions per wave
+        // instead of 64).
+        const int lq = lane >> 4;           // pixel of a group of 4
+        const int lc = (lane & 15) * 4;     // its first channel in the group
+        const uint32_t cvo = static_cast<uint32_t>(x.cg * 64 + lc) * 4u;
+#pragma unroll
+        for (int rr = 0; rr < 8; ++rr) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) scratch[q * 64 + lane] = acc[rr][q];
+            wave_sync();
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const float4 v = *reinterpret_cast<const float4 *>(scratch + (h * 4 + lq) * 64 + lc);
+                const u32x4 w = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                                 __float_as_uint(v.w)};
+                const uint32_t vo4 = static_cast<uint32_t>(h * 4 + lq) * sw4 + cvo;
+                __builtin_amdgcn_raw_buffer_store_b128(w, dst, vo4, base + rr * sh4, kStoreNT);
+            }
+            wave_sync();   // the row's values are read before the next row overwrites them
         }
         return;
     }
@@ -792,7 +818,10 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(GatherArgs a) {
         for (int q = 0; q < 8; ++q) acc[r][q] = 0.0f;
     gather_phase<TG, PH, PW, S>(a.head[0], a.lv, t, x, acc, sm, blk0.g,
                                 two ? blk1.g : nullptr);
-    gather_store(x, a.zero_init, acc);
+    static_assert(GatherSmem<TG, PH, PW, S>::GBP >= 4 * 512, "store scratch in the first slot");
+    __syncthreads();   // the staging slots are free: every wave has consumed its last RoI
+    gather_store(x, a.zero_init, acc,
+                 reinterpret_cast<float *>(blk0.g) + (threadIdx.x >> 6) * 512);
 }
 
 // Two heads on one pyramid (e.g. the 7x7 box head and the 14x14 mask head of a Mask
@@ -823,7 +852,10 @@ __global__ __launch_bounds__(256) void bwd_gather2_kernel(GatherArgs a) {
     __syncthreads();   // head 0's LDS is no longer read
     gather_phase<TG, PH1, PW1, 2>(a.head[1], a.lv, t, x, acc, sm.h1, stage,
                                   SM1::NBUF == 2 ? stage + SM1::GBP : nullptr);
-    gather_store(x, a.zero_init, acc);
+    static_assert(kStage0 >= 4 * 512 && kStage1 >= 4 * 512, "store scratch in the ring");
+    __syncthreads();   // the staging ring is free
+    gather_store(x, a.zero_init, acc,
+                 reinterpret_cast<float *>(stage) + (threadIdx.x >> 6) * 512);
 }
 
 bool gather_available(int PH, int PW, int S) {
