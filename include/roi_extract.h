@@ -127,7 +127,7 @@ re_status_t roi_extract_workspace_size(const re_level_t *levels, int32_t num_lev
  * spatial cell of the box centre) plus per-level offsets, stored in `workspace`; the
  * plan also lists, for every bin-tile (16 pixels or more a side) of every
  * (level, image), the RoIs whose footprint can reach it, and orders the tiles by
- * decreasing list length (used by the gather backward).  Up to 2048 RoIs (and bucket
+ * decreasing list length (used by the gather backward).  Up to 8192 RoIs (and bucket
  * and tile tables that fit one workgroup's LDS) this is one kernel launch, otherwise
  * five (all on `stream`, nothing allocated).  The forward and backward walk the RoIs in plan order,
  * so neighbouring work shares cache; any valid permutation gives the same

@@ -66,13 +66,13 @@ def test_two_calls_second_smaller():
 
 
 def test_large_plan_then_small():
-    """Above 2048 RoIs the plan takes its four-kernel form (counters cleared by a
+    """Above 8192 RoIs the plan takes its five-kernel form (bucket counters cleared by a
     kernel in the array); a small call after it reuses the dirty array."""
     hw = [(50, 84), (25, 42), (13, 21), (7, 11)]
-    f1, s1, r1 = _case(3, 4, 64, hw, 4000, "f32")
-    _run(f1, s1, r1, (7, 7), "f32", "4000 RoIs")
+    f1, s1, r1 = _case(3, 4, 64, hw, 9000, "f32")
+    _run(f1, s1, r1, (7, 7), "f32", "9000 RoIs")
     f2, s2, r2 = _case(4, 2, 64, hw, 40, "f32")
-    _run(f2, s2, r2, (7, 7), "f32", "40 RoIs after 4000")
+    _run(f2, s2, r2, (7, 7), "f32", "40 RoIs after 9000")
 
 
 def test_limit_is_refused():
