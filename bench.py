@@ -466,7 +466,9 @@ def main():
 
 def main_pool(args):
     """RoI max pooling on a workload's pyramid and RoIs: one step is roi_extract_plan,
-    roi_pool_fwd and roi_pool_bwd (clearing included; fp32 atomics)."""
+    roi_pool_fwd and roi_pool_bwd (with the plan's tile lists the backward is the tile
+    gather, which writes every gradient element once; otherwise clearing and fp32
+    atomics)."""
     import torch
 
     import oracle
@@ -524,7 +526,11 @@ def main_pool(args):
     by = accounting.count_pool(rois_np, lv_np, wl.level_hw, wl.scales, wl.n_images, C, wl.out_hw,
                                2 if bf16 else 4, 2 if wl.out_dtype == "bf16" else 4,
                                2 if wl.grad_dtype == "bf16" else 4)
-    alg = {"plan": 24 * K + 12 * K, "fwd": by.e_fwd, "bwd": by.e_bwd + by.zero}
+    # the library takes the tile gather for 7x7 bins when the plan holds tile lists (it
+    # does here); other grids take the clearing and the atomics
+    bwd_alg = "gather" if tuple(wl.out_hw) == (7, 7) else "scatter"
+    alg = {"plan": 24 * K + 12 * K, "fwd": by.e_fwd,
+           "bwd": by.g_bwd if bwd_alg == "gather" else by.e_bwd + by.zero}
     gbs = {n: alg[n] / (per[n] * 1e-3) / 1e9 for n in names}
     dominant = max(["fwd", "bwd"], key=lambda n: per[n])
     roofline = {"bound": "hbm", "achieved": round(gbs[dominant], 1), "peak": HBM_PEAK_GBS,
@@ -561,8 +567,9 @@ def main_pool(args):
         "extra": {"kernel_ms": {n: round(v, 5) for n, v in per.items()},
                   "ms_per_step_with_kernel_events": round(ms_with_events, 5),
                   "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
-                  "bytes": {"E_fwd": by.e_fwd, "E_bwd": by.e_bwd, "zero_fill": by.zero,
-                            "box_px": by.box_px},
+                  "bytes": {"E_fwd": by.e_fwd, "E_bwd": by.e_bwd, "G_bwd": by.g_bwd,
+                            "zero_fill": by.zero, "box_px": by.box_px},
+                  "bwd_algorithm": bwd_alg,
                   "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(result), flush=True)

@@ -370,8 +370,17 @@ re_status_t roi_pool_fwd(const re_level_t *levels, int32_t num_levels, const flo
 
 /* f1 -- RoI max pooling backward: grad_F_l[b, c, argmax / W, argmax % W] +=
  * grad_out[k, c, ph, pw] for every element whose argmax is in [0, H*W) (no gradient
- * for -1), summed with fp32 atomics (the order, hence the last bits, may vary).  The
- * gradient pyramid is cleared first when zero_init != 0.
+ * for -1).  The summation order, hence the last bits, may vary between runs.  Two
+ * forms:
+ *   - with a plan that holds tile lists (see roi_extract_workspace_size), a 7 x 7 grid
+ *     and gradient levels whose images span less than 2^30 bytes: per tile and 64
+ *     channels, the RoIs binned to the tile are added in LDS and every gradient element
+ *     is written once (zero_init != 0: no separate clearing).  The plan's levels must
+ *     be roi_levels (RoIs of another level are not found in the tile lists), and only
+ *     an argmax inside the RoI's bins, as roi_pool_fwd writes it, is certain to be
+ *     added;
+ *   - otherwise the gradient pyramid is cleared first when zero_init != 0 and every
+ *     element is added with an fp32 atomic.
  *   grad_out: device [num_rois][c][out_h][out_w] of grad_out_dtype;
  *   argmax: device int32, as written by roi_pool_fwd for the same RoIs and levels;
  *   grad_levels: binary32 levels with the forward's n, c, h, w;

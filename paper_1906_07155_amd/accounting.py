@@ -146,6 +146,7 @@ class PoolBytes:
     e_fwd: int               # box pixels x C read, values and argmax written
     e_bwd: int               # gradient and argmax read, one fp32 read-modify-write each
     zero: int
+    g_bwd: int               # tile-gather form: gradient and argmax read, every element written once
 
 
 def count_pool(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[int, int]],
@@ -157,6 +158,11 @@ def count_pool(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[in
 
       E_fwd = sum_r box_r*C*s_feat + K*C*PH*PW*(s_out + 4) + 24*K
       E_bwd = K*C*PH*PW*(s_gout + 4) + K*C*PH*PW*8 + 24*K     (+ clearing, reported apart)
+
+    The tile-gather backward reads the upstream gradient and the argmax once and writes
+    every element of the binary32 gradient pyramid once (no clearing, no atomics):
+
+      G_bwd = K*C*PH*PW*(s_gout + 4) + 24*K + N*C*sum_l H_l*W_l*4
     """
     K = rois.shape[0]
     PH, PW = out_hw
@@ -181,7 +187,8 @@ def count_pool(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[in
     elems = K * C * PH * PW
     zero = sum(n_images * C * H * W * 4 for (H, W) in level_hw)
     return PoolBytes(K=K, box_px=box, e_fwd=box * C * s_feat + elems * (s_out + 4) + 24 * K,
-                     e_bwd=elems * (s_gout + 4) + elems * 8 + 24 * K, zero=zero)
+                     e_bwd=elems * (s_gout + 4) + elems * 8 + 24 * K, zero=zero,
+                     g_bwd=elems * (s_gout + 4) + 24 * K + zero)
 
 
 def deform_footprint(rois: np.ndarray, levels: np.ndarray, level_hw: Sequence[Tuple[int, int]],

@@ -861,6 +861,25 @@ re_status_t roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype, const int
     if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
+    // With a plan that holds tile lists: the tile gather, which writes every gradient
+    // element once (clearing included)
+    const TileLayout tl = tile_layout(t, num_rois);
+    if (plan && num_rois > 0 && tl.ntiles > 0 && levels_buffered(t) &&
+        pool_gather_available(out_h, out_w)) {
+        BwdHead h{};
+        h.gout = grad_out;
+        h.gdt = grad_out_dtype;
+        h.rois = rois;
+        h.K = num_rois;
+        h.roi_levels = roi_levels;
+        h.out_h = out_h;
+        h.out_w = out_w;
+        h.plan = plan;
+        h.plan_bytes = plan_bytes;
+        GatherArgs g = gather_args(t, h, tl, zero_init);
+        g.head[0].argmax = argmax;
+        return from_hip(launch_pool_gather(g, grad_out_dtype, s));
+    }
     if (zero_init) {
         if ((st = from_hip(launch_zero(t, numel, dense, s))) != RE_OK) return st;
     }

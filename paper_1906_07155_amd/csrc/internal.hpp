@@ -72,6 +72,7 @@ struct TileLayout {
 // One head's RoIs for the gather backward (its upstream gradient and its plan).
 struct GatherHead {
     const void *gout;            // [K][C][PH][PW]
+    const int32_t *argmax;       // RoI max pooling: [K][C][PH][PW] pixel indices
     const float *rois;
     const int32_t *roi_levels;
     const int32_t *tile_start;   // the head's plan: tile -> RoI lists
@@ -131,6 +132,8 @@ struct GatherArgs {
     int32_t img_sh[kMaxLevels];
     uint32_t row_m[kMaxLevels];  // by the tiles of one row of a level
     int32_t row_sh[kMaxLevels];
+    uint32_t wid_m[kMaxLevels];  // by the width of a level (pixel index -> row)
+    int32_t wid_sh[kMaxLevels];
 };
 
 struct FwdArgs {
@@ -210,6 +213,9 @@ bool pool_fwd_fast_available(int PH, int PW);
 hipError_t launch_pool_fwd(PoolArgs a, int feat_dtype, int out_dtype, bool fast,
                            hipStream_t stream);
 hipError_t launch_pool_bwd(PoolArgs a, int gout_dtype, bool fast, hipStream_t stream);
+// The tile-gather backward of RoI max pooling (head 0 of `a`, with its argmax).
+bool pool_gather_available(int PH, int PW);
+hipError_t launch_pool_gather(GatherArgs a, int gout_dtype, hipStream_t stream);
 
 // Deformable (modulated) RoI pooling, forward and backward.
 struct DeformArgs {

@@ -19,10 +19,15 @@
 //                          its channel's gradients to the argmax pixels with no-return
 //                          fp32 atomics (each channel has its own argmax, so the targets
 //                          of one instruction are scattered).
+//   pool_gather_kernel     the backward with a plan that holds tile lists (7x7 bins):
+//                          per (tile, 64 channels), the RoIs binned to the tile are
+//                          gathered into register accumulators, one 8x8 quadrant per
+//                          wave, and every gradient element is stored once (no atomics,
+//                          no separate clearing); see the comment above the kernel.
 //   pool_bwd_generic_kernel any strides: one thread per upstream-gradient element.
 #include <float.h>
 
-#include "internal.hpp"
+#include "gather.hpp"
 
 namespace rex {
 
@@ -337,6 +342,169 @@ hipError_t launch_pool_bwd(PoolArgs a, int gout_dtype, bool fast, hipStream_t st
         pool_bwd_generic_kernel<float><<<blocks, 256, 0, stream>>>(a);
     else
         pool_bwd_generic_kernel<uint16_t><<<blocks, 256, 0, stream>>>(a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Backward, tile-gather form
+// ---------------------------------------------------------------------------
+// The gradient of a pixel is the sum of the upstream gradients of every (RoI, bin)
+// whose argmax it is, for its channel.  With the plan's tile lists a workgroup owns the
+// 256 pixels of a tile region and 64 channels, accumulated in LDS, and walks the RoIs
+// binned to the tile: each RoI's gradient and argmax blocks ([64 channels][bins],
+// contiguous in memory) are read coalesced, the next RoI's while the current one is
+// added, and every element whose argmax lies in the region is added to its (channel,
+// pixel) accumulator with an LDS atomic.  No bin geometry is needed: the tile lists
+// hold every RoI whose bins can reach the tile.  The accumulators then leave through
+// the quadrant store of the align gather, so every gradient element is written once,
+// which replaces both the clearing and the device-scope atomics of the per-RoI form
+// (many bins of overlapping RoIs share their maximum pixel, and device-scope atomics
+// on one address are serialised).
+
+constexpr int kPoolGatherBins = 49;      // 7 x 7 grids
+constexpr int kPoolAccPitch = 257;       // LDS words per channel: 256 pixels + 1, so the
+                                         // 64 channels of one pixel fall in 64 banks
+constexpr int kPoolBlock = 64 * kPoolGatherBins;                  // elements of one block
+constexpr int kPoolThreads = 512;                                // 8 waves
+constexpr int kPoolPerThread = (kPoolBlock + kPoolThreads - 1) / kPoolThreads;   // 7
+
+bool pool_gather_available(int PH, int PW) { return PH * PW == kPoolGatherBins && PH == 7; }
+
+template <typename TG>
+__global__ __launch_bounds__(kPoolThreads) void pool_gather_kernel(GatherArgs a) {
+    constexpr int NB = kPoolGatherBins;
+    constexpr int P = kPoolAccPitch;
+    constexpr int E = kPoolPerThread;
+    __shared__ float s_acc[64 * P];       // [channel][pixel of the region]
+    __shared__ int s_k[64];
+    __shared__ int s_n;
+    static_assert(64 * P >= 4 * 512, "store scratch in the accumulators");
+    GatherTile x;
+    const int t = gather_tile(a, a.tile_order, x);
+    const GatherHead &h = a.head[0];
+    const int tid = threadIdx.x;
+    const int wave = uniform_i(tid >> 6);
+    const int lane = tid & 63;
+    // waves 0-3 own the region's quadrants; waves 4-7 only read and add
+    if (wave >= 4) x.wave_on = false;
+    const LevelArg &L = x.L;
+    for (int e = tid; e < 64 * P; e += kPoolThreads) s_acc[e] = 0.0f;
+
+    int s0 = h.tile_start[t];
+    int s1 = h.tile_end[t];
+    s0 = max(0, min(s0, h.capacity));
+    s1 = max(s0, min(s1, h.capacity));
+    const int64_t kstride = static_cast<int64_t>(a.lv.C) * NB;
+    const uint32_t nvalid = static_cast<uint32_t>(x.nch * NB);
+    // The region's origin as an argmax index, its size, and the level width divisor.
+    const int RW = x.WC1 - x.WC0, RH = x.WR1 - x.WR0;   // RW * RH = 256
+    const uint32_t W = static_cast<uint32_t>(L.W);
+    const uint32_t wm = pick(a.wid_m, x.l);
+    const int32_t wsh = pick(a.wid_sh, x.l);
+    // Per element of this thread: its channel row of the accumulators (or -1 past the
+    // block), fixed for the whole walk.
+    int crow[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+        const int e = tid + kPoolThreads * i;
+        crow[i] = e < kPoolBlock ? (e / NB) * P : -1;
+    }
+    uint32_t gv[3][E], av[3][E];
+    auto fetch = [&](int j, uint32_t (&g)[E], uint32_t (&am)[E]) {
+        const int k = uniform_i(s_k[j]);
+        const int64_t e0 = static_cast<int64_t>(x.cg) * 64 * NB + static_cast<int64_t>(k) * kstride;
+        const __amdgpu_buffer_rsrc_t rg = make_rsrc(
+            static_cast<const char *>(h.gout) + e0 * int64_t(sizeof(TG)), nvalid * uint32_t(sizeof(TG)));
+        const __amdgpu_buffer_rsrc_t ra = make_rsrc(
+            reinterpret_cast<const char *>(h.argmax) + e0 * 4, nvalid * 4u);
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            const uint32_t e = static_cast<uint32_t>(tid + kPoolThreads * i);
+            g[i] = buf_load_raw<TG>(rg, e * uint32_t(sizeof(TG)));
+            am[i] = __builtin_amdgcn_raw_buffer_load_b32(ra, e * 4u, 0, 0);
+        }
+    };
+    // Adds one staged RoI: an element whose argmax (y W + x) lies in the region goes to
+    // its accumulator.  -1 (an empty bin) and indices off the level give rows past it.
+    auto add = [&](const uint32_t (&g)[E], const uint32_t (&am)[E]) {
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            const uint32_t u = am[i];
+            const uint32_t y = fdiv(u, wm, wsh);
+            const uint32_t xx = u - y * W;
+            const uint32_t ly = y - static_cast<uint32_t>(x.WR0);
+            const uint32_t lx = xx - static_cast<uint32_t>(x.WC0);
+            if (crow[i] >= 0 && ly < static_cast<uint32_t>(RH) && lx < static_cast<uint32_t>(RW))
+                atomicAdd(&s_acc[crow[i] + static_cast<int>(ly) * RW + static_cast<int>(lx)],
+                          raw_to_f32<TG>(g[i]));
+        }
+    };
+
+    for (int base = s0; base < s1; base += 64) {
+        const int n = min(64, s1 - base);
+        __syncthreads();   // the previous batch's records are no longer read
+        // Records of this batch (wave 0): RoIs of this tile's level and image, compacted.
+        if (wave == 0) {
+            bool keep = false;
+            int k = 0;
+            if (lane < n) {
+                k = h.tile_rois[base + lane];
+                if (k >= 0 && k < h.K) {
+                    const int lvl = h.roi_levels ? h.roi_levels[k] : 0;
+                    keep = lvl == x.l && roi_batch(h.rois[5 * static_cast<int64_t>(k)], a.lv.N) == x.b;
+                }
+            }
+            const uint64_t km = __ballot(keep);
+            if (keep) {
+                const int pos = static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                    static_cast<uint32_t>(km >> 32),
+                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(km), 0u)));
+                s_k[pos] = k;
+            }
+            if (lane == 0) s_n = __builtin_popcountll(km);
+        }
+        __syncthreads();
+        const int nk = s_n;
+        if (nk == 0) continue;
+        // Unrolled by three so that each register set is named statically: the loads
+        // of RoIs j + 1 and j + 2 are in flight while RoI j is added.
+        fetch(0, gv[0], av[0]);
+        if (nk > 1) fetch(1, gv[1], av[1]);
+        for (int j = 0; j < nk; j += 3) {
+            if (j + 2 < nk) fetch(j + 2, gv[2], av[2]);
+            add(gv[0], av[0]);
+            if (j + 1 >= nk) break;
+            if (j + 3 < nk) fetch(j + 3, gv[0], av[0]);
+            add(gv[1], av[1]);
+            if (j + 2 >= nk) break;
+            if (j + 4 < nk) fetch(j + 4, gv[1], av[1]);
+            add(gv[2], av[2]);
+        }
+    }
+    __syncthreads();   // every addition is done
+    float acc[8][8] = {};
+    if (x.wave_on) {
+        const int p0 = (x.R0 - x.WR0) * RW + (x.Q0 - x.WC0);
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[r][q] = s_acc[lane * P + p0 + r * RW + q];
+    }
+    __syncthreads();   // the accumulators are read: the store may reuse them as scratch
+    if (wave < 4) gather_store(x, a.zero_init, acc, s_acc + wave * 512);
+}
+
+hipError_t launch_pool_gather(GatherArgs a, int gout_dtype, hipStream_t stream) {
+    if (!gather_prepare(a)) return hipErrorInvalidConfiguration;
+    const int64_t grid = static_cast<int64_t>(a.ntiles) * a.wg_per_tile * a.ncg;
+    if (grid <= 0) return hipSuccess;
+    if (grid >= (int64_t(1) << 24) || !pool_gather_available(a.PH, a.PW))
+        return hipErrorInvalidConfiguration;
+    const uint32_t g = static_cast<uint32_t>(grid);
+    if (gout_dtype == kF32)
+        pool_gather_kernel<float><<<g, kPoolThreads, 0, stream>>>(a);
+    else
+        pool_gather_kernel<uint16_t><<<g, kPoolThreads, 0, stream>>>(a);
     return hipGetLastError();
 }
 

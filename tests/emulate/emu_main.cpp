@@ -268,6 +268,7 @@ bool fwd_fast_available(int, int, int) { return false; }
 bool bwd_fast_available(int, int, int) { return false; }
 bool gather_available(int, int, int) { return false; }
 bool pool_fwd_fast_available(int, int) { return false; }
+bool pool_gather_available(int, int) { return false; }
 hipError_t launch_fwd(FwdArgs, int, int, bool, hipStream_t) { std::abort(); }
 hipError_t launch_fwd_multi(FwdMultiArgs, int, int, hipStream_t) { std::abort(); }
 hipError_t launch_bwd(BwdArgs, int, bool, hipStream_t) { std::abort(); }
@@ -275,6 +276,7 @@ hipError_t launch_gather(GatherArgs, int, hipStream_t) { std::abort(); }
 hipError_t launch_zero(const LevelTable &, const int64_t *, const int *, hipStream_t) { std::abort(); }
 hipError_t launch_pool_fwd(PoolArgs, int, int, bool, hipStream_t) { std::abort(); }
 hipError_t launch_pool_bwd(PoolArgs, int, bool, hipStream_t) { std::abort(); }
+hipError_t launch_pool_gather(GatherArgs, int, hipStream_t) { std::abort(); }
 hipError_t launch_deform_fwd(DeformArgs, int, int, bool, hipStream_t) { std::abort(); }
 hipError_t launch_deform_bwd(DeformArgs, int, int, bool, hipStream_t) { std::abort(); }
 hipError_t launch_nms(NmsArgs, hipStream_t) { std::abort(); }

@@ -18,6 +18,7 @@ bool fwd_fast_available(int PH, int PW, int S) {
 bool bwd_fast_available(int PH, int PW, int S) { return fwd_fast_available(PH, PW, S); }
 bool gather_available(int PH, int PW, int S) { return fwd_fast_available(PH, PW, S); }
 bool pool_fwd_fast_available(int PH, int PW) { return PH * PW <= kPoolFastBins; }
+bool pool_gather_available(int PH, int PW) { return PH == 7 && PW == 7; }
 hipError_t launch_level_map(const float *, int32_t, int32_t, float, int32_t, int32_t *, hipStream_t) { return hipSuccess; }
 hipError_t launch_plan(const PlanArgs &, hipStream_t) { return hipSuccess; }
 hipError_t launch_fwd(FwdArgs, int, int, bool, hipStream_t) { return hipSuccess; }
@@ -26,6 +27,7 @@ hipError_t launch_bwd(BwdArgs, int, bool, hipStream_t) { return hipSuccess; }
 hipError_t launch_gather(GatherArgs, int, hipStream_t) { return hipSuccess; }
 hipError_t launch_pool_fwd(PoolArgs, int, int, bool, hipStream_t) { return hipSuccess; }
 hipError_t launch_pool_bwd(PoolArgs, int, bool, hipStream_t) { return hipSuccess; }
+hipError_t launch_pool_gather(GatherArgs, int, hipStream_t) { return hipSuccess; }
 hipError_t launch_deform_fwd(DeformArgs, int, int, bool, hipStream_t) { return hipSuccess; }
 hipError_t launch_deform_bwd(DeformArgs, int, int, bool, hipStream_t) { return hipSuccess; }
 hipError_t launch_nms(NmsArgs, hipStream_t) { return hipSuccess; }

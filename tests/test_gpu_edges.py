@@ -283,6 +283,15 @@ def test_plan_five_kernel_path():
     run("9400 RoIs (five-kernel plan) mask", _pyr(16), SC, rois, out_hw=(14, 14))
 
 
+def test_wide_tiles_on_a_large_map():
+    """A map with more 16-pixel tiles than the plan bins (one 2048 x 2048 image): the
+    tile layout widens the tiles to 32 pixels, so a gather workgroup owns a band of four
+    8 x 8 quadrants (8 x 32 pixels) of a tile instead of a whole 16 x 16 tile."""
+    rng = np.random.default_rng(90)
+    rois = _rois(rng, 48, 1, 8192, 8192, outside=0.05)
+    run("2048 x 2048 map, 32-pixel tiles", [(1, 8, 2048, 2048)], [0.25], rois)
+
+
 def test_forward_many_rois_ragged_slices():
     """Enough RoIs that a forward workgroup takes several 64-channel slices of its RoI:
     300 channels = 4 slices + one of 44, so RoIs split 4 + 1 across two workgroups."""

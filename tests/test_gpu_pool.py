@@ -3,8 +3,10 @@ against the CPU oracle.
 
 The forward value is one of the input values, so it is compared bit for bit (after
 rounding the oracle's value to the output dtype), and the argmax is compared exactly.
-The backward sums with fp32 atomics, so it is compared with the backward tolerance:
-|gpu - ref| <= 1e-4 * S elementwise, S = the oracle's backward of |g|.
+The backward sums in an order of its own (LDS atomics in the tile gather, which runs
+whenever the plan holds tile lists and the grid is 7x7; device atomics otherwise), so it
+is compared with the backward tolerance: |gpu - ref| <= 1e-4 * S elementwise, S = the
+oracle's backward of |g|.
 """
 import numpy as np
 import pytest
@@ -191,3 +193,36 @@ def test_pool_full_box_head_workload():
     feats = wl.features()
     rois = wl.rois()
     run("box head workload", feats, list(wl.scales), rois, seed=2)
+
+
+def test_pool_gather_long_lists_and_five_kernel_plan():
+    """The tile gather on many long tile lists (40 hot spots of 40 RoIs, accumulating too)
+    and on a plan of more than 8192 RoIs (five kernels)."""
+    rng = np.random.default_rng(170)
+    shapes = [(1, 64, 128, 128), (1, 64, 64, 64), (1, 64, 32, 32), (1, 64, 16, 16)]
+    feats = [rng.standard_normal(s, dtype=np.float32) for s in shapes]
+    centres = rng.uniform(40, 472, (40, 2))
+    rows = []
+    for cx, cy in centres:
+        half = rng.uniform(8, 24, (40, 2))
+        jit = rng.uniform(-6, 6, (40, 2))
+        x1 = np.clip(cx + jit[:, 0] - half[:, 0], 0, 512)
+        x2 = np.clip(cx + jit[:, 0] + half[:, 0], 0, 512)
+        y1 = np.clip(cy + jit[:, 1] - half[:, 1], 0, 512)
+        y2 = np.clip(cy + jit[:, 1] + half[:, 1], 0, 512)
+        rows.append(np.stack([np.zeros(40), x1, y1, x2, y2], 1))
+    rois = np.concatenate(rows).astype(np.float32)
+    run("40 hot spots", feats, SC, rois)
+    run("40 hot spots accumulate", feats, SC, rois, zero_init=False)
+    run("9400 RoIs (five-kernel plan)", _pyr(rng, 16), SC,
+        W.draw_rois(rng, 2, 4700, (96, 160), (4.0, 200.0)))
+
+
+def test_pool_gather_wide_tiles():
+    """One 2048 x 2048 map: the tile layout takes 32-pixel tiles and a gather workgroup
+    owns an 8 x 32 band of a tile."""
+    rng = np.random.default_rng(171)
+    feats = [rng.standard_normal((1, 8, 2048, 2048), dtype=np.float32)]
+    rois = _rois(rng, 48, outside=0.05, img=(8192, 8192))
+    rois[:, 0] = 0
+    run("2048 x 2048 map", feats, [0.25], rois)
