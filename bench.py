@@ -74,12 +74,12 @@ def parse():
     return ap.parse_args()
 
 
-ALL_SOURCES = ("common.hpp", "internal.hpp", "plan.hip", "fwd.hip", "bwd.hip", "pool.hip",
-               "deform.hip", "nms.hip", "select.hip", "api.hip")
+ALL_SOURCES = ("common.hpp", "internal.hpp", "gather.hpp", "plan.hip", "fwd.hip", "bwd.hip",
+               "pool.hip", "deform.hip", "nms.hip", "select.hip", "api.hip")
 # the sources a kernel's code comes from (its device code and the shared headers)
 KERNEL_SOURCES = {"fwd": ("common.hpp", "internal.hpp", "fwd.hip"),
-                  "bwd_gather": ("common.hpp", "internal.hpp", "bwd.hip"),
-                  "bwd_scatter": ("common.hpp", "internal.hpp", "bwd.hip")}
+                  "bwd_gather": ("common.hpp", "internal.hpp", "gather.hpp", "bwd.hip"),
+                  "bwd_scatter": ("common.hpp", "internal.hpp", "gather.hpp", "bwd.hip")}
 
 
 def kernel_source_hash(kernel: str = None) -> str:

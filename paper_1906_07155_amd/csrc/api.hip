@@ -831,7 +831,11 @@ re_status_t roi_pool_fwd(const re_level_t *levels, int32_t num_levels, const flo
     a.K = static_cast<int32_t>(num_rois);
     a.PH = out_h;
     a.PW = out_w;
-    const bool fast = cl && pool_fwd_fast_available(out_h, out_w);
+    // the channels-last kernel keeps pixel indices in 24 bits
+    bool small_maps = true;
+    for (int l = 0; l < num_levels; ++l)
+        if (int64_t(t.l[l].H) * t.l[l].W >= (int64_t(1) << 24)) small_maps = false;
+    const bool fast = cl && small_maps && pool_fwd_fast_available(out_h, out_w);
     return from_hip(launch_pool_fwd(a, levels[0].dtype, out_dtype, fast,
                                     static_cast<hipStream_t>(stream)));
 }

@@ -31,7 +31,8 @@
 
 namespace rex {
 
-constexpr int kPoolBatch = 16;   // pixel loads of one bin in flight at a time
+constexpr int kPoolBatch = 16;   // pixel loads per batch (two batches in flight)
+constexpr int kPoolWaveBins = (kPoolFastBins + 3) / 4;   // bins of one wave of the forward
 
 // Pixel range [lo, hi) of bin p along one axis, binary32, one rounding per operation:
 // the box end points are rounded to whole pixels (halves away from zero), the box
@@ -63,10 +64,13 @@ __device__ __forceinline__ PoolRange pool_bin(float c1, float c2, float scale, i
 // Bit pattern stored for the "no comparable value" sentinel -FLT_MAX: binary32 as is;
 // bfloat16 takes the most negative finite bf16 (-FLT_MAX rounded toward zero), since
 // rounding to nearest would give -inf.
+__device__ __forceinline__ uint16_t pool_bf16(float v) {
+    return (v == -FLT_MAX) ? static_cast<uint16_t>(0xFF7Fu) : f32_to_bf16(v);
+}
 template <typename TO> __device__ __forceinline__ void store_pool(gptr<TO> p, float v);
 template <> __device__ __forceinline__ void store_pool<float>(gptr<float> p, float v) { *p = v; }
 template <> __device__ __forceinline__ void store_pool<uint16_t>(gptr<uint16_t> p, float v) {
-    *p = (v == -FLT_MAX) ? static_cast<uint16_t>(0xFF7Fu) : f32_to_bf16(v);
+    *p = pool_bf16(v);
 }
 
 // ---------------------------------------------------------------------------
@@ -123,6 +127,8 @@ template <typename T, typename TO>
 __global__ __launch_bounds__(256) void pool_fwd_cl_kernel(PoolArgs a) {
     // [64][NB] values then [64][NB] argmax; sized at launch (64 * NB * 8 bytes)
     extern __shared__ __align__(16) float s_pool[];
+    __shared__ int s_rng[4][kPoolFastBins];   // per bin row: first, end row; per column: first, end
+    __shared__ int s_wbin[4][kPoolWaveBins * 5 + 1];   // per wave: its bins' layout, its element count
     const int PH = a.PH, PW = a.PW;
     const int NB = PH * PW;
     float *const s_val = s_pool;
@@ -141,8 +147,9 @@ __global__ __launch_bounds__(256) void pool_fwd_cl_kernel(PoolArgs a) {
     const int b = roi_batch(rb, a.lv.N);
     const bool active = kvalid && lvalid && b >= 0;
 
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
+    const int tid = threadIdx.x;
+    const int wave = uniform_i(tid >> 6);
+    const int lane = tid & 63;
     const int c = slice * 64 + lane;
     const int nch = min(64, a.lv.C - slice * 64);
     // one image of the level through a buffer resource; lanes past the last channel
@@ -154,55 +161,135 @@ __global__ __launch_bounds__(256) void pool_fwd_cl_kernel(PoolArgs a) {
     const uint32_t sh = static_cast<uint32_t>(L.sh) * uint32_t(sizeof(T));
     const uint32_t sw = static_cast<uint32_t>(L.sw) * uint32_t(sizeof(T));
 
-    // bins dealt round-robin to the four waves
+    // The bins' pixel ranges, once per workgroup (bin (ph, pw) covers rows
+    // [s_rng[0][ph], s_rng[1][ph]) and columns [s_rng[2][pw], s_rng[3][pw])), and the
+    // results of an empty bin (0, -1) in every slot this wave owns.
+    if (tid < PH) {
+        const PoolRange rr = pool_bin(y1, y2, L.scale, PH, tid, L.H);
+        s_rng[0][tid] = rr.lo;
+        s_rng[1][tid] = rr.hi;
+    } else if (tid < PH + PW) {
+        const PoolRange rr = pool_bin(x1, x2, L.scale, PW, tid - PH, L.W);
+        s_rng[2][tid - PH] = rr.lo;
+        s_rng[3][tid - PH] = rr.hi;
+    }
     for (int jb = wave; jb < NB; jb += 4) {
-        const int ph = jb / PW, pw = jb - (jb / PW) * PW;
-        {
-            const PoolRange ry = pool_bin(y1, y2, L.scale, PH, ph, L.H);
-            const PoolRange rx = pool_bin(x1, x2, L.scale, PW, pw, L.W);
-            float best = 0.0f;
-            int arg = -1;
-            if (active && ry.hi > ry.lo && rx.hi > rx.lo) {
-                best = -FLT_MAX;
-                // The bin's pixels in row-major order, kPoolBatch loads in flight at a
-                // time, then compared in order so the first maximum wins.  A position
-                // past the bin takes the out-of-range lane offset and reads zero without
-                // a memory access (the hardware range check covers the lane offset only,
-                // never the scalar one, so the scalar offset is always an in-map pixel);
-                // its value is skipped.
-                const int nx = rx.hi - rx.lo;
-                const int n = (ry.hi - ry.lo) * nx;
-                int y = ry.lo, x = rx.lo;
-                for (int i0 = 0; i0 < n; i0 += kPoolBatch) {
-                    float v[kPoolBatch];
-                    int yy = y, xx = x;
+        s_val[lane * NB + jb] = 0.0f;
+        s_arg[lane * NB + jb] = -1;
+    }
+    __syncthreads();
+
+    // Wave w takes bins w, w + 4, ... and streams their pixels as one sequence, each bin
+    // row by row, each row left to right: two batches of kPoolBatch loads are in
+    // flight, across bin boundaries, while the oldest batch is compared in order (so
+    // the first maximum of a bin still wins).  Where each element of the sequence lies
+    // is worked out 64 elements at a time, one element per lane (its bin by a search
+    // of the bins' starts, then row and column), and read back one element at a time
+    // with a lane read, so the walk costs no scalar bookkeeping per pixel.
+    //   per wave and bin i: start of the bin in the sequence, first row, first column,
+    //   width, pixel count
+    int *const wb = s_wbin[wave];
+    const int nbw = active && wave < NB ? (NB - wave + 3) >> 2 : 0;   // this wave's bins
+    {
+        int area = 0, ylo = 0, xlo = 0, w = 1;
+        if (lane < nbw) {
+            const int jb = wave + 4 * lane;
+            const int ph = jb / PW, pw = jb - ph * PW;
+            ylo = s_rng[0][ph];
+            xlo = s_rng[2][pw];
+            const int h = s_rng[1][ph] - ylo;
+            w = s_rng[3][pw] - xlo;
+            area = h > 0 && w > 0 ? h * w : 0;
+            if (w <= 0) w = 1;
+        }
+        const int incl = wave_inclusive_scan(area, lane);
+        if (lane < nbw) {
+            wb[lane * 5 + 0] = incl - area;
+            wb[lane * 5 + 1] = ylo;
+            wb[lane * 5 + 2] = xlo;
+            wb[lane * 5 + 3] = w;
+            wb[lane * 5 + 4] = area;
+        }
+        wb[kPoolWaveBins * 5] = __shfl(incl, 63);   // elements of this wave
+    }
+    wave_sync();
+    const int n_w = uniform_i(wb[kPoolWaveBins * 5]);
+    const uint32_t Wu = static_cast<uint32_t>(L.W);
+    // Element e0 + lane of the sequence: its byte offset in the image, and its argmax
+    // index with, in the top 8 bits, 1 + the bin's number when it is the bin's last
+    // pixel (0 otherwise).  Elements past the end load pixel 0 and end no bin.
+    auto locate = [&](int e0, uint32_t &off, uint32_t &pixf) {
+        const int e = e0 + lane;
+        int bi = 0;
+        for (int q = 1; q < nbw; ++q) bi = e >= uniform_i(wb[q * 5]) ? q : bi;
+        off = 0;
+        pixf = 0;
+        if (e < n_w) {
+            const int local = e - wb[bi * 5];
+            const int w = wb[bi * 5 + 3];
+            // row = local / w: the binary32 estimate (local < 2^24, exact as a float; the
+            // reciprocal and the product add under two units of the last place of a
+            // quotient below 2^23 when w >= 2, none when w = 1) is within two of it
+            int row = static_cast<int>(static_cast<float>(local) * __builtin_amdgcn_rcpf(static_cast<float>(w)));
+            if (row * w > local) --row;
+            if (row * w > local) --row;
+            if ((row + 1) * w <= local) ++row;
+            if ((row + 1) * w <= local) ++row;
+            const uint32_t y = static_cast<uint32_t>(wb[bi * 5 + 1] + row);
+            const uint32_t x = static_cast<uint32_t>(wb[bi * 5 + 2] + (local - row * w));
+            off = y * sh + x * sw;
+            const bool last = local == wb[bi * 5 + 4] - 1;
+            pixf = (y * Wu + x) | (last ? static_cast<uint32_t>(bi + 1) << 24 : 0u);
+        }
+    };
+    float best = -FLT_MAX;
+    int arg = -1;
+    auto issue = [&](uint32_t (&v)[kPoolBatch], uint32_t off, int base) {
 #pragma unroll
-                    for (int j = 0; j < kPoolBatch; ++j) {
-                        const bool in_bin = i0 + j < n;
-                        const uint32_t off = in_bin ? static_cast<uint32_t>(yy) * sh +
-                                                          static_cast<uint32_t>(xx) * sw
-                                                    : 0u;
-                        v[j] = raw_to_f32<T>(buf_load_raw_s<T>(rs, in_bin ? vo : kBufOOB, off));
-                        if (++xx == rx.hi) {
-                            xx = rx.lo;
-                            ++yy;
-                        }
-                    }
+        for (int j = 0; j < kPoolBatch; ++j)
+            v[j] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(off, base + j));
+    };
+    auto consume = [&](const uint32_t (&v)[kPoolBatch], uint32_t pixf, int base) {
 #pragma unroll
-                    for (int j = 0; j < kPoolBatch; ++j) {
-                        if (i0 + j < n && v[j] > best) {
-                            best = v[j];
-                            arg = y * L.W + x;
-                        }
-                        if (++x == rx.hi) {
-                            x = rx.lo;
-                            ++y;
-                        }
-                    }
-                }
+        for (int j = 0; j < kPoolBatch; ++j) {
+            const uint32_t pf = __builtin_amdgcn_readlane(pixf, base + j);
+            const float f = raw_to_f32<T>(v[j]);
+            if (f > best) {
+                best = f;
+                arg = static_cast<int>(pf & 0xFFFFFFu);
             }
-            s_val[lane * NB + ph * PW + pw] = best;
-            s_arg[lane * NB + ph * PW + pw] = arg;
+            if (pf >> 24) {   // the bin's last pixel: its results, then the next bin
+                const int jb = wave + 4 * static_cast<int>((pf >> 24) - 1);
+                s_val[lane * NB + jb] = best;
+                s_arg[lane * NB + jb] = arg;
+                best = -FLT_MAX;
+                arg = -1;
+            }
+        }
+    };
+    static_assert(64 % (2 * kPoolBatch) == 0, "batches per located chunk");
+    if (n_w > 0) {
+        uint32_t off, pixf, off_n, pixf_n;
+        uint32_t va[kPoolBatch], vb[kPoolBatch];
+        locate(0, off, pixf);
+        issue(va, off, 0);
+        issue(vb, off, kPoolBatch);
+        for (int e0 = 0; e0 < n_w; e0 += 64) {
+            // batches 0-1 of this chunk are in flight; 2-3 follow, then the next chunk's 0-1
+            consume(va, pixf, 0);
+            if (e0 + 2 * kPoolBatch < n_w) issue(va, off, 2 * kPoolBatch);
+            consume(vb, pixf, kPoolBatch);
+            if (e0 + 3 * kPoolBatch < n_w) issue(vb, off, 3 * kPoolBatch);
+            const bool more = e0 + 64 < n_w;
+            if (more) locate(e0 + 64, off_n, pixf_n);
+            if (e0 + 2 * kPoolBatch >= n_w) break;
+            consume(va, pixf, 2 * kPoolBatch);
+            if (more) issue(va, off_n, 0);
+            if (e0 + 3 * kPoolBatch >= n_w) break;
+            consume(vb, pixf, 3 * kPoolBatch);
+            if (more) issue(vb, off_n, kPoolBatch);
+            off = off_n;
+            pixf = pixf_n;
         }
     }
     __syncthreads();
@@ -211,7 +298,32 @@ __global__ __launch_bounds__(256) void pool_fwd_cl_kernel(PoolArgs a) {
     const int64_t o0 = (static_cast<int64_t>(k) * a.lv.C + static_cast<int64_t>(slice) * 64) * NB;
     const gptr<TO> out = as_global_mut<TO>(a.out) + o0;
     gptr<int32_t> am = as_global_mut<int32_t>(a.argmax) + o0;
-    for (int e = threadIdx.x; e < nch * NB; e += 256) {
+    const int n = nch * NB;
+    int done = 0;
+    // Four elements per store where both blocks are aligned to 4 elements (always for a
+    // multiple of 4 channels): 16-byte argmax stores, 16- or 8-byte value stores.  The
+    // values are never read back by this operator, so they stream past the caches; the
+    // argmax is read by the backward and is stored as usual.
+    if ((reinterpret_cast<uintptr_t>(out) & (4 * sizeof(TO) - 1)) == 0 &&
+        (reinterpret_cast<uintptr_t>(am) & 15u) == 0) {
+        const int nv = n >> 2;
+        for (int v = threadIdx.x; v < nv; v += 256) {
+            const float4 f = *reinterpret_cast<const float4 *>(s_val + 4 * v);
+            const u32x4 g = *reinterpret_cast<const u32x4 *>(s_arg + 4 * v);
+            *reinterpret_cast<REX_GLOBAL u32x4 *>(am + 4 * v) = g;
+            if constexpr (sizeof(TO) == 4) {
+                const u32x4 w = {__float_as_uint(f.x), __float_as_uint(f.y), __float_as_uint(f.z),
+                                 __float_as_uint(f.w)};
+                __builtin_nontemporal_store(w, reinterpret_cast<REX_GLOBAL u32x4 *>(out + 4 * v));
+            } else {
+                const u32x2 w = {static_cast<uint32_t>(pool_bf16(f.x)) | (static_cast<uint32_t>(pool_bf16(f.y)) << 16),
+                                 static_cast<uint32_t>(pool_bf16(f.z)) | (static_cast<uint32_t>(pool_bf16(f.w)) << 16)};
+                __builtin_nontemporal_store(w, reinterpret_cast<REX_GLOBAL u32x2 *>(out + 4 * v));
+            }
+        }
+        done = nv << 2;
+    }
+    for (int e = done + static_cast<int>(threadIdx.x); e < n; e += 256) {
         store_pool<TO>(out + e, s_val[e]);
         am[e] = s_arg[e];
     }
