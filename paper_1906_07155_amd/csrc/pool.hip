@@ -6,13 +6,14 @@
 // Definition, tie rule and sentinels are stated in include/roi_extract.h.
 //
 // Kernels:
-//   pool_fwd_cl_kernel     channels-last levels, out_h * out_w <= kPoolFastBins.  One
-//                          workgroup = one RoI x one slice of 64 channels; lanes run
-//                          over channels, so every pixel read is one coalesced load,
-//                          and each wave scans the pixels of its bins in row-major order
-//                          with sixteen loads in flight.  Values and argmax leave through
-//                          an LDS transpose so the [C][PH][PW] blocks are stored
-//                          contiguously at the RoI's original index.
+//   pool_fwd_cl_kernel     channels-last levels, out_h * out_w <= kPoolFastBins, maps
+//                          of fewer than 2^24 pixels.  One workgroup = one RoI x one
+//                          slice of 64 channels; lanes run over channels, so every
+//                          pixel read is one coalesced load, and each wave walks the
+//                          pixels of its bins as one sequence with two batches of loads
+//                          in flight.  Values and argmax leave through an LDS transpose
+//                          so the [C][PH][PW] blocks are stored contiguously at the
+//                          RoI's original index.
 //   pool_fwd_generic_kernel any strides and grid sizes: one thread per output element.
 //   pool_bwd_cl_kernel     channels-last gradient levels: the RoI's gradient and argmax
 //                          blocks are read coalesced through LDS, then every lane adds
@@ -20,10 +21,10 @@
 //                          fp32 atomics (each channel has its own argmax, so the targets
 //                          of one instruction are scattered).
 //   pool_gather_kernel     the backward with a plan that holds tile lists (7x7 bins):
-//                          per (tile, 64 channels), the RoIs binned to the tile are
-//                          gathered into register accumulators, one 8x8 quadrant per
-//                          wave, and every gradient element is stored once (no atomics,
-//                          no separate clearing); see the comment above the kernel.
+//                          per (tile region, 64 channels), the RoIs binned to the tile
+//                          are added into LDS accumulators and every gradient element
+//                          is stored once (no device atomics, no separate clearing);
+//                          see the comment above the kernel.
 //   pool_bwd_generic_kernel any strides: one thread per upstream-gradient element.
 #include <float.h>
 
