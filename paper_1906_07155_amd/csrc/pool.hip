@@ -475,8 +475,8 @@ hipError_t launch_pool_bwd(PoolArgs a, int gout_dtype, bool fast, hipStream_t st
 // on one address are serialised).
 
 constexpr int kPoolGatherBins = 49;      // 7 x 7 grids
-constexpr int kPoolAccPitch = 257;       // LDS words per channel: 256 pixels + 1, so the
-                                         // 64 channels of one pixel fall in 64 banks
+constexpr int kPoolAccPitch = 260;       // LDS words per channel: 256 pixels + 4, 16-byte
+                                         // rows whose channels start in different banks
 constexpr int kPoolBlock = 64 * kPoolGatherBins;                  // elements of one block
 constexpr int kPoolThreads = 512;                                // 8 waves
 constexpr int kPoolPerThread = (kPoolBlock + kPoolThreads - 1) / kPoolThreads;   // 7
@@ -488,7 +488,7 @@ __global__ __launch_bounds__(kPoolThreads) void pool_gather_kernel(GatherArgs a)
     constexpr int NB = kPoolGatherBins;
     constexpr int P = kPoolAccPitch;
     constexpr int E = kPoolPerThread;
-    __shared__ float s_acc[64 * P];       // [channel][pixel of the region]
+    __shared__ __align__(16) float s_acc[64 * P];   // [channel][pixel of the region]
     __shared__ int s_k[64];
     __shared__ int s_n;
     static_assert(64 * P >= 4 * 512, "store scratch in the accumulators");
@@ -501,7 +501,9 @@ __global__ __launch_bounds__(kPoolThreads) void pool_gather_kernel(GatherArgs a)
     // waves 0-3 own the region's quadrants; waves 4-7 only read and add
     if (wave >= 4) x.wave_on = false;
     const LevelArg &L = x.L;
-    for (int e = tid; e < 64 * P; e += kPoolThreads) s_acc[e] = 0.0f;
+    static_assert(P % 4 == 0, "16-byte accumulator rows");
+    for (int e = tid; e < 64 * P / 4; e += kPoolThreads)
+        reinterpret_cast<float4 *>(s_acc)[e] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 
     int s0 = h.tile_start[t];
     int s1 = h.tile_end[t];
@@ -597,11 +599,22 @@ __global__ __launch_bounds__(kPoolThreads) void pool_gather_kernel(GatherArgs a)
     __syncthreads();   // every addition is done
     float acc[8][8] = {};
     if (x.wave_on) {
+        // a quadrant row is 8 words at a multiple of 8 (RW and the quadrant's origin are
+        // multiples of 8): two 16-byte reads
         const int p0 = (x.R0 - x.WR0) * RW + (x.Q0 - x.WC0);
 #pragma unroll
-        for (int r = 0; r < 8; ++r)
-#pragma unroll
-            for (int q = 0; q < 8; ++q) acc[r][q] = s_acc[lane * P + p0 + r * RW + q];
+        for (int r = 0; r < 8; ++r) {
+            const float4 lo = *reinterpret_cast<const float4 *>(s_acc + lane * P + p0 + r * RW);
+            const float4 hi = *reinterpret_cast<const float4 *>(s_acc + lane * P + p0 + r * RW + 4);
+            acc[r][0] = lo.x;
+            acc[r][1] = lo.y;
+            acc[r][2] = lo.z;
+            acc[r][3] = lo.w;
+            acc[r][4] = hi.x;
+            acc[r][5] = hi.y;
+            acc[r][6] = hi.z;
+            acc[r][7] = hi.w;
+        }
     }
     __syncthreads();   // the accumulators are read: the store may reuse them as scratch
     if (wave < 4) gather_store(x, a.zero_init, acc, s_acc + wave * 512);
