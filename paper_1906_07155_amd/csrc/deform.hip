@@ -6,6 +6,10 @@
 // Definition and gradients are stated in include/roi_extract.h.
 //
 // Kernels:
+//   deform_fwd_stream_kernel channels-last features, a fixed grid of up to 4 x 4 samples:
+//                            as deform_fwd_cl_kernel, but each wave walks the samples of
+//                            its bins as one sequence with two batches of corner loads
+//                            in flight (see the comment above the kernel).
 //   deform_fwd_cl_kernel     channels-last features.  One workgroup = one RoI x one
 //                            slice of 64 channels; lanes run over channels, so every tap
 //                            is one coalesced load; the bins are dealt round-robin to
@@ -313,6 +317,159 @@ __global__ __launch_bounds__(256) void deform_fwd_cl_kernel(DeformArgs a) {
     for (int e = threadIdx.x; e < d.nch * NB; e += 256) store_f32<TO>(out + e, s_out[e]);
 }
 
+// The forward for a fixed grid of S x S samples per bin (S <= 4), pipelined: wave w
+// takes bins w, w + 4, ... and walks their samples as one sequence (each bin's samples
+// row by row), the four corner loads of two batches of kDeformBatch samples in flight
+// across bin boundaries while the oldest batch is summed in the order of the
+// definition.  Where each sample lies (its four byte offsets, its four weights, whether
+// it is valid and whether it ends its bin) is worked out 64 samples at a time, one per
+// lane, and read back per sample with lane reads.  Taps, weights and the bin sum are
+// those of deform_fwd_cl_kernel, operation for operation.
+constexpr int kDeformBatch = 4;              // samples per batch: 16 loads
+constexpr int kDeformStreamBins = 196;       // bins of the channels-last kernels
+
+struct DeformMeta {
+    uint32_t o11, o12, o21, o22;             // byte offsets of the corners in the image
+    uint32_t w11, w12, w21, w22;             // their weights (binary32 bits)
+    uint32_t flags;                          // 1: valid, 2: last sample of its bin, bin << 2
+};
+
+template <typename T, typename TO>
+__global__ __launch_bounds__(256) void deform_fwd_stream_kernel(DeformArgs a) {
+    extern __shared__ __align__(16) float s_out[];   // [64][NB]
+    __shared__ float s_sx[kDeformStreamBins], s_sy[kDeformStreamBins], s_m[kDeformStreamBins];
+    const int PW = a.PW;
+    const int NB = a.PH * PW;
+    const DeformRoi d = deform_roi(a);
+    const int tid = threadIdx.x;
+    const int wave = uniform_i(tid >> 6);
+    const int lane = tid & 63;
+    const LevelArg &L = d.L;
+    const char *img = static_cast<const char *>(L.data) +
+                      static_cast<int64_t>(d.active ? d.b : 0) * L.sn * static_cast<int64_t>(sizeof(T));
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(img, L.img_bytes);
+    const uint32_t vo =
+        lane < d.nch ? static_cast<uint32_t>(d.slice * 64 + lane) * uint32_t(sizeof(T)) : kBufOOB;
+    const uint32_t sh = static_cast<uint32_t>(L.sh) * uint32_t(sizeof(T));
+    const uint32_t sw = static_cast<uint32_t>(L.sw) * uint32_t(sizeof(T));
+    // the bins' shifts and modulation, once per workgroup; an inactive RoI stores zeros
+    if (d.active && tid < NB) {
+        const int64_t k = d.k;
+        s_sx[tid] = deform_shift(a.gamma, a.offset[2 * k * NB + tid], d.ax.len);
+        s_sy[tid] = deform_shift(a.gamma, a.offset[(2 * k + 1) * NB + tid], d.ay.len);
+        s_m[tid] = a.mask ? a.mask[k * NB + tid] : 1.0f;
+    }
+    for (int jb = wave; jb < NB; jb += 4) s_out[lane * NB + jb] = 0.0f;
+    __syncthreads();
+
+    const int S = a.S, G = S * S;
+    const int nbw = d.active && wave < NB ? (NB - wave + 3) >> 2 : 0;   // this wave's bins
+    const int n_w = nbw * G;                                            // and their samples
+    const float fcount = static_cast<float>(max(d.ay.grid * d.ax.grid, 1));
+    // floor(n / D) = (n * ceil(2^16 / D)) >> 16 exactly for the small n and D used here
+    // (n < 2^10, D <= 196: the rounding up adds less than 1/D to the quotient)
+    const uint32_t mG = (65536u + G - 1) / G, mS = (65536u + S - 1) / S;
+    const uint32_t mPW = (65536u + PW - 1) / PW;
+    auto locate = [&](int e0, DeformMeta &m) {
+        const int e = e0 + lane;
+        m.o11 = m.o12 = m.o21 = m.o22 = 0;
+        m.w11 = m.w12 = m.w21 = m.w22 = 0;
+        m.flags = 0;
+        if (e < n_w) {
+            const int i = static_cast<int>((static_cast<uint32_t>(e) * mG) >> 16);
+            const int sm = e - i * G;
+            const int iy = static_cast<int>((static_cast<uint32_t>(sm) * mS) >> 16);
+            const int ix = sm - iy * S;
+            const int jb = wave + 4 * i;
+            const int ph = static_cast<int>((static_cast<uint32_t>(jb) * mPW) >> 16);
+            const int pw = jb - ph * PW;
+            const DTap ty = deform_tap(d.ay, s_sy[jb], ph, iy, L.H);
+            const DTap tx = deform_tap(d.ax, s_sx[jb], pw, ix, L.W);
+            const bool valid = ty.valid && tx.valid;
+            if (valid) {
+                const uint32_t r0 = static_cast<uint32_t>(ty.lo) * sh, r1 = static_cast<uint32_t>(ty.hi) * sh;
+                const uint32_t c0 = static_cast<uint32_t>(tx.lo) * sw, c1 = static_cast<uint32_t>(tx.hi) * sw;
+                m.o11 = r0 + c0;
+                m.o12 = r0 + c1;
+                m.o21 = r1 + c0;
+                m.o22 = r1 + c1;
+                m.w11 = __float_as_uint(ty.wlo * tx.wlo);
+                m.w12 = __float_as_uint(ty.wlo * tx.whi);
+                m.w21 = __float_as_uint(ty.whi * tx.wlo);
+                m.w22 = __float_as_uint(ty.whi * tx.whi);
+            }
+            m.flags = (valid ? 1u : 0u) | (sm == G - 1 ? 2u : 0u) | (static_cast<uint32_t>(i) << 2);
+        }
+    };
+    auto issue = [&](uint32_t (&v)[4 * kDeformBatch], const DeformMeta &m, int base) {
+#pragma unroll
+        for (int j = 0; j < kDeformBatch; ++j) {
+            v[4 * j + 0] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(m.o11, base + j));
+            v[4 * j + 1] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(m.o12, base + j));
+            v[4 * j + 2] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(m.o21, base + j));
+            v[4 * j + 3] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(m.o22, base + j));
+        }
+    };
+    float sum = 0.0f;
+    auto consume = [&](const uint32_t (&v)[4 * kDeformBatch], const DeformMeta &m, int base) {
+#pragma unroll
+        for (int j = 0; j < kDeformBatch; ++j) {
+            const uint32_t f = __builtin_amdgcn_readlane(m.flags, base + j);
+            if (f & 1u) {
+                sum = fmaf(__uint_as_float(__builtin_amdgcn_readlane(m.w11, base + j)),
+                           raw_to_f32<T>(v[4 * j + 0]), sum);
+                sum = fmaf(__uint_as_float(__builtin_amdgcn_readlane(m.w12, base + j)),
+                           raw_to_f32<T>(v[4 * j + 1]), sum);
+                sum = fmaf(__uint_as_float(__builtin_amdgcn_readlane(m.w21, base + j)),
+                           raw_to_f32<T>(v[4 * j + 2]), sum);
+                sum = fmaf(__uint_as_float(__builtin_amdgcn_readlane(m.w22, base + j)),
+                           raw_to_f32<T>(v[4 * j + 3]), sum);
+            }
+            if (f & 2u) {   // the bin's last sample
+                const int jb = wave + 4 * static_cast<int>(f >> 2);
+                s_out[lane * NB + jb] = s_m[jb] * (sum / fcount);
+                sum = 0.0f;
+            }
+        }
+    };
+    if (n_w > 0) {
+        constexpr int kPerChunk = 64 / kDeformBatch;   // batches per located chunk
+        DeformMeta cur, nxt;
+        locate(0, cur);
+        if (n_w > 64) locate(64, nxt);
+        const int nbatch = (n_w + kDeformBatch - 1) / kDeformBatch;
+        uint32_t va[4 * kDeformBatch], vb[4 * kDeformBatch];
+        issue(va, cur, 0);
+        if (nbatch > 1) issue(vb, cur, kDeformBatch);
+        int c0 = 0;   // first batch of the current chunk
+        for (int q = 0; q < nbatch; q += 2) {
+            const int qs = q - c0;
+            consume(va, cur, qs * kDeformBatch);
+            if (q + 2 < nbatch) {
+                if (qs + 2 < kPerChunk) issue(va, cur, (qs + 2) * kDeformBatch);
+                else issue(va, nxt, (qs + 2 - kPerChunk) * kDeformBatch);
+            }
+            if (q + 1 >= nbatch) break;
+            consume(vb, cur, (qs + 1) * kDeformBatch);
+            if (q + 3 < nbatch) {
+                if (qs + 3 < kPerChunk) issue(vb, cur, (qs + 3) * kDeformBatch);
+                else issue(vb, nxt, (qs + 3 - kPerChunk) * kDeformBatch);
+            }
+            if (qs + 2 == kPerChunk) {   // the next chunk becomes the current one
+                cur = nxt;
+                c0 += kPerChunk;
+                if ((c0 + kPerChunk) * kDeformBatch < n_w) locate((c0 + kPerChunk) * kDeformBatch, nxt);
+            }
+        }
+    }
+    __syncthreads();
+    if (!d.kvalid) return;   // uniform over the workgroup, after the last barrier
+    const int64_t o0 =
+        (static_cast<int64_t>(d.k) * a.lv.C + static_cast<int64_t>(d.slice) * 64) * NB;
+    const gptr<TO> out = as_global_mut<TO>(a.out) + o0;
+    for (int e = threadIdx.x; e < d.nch * NB; e += 256) store_f32<TO>(out + e, s_out[e]);
+}
+
 template <typename T, typename TG>
 __global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
     extern __shared__ __align__(16) float s_g[];   // [64][NB] upstream gradient of the slice
@@ -472,7 +629,10 @@ static void fwd_typed(const DeformArgs &a, bool fast, hipStream_t stream) {
     const int NB = a.PH * a.PW;
     if (fast) {
         const uint32_t g = static_cast<uint32_t>(static_cast<int64_t>(a.K) * a.nslices);
-        deform_fwd_cl_kernel<T, TO><<<g, 256, static_cast<size_t>(64) * NB * 4, stream>>>(a);
+        if (a.S >= 1 && a.S <= 4 && NB <= kDeformStreamBins)
+            deform_fwd_stream_kernel<T, TO><<<g, 256, static_cast<size_t>(64) * NB * 4, stream>>>(a);
+        else
+            deform_fwd_cl_kernel<T, TO><<<g, 256, static_cast<size_t>(64) * NB * 4, stream>>>(a);
     } else {
         const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * NB;
         const uint32_t blocks = static_cast<uint32_t>(std::min<int64_t>((total + 255) / 256, 16384));

@@ -111,7 +111,7 @@ def test_deform_channels_ragged(C):
     run("C=%d" % C, _pyr(rng, C), SC, W.draw_rois(rng, 2, 17, (96, 160), (4.0, 200.0)))
 
 
-@pytest.mark.parametrize("S,aligned", [(0, True), (1, False), (3, True)])
+@pytest.mark.parametrize("S,aligned", [(0, True), (1, False), (3, True), (4, False)])
 def test_deform_sampling_and_alignment(S, aligned):
     rng = np.random.default_rng(210 + S)
     run("S=%d aligned=%d" % (S, aligned), _pyr(rng, 40), SC,
@@ -131,6 +131,7 @@ def test_deform_layouts_grids_and_no_mask():
     r = W.draw_rois(rng, 2, 11, (96, 160), (4.0, 200.0))
     run("NCHW levels (general kernels)", f, SC, r, layout="nchw")
     run("14x14", f, SC, r, out_hw=(14, 14))
+    run("14x14 S=4 (784 samples per wave: 13 located chunks)", f, SC, r, out_hw=(14, 14), S=4)
     run("16x16 (general kernels)", f, SC, r, out_hw=(16, 16))
     run("5x3 without mask", f, SC, r, out_hw=(5, 3), with_mask=False)
     run("without plan, accumulate", f, SC, r, use_plan=False, zero_init=False)
