@@ -268,7 +268,7 @@ __global__ __launch_bounds__(256) void pool_fwd_cl_kernel(PoolArgs a) {
             }
         }
     };
-    static_assert(64 % (2 * kPoolBatch) == 0, "batches per located chunk");
+    static_assert(4 * kPoolBatch == 64, "a located chunk is four batches");
     if (n_w > 0) {
         uint32_t off, pixf, off_n, pixf_n;
         uint32_t va[kPoolBatch], vb[kPoolBatch];
