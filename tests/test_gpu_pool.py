@@ -226,3 +226,15 @@ def test_pool_gather_wide_tiles():
     rois = _rois(rng, 48, outside=0.05, img=(8192, 8192))
     rois[:, 0] = 0
     run("2048 x 2048 map", feats, [0.25], rois)
+
+
+def test_pool_map_of_2_24_pixels():
+    """A 4096 x 4096 map: pixel indices no longer fit the 24 bits of the channels-last
+    forward's pixel sequence, so the forward takes the general kernel; the backward's
+    tile layout widens the tiles to 64 pixels (a gather workgroup owns an 8 x 32 band of
+    a tile, 16 workgroups per tile)."""
+    rng = np.random.default_rng(172)
+    feats = [rng.standard_normal((1, 4, 4096, 4096), dtype=np.float32)]
+    rois = _rois(rng, 24, outside=0.05, img=(4096, 4096))
+    rois[:, 0] = 0
+    run("4096 x 4096 map", feats, [1.0], rois)
