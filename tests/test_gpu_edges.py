@@ -284,12 +284,16 @@ def test_plan_five_kernel_path():
 
 
 def test_wide_tiles_on_a_large_map():
-    """A map with more 16-pixel tiles than the plan bins (one 2048 x 2048 image): the
-    tile layout widens the tiles to 32 pixels, so a gather workgroup owns a band of four
-    8 x 8 quadrants (8 x 32 pixels) of a tile instead of a whole 16 x 16 tile."""
+    """Maps with more 16-pixel tiles than the plan bins (one 2048 x 2048 or 4096 x 4096
+    image): the tile layout widens the tiles to 32 or 64 pixels, so a gather workgroup
+    owns a band of four 8 x 8 quadrants (8 x 32 pixels) of a tile instead of a whole
+    16 x 16 tile (4 or 16 workgroups per tile)."""
     rng = np.random.default_rng(90)
     rois = _rois(rng, 48, 1, 8192, 8192, outside=0.05)
     run("2048 x 2048 map, 32-pixel tiles", [(1, 8, 2048, 2048)], [0.25], rois)
+    # 4096 x 4096: 64-pixel tiles, 16 workgroups per tile
+    rois = _rois(rng, 24, 1, 4096, 4096, outside=0.05)
+    run("4096 x 4096 map, 64-pixel tiles", [(1, 4, 4096, 4096)], [1.0], rois)
 
 
 def test_forward_many_rois_ragged_slices():
