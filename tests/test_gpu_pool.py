@@ -147,6 +147,8 @@ def test_pool_output_sizes_and_generic_path():
     r = _rois(rng, 19)
     run("out 14x14 (general kernel)", f, SC, r, out_hw=(14, 14))
     run("out 5x3", f, SC, r, out_hw=(5, 3))
+    run("out 8x12 (96 bins, the largest channels-last grid)", f, SC, r, out_hw=(8, 12))
+    run("out 4x24", f, SC, r, out_hw=(4, 24))
     run("out 1x1", f, SC, r, out_hw=(1, 1))
     run("out 7x7 without plan", f, SC, r, use_plan=False)
 
