@@ -996,7 +996,15 @@ re_status_t deform_roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype,
     if (zero_init != 0 && zero_init != 1) return RE_ERR_INVALID_ARG;
     if ((st = check_plan(plan, plan_bytes, num_rois, t)) != RE_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (zero_init) {
+    const bool fast = cl && gcl && out_h * out_w <= kDeformFastBins &&
+                      num_rois * ((levels[0].c + 63) / 64) < (int64_t(1) << 24);
+    // With a plan that holds tile lists: the feature gradient by the tile gather, which
+    // writes every gradient element once (clearing included); the per-RoI kernel then
+    // adds the taps the lists do not reach
+    const TileLayout tl = tile_layout(g, num_rois);
+    const bool gather = fast && plan && num_rois > 0 && tl.ntiles > 0 && levels_buffered(g) &&
+                        deform_gather_available(out_h, out_w, sampling_ratio);
+    if (zero_init && !gather) {
         if ((st = from_hip(launch_zero(g, numel, dense, s))) != RE_OK) return st;
     }
     if (num_rois == 0) return RE_OK;
@@ -1019,7 +1027,29 @@ re_status_t deform_roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype,
     a.PW = out_w;
     a.S = sampling_ratio;
     a.aligned = aligned;
-    const bool fast = cl && gcl && out_h * out_w <= kDeformFastBins;
+    if (gather) {
+        BwdHead h{};
+        h.gout = grad_out;
+        h.gdt = grad_out_dtype;
+        h.rois = rois;
+        h.K = num_rois;
+        h.roi_levels = roi_levels;
+        h.out_h = out_h;
+        h.out_w = out_w;
+        h.S = sampling_ratio;
+        h.aligned = aligned;
+        h.plan = plan;
+        h.plan_bytes = plan_bytes;
+        if ((st = from_hip(launch_deform_gather(gather_args(g, h, tl, zero_init), a,
+                                                grad_out_dtype, s))) != RE_OK)
+            return st;
+        a.gathered = 1;
+        a.tile_shift = tl.shift;
+        for (int l = 0; l < kMaxLevels; ++l) {
+            a.ntx[l] = tl.ntx[l];
+            a.nty[l] = tl.nty[l];
+        }
+    }
     return from_hip(launch_deform_bwd(a, levels[0].dtype, grad_out_dtype, fast, s));
 }
 

@@ -233,6 +233,32 @@ struct Axis {
     float len;   // box length on the level (after the minimum size)
 };
 
+// Bin-tiles met by a conservative box around the footprint of a RoI on its level (scale
+// s, W x H map, tiles of 2^shift pixels, ntx x nty of them): every sample of the RoI
+// lies between the (shifted) box edges for any output size, sampling ratio and
+// alignment; taps add one pixel, and a 1.5-pixel margin absorbs rounding.  Non-finite
+// boxes cover the whole map.  The plan bins RoIs to tiles with it, and the backward of
+// deformable pooling uses it to tell which taps the tile lists reach.
+__device__ __forceinline__ void roi_tile_range(float x1, float y1, float x2, float y2, float s,
+                                               int Wi, int Hi, int shift, int ntx, int nty,
+                                               int &tx0, int &tx1, int &ty0, int &ty1) {
+    const float W = static_cast<float>(Wi - 1);
+    const float H = static_cast<float>(Hi - 1);
+    float lx = 0.0f, hx = W, ly = 0.0f, hy = H;
+    if (isfinite(x1) && isfinite(x2) && isfinite(y1) && isfinite(y2)) {
+        lx = fminf(fmaxf(fminf(x1, x2) * s - 1.5f, 0.0f), W);
+        hx = fminf(fmaxf(fmaxf(fmaxf(x1, x2) * s, x1 * s + 1.0f) + 2.5f, 0.0f), W);
+        ly = fminf(fmaxf(fminf(y1, y2) * s - 1.5f, 0.0f), H);
+        hy = fminf(fmaxf(fmaxf(fmaxf(y1, y2) * s, y1 * s + 1.0f) + 2.5f, 0.0f), H);
+    }
+    tx0 = static_cast<int>(lx) >> shift;
+    tx1 = max(static_cast<int>(hx) >> shift, tx0);
+    ty0 = static_cast<int>(ly) >> shift;
+    ty1 = max(static_cast<int>(hy) >> shift, ty0);
+    tx1 = min(tx1, ntx - 1);
+    ty1 = min(ty1, nty - 1);
+}
+
 __device__ __forceinline__ Axis axis_setup(float c1, float c2, float scale, int aligned, int P,
                                            int S) {
     const float off = aligned ? 0.5f : 0.0f;

@@ -23,7 +23,7 @@
 //                            the wave's channels with lane shuffles and added once per
 //                            wave.
 //   deform_*_generic_kernel  any strides: one thread per output element.
-#include "internal.hpp"
+#include "gather.hpp"
 
 namespace rex {
 
@@ -498,6 +498,19 @@ __global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
     const uint32_t sw = static_cast<uint32_t>(L.sw) * uint32_t(sizeof(T));
     float *const gbase = gdata + static_cast<int64_t>(d.b) * gsn + (d.slice * 64 + (lane_on ? lane : 0));
     const int count = max(d.ay.grid * d.ax.grid, 1);
+    // After the tile gather, a tap whose tile lies in the RoI's tile range is written
+    // already: only the others are added here.
+    int tx0 = 0, tx1 = -1, ty0 = 0, ty1 = -1;
+    if (a.gathered) {
+        const int lvl = a.roi_levels ? a.roi_levels[d.k] : 0;
+        const float *r = a.rois + 5 * static_cast<int64_t>(d.k);
+        roi_tile_range(r[1], r[2], r[3], r[4], L.scale, L.W, L.H, a.tile_shift, pick(a.ntx, lvl),
+                       pick(a.nty, lvl), tx0, tx1, ty0, ty1);
+    }
+    auto gathered_px = [&](int y, int x) {
+        const int ty = y >> a.tile_shift, tx = x >> a.tile_shift;
+        return ty >= ty0 && ty <= ty1 && tx >= tx0 && tx <= tx1;
+    };
     const float jx = a.gamma * d.ax.len, jy = a.gamma * d.ay.len;
     for (int jb = wave; jb < NB; jb += 4) {
         const int ph = jb / a.PW, pw = jb - (jb / a.PW) * a.PW;
@@ -522,10 +535,14 @@ __global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
             const float v21 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c0));
             const float v22 = raw_to_f32<T>(buf_load_raw_s<T>(rs, vo, r1 + c1));
             if (scatter && lane_on) {
-                unsafeAtomicAdd(gbase + ty.lo * gsh + tx.lo * gsw, gq * (ty.wlo * tx.wlo));
-                unsafeAtomicAdd(gbase + ty.lo * gsh + tx.hi * gsw, gq * (ty.wlo * tx.whi));
-                unsafeAtomicAdd(gbase + ty.hi * gsh + tx.lo * gsw, gq * (ty.whi * tx.wlo));
-                unsafeAtomicAdd(gbase + ty.hi * gsh + tx.hi * gsw, gq * (ty.whi * tx.whi));
+                if (!gathered_px(ty.lo, tx.lo))
+                    unsafeAtomicAdd(gbase + ty.lo * gsh + tx.lo * gsw, gq * (ty.wlo * tx.wlo));
+                if (!gathered_px(ty.lo, tx.hi))
+                    unsafeAtomicAdd(gbase + ty.lo * gsh + tx.hi * gsw, gq * (ty.wlo * tx.whi));
+                if (!gathered_px(ty.hi, tx.lo))
+                    unsafeAtomicAdd(gbase + ty.hi * gsh + tx.lo * gsw, gq * (ty.whi * tx.wlo));
+                if (!gathered_px(ty.hi, tx.hi))
+                    unsafeAtomicAdd(gbase + ty.hi * gsh + tx.hi * gsw, gq * (ty.whi * tx.whi));
             }
             if (tx.slope) px += ty.wlo * (v12 - v11) + ty.whi * (v22 - v21);
             if (ty.slope) py += tx.wlo * (v21 - v11) + tx.whi * (v22 - v12);
@@ -581,7 +598,7 @@ __global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
                 for (int ey = 0; ey < 4; ++ey)
 #pragma unroll
                     for (int ex = 0; ex < 4; ++ex)
-                        if (hy[ey] && hx[ex])
+                        if (hy[ey] && hx[ex] && !gathered_px(by + ey, bx + ex))
                             unsafeAtomicAdd(gbase + (by + ey) * gsh + (bx + ex) * gsw,
                                             gq * (wy[ey] * wx[ex]));
             }
@@ -607,6 +624,243 @@ __global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
             if (a.grad_mask) unsafeAtomicAdd(a.grad_mask + kb, sm_sum / static_cast<float>(count));
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// Feature gradient, tile-gather form
+// ---------------------------------------------------------------------------
+// With the plan's tile lists, a workgroup owns one tile region and 64 channels (each
+// wave an 8x8 quadrant, accumulators in registers) and walks the RoIs binned to the
+// tile.  Within a bin, validity and tap weights are separable (RoIAlign's sampling,
+// shifted), so the bin adds to the quadrant the outer product
+//   acc[r][q] += Wy[r] * (gq * Wx[q]),   gq = g[c][bin] * m / count,
+// with Wy[r] (Wx[q]) the summed tap weights of the bin's valid y (x) samples on row
+// R0 + r (column Q0 + q), over the rows and columns some valid sample taps (so a
+// non-finite gradient reaches the tapped pixels only).  Every element of the region
+// is then written once.  A tap whose tile is not in its RoI's tile range (a shift
+// larger than the range's margins) is never listed here; the per-RoI kernel adds those
+// with atomics afterwards (DeformArgs::gathered).
+
+constexpr int kDeformGatherBins = 49;   // 7 x 7 grids
+constexpr int kDeformGatherS = 2;       // at most 2 samples per axis
+
+bool deform_gather_available(int PH, int PW, int S) {
+    return PH == 7 && PW == 7 && S >= 1 && S <= kDeformGatherS;
+}
+
+struct DeformGatherArgs {
+    GatherArgs g;
+    const float *offset;
+    const float *mask;
+    float gamma;
+    int32_t S;
+    int32_t aligned;
+};
+
+struct DeformGatherSmem {
+    int k[64];
+    Tap ty[kDeformGatherBins][kDeformGatherS];   // invalid taps: lo = hi = -1
+    Tap tx[kDeformGatherBins][kDeformGatherS];
+    float m[kDeformGatherBins];
+    int n;
+};
+
+template <typename TG>
+__global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg) {
+    constexpr int PH = 7, PW = 7, NB = kDeformGatherBins;
+    const GatherArgs &a = dg.g;
+    __shared__ DeformGatherSmem sm;
+    __shared__ __align__(16) uint32_t blk[64 * NB];   // one RoI's gradient block
+    GatherTile x;
+    const int t = gather_tile(a, a.tile_order, x);
+    const GatherHead &h = a.head[0];
+    const int tid = threadIdx.x;
+    const int wave = uniform_i(tid >> 6);
+    const int lane = tid & 63;
+    const LevelArg &L = x.L;
+    const int R0 = x.R0, Q0 = x.Q0;
+    const int S = dg.S;
+    const float fcount = static_cast<float>(S * S);
+    float acc[8][8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[r][q] = 0.0f;
+
+    int s0 = h.tile_start[t];
+    int s1 = h.tile_end[t];
+    s0 = max(0, min(s0, h.capacity));
+    s1 = max(s0, min(s1, h.capacity));
+    const int64_t kstride = static_cast<int64_t>(a.lv.C) * NB;
+    const uint32_t nvalid = static_cast<uint32_t>(x.nch * NB);
+    const bool wide = sizeof(TG) == 4 && (a.lv.C & 3) == 0 &&
+                      (reinterpret_cast<uintptr_t>(h.gout) & 15u) == 0;
+
+    // the gradient block of RoI k (channel group cg) into LDS, one 32-bit word per
+    // element: runs of 256 words as 16-byte copies when `wide`, else runs of 64
+    auto fetch = [&](int k) {
+        const char *src = static_cast<const char *>(h.gout) +
+                          (static_cast<int64_t>(x.cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
+                              int64_t(sizeof(TG));
+        const __amdgpu_buffer_rsrc_t rs = make_rsrc(src, nvalid * uint32_t(sizeof(TG)));
+        int w0 = 0;
+        if (wide) {
+            constexpr int NR = 64 * NB / 256;
+#pragma unroll
+            for (int m = 0; m < (NR + 3) / 4; ++m) {
+                const int run = wave + 4 * m;
+                if (m < NR / 4 || run < NR) {
+                    auto *d = (__attribute__((address_space(3))) void *)(blk + 256 * run);
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        rs, d, 16, static_cast<uint32_t>(256 * run + lane * 4) * 4u, 0, 0, 0);
+                }
+            }
+            w0 = NR * 256;
+        }
+        const int nr = (64 * NB - w0) / 64;
+        for (int run = wave; run < nr; run += 4) {
+            auto *d = (__attribute__((address_space(3))) void *)(blk + w0 + 64 * run);
+            const uint32_t off = static_cast<uint32_t>(w0 + 64 * run + lane) * uint32_t(sizeof(TG));
+            if constexpr (sizeof(TG) == 4)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 4, off, 0, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 2, off, 0, 0, 0);
+        }
+    };
+
+    for (int base = s0; base < s1; base += 64) {
+        const int n = min(64, s1 - base);
+        __syncthreads();   // the previous batch is fully consumed
+        if (wave == 0) {
+            bool keep = false;
+            int k = 0;
+            if (lane < n) {
+                k = h.tile_rois[base + lane];
+                if (k >= 0 && k < h.K) {
+                    const int lvl = h.roi_levels ? h.roi_levels[k] : 0;
+                    keep = lvl == x.l && roi_batch(h.rois[5 * static_cast<int64_t>(k)], a.lv.N) == x.b;
+                }
+            }
+            const uint64_t km = __ballot(keep);
+            if (keep) {
+                const int pos = static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                    static_cast<uint32_t>(km >> 32),
+                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(km), 0u)));
+                sm.k[pos] = k;
+            }
+            if (lane == 0) sm.n = __builtin_popcountll(km);
+        }
+        __syncthreads();
+        const int nk = sm.n;
+        for (int j = 0; j < nk; ++j) {
+            if (j > 0) __syncthreads();   // the previous RoI is fully consumed
+            const int k = uniform_i(sm.k[j]);
+            fetch(k);
+            // the taps of every bin (thread = bin x axis x sample), shifted as the forward
+            if (tid < NB * 2 * kDeformGatherS) {
+                const int b = tid % NB, ax = (tid / NB) & 1, i = tid / (2 * NB);
+                const float *r = h.rois + 5 * static_cast<int64_t>(k);
+                const int ph = b / PW, pw = b - (b / PW) * PW;
+                Tap tp;
+                tp.lo = tp.hi = -1;
+                tp.wlo = tp.whi = 0.0f;
+                if (i < S) {
+                    const Axis axis = ax ? axis_setup(r[2], r[4], L.scale, dg.aligned, PH, S)
+                                         : axis_setup(r[1], r[3], L.scale, dg.aligned, PW, S);
+                    const float off = dg.offset[(2 * static_cast<int64_t>(k) + ax) * NB + b];
+                    const DTap d = deform_tap(axis, deform_shift(dg.gamma, off, axis.len),
+                                              ax ? ph : pw, i, ax ? L.H : L.W);
+                    if (d.valid) {
+                        tp.lo = d.lo;
+                        tp.hi = d.hi;
+                        tp.wlo = d.wlo;
+                        tp.whi = d.whi;
+                    }
+                }
+                if (ax) sm.ty[b][i] = tp;
+                else sm.tx[b][i] = tp;
+                if (ax == 0 && i == 0) sm.m[b] = dg.mask ? dg.mask[static_cast<int64_t>(k) * NB + b] : 1.0f;
+            }
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // this wave's copies are complete
+            __syncthreads();
+            if (!x.wave_on) continue;
+            // bins with a valid tap on a row and on a column of the quadrant
+            bool reach = false;
+            if (lane < NB) {
+                bool ry = false, rx = false;
+#pragma unroll
+                for (int i = 0; i < kDeformGatherS; ++i) {
+                    const Tap a_ = sm.ty[lane][i], b_ = sm.tx[lane][i];
+                    ry = ry || (a_.lo >= 0 && a_.hi >= R0 && a_.lo < R0 + 8);
+                    rx = rx || (b_.lo >= 0 && b_.hi >= Q0 && b_.lo < Q0 + 8);
+                }
+                reach = ry && rx;
+            }
+            uint64_t bins = __ballot(reach);
+            while (bins) {
+                const int b = __builtin_ctzll(bins);
+                bins &= bins - 1;
+                // lanes 0-7: Wy and whether a valid sample taps row R0 + lane; lanes 8-15
+                // the same for the columns
+                float w = 0.0f;
+                bool hit = false;
+                if (lane < 16) {
+                    const int pos = lane < 8 ? R0 + lane : Q0 + lane - 8;
+#pragma unroll
+                    for (int i = 0; i < kDeformGatherS; ++i) {
+                        const Tap tp = lane < 8 ? sm.ty[b][i] : sm.tx[b][i];
+                        const bool a_ = tp.lo == pos, c_ = tp.hi == pos;   // invalid: -1
+                        w += a_ ? tp.wlo : 0.0f;
+                        w += c_ ? tp.whi : 0.0f;
+                        hit = hit || a_ || c_;
+                    }
+                }
+                const uint64_t hits = __ballot(hit);
+                const uint32_t rows = static_cast<uint32_t>(hits) & 0xffu;
+                const uint32_t cols = (static_cast<uint32_t>(hits) >> 8) & 0xffu;
+                if (rows == 0 || cols == 0) continue;
+                const float gq = (raw_to_f32<TG>(blk[lane * NB + b]) * sm.m[b]) / fcount;
+                float X[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const float wx = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(w), 8 + q));
+                    X[q] = (cols >> q & 1u) ? gq * wx : 0.0f;
+                }
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    if (!(rows >> r & 1u)) continue;
+                    const float wy = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(w), r));
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) acc[r][q] = fmaf(wy, X[q], acc[r][q]);
+                }
+            }
+        }
+    }
+    __syncthreads();   // the block is free: the store uses it as scratch
+    static_assert(64 * NB >= 4 * 512, "store scratch in the block");
+    gather_store(x, a.zero_init, acc, reinterpret_cast<float *>(blk) + wave * 512);
+}
+
+hipError_t launch_deform_gather(GatherArgs g, const DeformArgs &d, int gout_dtype,
+                                hipStream_t stream) {
+    if (!gather_prepare(g)) return hipErrorInvalidConfiguration;
+    const int64_t grid = static_cast<int64_t>(g.ntiles) * g.wg_per_tile * g.ncg;
+    if (grid <= 0) return hipSuccess;
+    if (grid >= (int64_t(1) << 24) || !deform_gather_available(d.PH, d.PW, d.S))
+        return hipErrorInvalidConfiguration;
+    DeformGatherArgs dg;
+    dg.g = g;
+    dg.offset = d.offset;
+    dg.mask = d.mask;
+    dg.gamma = d.gamma;
+    dg.S = d.S;
+    dg.aligned = d.aligned;
+    const uint32_t n = static_cast<uint32_t>(grid);
+    if (gout_dtype == kF32)
+        deform_gather_kernel<float><<<n, 256, 0, stream>>>(dg);
+    else
+        deform_gather_kernel<uint16_t><<<n, 256, 0, stream>>>(dg);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -682,6 +936,8 @@ hipError_t launch_deform_bwd(DeformArgs a, int feat_dtype, int gout_dtype, bool 
     if (e != hipSuccess) return e;
     a.nslices = (a.lv.C + 63) / 64;
     if (static_cast<int64_t>(a.K) * a.nslices >= (int64_t(1) << 24)) fast = false;
+    // only the channels-last kernel knows which taps the gather has written
+    if (a.gathered && !fast) return hipErrorInvalidConfiguration;
     if (feat_dtype == kF32 && gout_dtype == kF32)
         bwd_typed<float, float>(a, fast, stream);
     else if (feat_dtype == kF32)

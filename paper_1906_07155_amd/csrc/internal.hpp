@@ -235,11 +235,20 @@ struct DeformArgs {
     int32_t PH, PW, S;
     int32_t aligned;
     int32_t nslices;
-    int32_t pad;
+    // backward after the tile gather: the feature gradient of every tap whose tile is in
+    // its RoI's tile range (roi_tile_range) is already written; add only the others
+    int32_t gathered;
+    int32_t tile_shift;
+    int32_t ntx[kMaxLevels], nty[kMaxLevels];
 };
 
 hipError_t launch_deform_fwd(DeformArgs a, int feat_dtype, int out_dtype, bool fast,
                              hipStream_t stream);
+// The feature gradient of deformable pooling as a tile gather (7x7 bins, 1 or 2 samples
+// per axis): every tap whose tile is in its RoI's tile range, written once per element.
+bool deform_gather_available(int PH, int PW, int S);
+hipError_t launch_deform_gather(GatherArgs g, const DeformArgs &d, int gout_dtype,
+                                hipStream_t stream);
 // Clears grad_offset / grad_mask, then adds the gradients (features with atomics).
 hipError_t launch_deform_bwd(DeformArgs a, int feat_dtype, int gout_dtype, bool fast,
                              hipStream_t stream);

@@ -60,29 +60,11 @@ __device__ __forceinline__ void load_tab(const PlanArgs &a, LevelTab &t) {
     }
 }
 
-// Bin-tiles met by a conservative box around the footprint of a RoI on its level.
-// Every sample of the RoI lies between the (shifted) box edges for any output size,
-// sampling ratio and alignment; taps add one pixel, and a 1.5-pixel margin absorbs
-// rounding.  Non-finite boxes cover the whole map.
 __device__ __forceinline__ void roi_tile_box(const PlanArgs &a, const LevelRow &R, float x1,
                                              float y1, float x2, float y2, int &tx0, int &tx1,
                                              int &ty0, int &ty1) {
-    const float s = R.scale;
-    const float W = static_cast<float>(R.W - 1);
-    const float H = static_cast<float>(R.H - 1);
-    float lx = 0.0f, hx = W, ly = 0.0f, hy = H;
-    if (isfinite(x1) && isfinite(x2) && isfinite(y1) && isfinite(y2)) {
-        lx = fminf(fmaxf(fminf(x1, x2) * s - 1.5f, 0.0f), W);
-        hx = fminf(fmaxf(fmaxf(fmaxf(x1, x2) * s, x1 * s + 1.0f) + 2.5f, 0.0f), W);
-        ly = fminf(fmaxf(fminf(y1, y2) * s - 1.5f, 0.0f), H);
-        hy = fminf(fmaxf(fmaxf(fmaxf(y1, y2) * s, y1 * s + 1.0f) + 2.5f, 0.0f), H);
-    }
-    tx0 = static_cast<int>(lx) >> a.tile_shift;
-    tx1 = max(static_cast<int>(hx) >> a.tile_shift, tx0);
-    ty0 = static_cast<int>(ly) >> a.tile_shift;
-    ty1 = max(static_cast<int>(hy) >> a.tile_shift, ty0);
-    tx1 = min(tx1, R.ntx - 1);
-    ty1 = min(ty1, R.nty - 1);
+    roi_tile_range(x1, y1, x2, y2, R.scale, R.W, R.H, a.tile_shift, R.ntx, R.nty, tx0, tx1, ty0,
+                   ty1);
 }
 
 // Sort key of a RoI: level bucket + image + spatial cell of the box centre.

@@ -279,6 +279,8 @@ hipError_t launch_pool_bwd(PoolArgs, int, bool, hipStream_t) { std::abort(); }
 hipError_t launch_pool_gather(GatherArgs, int, hipStream_t) { std::abort(); }
 hipError_t launch_deform_fwd(DeformArgs, int, int, bool, hipStream_t) { std::abort(); }
 hipError_t launch_deform_bwd(DeformArgs, int, int, bool, hipStream_t) { std::abort(); }
+hipError_t launch_deform_gather(GatherArgs, const DeformArgs &, int, hipStream_t) { std::abort(); }
+bool deform_gather_available(int, int, int) { return false; }
 hipError_t launch_nms(NmsArgs, hipStream_t) { std::abort(); }
 hipError_t launch_nms_batched(const NmsBatchArgs &, hipStream_t) { std::abort(); }
 }  // namespace rex

@@ -30,6 +30,8 @@ hipError_t launch_pool_bwd(PoolArgs, int, bool, hipStream_t) { return hipSuccess
 hipError_t launch_pool_gather(GatherArgs, int, hipStream_t) { return hipSuccess; }
 hipError_t launch_deform_fwd(DeformArgs, int, int, bool, hipStream_t) { return hipSuccess; }
 hipError_t launch_deform_bwd(DeformArgs, int, int, bool, hipStream_t) { return hipSuccess; }
+hipError_t launch_deform_gather(GatherArgs, const DeformArgs &, int, hipStream_t) { return hipSuccess; }
+bool deform_gather_available(int PH, int PW, int S) { return PH == 7 && PW == 7 && S >= 1 && S <= 2; }
 hipError_t launch_nms(NmsArgs, hipStream_t) { return hipSuccess; }
 hipError_t launch_nms_batched(const NmsBatchArgs &, hipStream_t) { return hipSuccess; }
 hipError_t launch_zero(const LevelTable &, const int64_t *, const int *, hipStream_t) { return hipSuccess; }
