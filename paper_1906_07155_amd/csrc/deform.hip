@@ -626,6 +626,209 @@ __global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
     }
 }
 
+// After the tile gather (DeformArgs::gathered), the rest of the backward for a fixed
+// grid of S x S samples per bin (S <= 2, the grids the gather takes): the offset and
+// modulation gradients, and the feature gradient of the taps outside the RoI's tile
+// range.  Samples are walked as in deform_fwd_stream_kernel (the four corner loads of
+// two batches in flight across bin boundaries, each sample located by a lane and read
+// back with lane reads); per bin the sums over the wave's channels and their atomics
+// are those of deform_bwd_cl_kernel, operation for operation.
+struct DeformBwdMeta {
+    uint32_t o11, o12, o21, o22;   // byte offsets of the corners in the image
+    uint32_t wyl, wyh, wxl, wxh;   // tap weights (binary32 bits): rows lo / hi, columns lo / hi
+    uint32_t ylo, yhi, xlo, xhi;   // tap pixels
+    uint32_t flags;                // 1 valid, 2 last of its bin, 4 x slope, 8 y slope,
+                                   // 16 a corner outside the tile range, bin << 5
+};
+
+template <typename T, typename TG>
+__global__ __launch_bounds__(256) void deform_bwd_stream_kernel(DeformArgs a) {
+    extern __shared__ __align__(16) float s_g[];   // [64][NB] upstream gradient of the slice
+    __shared__ float s_sx[kDeformStreamBins], s_sy[kDeformStreamBins], s_m[kDeformStreamBins];
+    const int PW = a.PW;
+    const int NB = a.PH * PW;
+    const DeformRoi d = deform_roi(a);
+    if (!d.active) return;   // uniform over the workgroup, before any barrier
+    const int tid = threadIdx.x;
+    const int wave = uniform_i(tid >> 6);
+    const int lane = tid & 63;
+    const int64_t o0 =
+        (static_cast<int64_t>(d.k) * a.lv.C + static_cast<int64_t>(d.slice) * 64) * NB;
+    const gcptr<TG> gsrc = as_global<TG>(a.gout) + o0;
+    for (int e = tid; e < d.nch * NB; e += 256) s_g[e] = load_f32(gsrc + e);
+    for (int jb = tid; jb < NB; jb += 256) {
+        const int64_t k = d.k;
+        s_sx[jb] = deform_shift(a.gamma, a.offset[2 * k * NB + jb], d.ax.len);
+        s_sy[jb] = deform_shift(a.gamma, a.offset[(2 * k + 1) * NB + jb], d.ay.len);
+        s_m[jb] = a.mask ? a.mask[k * NB + jb] : 1.0f;
+    }
+    __syncthreads();
+
+    const bool lane_on = lane < d.nch;
+    const LevelArg &L = d.L;
+    const int lvl = a.roi_levels ? a.roi_levels[d.k] : 0;
+    float *gdata;
+    int64_t gsn, gsc, gsh, gsw;
+    grad_level(a, lvl, gdata, gsn, gsc, gsh, gsw);
+    const char *img = static_cast<const char *>(L.data) +
+                      static_cast<int64_t>(d.b) * L.sn * static_cast<int64_t>(sizeof(T));
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(img, L.img_bytes);
+    const uint32_t vo =
+        lane_on ? static_cast<uint32_t>(d.slice * 64 + lane) * uint32_t(sizeof(T)) : kBufOOB;
+    const uint32_t sh = static_cast<uint32_t>(L.sh) * uint32_t(sizeof(T));
+    const uint32_t sw = static_cast<uint32_t>(L.sw) * uint32_t(sizeof(T));
+    float *const gbase = gdata + static_cast<int64_t>(d.b) * gsn + (d.slice * 64 + (lane_on ? lane : 0));
+    const int count = max(d.ay.grid * d.ax.grid, 1);
+    const float jx = a.gamma * d.ax.len, jy = a.gamma * d.ay.len;
+    int tx0, tx1, ty0, ty1;
+    {
+        const float *r = a.rois + 5 * static_cast<int64_t>(d.k);
+        roi_tile_range(r[1], r[2], r[3], r[4], L.scale, L.W, L.H, a.tile_shift, pick(a.ntx, lvl),
+                       pick(a.nty, lvl), tx0, tx1, ty0, ty1);
+    }
+    auto in_range = [&](int y, int x) {
+        const int ty = y >> a.tile_shift, tx = x >> a.tile_shift;
+        return ty >= ty0 && ty <= ty1 && tx >= tx0 && tx <= tx1;
+    };
+
+    const int S = a.S, G = S * S;
+    const int nbw = wave < NB ? (NB - wave + 3) >> 2 : 0;
+    const int n_w = nbw * G;
+    const uint32_t mG = (65536u + G - 1) / G, mS = (65536u + S - 1) / S;
+    const uint32_t mPW = (65536u + PW - 1) / PW;
+    auto locate = [&](int e0, DeformBwdMeta &m) {
+        const int e = e0 + lane;
+        m.o11 = m.o12 = m.o21 = m.o22 = 0;
+        m.wyl = m.wyh = m.wxl = m.wxh = 0;
+        m.ylo = m.yhi = m.xlo = m.xhi = 0;
+        m.flags = 0;
+        if (e < n_w) {
+            const int i = static_cast<int>((static_cast<uint32_t>(e) * mG) >> 16);
+            const int sm = e - i * G;
+            const int iy = static_cast<int>((static_cast<uint32_t>(sm) * mS) >> 16);
+            const int ix = sm - iy * S;
+            const int jb = wave + 4 * i;
+            const int ph = static_cast<int>((static_cast<uint32_t>(jb) * mPW) >> 16);
+            const int pw = jb - ph * PW;
+            const DTap ty = deform_tap(d.ay, s_sy[jb], ph, iy, L.H);
+            const DTap tx = deform_tap(d.ax, s_sx[jb], pw, ix, L.W);
+            const bool valid = ty.valid && tx.valid;
+            uint32_t f = (sm == G - 1 ? 2u : 0u) | (static_cast<uint32_t>(i) << 5);
+            if (valid) {
+                const uint32_t r0 = static_cast<uint32_t>(ty.lo) * sh, r1 = static_cast<uint32_t>(ty.hi) * sh;
+                const uint32_t c0 = static_cast<uint32_t>(tx.lo) * sw, c1 = static_cast<uint32_t>(tx.hi) * sw;
+                m.o11 = r0 + c0;
+                m.o12 = r0 + c1;
+                m.o21 = r1 + c0;
+                m.o22 = r1 + c1;
+                m.wyl = __float_as_uint(ty.wlo);
+                m.wyh = __float_as_uint(ty.whi);
+                m.wxl = __float_as_uint(tx.wlo);
+                m.wxh = __float_as_uint(tx.whi);
+                m.ylo = ty.lo;
+                m.yhi = ty.hi;
+                m.xlo = tx.lo;
+                m.xhi = tx.hi;
+                const bool out = !in_range(ty.lo, tx.lo) || !in_range(ty.lo, tx.hi) ||
+                                 !in_range(ty.hi, tx.lo) || !in_range(ty.hi, tx.hi);
+                f |= 1u | (tx.slope ? 4u : 0u) | (ty.slope ? 8u : 0u) | (out ? 16u : 0u);
+            }
+            m.flags = f;
+        }
+    };
+    auto issue = [&](uint32_t (&v)[4 * kDeformBatch], const DeformBwdMeta &m, int base) {
+#pragma unroll
+        for (int j = 0; j < kDeformBatch; ++j) {
+            v[4 * j + 0] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(m.o11, base + j));
+            v[4 * j + 1] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(m.o12, base + j));
+            v[4 * j + 2] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(m.o21, base + j));
+            v[4 * j + 3] = buf_load_raw_s<T>(rs, vo, __builtin_amdgcn_readlane(m.o22, base + j));
+        }
+    };
+    float px = 0.0f, py = 0.0f, pm = 0.0f;
+    auto rdf = [&](uint32_t v, int l) { return __uint_as_float(__builtin_amdgcn_readlane(v, l)); };
+    auto consume = [&](const uint32_t (&v)[4 * kDeformBatch], const DeformBwdMeta &m, int base) {
+#pragma unroll
+        for (int j = 0; j < kDeformBatch; ++j) {
+            const int l = base + j;
+            const uint32_t f = __builtin_amdgcn_readlane(m.flags, l);
+            const int jb = wave + 4 * static_cast<int>(f >> 5);
+            if (f & 1u) {
+                const float v11 = raw_to_f32<T>(v[4 * j + 0]), v12 = raw_to_f32<T>(v[4 * j + 1]);
+                const float v21 = raw_to_f32<T>(v[4 * j + 2]), v22 = raw_to_f32<T>(v[4 * j + 3]);
+                const float wyl = rdf(m.wyl, l), wyh = rdf(m.wyh, l);
+                const float wxl = rdf(m.wxl, l), wxh = rdf(m.wxh, l);
+                if (f & 16u) {   // corners the gather does not reach
+                    const int ylo = static_cast<int>(__builtin_amdgcn_readlane(m.ylo, l));
+                    const int yhi = static_cast<int>(__builtin_amdgcn_readlane(m.yhi, l));
+                    const int xlo = static_cast<int>(__builtin_amdgcn_readlane(m.xlo, l));
+                    const int xhi = static_cast<int>(__builtin_amdgcn_readlane(m.xhi, l));
+                    const float gv = lane_on ? s_g[lane * NB + jb] : 0.0f;
+                    const float gq = (gv * s_m[jb]) / static_cast<float>(count);
+                    if (lane_on) {
+                        if (!in_range(ylo, xlo))
+                            unsafeAtomicAdd(gbase + ylo * gsh + xlo * gsw, gq * (wyl * wxl));
+                        if (!in_range(ylo, xhi))
+                            unsafeAtomicAdd(gbase + ylo * gsh + xhi * gsw, gq * (wyl * wxh));
+                        if (!in_range(yhi, xlo))
+                            unsafeAtomicAdd(gbase + yhi * gsh + xlo * gsw, gq * (wyh * wxl));
+                        if (!in_range(yhi, xhi))
+                            unsafeAtomicAdd(gbase + yhi * gsh + xhi * gsw, gq * (wyh * wxh));
+                    }
+                }
+                if (f & 4u) px += wyl * (v12 - v11) + wyh * (v22 - v21);
+                if (f & 8u) py += wxl * (v21 - v11) + wxh * (v22 - v12);
+                pm += wyl * wxl * v11 + wyl * wxh * v12 + wyh * wxl * v21 + wyh * wxh * v22;
+            }
+            if (f & 2u) {   // the bin's last sample: its sums over the wave's channels
+                const float gv = lane_on ? s_g[lane * NB + jb] : 0.0f;
+                const float gq = (gv * s_m[jb]) / static_cast<float>(count);
+                const float sx_sum = wave_sum(gq * px);
+                const float sy_sum = wave_sum(gq * py);
+                const float sm_sum = wave_sum(gv * pm);
+                if (lane == 0) {
+                    const int64_t kb = static_cast<int64_t>(d.k) * NB + jb;
+                    unsafeAtomicAdd(a.grad_offset + 2 * static_cast<int64_t>(d.k) * NB + jb, sx_sum * jx);
+                    unsafeAtomicAdd(a.grad_offset + (2 * static_cast<int64_t>(d.k) + 1) * NB + jb,
+                                    sy_sum * jy);
+                    if (a.grad_mask) unsafeAtomicAdd(a.grad_mask + kb, sm_sum / static_cast<float>(count));
+                }
+                px = py = pm = 0.0f;
+            }
+        }
+    };
+    if (n_w > 0) {
+        constexpr int kPerChunk = 64 / kDeformBatch;
+        DeformBwdMeta cur, nxt;
+        locate(0, cur);
+        if (n_w > 64) locate(64, nxt);
+        const int nbatch = (n_w + kDeformBatch - 1) / kDeformBatch;
+        uint32_t va[4 * kDeformBatch], vb[4 * kDeformBatch];
+        issue(va, cur, 0);
+        if (nbatch > 1) issue(vb, cur, kDeformBatch);
+        int c0 = 0;
+        for (int q = 0; q < nbatch; q += 2) {
+            const int qs = q - c0;
+            consume(va, cur, qs * kDeformBatch);
+            if (q + 2 < nbatch) {
+                if (qs + 2 < kPerChunk) issue(va, cur, (qs + 2) * kDeformBatch);
+                else issue(va, nxt, (qs + 2 - kPerChunk) * kDeformBatch);
+            }
+            if (q + 1 >= nbatch) break;
+            consume(vb, cur, (qs + 1) * kDeformBatch);
+            if (q + 3 < nbatch) {
+                if (qs + 3 < kPerChunk) issue(vb, cur, (qs + 3) * kDeformBatch);
+                else issue(vb, nxt, (qs + 3 - kPerChunk) * kDeformBatch);
+            }
+            if (qs + 2 == kPerChunk) {
+                cur = nxt;
+                c0 += kPerChunk;
+                if ((c0 + kPerChunk) * kDeformBatch < n_w) locate((c0 + kPerChunk) * kDeformBatch, nxt);
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Feature gradient, tile-gather form
 // ---------------------------------------------------------------------------
@@ -657,11 +860,14 @@ struct DeformGatherArgs {
     int32_t aligned;
 };
 
-struct DeformGatherSmem {
-    int k[64];
+struct DeformGatherTaps {
     Tap ty[kDeformGatherBins][kDeformGatherS];   // invalid taps: lo = hi = -1
     Tap tx[kDeformGatherBins][kDeformGatherS];
     float m[kDeformGatherBins];
+};
+
+struct DeformGatherSmem {
+    int k[64];
     int n;
 };
 
@@ -670,7 +876,11 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
     constexpr int PH = 7, PW = 7, NB = kDeformGatherBins;
     const GatherArgs &a = dg.g;
     __shared__ DeformGatherSmem sm;
-    __shared__ __align__(16) uint32_t blk[64 * NB];   // one RoI's gradient block
+    // two staging slots (gradient block and taps of one RoI each), separate variables so
+    // the compiler can tell that reading one does not wait for the copy into the other
+    __shared__ __align__(16) uint32_t blk0[64 * NB];
+    __shared__ __align__(16) uint32_t blk1[64 * NB];
+    __shared__ DeformGatherTaps tp0, tp1;
     GatherTile x;
     const int t = gather_tile(a, a.tile_order, x);
     const GatherHead &h = a.head[0];
@@ -698,7 +908,7 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
 
     // the gradient block of RoI k (channel group cg) into LDS, one 32-bit word per
     // element: runs of 256 words as 16-byte copies when `wide`, else runs of 64
-    auto fetch = [&](int k) {
+    auto fetch = [&](int k, uint32_t *blk) {
         const char *src = static_cast<const char *>(h.gout) +
                           (static_cast<int64_t>(x.cg) * 64 * NB + static_cast<int64_t>(k) * kstride) *
                               int64_t(sizeof(TG));
@@ -752,23 +962,35 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
         }
         __syncthreads();
         const int nk = sm.n;
-        for (int j = 0; j < nk; ++j) {
-            if (j > 0) __syncthreads();   // the previous RoI is fully consumed
-            const int k = uniform_i(sm.k[j]);
-            fetch(k);
-            // the taps of every bin (thread = bin x axis x sample), shifted as the forward
+        if (nk == 0) continue;
+        // Per RoI: its block copied by the buffer unit, its RoI record and shifts loaded
+        // into registers (threads of a bin x axis x sample), then, after the previous RoI
+        // is consumed, the taps worked out into the slot's tap table.
+        struct TapIn {
+            float c1, c2, off, m;
+            int k;
+        };
+        auto load_taps = [&](int k, TapIn &in) {
+            in.k = k;
+            if (tid < NB * 2 * kDeformGatherS) {
+                const int b = tid % NB, ax = (tid / NB) & 1;
+                const float *r = h.rois + 5 * static_cast<int64_t>(k);
+                in.c1 = ax ? r[2] : r[1];
+                in.c2 = ax ? r[4] : r[3];
+                in.off = dg.offset[(2 * static_cast<int64_t>(k) + ax) * NB + b];
+                in.m = dg.mask ? dg.mask[static_cast<int64_t>(k) * NB + b] : 1.0f;
+            }
+        };
+        auto store_taps = [&](const TapIn &in, DeformGatherTaps &tb) {
             if (tid < NB * 2 * kDeformGatherS) {
                 const int b = tid % NB, ax = (tid / NB) & 1, i = tid / (2 * NB);
-                const float *r = h.rois + 5 * static_cast<int64_t>(k);
                 const int ph = b / PW, pw = b - (b / PW) * PW;
                 Tap tp;
                 tp.lo = tp.hi = -1;
                 tp.wlo = tp.whi = 0.0f;
                 if (i < S) {
-                    const Axis axis = ax ? axis_setup(r[2], r[4], L.scale, dg.aligned, PH, S)
-                                         : axis_setup(r[1], r[3], L.scale, dg.aligned, PW, S);
-                    const float off = dg.offset[(2 * static_cast<int64_t>(k) + ax) * NB + b];
-                    const DTap d = deform_tap(axis, deform_shift(dg.gamma, off, axis.len),
+                    const Axis axis = axis_setup(in.c1, in.c2, L.scale, dg.aligned, ax ? PH : PW, S);
+                    const DTap d = deform_tap(axis, deform_shift(dg.gamma, in.off, axis.len),
                                               ax ? ph : pw, i, ax ? L.H : L.W);
                     if (d.valid) {
                         tp.lo = d.lo;
@@ -777,20 +999,20 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
                         tp.whi = d.whi;
                     }
                 }
-                if (ax) sm.ty[b][i] = tp;
-                else sm.tx[b][i] = tp;
-                if (ax == 0 && i == 0) sm.m[b] = dg.mask ? dg.mask[static_cast<int64_t>(k) * NB + b] : 1.0f;
+                if (ax) tb.ty[b][i] = tp;
+                else tb.tx[b][i] = tp;
+                if (ax == 0 && i == 0) tb.m[b] = in.m;
             }
-            __builtin_amdgcn_s_waitcnt(0x0F70);   // this wave's copies are complete
-            __syncthreads();
-            if (!x.wave_on) continue;
+        };
+        auto consume = [&](const uint32_t *blk, const DeformGatherTaps &tb) {
+            if (!x.wave_on) return;
             // bins with a valid tap on a row and on a column of the quadrant
             bool reach = false;
             if (lane < NB) {
                 bool ry = false, rx = false;
 #pragma unroll
                 for (int i = 0; i < kDeformGatherS; ++i) {
-                    const Tap a_ = sm.ty[lane][i], b_ = sm.tx[lane][i];
+                    const Tap a_ = tb.ty[lane][i], b_ = tb.tx[lane][i];
                     ry = ry || (a_.lo >= 0 && a_.hi >= R0 && a_.lo < R0 + 8);
                     rx = rx || (b_.lo >= 0 && b_.hi >= Q0 && b_.lo < Q0 + 8);
                 }
@@ -808,7 +1030,7 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
                     const int pos = lane < 8 ? R0 + lane : Q0 + lane - 8;
 #pragma unroll
                     for (int i = 0; i < kDeformGatherS; ++i) {
-                        const Tap tp = lane < 8 ? sm.ty[b][i] : sm.tx[b][i];
+                        const Tap tp = lane < 8 ? tb.ty[b][i] : tb.tx[b][i];
                         const bool a_ = tp.lo == pos, c_ = tp.hi == pos;   // invalid: -1
                         w += a_ ? tp.wlo : 0.0f;
                         w += c_ ? tp.whi : 0.0f;
@@ -819,7 +1041,7 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
                 const uint32_t rows = static_cast<uint32_t>(hits) & 0xffu;
                 const uint32_t cols = (static_cast<uint32_t>(hits) >> 8) & 0xffu;
                 if (rows == 0 || cols == 0) continue;
-                const float gq = (raw_to_f32<TG>(blk[lane * NB + b]) * sm.m[b]) / fcount;
+                const float gq = (raw_to_f32<TG>(blk[lane * NB + b]) * tb.m[b]) / fcount;
                 float X[8];
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
@@ -834,11 +1056,39 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
                     for (int q = 0; q < 8; ++q) acc[r][q] = fmaf(wy, X[q], acc[r][q]);
                 }
             }
+        };
+        auto fetch_wait = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };
+        TapIn in;
+        // Unrolled by two so that each slot is named statically: RoI j + 1 is staged
+        // into one slot while RoI j is read from the other.
+        fetch(uniform_i(sm.k[0]), blk0);
+        load_taps(uniform_i(sm.k[0]), in);
+        store_taps(in, tp0);
+        fetch_wait();
+        __syncthreads();
+        for (int j = 0; j < nk; j += 2) {
+            if (j + 1 < nk) {
+                fetch(uniform_i(sm.k[j + 1]), blk1);
+                load_taps(uniform_i(sm.k[j + 1]), in);
+            }
+            consume(blk0, tp0);
+            if (j + 1 < nk) store_taps(in, tp1);
+            fetch_wait();
+            __syncthreads();   // slot 0 consumed, slot 1 staged
+            if (j + 1 >= nk) break;
+            if (j + 2 < nk) {
+                fetch(uniform_i(sm.k[j + 2]), blk0);
+                load_taps(uniform_i(sm.k[j + 2]), in);
+            }
+            consume(blk1, tp1);
+            if (j + 2 < nk) store_taps(in, tp0);
+            fetch_wait();
+            __syncthreads();
         }
     }
-    __syncthreads();   // the block is free: the store uses it as scratch
-    static_assert(64 * NB >= 4 * 512, "store scratch in the block");
-    gather_store(x, a.zero_init, acc, reinterpret_cast<float *>(blk) + wave * 512);
+    __syncthreads();   // the slots are free: the store uses one as scratch
+    static_assert(64 * NB >= 4 * 512, "store scratch in a slot");
+    gather_store(x, a.zero_init, acc, reinterpret_cast<float *>(blk0) + wave * 512);
 }
 
 hipError_t launch_deform_gather(GatherArgs g, const DeformArgs &d, int gout_dtype,
@@ -915,7 +1165,10 @@ static void bwd_typed(const DeformArgs &a, bool fast, hipStream_t stream) {
     const int NB = a.PH * a.PW;
     if (fast) {
         const uint32_t g = static_cast<uint32_t>(static_cast<int64_t>(a.K) * a.nslices);
-        deform_bwd_cl_kernel<T, TG><<<g, 256, static_cast<size_t>(64) * NB * 4, stream>>>(a);
+        if (a.gathered && a.S >= 1 && a.S <= 4 && NB <= kDeformStreamBins)
+            deform_bwd_stream_kernel<T, TG><<<g, 256, static_cast<size_t>(64) * NB * 4, stream>>>(a);
+        else
+            deform_bwd_cl_kernel<T, TG><<<g, 256, static_cast<size_t>(64) * NB * 4, stream>>>(a);
     } else {
         const int64_t total = static_cast<int64_t>(a.K) * a.lv.C * NB;
         const uint32_t blocks = static_cast<uint32_t>(std::min<int64_t>((total + 255) / 256, 16384));

@@ -135,6 +135,8 @@ def test_deform_layouts_grids_and_no_mask():
     run("16x16 (general kernels)", f, SC, r, out_hw=(16, 16))
     run("5x3 without mask", f, SC, r, out_hw=(5, 3), with_mask=False)
     run("without plan, accumulate", f, SC, r, use_plan=False, zero_init=False)
+    run("with plan (tile gather), accumulate", f, SC, r, zero_init=False)
+    run("with plan (tile gather), S=1, large offsets", f, SC, r, S=1, offset_std=3.0)
 
 
 def test_deform_large_offsets_and_degenerate_inputs():
