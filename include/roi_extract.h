@@ -332,7 +332,12 @@ re_status_t deform_roi_pool_fwd(const re_level_t *levels, int32_t num_levels, co
  *     xl < W-1) and 0 for a clamped one; grad_offset[k,1] likewise along y;
  *   grad_mask[k,ph,pw] (written; NULL allowed, and required when mask is NULL) =
  *     sum over channels of g * (sum of weighted taps) / count.
- * Sums use fp32 atomics, so the last bits may vary between runs.
+ * Sums use fp32 atomics, so the last bits may vary between runs.  With a plan that
+ * holds tile lists, a 7 x 7 grid, 1 or 2 samples per axis and channels-last levels,
+ * the feature gradient is gathered per tile (every gradient element written once,
+ * zero_init != 0 needing no separate clearing) and only the taps outside their RoI's
+ * tile range are added with atomics; the plan's levels must then be roi_levels (RoIs
+ * of another level are not found in the tile lists).
  *   levels: the forward's features (read);  grad_levels: binary32 levels with the
  *   features' n, c, h, w and spatial_scale;  grad_out: [num_rois][c][out_h][out_w]. */
 re_status_t deform_roi_pool_bwd(const void *grad_out, int32_t grad_out_dtype,
