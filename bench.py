@@ -770,8 +770,16 @@ def main_deform(args):
     elems = K * C * PH * PW
     side = K * PH * PW * 3 * 4                       # offsets and modulation
     zero = sum(wl.n_images * C * H * W * 4 for (H, W) in wl.level_hw)
+    # the library takes the tile gather for 7x7 grids with 1-2 samples per axis when the
+    # plan holds tile lists (it does here): the upstream gradient read by the gather and
+    # by the per-RoI pass, the features read once, every gradient element written once;
+    # otherwise one fp32 read-modify-write per footprint pixel and channel plus clearing
+    bwd_alg = ("gather" if tuple(wl.out_hw) == (7, 7) and 1 <= wl.sampling_ratio <= 2
+               else "atomic")
     alg = {"plan": 36 * K, "fwd": fp * C * s_f + elems * s_o + side + 24 * K,
-           "bwd": elems * s_g + fp * C * (s_f + 8) + 2 * side + zero + 24 * K}
+           "bwd": (2 * elems * s_g + fp * C * s_f + 2 * side + zero + 24 * K
+                   if bwd_alg == "gather" else
+                   elems * s_g + fp * C * (s_f + 8) + 2 * side + zero + 24 * K)}
     gbs = {n: alg[n] / (per[n] * 1e-3) / 1e9 for n in names}
     dominant = max(["fwd", "bwd"], key=lambda n: per[n])
     cpu = None
@@ -815,7 +823,8 @@ def main_deform(args):
         "extra": {"kernel_ms": {n: round(v, 5) for n, v in per.items()},
                   "ms_per_step_with_kernel_events": round(ms_with_events, 5),
                   "kernel_GBps_effective": {n: round(v, 1) for n, v in gbs.items()},
-                  "footprint_px": fp, "kernel_source_hash": kernel_source_hash()},
+                  "footprint_px": fp, "bwd_algorithm": bwd_alg,
+                  "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(result), flush=True)
 

@@ -22,6 +22,13 @@
 //                            offset and modulation gradients of a bin are summed over
 //                            the wave's channels with lane shuffles and added once per
 //                            wave.
+//   deform_gather_kernel     the feature gradient with a plan that holds tile lists (7x7,
+//                            1-2 samples per axis): per (tile region, 64 channels) the
+//                            RoIs of the tile's list are added into register
+//                            accumulators and every element is stored once.
+//   deform_bwd_stream_kernel after the gather: offset and modulation gradients, and the
+//                            taps outside their RoI's tile range, walking the samples as
+//                            deform_fwd_stream_kernel does.
 //   deform_*_generic_kernel  any strides: one thread per output element.
 #include "gather.hpp"
 
