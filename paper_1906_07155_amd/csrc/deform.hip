@@ -1027,17 +1027,24 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
             }
             uint64_t bins = __ballot(reach);
             while (bins) {
-                const int b = __builtin_ctzll(bins);
-                bins &= bins - 1;
-                // lanes 0-7: Wy and whether a valid sample taps row R0 + lane; lanes 8-15
-                // the same for the columns
+                // up to four bins per pass: lane group g (16 lanes) builds bin bs[g]'s
+                // weights, lanes 0-7 of the group Wy and whether a valid sample taps row
+                // R0 + lane, lanes 8-15 the same for the columns
+                int bs[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    bs[g] = bins ? __builtin_ctzll(bins) : -1;
+                    bins &= bins - 1;   // no-op once empty
+                }
+                const int g_l = lane >> 4, sub = lane & 15;
+                const int b_l = g_l == 0 ? bs[0] : g_l == 1 ? bs[1] : g_l == 2 ? bs[2] : bs[3];
                 float w = 0.0f;
                 bool hit = false;
-                if (lane < 16) {
-                    const int pos = lane < 8 ? R0 + lane : Q0 + lane - 8;
+                if (b_l >= 0) {
+                    const int pos = sub < 8 ? R0 + sub : Q0 + sub - 8;
 #pragma unroll
                     for (int i = 0; i < kDeformGatherS; ++i) {
-                        const Tap tp = lane < 8 ? tb.ty[b][i] : tb.tx[b][i];
+                        const Tap tp = sub < 8 ? tb.ty[b_l][i] : tb.tx[b_l][i];
                         const bool a_ = tp.lo == pos, c_ = tp.hi == pos;   // invalid: -1
                         w += a_ ? tp.wlo : 0.0f;
                         w += c_ ? tp.whi : 0.0f;
@@ -1045,22 +1052,29 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
                     }
                 }
                 const uint64_t hits = __ballot(hit);
-                const uint32_t rows = static_cast<uint32_t>(hits) & 0xffu;
-                const uint32_t cols = (static_cast<uint32_t>(hits) >> 8) & 0xffu;
-                if (rows == 0 || cols == 0) continue;
-                const float gq = (raw_to_f32<TG>(blk[lane * NB + b]) * tb.m[b]) / fcount;
-                float X[8];
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const float wx = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(w), 8 + q));
-                    X[q] = (cols >> q & 1u) ? gq * wx : 0.0f;
-                }
+                for (int g = 0; g < 4; ++g) {
+                    const int b = bs[g];
+                    if (b < 0) break;
+                    const uint32_t rows = static_cast<uint32_t>(hits >> (16 * g)) & 0xffu;
+                    const uint32_t cols = static_cast<uint32_t>(hits >> (16 * g + 8)) & 0xffu;
+                    if (rows == 0 || cols == 0) continue;
+                    const float gq = (raw_to_f32<TG>(blk[lane * NB + b]) * tb.m[b]) / fcount;
+                    float X[8];
 #pragma unroll
-                for (int r = 0; r < 8; ++r) {
-                    if (!(rows >> r & 1u)) continue;
-                    const float wy = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(w), r));
+                    for (int q = 0; q < 8; ++q) {
+                        const float wx = __uint_as_float(
+                            __builtin_amdgcn_readlane(__float_as_uint(w), 16 * g + 8 + q));
+                        X[q] = (cols >> q & 1u) ? gq * wx : 0.0f;
+                    }
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) acc[r][q] = fmaf(wy, X[q], acc[r][q]);
+                    for (int r = 0; r < 8; ++r) {
+                        if (!(rows >> r & 1u)) continue;
+                        const float wy = __uint_as_float(
+                            __builtin_amdgcn_readlane(__float_as_uint(w), 16 * g + r));
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) acc[r][q] = fmaf(wy, X[q], acc[r][q]);
+                    }
                 }
             }
         };
