@@ -465,9 +465,9 @@ hipError_t launch_pool_bwd(PoolArgs a, int gout_dtype, bool fast, hipStream_t st
 // whose argmax it is, for its channel.  With the plan's tile lists a workgroup owns the
 // 256 pixels of a tile region and 64 channels, accumulated in LDS, and walks the RoIs
 // binned to the tile: each RoI's gradient and argmax blocks ([64 channels][bins],
-// contiguous in memory) are read coalesced, the next RoI's while the current one is
-// added, and every element whose argmax lies in the region is added to its (channel,
-// pixel) accumulator with an LDS atomic.  No bin geometry is needed: the tile lists
+// contiguous in memory) are read coalesced into registers, those of the next two RoIs
+// while the current one is added, and every element whose argmax lies in the region is
+// added to its (channel, pixel) accumulator with an LDS atomic.  No bin geometry is needed: the tile lists
 // hold every RoI whose bins can reach the tile.  The accumulators then leave through
 // the quadrant store of the align gather, so every gradient element is written once,
 // which replaces both the clearing and the device-scope atomics of the per-RoI form
