@@ -169,3 +169,19 @@ def test_deform_full_box_head_workload():
     offsets ~ N(0, 0.3^2) and modulation ~ U(0, 1)."""
     wl = W.config(2)
     run("box head workload", wl.features(), list(wl.scales), wl.rois(), seed=5)
+
+
+def test_deform_gather_wide_tiles_and_five_kernel_plan():
+    """The feature-gradient gather on a map with 32-pixel tiles (one 2048 x 2048 image:
+    a workgroup owns an 8 x 32 band of a tile) and on a plan of more than 8192 RoIs
+    (five kernels)."""
+    rng = np.random.default_rng(260)
+    feats = [rng.standard_normal((1, 8, 2048, 2048), dtype=np.float32)]
+    a = rng.uniform(0, 8192, (40, 2))
+    b = rng.uniform(0, 8192, (40, 2))
+    rois = np.zeros((40, 5), np.float32)
+    rois[:, 1], rois[:, 3] = a.min(1), a.max(1)
+    rois[:, 2], rois[:, 4] = b.min(1), b.max(1)
+    run("2048 x 2048 map, 32-pixel tiles", feats, [0.25], rois)
+    run("9400 RoIs (five-kernel plan)", _pyr(rng, 16), SC,
+        W.draw_rois(rng, 2, 4700, (96, 160), (4.0, 200.0)))
