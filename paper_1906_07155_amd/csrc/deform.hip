@@ -87,10 +87,22 @@ __device__ __forceinline__ float deform_shift(float gamma, float off, float len)
     return t * len;
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+// Sum over the 64 lanes by DPP moves (VALU only, no LDS round trips): an inclusive scan
+// within rows of 16 lanes, then across rows, and the total read from lane 63.  Every
+// lane of the wave must be active.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_add(float v) {
+    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK,
+                                                          0xf, false));
+}
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+    v = dpp_add<0x111, 0xf>(v);   // row_shr:1
+    v = dpp_add<0x112, 0xf>(v);   // row_shr:2
+    v = dpp_add<0x114, 0xf>(v);   // row_shr:4
+    v = dpp_add<0x118, 0xf>(v);   // row_shr:8
+    v = dpp_add<0x142, 0xa>(v);   // row_bcast:15
+    v = dpp_add<0x143, 0xc>(v);   // row_bcast:31
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
 // Gradient level `l` of the table, by constant indices only (as level_at).
@@ -621,9 +633,9 @@ __global__ __launch_bounds__(256) void deform_bwd_cl_kernel(DeformArgs a) {
             }
         }
         // lanes past the last channel have gv = 0 and read zeros, so they add nothing
-        const float sx_sum = wave_sum(gq * px);
-        const float sy_sum = wave_sum(gq * py);
-        const float sm_sum = wave_sum(gv * pm);
+        const float sx_sum = wave_sum_dpp(gq * px);
+        const float sy_sum = wave_sum_dpp(gq * py);
+        const float sm_sum = wave_sum_dpp(gv * pm);
         if (lane == 0) {
             unsafeAtomicAdd(a.grad_offset + 2 * static_cast<int64_t>(d.k) * NB + jb, sx_sum * jx);
             unsafeAtomicAdd(a.grad_offset + (2 * static_cast<int64_t>(d.k) + 1) * NB + jb,
@@ -790,9 +802,9 @@ __global__ __launch_bounds__(256) void deform_bwd_stream_kernel(DeformArgs a) {
             if (f & 2u) {   // the bin's last sample: its sums over the wave's channels
                 const float gv = lane_on ? s_g[lane * NB + jb] : 0.0f;
                 const float gq = (gv * s_m[jb]) / static_cast<float>(count);
-                const float sx_sum = wave_sum(gq * px);
-                const float sy_sum = wave_sum(gq * py);
-                const float sm_sum = wave_sum(gv * pm);
+                const float sx_sum = wave_sum_dpp(gq * px);
+                const float sy_sum = wave_sum_dpp(gq * py);
+                const float sm_sum = wave_sum_dpp(gv * pm);
                 if (lane == 0) {
                     const int64_t kb = static_cast<int64_t>(d.k) * NB + jb;
                     unsafeAtomicAdd(a.grad_offset + 2 * static_cast<int64_t>(d.k) * NB + jb, sx_sum * jx);
