@@ -1072,12 +1072,19 @@ __global__ __launch_bounds__(256) void deform_gather_kernel(DeformGatherArgs dg)
                     const uint32_t cols = static_cast<uint32_t>(hits >> (16 * g + 8)) & 0xffu;
                     if (rows == 0 || cols == 0) continue;
                     const float gq = (raw_to_f32<TG>(blk[lane * NB + b]) * tb.m[b]) / fcount;
+                    // a column no valid sample taps has Wx = 0, so gq * Wx is a zero that
+                    // leaves the sums as they are unless gq is not finite
+                    const bool finite = __ballot(!isfinite(gq)) == 0;
                     float X[8];
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
                         const float wx = __uint_as_float(
                             __builtin_amdgcn_readlane(__float_as_uint(w), 16 * g + 8 + q));
-                        X[q] = (cols >> q & 1u) ? gq * wx : 0.0f;
+                        X[q] = gq * wx;
+                    }
+                    if (!finite) {
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) X[q] = (cols >> q & 1u) ? X[q] : 0.0f;
                     }
 #pragma unroll
                     for (int r = 0; r < 8; ++r) {
