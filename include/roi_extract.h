@@ -231,7 +231,9 @@ re_status_t roi_extract_zero_grad(const re_level_t *grad_levels, int32_t num_lev
  *           (no atomics; clearing is part of the same pass), which requires `plan`
  *           built by roi_extract_plan for these RoIs with levels_out == roi_levels;
  *           RE_BWD_AUTO picks gather when eligible.  RE_ERR_UNSUPPORTED if gather is
- *           requested but not eligible;
+ *           requested but not eligible.  With a NaN or infinity in grad_out the
+ *           scatter follows the definition exactly, while the gather may also put it
+ *           on untapped pixels of the rows the RoI's bin row touches in a quadrant;
  *   other arguments as roi_align_fwd. */
 re_status_t roi_align_bwd(const void *grad_out, int32_t grad_out_dtype,
                           const float *rois, int64_t num_rois, const int32_t *roi_levels,
